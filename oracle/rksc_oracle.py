@@ -1,0 +1,267 @@
+"""Plain float64 CPU oracle for the RKSC verify pass and the ASKS similarity.
+
+TEST INFRASTRUCTURE ONLY. Only tests/, __graft_entry__.smoke() and the
+cpu_baseline leg of bench.py may import this module. The HIP product path never
+calls it, and this module imports nothing from the product package.
+
+Everything is computed from the definitions, in float64, with numpy's matmul as
+the only library primitive. Weights and KV arrive in their storage precision
+(fp32, or bf16 already widened exactly to fp32) and are widened to float64 on
+use. No blocking, fusion or reordering beyond what each definition states.
+
+Model (RKSC paper, Sec. 3 "Problem Setting"; the decoder itself is the standard
+pre-norm Llama-style block the paper runs through HF Transformers, Appendix
+"Implementation Details"):
+  x_0 = E[token]
+  per layer: u = RMSNorm(x; g_attn); q,k,v = u W_q^T, u W_k^T, u W_v^T;
+             rotate-half RoPE on q,k at the token's absolute position;
+             grouped-query attention (query head h reads KV head floor(h/G)),
+             scale 1/sqrt(hd); x += o W_o^T;
+             w = RMSNorm(x; g_ffn); x += (silu(w W_g^T) * (w W_u^T)) W_d^T.
+Verify pass (Sec. 3.2 "KV broadcast and batched decode", Eq. prefix_fwd):
+  every branch's tokens sit at positions n..n+s-1 and attend to the one shared
+  prefix cache plus their own earlier tokens.
+Layer entropy (Eq. entropy, Alg. VerifyWithEntropyExit): last token of the
+  branch, final RMSNorm, lm_head, softmax entropy in nats.
+Exit rule (Sec. 3.3 "Layer-level entropy exit"), as (tau, patience): the layer
+  delta is |H_l - H_{l-1}| with H_0 = +inf; a streak counts consecutive layers
+  with delta < tau (strict); the branch exits at the first layer whose streak
+  reaches patience, else at L.
+ASKS (Eq. asks_sim with its exponential layer weights): S_ij = sum_l w_l *
+  cos(h_i^(l), h_j^(l)), w_l = exp(alpha l/L) / sum_l' exp(alpha l'/L).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "f64", "rmsnorm", "rope_inv_freq", "apply_rope", "silu", "attention",
+    "decoder_stack", "prefill", "forward_full", "softmax_entropy",
+    "layer_entropies", "exit_layer", "verify_forward", "asks_weights",
+    "asks_similarity",
+]
+
+
+def f64(a) -> np.ndarray:
+    """Widen a numpy array or a torch tensor (any float dtype; bf16 is exact via fp32) to float64."""
+    if hasattr(a, "detach"):           # torch tensor: bf16 widens exactly through fp32
+        a = a.detach().cpu()
+        if not a.dtype.is_floating_point or a.element_size() < 4:
+            a = a.float()
+        a = a.numpy()
+    return np.asarray(a, dtype=np.float64)
+
+
+def rmsnorm(x, gamma, eps: float) -> np.ndarray:
+    """RMSNorm over the last axis: gamma * x / sqrt(mean(x^2) + eps)."""
+    x = f64(x)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return f64(gamma) * x / np.sqrt(ms + eps)
+
+
+def rope_inv_freq(head_dim: int, base: float) -> np.ndarray:
+    """theta_j = base^(-2j/hd), j = 0..hd/2-1."""
+    j = np.arange(head_dim // 2, dtype=np.float64)
+    return np.power(float(base), -2.0 * j / head_dim)
+
+
+def apply_rope(x, positions, base: float) -> np.ndarray:
+    """Rotate-half RoPE. x: [T, nh, hd]; positions: [T] absolute positions.
+
+    For j < hd/2 the pair (x_j, x_{j+hd/2}) is rotated by the angle p*theta_j.
+    """
+    x = f64(x)
+    hd = x.shape[-1]
+    half = hd // 2
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * rope_inv_freq(hd, base)[None, :]
+    c = np.cos(ang)[:, None, :]
+    s = np.sin(ang)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def silu(z) -> np.ndarray:
+    """silu(z) = z / (1 + exp(-z))."""
+    z = f64(z)
+    with np.errstate(over="ignore"):
+        return z / (1.0 + np.exp(-z))
+
+
+def attention(q, k_keys, v_keys, n_prefix: int) -> np.ndarray:
+    """Grouped-query attention of one sequence over [shared prefix ; own tokens].
+
+    q:      [T, H, hd]        queries of the sequence's T tokens (post-RoPE)
+    k_keys: [Hkv, n+T, hd]    keys: n_prefix shared prefix keys, then the T own keys
+    v_keys: [Hkv, n+T, hd]
+    Query token i may read every prefix key and own keys 0..i (causal).
+    Returns o: [T, H, hd].
+    """
+    q = f64(q)
+    k_keys = f64(k_keys)
+    v_keys = f64(v_keys)
+    T, H, hd = q.shape
+    Hkv = k_keys.shape[0]
+    G = H // Hkv
+    n_keys = k_keys.shape[1]
+    key_pos = np.arange(n_keys)
+    allowed = (key_pos[None, :] < n_prefix) | ((key_pos[None, :] - n_prefix) <= np.arange(T)[:, None])
+    o = np.empty((T, H, hd), dtype=np.float64)
+    for h in range(H):
+        g = h // G
+        scores = q[:, h, :] @ k_keys[g].T / np.sqrt(hd)          # [T, n_keys]
+        scores = np.where(allowed, scores, -np.inf)
+        m = scores.max(axis=1, keepdims=True)
+        p = np.exp(scores - m)
+        p /= p.sum(axis=1, keepdims=True)
+        o[:, h, :] = p @ v_keys[g]
+    return o
+
+
+def decoder_stack(weights, cfg, tokens, start_pos: int = 0, prefix_k=None, prefix_v=None):
+    """Run all L decoder layers on a batch of independent token sequences.
+
+    weights: object with .embed [V,d], .layers (sequence of mappings with
+             attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down), .final_norm, .lm_head
+    cfg:     object with n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff,
+             rms_eps, rope_base
+    tokens:  int [B, T]; token t of every sequence sits at position start_pos + t
+    prefix_k, prefix_v: [L, Hkv, n, hd] shared post-RoPE prefix cache (or None)
+
+    Returns (hidden [L, B, T, d], k [L, B, Hkv, T, hd], v [L, B, Hkv, T, hd]):
+    hidden[l] is the output of layer l+1 (before any final norm); k is post-RoPE.
+    """
+    tokens = np.asarray(tokens, dtype=np.int64)
+    B, T = tokens.shape
+    L, d = cfg.n_layers, cfg.d_model
+    H, Hkv, hd, F = cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.d_ff
+    n = 0 if prefix_k is None else int(prefix_k.shape[2])
+    positions = start_pos + np.arange(T)
+    embed = weights.embed
+    x = np.stack([f64(embed[tokens[b].tolist()]) for b in range(B)])   # [B, T, d]
+    hidden = np.empty((L, B, T, d), dtype=np.float64)
+    ks = np.empty((L, B, Hkv, T, hd), dtype=np.float64)
+    vs = np.empty((L, B, Hkv, T, hd), dtype=np.float64)
+    for l in range(L):
+        W = weights.layers[l]
+        u = rmsnorm(x, W["attn_norm"], cfg.rms_eps)
+        qkv = u.reshape(B * T, d) @ f64(W["w_qkv"]).T
+        q = qkv[:, : H * hd].reshape(B, T, H, hd)
+        k = qkv[:, H * hd: (H + Hkv) * hd].reshape(B, T, Hkv, hd)
+        v = qkv[:, (H + Hkv) * hd:].reshape(B, T, Hkv, hd)
+        o = np.empty((B, T, H, hd), dtype=np.float64)
+        for b in range(B):
+            qb = apply_rope(q[b], positions, cfg.rope_base)
+            kb = apply_rope(k[b], positions, cfg.rope_base).transpose(1, 0, 2)   # [Hkv, T, hd]
+            vb = v[b].transpose(1, 0, 2)
+            ks[l, b] = kb
+            vs[l, b] = vb
+            if n:
+                k_keys = np.concatenate([f64(prefix_k[l]), kb], axis=1)
+                v_keys = np.concatenate([f64(prefix_v[l]), vb], axis=1)
+            else:
+                k_keys, v_keys = kb, vb
+            o[b] = attention(qb, k_keys, v_keys, n)
+        x = x + (o.reshape(B * T, H * hd) @ f64(W["w_o"]).T).reshape(B, T, d)
+        w = rmsnorm(x, W["ffn_norm"], cfg.rms_eps)
+        gu = w.reshape(B * T, d) @ f64(W["w_gate_up"]).T
+        a = silu(gu[:, :F]) * gu[:, F:]
+        x = x + (a @ f64(W["w_down"]).T).reshape(B, T, d)
+        hidden[l] = x
+    return hidden, ks, vs
+
+
+def prefill(weights, cfg, prefix_tokens):
+    """Root forward over the prefix (Eq. prefix_fwd): causal, positions 0..n-1.
+
+    Returns (k [L, Hkv, n, hd], v [L, Hkv, n, hd], h_root [L, d]); h_root is the
+    last prefix token's per-layer output.
+    """
+    hidden, ks, vs = decoder_stack(weights, cfg, np.asarray(prefix_tokens)[None, :], 0)
+    return ks[:, 0], vs[:, 0], hidden[:, 0, -1, :]
+
+
+def forward_full(weights, cfg, tokens):
+    """Plain causal forward of one sequence from position 0: hidden [L, T, d]."""
+    hidden, _, _ = decoder_stack(weights, cfg, np.asarray(tokens)[None, :], 0)
+    return hidden[:, 0]
+
+
+def softmax_entropy(z) -> np.ndarray:
+    """H = -sum_v p_v log p_v, p = softmax(z) over the last axis, in nats (Eq. entropy)."""
+    z = f64(z)
+    m = z.max(axis=-1, keepdims=True)
+    lse = m + np.log(np.exp(z - m).sum(axis=-1, keepdims=True))
+    logp = z - lse
+    p = np.exp(logp)
+    return -(p * logp).sum(axis=-1)
+
+
+def layer_entropies(weights, cfg, h_last) -> np.ndarray:
+    """Per-layer entropy of last-token rows h_last [L, B, d]: final RMSNorm, lm_head, entropy."""
+    h_last = f64(h_last)
+    L, B, _ = h_last.shape
+    lm = f64(weights.lm_head)
+    out = np.empty((L, B), dtype=np.float64)
+    for l in range(L):
+        z = rmsnorm(h_last[l], weights.final_norm, cfg.rms_eps) @ lm.T     # [B, V]
+        out[l] = softmax_entropy(z)
+    return out
+
+
+def exit_layer(entropies, tau: float, patience: int) -> int:
+    """1-based exit layer of one branch from its full-depth entropy sequence H_1..H_L."""
+    L = len(entropies)
+    prev = np.inf
+    streak = 0
+    for l in range(1, L + 1):
+        h = float(entropies[l - 1])
+        delta = abs(h - prev)
+        streak = streak + 1 if delta < tau else 0
+        if streak >= patience:
+            return l
+        prev = h
+    return L
+
+
+def verify_forward(weights, cfg, prefix_k, prefix_v, branch_tokens, tau: float, patience: int):
+    """RKSC verify pass with the layer-level entropy exit.
+
+    Branches never attend to each other, so the exit of each branch is a pure
+    function of its full-depth entropy sequence: run full depth, then apply the
+    rule. Returns (entropy [L,B] with NaN after exit, exit_layer [B] int32,
+    hidden_last [L,B,d] with NaN rows after exit, entropy_full [L,B],
+    hidden_full [L,B,d]).
+    """
+    tokens = np.asarray(branch_tokens, dtype=np.int64)
+    B, s = tokens.shape
+    n = int(prefix_k.shape[2])
+    hidden, _, _ = decoder_stack(weights, cfg, tokens, n, prefix_k, prefix_v)
+    h_last = hidden[:, :, s - 1, :]                                        # [L, B, d]
+    ent = layer_entropies(weights, cfg, h_last)
+    exits = np.array([exit_layer(ent[:, b], tau, patience) for b in range(B)], dtype=np.int32)
+    L = cfg.n_layers
+    after = np.arange(1, L + 1)[:, None] > exits[None, :]                 # [L, B]
+    ent_out = np.where(after, np.nan, ent)
+    hid_out = np.where(after[:, :, None], np.nan, h_last)
+    return ent_out, exits, hid_out, ent, h_last
+
+
+def asks_weights(alpha: float, L: int) -> np.ndarray:
+    """w_l = exp(alpha*l/L) / sum_{l'=1..L} exp(alpha*l'/L), l = 1..L."""
+    e = np.exp(float(alpha) * np.arange(1, L + 1, dtype=np.float64) / L)
+    return e / e.sum()
+
+
+def asks_similarity(hidden, alpha: float) -> np.ndarray:
+    """S[i,j] = sum_l w_l cos(h_i^(l), h_j^(l)) for hidden [L, B, d]; a zero row has cosine 0."""
+    h = f64(hidden)
+    L, B, _ = h.shape
+    w = asks_weights(alpha, L)
+    S = np.zeros((B, B), dtype=np.float64)
+    for l in range(L):
+        norms = np.sqrt((h[l] * h[l]).sum(axis=1))
+        hat = np.zeros_like(h[l])
+        nz = norms > 0
+        hat[nz] = h[l][nz] / norms[nz, None]
+        S += w[l] * (hat @ hat.T)
+    return S

@@ -1,0 +1,411 @@
+"""Pins of the float64 oracle against facts the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: a closed
+form, a library routine (scipy, torch), values printed in the paper, or a brute
+force recomputation. CPU only.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.spatial.distance
+import scipy.special
+import scipy.stats
+import torch
+
+import oracle
+import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ----------------------------------------------------------------- entropy (Eq. entropy)
+
+@pytest.mark.parametrize("V", [2, 7, 4096, 128256])
+def test_entropy_uniform_is_log_v(V):
+    for c in (0.0, -3.5, 17.0):
+        H = oracle.softmax_entropy(np.full(V, c))
+        assert abs(H - math.log(V)) < 1e-12 * max(1.0, math.log(V))
+
+
+def test_entropy_one_hot_is_zero():
+    z = np.zeros(4096)
+    z[1234] = 1e4
+    assert abs(oracle.softmax_entropy(z)) < 1e-12
+
+
+@pytest.mark.parametrize("a", [-5.0, 0.5, 3.0, 12.0, 40.0])
+@pytest.mark.parametrize("pos", [0, 511, 4095])
+def test_entropy_two_level_closed_form(a, pos):
+    # z = [0,..,a,..,0]: with E = e^a, H = log(E + V - 1) - a E / (E + V - 1)
+    V = 4096
+    z = np.zeros(V)
+    z[pos] = a
+    E = math.exp(a)
+    ref = math.log(E + V - 1) - a * E / (E + V - 1)
+    assert abs(oracle.softmax_entropy(z) - ref) < 1e-11
+
+
+def test_entropy_matches_scipy_and_invariances():
+    rng = np.random.default_rng(0)
+    z = 4.0 * rng.standard_normal((5, 3000))
+    H = oracle.softmax_entropy(z)
+    ref = scipy.stats.entropy(scipy.special.softmax(z, axis=1), axis=1)
+    np.testing.assert_allclose(H, ref, rtol=0, atol=1e-10)
+    perm = rng.permutation(3000)
+    np.testing.assert_allclose(oracle.softmax_entropy(z[:, perm] + 9.0), H, rtol=0, atol=1e-10)
+
+
+# ----------------------------------------------------------------- exit rule (Sec. 3.3)
+
+def test_exit_tau_zero_never_exits():
+    H = np.linspace(5.0, 5.0, 12)          # constant: every delta is 0, still not < 0
+    for p in (1, 2, 3):
+        assert oracle.exit_layer(H, 0.0, p) == 12
+
+
+def test_exit_tau_inf_exits_after_patience():
+    H = np.random.default_rng(1).standard_normal(10)
+    for p in (1, 2, 3, 9, 10, 20):
+        assert oracle.exit_layer(H, math.inf, p) == min(1 + p, 10)
+
+
+def test_exit_streak_resets_and_is_strict():
+    # Binary fractions, so every delta below is exact.
+    e = 2.0 ** -8
+    #        l:  1    2              3    4        5            6            7
+    H = np.array([5.0, 5.0 - 2 * e, 4.0, 4.0 - e, 4.0 - 2 * e, 4.0 - 3 * e, 3.0])
+    # deltas: inf, 2e, 1-2e, e, e, e, 1-3e
+    assert oracle.exit_layer(H, 0.02, 1) == 2
+    assert oracle.exit_layer(H, 0.02, 2) == 5          # streak reset by l=3
+    assert oracle.exit_layer(H, 0.02, 3) == 6
+    assert oracle.exit_layer(H, 0.02, 4) == 7          # never: defaults to L
+    assert oracle.exit_layer(H, e, 1) == 7             # |delta| == tau is not < tau
+    assert oracle.exit_layer(H, 2 * e, 1) == 4
+    assert oracle.exit_layer(np.array([1.0, 1.0]), 1e-9, 1) == 2   # H_0 = +inf
+
+
+def _trajectory():
+    with open(os.path.join(GOLDEN, "entropy_trajectory.json")) as f:
+        return json.load(f)
+
+
+def test_exit_paper_trajectory_delta_reading():
+    """The printed delta column puts the first |dH| < 0.02 at layer 19, the paper's l*."""
+    g = _trajectory()
+    L = g["n_layers"]
+    # Unprinted layers take the delta printed at the next printed layer (piecewise constant).
+    deltas = np.empty(L)
+    printed = dict(zip(g["layers"], g["delta"]))
+    nxt = None
+    for l in range(L, 0, -1):
+        if l in printed and printed[l] is not None:
+            nxt = printed[l]
+        deltas[l - 1] = nxt if l > 1 else np.inf
+    H = np.empty(L)
+    H[0] = g["entropy"][0]
+    for l in range(2, L + 1):
+        H[l - 1] = H[l - 2] - deltas[l - 1]            # entropy decays monotonically
+    assert oracle.exit_layer(H, 0.02, 1) == g["claimed_exit_layer"]
+    assert oracle.exit_layer(H, 0.02, 2) == 20
+
+
+def test_exit_paper_trajectory_entropy_reading():
+    """Read from the printed entropy column (linear between printed layers) the exit is 21."""
+    g = _trajectory()
+    L = g["n_layers"]
+    H = np.interp(np.arange(1, L + 1), g["layers"], g["entropy"])
+    assert oracle.exit_layer(H, 0.02, 1) == 21
+    assert oracle.exit_layer(H, 0.07, 1) == 19          # |1.08 - 1.14| = 0.06 < 0.07
+
+
+# ----------------------------------------------------------------- ASKS (Eq. asks_sim)
+
+def test_asks_weights_closed_form():
+    for alpha, L in ((1.5, 28), (0.1, 32), (0.5, 2), (-2.0, 7)):
+        w = oracle.asks_weights(alpha, L)
+        r = math.exp(alpha / L)
+        geo = np.array([r ** l * (r - 1) / (r * (r ** L - 1)) for l in range(1, L + 1)])
+        np.testing.assert_allclose(w, geo, rtol=1e-12)
+        assert abs(w.sum() - 1.0) < 1e-14
+    np.testing.assert_allclose(oracle.asks_weights(0.0, 9), np.full(9, 1 / 9), rtol=1e-15)
+
+
+def test_asks_single_layer_is_cosine():
+    rng = np.random.default_rng(2)
+    h = rng.standard_normal((1, 5, 64))
+    S = oracle.asks_similarity(h, 0.7)
+    for i in range(5):
+        for j in range(5):
+            assert abs(S[i, j] - (1 - scipy.spatial.distance.cosine(h[0, i], h[0, j]))) < 1e-12
+
+
+def test_asks_identical_orthogonal_antipodal_zero():
+    rng = np.random.default_rng(3)
+    L, d = 6, 32
+    h = np.zeros((L, 5, d))
+    base = rng.standard_normal((L, d))
+    h[:, 0] = base
+    h[:, 1] = 3.0 * base                     # same direction, other norm
+    h[:, 2] = -base                          # antipodal
+    for l in range(L):                       # orthogonal to base in every layer
+        v = rng.standard_normal(d)
+        h[l, 3] = v - (v @ base[l]) / (base[l] @ base[l]) * base[l]
+    # h[:, 4] stays zero
+    S = oracle.asks_similarity(h, 1.5)
+    assert abs(S[0, 1] - 1.0) < 1e-12 and abs(S[0, 0] - 1.0) < 1e-12
+    assert abs(S[0, 2] + 1.0) < 1e-12
+    assert abs(S[0, 3]) < 1e-12
+    assert S[4, 4] == 0.0 and np.all(S[4] == 0.0)
+
+
+def test_asks_alpha_zero_is_mean_cosine_and_psd():
+    rng = np.random.default_rng(4)
+    h = rng.standard_normal((4, 6, 48))
+    S = oracle.asks_similarity(h, 0.0)
+    ref = np.zeros((6, 6))
+    for l in range(4):
+        ref += 1 - scipy.spatial.distance.cdist(h[l], h[l], "cosine")
+    np.testing.assert_allclose(S, ref / 4, atol=1e-12)
+    S2 = oracle.asks_similarity(h, 2.0)
+    np.testing.assert_allclose(S2, S2.T, atol=0)
+    assert np.linalg.eigvalsh(S2).min() > -1e-12
+    assert np.all(np.abs(S2) <= 1 + 1e-12)
+
+
+# ----------------------------------------------------------------- layer pieces
+
+def test_rmsnorm_matches_torch_and_is_scale_invariant():
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((7, 96))
+    g = rng.standard_normal(96)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (96,), torch.from_numpy(g), eps=1e-6).numpy()
+    np.testing.assert_allclose(oracle.rmsnorm(x, g, 1e-6), ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.rmsnorm(37.0 * x, g, 0.0), oracle.rmsnorm(x, g, 0.0), rtol=1e-12)
+
+
+def test_rope_is_complex_rotation_and_relative():
+    rng = np.random.default_rng(6)
+    hd, base = 64, 1e4
+    x = rng.standard_normal((5, 3, hd))
+    pos = np.array([0, 1, 17, 1000, 16639])
+    out = oracle.apply_rope(x, pos, base)
+    # Rotate-half RoPE = multiply (x_j + i x_{j+hd/2}) by exp(i p theta_j).
+    theta = base ** (-np.arange(0, hd, 2) / hd)
+    zc = (x[..., : hd // 2] + 1j * x[..., hd // 2:]) * np.exp(1j * pos[:, None, None] * theta[None, None, :])
+    np.testing.assert_allclose(out[..., : hd // 2], zc.real, atol=1e-10)
+    np.testing.assert_allclose(out[..., hd // 2:], zc.imag, atol=1e-10)
+    np.testing.assert_allclose(out[0], x[0], atol=0)                       # position 0: identity
+    # q(p).k(p') depends only on p - p'
+    q = rng.standard_normal((1, 1, hd))
+    k = rng.standard_normal((1, 1, hd))
+    d1 = (oracle.apply_rope(q, [40], base) * oracle.apply_rope(k, [13], base)).sum()
+    d2 = (oracle.apply_rope(q, [1027], base) * oracle.apply_rope(k, [1000], base)).sum()
+    assert abs(d1 - d2) < 1e-9
+
+
+def test_attention_single_key_returns_value():
+    rng = np.random.default_rng(7)
+    q = rng.standard_normal((1, 4, 16))
+    k = rng.standard_normal((2, 1, 16))
+    v = rng.standard_normal((2, 1, 16))
+    o = oracle.attention(q, k, v, n_prefix=0)
+    for h in range(4):
+        np.testing.assert_allclose(o[0, h], v[h // 2, 0], atol=1e-15)
+
+
+def test_attention_matches_torch_sdpa_with_prefix_and_gqa():
+    rng = np.random.default_rng(8)
+    T, n, H, Hkv, hd = 9, 13, 6, 2, 16
+    q = rng.standard_normal((T, H, hd))
+    k = rng.standard_normal((Hkv, n + T, hd))
+    v = rng.standard_normal((Hkv, n + T, hd))
+    o = oracle.attention(q, k, v, n_prefix=n)
+    mask = np.ones((T, n + T), dtype=bool)
+    mask[:, n:] = np.tril(np.ones((T, T), dtype=bool))
+    G = H // Hkv
+    qt = torch.from_numpy(q).permute(1, 0, 2)[None]                       # [1, H, T, hd]
+    kt = torch.from_numpy(np.repeat(k, G, axis=0))[None]
+    vt = torch.from_numpy(np.repeat(v, G, axis=0))[None]
+    ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=torch.from_numpy(mask))
+    np.testing.assert_allclose(o, ref[0].permute(1, 0, 2).numpy(), atol=1e-12)
+
+
+# ----------------------------------------------------------------- whole decoder vs HF Llama
+
+GQA_SHAPE = workloads.ModelShape(n_layers=3, d_model=128, n_heads=8, n_kv_heads=2, head_dim=32,
+                                 d_ff=200, vocab=512, dtype="f32", lm_head_scale=8.0)
+
+
+def _randomise_gains(mw, seed=11):
+    g = torch.Generator().manual_seed(seed)
+    for lw in mw.layers:
+        lw["attn_norm"] = 1.0 + 0.3 * torch.randn(lw["attn_norm"].shape, generator=g)
+        lw["ffn_norm"] = 1.0 + 0.3 * torch.randn(lw["ffn_norm"].shape, generator=g)
+    mw.final_norm = 1.0 + 0.3 * torch.randn(mw.final_norm.shape, generator=g)
+    return mw
+
+
+def _close(a, b, tol=1e-6):
+    """Norm-relative agreement; HF evaluates RoPE's cos/sin in fp32, so exact match is not expected."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    err = np.linalg.norm(a - b) / np.linalg.norm(b)
+    assert err < tol, f"relative error {err:.3e}"
+
+
+def _hf_model(mw, shape):
+    transformers = pytest.importorskip("transformers")
+    cfg = transformers.LlamaConfig(
+        vocab_size=shape.vocab, hidden_size=shape.d_model, intermediate_size=shape.d_ff,
+        num_hidden_layers=shape.n_layers, num_attention_heads=shape.n_heads,
+        num_key_value_heads=shape.n_kv_heads, head_dim=shape.head_dim, rms_norm_eps=shape.rms_eps,
+        rope_theta=shape.rope_base, tie_word_embeddings=False, attention_bias=False, mlp_bias=False,
+        max_position_embeddings=4096)
+    cfg._attn_implementation = "eager"
+    m = transformers.LlamaForCausalLM(cfg).double().eval()
+    H, Hkv, hd, F = shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.d_ff
+    with torch.no_grad():
+        m.model.embed_tokens.weight.copy_(mw.embed.double())
+        for l, lw in enumerate(mw.layers):
+            layer = m.model.layers[l]
+            wqkv = lw["w_qkv"].double()
+            layer.self_attn.q_proj.weight.copy_(wqkv[: H * hd])
+            layer.self_attn.k_proj.weight.copy_(wqkv[H * hd: (H + Hkv) * hd])
+            layer.self_attn.v_proj.weight.copy_(wqkv[(H + Hkv) * hd:])
+            layer.self_attn.o_proj.weight.copy_(lw["w_o"].double())
+            layer.mlp.gate_proj.weight.copy_(lw["w_gate_up"][:F].double())
+            layer.mlp.up_proj.weight.copy_(lw["w_gate_up"][F:].double())
+            layer.mlp.down_proj.weight.copy_(lw["w_down"].double())
+            layer.input_layernorm.weight.copy_(lw["attn_norm"].double())
+            layer.post_attention_layernorm.weight.copy_(lw["ffn_norm"].double())
+        m.model.norm.weight.copy_(mw.final_norm.double())
+        m.lm_head.weight.copy_(mw.lm_head.double())
+        # HF derives the inverse frequencies in fp32; use the exact float64 values.
+        inv = torch.pow(torch.tensor(shape.rope_base, dtype=torch.float64),
+                        -torch.arange(0, hd, 2, dtype=torch.float64) / hd)
+        m.model.rotary_emb.inv_freq = inv
+        if hasattr(m.model.rotary_emb, "original_inv_freq"):
+            m.model.rotary_emb.original_inv_freq = inv
+    return m
+
+
+@pytest.mark.parametrize("shape", [GQA_SHAPE, workloads.get("tiny").model], ids=["gqa", "tiny"])
+def test_forward_full_matches_hf_llama(shape):
+    mw = _randomise_gains(workloads.make_model(shape, seed=3))
+    T = 24
+    toks = workloads.make_tokens(T, shape.vocab, seed=3).numpy()
+    hid = oracle.forward_full(mw, shape, toks)
+    m = _hf_model(mw, shape)
+    with torch.no_grad():
+        out = m(torch.from_numpy(toks.astype(np.int64))[None], output_hidden_states=True)
+    L = shape.n_layers
+    for l in range(L - 1):
+        _close(hid[l], out.hidden_states[l + 1][0].numpy())
+    # HF reports the last layer after the final norm.
+    last = oracle.rmsnorm(hid[L - 1], mw.final_norm, shape.rms_eps)
+    _close(last, out.hidden_states[L][0].numpy())
+    z = last @ oracle.f64(mw.lm_head).T
+    _close(z, out.logits[0].numpy())
+
+
+def test_prefix_cache_verify_matches_hf_dynamic_cache():
+    """Prefill + shared-cache branch forward vs HF's own KV-cache path (the paper's stack)."""
+    transformers = pytest.importorskip("transformers")
+    import copy
+    shape = GQA_SHAPE
+    mw = _randomise_gains(workloads.make_model(shape, seed=4))
+    n, s, B = 20, 7, 3
+    prefix = workloads.make_tokens(n, shape.vocab, seed=4, name="prefix").numpy()
+    branches = workloads.make_tokens(B * s, shape.vocab, seed=4).numpy().reshape(B, s)
+    pk, pv, h_root = oracle.prefill(mw, shape, prefix)
+    ent, ex, hid, ent_full, h_last = oracle.verify_forward(mw, shape, pk, pv, branches, 0.0, 1)
+    m = _hf_model(mw, shape)
+    with torch.no_grad():
+        pre = m(torch.from_numpy(prefix.astype(np.int64))[None], use_cache=True, output_hidden_states=True)
+        cache = pre.past_key_values
+        for l in range(shape.n_layers):
+            layer_cache = cache.layers[l] if hasattr(cache, "layers") else None
+            kk = layer_cache.keys if layer_cache is not None else cache.key_cache[l]
+            vv = layer_cache.values if layer_cache is not None else cache.value_cache[l]
+            _close(pk[l], kk[0].numpy())
+            _close(pv[l], vv[0].numpy())
+        for b in range(B):
+            out = m(torch.from_numpy(branches[b].astype(np.int64))[None],
+                    past_key_values=copy.deepcopy(cache), use_cache=True, output_hidden_states=True)
+            for l in range(shape.n_layers - 1):
+                _close(h_last[l, b], out.hidden_states[l + 1][0, -1].numpy())
+            H_hf = oracle.softmax_entropy(out.logits[0, -1].numpy())
+            assert abs(H_hf - ent_full[-1, b]) < 1e-6
+
+
+# ----------------------------------------------------------------- whole-pass invariants
+
+def _tiny_inputs(name, seed=42):
+    wl = workloads.get(name)
+    shape = wl.model
+    mw = workloads.make_model(shape, seed=seed)
+    prefix = workloads.make_tokens(wl.prefix_len, shape.vocab, seed=seed, name="prefix").numpy()
+    toks = workloads.make_tokens(wl.n_branches * wl.branch_len, shape.vocab, seed=seed).numpy()
+    return wl, mw, prefix, toks.reshape(wl.n_branches, wl.branch_len)
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_deep"])
+def test_shared_prefix_equals_recomputation(name):
+    """Shared-prefix verify equals a per-branch full forward of [prefix; branch] (brute force)."""
+    wl, mw, prefix, toks = _tiny_inputs(name)
+    shape = wl.model
+    pk, pv, _ = oracle.prefill(mw, shape, prefix)
+    _, _, _, ent_full, h_last = oracle.verify_forward(mw, shape, pk, pv, toks, wl.tau, wl.patience)
+    for b in range(wl.n_branches):
+        full = oracle.forward_full(mw, shape, np.concatenate([prefix, toks[b]]))
+        np.testing.assert_allclose(h_last[:, b], full[:, -1], rtol=1e-10, atol=1e-12)
+    ref_ent = oracle.layer_entropies(mw, shape, np.stack(
+        [oracle.forward_full(mw, shape, np.concatenate([prefix, toks[b]]))[:, -1] for b in range(wl.n_branches)], 1))
+    np.testing.assert_allclose(ent_full, ref_ent, atol=1e-10)
+
+
+def test_tau_zero_is_full_depth_forward():
+    wl, mw, prefix, toks = _tiny_inputs("tiny_deep")
+    shape = wl.model
+    pk, pv, _ = oracle.prefill(mw, shape, prefix)
+    ent, ex, hid, ent_full, h_last = oracle.verify_forward(mw, shape, pk, pv, toks, 0.0, 1)
+    assert np.all(ex == shape.n_layers)
+    assert not np.isnan(ent).any() and not np.isnan(hid).any()
+    np.testing.assert_array_equal(ent, ent_full)
+    np.testing.assert_array_equal(hid, h_last)
+    # With a finite tau, the outputs agree up to each exit and are NaN after it.
+    ent2, ex2, hid2, _, _ = oracle.verify_forward(mw, shape, pk, pv, toks, 10.0, 1)
+    assert np.all(ex2 == 2)
+    np.testing.assert_array_equal(ent2[:2], ent[:2])
+    assert np.isnan(ent2[2:]).all() and np.isnan(hid2[2:]).all()
+
+
+def test_branches_are_independent():
+    wl, mw, prefix, toks = _tiny_inputs("tiny")
+    shape = wl.model
+    pk, pv, _ = oracle.prefill(mw, shape, prefix)
+    _, _, _, e1, h1 = oracle.verify_forward(mw, shape, pk, pv, toks, 0.0, 1)
+    perm = np.array([2, 0, 3, 1])
+    _, _, _, e2, h2 = oracle.verify_forward(mw, shape, pk, pv, toks[perm], 0.0, 1)
+    np.testing.assert_allclose(e2, e1[:, perm], atol=1e-12)
+    np.testing.assert_allclose(h2, h1[:, perm], atol=1e-12)
+    # identical branches -> ASKS similarity 1 between them
+    same = np.stack([toks[0], toks[1], toks[0]])
+    _, _, _, _, h3 = oracle.verify_forward(mw, shape, pk, pv, same, 0.0, 1)
+    S = oracle.asks_similarity(h3, wl.alpha)
+    assert abs(S[0, 2] - 1.0) < 1e-12 and S[0, 1] < 0.999
+
+
+def test_zero_lm_head_gives_log_vocab_every_layer():
+    wl, mw, prefix, toks = _tiny_inputs("tiny_deep")
+    shape = wl.model
+    mw.lm_head = torch.zeros_like(mw.lm_head)
+    pk, pv, _ = oracle.prefill(mw, shape, prefix)
+    ent, ex, _, _, _ = oracle.verify_forward(mw, shape, pk, pv, toks, 0.0, 1)
+    np.testing.assert_allclose(ent, math.log(shape.vocab), rtol=0, atol=1e-12)
+    # Every delta is 0 after layer 1, so any tau > 0 exits at 1 + patience.
+    _, ex, _, _, _ = oracle.verify_forward(mw, shape, pk, pv, toks, 1e-9, 2)
+    assert np.all(ex == 3)
