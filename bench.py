@@ -1,0 +1,322 @@
+#!/usr/bin/env python3
+"""Benchmark of the RKSC verify pass on one MI355X.
+
+One step = one rksc_verify_forward call over the whole workload: every layer of
+the multi-branch forward over the shared prefix cache, the fused
+lm_head-entropy probe after every layer and the exit rule (branches that exit
+stop being computed). Inputs (random-init bf16 weights, synthetic prefix K/V,
+uniform tokens) are generated on the GPU and are resident in HBM before the
+timed region; the workspace and outputs are allocated once.
+
+Prints ONE JSON line on stdout (progress goes to stderr):
+  value        verify tokens/s = n_branches * branch_len / step time
+  roofline     the dominant kernel (fused lm_head-entropy at the default
+               workload) against the HBM peak, timed with HIP events recorded
+               around its launches inside the timed steps
+  kernels      the same measurement for the projections and the attention
+  full_depth   the same workload with tau = 0 (no exit)
+  cpu_baseline the float64 CPU oracle on a bounded sample of the workload
+
+    python bench.py [--steps K] [--warmup W] [--workload 7b_single]
+"""
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "verify tokens/s at 7B shape w/ entropy exit; % peak HBM BW and MFMA util"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 vector / MFMA
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """hipEvent_t handles through the HIP runtime (events recorded by librksc on the call's stream)."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self, n):
+        evs = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            rc = self.lib.hipEventCreate(ctypes.byref(e))
+            if rc != 0:
+                raise RuntimeError(f"hipEventCreate failed ({rc})")
+            evs.append(e.value)
+        return evs
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        rc = self.lib.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b))
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return ms.value
+
+    def destroy(self, evs):
+        for e in evs:
+            self.lib.hipEventDestroy(ctypes.c_void_p(e))
+
+
+def kernel_work(shape, B_live, n, s):
+    """Algorithmic bytes and flops per launch of each timed kernel class at B_live live branches."""
+    d, H, Hkv, hd, F, V = shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.d_ff, shape.vocab
+    T = 2 if shape.dtype == "bf16" else 4
+    M = B_live * s
+    Nqkv = (H + 2 * Hkv) * hd
+
+    def gemm(N, K):
+        # weights + activation in + fp32 result out
+        return {"bytes": N * K * T + M * K * T + M * N * 4, "flops": 2.0 * M * N * K}
+
+    attn_flops = 4.0 * hd * H * B_live * (s * n + s * (s + 1) / 2)
+    attn_bytes = 2 * Hkv * n * hd * T + B_live * 2 * Hkv * s * hd * T + 2 * M * H * hd * T
+    return {
+        "qkv_proj": gemm(Nqkv, d), "o_proj": gemm(d, H * hd), "gate_up_proj": gemm(2 * F, d),
+        "down_proj": gemm(d, F), "attention": {"bytes": attn_bytes, "flops": attn_flops},
+        # W_lm once, the hi+lo bf16 normalised rows, the per-workgroup statistics
+        "lm_head_entropy": {"bytes": V * d * T + B_live * d * 4, "flops": 2.0 * B_live * V * d},
+    }
+
+
+EVENT_SLOTS = {"qkv_proj": 0, "attention": 2, "o_proj": 4, "gate_up_proj": 6, "down_proj": 8, "lm_head_entropy": 10}
+
+
+def cpu_baseline(mw, kv, toks, wl, layers):
+    """Float64 oracle on the first `layers` layers of the same workload; time scaled to all layers."""
+    import dataclasses
+
+    import oracle
+    from threadpoolctl import threadpool_info
+
+    shape = mw.shape
+    sub = dataclasses.replace(shape, n_layers=layers)
+
+    class Host:
+        pass
+
+    host = Host()
+    host.embed = mw.embed.cpu()
+    host.layers = [{k: v.cpu() for k, v in mw.layers[i].items()} for i in range(layers)]
+    host.final_norm = mw.final_norm.cpu()
+    host.lm_head = mw.lm_head.cpu()
+    pk, pv = kv.k[:layers].cpu(), kv.v[:layers].cpu()
+    t_np = toks.cpu().numpy()
+    t0 = time.perf_counter()
+    oracle.verify_forward(host, sub, pk, pv, t_np, wl.tau, wl.patience)
+    dt = time.perf_counter() - t0
+    per_step = dt * shape.n_layers / layers
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    tokens = wl.n_branches * wl.branch_len
+    return {
+        "value": tokens / per_step, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+        "sample": (f"float64 oracle verify pass over the first {layers} of {shape.n_layers} layers of the same "
+                   f"workload ({wl.n_branches} branch(es) x {wl.branch_len} tokens, {kv.k.shape[2]}-token prefix), "
+                   f"{dt:.1f} s, time scaled by {shape.n_layers}/{layers}"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="7b_single")
+    ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--patience", type=int, default=None)
+    ap.add_argument("--seed", type=int, default=42)
+    ap.add_argument("--cpu-layers", type=int, default=4, help="layers in the oracle's bounded sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-full-depth", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the verify pass runs on a single MI355X (no multi-GPU path); "
+              "run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2606_09937_amd as rk
+    import workloads
+
+    wl = workloads.get(args.workload)
+    if args.tau is not None or args.patience is not None:
+        wl = wl.with_(tau=wl.tau if args.tau is None else args.tau,
+                      patience=wl.patience if args.patience is None else args.patience)
+    shape = wl.model
+    B, n, s, L = wl.n_branches, wl.prefix_len, wl.branch_len, shape.n_layers
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    log(f"workload {wl.name}: {wl.description}; generating inputs on {torch.cuda.get_device_name(0)}")
+    t0 = time.perf_counter()
+    mw = workloads.make_model(shape, seed=args.seed, device=dev)
+    kv = workloads.make_prefix_kv(shape, n, seed=args.seed, device=dev)
+    toks = workloads.make_tokens(B * s, shape.vocab, seed=args.seed, device=dev).reshape(B, s).contiguous()
+    ws = torch.empty(rk.rksc_verify_workspace_size(shape, B, s), dtype=torch.uint8, device=dev)
+    ent = torch.empty((L, B), dtype=torch.float32, device=dev)
+    ex = torch.empty((B,), dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    log(f"inputs ready in {time.perf_counter() - t0:.1f} s; workspace {ws.numel() / 2**20:.1f} MiB")
+
+    lib = rk.load_library()
+    w_struct, keep = rk._weights_struct(mw)
+    kv_struct = rk.PrefixKV(n, rk._ptr(kv.k), rk._ptr(kv.v))
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    common = (ctypes.byref(w_struct), ctypes.byref(kv_struct), rk._ptr(toks), B, s)
+
+    def step(tau, patience, events=None):
+        if events is None:
+            st = lib.rksc_verify_forward(*common, float(tau), int(patience), rk._ptr(ent), rk._ptr(ex), None,
+                                         rk._ptr(ws), ws.numel(), sp)
+        else:
+            st = lib.rksc_verify_forward_profiled(*common, float(tau), int(patience), rk._ptr(ent), rk._ptr(ex),
+                                                  None, rk._ptr(ws), ws.numel(), sp, events)
+        if st != 0:
+            raise RuntimeError(f"rksc_verify_forward failed: {rk.rksc_last_error()}")
+
+    lib.rksc_verify_forward_profiled.restype = ctypes.c_int32
+    lib.rksc_verify_forward_profiled.argtypes = list(lib.rksc_verify_forward.argtypes) + [ctypes.c_void_p]
+
+    for i in range(args.warmup):
+        step(wl.tau, wl.patience)
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    hip = HipEvents()
+    per_step = 12 * L
+    ev = hip.create(per_step * args.steps)
+    ev_arrays = [(ctypes.c_void_p * per_step)(*ev[k * per_step:(k + 1) * per_step]) for k in range(args.steps)]
+    ev_ptrs = [ctypes.cast(a, ctypes.c_void_p) for a in ev_arrays]
+    start, stop = hip.create(2)
+    torch.cuda.synchronize()
+    hip.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    hip.lib.hipEventRecord(ctypes.c_void_p(start), sp)
+    t_wall = time.perf_counter()
+    for k in range(args.steps):
+        step(wl.tau, wl.patience, ev_ptrs[k])
+    hip.lib.hipEventRecord(ctypes.c_void_p(stop), sp)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    total_ms = hip.elapsed_ms(start, stop)
+    ms_per_step = total_ms / args.steps
+    exits = ex.cpu().tolist()
+    tokens = B * s
+    value = tokens / (ms_per_step / 1e3)
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall / args.steps * 1e3:.3f} ms), "
+        f"{value:.1f} tokens/s, exit layers {exits}")
+
+    # Per-kernel durations inside the timed steps. Layers past every branch's exit
+    # run kernels that return at once; the roofline averages the layers still live.
+    live_layers = max(exits)
+    ent_cpu = ent.cpu()
+    kernels = {}
+    for name, slot in EVENT_SLOTS.items():
+        durs_live = []
+        for k in range(args.steps):
+            base = k * per_step
+            for l in range(live_layers):
+                durs_live.append(hip.elapsed_ms(ev[base + 12 * l + slot], ev[base + 12 * l + slot + 1]))
+        avg_ms = sum(durs_live) / len(durs_live)
+        kernels[name] = {"avg_us": avg_ms * 1e3, "launches_timed": len(durs_live)}
+    # live branches per layer (all branches are live up to the first exit)
+    live_per_layer = [sum(1 for e in exits if e >= l + 1) for l in range(L)]
+    mean_live = sum(live_per_layer[:live_layers]) / live_layers
+    work = kernel_work(shape, max(1, round(mean_live)), n, s)
+    for name, rec in kernels.items():
+        wk = work[name]
+        sec = rec["avg_us"] * 1e-6
+        rec["hbm_gbs"] = wk["bytes"] / sec / 1e9
+        rec["tflops"] = wk["flops"] / sec / 1e12
+        rec["hbm_frac"] = rec["hbm_gbs"] / HBM_PEAK_GBS
+        peak = BF16_PEAK_TFLOPS if shape.dtype == "bf16" else FP32_PEAK_TFLOPS
+        rec["mfma_frac"] = rec["tflops"] / peak
+        rec["algorithmic_bytes"] = wk["bytes"]
+        rec["algorithmic_flops"] = wk["flops"]
+    shares = {k: v["avg_us"] * live_layers for k, v in kernels.items()}
+    dom = "lm_head_entropy" if shares["lm_head_entropy"] >= max(shares.values()) * 0.999 else max(shares, key=shares.get)
+    dk = kernels[dom]
+    gemm_like = dom.endswith("_proj") and work[dom]["flops"] / work[dom]["bytes"] > 315
+    roofline = {
+        "kernel": dom,
+        "bound": "mfma" if gemm_like else "hbm",
+        "achieved": dk["tflops"] if gemm_like else dk["hbm_gbs"],
+        "peak": BF16_PEAK_TFLOPS if gemm_like else HBM_PEAK_GBS,
+        "unit": "TFLOP/s" if gemm_like else "GB/s",
+        "traffic": None,
+        "avg_launch_us": dk["avg_us"],
+        "algorithmic_bytes_per_launch": work[dom]["bytes"],
+    }
+    roofline["frac"] = roofline["achieved"] / roofline["peak"]
+    hip.destroy(ev + [start, stop])
+
+    full_depth = None
+    if not args.no_full_depth:
+        for _ in range(max(1, args.warmup)):
+            step(0.0, 1)
+        torch.cuda.synchronize()
+        a, b = hip.create(2)
+        hip.lib.hipEventRecord(ctypes.c_void_p(a), sp)
+        for _ in range(args.steps):
+            step(0.0, 1)
+        hip.lib.hipEventRecord(ctypes.c_void_p(b), sp)
+        torch.cuda.synchronize()
+        fd_ms = hip.elapsed_ms(a, b) / args.steps
+        hip.destroy([a, b])
+        full_depth = {"tau": 0.0, "ms_per_step": fd_ms, "value": tokens / (fd_ms / 1e3), "unit": "tokens/s"}
+        log(f"full depth (tau=0): {fd_ms:.3f} ms/step, {full_depth['value']:.1f} tokens/s")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle on {args.cpu_layers} layer(s)")
+        cpu = cpu_baseline(mw, kv, toks, wl, min(args.cpu_layers, L))
+        log(f"cpu baseline: {cpu['value']:.3f} tokens/s on {cpu['cores']} threads")
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": shape.dtype,
+        "data": "synthetic: random-init weights N(0,0.02^2), synthetic prefix K/V, uniform tokens (seeded)",
+        "config": {
+            "workload": wl.name,
+            "description": wl.description,
+            "layers": L, "d_model": shape.d_model, "heads": shape.n_heads, "kv_heads": shape.n_kv_heads,
+            "head_dim": shape.head_dim, "d_ff": shape.d_ff, "vocab": shape.vocab,
+            "n_branches": B, "prefix_len": n, "branch_len": s, "tau": wl.tau, "patience": wl.patience,
+            "exit_layers": exits, "parallelism": "single GPU",
+        },
+        "roofline": roofline,
+        "kernels": kernels,
+        "full_depth": full_depth,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,156 @@
+/*
+ * rksc.h -- C ABI of the RKSC verify-pass library for MI355X (gfx950).
+ *
+ * RKSC (arXiv 2606.09937) verifies B reasoning branches that share one prefix.
+ * This library implements the verify pass of its layer-level early exit
+ * (Sec. 3.3 "Layer-level entropy exit", Alg. VerifyWithEntropyExit) over a
+ * prefix KV cache that is computed once and read by every branch
+ * (Sec. 3.2 "KV broadcast and batched decode"), and the layer-weighted cosine
+ * similarity of the ASKS gate (Eq. asks_sim, Alg. AsksGate).
+ *
+ * Conventions shared by every entry point:
+ *   - Tensor arguments are DEVICE pointers to dense row-major arrays.
+ *   - The caller owns all memory. The library allocates no device memory and
+ *     keeps no state between calls; the verify pass uses the caller's
+ *     workspace.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL is the default
+ *     stream). Outputs are valid once the stream is synchronised; inputs must
+ *     stay alive until then. Concurrent calls on different streams must use
+ *     different workspaces and outputs.
+ *   - Arguments are validated before anything is launched. On a non-OK
+ *     status nothing has been written and rksc_last_error() describes the
+ *     cause. A failing HIP launch returns RKSC_ERR_HIP.
+ *   - Results are deterministic: no floating-point atomics are used, so two
+ *     calls with the same inputs produce bitwise-identical outputs.
+ */
+#ifndef RKSC_H_
+#define RKSC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RKSC_ABI_VERSION 1
+
+/* Largest number of branches one verify call accepts. */
+#define RKSC_MAX_BRANCHES 64
+
+typedef enum {
+  RKSC_OK = 0,
+  RKSC_ERR_INVALID_ARGUMENT = -1,   /* NULL pointer, bad size or bad value */
+  RKSC_ERR_UNSUPPORTED = -2,        /* valid but outside what the kernels handle */
+  RKSC_ERR_WORKSPACE_TOO_SMALL = -3,
+  RKSC_ERR_HIP = -4                 /* a HIP runtime call or kernel launch failed */
+} rksc_status;
+
+/* Storage type of the weight matrices, the embedding, the lm_head and the
+ * prefix K/V. RMSNorm gains are always fp32. */
+typedef enum { RKSC_F32 = 0, RKSC_BF16 = 1 } rksc_dtype;
+
+/* Decoder shape. Pre-norm Llama-style blocks: RMSNorm, grouped-query attention
+ * with rotate-half RoPE, SwiGLU FFN, no biases, untied lm_head.
+ * Requirements: head_dim in {64, 128}; n_heads % n_kv_heads == 0;
+ * d_model, d_ff and n_heads*head_dim multiples of 8 (16-byte rows). */
+typedef struct {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t d_ff;
+  int32_t vocab;
+  float rms_eps;      /* RMSNorm: g * x / sqrt(mean(x^2) + rms_eps) */
+  float rope_base;    /* RoPE: theta_j = rope_base^(-2j/head_dim) */
+  int32_t dtype;      /* rksc_dtype */
+} rksc_model_config;
+
+/* One decoder layer; every pointer is a device pointer. */
+typedef struct {
+  const float* attn_norm;   /* [d] RMSNorm gain before attention */
+  const void* w_qkv;        /* [(H + 2*Hkv)*hd, d]: the q rows, then k rows, then v rows */
+  const void* w_o;          /* [d, H*hd] */
+  const float* ffn_norm;    /* [d] RMSNorm gain before the FFN */
+  const void* w_gate_up;    /* [2*F, d]: the gate rows, then the up rows */
+  const void* w_down;       /* [d, F] */
+} rksc_layer_weights;
+
+typedef struct {
+  rksc_model_config cfg;
+  const void* embed;                 /* [V, d] device */
+  const rksc_layer_weights* layers;  /* HOST array of n_layers entries */
+  const float* final_norm;           /* [d] device, RMSNorm gain before lm_head */
+  const void* lm_head;               /* [V, d] device */
+} rksc_weights;
+
+/* The shared prefix cache C = {(K^(l), V^(l))} of Eq. prefix_fwd, computed once
+ * for the n_prefix prefix tokens and read (never copied) by every branch. */
+typedef struct {
+  int32_t n_prefix;   /* n >= 0 */
+  const void* k;      /* [L, Hkv, n, hd], keys after RoPE at positions 0..n-1 */
+  const void* v;      /* [L, Hkv, n, hd] */
+} rksc_prefix_kv;
+
+int32_t rksc_abi_version(void);
+
+/* Bytes of workspace rksc_verify_forward needs for this shape; 0 if the shape
+ * is invalid (rksc_last_error() says why). */
+size_t rksc_verify_workspace_size(const rksc_model_config* cfg, int32_t n_branches,
+                                  int32_t branch_len);
+
+/*
+ * Verify pass with the layer-level entropy exit.
+ *
+ * Every branch b's tokens branch_tokens[b, 0..s-1] sit at positions n..n+s-1;
+ * each attends to the whole shared prefix and, causally, to its own earlier
+ * tokens (Sec. 3.2). After every layer l (1-based) the last token's hidden row
+ * h goes through the final RMSNorm and the lm_head, and its softmax entropy in
+ * nats H_l[b] is taken (Eq. entropy; the final norm is applied before the
+ * projection so that layer L gives the model's real output distribution).
+ * Exit rule (Sec. 3.3, condition (iii) with the entropy-stabilisation
+ * tolerance tau and a patience): with H_0 = +inf, a layer counts toward the
+ * streak when |H_l - H_{l-1}| < tau (strict) and resets it otherwise; branch b
+ * exits at the first layer whose streak reaches `patience` and is not
+ * computed beyond it. tau = 0 never exits (plain full-depth forward).
+ *
+ * branch_tokens  [B, s] int32 device, ids in [0, V) (not checked).
+ * n_branches     B in [1, RKSC_MAX_BRANCHES]; branch_len s >= 1.
+ * tau            >= 0 and not NaN (+inf allowed); patience >= 1.
+ * entropy        [L, B] fp32 device out: H_l[b] in nats, NaN for l > exit_layer[b].
+ * exit_layer     [B] int32 device out: 1-based exit layer, L if the rule never fired.
+ * hidden_last    [L, B, d] fp32 device out or NULL: layer-l output row of the
+ *                branch's last token (before the final norm), NaN rows after exit.
+ * workspace      device buffer of at least rksc_verify_workspace_size() bytes,
+ *                256-byte aligned; its contents on entry do not matter.
+ */
+rksc_status rksc_verify_forward(const rksc_weights* weights, const rksc_prefix_kv* prefix_kv,
+                                const int32_t* branch_tokens, int32_t n_branches,
+                                int32_t branch_len, float tau, int32_t patience,
+                                float* entropy, int32_t* exit_layer, float* hidden_last,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * ASKS similarity (Eq. asks_sim with the weights of Alg. AsksGate, generalised
+ * from branch-vs-root to all branch pairs):
+ *   w_l = exp(alpha*l/L) / sum_{l'=1..L} exp(alpha*l'/L),  l = 1..L
+ *   S[i][j] = sum_l w_l * <h_i^(l), h_j^(l)> / (|h_i^(l)| |h_j^(l)|)
+ * A zero row has cosine 0 with everything. To get the paper's sigma_b against
+ * the root, append the root's rows as one more "branch".
+ * hidden [L, B, d] fp32 device; S [B, B] fp32 device out.
+ * L >= 1, B >= 1, d >= 1, alpha finite.
+ */
+rksc_status rksc_asks_similarity(const float* hidden, int32_t n_layers, int32_t n_branches,
+                                 int32_t d_model, float alpha, float* S, void* stream);
+
+const char* rksc_status_string(rksc_status status);
+
+/* Detail of the last non-OK status returned on this thread ("" if none). */
+const char* rksc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RKSC_H_ */

@@ -1,0 +1,57 @@
+/*
+ * rksc_testing.h -- kernel-level entry points of librksc for unit tests.
+ *
+ * These expose single kernels of the verify pass so that tests can compare
+ * them one by one with a CPU reference. They follow the conventions of
+ * rksc.h (device pointers, asynchronous on `stream`, validation before any
+ * launch, rksc_last_error() on failure). They are not needed to run the verify
+ * pass and make no stability promise beyond RKSC_ABI_VERSION.
+ */
+#ifndef RKSC_TESTING_H_
+#define RKSC_TESTING_H_
+
+#include "rksc.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Dense projection as the verify pass runs it: for split z, P[z][m][n] =
+ * sum over the split's K range of A[m][k] * W[n][k]. A [M, K] and W [N, K] are
+ * of `dtype`; P is fp32 and must hold 8 * M * N floats. splits = 0 uses the
+ * library's own split-K plan for this shape; the number used is written to
+ * *splits_used (host pointer). K % 8 == 0. */
+rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* W, float* P, int32_t M, int32_t N,
+                           int32_t K, int32_t splits, int32_t* splits_used, void* stream);
+
+/* Shared-prefix attention of one layer for B branches of s tokens:
+ * q [B*s, H, hd]; prefix_k/prefix_v [Hkv, n, hd]; k_own/v_own [B, Hkv, s, hd];
+ * o [B*s, H*hd] out. All of `dtype`. `scratch` is a device buffer of at least
+ * 4096 bytes used for the control block. */
+rksc_status rksc_test_attention(int32_t dtype, const void* q, const void* prefix_k, const void* prefix_v,
+                                const void* k_own, const void* v_own, void* o, int32_t B, int32_t n,
+                                int32_t s, int32_t H, int32_t Hkv, int32_t hd, void* scratch, void* stream);
+
+/* Measurement variant of rksc_verify_forward: the same validation, kernels and
+ * launches, plus a HIP event recorded on `stream` right before and right after
+ * the launches named below, so that a benchmark can time single kernels inside
+ * the real sequence with hipEventElapsedTime. `events` is a HOST array of
+ * RKSC_PROFILE_EVENTS_PER_LAYER * n_layers hipEvent_t handles created by the
+ * caller; NULL entries are skipped. Per layer l the entries at
+ * l * RKSC_PROFILE_EVENTS_PER_LAYER + k are, for k =
+ *   0/1 QKV projection, 2/3 attention, 4/5 O projection, 6/7 gate|up
+ *   projection, 8/9 down projection, 10/11 fused lm_head-entropy.
+ * Events of layers a branch set never reaches are recorded too (their kernels
+ * exit at once). */
+#define RKSC_PROFILE_EVENTS_PER_LAYER 12
+rksc_status rksc_verify_forward_profiled(const rksc_weights* weights, const rksc_prefix_kv* prefix_kv,
+                                         const int32_t* branch_tokens, int32_t n_branches, int32_t branch_len,
+                                         float tau, int32_t patience, float* entropy, int32_t* exit_layer,
+                                         float* hidden_last, void* workspace, size_t workspace_bytes,
+                                         void* stream, void* const* events);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RKSC_TESTING_H_ */

@@ -1,0 +1,254 @@
+"""Python binding of librksc, the MI355X (gfx950) RKSC verify-pass library.
+
+The functions named like the C ABI (rksc_verify_forward, rksc_asks_similarity,
+...) only marshal torch device tensors into pointers and call the library;
+every step of the verify pass runs in the library's HIP kernels. torch is used
+for device memory and streams only. If librksc.so is not built, every call
+raises: there is no fallback path.
+
+Convenience wrappers (verify_forward, asks_similarity) allocate the outputs and
+the workspace with torch and call the C ABI.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+__all__ = [
+    "RkscError", "load_library", "library_path",
+    "rksc_abi_version", "rksc_verify_workspace_size", "rksc_verify_forward",
+    "rksc_asks_similarity", "rksc_status_string", "rksc_last_error",
+    "rksc_test_gemm", "rksc_test_attention",
+    "verify_forward", "asks_similarity", "model_config",
+    "RKSC_OK", "RKSC_ERR_INVALID_ARGUMENT", "RKSC_ERR_UNSUPPORTED",
+    "RKSC_ERR_WORKSPACE_TOO_SMALL", "RKSC_ERR_HIP", "RKSC_F32", "RKSC_BF16", "RKSC_MAX_BRANCHES",
+]
+
+RKSC_OK = 0
+RKSC_ERR_INVALID_ARGUMENT = -1
+RKSC_ERR_UNSUPPORTED = -2
+RKSC_ERR_WORKSPACE_TOO_SMALL = -3
+RKSC_ERR_HIP = -4
+RKSC_F32 = 0
+RKSC_BF16 = 1
+RKSC_MAX_BRANCHES = 64
+
+_PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+
+
+def library_path() -> str:
+    return os.path.join(_PKG_DIR, "librksc.so")
+
+
+class RkscError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"rksc status {status}: {message}")
+        self.status = status
+
+
+class ModelConfig(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("d_ff", ctypes.c_int32),
+        ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_float),
+        ("dtype", ctypes.c_int32),
+    ]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [
+        ("attn_norm", ctypes.c_void_p), ("w_qkv", ctypes.c_void_p), ("w_o", ctypes.c_void_p),
+        ("ffn_norm", ctypes.c_void_p), ("w_gate_up", ctypes.c_void_p), ("w_down", ctypes.c_void_p),
+    ]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [
+        ("cfg", ModelConfig), ("embed", ctypes.c_void_p), ("layers", ctypes.POINTER(LayerWeights)),
+        ("final_norm", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
+    ]
+
+
+class PrefixKV(ctypes.Structure):
+    _fields_ = [("n_prefix", ctypes.c_int32), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load_library():
+    """Load librksc.so from the package directory (raises if it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build it with `python -m paper_2606_09937_amd.build` "
+            "(the verify pass has no non-HIP implementation)")
+    lib = ctypes.CDLL(path)
+    vp, i32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+    lib.rksc_abi_version.restype = i32
+    lib.rksc_abi_version.argtypes = []
+    lib.rksc_verify_workspace_size.restype = sz
+    lib.rksc_verify_workspace_size.argtypes = [ctypes.POINTER(ModelConfig), i32, i32]
+    lib.rksc_verify_forward.restype = i32
+    lib.rksc_verify_forward.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32, i32,
+                                        vp, vp, vp, vp, sz, vp]
+    lib.rksc_asks_similarity.restype = i32
+    lib.rksc_asks_similarity.argtypes = [vp, i32, i32, i32, f32, vp, vp]
+    lib.rksc_status_string.restype = ctypes.c_char_p
+    lib.rksc_status_string.argtypes = [i32]
+    lib.rksc_last_error.restype = ctypes.c_char_p
+    lib.rksc_last_error.argtypes = []
+    lib.rksc_test_gemm.restype = i32
+    lib.rksc_test_gemm.argtypes = [i32, vp, vp, vp, i32, i32, i32, i32, ctypes.POINTER(i32), vp]
+    lib.rksc_test_attention.restype = i32
+    lib.rksc_test_attention.argtypes = [i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != RKSC_OK:
+        lib = load_library()
+        raise RkscError(status, lib.rksc_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to librksc must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def model_config(shape) -> ModelConfig:
+    """C config from any object with the decoder shape attributes (e.g. workloads.ModelShape)."""
+    return ModelConfig(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
+                       shape.d_ff, shape.vocab, float(shape.rms_eps), float(shape.rope_base),
+                       RKSC_BF16 if shape.dtype == "bf16" else RKSC_F32)
+
+
+def rksc_abi_version() -> int:
+    return int(load_library().rksc_abi_version())
+
+
+def rksc_status_string(status: int) -> str:
+    return load_library().rksc_status_string(status).decode()
+
+
+def rksc_last_error() -> str:
+    return load_library().rksc_last_error().decode()
+
+
+def rksc_verify_workspace_size(shape, n_branches: int, branch_len: int) -> int:
+    cfg = model_config(shape)
+    n = int(load_library().rksc_verify_workspace_size(ctypes.byref(cfg), n_branches, branch_len))
+    if n == 0:
+        raise RkscError(RKSC_ERR_INVALID_ARGUMENT, rksc_last_error())
+    return n
+
+
+def _weights_struct(weights):
+    shape = weights.shape
+    layers = (LayerWeights * len(weights.layers))()
+    for i, lw in enumerate(weights.layers):
+        layers[i] = LayerWeights(_ptr(lw["attn_norm"]), _ptr(lw["w_qkv"]), _ptr(lw["w_o"]), _ptr(lw["ffn_norm"]),
+                                 _ptr(lw["w_gate_up"]), _ptr(lw["w_down"]))
+    cfg = model_config(shape)
+    cfg.n_layers = len(weights.layers)
+    w = Weights(cfg, _ptr(weights.embed), layers, _ptr(weights.final_norm), _ptr(weights.lm_head))
+    return w, layers
+
+
+def rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, patience: int,
+                        entropy: torch.Tensor, exit_layer: torch.Tensor, hidden_last: Optional[torch.Tensor],
+                        workspace: torch.Tensor, stream=None) -> None:
+    """Marshal torch device tensors into rksc_verify_forward (asynchronous on `stream`).
+
+    weights: object with .shape (decoder shape), .embed, .layers (dicts of tensors), .final_norm, .lm_head.
+    prefix_k/prefix_v: [L, Hkv, n, hd] device tensors. branch_tokens: [B, s] int32 device.
+    """
+    lib = load_library()
+    w, layers_keepalive = _weights_struct(weights)
+    B, s = branch_tokens.shape
+    n = int(prefix_k.shape[2]) if prefix_k is not None else 0
+    kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
+    st = lib.rksc_verify_forward(ctypes.byref(w), ctypes.byref(kv), _ptr(branch_tokens), int(B), int(s),
+                                 float(tau), int(patience), _ptr(entropy), _ptr(exit_layer), _ptr(hidden_last),
+                                 _ptr(workspace), int(workspace.numel() * workspace.element_size()),
+                                 _stream(stream))
+    del layers_keepalive
+    _check(st)
+
+
+def rksc_asks_similarity(hidden: torch.Tensor, alpha: float, S: torch.Tensor, stream=None) -> None:
+    """Marshal hidden [L, B, d] fp32 and S [B, B] fp32 device tensors into rksc_asks_similarity."""
+    L, B, d = hidden.shape
+    _check(load_library().rksc_asks_similarity(_ptr(hidden), int(L), int(B), int(d), float(alpha), _ptr(S),
+                                               _stream(stream)))
+
+
+def rksc_test_gemm(A: torch.Tensor, W: torch.Tensor, splits: int = 0, stream=None):
+    """Kernel-level GEMM: returns the fp32 split partials [splits_used, M, N]."""
+    M, K = A.shape
+    N = W.shape[0]
+    dt = RKSC_BF16 if A.dtype == torch.bfloat16 else RKSC_F32
+    P = torch.empty((8, M, N), dtype=torch.float32, device=A.device)
+    used = ctypes.c_int32(0)
+    _check(load_library().rksc_test_gemm(dt, _ptr(A), _ptr(W), _ptr(P), M, N, K, splits, ctypes.byref(used),
+                                         _stream(stream)))
+    return P[: used.value]
+
+
+def rksc_test_attention(q, prefix_k, prefix_v, k_own, v_own, n_kv_heads: int, stream=None):
+    """Kernel-level shared-prefix attention: q [B*s, H, hd], prefix [Hkv, n, hd], own [B, Hkv, s, hd]."""
+    Ms, H, hd = q.shape
+    B, Hkv, s, _ = k_own.shape
+    n = int(prefix_k.shape[1]) if prefix_k is not None else 0
+    dt = RKSC_BF16 if q.dtype == torch.bfloat16 else RKSC_F32
+    o = torch.empty((Ms, H * hd), dtype=q.dtype, device=q.device)
+    scratch = torch.empty(4096, dtype=torch.uint8, device=q.device)
+    _check(load_library().rksc_test_attention(dt, _ptr(q), _ptr(prefix_k), _ptr(prefix_v), _ptr(k_own),
+                                              _ptr(v_own), _ptr(o), B, n, s, H, Hkv, hd, _ptr(scratch),
+                                              _stream(stream)))
+    return o
+
+
+def verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, patience: int,
+                   return_hidden: bool = False, workspace: Optional[torch.Tensor] = None, stream=None):
+    """Allocate outputs (and the workspace unless given) and run the verify pass.
+
+    Returns (entropy [L, B] fp32, exit_layer [B] int32[, hidden_last [L, B, d] fp32]) on the device.
+    """
+    shape = weights.shape
+    B, s = branch_tokens.shape
+    dev = branch_tokens.device
+    L = len(weights.layers)
+    if workspace is None:
+        workspace = torch.empty(rksc_verify_workspace_size(shape, B, s), dtype=torch.uint8, device=dev)
+    entropy = torch.empty((L, B), dtype=torch.float32, device=dev)
+    exit_layer = torch.empty((B,), dtype=torch.int32, device=dev)
+    hidden = torch.empty((L, B, shape.d_model), dtype=torch.float32, device=dev) if return_hidden else None
+    rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau, patience, entropy, exit_layer, hidden,
+                        workspace, stream)
+    return (entropy, exit_layer, hidden) if return_hidden else (entropy, exit_layer)
+
+
+def asks_similarity(hidden: torch.Tensor, alpha: float, stream=None) -> torch.Tensor:
+    L, B, d = hidden.shape
+    S = torch.empty((B, B), dtype=torch.float32, device=hidden.device)
+    rksc_asks_similarity(hidden, alpha, S, stream)
+    return S

@@ -1,0 +1,87 @@
+// Device-side helpers shared by the gfx950 kernels: bf16 conversion, vector
+// types, wavefront reductions and the MFMA operand types.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rksc {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t u) {
+  return __uint_as_float(static_cast<uint32_t>(u) << 16);
+}
+
+// Round-to-nearest-even fp32 -> bf16 bits (finite inputs; NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(bf16 v) { return static_cast<float>(v); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) {
+  uint16_t b = f32_to_bf16_bits(v);
+  return __builtin_bit_cast(bf16, b);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+
+// Block-wide sum for blockDim.x a multiple of 64 (<= 1024); every thread gets the result.
+// Fixed reduction order, so the result is deterministic.
+__device__ __forceinline__ float block_sum(float v, float* smem /* >= 16 floats */) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) smem[wid] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += smem[i];
+  return t;
+}
+
+// Online softmax statistics of a set of logits z: m = max z,
+// s = sum exp(z - m), t = sum exp(z - m) * (z - m). Entropy = log(s) - t/s.
+struct EntStats {
+  float m, s, t;
+};
+
+__device__ __forceinline__ EntStats ent_empty() { return {-INFINITY, 0.f, 0.f}; }
+
+// Merge of two statistic triples (associative up to rounding).
+__device__ __forceinline__ EntStats ent_merge(EntStats a, EntStats b) {
+  if (b.m == -INFINITY) return a;
+  if (a.m == -INFINITY) return b;
+  const float m = fmaxf(a.m, b.m);
+  const float da = a.m - m, db = b.m - m;
+  const float ea = __expf(da), eb = __expf(db);
+  EntStats r;
+  r.m = m;
+  r.s = a.s * ea + b.s * eb;
+  r.t = (a.t + a.s * da) * ea + (b.t + b.s * db) * eb;
+  return r;
+}
+
+}  // namespace rksc

@@ -1,0 +1,64 @@
+// ASKS similarity (Eq. asks_sim with the exponential layer weights of
+// Alg. AsksGate), for every pair of branches:
+//   S[i][j] = sum_l w_l <h_i^l, h_j^l> / (|h_i^l| |h_j^l|),
+//   w_l = exp(alpha l / L) / sum_l' exp(alpha l' / L), l = 1..L.
+// One workgroup per pair (i, j). For each layer it reduces the dot product and
+// both squared norms in one pass over d with a fixed reduction order, so
+// S[i][j] and S[j][i] are computed identically (S is exactly symmetric).
+#include "common.h"
+#include "kernels.h"
+
+namespace rksc {
+
+namespace {
+
+__global__ __launch_bounds__(256) void k_asks(const float* __restrict__ hidden, int L, int B, int d, float alpha,
+                                              float* __restrict__ S) {
+  __shared__ float red[3][4];
+  const int i = blockIdx.x, j = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  // Weights in double with the largest exponent subtracted (no overflow for large |alpha|).
+  const double a = (double)alpha;
+  const double top = a >= 0.0 ? a : a / (double)L;
+  double wsum = 0.0;
+  for (int l = 1; l <= L; ++l) wsum += exp(a * (double)l / (double)L - top);
+  float acc = 0.f;
+  for (int l = 0; l < L; ++l) {
+    const float* hi = hidden + ((size_t)l * B + i) * d;
+    const float* hj = hidden + ((size_t)l * B + j) * d;
+    float dot = 0.f, ni = 0.f, nj = 0.f;
+    for (int k = tid; k < d; k += 256) {
+      const float x = hi[k], y = hj[k];
+      dot = fmaf(x, y, dot);
+      ni = fmaf(x, x, ni);
+      nj = fmaf(y, y, nj);
+    }
+    dot = wave_sum(dot);
+    ni = wave_sum(ni);
+    nj = wave_sum(nj);
+    if (lane == 0) {
+      red[0][wid] = dot;
+      red[1][wid] = ni;
+      red[2][wid] = nj;
+    }
+    __syncthreads();
+    dot = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    ni = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    nj = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
+    __syncthreads();
+    // The two norms enter symmetrically (ni*nj), so S[i][j] == S[j][i] bit for bit.
+    const float cosv = (ni > 0.f && nj > 0.f) ? dot / sqrtf(ni * nj) : 0.f;
+    const float w = (float)(exp(a * (double)(l + 1) / (double)L - top) / wsum);
+    acc = fmaf(w, cosv, acc);
+  }
+  if (tid == 0) S[(size_t)i * B + j] = acc;
+}
+
+}  // namespace
+
+hipError_t launch_asks(const float* hidden, int L, int B, int d, float alpha, float* S, hipStream_t st) {
+  hipLaunchKernelGGL(k_asks, dim3(B, B), dim3(256), 0, st, hidden, L, B, d, alpha, S);
+  return hipGetLastError();
+}
+
+}  // namespace rksc

@@ -1,0 +1,199 @@
+// Dense projections of the decoder layer: P[split][m][n] = sum_k A[m][k] * W[n][k]
+// over the split's K range. A is the [rows, K] activation, W a [N, K] weight
+// (torch Linear layout), P fp32. Split partials are summed by the consumer.
+//
+// bf16: CDNA4 MFMA (v_mfma_f32_16x16x32_bf16, fp32 accumulate), LDS double
+// buffered. Both operands are K-contiguous, so every lane reads its fragment
+// as one 16-byte LDS load. Within a 64-wide K tile, lane group g (= lane / 16)
+// supplies k = 16g + 8ks + e in substep ks (e = 0..7) -- the same permutation
+// for A and W, so the contraction is unchanged while each row's 4 lane groups
+// read 128 contiguous bytes.
+// fp32: a plain LDS-tiled FMA kernel (used by the fp32 models).
+#include "common.h"
+#include "kernels.h"
+
+namespace rksc {
+
+namespace {
+
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void k_gemm_bf16(const bf16* __restrict__ A, const bf16* __restrict__ W,
+                                                   float* __restrict__ P, size_t split_stride, const Ctrl* c,
+                                                   int s, int max_rows, int N, int K, int kps) {
+  constexpr int BK = 64, LDK = BK + 8;   // padded LDS rows: conflict-free 16-byte fragment reads
+  constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
+  constexpr int AC = BM * 8 / 256, BC = BN * 8 / 256;   // 16-byte chunks per thread per tile
+  __shared__ __attribute__((aligned(16))) bf16 As[2][BM * LDK];
+  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * LDK];
+
+  const int Ml = c ? min(c->live_count * s, max_rows) : max_rows;
+  const int m0 = blockIdx.y * BM;
+  if (m0 >= Ml) return;
+  const int n0 = blockIdx.x * BN;
+  const int kb = blockIdx.z * kps;
+  const int ke = min(K, kb + kps);
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm0 = (wid >> 1) * WM, wn0 = (wid & 1) * WN;
+  const int r16 = lane & 15, g = lane >> 4;
+
+  uint4 ra[AC], rb[BC];
+  const uint4 zero = make_uint4(0, 0, 0, 0);
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int j = 0; j < AC; ++j) {
+      const int idx = tid + 256 * j, row = idx >> 3, gk = k0 + (idx & 7) * 8, gr = m0 + row;
+      ra[j] = (gr < Ml && gk < ke) ? *reinterpret_cast<const uint4*>(A + (size_t)gr * K + gk) : zero;
+    }
+#pragma unroll
+    for (int j = 0; j < BC; ++j) {
+      const int idx = tid + 256 * j, row = idx >> 3, gk = k0 + (idx & 7) * 8, gr = n0 + row;
+      rb[j] = (gr < N && gk < ke) ? *reinterpret_cast<const uint4*>(W + (size_t)gr * K + gk) : zero;
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < AC; ++j) {
+      const int idx = tid + 256 * j;
+      *reinterpret_cast<uint4*>(&As[buf][(idx >> 3) * LDK + (idx & 7) * 8]) = ra[j];
+    }
+#pragma unroll
+    for (int j = 0; j < BC; ++j) {
+      const int idx = tid + 256 * j;
+      *reinterpret_cast<uint4*>(&Bs[buf][(idx >> 3) * LDK + (idx & 7) * 8]) = rb[j];
+    }
+  };
+
+  floatx4 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  gload(kb);
+  sstore(0);
+  __syncthreads();
+  int buf = 0;
+  for (int k0 = kb; k0 < ke; k0 += BK) {
+    const bool more = k0 + BK < ke;
+    if (more) gload(k0 + BK);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 af[TM], bw[TN];
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+        af[tm] = *reinterpret_cast<const bf16x8*>(&As[buf][(wm0 + 16 * tm + r16) * LDK + 16 * g + 8 * ks]);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+        bw[tn] = *reinterpret_cast<const bf16x8*>(&Bs[buf][(wn0 + 16 * tn + r16) * LDK + 16 * g + 8 * ks]);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+          acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[tm], bw[tn], acc[tm][tn], 0, 0, 0);
+    }
+    if (more) sstore(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
+
+  // Lane (r16, g) holds C[4g + i][r16] of each 16x16 tile.
+  float* out = P + blockIdx.z * split_stride;
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int col = n0 + wn0 + 16 * tn + r16;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = m0 + wm0 + 16 * tm + 4 * g + i;
+        if (row < Ml && col < N) out[(size_t)row * N + col] = acc[tm][tn][i];
+      }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, const float* __restrict__ W,
+                                                  float* __restrict__ P, size_t split_stride, const Ctrl* c,
+                                                  int s, int max_rows, int N, int K, int kps) {
+  constexpr int T = 64, BK = 16;
+  __shared__ float As[BK][T + 4];
+  __shared__ float Ws[BK][T + 4];
+  const int Ml = c ? min(c->live_count * s, max_rows) : max_rows;
+  const int m0 = blockIdx.y * T;
+  if (m0 >= Ml) return;
+  const int n0 = blockIdx.x * T;
+  const int kb = blockIdx.z * kps;
+  const int ke = min(K, kb + kps);
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  float acc[4][4] = {};
+  for (int k0 = kb; k0 < ke; k0 += BK) {
+    for (int j = 0; j < 4; ++j) {
+      const int idx = tid + 256 * j, row = idx / BK, kk = idx % BK, gk = k0 + kk;
+      As[kk][row] = (m0 + row < Ml && gk < ke) ? A[(size_t)(m0 + row) * K + gk] : 0.f;
+      Ws[kk][row] = (n0 + row < N && gk < ke) ? W[(size_t)(n0 + row) * K + gk] : 0.f;
+    }
+    __syncthreads();
+    for (int kk = 0; kk < BK; ++kk) {
+      float a[4], b[4];
+      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+      for (int j = 0; j < 4; ++j) b[j] = Ws[kk][tx * 4 + j];
+      for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+  float* out = P + blockIdx.z * split_stride;
+  for (int i = 0; i < 4; ++i) {
+    const int row = m0 + ty * 4 + i;
+    if (row >= Ml) continue;
+    for (int j = 0; j < 4; ++j) {
+      const int col = n0 + tx * 4 + j;
+      if (col < N) out[(size_t)row * N + col] = acc[i][j];
+    }
+  }
+}
+
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
+  GemmPlan p;
+  if (dt == DType::F32) {
+    p.bm = 64; p.bn = 64;
+  } else if (max_rows >= 512) {
+    p.bm = 128; p.bn = 128;
+  } else if (max_rows > 64) {
+    p.bm = 128; p.bn = 64;
+  } else {
+    p.bm = 64; p.bn = 64;
+  }
+  const int kstep = dt == DType::BF16 ? 64 : 16;
+  const int tiles = cdiv(N, p.bn) * cdiv(max_rows, p.bm);
+  int splits = 1;
+  while (tiles * splits < 256 && K / (splits * 2) >= 8 * kstep && splits < 8) splits *= 2;
+  const int ktiles = cdiv(K, kstep);
+  p.k_per_split = cdiv(ktiles, splits) * kstep;
+  p.splits = cdiv(K, p.k_per_split);
+  return p;
+}
+
+hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A, const void* W, float* P, size_t split_stride,
+                       const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st) {
+  const dim3 grid(cdiv(N, p.bn), cdiv(max_rows, p.bm), p.splits);
+  if (dt == DType::F32) {
+    hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, st, static_cast<const float*>(A),
+                       static_cast<const float*>(W), P, split_stride, c, s, max_rows, N, K, p.k_per_split);
+  } else if (p.bm == 128 && p.bn == 128) {
+    hipLaunchKernelGGL((k_gemm_bf16<128, 128>), grid, dim3(256), 0, st, static_cast<const bf16*>(A),
+                       static_cast<const bf16*>(W), P, split_stride, c, s, max_rows, N, K, p.k_per_split);
+  } else if (p.bm == 128 && p.bn == 64) {
+    hipLaunchKernelGGL((k_gemm_bf16<128, 64>), grid, dim3(256), 0, st, static_cast<const bf16*>(A),
+                       static_cast<const bf16*>(W), P, split_stride, c, s, max_rows, N, K, p.k_per_split);
+  } else {
+    hipLaunchKernelGGL((k_gemm_bf16<64, 64>), grid, dim3(256), 0, st, static_cast<const bf16*>(A),
+                       static_cast<const bf16*>(W), P, split_stride, c, s, max_rows, N, K, p.k_per_split);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace rksc

@@ -1,0 +1,78 @@
+// Internal launch interface between the C-ABI layer (rksc_api.cpp) and the
+// gfx950 kernels. Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace rksc {
+
+// Per-call control block in the workspace. Slots are the compacted positions of
+// the branches still being computed; `live_idx[slot]` is the caller's branch
+// index, `gather_src[new_slot]` the previous layer's slot of a survivor.
+struct Ctrl {
+  int live_count;
+  int pad0[63];
+  int live_idx[64];
+  int gather_src[64];
+  int streak[64];     // indexed by branch
+  float h_prev[64];   // indexed by branch
+  float h_cur[64];    // indexed by slot
+};
+
+enum class DType { F32 = 0, BF16 = 1 };
+
+// ---- setup
+hipError_t launch_init(Ctrl* c, int B, int L, float* entropy, int* exit_layer, float* hidden_last,
+                       size_t hidden_elems, hipStream_t st);
+hipError_t launch_rope_table(float2* tab, int s, int n, int hd, double base, hipStream_t st);
+hipError_t launch_embed(DType dt, const void* E, const int* tok, int V, float* x, int rows, int d,
+                        hipStream_t st);
+
+// ---- per-layer row kernels
+// x_out[r] = x_in[src(r)] + sum_sp P[sp][src(r)] ; xn[r] = RMSNorm(x_out[r]; gamma).
+// gather: src(r) = gather_src[r / s] * s + r % s, else src(r) = r (x_in may equal x_out).
+hipError_t launch_add_norm(DType dt, const float* x_in, const float* P, int nsplit, size_t split_stride,
+                           bool gather, const Ctrl* c, int s, float* x_out, void* xn, const float* gamma,
+                           int d, float eps, int max_rows, hipStream_t st);
+// q/k/v from the summed QKV partials with RoPE on q,k.
+hipError_t launch_qkv_post(DType dt, const float* P, int nsplit, size_t split_stride, const Ctrl* c,
+                           int s, int H, int Hkv, int hd, const float2* rope, void* q, void* k_own,
+                           void* v_own, int max_rows, hipStream_t st);
+// a = silu(gate) * up from the summed gate|up partials.
+hipError_t launch_swiglu_post(DType dt, const float* P, int nsplit, size_t split_stride, const Ctrl* c,
+                              int s, int F, void* a, int max_rows, hipStream_t st);
+// Last token of each live branch: h = x + sum_sp P; hidden_last[l][branch] = h;
+// hn = RMSNorm(h; final_norm) as fp32 (F32) or as a bf16 hi+lo pair (BF16).
+hipError_t launch_tap(DType dt, const float* x, const float* P, int nsplit, size_t split_stride,
+                      const Ctrl* c, int s, int d, int B, int layer0, float* hidden_last,
+                      const float* gamma, float eps, void* hn_a, void* hn_b, int max_branches,
+                      hipStream_t st);
+
+// ---- GEMM: P[split][m][n] = sum_{k in split} A[m][k] * W[n][k], rows m < live*s.
+struct GemmPlan {
+  int bm, bn, splits, k_per_split;
+};
+GemmPlan plan_gemm(DType dt, int max_rows, int N, int K);
+hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A, const void* W, float* P, size_t split_stride,
+                       const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st);
+
+// ---- attention over [shared prefix ; own causal span]
+hipError_t launch_attention(DType dt, const void* q, const void* pk, const void* pv, const void* k_own,
+                            const void* v_own, void* o, const Ctrl* c, int n, int s, int H, int Hkv, int hd,
+                            int max_branches, hipStream_t st);
+
+// ---- entropy of the live branches' last-token logits
+int entropy_parts(DType dt, int V, int max_branches);
+hipError_t launch_entropy(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c,
+                          int V, int d, int max_branches, float* parts, hipStream_t st);
+// Merges the partial statistics, writes entropy[l-1][branch], applies the exit
+// rule and compacts the live list.
+hipError_t launch_finalize_exit(const float* parts, int nparts, Ctrl* c, int layer1, int L, int B,
+                                float tau, int patience, float* entropy, int* exit_layer, hipStream_t st);
+
+// ---- ASKS similarity
+hipError_t launch_asks(const float* hidden, int L, int B, int d, float alpha, float* S, hipStream_t st);
+
+}  // namespace rksc

@@ -1,0 +1,331 @@
+// C ABI of librksc: argument validation, workspace layout and the layer loop of
+// the verify pass (all kernels are launched on the caller's stream; nothing is
+// allocated).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/rksc.h"
+#include "../../include/rksc_testing.h"
+#include "kernels.h"
+
+#define RKSC_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+thread_local std::string g_last_error;
+
+rksc_status fail(rksc_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+rksc_status ok() {
+  g_last_error.clear();
+  return RKSC_OK;
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+using rksc::DType;
+using rksc::GemmPlan;
+
+struct Layout {
+  size_t ctrl, x0, x1, act, ffn, q, kown, vown, pbig, pres, hn_a, hn_b, parts, rope, total;
+  GemmPlan qkv, o, gu, down;
+  int nparts;
+  int max_rows;
+};
+
+rksc_status check_config(const rksc_model_config* c) {
+  if (!c) return fail(RKSC_ERR_INVALID_ARGUMENT, "model config is NULL");
+  if (c->n_layers < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_layers must be >= 1 (got %d)", c->n_layers);
+  if (c->d_model < 8 || c->d_model % 8)
+    return fail(RKSC_ERR_UNSUPPORTED, "d_model must be a positive multiple of 8 (got %d)", c->d_model);
+  if (c->d_model > 65536) return fail(RKSC_ERR_UNSUPPORTED, "d_model above 65536 (got %d)", c->d_model);
+  if (c->n_heads < 1 || c->n_kv_heads < 1)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "head counts must be >= 1 (got %d, %d)", c->n_heads, c->n_kv_heads);
+  if (c->n_heads % c->n_kv_heads)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "n_heads %% n_kv_heads != 0 (%d, %d)", c->n_heads, c->n_kv_heads);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(RKSC_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", c->head_dim);
+  if (c->d_ff < 8 || c->d_ff % 8)
+    return fail(RKSC_ERR_UNSUPPORTED, "d_ff must be a positive multiple of 8 (got %d)", c->d_ff);
+  if (c->vocab < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "vocab must be >= 1 (got %d)", c->vocab);
+  if (!(c->rms_eps >= 0.f) || !std::isfinite(c->rms_eps))
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "rms_eps must be finite and >= 0");
+  if (!(c->rope_base > 0.f) || !std::isfinite(c->rope_base))
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "rope_base must be finite and > 0");
+  if (c->dtype != RKSC_F32 && c->dtype != RKSC_BF16)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "unknown dtype %d", c->dtype);
+  return RKSC_OK;
+}
+
+rksc_status make_layout(const rksc_model_config* c, int B, int s, Layout* lay) {
+  rksc_status st = check_config(c);
+  if (st != RKSC_OK) return st;
+  if (B < 1 || B > RKSC_MAX_BRANCHES)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "n_branches must be in [1, %d] (got %d)", RKSC_MAX_BRANCHES, B);
+  if (s < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_len must be >= 1 (got %d)", s);
+  if ((long long)B * s > (1 << 20))
+    return fail(RKSC_ERR_UNSUPPORTED, "n_branches * branch_len above 2^20 (got %lld)", (long long)B * s);
+  const DType dt = c->dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
+  const size_t T = dt == DType::BF16 ? 2 : 4;
+  const int d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, hd = c->head_dim, F = c->d_ff;
+  const int M = B * s;
+  const int Nqkv = (H + 2 * Hkv) * hd;
+  lay->max_rows = M;
+  lay->qkv = rksc::plan_gemm(dt, M, Nqkv, d);
+  lay->o = rksc::plan_gemm(dt, M, d, H * hd);
+  lay->gu = rksc::plan_gemm(dt, M, 2 * F, d);
+  lay->down = rksc::plan_gemm(dt, M, d, F);
+  lay->nparts = rksc::entropy_parts(dt, c->vocab, B);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  const size_t Ms = (size_t)M;
+  lay->ctrl = take(sizeof(rksc::Ctrl));
+  lay->x0 = take(Ms * d * 4);
+  lay->x1 = take(Ms * d * 4);
+  lay->act = take(Ms * (size_t)(d > H * hd ? d : H * hd) * T);
+  lay->ffn = take(Ms * F * T);
+  lay->q = take(Ms * H * hd * T);
+  lay->kown = take((size_t)B * Hkv * s * hd * T);
+  lay->vown = take((size_t)B * Hkv * s * hd * T);
+  const size_t pq = (size_t)lay->qkv.splits * Ms * Nqkv, pg = (size_t)lay->gu.splits * Ms * 2 * F;
+  lay->pbig = take((pq > pg ? pq : pg) * 4);
+  const int sres = lay->o.splits > lay->down.splits ? lay->o.splits : lay->down.splits;
+  lay->pres = take((size_t)sres * Ms * d * 4);
+  lay->hn_a = take((size_t)RKSC_MAX_BRANCHES * d * (dt == DType::BF16 ? 2 : 4));
+  lay->hn_b = take((size_t)RKSC_MAX_BRANCHES * d * 2);
+  lay->parts = take((size_t)lay->nparts * 64 * 3 * 4);
+  lay->rope = take((size_t)s * (hd / 2) * 8);
+  lay->total = off;
+  return RKSC_OK;
+}
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess)                                                               \
+      return fail(RKSC_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));         \
+  } while (0)
+
+}  // namespace
+
+RKSC_EXPORT int32_t rksc_abi_version(void) { return RKSC_ABI_VERSION; }
+
+RKSC_EXPORT const char* rksc_status_string(rksc_status s) {
+  switch (s) {
+    case RKSC_OK: return "ok";
+    case RKSC_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case RKSC_ERR_UNSUPPORTED: return "unsupported";
+    case RKSC_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case RKSC_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+RKSC_EXPORT const char* rksc_last_error(void) { return g_last_error.c_str(); }
+
+RKSC_EXPORT size_t rksc_verify_workspace_size(const rksc_model_config* cfg, int32_t n_branches,
+                                              int32_t branch_len) {
+  Layout lay;
+  if (make_layout(cfg, n_branches, branch_len, &lay) != RKSC_OK) return 0;
+  return lay.total;
+}
+
+namespace {
+
+// Shared body of rksc_verify_forward and rksc_verify_forward_profiled. `events`
+// (may be NULL) holds RKSC_PROFILE_EVENTS_PER_LAYER events per layer.
+rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const int32_t* branch_tokens,
+                        int32_t n_branches, int32_t branch_len, float tau, int32_t patience, float* entropy,
+                        int32_t* exit_layer, float* hidden_last, void* workspace, size_t workspace_bytes,
+                        void* stream, void* const* events) {
+  if (!w) return fail(RKSC_ERR_INVALID_ARGUMENT, "weights is NULL");
+  if (!kv) return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix_kv is NULL");
+  if (!branch_tokens) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_tokens is NULL");
+  if (!entropy) return fail(RKSC_ERR_INVALID_ARGUMENT, "entropy is NULL");
+  if (!exit_layer) return fail(RKSC_ERR_INVALID_ARGUMENT, "exit_layer is NULL");
+  if (!workspace) return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  if (std::isnan(tau) || tau < 0.f) return fail(RKSC_ERR_INVALID_ARGUMENT, "tau must be >= 0 and not NaN");
+  if (patience < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "patience must be >= 1 (got %d)", patience);
+  const rksc_model_config* c = &w->cfg;
+  Layout lay;
+  rksc_status st = make_layout(c, n_branches, branch_len, &lay);
+  if (st != RKSC_OK) return st;
+  if (workspace_bytes < lay.total)
+    return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
+  if (!w->embed || !w->final_norm || !w->lm_head || !w->layers)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "embed, final_norm, lm_head and layers must not be NULL");
+  for (int l = 0; l < c->n_layers; ++l) {
+    const rksc_layer_weights& lw = w->layers[l];
+    if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
+      return fail(RKSC_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
+  }
+  if (kv->n_prefix < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", kv->n_prefix);
+  if (kv->n_prefix > 0 && (!kv->k || !kv->v))
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix k/v are NULL with n_prefix = %d", kv->n_prefix);
+
+  const DType dt = c->dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
+  const size_t T = dt == DType::BF16 ? 2 : 4;
+  const int L = c->n_layers, d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, hd = c->head_dim;
+  const int F = c->d_ff, V = c->vocab, B = n_branches, s = branch_len, n = kv->n_prefix;
+  const int M = lay.max_rows;
+  const int Nqkv = (H + 2 * Hkv) * hd;
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  rksc::Ctrl* ctrl = reinterpret_cast<rksc::Ctrl*>(ws + lay.ctrl);
+  float* x0 = reinterpret_cast<float*>(ws + lay.x0);
+  float* x1 = reinterpret_cast<float*>(ws + lay.x1);
+  void* act = ws + lay.act;
+  void* ffn = ws + lay.ffn;
+  void* qb = ws + lay.q;
+  void* kown = ws + lay.kown;
+  void* vown = ws + lay.vown;
+  float* pbig = reinterpret_cast<float*>(ws + lay.pbig);
+  float* pres = reinterpret_cast<float*>(ws + lay.pres);
+  void* hn_a = ws + lay.hn_a;
+  void* hn_b = ws + lay.hn_b;
+  float* parts = reinterpret_cast<float*>(ws + lay.parts);
+  float2* rope = reinterpret_cast<float2*>(ws + lay.rope);
+  const size_t res_stride = (size_t)M * d;
+
+  HIP_TRY(rksc::launch_init(ctrl, B, L, entropy, exit_layer, hidden_last, (size_t)L * B * d, strm));
+  HIP_TRY(rksc::launch_rope_table(rope, s, n, hd, (double)c->rope_base, strm));
+  HIP_TRY(rksc::launch_embed(dt, w->embed, branch_tokens, V, x0, M, d, strm));
+
+  auto mark = [&](int l, int slot) -> hipError_t {
+    if (!events) return hipSuccess;
+    void* e = events[(size_t)l * RKSC_PROFILE_EVENTS_PER_LAYER + slot];
+    return e ? hipEventRecord(static_cast<hipEvent_t>(e), strm) : hipSuccess;
+  };
+  const char* pk_base = static_cast<const char*>(kv->k);
+  const char* pv_base = static_cast<const char*>(kv->v);
+  const size_t kv_layer = (size_t)Hkv * n * hd * T;
+  for (int l = 0; l < L; ++l) {
+    const rksc_layer_weights& lw = w->layers[l];
+    float* x_prev = (l % 2 == 0) ? x0 : x1;
+    float* x_cur = (l % 2 == 0) ? x1 : x0;
+    // Residual stream of the live rows (gathered), plus the previous layer's FFN output.
+    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, true, ctrl, s,
+                                  x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
+    HIP_TRY(mark(l, 0));
+    HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl, s, M, Nqkv, d, strm));
+    HIP_TRY(mark(l, 1));
+    HIP_TRY(rksc::launch_qkv_post(dt, pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
+                                  vown, M, strm));
+    const void* pk = n > 0 ? pk_base + l * kv_layer : nullptr;
+    const void* pv = n > 0 ? pv_base + l * kv_layer : nullptr;
+    HIP_TRY(mark(l, 2));
+    HIP_TRY(rksc::launch_attention(dt, qb, pk, pv, kown, vown, act, ctrl, n, s, H, Hkv, hd, B, strm));
+    HIP_TRY(mark(l, 3));
+    HIP_TRY(mark(l, 4));
+    HIP_TRY(rksc::launch_gemm(dt, lay.o, act, lw.w_o, pres, res_stride, ctrl, s, M, d, H * hd, strm));
+    HIP_TRY(mark(l, 5));
+    HIP_TRY(rksc::launch_add_norm(dt, x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
+                                  lw.ffn_norm, d, c->rms_eps, M, strm));
+    HIP_TRY(mark(l, 6));
+    HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, lw.w_gate_up, pbig, (size_t)M * 2 * F, ctrl, s, M, 2 * F, d, strm));
+    HIP_TRY(mark(l, 7));
+    HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
+    HIP_TRY(mark(l, 8));
+    HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, lw.w_down, pres, res_stride, ctrl, s, M, d, F, strm));
+    HIP_TRY(mark(l, 9));
+    HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, B, l, hidden_last,
+                             w->final_norm, c->rms_eps, hn_a, hn_b, B, strm));
+    HIP_TRY(mark(l, 10));
+    HIP_TRY(rksc::launch_entropy(dt, w->lm_head, hn_a, hn_b, ctrl, V, d, B, parts, strm));
+    HIP_TRY(mark(l, 11));
+    HIP_TRY(rksc::launch_finalize_exit(parts, lay.nparts, ctrl, l + 1, L, B, tau, patience, entropy, exit_layer,
+                                       strm));
+  }
+  return ok();
+}
+
+}  // namespace
+
+RKSC_EXPORT rksc_status rksc_verify_forward(const rksc_weights* w, const rksc_prefix_kv* kv,
+                                            const int32_t* branch_tokens, int32_t n_branches, int32_t branch_len,
+                                            float tau, int32_t patience, float* entropy, int32_t* exit_layer,
+                                            float* hidden_last, void* workspace, size_t workspace_bytes,
+                                            void* stream) {
+  return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
+                     hidden_last, workspace, workspace_bytes, stream, nullptr);
+}
+
+RKSC_EXPORT rksc_status rksc_verify_forward_profiled(const rksc_weights* w, const rksc_prefix_kv* kv,
+                                                     const int32_t* branch_tokens, int32_t n_branches,
+                                                     int32_t branch_len, float tau, int32_t patience,
+                                                     float* entropy, int32_t* exit_layer, float* hidden_last,
+                                                     void* workspace, size_t workspace_bytes, void* stream,
+                                                     void* const* events) {
+  if (!events) return fail(RKSC_ERR_INVALID_ARGUMENT, "events is NULL");
+  return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
+                     hidden_last, workspace, workspace_bytes, stream, events);
+}
+
+RKSC_EXPORT rksc_status rksc_asks_similarity(const float* hidden, int32_t n_layers, int32_t n_branches,
+                                             int32_t d_model, float alpha, float* S, void* stream) {
+  if (!hidden || !S) return fail(RKSC_ERR_INVALID_ARGUMENT, "hidden and S must not be NULL");
+  if (n_layers < 1 || n_branches < 1 || d_model < 1)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "L, B and d must be >= 1 (got %d, %d, %d)", n_layers, n_branches,
+                d_model);
+  if (n_branches > 65535) return fail(RKSC_ERR_UNSUPPORTED, "n_branches above 65535 (got %d)", n_branches);
+  if (!std::isfinite(alpha)) return fail(RKSC_ERR_INVALID_ARGUMENT, "alpha must be finite");
+  HIP_TRY(rksc::launch_asks(hidden, n_layers, n_branches, d_model, alpha, S, static_cast<hipStream_t>(stream)));
+  return ok();
+}
+
+// ------------------------------------------------------------------ kernel-level test entry points
+
+RKSC_EXPORT rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* W, float* P, int32_t M, int32_t N,
+                                       int32_t K, int32_t splits, int32_t* splits_used, void* stream) {
+  if (!A || !W || !P) return fail(RKSC_ERR_INVALID_ARGUMENT, "A, W and P must not be NULL");
+  if (dtype != RKSC_F32 && dtype != RKSC_BF16) return fail(RKSC_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (M < 1 || N < 1 || K < 8 || K % 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "bad shape %d x %d x %d", M, N, K);
+  if (splits < 0 || splits > 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "splits must be in [0, 8]");
+  const DType dt = dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
+  GemmPlan p = rksc::plan_gemm(dt, M, N, K);
+  if (splits > 0) {
+    const int kstep = dt == DType::BF16 ? 64 : 16;
+    const int ktiles = (K + kstep - 1) / kstep;
+    p.k_per_split = (ktiles + splits - 1) / splits * kstep;
+    p.splits = (K + p.k_per_split - 1) / p.k_per_split;
+  }
+  if (splits_used) *splits_used = p.splits;
+  HIP_TRY(rksc::launch_gemm(dt, p, A, W, P, (size_t)M * N, nullptr, 1, M, N, K, static_cast<hipStream_t>(stream)));
+  return ok();
+}
+
+RKSC_EXPORT rksc_status rksc_test_attention(int32_t dtype, const void* q, const void* prefix_k, const void* prefix_v,
+                                            const void* k_own, const void* v_own, void* o, int32_t B, int32_t n,
+                                            int32_t s, int32_t H, int32_t Hkv, int32_t hd, void* scratch,
+                                            void* stream) {
+  if (!q || !k_own || !v_own || !o || !scratch) return fail(RKSC_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if (n > 0 && (!prefix_k || !prefix_v)) return fail(RKSC_ERR_INVALID_ARGUMENT, "NULL prefix with n > 0");
+  if (dtype != RKSC_F32 && dtype != RKSC_BF16) return fail(RKSC_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (B < 1 || B > RKSC_MAX_BRANCHES || s < 1 || n < 0 || H < 1 || Hkv < 1 || H % Hkv)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "bad attention shape");
+  if (hd != 64 && hd != 128) return fail(RKSC_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  rksc::Ctrl* ctrl = static_cast<rksc::Ctrl*>(scratch);
+  HIP_TRY(rksc::launch_init(ctrl, B, 1, nullptr, nullptr, nullptr, 0, st));
+  HIP_TRY(rksc::launch_attention(dtype == RKSC_BF16 ? DType::BF16 : DType::F32, q, prefix_k, prefix_v, k_own, v_own,
+                                 o, ctrl, n, s, H, Hkv, hd, B, st));
+  return ok();
+}

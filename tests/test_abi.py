@@ -1,0 +1,143 @@
+"""The C ABI library loads, exports every declared symbol, and rejects bad
+arguments before touching the device. CPU only: no call here reaches a launch."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2606_09937_amd as rk
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails before any launch
+
+
+def _declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names |= set(re.findall(r"\b(rksc_\w+)\s*\(", text))
+    return sorted(names)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(rk.library_path()):
+        pytest.fail("librksc.so is not built (run __graft_entry__.build())")
+    return rk.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared_functions()
+    assert "rksc_verify_forward" in names and "rksc_asks_similarity" in names
+    for name in names:
+        assert hasattr(lib, name), f"{name} declared in include/ but not exported"
+    assert rk.rksc_abi_version() == 1
+
+
+def test_status_strings(lib):
+    assert rk.rksc_status_string(0) == "ok"
+    assert rk.rksc_status_string(-3) == "workspace too small"
+    assert rk.rksc_status_string(-4) == "HIP error"
+
+
+def _shape(**kw):
+    return workloads.get("tiny").model.__class__(**{**workloads.get("tiny").model.__dict__, **kw})
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(head_dim=96), "head_dim"),
+    (dict(n_heads=6, n_kv_heads=4), "n_heads"),
+    (dict(d_ff=690), "d_ff"),
+    (dict(d_model=250), "d_model"),
+    (dict(vocab=0), "vocab"),
+    (dict(n_layers=0), "n_layers"),
+])
+def test_workspace_size_rejects_bad_shapes(lib, kw, needle):
+    with pytest.raises(rk.RkscError) as e:
+        rk.rksc_verify_workspace_size(_shape(**kw), 4, 16)
+    assert needle in str(e.value)
+
+
+@pytest.mark.parametrize("B,s", [(0, 16), (65, 16), (4, 0)])
+def test_workspace_size_rejects_bad_batch(lib, B, s):
+    with pytest.raises(rk.RkscError):
+        rk.rksc_verify_workspace_size(workloads.get("tiny").model, B, s)
+
+
+def test_workspace_size_grows_with_batch(lib):
+    shape = workloads.get("tiny").model
+    a = rk.rksc_verify_workspace_size(shape, 1, 16)
+    b = rk.rksc_verify_workspace_size(shape, 4, 16)
+    c = rk.rksc_verify_workspace_size(shape, 4, 64)
+    assert 0 < a < b < c
+
+
+def _call(lib, shape, B=4, s=16, tau=0.05, patience=1, ws_bytes=None, ws_ptr=0x10000, null=None, n_prefix=8):
+    cfg = rk.model_config(shape)
+    layers = (rk.LayerWeights * shape.n_layers)()
+    for i in range(shape.n_layers):
+        layers[i] = rk.LayerWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    if null == "layer":
+        layers[shape.n_layers - 1] = rk.LayerWeights(FAKE, FAKE, None, FAKE, FAKE, FAKE)
+    w = rk.Weights(cfg, FAKE, layers, FAKE, None if null == "lm_head" else FAKE)
+    kv = rk.PrefixKV(n_prefix, None if null == "prefix" else FAKE, FAKE)
+    need = lib.rksc_verify_workspace_size(ctypes.byref(cfg), B, s) if 1 <= B <= 64 and s >= 1 else 0
+    size = need if ws_bytes is None else ws_bytes
+    args = [ctypes.byref(w), ctypes.byref(kv), None if null == "tokens" else FAKE, B, s, tau, patience,
+            None if null == "entropy" else FAKE, None if null == "exit" else FAKE, None,
+            ctypes.c_void_p(ws_ptr), size, None]
+    if null == "weights":
+        args[0] = None
+    return lib.rksc_verify_forward(*args)
+
+
+@pytest.mark.parametrize("null", ["weights", "tokens", "entropy", "exit", "lm_head", "layer", "prefix"])
+def test_verify_rejects_null_pointers(lib, null):
+    assert _call(lib, workloads.get("tiny").model, null=null) == rk.RKSC_ERR_INVALID_ARGUMENT
+    assert rk.rksc_last_error() != ""
+
+
+@pytest.mark.parametrize("tau,patience", [(float("nan"), 1), (-0.1, 1), (0.1, 0), (0.1, -3)])
+def test_verify_rejects_bad_rule(lib, tau, patience):
+    assert _call(lib, workloads.get("tiny").model, tau=tau, patience=patience) == rk.RKSC_ERR_INVALID_ARGUMENT
+
+
+def test_verify_rejects_small_or_misaligned_workspace(lib):
+    shape = workloads.get("tiny").model
+    cfg = rk.model_config(shape)
+    need = lib.rksc_verify_workspace_size(ctypes.byref(cfg), 4, 16)
+    assert _call(lib, shape, ws_bytes=need - 1) == rk.RKSC_ERR_WORKSPACE_TOO_SMALL
+    assert str(need) in rk.rksc_last_error()
+    assert _call(lib, shape, ws_ptr=0x10010) == rk.RKSC_ERR_INVALID_ARGUMENT
+
+
+@pytest.mark.parametrize("B,s,code", [(0, 16, rk.RKSC_ERR_INVALID_ARGUMENT), (65, 16, rk.RKSC_ERR_INVALID_ARGUMENT),
+                                      (4, 0, rk.RKSC_ERR_INVALID_ARGUMENT)])
+def test_verify_rejects_bad_batch(lib, B, s, code):
+    assert _call(lib, workloads.get("tiny").model, B=B, s=s, ws_bytes=1 << 30) == code
+
+
+def test_verify_rejects_unsupported_head_dim(lib):
+    shape = _shape(head_dim=32)
+    assert _call(lib, shape, ws_bytes=1 << 30) == rk.RKSC_ERR_UNSUPPORTED
+    assert "head_dim" in rk.rksc_last_error()
+
+
+def test_asks_rejects_bad_arguments(lib):
+    assert lib.rksc_asks_similarity(None, 2, 2, 8, 0.5, FAKE, None) == rk.RKSC_ERR_INVALID_ARGUMENT
+    assert lib.rksc_asks_similarity(FAKE, 0, 2, 8, 0.5, FAKE, None) == rk.RKSC_ERR_INVALID_ARGUMENT
+    assert lib.rksc_asks_similarity(FAKE, 2, 2, 8, math.inf, FAKE, None) == rk.RKSC_ERR_INVALID_ARGUMENT
+    assert lib.rksc_asks_similarity(FAKE, 2, 2, 8, math.nan, FAKE, None) == rk.RKSC_ERR_INVALID_ARGUMENT
+
+
+def test_testing_entry_points_reject_bad_shapes(lib):
+    used = ctypes.c_int32(0)
+    assert lib.rksc_test_gemm(1, FAKE, FAKE, FAKE, 4, 4, 12, 0, ctypes.byref(used), None) == \
+        rk.RKSC_ERR_INVALID_ARGUMENT
+    assert lib.rksc_test_attention(1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 4, 4, 4, 2, 32, FAKE, None) == \
+        rk.RKSC_ERR_UNSUPPORTED

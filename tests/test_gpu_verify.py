@@ -1,0 +1,155 @@
+"""Parity of the HIP verify pass (rksc_verify_forward through the C ABI) with the
+float64 oracle, on the same seeded inputs.
+
+Bars: exit_layer identical except where an oracle entropy delta lies within
+1e-2 nats of tau; entropy within 1e-2 nats; hidden rows within 2e-2 relative;
+outputs NaN exactly after each branch's exit.
+"""
+import dataclasses
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_09937_amd as rk
+import workloads
+from gpu_util import compare_verify, host_view, log, oracle_cfg, to_np
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+# Small bf16 decoders with ragged tails everywhere: d_ff and vocab not multiples
+# of the tiles, G = 4 and G = 7 grouped-query attention, odd branch counts.
+GQA_BF16 = workloads.ModelShape(n_layers=4, d_model=512, n_heads=8, n_kv_heads=2, head_dim=128, d_ff=1376,
+                                vocab=5000, dtype="bf16", lm_head_scale=6.0)
+G7_BF16 = workloads.ModelShape(n_layers=3, d_model=448, n_heads=7, n_kv_heads=1, head_dim=64, d_ff=1200,
+                               vocab=3001, dtype="bf16", lm_head_scale=6.0)
+
+
+def _inputs(shape, B, n, s, seed, device=DEV, n_layers=None):
+    mw = workloads.make_model(shape, seed=seed, device=device, n_layers=n_layers)
+    kv = workloads.make_prefix_kv(shape, n, seed=seed, device=device, n_layers=n_layers)
+    toks = workloads.make_tokens(B * s, shape.vocab, seed=seed, device=device).reshape(B, s).contiguous()
+    return mw, kv, toks
+
+
+def _run_gpu(mw, kv, toks, tau, patience):
+    ent, ex, hid = rk.verify_forward(mw, kv.k, kv.v, toks, tau, patience, return_hidden=True)
+    torch.cuda.synchronize()
+    return to_np(ent), to_np(ex), to_np(hid)
+
+
+def _run_oracle(mw, kv, toks, tau, patience, branches=None):
+    shape = mw.shape
+    L = len(mw.layers)
+    hv = host_view(mw)
+    t = toks.cpu().numpy()
+    if branches is not None:
+        t = t[branches]
+    _, ex, _, ent_full, hid_full = oracle.verify_forward(hv, oracle_cfg(shape, L), kv.k.cpu(), kv.v.cpu(), t,
+                                                         tau, patience)
+    return ent_full, hid_full, ex
+
+
+def _parity(mw, kv, toks, tau, patience, label, branches=None):
+    log(f"[{label}] gpu")
+    ent, ex, hid = _run_gpu(mw, kv, toks, tau, patience)
+    log(f"[{label}] oracle")
+    ent_ref, hid_ref, ex_ref = _run_oracle(mw, kv, toks, tau, patience, branches)
+    stats = compare_verify(ent, ex, hid, ent_ref, hid_ref, ex_ref, tau, branches=branches, label=label)
+    log(f"[{label}] exits gpu={ex.tolist()} oracle={ex_ref.tolist()} {stats}")
+    return ent, ex, hid, stats
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_deep"])
+def test_tiny_fp32_synthetic_prefix(name):
+    wl = workloads.get(name)
+    mw, kv, toks = _inputs(wl.model, wl.n_branches, wl.prefix_len, wl.branch_len, seed=42)
+    _parity(mw, kv, toks, wl.tau, wl.patience, name)
+
+
+def test_tiny_deep_fp32_prefill_prefix_and_exits():
+    """Prefix cache from the oracle's own root forward (Eq. prefix_fwd); several taus so exits fire."""
+    wl = workloads.get("tiny_deep")
+    shape = wl.model
+    mw = workloads.make_model(shape, seed=7, device=DEV)
+    prefix = workloads.make_tokens(wl.prefix_len, shape.vocab, seed=7, name="prefix").numpy()
+    pk, pv, _ = oracle.prefill(host_view(mw), shape, prefix)
+    kv = workloads.PrefixKV(torch.from_numpy(pk).float().to(DEV), torch.from_numpy(pv).float().to(DEV))
+    toks = workloads.make_tokens(wl.n_branches * wl.branch_len, shape.vocab, seed=7,
+                                 device=DEV).reshape(wl.n_branches, wl.branch_len).contiguous()
+    exits = set()
+    for tau, pat in ((wl.tau, wl.patience), (0.3, 1), (1.0, 2), (0.0, 1), (math.inf, 3)):
+        _, ex, _, _ = _parity(mw, kv, toks, tau, pat, f"tiny_deep_prefill tau={tau} p={pat}")
+        exits |= set(ex.tolist())
+    assert len(exits) > 1, "the sweep should produce more than one exit depth"
+
+
+@pytest.mark.parametrize("shape,B,n,s", [
+    (dataclasses.replace(workloads.get("tiny").model, dtype="bf16"), 4, 64, 16),
+    (dataclasses.replace(workloads.get("tiny_deep").model, dtype="bf16"), 3, 50, 21),
+    (GQA_BF16, 5, 100, 40),
+    (G7_BF16, 2, 129, 65),
+], ids=["tiny_bf16", "tiny_deep_bf16", "gqa_bf16", "g7_bf16"])
+def test_small_bf16(shape, B, n, s):
+    mw, kv, toks = _inputs(shape, B, n, s, seed=3)
+    for tau, pat in ((0.05, 1), (0.5, 1), (0.0, 1)):
+        _parity(mw, kv, toks, tau, pat, f"{shape.d_model}x{shape.n_layers} B={B} tau={tau}")
+
+
+def test_zero_lm_head_gives_log_vocab():
+    shape = GQA_BF16
+    mw, kv, toks = _inputs(shape, 3, 20, 9, seed=5)
+    mw.lm_head = torch.zeros_like(mw.lm_head)
+    ent, ex, _ = _run_gpu(mw, kv, toks, 0.0, 1)
+    np.testing.assert_allclose(ent, math.log(shape.vocab), rtol=0, atol=2e-5)
+    assert (ex == shape.n_layers).all()
+    ent, ex, _ = _run_gpu(mw, kv, toks, 1e-3, 2)    # every delta is 0 after layer 1
+    assert (ex == 3).all()
+
+
+def test_tau_extremes_and_nan_fill():
+    shape = GQA_BF16
+    mw, kv, toks = _inputs(shape, 4, 33, 17, seed=6)
+    ent0, ex0, hid0 = _run_gpu(mw, kv, toks, 0.0, 1)
+    assert (ex0 == shape.n_layers).all() and not np.isnan(ent0).any() and not np.isnan(hid0).any()
+    for pat in (1, 2, 5):
+        ent, ex, hid = _run_gpu(mw, kv, toks, math.inf, pat)
+        e = min(1 + pat, shape.n_layers)
+        assert (ex == e).all()
+        np.testing.assert_array_equal(ent[:e], ent0[:e])      # same arithmetic up to the exit
+        np.testing.assert_array_equal(hid[:e], hid0[:e])
+        assert np.isnan(ent[e:]).all() and np.isnan(hid[e:]).all()
+
+
+def test_deterministic_and_batch_position_invariant():
+    shape = GQA_BF16
+    mw, kv, toks = _inputs(shape, 5, 40, 24, seed=8)
+    a = _run_gpu(mw, kv, toks, 0.02, 1)
+    b = _run_gpu(mw, kv, toks, 0.02, 1)
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+    perm = torch.tensor([3, 0, 4, 2, 1], device=DEV)
+    c = _run_gpu(mw, kv, toks[perm].contiguous(), 0.0, 1)
+    ref = _run_gpu(mw, kv, toks, 0.0, 1)
+    p = perm.cpu().numpy()
+    np.testing.assert_allclose(c[0], ref[0][:, p], atol=1e-5)
+    np.testing.assert_allclose(c[2], ref[2][:, p], rtol=1e-5, atol=1e-5)
+
+
+def test_7b_single_full():
+    """The 7B-shape single-branch verify (32 layers, 1024-token prefix, 128 tokens) in full."""
+    wl = workloads.get("7b_single")
+    mw, kv, toks = _inputs(wl.model, wl.n_branches, wl.prefix_len, wl.branch_len, seed=42)
+    _parity(mw, kv, toks, wl.tau, wl.patience, "7b_single")
+
+
+@pytest.mark.parametrize("name,layers", [("7b_tot", 2), ("7b_large_vocab", 2), ("10b_long", 2)])
+def test_large_shapes_sampled_branches(name, layers):
+    """Full model width, branch count, prefix and span; first layers only; oracle on two branches."""
+    wl = workloads.get(name)
+    mw, kv, toks = _inputs(wl.model, wl.n_branches, wl.prefix_len, wl.branch_len, seed=42, n_layers=layers)
+    branches = [0, wl.n_branches - 1]
+    _parity(mw, kv, toks, wl.tau, wl.patience, name, branches=branches)
