@@ -17,17 +17,18 @@ extern "C" {
 #endif
 
 /* Dense projection as the verify pass runs it: for split z, P[z][m][n] =
- * sum over the split's K range of A[m][k] * W[n][k]. A [M, K] and W [N, K] are
- * of `dtype`; P is fp32 and must hold 8 * M * N floats. splits = 0 uses the
- * library's own split-K plan for this shape; the number used is written to
- * *splits_used (host pointer). K % 8 == 0. */
+ * sum over the split's K range of A[m][k] * W[n][k]. A [M, K] is fp32 (the
+ * activation), W [N, K] is of `dtype` (the weight); P is fp32 and must hold
+ * 8 * M * N floats. splits = 0 uses the library's own split-K plan for this
+ * shape; the number used is written to *splits_used (host pointer).
+ * K % 8 == 0. */
 rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* W, float* P, int32_t M, int32_t N,
                            int32_t K, int32_t splits, int32_t* splits_used, void* stream);
 
 /* Shared-prefix attention of one layer for B branches of s tokens:
- * q [B*s, H, hd]; prefix_k/prefix_v [Hkv, n, hd]; k_own/v_own [B, Hkv, s, hd];
- * o [B*s, H*hd] out. All of `dtype`. `scratch` is a device buffer of at least
- * 4096 bytes used for the control block. */
+ * q [B*s, H, hd], k_own/v_own [B, Hkv, s, hd] and the output o [B*s, H*hd] are
+ * fp32; prefix_k/prefix_v [Hkv, n, hd] are of `dtype`. `scratch` is a device
+ * buffer of at least 4096 bytes used for the control block. */
 rksc_status rksc_test_attention(int32_t dtype, const void* q, const void* prefix_k, const void* prefix_v,
                                 const void* k_own, const void* v_own, void* o, int32_t B, int32_t n,
                                 int32_t s, int32_t H, int32_t Hkv, int32_t hd, void* scratch, void* stream);

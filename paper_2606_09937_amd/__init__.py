@@ -202,10 +202,12 @@ def rksc_asks_similarity(hidden: torch.Tensor, alpha: float, S: torch.Tensor, st
 
 
 def rksc_test_gemm(A: torch.Tensor, W: torch.Tensor, splits: int = 0, stream=None):
-    """Kernel-level GEMM: returns the fp32 split partials [splits_used, M, N]."""
+    """Kernel-level GEMM: A [M, K] fp32, W [N, K] bf16 or fp32; returns the fp32 split partials."""
     M, K = A.shape
     N = W.shape[0]
-    dt = RKSC_BF16 if A.dtype == torch.bfloat16 else RKSC_F32
+    if A.dtype != torch.float32:
+        raise ValueError("A must be fp32")
+    dt = RKSC_BF16 if W.dtype == torch.bfloat16 else RKSC_F32
     P = torch.empty((8, M, N), dtype=torch.float32, device=A.device)
     used = ctypes.c_int32(0)
     _check(load_library().rksc_test_gemm(dt, _ptr(A), _ptr(W), _ptr(P), M, N, K, splits, ctypes.byref(used),
@@ -213,13 +215,14 @@ def rksc_test_gemm(A: torch.Tensor, W: torch.Tensor, splits: int = 0, stream=Non
     return P[: used.value]
 
 
-def rksc_test_attention(q, prefix_k, prefix_v, k_own, v_own, n_kv_heads: int, stream=None):
-    """Kernel-level shared-prefix attention: q [B*s, H, hd], prefix [Hkv, n, hd], own [B, Hkv, s, hd]."""
+def rksc_test_attention(q, prefix_k, prefix_v, k_own, v_own, dtype, stream=None):
+    """Kernel-level shared-prefix attention: q [B*s, H, hd], own [B, Hkv, s, hd] fp32; prefix [Hkv, n, hd]
+    of `dtype` (torch.bfloat16 or torch.float32). Returns o [B*s, H*hd] fp32."""
     Ms, H, hd = q.shape
     B, Hkv, s, _ = k_own.shape
     n = int(prefix_k.shape[1]) if prefix_k is not None else 0
-    dt = RKSC_BF16 if q.dtype == torch.bfloat16 else RKSC_F32
-    o = torch.empty((Ms, H * hd), dtype=q.dtype, device=q.device)
+    dt = RKSC_BF16 if dtype == torch.bfloat16 else RKSC_F32
+    o = torch.empty((Ms, H * hd), dtype=torch.float32, device=q.device)
     scratch = torch.empty(4096, dtype=torch.uint8, device=q.device)
     _check(load_library().rksc_test_attention(dt, _ptr(q), _ptr(prefix_k), _ptr(prefix_v), _ptr(k_own),
                                               _ptr(v_own), _ptr(o), B, n, s, H, Hkv, hd, _ptr(scratch),

@@ -27,6 +27,19 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
   return static_cast<uint16_t>(u >> 16);
 }
 
+// Split of an fp32 value into bf16 hi + lo (hi = RNE(x), lo = RNE(x - hi); x - hi
+// is exact in fp32). hi + lo carries x to ~2^-17 relative, and a bf16 value
+// times each part is exact in the MFMA's fp32 products, so two bf16 MFMAs give
+// an fp32-accurate product with a bf16 operand.
+__device__ __forceinline__ void split2(float x, uint16_t& hi, uint16_t& lo) {
+  hi = f32_to_bf16_bits(x);
+  lo = f32_to_bf16_bits(x - bf16_to_f32(hi));
+}
+
+__device__ __forceinline__ uint32_t pack2(uint16_t a, uint16_t b) {
+  return static_cast<uint32_t>(a) | (static_cast<uint32_t>(b) << 16);
+}
+
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(bf16 v) { return static_cast<float>(v); }
 

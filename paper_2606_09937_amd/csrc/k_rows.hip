@@ -286,40 +286,25 @@ hipError_t launch_embed(DType dt, const void* E, const int* tok, int V, float* x
   return hipGetLastError();
 }
 
-hipError_t launch_add_norm(DType dt, const float* x_in, const float* P, int nsplit, size_t split_stride,
-                           bool gather, const Ctrl* c, int s, float* x_out, void* xn, const float* gamma,
-                           int d, float eps, int max_rows, hipStream_t st) {
-  if (dt == DType::BF16)
-    hipLaunchKernelGGL(k_add_norm<bf16>, dim3(max_rows), dim3(256), 0, st, x_in, P, nsplit, split_stride,
-                       (int)gather, c, s, x_out, static_cast<bf16*>(xn), gamma, d, eps);
-  else
-    hipLaunchKernelGGL(k_add_norm<float>, dim3(max_rows), dim3(256), 0, st, x_in, P, nsplit, split_stride,
-                       (int)gather, c, s, x_out, static_cast<float*>(xn), gamma, d, eps);
-  return hipGetLastError();
-}
-
-hipError_t launch_qkv_post(DType dt, const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s,
-                           int H, int Hkv, int hd, const float2* rope, void* q, void* k_own, void* v_own,
+hipError_t launch_add_norm(const float* x_in, const float* P, int nsplit, size_t split_stride, bool gather,
+                           const Ctrl* c, int s, float* x_out, float* xn, const float* gamma, int d, float eps,
                            int max_rows, hipStream_t st) {
-  if (dt == DType::BF16)
-    hipLaunchKernelGGL(k_qkv_post<bf16>, dim3(max_rows), dim3(256), 0, st, P, nsplit, split_stride, c, s, H,
-                       Hkv, hd, rope, static_cast<bf16*>(q), static_cast<bf16*>(k_own),
-                       static_cast<bf16*>(v_own));
-  else
-    hipLaunchKernelGGL(k_qkv_post<float>, dim3(max_rows), dim3(256), 0, st, P, nsplit, split_stride, c, s, H,
-                       Hkv, hd, rope, static_cast<float*>(q), static_cast<float*>(k_own),
-                       static_cast<float*>(v_own));
+  hipLaunchKernelGGL(k_add_norm<float>, dim3(max_rows), dim3(256), 0, st, x_in, P, nsplit, split_stride,
+                     (int)gather, c, s, x_out, xn, gamma, d, eps);
   return hipGetLastError();
 }
 
-hipError_t launch_swiglu_post(DType dt, const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s,
-                              int F, void* a, int max_rows, hipStream_t st) {
-  if (dt == DType::BF16)
-    hipLaunchKernelGGL(k_swiglu_post<bf16>, dim3(max_rows), dim3(256), 0, st, P, nsplit, split_stride, c, s, F,
-                       static_cast<bf16*>(a));
-  else
-    hipLaunchKernelGGL(k_swiglu_post<float>, dim3(max_rows), dim3(256), 0, st, P, nsplit, split_stride, c, s, F,
-                       static_cast<float*>(a));
+hipError_t launch_qkv_post(const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s, int H,
+                           int Hkv, int hd, const float2* rope, float* q, float* k_own, float* v_own,
+                           int max_rows, hipStream_t st) {
+  hipLaunchKernelGGL(k_qkv_post<float>, dim3(max_rows), dim3(256), 0, st, P, nsplit, split_stride, c, s, H, Hkv,
+                     hd, rope, q, k_own, v_own);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_post(const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s, int F,
+                              float* a, int max_rows, hipStream_t st) {
+  hipLaunchKernelGGL(k_swiglu_post<float>, dim3(max_rows), dim3(256), 0, st, P, nsplit, split_stride, c, s, F, a);
   return hipGetLastError();
 }
 

@@ -78,7 +78,6 @@ rksc_status make_layout(const rksc_model_config* c, int B, int s, Layout* lay) {
   if ((long long)B * s > (1 << 20))
     return fail(RKSC_ERR_UNSUPPORTED, "n_branches * branch_len above 2^20 (got %lld)", (long long)B * s);
   const DType dt = c->dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
-  const size_t T = dt == DType::BF16 ? 2 : 4;
   const int d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, hd = c->head_dim, F = c->d_ff;
   const int M = B * s;
   const int Nqkv = (H + 2 * Hkv) * hd;
@@ -98,11 +97,12 @@ rksc_status make_layout(const rksc_model_config* c, int B, int s, Layout* lay) {
   lay->ctrl = take(sizeof(rksc::Ctrl));
   lay->x0 = take(Ms * d * 4);
   lay->x1 = take(Ms * d * 4);
-  lay->act = take(Ms * (size_t)(d > H * hd ? d : H * hd) * T);
-  lay->ffn = take(Ms * F * T);
-  lay->q = take(Ms * H * hd * T);
-  lay->kown = take((size_t)B * Hkv * s * hd * T);
-  lay->vown = take((size_t)B * Hkv * s * hd * T);
+  // Activations are fp32 for every model dtype.
+  lay->act = take(Ms * (size_t)(d > H * hd ? d : H * hd) * 4);
+  lay->ffn = take(Ms * F * 4);
+  lay->q = take(Ms * H * hd * 4);
+  lay->kown = take((size_t)B * Hkv * s * hd * 4);
+  lay->vown = take((size_t)B * Hkv * s * hd * 4);
   const size_t pq = (size_t)lay->qkv.splits * Ms * Nqkv, pg = (size_t)lay->gu.splits * Ms * 2 * F;
   lay->pbig = take((pq > pg ? pq : pg) * 4);
   const int sres = lay->o.splits > lay->down.splits ? lay->o.splits : lay->down.splits;
@@ -192,11 +192,11 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
   rksc::Ctrl* ctrl = reinterpret_cast<rksc::Ctrl*>(ws + lay.ctrl);
   float* x0 = reinterpret_cast<float*>(ws + lay.x0);
   float* x1 = reinterpret_cast<float*>(ws + lay.x1);
-  void* act = ws + lay.act;
-  void* ffn = ws + lay.ffn;
-  void* qb = ws + lay.q;
-  void* kown = ws + lay.kown;
-  void* vown = ws + lay.vown;
+  float* act = reinterpret_cast<float*>(ws + lay.act);
+  float* ffn = reinterpret_cast<float*>(ws + lay.ffn);
+  float* qb = reinterpret_cast<float*>(ws + lay.q);
+  float* kown = reinterpret_cast<float*>(ws + lay.kown);
+  float* vown = reinterpret_cast<float*>(ws + lay.vown);
   float* pbig = reinterpret_cast<float*>(ws + lay.pbig);
   float* pres = reinterpret_cast<float*>(ws + lay.pres);
   void* hn_a = ws + lay.hn_a;
@@ -222,12 +222,12 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     float* x_prev = (l % 2 == 0) ? x0 : x1;
     float* x_cur = (l % 2 == 0) ? x1 : x0;
     // Residual stream of the live rows (gathered), plus the previous layer's FFN output.
-    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, true, ctrl, s,
+    HIP_TRY(rksc::launch_add_norm(x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, true, ctrl, s,
                                   x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
     HIP_TRY(mark(l, 0));
     HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl, s, M, Nqkv, d, strm));
     HIP_TRY(mark(l, 1));
-    HIP_TRY(rksc::launch_qkv_post(dt, pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
+    HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
                                   vown, M, strm));
     const void* pk = n > 0 ? pk_base + l * kv_layer : nullptr;
     const void* pv = n > 0 ? pv_base + l * kv_layer : nullptr;
@@ -237,12 +237,12 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     HIP_TRY(mark(l, 4));
     HIP_TRY(rksc::launch_gemm(dt, lay.o, act, lw.w_o, pres, res_stride, ctrl, s, M, d, H * hd, strm));
     HIP_TRY(mark(l, 5));
-    HIP_TRY(rksc::launch_add_norm(dt, x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
+    HIP_TRY(rksc::launch_add_norm(x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
                                   lw.ffn_norm, d, c->rms_eps, M, strm));
     HIP_TRY(mark(l, 6));
     HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, lw.w_gate_up, pbig, (size_t)M * 2 * F, ctrl, s, M, 2 * F, d, strm));
     HIP_TRY(mark(l, 7));
-    HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
+    HIP_TRY(rksc::launch_swiglu_post(pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
     HIP_TRY(mark(l, 8));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, lw.w_down, pres, res_stride, ctrl, s, M, d, F, strm));
     HIP_TRY(mark(l, 9));

@@ -23,16 +23,18 @@ def _rand(shape, dtype, seed, std=1.0):
 ])
 def test_gemm_matches_fp64(dtype, M, N, K, splits):
     log(f"gemm {dtype} M={M} N={N} K={K} splits={splits}")
-    A = _rand((M, K), dtype, 1 + M, 0.5)
+    A = _rand((M, K), torch.float32, 1 + M, 0.5)     # activations are fp32 in every mode
     W = _rand((N, K), dtype, 2 + N, 0.05)
     P = rk.rksc_test_gemm(A.to(DEV), W.to(DEV), splits=splits)
     torch.cuda.synchronize()
     if splits:
-        assert P.shape[0] == splits
+        # a split never gets less than one K tile, so tiny K can use fewer splits than asked
+        assert 1 <= P.shape[0] <= splits
     got = P.double().sum(0).cpu().numpy()
     a = A.double().numpy()
     w = W.double().numpy()
     ref = a @ w.T
+    # fp32-level accuracy in both modes (bf16 weights meet a hi+lo split of A)
     bound = 1e-5 * (np.abs(a) @ np.abs(w).T) + 1e-7
     err = np.abs(got - ref)
     assert (err <= bound).all(), f"max err {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}"
@@ -48,16 +50,17 @@ def test_attention_matches_oracle(dtype, B, n, s, H, Hkv, hd):
         pytest.skip("fp32 kernel is the plain per-thread path; large shapes are covered in bf16")
     log(f"attention {dtype} B={B} n={n} s={s} H={H} Hkv={Hkv} hd={hd}")
     std = 1.28
-    q = _rand((B * s, H, hd), dtype, 10, std)
-    pk = _rand((Hkv, n, hd), dtype, 11, std)
+    f32 = torch.float32
+    q = _rand((B * s, H, hd), f32, 10, std)          # queries and the branch's own K/V are fp32
+    pk = _rand((Hkv, n, hd), dtype, 11, std)         # the shared prefix is in the model dtype
     pv = _rand((Hkv, n, hd), dtype, 12, std)
-    ko = _rand((B, Hkv, s, hd), dtype, 13, std)
-    vo = _rand((B, Hkv, s, hd), dtype, 14, std)
+    ko = _rand((B, Hkv, s, hd), f32, 13, std)
+    vo = _rand((B, Hkv, s, hd), f32, 14, std)
     o = rk.rksc_test_attention(q.to(DEV), pk.to(DEV) if n else None, pv.to(DEV) if n else None,
-                               ko.to(DEV), vo.to(DEV), Hkv)
+                               ko.to(DEV), vo.to(DEV), dtype)
     torch.cuda.synchronize()
     got = o.float().cpu().numpy().reshape(B, s, H, hd)
-    tol = 1e-2 if dtype == torch.bfloat16 else 1e-5
+    tol = 5e-5
     for b in range(B):
         qb = q[b * s:(b + 1) * s].float().numpy()
         kk = np.concatenate([pk.float().numpy(), ko[b].float().numpy()], axis=1)
