@@ -169,7 +169,7 @@ def main():
     mw = workloads.make_model(shape, seed=args.seed, device=dev)
     kv = workloads.make_prefix_kv(shape, n, seed=args.seed, device=dev)
     toks = workloads.make_tokens(B * s, shape.vocab, seed=args.seed, device=dev).reshape(B, s).contiguous()
-    ws = torch.empty(rk.rksc_verify_workspace_size(shape, B, s), dtype=torch.uint8, device=dev)
+    ws = torch.empty(rk.rksc_verify_workspace_size(shape, B, s, n), dtype=torch.uint8, device=dev)
     ent = torch.empty((L, B), dtype=torch.float32, device=dev)
     ex = torch.empty((B,), dtype=torch.int32, device=dev)
     torch.cuda.synchronize()

@@ -33,7 +33,7 @@
 extern "C" {
 #endif
 
-#define RKSC_ABI_VERSION 1
+#define RKSC_ABI_VERSION 2
 
 /* Largest number of branches one verify call accepts. */
 #define RKSC_MAX_BRANCHES 64
@@ -95,10 +95,11 @@ typedef struct {
 
 int32_t rksc_abi_version(void);
 
-/* Bytes of workspace rksc_verify_forward needs for this shape; 0 if the shape
- * is invalid (rksc_last_error() says why). */
+/* Bytes of workspace rksc_verify_forward needs for this shape (n_branches
+ * branches of branch_len tokens over an n_prefix-token prefix cache); 0 if the
+ * shape is invalid (rksc_last_error() says why). */
 size_t rksc_verify_workspace_size(const rksc_model_config* cfg, int32_t n_branches,
-                                  int32_t branch_len);
+                                  int32_t branch_len, int32_t n_prefix);
 
 /*
  * Verify pass with the layer-level entropy exit.

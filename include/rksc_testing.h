@@ -17,21 +17,28 @@ extern "C" {
 #endif
 
 /* Dense projection as the verify pass runs it: for split z, P[z][m][n] =
- * sum over the split's K range of A[m][k] * W[n][k]. A [M, K] is fp32 (the
- * activation), W [N, K] is of `dtype` (the weight); P is fp32 and must hold
- * 8 * M * N floats. splits = 0 uses the library's own split-K plan for this
- * shape; the number used is written to *splits_used (host pointer).
- * K % 8 == 0. */
-rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* W, float* P, int32_t M, int32_t N,
-                           int32_t K, int32_t splits, int32_t* splits_used, void* stream);
+ * sum over the split's K range of A[m][k] * W[n][k], W [N, K] of `dtype`.
+ * RKSC_BF16: the activation is given as its bf16 hi/lo planes A and A_lo
+ * ([M, K] each, A = hi + lo). RKSC_F32: A is fp32 [M, K], A_lo unused.
+ * P is fp32 and must hold 8 * M * N floats. splits = 0 uses the library's
+ * own split-K plan for this shape; the number used is written to
+ * *splits_used (host pointer). K % 8 == 0. */
+rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P, int32_t M,
+                           int32_t N, int32_t K, int32_t splits, int32_t* splits_used, void* stream);
 
-/* Shared-prefix attention of one layer for B branches of s tokens:
- * q [B*s, H, hd], k_own/v_own [B, Hkv, s, hd] and the output o [B*s, H*hd] are
- * fp32; prefix_k/prefix_v [Hkv, n, hd] are of `dtype`. `scratch` is a device
- * buffer of at least 4096 bytes used for the control block. */
+/* Shared-prefix attention of one layer for B branches of s tokens, with the
+ * same split of the prefix across workgroups as the verify pass:
+ * q [B*s, H, hd], k_own/v_own [B, Hkv, s, hd] are fp32 and prefix_k/prefix_v
+ * [Hkv, n, hd] of `dtype`. The output o [B*s, H*hd] is fp32 for RKSC_F32 and
+ * for RKSC_BF16 its bf16 hi/lo planes (hi at o, lo B*s*H*hd elements later:
+ * 4 bytes per element in total). `scratch` is a device buffer of at least
+ * rksc_test_attention_scratch_size() bytes. */
+size_t rksc_test_attention_scratch_size(int32_t dtype, int32_t B, int32_t n, int32_t s, int32_t H, int32_t Hkv,
+                                        int32_t hd);
 rksc_status rksc_test_attention(int32_t dtype, const void* q, const void* prefix_k, const void* prefix_v,
                                 const void* k_own, const void* v_own, void* o, int32_t B, int32_t n,
-                                int32_t s, int32_t H, int32_t Hkv, int32_t hd, void* scratch, void* stream);
+                                int32_t s, int32_t H, int32_t Hkv, int32_t hd, void* scratch,
+                                size_t scratch_bytes, void* stream);
 
 /* Measurement variant of rksc_verify_forward: the same validation, kernels and
  * launches, plus a HIP event recorded on `stream` right before and right after

@@ -94,7 +94,7 @@ def load_library():
     lib.rksc_abi_version.restype = i32
     lib.rksc_abi_version.argtypes = []
     lib.rksc_verify_workspace_size.restype = sz
-    lib.rksc_verify_workspace_size.argtypes = [ctypes.POINTER(ModelConfig), i32, i32]
+    lib.rksc_verify_workspace_size.argtypes = [ctypes.POINTER(ModelConfig), i32, i32, i32]
     lib.rksc_verify_forward.restype = i32
     lib.rksc_verify_forward.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32, i32,
                                         vp, vp, vp, vp, sz, vp]
@@ -105,9 +105,11 @@ def load_library():
     lib.rksc_last_error.restype = ctypes.c_char_p
     lib.rksc_last_error.argtypes = []
     lib.rksc_test_gemm.restype = i32
-    lib.rksc_test_gemm.argtypes = [i32, vp, vp, vp, i32, i32, i32, i32, ctypes.POINTER(i32), vp]
+    lib.rksc_test_gemm.argtypes = [i32, vp, vp, vp, vp, i32, i32, i32, i32, ctypes.POINTER(i32), vp]
     lib.rksc_test_attention.restype = i32
-    lib.rksc_test_attention.argtypes = [i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp]
+    lib.rksc_test_attention_scratch_size.restype = sz
+    lib.rksc_test_attention_scratch_size.argtypes = [i32, i32, i32, i32, i32, i32, i32]
+    lib.rksc_test_attention.argtypes = [i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, sz, vp]
     _lib = lib
     return lib
 
@@ -153,9 +155,9 @@ def rksc_last_error() -> str:
     return load_library().rksc_last_error().decode()
 
 
-def rksc_verify_workspace_size(shape, n_branches: int, branch_len: int) -> int:
+def rksc_verify_workspace_size(shape, n_branches: int, branch_len: int, n_prefix: int) -> int:
     cfg = model_config(shape)
-    n = int(load_library().rksc_verify_workspace_size(ctypes.byref(cfg), n_branches, branch_len))
+    n = int(load_library().rksc_verify_workspace_size(ctypes.byref(cfg), n_branches, branch_len, n_prefix))
     if n == 0:
         raise RkscError(RKSC_ERR_INVALID_ARGUMENT, rksc_last_error())
     return n
@@ -201,32 +203,43 @@ def rksc_asks_similarity(hidden: torch.Tensor, alpha: float, S: torch.Tensor, st
                                                _stream(stream)))
 
 
-def rksc_test_gemm(A: torch.Tensor, W: torch.Tensor, splits: int = 0, stream=None):
-    """Kernel-level GEMM: A [M, K] fp32, W [N, K] bf16 or fp32; returns the fp32 split partials."""
-    M, K = A.shape
+def rksc_test_gemm(A, W: torch.Tensor, splits: int = 0, stream=None):
+    """Kernel-level GEMM: returns the fp32 split partials [splits_used, M, N].
+
+    bf16 W: A is the pair (A_hi, A_lo) of bf16 [M, K] planes; fp32 W: A is an fp32 [M, K] tensor.
+    """
+    if W.dtype == torch.bfloat16:
+        a_hi, a_lo = A
+        dt = RKSC_BF16
+    else:
+        a_hi, a_lo = A, None
+        dt = RKSC_F32
+    M, K = a_hi.shape
     N = W.shape[0]
-    if A.dtype != torch.float32:
-        raise ValueError("A must be fp32")
-    dt = RKSC_BF16 if W.dtype == torch.bfloat16 else RKSC_F32
-    P = torch.empty((8, M, N), dtype=torch.float32, device=A.device)
+    P = torch.empty((8, M, N), dtype=torch.float32, device=a_hi.device)
     used = ctypes.c_int32(0)
-    _check(load_library().rksc_test_gemm(dt, _ptr(A), _ptr(W), _ptr(P), M, N, K, splits, ctypes.byref(used),
-                                         _stream(stream)))
+    _check(load_library().rksc_test_gemm(dt, _ptr(a_hi), _ptr(a_lo), _ptr(W), _ptr(P), M, N, K, splits,
+                                         ctypes.byref(used), _stream(stream)))
     return P[: used.value]
 
 
 def rksc_test_attention(q, prefix_k, prefix_v, k_own, v_own, dtype, stream=None):
     """Kernel-level shared-prefix attention: q [B*s, H, hd], own [B, Hkv, s, hd] fp32; prefix [Hkv, n, hd]
-    of `dtype` (torch.bfloat16 or torch.float32). Returns o [B*s, H*hd] fp32."""
+    of `dtype` (torch.bfloat16 or torch.float32). Returns o [B*s, H*hd] as fp32 (bf16 hi/lo planes are
+    recombined here for the bf16 path)."""
     Ms, H, hd = q.shape
     B, Hkv, s, _ = k_own.shape
     n = int(prefix_k.shape[1]) if prefix_k is not None else 0
     dt = RKSC_BF16 if dtype == torch.bfloat16 else RKSC_F32
     o = torch.empty((Ms, H * hd), dtype=torch.float32, device=q.device)
-    scratch = torch.empty(4096, dtype=torch.uint8, device=q.device)
-    _check(load_library().rksc_test_attention(dt, _ptr(q), _ptr(prefix_k), _ptr(prefix_v), _ptr(k_own),
-                                              _ptr(v_own), _ptr(o), B, n, s, H, Hkv, hd, _ptr(scratch),
-                                              _stream(stream)))
+    lib = load_library()
+    nbytes = int(lib.rksc_test_attention_scratch_size(dt, B, n, s, H, Hkv, hd))
+    scratch = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    _check(lib.rksc_test_attention(dt, _ptr(q), _ptr(prefix_k), _ptr(prefix_v), _ptr(k_own), _ptr(v_own), _ptr(o),
+                                   B, n, s, H, Hkv, hd, _ptr(scratch), nbytes, _stream(stream)))
+    if dt == RKSC_BF16:
+        planes = o.view(torch.bfloat16).view(2, Ms, H * hd)
+        return planes[0].float() + planes[1].float()
     return o
 
 
@@ -241,7 +254,8 @@ def verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, patie
     dev = branch_tokens.device
     L = len(weights.layers)
     if workspace is None:
-        workspace = torch.empty(rksc_verify_workspace_size(shape, B, s), dtype=torch.uint8, device=dev)
+        n_prefix = int(prefix_k.shape[2]) if prefix_k is not None else 0
+        workspace = torch.empty(rksc_verify_workspace_size(shape, B, s, n_prefix), dtype=torch.uint8, device=dev)
     entropy = torch.empty((L, B), dtype=torch.float32, device=dev)
     exit_layer = torch.empty((B,), dtype=torch.int32, device=dev)
     hidden = torch.empty((L, B, shape.d_model), dtype=torch.float32, device=dev) if return_hidden else None

@@ -15,6 +15,18 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int kWave = 64;
 
+// 16-byte load through a global-address-space pointer (keeps the compiler from
+// falling back to flat loads when it cannot infer the address space).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ldg16(const void* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const u32x4 v = *(const __attribute__((address_space(1))) u32x4*)p;
+#else
+  const u32x4 v = *static_cast<const u32x4*>(p);
+#endif
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t u) {
   return __uint_as_float(static_cast<uint32_t>(u) << 16);
 }

@@ -23,21 +23,33 @@ namespace rksc {
 
 namespace {
 
+// V^T tile layout: row = head dimension, column = key. The 4-key group of a
+// row is XOR-swizzled by the row's 8-dimension block so that the packed stores
+// (4 keys of one dimension) and the fragment reads are bank-conflict free.
+__device__ __forceinline__ int vt_col(int dim, int key) { return key ^ (((dim >> 3) & 15) << 2); }
+
+// Split-KV work unit: chunk `chunk` of `nchunks` covers prefix tiles
+// [t0, t1); with nchunks > 1 the last chunk covers the own-span tiles only.
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, const bf16* __restrict__ pk,
                                                    const bf16* __restrict__ pv, const float* __restrict__ ko,
-                                                   const float* __restrict__ vo, float* __restrict__ o,
-                                                   const Ctrl* c, int n, int s, int H, int Hkv, float sl2) {
+                                                   const float* __restrict__ vo, void* __restrict__ o,
+                                                   float* __restrict__ opart, float* __restrict__ mlpart,
+                                                   const Ctrl* c, int n, int s, int H, int Hkv, float sl2,
+                                                   int nchunks, int max_rows) {
   constexpr int KT = 64;          // keys per tile
   constexpr int LDK = HD + 8;     // K tile row stride (elements)
   constexpr int LDV = KT + 8;     // V^T row stride (elements)
   constexpr int NC = HD / 32;     // 32-dim chunks of the QK^T contraction
   constexpr int ND = HD / 16;     // 16-dim tiles of the output
+  static_assert(KT * HD / 8 % 256 == 0 && KT * HD / 4 % 256 == 0, "tile staging assumes 256 threads");
   // [0]: the prefix tile (exact bf16) or the hi part of an own-span tile; [1]: its lo part.
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * LDK];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[2][HD * LDV];
 
-  const int slot = blockIdx.z;
+  const int B_slots = gridDim.z / nchunks;
+  const int slot = blockIdx.z % B_slots;
+  const int chunk = blockIdx.z / B_slots;
   if (slot >= c->live_count) return;
   const int kvh = blockIdx.y;
   const int G = H / Hkv;
@@ -46,6 +58,21 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
   if (row0 >= rows) return;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
+
+  const int i_max = min(s - 1, (min(row0 + 63, rows - 1)) / G);
+  const int n_ptiles = (n + KT - 1) / KT;
+  const int n_otiles = i_max / KT + 1;
+  int t_begin, t_end;   // tile range, prefix tiles first, then own-span tiles
+  if (nchunks == 1) {
+    t_begin = 0;
+    t_end = n_ptiles + n_otiles;
+  } else if (chunk == nchunks - 1) {
+    t_begin = n_ptiles;
+    t_end = n_ptiles + n_otiles;
+  } else {
+    t_begin = chunk * n_ptiles / (nchunks - 1);
+    t_end = (chunk + 1) * n_ptiles / (nchunks - 1);
+  }
 
   // The query this lane owns as an MFMA column. Rows past the end compute a
   // duplicate of the last row and are not stored.
@@ -77,47 +104,76 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
   const bf16* Vp = pv + (size_t)kvh * n * HD;
   const float* Ko = ko + ((size_t)slot * Hkv + kvh) * s * HD;
   const float* Vo = vo + ((size_t)slot * Hkv + kvh) * s * HD;
-  const int i_max = min(s - 1, (min(row0 + 63, rows - 1)) / G);
-  const int n_ptiles = (n + KT - 1) / KT;
-  const int n_tiles = n_ptiles + i_max / KT + 1;
 
-  for (int t = 0; t < n_tiles; ++t) {
+  for (int t = t_begin; t < t_end; ++t) {
     const bool own = t >= n_ptiles;
     const int kbase = own ? (t - n_ptiles) * KT : t * KT;
     if (!own) {
-      // Prefix tile: K rows as stored, V transposed (exact bf16, no split needed).
+      // Prefix tile (exact bf16). K: 16-byte row chunks. V: each thread takes 4
+      // consecutive keys of 8 dimensions and stores 4-key words per dimension.
 #pragma unroll
       for (int j = 0; j < KT * HD / 8 / 256; ++j) {
         const int idx = tid + 256 * j, key = idx / (HD / 8), dc = idx % (HD / 8);
-        uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-        if (kbase + key < n) {
-          kv = *reinterpret_cast<const uint4*>(Kp + (size_t)(kbase + key) * HD + dc * 8);
-          vv = *reinterpret_cast<const uint4*>(Vp + (size_t)(kbase + key) * HD + dc * 8);
-        }
+        const int kk = kbase + key < n ? kbase + key : 0;
+        uint4 kv = ldg16(Kp + (size_t)kk * HD + dc * 8);
+        if (kbase + key >= n) kv = make_uint4(0, 0, 0, 0);
         *reinterpret_cast<uint4*>(&Ks[0][key * LDK + dc * 8]) = kv;
-        const uint16_t* ve = reinterpret_cast<const uint16_t*>(&vv);
+      }
+      // KT * HD / 32 units of 4 keys x 8 dimensions (128 for HD = 64: half the threads idle).
+      for (int idx = tid; idx < KT * HD / 32; idx += 256) {
+        const int dc = idx % (HD / 8), kg = idx / (HD / 8);
+        uint4 v4[4];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) Vt[0][(dc * 8 + e) * LDV + key] = ve[e];
+        for (int e = 0; e < 4; ++e) {
+          const int key = kbase + 4 * kg + e;
+          v4[e] = ldg16(Vp + (size_t)(key < n ? key : 0) * HD + dc * 8);
+          if (key >= n) v4[e] = make_uint4(0, 0, 0, 0);
+        }
+        const uint16_t* ve0 = reinterpret_cast<const uint16_t*>(&v4[0]);
+        const uint16_t* ve1 = reinterpret_cast<const uint16_t*>(&v4[1]);
+        const uint16_t* ve2 = reinterpret_cast<const uint16_t*>(&v4[2]);
+        const uint16_t* ve3 = reinterpret_cast<const uint16_t*>(&v4[3]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int dim = dc * 8 + e;
+          *reinterpret_cast<uint2*>(&Vt[0][dim * LDV + vt_col(dim, 4 * kg)]) =
+              make_uint2(pack2(ve0[e], ve1[e]), pack2(ve2[e], ve3[e]));
+        }
       }
     } else {
       // Own-span tile: fp32 keys/values of the branch, split into hi/lo.
 #pragma unroll
       for (int j = 0; j < KT * HD / 4 / 256; ++j) {
         const int idx = tid + 256 * j, key = idx / (HD / 4), dq = idx % (HD / 4);
-        float4 kf = make_float4(0.f, 0.f, 0.f, 0.f), vf = kf;
-        if (kbase + key < s) {
-          kf = *reinterpret_cast<const float4*>(Ko + (size_t)(kbase + key) * HD + dq * 4);
-          vf = *reinterpret_cast<const float4*>(Vo + (size_t)(kbase + key) * HD + dq * 4);
-        }
-        uint16_t kh[4], kl[4], vh[4], vl[4];
+        const int kk = kbase + key < s ? kbase + key : 0;
+        float4 kf = __builtin_bit_cast(float4, ldg16(Ko + (size_t)kk * HD + dq * 4));
+        if (kbase + key >= s) kf = make_float4(0.f, 0.f, 0.f, 0.f);
+        uint16_t kh[4], kl[4];
         split2(kf.x, kh[0], kl[0]); split2(kf.y, kh[1], kl[1]); split2(kf.z, kh[2], kl[2]); split2(kf.w, kh[3], kl[3]);
-        split2(vf.x, vh[0], vl[0]); split2(vf.y, vh[1], vl[1]); split2(vf.z, vh[2], vl[2]); split2(vf.w, vh[3], vl[3]);
         *reinterpret_cast<uint2*>(&Ks[0][key * LDK + dq * 4]) = make_uint2(pack2(kh[0], kh[1]), pack2(kh[2], kh[3]));
         *reinterpret_cast<uint2*>(&Ks[1][key * LDK + dq * 4]) = make_uint2(pack2(kl[0], kl[1]), pack2(kl[2], kl[3]));
+      }
+      for (int idx = tid; idx < KT * HD / 16; idx += 256) {
+        const int dq = idx % (HD / 4), kg = idx / (HD / 4);
+        float4 v4[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          Vt[0][(dq * 4 + e) * LDV + key] = vh[e];
-          Vt[1][(dq * 4 + e) * LDV + key] = vl[e];
+          const int key = kbase + 4 * kg + e;
+          v4[e] = __builtin_bit_cast(float4, ldg16(Vo + (size_t)(key < s ? key : 0) * HD + dq * 4));
+          if (key >= s) v4[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int dim = dq * 4 + e;
+          uint16_t hh[4], lw[4];
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const float x = e == 0 ? v4[q4].x : (e == 1 ? v4[q4].y : (e == 2 ? v4[q4].z : v4[q4].w));
+            split2(x, hh[q4], lw[q4]);
+          }
+          const int col = vt_col(dim, 4 * kg);
+          *reinterpret_cast<uint2*>(&Vt[0][dim * LDV + col]) = make_uint2(pack2(hh[0], hh[1]), pack2(hh[2], hh[3]));
+          *reinterpret_cast<uint2*>(&Vt[1][dim * LDV + col]) = make_uint2(pack2(lw[0], lw[1]), pack2(lw[2], lw[3]));
         }
       }
     }
@@ -152,7 +208,9 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
       }
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    // Every query sees key 0 of its first tile, so mn is finite from the first tile on.
+    // A tile can be fully masked for a query only after an earlier tile of the same
+    // chunk gave it a finite maximum (prefix tiles are never fully masked; own tile
+    // 0 always holds key 0), so mn is finite whenever scores are used.
     const float mn = fmaxf(m, mt);
     const float alpha = exp2f((m - mn) * sl2);
     m = mn;
@@ -183,15 +241,17 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
                                                                pack2(pl[4], pl[5]), pack2(pl[6], pl[7])));
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt) {
-        const int off = (16 * dt + r16) * LDV + 32 * kb + 4 * g;
-        const uint2 a0 = *reinterpret_cast<const uint2*>(&Vt[0][off]);
-        const uint2 a1 = *reinterpret_cast<const uint2*>(&Vt[0][off + 16]);
+        const int dim = 16 * dt + r16;
+        const int off0 = dim * LDV + vt_col(dim, 32 * kb + 4 * g);
+        const int off1 = dim * LDV + vt_col(dim, 32 * kb + 16 + 4 * g);
+        const uint2 a0 = *reinterpret_cast<const uint2*>(&Vt[0][off0]);
+        const uint2 a1 = *reinterpret_cast<const uint2*>(&Vt[0][off1]);
         const bf16x8 v0 = __builtin_bit_cast(bf16x8, make_uint4(a0.x, a0.y, a1.x, a1.y));
         oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, pbh, oacc[dt], 0, 0, 0);
         oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, pbl, oacc[dt], 0, 0, 0);
         if (own) {
-          const uint2 b0 = *reinterpret_cast<const uint2*>(&Vt[1][off]);
-          const uint2 b1 = *reinterpret_cast<const uint2*>(&Vt[1][off + 16]);
+          const uint2 b0 = *reinterpret_cast<const uint2*>(&Vt[1][off0]);
+          const uint2 b1 = *reinterpret_cast<const uint2*>(&Vt[1][off1]);
           const bf16x8 v1 = __builtin_bit_cast(bf16x8, make_uint4(b0.x, b0.y, b1.x, b1.y));
           oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, pbh, oacc[dt], 0, 0, 0);
         }
@@ -202,13 +262,68 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
 
   l += __shfl_xor(l, 16, 64);
   l += __shfl_xor(l, 32, 64);
-  if (qvalid) {
+  if (!qvalid) return;
+  if (nchunks == 1) {
+    // The output feeds the O projection: bf16 hi/lo planes [max_rows, H*hd] each.
     const float inv = 1.f / l;
-    float* orow = o + (qrow * H + h) * HD;
+    const size_t plane = (size_t)max_rows * H * HD;
+    bf16* ob = reinterpret_cast<bf16*>(o);
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) {
+      uint16_t h4[4], l4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) split2(oacc[dt][i] * inv, h4[i], l4[i]);
+      const size_t idx = (qrow * H + h) * HD + 16 * dt + 4 * g;
+      *reinterpret_cast<uint2*>(ob + idx) = make_uint2(pack2(h4[0], h4[1]), pack2(h4[2], h4[3]));
+      *reinterpret_cast<uint2*>(ob + plane + idx) = make_uint2(pack2(l4[0], l4[1]), pack2(l4[2], l4[3]));
+    }
+  } else {
+    // Unnormalised partial output and its (max, sum) for the combine kernel.
+    const size_t prow = ((size_t)chunk * max_rows + qrow) * H + h;
+    float* orow = opart + prow * HD;
 #pragma unroll
     for (int dt = 0; dt < ND; ++dt)
       *reinterpret_cast<float4*>(orow + 16 * dt + 4 * g) =
-          make_float4(oacc[dt][0] * inv, oacc[dt][1] * inv, oacc[dt][2] * inv, oacc[dt][3] * inv);
+          make_float4(oacc[dt][0], oacc[dt][1], oacc[dt][2], oacc[dt][3]);
+    if (g == 0) *reinterpret_cast<float2*>(mlpart + prow * 2) = make_float2(m, l);
+  }
+}
+
+// Merges the split-KV partials of each (row, head):
+// o = sum_c e^{(m_c - M) sl} o_c / sum_c e^{(m_c - M) sl} l_c, M = max_c m_c.
+// A chunk that saw no key for a query (m = -inf) contributes nothing.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_combine(const float* __restrict__ opart, const float* __restrict__ mlpart,
+                                                      void* __restrict__ o, const Ctrl* c, int s, int H, float sl2,
+                                                      int nchunks, int max_rows) {
+  const int rows = c->live_count * s * H;
+  const int wid = (blockIdx.x * blockDim.x + threadIdx.x) >> 6, lane = threadIdx.x & 63;
+  if (wid >= rows) return;    // one wave per (row, head)
+  float M = -INFINITY;
+  for (int ch = 0; ch < nchunks; ++ch) M = fmaxf(M, mlpart[((size_t)ch * max_rows * H + wid) * 2]);
+  float den = 0.f;
+  float acc[HD / 64];
+#pragma unroll
+  for (int j = 0; j < HD / 64; ++j) acc[j] = 0.f;
+  for (int ch = 0; ch < nchunks; ++ch) {
+    const float2 ml = *reinterpret_cast<const float2*>(mlpart + ((size_t)ch * max_rows * H + wid) * 2);
+    if (ml.x == -INFINITY) continue;
+    const float w = exp2f((ml.x - M) * sl2);
+    den += w * ml.y;
+    const float* op = opart + ((size_t)ch * max_rows * H + wid) * HD;
+#pragma unroll
+    for (int j = 0; j < HD / 64; ++j) acc[j] += w * op[lane + 64 * j];
+  }
+  // bf16 hi/lo planes of the output, as in the single-chunk path.
+  const float inv = 1.f / den;
+  const size_t plane = (size_t)max_rows * H * HD;
+  uint16_t* ob = reinterpret_cast<uint16_t*>(o);
+#pragma unroll
+  for (int j = 0; j < HD / 64; ++j) {
+    uint16_t hb, lb;
+    split2(acc[j] * inv, hb, lb);
+    ob[(size_t)wid * HD + lane + 64 * j] = hb;
+    ob[plane + (size_t)wid * HD + lane + 64 * j] = lb;
   }
 }
 
@@ -249,21 +364,44 @@ __global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ q, c
 
 }  // namespace
 
+int attention_chunks(DType dt, int B, int n, int s, int H, int Hkv) {
+  if (dt != DType::BF16 || n == 0) return 1;
+  const int base = ((H / Hkv) * s + 63) / 64 * Hkv * B;
+  const int n_ptiles = (n + 63) / 64;
+  int chunks = 1;
+  // Split the prefix until the launch has about two workgroups per CU.
+  while (base * chunks < 512 && chunks - 1 < n_ptiles) chunks = chunks == 1 ? 3 : chunks + 1;
+  if (chunks > 1 && chunks - 1 > n_ptiles) chunks = n_ptiles + 1;
+  return chunks;
+}
+
 hipError_t launch_attention(DType dt, const void* q, const void* pk, const void* pv, const void* k_own,
-                            const void* v_own, void* o, const Ctrl* c, int n, int s, int H, int Hkv, int hd,
-                            int max_branches, hipStream_t st) {
+                            const void* v_own, void* o, float* opart, float* mlpart, int nchunks, const Ctrl* c,
+                            int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st) {
   if (dt == DType::BF16) {
     const float sl2 = 1.4426950408889634f / sqrtf((float)hd);
-    const dim3 grid(((H / Hkv) * s + 63) / 64, Hkv, max_branches);
+    const dim3 grid(((H / Hkv) * s + 63) / 64, Hkv, max_branches * nchunks);
+    const int max_rows = max_branches * s;
     const float* qq = static_cast<const float*>(q);
     const bf16 *kk = static_cast<const bf16*>(pk), *vv = static_cast<const bf16*>(pv);
     const float *ko = static_cast<const float*>(k_own), *vo = static_cast<const float*>(v_own);
+    void* oo = o;
     if (hd == 128)
-      hipLaunchKernelGGL(k_attn_bf16<128>, grid, dim3(256), 0, st, qq, kk, vv, ko, vo, static_cast<float*>(o), c,
-                         n, s, H, Hkv, sl2);
+      hipLaunchKernelGGL(k_attn_bf16<128>, grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c, n, s, H,
+                         Hkv, sl2, nchunks, max_rows);
     else
-      hipLaunchKernelGGL(k_attn_bf16<64>, grid, dim3(256), 0, st, qq, kk, vv, ko, vo, static_cast<float*>(o), c, n,
-                         s, H, Hkv, sl2);
+      hipLaunchKernelGGL(k_attn_bf16<64>, grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c, n, s, H,
+                         Hkv, sl2, nchunks, max_rows);
+    if (nchunks > 1) {
+      const int waves = max_rows * H;
+      const dim3 cgrid((waves * 64 + 255) / 256);
+      if (hd == 128)
+        hipLaunchKernelGGL(k_attn_combine<128>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, sl2, nchunks,
+                           max_rows);
+      else
+        hipLaunchKernelGGL(k_attn_combine<64>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, sl2, nchunks,
+                           max_rows);
+    }
   } else {
     const float scale = 1.f / sqrtf((float)hd);
     const int total = max_branches * s * H;

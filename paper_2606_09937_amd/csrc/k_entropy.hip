@@ -73,6 +73,12 @@ __device__ __forceinline__ void write_block_stats(EntStats (&st)[NCB], int Bl, f
   }
 }
 
+// W fragments of one 64-wide K step: NT row tiles, two 16-byte halves each.
+template <int NT>
+struct WStep {
+  uint4 w[NT][2];
+};
+
 template <int NCB, int NT>
 __global__ __launch_bounds__(256) void k_entropy_bf16(const bf16* __restrict__ W, const bf16* __restrict__ hi,
                                                       const bf16* __restrict__ lo, const Ctrl* c, int V, int d,
@@ -86,62 +92,107 @@ __global__ __launch_bounds__(256) void k_entropy_bf16(const bf16* __restrict__ W
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) st[cb] = ent_empty();
   const uint4 zero = make_uint4(0, 0, 0, 0);
+  bool cv[NCB];
+  size_t hoff[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    const int col = 16 * cb + r16;
+    cv[cb] = col < Bl;
+    hoff[cb] = (size_t)(cv[cb] ? col : 0) * d + 16 * g;
+  }
 
   for (int pass = blockIdx.x * kEntWaves + wid; pass * ROWS < V; pass += gridDim.x * kEntWaves) {
     const int v0 = pass * ROWS;
+    const bf16* wrow[NT];
+    bool rv[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int row = v0 + 16 * t + r16;
+      rv[t] = row < V;
+      wrow[t] = W + (size_t)(rv[t] ? row : 0) * d + 16 * g;
+    }
+    // Lane group g supplies k = k0 + 16g + 8ks + e in substep ks: each row's four
+    // lane groups read 128 contiguous bytes per step.
+    // Loads always hit valid memory (row clamped to 0, k clamped to the row start)
+    // and are never masked, so no predicate forces an early wait on them:
+    // weights past d meet zero hidden values, rows past V are left out of the
+    // statistics.
+    auto load = [&](WStep<NT>& f, int k0) {
+      const int ka = k0 + 16 * g < d ? k0 : -16 * g, kb = k0 + 16 * g + 8 < d ? k0 + 8 : -16 * g;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        f.w[t][0] = ldg16(wrow[t] + ka);
+        f.w[t][1] = ldg16(wrow[t] + kb);
+      }
+    };
     floatx4 acc[NT][NCB];
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
       for (int cb = 0; cb < NCB; ++cb) acc[t][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < d; k0 += 64) {
-      // Lane group g supplies k = k0 + 16g + 8ks + e in substep ks.
-      const int k = k0 + 16 * g;
-      const bool k_in0 = k < d, k_in1 = k + 8 < d;
-      uint4 w0[NT], w1[NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        const int row = v0 + 16 * t + r16;
-        const bf16* p = W + (size_t)row * d + k;
-        w0[t] = (row < V && k_in0) ? *reinterpret_cast<const uint4*>(p) : zero;
-        w1[t] = (row < V && k_in1) ? *reinterpret_cast<const uint4*>(p + 8) : zero;
-      }
+    auto mma = [&](const WStep<NT>& f, int k0) {
+      const bool in0 = k0 + 16 * g < d, in1 = k0 + 16 * g + 8 < d;
+      const int ka = in0 ? k0 : -16 * g, kb = in1 ? k0 + 8 : -16 * g;
 #pragma unroll
       for (int cb = 0; cb < NCB; ++cb) {
-        const int col = 16 * cb + r16;
-        const bool cv = col < Bl;
-        const size_t off = (size_t)col * d + k;
-        const uint4 h0 = (cv && k_in0) ? *reinterpret_cast<const uint4*>(hi + off) : zero;
-        const uint4 h1 = (cv && k_in1) ? *reinterpret_cast<const uint4*>(hi + off + 8) : zero;
-        const uint4 l0 = (cv && k_in0) ? *reinterpret_cast<const uint4*>(lo + off) : zero;
-        const uint4 l1 = (cv && k_in1) ? *reinterpret_cast<const uint4*>(lo + off + 8) : zero;
+        // Hidden fragments (hi/lo): a few KB shared by every wave, served by the caches.
+        const bool ok0 = cv[cb] && in0, ok1 = cv[cb] && in1;
+        const uint4 xh0 = ldg16(hi + hoff[cb] + ka);
+        const uint4 xh1 = ldg16(hi + hoff[cb] + kb);
+        const uint4 xl0 = ldg16(lo + hoff[cb] + ka);
+        const uint4 xl1 = ldg16(lo + hoff[cb] + kb);
+        const bf16x8 h0 = __builtin_bit_cast(bf16x8, ok0 ? xh0 : zero);
+        const bf16x8 h1 = __builtin_bit_cast(bf16x8, ok1 ? xh1 : zero);
+        const bf16x8 l0 = __builtin_bit_cast(bf16x8, ok0 ? xl0 : zero);
+        const bf16x8 l1 = __builtin_bit_cast(bf16x8, ok1 ? xl1 : zero);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-          const bf16x8 a0 = __builtin_bit_cast(bf16x8, w0[t]), a1 = __builtin_bit_cast(bf16x8, w1[t]);
-          acc[t][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8, h0), acc[t][cb], 0, 0, 0);
-          acc[t][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, __builtin_bit_cast(bf16x8, l0), acc[t][cb], 0, 0, 0);
-          acc[t][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8, h1), acc[t][cb], 0, 0, 0);
-          acc[t][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, __builtin_bit_cast(bf16x8, l1), acc[t][cb], 0, 0, 0);
+          const bf16x8 a0 = __builtin_bit_cast(bf16x8, f.w[t][0]), a1 = __builtin_bit_cast(bf16x8, f.w[t][1]);
+          acc[t][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, h0, acc[t][cb], 0, 0, 0);
+          acc[t][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, l0, acc[t][cb], 0, 0, 0);
+          acc[t][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, h1, acc[t][cb], 0, 0, 0);
+          acc[t][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, l1, acc[t][cb], 0, 0, 0);
         }
       }
+    };
+    // Two K steps of W in flight: while one step feeds the MFMAs, the next
+    // step's loads are outstanding.
+    WStep<NT> fa, fb;
+    load(fa, 0);
+    for (int k0 = 0; k0 < d; k0 += 128) {
+      const bool has_b = k0 + 64 < d;
+      if (has_b) load(fb, k0 + 64);
+      mma(fa, k0);
+      if (k0 + 128 < d) load(fa, k0 + 128);
+      if (has_b) mma(fb, k0 + 64);
     }
     // Lane (r16, g) holds z[v0 + 16t + 4g + i] for branch column 16cb + r16.
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
-      float z[4 * NT];
-      int cnt = 0;
       float mx = -INFINITY;
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = v0 + 16 * t + 4 * g + i;
-          if (row < V) {
-            z[cnt++] = acc[t][cb][i];
-            mx = fmaxf(mx, acc[t][cb][i]);
+        for (int i = 0; i < 4; ++i)
+          if (v0 + 16 * t + 4 * g + i < V) mx = fmaxf(mx, acc[t][cb][i]);
+      if (mx == -INFINITY) continue;
+      const float mn = fmaxf(st[cb].m, mx);
+      float s_new = 0.f, t_new = 0.f;
+      if (st[cb].m != -INFINITY) {
+        const float dm = st[cb].m - mn, sc = __expf(dm);
+        s_new = st[cb].s * sc;
+        t_new = (st[cb].t + st[cb].s * dm) * sc;
+      }
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (v0 + 16 * t + 4 * g + i < V) {
+            const float dz = acc[t][cb][i] - mn, e = __expf(dz);
+            s_new += e;
+            t_new = fmaf(e, dz, t_new);
           }
-        }
-      if (cnt > 0) stats_fold(st[cb], mx, z, cnt);
+      st[cb] = EntStats{mn, s_new, t_new};
     }
   }
   write_block_stats<NCB>(st, Bl, parts);
@@ -182,17 +233,18 @@ __global__ __launch_bounds__(256) void k_entropy_f32(const float* __restrict__ W
   }
 }
 
-constexpr int kNT = 4;   // 64 vocabulary rows per wave pass
+// Vocabulary rows per wave pass: 64 for up to 16 branches, 32 beyond (register budget).
+constexpr int kNT = 4;
+constexpr int kNTWide = 2;
 
 }  // namespace
 
 int entropy_parts(DType dt, int V, int max_branches) {
-  (void)max_branches;
   if (dt == DType::F32) {
     const int b = (V + kEntWaves - 1) / kEntWaves;
     return b < 256 ? b : 256;
   }
-  const int rows_per_block = 16 * kNT * kEntWaves;
+  const int rows_per_block = 16 * (max_branches <= 16 ? kNT : kNTWide) * kEntWaves;
   return (V + rows_per_block - 1) / rows_per_block;
 }
 
@@ -210,9 +262,9 @@ hipError_t launch_entropy(DType dt, const void* W, const void* hn_a, const void*
   if (max_branches <= 16)
     hipLaunchKernelGGL((k_entropy_bf16<1, kNT>), dim3(blocks), dim3(256), 0, st, w, a, b, c, V, d, parts);
   else if (max_branches <= 32)
-    hipLaunchKernelGGL((k_entropy_bf16<2, kNT>), dim3(blocks), dim3(256), 0, st, w, a, b, c, V, d, parts);
+    hipLaunchKernelGGL((k_entropy_bf16<2, kNTWide>), dim3(blocks), dim3(256), 0, st, w, a, b, c, V, d, parts);
   else
-    hipLaunchKernelGGL((k_entropy_bf16<4, kNT>), dim3(blocks), dim3(256), 0, st, w, a, b, c, V, d, parts);
+    hipLaunchKernelGGL((k_entropy_bf16<4, kNTWide>), dim3(blocks), dim3(256), 0, st, w, a, b, c, V, d, parts);
   return hipGetLastError();
 }
 

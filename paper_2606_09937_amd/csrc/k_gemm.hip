@@ -3,10 +3,11 @@
 // weight (torch Linear layout) in the model's storage type, P fp32. Split
 // partials are summed by the consumer.
 //
-// bf16 weights: CDNA4 MFMA (v_mfma_f32_16x16x32_bf16, fp32 accumulate), LDS
-// double buffered; both operands are K-contiguous, so every lane reads its
-// fragment as one 16-byte LDS load.
-// fp32 weights: a plain LDS-tiled FMA kernel.
+// bf16 weights: the activation arrives as two bf16 planes (hi + lo of the fp32
+// value), and both meet every weight fragment in v_mfma_f32_16x16x32_bf16 with
+// fp32 accumulation, so the product keeps fp32-level accuracy at twice the
+// bf16 MFMA work. Operands stream through an LDS ring by direct DMA.
+// fp32 weights: a plain LDS-tiled FMA kernel on fp32 activations.
 #include "common.h"
 #include "kernels.h"
 
@@ -14,22 +15,49 @@ namespace rksc {
 
 namespace {
 
-// bf16 weights W [N, K] times fp32 activations A [rows, K]. A is split into
-// bf16 hi/lo tiles when it is staged into LDS, and every W fragment meets both
-// (two v_mfma_f32_16x16x32_bf16 into one fp32 accumulator), so the product
-// keeps fp32-level accuracy at twice the bf16 MFMA work.
-template <int BM, int BN>
-__global__ __launch_bounds__(256) void k_gemm_bf16(const float* __restrict__ A, const bf16* __restrict__ W,
-                                                   float* __restrict__ P, size_t split_stride, const Ctrl* c,
-                                                   int s, int max_rows, int N, int K, int kps) {
-  constexpr int BK = 32, LDK = BK + 8;   // 80-byte LDS rows: conflict-free 16-byte fragment reads
+// ---------------------------------------------------------------------------
+// Multi-stage LDS pipeline fed by direct global->LDS DMA (global_load_lds_dwordx4).
+//
+// The activation arrives pre-split as two bf16 planes (A = Ahi + Alo, both
+// [rows, K]), the weight as bf16 [N, K]. Each K step of 32 moves three
+// sub-tiles (Ahi, Alo: BM x 64 B; W: BN x 64 B) straight from memory into one
+// slot of an R-deep LDS ring without touching registers, so R-1 steps of loads
+// are in flight while the MFMAs consume the current slot. Within a 64-byte row
+// the four 16-byte chunks are stored at position chunk ^ ((row >> 2) & 3): the
+// DMA writes stay contiguous per wave and the 16-row fragment reads are
+// bank-conflict free. Every wave issues the same number of DMA instructions
+// per step, so "slot ready" is an explicit vmcnt wait followed by a barrier.
+// K needs only to be a multiple of 8: a chunk that would start at or past the
+// end of the split reads the split's first chunk instead (valid memory), and
+// activation chunks past the end are zeroed before the last step is consumed.
+
+__device__ __forceinline__ void dma16(const void* gsrc, void* lds_base) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)gsrc,
+                                   (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
+
+template <int BM, int BN, int R>
+__global__ __launch_bounds__(256) void k_gemm_dma(const bf16* __restrict__ Ahi, const bf16* __restrict__ Alo,
+                                                  const bf16* __restrict__ W, float* __restrict__ P,
+                                                  size_t split_stride, const Ctrl* c, int s, int max_rows, int N,
+                                                  int K, int kps) {
+  constexpr int BK = 32;
+  constexpr int AI = BM / 16, WI = BN / 16;           // wave DMA instructions per sub-tile
+  constexpr int NDMA = (2 * AI + WI) / 4;             // per wave per step
+  static_assert((2 * AI + WI) % 4 == 0, "DMA instructions must split evenly over 4 waves");
+  constexpr int A_BYTES = BM * 64, W_BYTES = BN * 64;
+  constexpr int SLOT = 2 * A_BYTES + W_BYTES;
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
-  constexpr int AC = BM * 8 / 256;   // float4 chunks of A per thread per stage
-  constexpr int WC = BN * 4 / 256;   // 16-byte chunks of W per thread per stage
-  static_assert(AC >= 1 && WC >= 1, "tile too small for 256 threads");
-  __shared__ __attribute__((aligned(16))) uint16_t Ah[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Al[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Ws[2][BN * LDK];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[R * SLOT];
 
   const int Ml = c ? min(c->live_count * s, max_rows) : max_rows;
   const int m0 = blockIdx.y * BM;
@@ -37,45 +65,41 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const float* __restrict__ A, 
   const int n0 = blockIdx.x * BN;
   const int kb = blockIdx.z * kps;
   const int ke = min(K, kb + kps);
+  const int nsteps = (ke - kb + BK - 1) / BK;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wm0 = (wid >> 1) * WM, wn0 = (wid & 1) * WN;
   const int r16 = lane & 15, g = lane >> 4;
 
-  float4 ra[AC];
-  uint4 rw[WC];
-  auto gload = [&](int k0) {
+  // Per-wave DMA sources: instruction j (global index wid + 4j) covers 16 rows of
+  // one sub-tile; lane L fills chunk position L % 4 of row 16*i + L / 4, i.e.
+  // the 8-element chunk swz(row, L % 4) of that row.
+  const bf16* src[NDMA];
+  int dst[NDMA];
+  const int chunk_off = 8 * swz(lane >> 2, lane & 3);   // 16-row groups keep (row >> 2) & 3
 #pragma unroll
-    for (int j = 0; j < AC; ++j) {
-      const int idx = tid + 256 * j, row = idx >> 3, gk = k0 + (idx & 7) * 4, gr = m0 + row;
-      ra[j] = (gr < Ml && gk < ke) ? *reinterpret_cast<const float4*>(A + (size_t)gr * K + gk)
-                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int j = 0; j < NDMA; ++j) {
+    const int ins = wid + 4 * j;
+    const int row_in = lane >> 2;
+    if (ins < 2 * AI) {
+      const int plane = ins / AI, i = ins % AI;
+      const int gr = min(m0 + 16 * i + row_in, max_rows - 1);
+      src[j] = (plane ? Alo : Ahi) + (size_t)gr * K;
+      dst[j] = plane * A_BYTES + i * 1024;
+    } else {
+      const int i = ins - 2 * AI;
+      const int gn = min(n0 + 16 * i + row_in, N - 1);
+      src[j] = W + (size_t)gn * K;
+      dst[j] = 2 * A_BYTES + i * 1024;
     }
+  }
+  auto issue = [&](int step) {
+    // Steps past the end re-read the split's first step (valid memory, never used);
+    // a chunk starting at or past ke reads the split's first chunk instead.
+    const int k = (step < nsteps ? kb + step * BK : kb) + chunk_off;
+    const int col = k < ke ? k : kb;
+    uint8_t* slot = smem + (step % R) * SLOT;
 #pragma unroll
-    for (int j = 0; j < WC; ++j) {
-      const int idx = tid + 256 * j, row = idx >> 2, gk = k0 + (idx & 3) * 8, gr = n0 + row;
-      rw[j] = (gr < N && gk < ke) ? *reinterpret_cast<const uint4*>(W + (size_t)gr * K + gk)
-                                  : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int j = 0; j < AC; ++j) {
-      const int idx = tid + 256 * j, off = (idx >> 3) * LDK + (idx & 7) * 4;
-      uint16_t h0, l0, h1, l1, h2, l2, h3, l3;
-      split2(ra[j].x, h0, l0);
-      split2(ra[j].y, h1, l1);
-      split2(ra[j].z, h2, l2);
-      split2(ra[j].w, h3, l3);
-      *reinterpret_cast<uint2*>(&Ah[buf][off]) =
-          make_uint2((uint32_t)h0 | ((uint32_t)h1 << 16), (uint32_t)h2 | ((uint32_t)h3 << 16));
-      *reinterpret_cast<uint2*>(&Al[buf][off]) =
-          make_uint2((uint32_t)l0 | ((uint32_t)l1 << 16), (uint32_t)l2 | ((uint32_t)l3 << 16));
-    }
-#pragma unroll
-    for (int j = 0; j < WC; ++j) {
-      const int idx = tid + 256 * j;
-      *reinterpret_cast<uint4*>(&Ws[buf][(idx >> 2) * LDK + (idx & 3) * 8]) = rw[j];
-    }
+    for (int j = 0; j < NDMA; ++j) dma16(src[j] + col, slot + dst[j]);
   };
 
   floatx4 acc[TM][TN];
@@ -84,23 +108,41 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const float* __restrict__ A, 
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  gload(kb);
-  sstore(0);
-  __syncthreads();
-  int buf = 0;
-  for (int k0 = kb; k0 < ke; k0 += BK) {
-    const bool more = k0 + BK < ke;
-    if (more) gload(k0 + BK);
+#pragma unroll
+  for (int st = 0; st < R - 1; ++st) issue(st);
+
+  for (int st = 0; st < nsteps; ++st) {
+    wait_vmcnt<NDMA * (R - 2)>();   // this thread's DMAs for step st have landed
+    uint8_t* slot = smem + (st % R) * SLOT;
+    const int kst = kb + st * BK;
+    if (kst + BK > ke) {
+      // Partial last step: zero activation chunks at k >= ke (both planes).
+      for (int ci = tid; ci < 2 * BM * 4; ci += 256) {
+        const int plane = ci / (BM * 4), row = (ci / 4) % BM, pos = ci & 3;
+        const int chunk = swz(row, pos);
+        if (kst + 8 * chunk >= ke)
+          *reinterpret_cast<uint4*>(slot + plane * A_BYTES + row * 64 + pos * 16) = make_uint4(0, 0, 0, 0);
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the zeros are in LDS before the barrier
+    }
+    __builtin_amdgcn_s_barrier();        // every wave's DMAs for st landed; step st-1 fully consumed
+    issue(st + R - 1);                   // refills the slot step st-1 used
+    const uint8_t* ah_t = slot;
+    const uint8_t* al_t = slot + A_BYTES;
+    const uint8_t* w_t = slot + 2 * A_BYTES;
     bf16x8 ah[TM], al[TM], bw[TN];
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
-      const int off = (wm0 + 16 * tm + r16) * LDK + 8 * g;
-      ah[tm] = *reinterpret_cast<const bf16x8*>(&Ah[buf][off]);
-      al[tm] = *reinterpret_cast<const bf16x8*>(&Al[buf][off]);
+      const int row = wm0 + 16 * tm + r16;
+      const int off = row * 64 + swz(row, g) * 16;
+      ah[tm] = *reinterpret_cast<const bf16x8*>(ah_t + off);
+      al[tm] = *reinterpret_cast<const bf16x8*>(al_t + off);
     }
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn)
-      bw[tn] = *reinterpret_cast<const bf16x8*>(&Ws[buf][(wn0 + 16 * tn + r16) * LDK + 8 * g]);
+    for (int tn = 0; tn < TN; ++tn) {
+      const int row = wn0 + 16 * tn + r16;
+      bw[tn] = *reinterpret_cast<const bf16x8*>(w_t + row * 64 + swz(row, g) * 16);
+    }
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
@@ -108,12 +150,9 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const float* __restrict__ A, 
         acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[tm], bw[tn], acc[tm][tn], 0, 0, 0);
         acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[tm], bw[tn], acc[tm][tn], 0, 0, 0);
       }
-    if (more) sstore(buf ^ 1);
-    __syncthreads();
-    buf ^= 1;
   }
+  wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
 
-  // Lane (r16, g) holds C[4g + i][r16] of each 16x16 tile.
   float* out = P + blockIdx.z * split_stride;
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
@@ -175,35 +214,35 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
   GemmPlan p;
-  if (dt == DType::F32) {
-    p.bm = 64; p.bn = 64;
-  } else if (max_rows > 64) {
-    p.bm = 128; p.bn = 128;
-  } else {
-    p.bm = 64; p.bn = 128;
-  }
+  p.bm = 64;
+  p.bn = dt == DType::F32 ? 64 : 128;
+  if (dt == DType::BF16 && max_rows > 64) p.bm = 128;
   const int kstep = dt == DType::BF16 ? 32 : 16;
   const int tiles = cdiv(N, p.bn) * cdiv(max_rows, p.bm);
+  // Split K until the launch has ~1.5 workgroups per CU (split partials are
+  // summed by the consumer kernel), keeping at least 256 K per split.
   int splits = 1;
-  while (tiles * splits < 256 && K / (splits * 2) >= 8 * kstep && splits < 8) splits *= 2;
+  while (tiles * splits < 384 && K / (splits * 2) >= 256 && splits < kMaxSplitsGemm) splits *= 2;
   const int ktiles = cdiv(K, kstep);
   p.k_per_split = cdiv(ktiles, splits) * kstep;
   p.splits = cdiv(K, p.k_per_split);
   return p;
 }
 
-hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A, const void* W, float* P, size_t split_stride,
-                       const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st) {
+hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W, float* P,
+                       size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st) {
   const dim3 grid(cdiv(N, p.bn), cdiv(max_rows, p.bm), p.splits);
   if (dt == DType::F32) {
-    hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, st, static_cast<const float*>(A),
+    hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, st, static_cast<const float*>(A0),
                        static_cast<const float*>(W), P, split_stride, c, s, max_rows, N, K, p.k_per_split);
   } else if (p.bm == 128) {
-    hipLaunchKernelGGL((k_gemm_bf16<128, 128>), grid, dim3(256), 0, st, static_cast<const float*>(A),
-                       static_cast<const bf16*>(W), P, split_stride, c, s, max_rows, N, K, p.k_per_split);
+    hipLaunchKernelGGL((k_gemm_dma<128, 128, 3>), grid, dim3(256), 0, st, static_cast<const bf16*>(A0),
+                       static_cast<const bf16*>(A1), static_cast<const bf16*>(W), P, split_stride, c, s, max_rows,
+                       N, K, p.k_per_split);
   } else {
-    hipLaunchKernelGGL((k_gemm_bf16<64, 128>), grid, dim3(256), 0, st, static_cast<const float*>(A),
-                       static_cast<const bf16*>(W), P, split_stride, c, s, max_rows, N, K, p.k_per_split);
+    hipLaunchKernelGGL((k_gemm_dma<64, 128, 3>), grid, dim3(256), 0, st, static_cast<const bf16*>(A0),
+                       static_cast<const bf16*>(A1), static_cast<const bf16*>(W), P, split_stride, c, s, max_rows,
+                       N, K, p.k_per_split);
   }
   return hipGetLastError();
 }

@@ -66,144 +66,198 @@ __global__ void k_embed(const T* E, const int* tok, int V, float* x, int d) {
 
 // ------------------------------------------------------------------ add + RMSNorm
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_add_norm(const float* x_in, const float* P, int nsplit,
-                                                  size_t split_stride, int gather, const Ctrl* c, int s,
-                                                  float* x_out, T* xn, const float* gamma, int d, float eps) {
+// One 1024-thread block per row; each thread keeps up to MAXC float4 chunks of
+// the row in registers, so every load of the row is issued before the first
+// wait and the row is read exactly once.
+constexpr int kMaxSplits = kMaxSplitsGemm;
+
+// Writes 4 consecutive projection-input values: fp32, or (kSplit) as the bf16
+// hi/lo planes, the lo plane starting plane_stride elements after the hi plane.
+template <bool kSplit>
+__device__ __forceinline__ void store_act4(void* base, size_t idx, size_t plane_stride, float a, float b, float c,
+                                           float d) {
+  if (kSplit) {
+    uint16_t h0, l0, h1, l1, h2, l2, h3, l3;
+    split2(a, h0, l0);
+    split2(b, h1, l1);
+    split2(c, h2, l2);
+    split2(d, h3, l3);
+    bf16* p = static_cast<bf16*>(base);
+    *reinterpret_cast<uint2*>(p + idx) = make_uint2(pack2(h0, h1), pack2(h2, h3));
+    *reinterpret_cast<uint2*>(p + plane_stride + idx) = make_uint2(pack2(l0, l1), pack2(l2, l3));
+  } else {
+    *reinterpret_cast<float4*>(static_cast<float*>(base) + idx) = make_float4(a, b, c, d);
+  }
+}
+
+template <int MAXC, bool kSplit>
+__global__ __launch_bounds__(1024) void k_add_norm(const float* __restrict__ x_in, const float* __restrict__ P,
+                                                   int nsplit, size_t split_stride, int gather, const Ctrl* c,
+                                                   int s, float* __restrict__ x_out, void* __restrict__ xn,
+                                                   const float* __restrict__ gamma, int d, float eps) {
   __shared__ float red[16];
   const int r = blockIdx.x;
   if (r >= c->live_count * s) return;
   const int src = gather ? c->gather_src[r / s] * s + (r % s) : r;
   const float* xi = x_in + (size_t)src * d;
-  float* xo = x_out + (size_t)r * d;
+  float4 v[MAXC];
   float ss = 0.f;
-  for (int col = threadIdx.x * 4; col < d; col += blockDim.x * 4) {
-    float4 v = *reinterpret_cast<const float4*>(xi + col);
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const float4 p = *reinterpret_cast<const float4*>(P + sp * split_stride + (size_t)src * d + col);
-      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) {
+    const int col = (threadIdx.x + j * 1024) * 4;
+    v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (col < d) {
+      v[j] = *reinterpret_cast<const float4*>(xi + col);
+#pragma unroll
+      for (int sp = 0; sp < kMaxSplits; ++sp) {
+        if (sp < nsplit) {
+          const float4 p = *reinterpret_cast<const float4*>(P + sp * split_stride + (size_t)src * d + col);
+          v[j].x += p.x; v[j].y += p.y; v[j].z += p.z; v[j].w += p.w;
+        }
+      }
+      ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
     }
-    *reinterpret_cast<float4*>(xo + col) = v;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float tot = block_sum(ss, red);
   const float rinv = rsqrtf(tot / (float)d + eps);
-  T* xr = xn + (size_t)r * d;
-  for (int col = threadIdx.x * 4; col < d; col += blockDim.x * 4) {
-    const float4 v = *reinterpret_cast<const float4*>(xo + col);
-    const float4 g = *reinterpret_cast<const float4*>(gamma + col);
-    store4(xr + col, g.x * v.x * rinv, g.y * v.y * rinv, g.z * v.z * rinv, g.w * v.w * rinv);
+  float* xo = x_out + (size_t)r * d;
+  const size_t plane = (size_t)gridDim.x * d;
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) {
+    const int col = (threadIdx.x + j * 1024) * 4;
+    if (col < d) {
+      *reinterpret_cast<float4*>(xo + col) = v[j];
+      const float4 g = *reinterpret_cast<const float4*>(gamma + col);
+      store_act4<kSplit>(xn, (size_t)r * d + col, plane, g.x * v[j].x * rinv, g.y * v[j].y * rinv,
+                         g.z * v[j].z * rinv, g.w * v[j].w * rinv);
+    }
   }
 }
 
 // ------------------------------------------------------------------ QKV epilogue
 
-// One block per row. Pair unit u covers columns (hh*hd + j, hh*hd + j + hd/2) of
-// head hh of the [q | k | v] output; q and k pairs are rotated by RoPE.
+// Thread (unit u, row r): unit u covers columns (hh*hd + j, hh*hd + j + hd/2)
+// of head hh of the [q | k | v] output; q and k pairs are rotated by RoPE.
 template <typename T>
-__global__ __launch_bounds__(256) void k_qkv_post(const float* P, int nsplit, size_t split_stride,
+__global__ __launch_bounds__(256) void k_qkv_post(const float* __restrict__ P, int nsplit, size_t split_stride,
                                                   const Ctrl* c, int s, int H, int Hkv, int hd,
-                                                  const float2* rope, T* q, T* k_own, T* v_own) {
-  const int r = blockIdx.x;
+                                                  const float2* __restrict__ rope, T* __restrict__ q,
+                                                  T* __restrict__ k_own, T* __restrict__ v_own) {
+  const int r = blockIdx.y;
   if (r >= c->live_count * s) return;
-  const int slot = r / s, i = r % s;
   const int half = hd / 2;
-  const int N = (H + 2 * Hkv) * hd;
   const int units = (H + 2 * Hkv) * half;
+  const int u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= units) return;
+  const int slot = r / s, i = r % s;
+  const int N = (H + 2 * Hkv) * hd;
   const float* pr = P + (size_t)r * N;
-  for (int u = threadIdx.x; u < units; u += blockDim.x) {
-    const int hh = u / half, j = u % half;
-    const int c1 = hh * hd + j, c2 = c1 + half;
-    float x1 = 0.f, x2 = 0.f;
-    for (int sp = 0; sp < nsplit; ++sp) {
+  const int hh = u / half, j = u % half;
+  const int c1 = hh * hd + j, c2 = c1 + half;
+  float x1 = 0.f, x2 = 0.f;
+#pragma unroll
+  for (int sp = 0; sp < kMaxSplits; ++sp) {
+    if (sp < nsplit) {
       x1 += pr[sp * split_stride + c1];
       x2 += pr[sp * split_stride + c2];
     }
-    if (hh < H + Hkv) {
-      const float2 cs = rope[i * half + j];
-      const float y1 = x1 * cs.x - x2 * cs.y;
-      const float y2 = x2 * cs.x + x1 * cs.y;
-      x1 = y1;
-      x2 = y2;
-    }
-    T* dst;
-    if (hh < H) {
-      dst = q + ((size_t)r * H + hh) * hd;
-    } else if (hh < H + Hkv) {
-      dst = k_own + (((size_t)slot * Hkv + (hh - H)) * s + i) * hd;
-    } else {
-      dst = v_own + (((size_t)slot * Hkv + (hh - H - Hkv)) * s + i) * hd;
-    }
-    dst[j] = from_f32<T>(x1);
-    dst[j + half] = from_f32<T>(x2);
   }
+  if (hh < H + Hkv) {
+    const float2 cs = rope[i * half + j];
+    const float y1 = x1 * cs.x - x2 * cs.y;
+    const float y2 = x2 * cs.x + x1 * cs.y;
+    x1 = y1;
+    x2 = y2;
+  }
+  T* dst;
+  if (hh < H) {
+    dst = q + ((size_t)r * H + hh) * hd;
+  } else if (hh < H + Hkv) {
+    dst = k_own + (((size_t)slot * Hkv + (hh - H)) * s + i) * hd;
+  } else {
+    dst = v_own + (((size_t)slot * Hkv + (hh - H - Hkv)) * s + i) * hd;
+  }
+  dst[j] = from_f32<T>(x1);
+  dst[j + half] = from_f32<T>(x2);
 }
 
 // ------------------------------------------------------------------ SwiGLU epilogue
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_swiglu_post(const float* P, int nsplit, size_t split_stride,
-                                                     const Ctrl* c, int s, int F, T* a) {
-  const int r = blockIdx.x;
+// Thread (4 columns, row r); F is a multiple of 8, so float4 groups never straddle.
+template <bool kSplit>
+__global__ __launch_bounds__(256) void k_swiglu_post(const float* __restrict__ P, int nsplit, size_t split_stride,
+                                                     const Ctrl* c, int s, int F, void* __restrict__ a) {
+  const int r = blockIdx.y;
   if (r >= c->live_count * s) return;
+  const int f = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (f >= F) return;
   const float* pr = P + (size_t)r * 2 * F;
-  T* ar = a + (size_t)r * F;
-  for (int f = threadIdx.x; f < F; f += blockDim.x) {
-    float g = 0.f, u = 0.f;
-    for (int sp = 0; sp < nsplit; ++sp) {
-      g += pr[sp * split_stride + f];
-      u += pr[sp * split_stride + F + f];
+  float4 g = make_float4(0.f, 0.f, 0.f, 0.f), u = g;
+#pragma unroll
+  for (int sp = 0; sp < kMaxSplits; ++sp) {
+    if (sp < nsplit) {
+      const float4 pg = *reinterpret_cast<const float4*>(pr + sp * split_stride + f);
+      const float4 pu = *reinterpret_cast<const float4*>(pr + sp * split_stride + F + f);
+      g.x += pg.x; g.y += pg.y; g.z += pg.z; g.w += pg.w;
+      u.x += pu.x; u.y += pu.y; u.z += pu.z; u.w += pu.w;
     }
-    const float silu = g / (1.f + expf(-g));
-    ar[f] = from_f32<T>(silu * u);
   }
+  store_act4<kSplit>(a, (size_t)r * F + f, (size_t)gridDim.y * F, g.x / (1.f + expf(-g.x)) * u.x,
+                     g.y / (1.f + expf(-g.y)) * u.y, g.z / (1.f + expf(-g.z)) * u.z, g.w / (1.f + expf(-g.w)) * u.w);
 }
 
 // ------------------------------------------------------------------ last-token tap
 
-template <bool kSplitBf16>
-__global__ __launch_bounds__(256) void k_tap(const float* x, const float* P, int nsplit, size_t split_stride,
-                                             const Ctrl* c, int s, int d, int B, int layer0,
-                                             float* hidden_last, const float* gamma, float eps, void* hn_a,
-                                             void* hn_b) {
+template <bool kSplitBf16, int MAXC>
+__global__ __launch_bounds__(1024) void k_tap(const float* __restrict__ x, const float* __restrict__ P, int nsplit,
+                                              size_t split_stride, const Ctrl* c, int s, int d, int B, int layer0,
+                                              float* __restrict__ hidden_last, const float* __restrict__ gamma,
+                                              float eps, void* hn_a, void* hn_b) {
   __shared__ float red[16];
   const int slot = blockIdx.x;
   if (slot >= c->live_count) return;
   const int branch = c->live_idx[slot];
   const size_t row = (size_t)slot * s + (s - 1);
+  float4 v[MAXC];
   float ss = 0.f;
-  for (int col = threadIdx.x * 4; col < d; col += blockDim.x * 4) {
-    float4 v = *reinterpret_cast<const float4*>(x + row * d + col);
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const float4 p = *reinterpret_cast<const float4*>(P + sp * split_stride + row * d + col);
-      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) {
+    const int col = (threadIdx.x + j * 1024) * 4;
+    v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (col < d) {
+      v[j] = *reinterpret_cast<const float4*>(x + row * d + col);
+#pragma unroll
+      for (int sp = 0; sp < kMaxSplits; ++sp) {
+        if (sp < nsplit) {
+          const float4 p = *reinterpret_cast<const float4*>(P + sp * split_stride + row * d + col);
+          v[j].x += p.x; v[j].y += p.y; v[j].z += p.z; v[j].w += p.w;
+        }
+      }
+      ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
     }
-    if (hidden_last)
-      *reinterpret_cast<float4*>(hidden_last + ((size_t)layer0 * B + branch) * d + col) = v;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float tot = block_sum(ss, red);
   const float rinv = rsqrtf(tot / (float)d + eps);
-  for (int col = threadIdx.x * 4; col < d; col += blockDim.x * 4) {
-    // Second pass recomputes h (same additions in the same order, so the same value).
-    float4 v = *reinterpret_cast<const float4*>(x + row * d + col);
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const float4 p = *reinterpret_cast<const float4*>(P + sp * split_stride + row * d + col);
-      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
-    }
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) {
+    const int col = (threadIdx.x + j * 1024) * 4;
+    if (col >= d) continue;
+    if (hidden_last)
+      *reinterpret_cast<float4*>(hidden_last + ((size_t)layer0 * B + branch) * d + col) = v[j];
     const float4 g = *reinterpret_cast<const float4*>(gamma + col);
-    const float h0 = g.x * v.x * rinv, h1 = g.y * v.y * rinv, h2 = g.z * v.z * rinv, h3 = g.w * v.w * rinv;
+    const float h0 = g.x * v[j].x * rinv, h1 = g.y * v[j].y * rinv, h2 = g.z * v[j].z * rinv, h3 = g.w * v[j].w * rinv;
     if (kSplitBf16) {
       // hn = hi + lo with hi = bf16(hn) and lo = bf16(hn - hi): the lm_head product
       // then runs on bf16 MFMA with ~2^-16 relative error on the activation.
-      bf16* hi = static_cast<bf16*>(hn_a) + (size_t)slot * d + col;
-      bf16* lo = static_cast<bf16*>(hn_b) + (size_t)slot * d + col;
-      const uint16_t b0 = f32_to_bf16_bits(h0), b1 = f32_to_bf16_bits(h1);
-      const uint16_t b2 = f32_to_bf16_bits(h2), b3 = f32_to_bf16_bits(h3);
-      store4(hi, bf16_to_f32(b0), bf16_to_f32(b1), bf16_to_f32(b2), bf16_to_f32(b3));
-      store4(lo, h0 - bf16_to_f32(b0), h1 - bf16_to_f32(b1), h2 - bf16_to_f32(b2), h3 - bf16_to_f32(b3));
+      uint16_t b0, b1, b2, b3, l0, l1, l2, l3;
+      split2(h0, b0, l0);
+      split2(h1, b1, l1);
+      split2(h2, b2, l2);
+      split2(h3, b3, l3);
+      *reinterpret_cast<uint2*>(static_cast<bf16*>(hn_a) + (size_t)slot * d + col) = make_uint2(pack2(b0, b1), pack2(b2, b3));
+      *reinterpret_cast<uint2*>(static_cast<bf16*>(hn_b) + (size_t)slot * d + col) = make_uint2(pack2(l0, l1), pack2(l2, l3));
     } else {
-      store4(static_cast<float*>(hn_a) + (size_t)slot * d + col, h0, h1, h2, h3);
+      *reinterpret_cast<float4*>(static_cast<float*>(hn_a) + (size_t)slot * d + col) = make_float4(h0, h1, h2, h3);
     }
   }
 }
@@ -286,37 +340,53 @@ hipError_t launch_embed(DType dt, const void* E, const int* tok, int V, float* x
   return hipGetLastError();
 }
 
-hipError_t launch_add_norm(const float* x_in, const float* P, int nsplit, size_t split_stride, bool gather,
-                           const Ctrl* c, int s, float* x_out, float* xn, const float* gamma, int d, float eps,
-                           int max_rows, hipStream_t st) {
-  hipLaunchKernelGGL(k_add_norm<float>, dim3(max_rows), dim3(256), 0, st, x_in, P, nsplit, split_stride,
-                     (int)gather, c, s, x_out, xn, gamma, d, eps);
+hipError_t launch_add_norm(DType dt, const float* x_in, const float* P, int nsplit, size_t split_stride,
+                           bool gather, const Ctrl* c, int s, float* x_out, void* xn, const float* gamma, int d,
+                           float eps, int max_rows, hipStream_t st) {
+  const int chunks = (d / 4 + 1023) / 1024;
+#define RKSC_NORM(MAXC, SPLIT)                                                                                   \
+  hipLaunchKernelGGL((k_add_norm<MAXC, SPLIT>), dim3(max_rows), dim3(1024), 0, st, x_in, P, nsplit, split_stride, \
+                     (int)gather, c, s, x_out, xn, gamma, d, eps)
+  const bool sp = dt == DType::BF16;
+  if (chunks <= 1) { if (sp) RKSC_NORM(1, true); else RKSC_NORM(1, false); }
+  else if (chunks <= 2) { if (sp) RKSC_NORM(2, true); else RKSC_NORM(2, false); }
+  else { if (sp) RKSC_NORM(4, true); else RKSC_NORM(4, false); }
+#undef RKSC_NORM
   return hipGetLastError();
 }
 
 hipError_t launch_qkv_post(const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s, int H,
                            int Hkv, int hd, const float2* rope, float* q, float* k_own, float* v_own,
                            int max_rows, hipStream_t st) {
-  hipLaunchKernelGGL(k_qkv_post<float>, dim3(max_rows), dim3(256), 0, st, P, nsplit, split_stride, c, s, H, Hkv,
-                     hd, rope, q, k_own, v_own);
+  const int units = (H + 2 * Hkv) * hd / 2;
+  hipLaunchKernelGGL(k_qkv_post<float>, dim3((units + 255) / 256, max_rows), dim3(256), 0, st, P, nsplit,
+                     split_stride, c, s, H, Hkv, hd, rope, q, k_own, v_own);
   return hipGetLastError();
 }
 
-hipError_t launch_swiglu_post(const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s, int F,
-                              float* a, int max_rows, hipStream_t st) {
-  hipLaunchKernelGGL(k_swiglu_post<float>, dim3(max_rows), dim3(256), 0, st, P, nsplit, split_stride, c, s, F, a);
+hipError_t launch_swiglu_post(DType dt, const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s,
+                              int F, void* a, int max_rows, hipStream_t st) {
+  const dim3 grid((F / 4 + 255) / 256, max_rows);
+  if (dt == DType::BF16)
+    hipLaunchKernelGGL(k_swiglu_post<true>, grid, dim3(256), 0, st, P, nsplit, split_stride, c, s, F, a);
+  else
+    hipLaunchKernelGGL(k_swiglu_post<false>, grid, dim3(256), 0, st, P, nsplit, split_stride, c, s, F, a);
   return hipGetLastError();
 }
 
 hipError_t launch_tap(DType dt, const float* x, const float* P, int nsplit, size_t split_stride, const Ctrl* c,
                       int s, int d, int B, int layer0, float* hidden_last, const float* gamma, float eps,
                       void* hn_a, void* hn_b, int max_branches, hipStream_t st) {
-  if (dt == DType::BF16)
-    hipLaunchKernelGGL(k_tap<true>, dim3(max_branches), dim3(256), 0, st, x, P, nsplit, split_stride, c, s, d, B,
-                       layer0, hidden_last, gamma, eps, hn_a, hn_b);
-  else
-    hipLaunchKernelGGL(k_tap<false>, dim3(max_branches), dim3(256), 0, st, x, P, nsplit, split_stride, c, s, d,
-                       B, layer0, hidden_last, gamma, eps, hn_a, hn_b);
+  const int chunks = (d / 4 + 1023) / 1024;
+#define RKSC_TAP(SPLIT, MAXC)                                                                                   \
+  hipLaunchKernelGGL((k_tap<SPLIT, MAXC>), dim3(max_branches), dim3(1024), 0, st, x, P, nsplit, split_stride, c, \
+                     s, d, B, layer0, hidden_last, gamma, eps, hn_a, hn_b)
+  if (dt == DType::BF16) {
+    if (chunks <= 1) RKSC_TAP(true, 1); else if (chunks <= 2) RKSC_TAP(true, 2); else RKSC_TAP(true, 4);
+  } else {
+    if (chunks <= 1) RKSC_TAP(false, 1); else if (chunks <= 2) RKSC_TAP(false, 2); else RKSC_TAP(false, 4);
+  }
+#undef RKSC_TAP
   return hipGetLastError();
 }
 

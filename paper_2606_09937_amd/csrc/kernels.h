@@ -31,19 +31,21 @@ hipError_t launch_embed(DType dt, const void* E, const int* tok, int V, float* x
                         hipStream_t st);
 
 // ---- per-layer row kernels
-// Activations between kernels are fp32 for every model dtype.
+// Projection inputs (xn, attention output o, SwiGLU output a) are written as bf16
+// hi/lo planes for BF16 models (plane lo follows plane hi: max_rows rows each)
+// and as fp32 for F32 models; q, k_own, v_own and the residual stream are fp32.
 // x_out[r] = x_in[src(r)] + sum_sp P[sp][src(r)] ; xn[r] = RMSNorm(x_out[r]; gamma).
 // gather: src(r) = gather_src[r / s] * s + r % s, else src(r) = r (x_in may equal x_out).
-hipError_t launch_add_norm(const float* x_in, const float* P, int nsplit, size_t split_stride, bool gather,
-                           const Ctrl* c, int s, float* x_out, float* xn, const float* gamma, int d, float eps,
-                           int max_rows, hipStream_t st);
+hipError_t launch_add_norm(DType dt, const float* x_in, const float* P, int nsplit, size_t split_stride,
+                           bool gather, const Ctrl* c, int s, float* x_out, void* xn, const float* gamma, int d,
+                           float eps, int max_rows, hipStream_t st);
 // q [rows, H, hd], k_own/v_own [B, Hkv, s, hd] from the summed QKV partials, RoPE on q and k.
 hipError_t launch_qkv_post(const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s, int H,
                            int Hkv, int hd, const float2* rope, float* q, float* k_own, float* v_own,
                            int max_rows, hipStream_t st);
 // a = silu(gate) * up from the summed gate|up partials.
-hipError_t launch_swiglu_post(const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s, int F,
-                              float* a, int max_rows, hipStream_t st);
+hipError_t launch_swiglu_post(DType dt, const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s,
+                              int F, void* a, int max_rows, hipStream_t st);
 // Last token of each live branch: h = x + sum_sp P; hidden_last[l][branch] = h;
 // hn = RMSNorm(h; final_norm) as fp32 (F32) or as a bf16 hi+lo pair (BF16).
 hipError_t launch_tap(DType dt, const float* x, const float* P, int nsplit, size_t split_stride,
@@ -51,19 +53,25 @@ hipError_t launch_tap(DType dt, const float* x, const float* P, int nsplit, size
                       const float* gamma, float eps, void* hn_a, void* hn_b, int max_branches,
                       hipStream_t st);
 
-// ---- GEMM: P[split][m][n] = sum_{k in split} A[m][k] * W[n][k], rows m < live*s;
-// A fp32, W of the model dtype.
+// ---- GEMM: P[split][m][n] = sum_{k in split} A[m][k] * W[n][k], rows m < live*s.
+// BF16 models: A0/A1 are the bf16 hi/lo planes of the activation, W bf16.
+// F32 models: A0 is the fp32 activation (A1 unused), W fp32.
+constexpr int kMaxSplitsGemm = 8;   // the consumers of split partials sum at most this many
 struct GemmPlan {
   int bm, bn, splits, k_per_split;
 };
 GemmPlan plan_gemm(DType dt, int max_rows, int N, int K);
-hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A, const void* W, float* P, size_t split_stride,
-                       const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st);
+hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W, float* P,
+                       size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st);
 
-// ---- attention over [shared prefix ; own causal span]: q, k_own, v_own, o fp32; prefix of the model dtype.
+// ---- attention over [shared prefix ; own causal span]: q, k_own, v_own fp32; prefix of the
+// model dtype; o is the projection input (bf16 hi/lo planes for BF16 models, fp32 otherwise).
+// With nchunks > 1 the prefix is split across workgroups (split-KV); opart
+// [nchunks, B*s, H, hd] and mlpart [nchunks, B*s, H, 2] hold the partials.
+int attention_chunks(DType dt, int B, int n, int s, int H, int Hkv);
 hipError_t launch_attention(DType dt, const void* q, const void* pk, const void* pv, const void* k_own,
-                            const void* v_own, void* o, const Ctrl* c, int n, int s, int H, int Hkv, int hd,
-                            int max_branches, hipStream_t st);
+                            const void* v_own, void* o, float* opart, float* mlpart, int nchunks, const Ctrl* c,
+                            int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st);
 
 // ---- entropy of the live branches' last-token logits
 int entropy_parts(DType dt, int V, int max_branches);

@@ -39,9 +39,10 @@ using rksc::DType;
 using rksc::GemmPlan;
 
 struct Layout {
-  size_t ctrl, x0, x1, act, ffn, q, kown, vown, pbig, pres, hn_a, hn_b, parts, rope, total;
+  size_t ctrl, x0, x1, act, ffn, q, kown, vown, pbig, pres, hn_a, hn_b, parts, rope, opart, mlpart, total;
   GemmPlan qkv, o, gu, down;
   int nparts;
+  int attn_chunks;
   int max_rows;
 };
 
@@ -50,7 +51,7 @@ rksc_status check_config(const rksc_model_config* c) {
   if (c->n_layers < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_layers must be >= 1 (got %d)", c->n_layers);
   if (c->d_model < 8 || c->d_model % 8)
     return fail(RKSC_ERR_UNSUPPORTED, "d_model must be a positive multiple of 8 (got %d)", c->d_model);
-  if (c->d_model > 65536) return fail(RKSC_ERR_UNSUPPORTED, "d_model above 65536 (got %d)", c->d_model);
+  if (c->d_model > 16384) return fail(RKSC_ERR_UNSUPPORTED, "d_model above 16384 (got %d)", c->d_model);
   if (c->n_heads < 1 || c->n_kv_heads < 1)
     return fail(RKSC_ERR_INVALID_ARGUMENT, "head counts must be >= 1 (got %d, %d)", c->n_heads, c->n_kv_heads);
   if (c->n_heads % c->n_kv_heads)
@@ -69,7 +70,7 @@ rksc_status check_config(const rksc_model_config* c) {
   return RKSC_OK;
 }
 
-rksc_status make_layout(const rksc_model_config* c, int B, int s, Layout* lay) {
+rksc_status make_layout(const rksc_model_config* c, int B, int s, int n_prefix, Layout* lay) {
   rksc_status st = check_config(c);
   if (st != RKSC_OK) return st;
   if (B < 1 || B > RKSC_MAX_BRANCHES)
@@ -111,6 +112,10 @@ rksc_status make_layout(const rksc_model_config* c, int B, int s, Layout* lay) {
   lay->hn_b = take((size_t)RKSC_MAX_BRANCHES * d * 2);
   lay->parts = take((size_t)lay->nparts * 64 * 3 * 4);
   lay->rope = take((size_t)s * (hd / 2) * 8);
+  lay->attn_chunks = rksc::attention_chunks(dt, B, n_prefix, s, H, Hkv);
+  const size_t nch = lay->attn_chunks > 1 ? (size_t)lay->attn_chunks : 0;
+  lay->opart = take(nch * Ms * H * hd * 4);
+  lay->mlpart = take(nch * Ms * H * 2 * 4);
   lay->total = off;
   return RKSC_OK;
 }
@@ -140,9 +145,13 @@ RKSC_EXPORT const char* rksc_status_string(rksc_status s) {
 RKSC_EXPORT const char* rksc_last_error(void) { return g_last_error.c_str(); }
 
 RKSC_EXPORT size_t rksc_verify_workspace_size(const rksc_model_config* cfg, int32_t n_branches,
-                                              int32_t branch_len) {
+                                              int32_t branch_len, int32_t n_prefix) {
+  if (n_prefix < 0) {
+    fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", n_prefix);
+    return 0;
+  }
   Layout lay;
-  if (make_layout(cfg, n_branches, branch_len, &lay) != RKSC_OK) return 0;
+  if (make_layout(cfg, n_branches, branch_len, n_prefix, &lay) != RKSC_OK) return 0;
   return lay.total;
 }
 
@@ -165,8 +174,9 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
   if (std::isnan(tau) || tau < 0.f) return fail(RKSC_ERR_INVALID_ARGUMENT, "tau must be >= 0 and not NaN");
   if (patience < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "patience must be >= 1 (got %d)", patience);
   const rksc_model_config* c = &w->cfg;
+  if (kv->n_prefix < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", kv->n_prefix);
   Layout lay;
-  rksc_status st = make_layout(c, n_branches, branch_len, &lay);
+  rksc_status st = make_layout(c, n_branches, branch_len, kv->n_prefix, &lay);
   if (st != RKSC_OK) return st;
   if (workspace_bytes < lay.total)
     return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
@@ -203,7 +213,13 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
   void* hn_b = ws + lay.hn_b;
   float* parts = reinterpret_cast<float*>(ws + lay.parts);
   float2* rope = reinterpret_cast<float2*>(ws + lay.rope);
+  float* opart = reinterpret_cast<float*>(ws + lay.opart);
+  float* mlpart = reinterpret_cast<float*>(ws + lay.mlpart);
   const size_t res_stride = (size_t)M * d;
+  // Start of the lo plane of a BF16-model projection input of `elems` elements per plane.
+  auto plane_lo = [&](float* buf, size_t elems) -> const void* {
+    return dt == DType::BF16 ? static_cast<const void*>(reinterpret_cast<const uint16_t*>(buf) + elems) : nullptr;
+  };
 
   HIP_TRY(rksc::launch_init(ctrl, B, L, entropy, exit_layer, hidden_last, (size_t)L * B * d, strm));
   HIP_TRY(rksc::launch_rope_table(rope, s, n, hd, (double)c->rope_base, strm));
@@ -222,29 +238,35 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     float* x_prev = (l % 2 == 0) ? x0 : x1;
     float* x_cur = (l % 2 == 0) ? x1 : x0;
     // Residual stream of the live rows (gathered), plus the previous layer's FFN output.
-    HIP_TRY(rksc::launch_add_norm(x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, true, ctrl, s,
+    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, true, ctrl, s,
                                   x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
     HIP_TRY(mark(l, 0));
-    HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl, s, M, Nqkv, d, strm));
+    // Projection inputs: bf16 planes hi = act[0, M*K), lo = act[M*K, 2*M*K) for BF16 models.
+    HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
+                              s, M, Nqkv, d, strm));
     HIP_TRY(mark(l, 1));
     HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
                                   vown, M, strm));
     const void* pk = n > 0 ? pk_base + l * kv_layer : nullptr;
     const void* pv = n > 0 ? pv_base + l * kv_layer : nullptr;
     HIP_TRY(mark(l, 2));
-    HIP_TRY(rksc::launch_attention(dt, qb, pk, pv, kown, vown, act, ctrl, n, s, H, Hkv, hd, B, strm));
+    HIP_TRY(rksc::launch_attention(dt, qb, pk, pv, kown, vown, act, opart, mlpart, lay.attn_chunks, ctrl, n, s, H,
+                                   Hkv, hd, B, strm));
     HIP_TRY(mark(l, 3));
     HIP_TRY(mark(l, 4));
-    HIP_TRY(rksc::launch_gemm(dt, lay.o, act, lw.w_o, pres, res_stride, ctrl, s, M, d, H * hd, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.o, act, plane_lo(act, (size_t)M * H * hd), lw.w_o, pres, res_stride, ctrl, s,
+                              M, d, H * hd, strm));
     HIP_TRY(mark(l, 5));
-    HIP_TRY(rksc::launch_add_norm(x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
+    HIP_TRY(rksc::launch_add_norm(dt, x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
                                   lw.ffn_norm, d, c->rms_eps, M, strm));
     HIP_TRY(mark(l, 6));
-    HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, lw.w_gate_up, pbig, (size_t)M * 2 * F, ctrl, s, M, 2 * F, d, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig, (size_t)M * 2 * F,
+                              ctrl, s, M, 2 * F, d, strm));
     HIP_TRY(mark(l, 7));
-    HIP_TRY(rksc::launch_swiglu_post(pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
+    HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
     HIP_TRY(mark(l, 8));
-    HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, lw.w_down, pres, res_stride, ctrl, s, M, d, F, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
+                              M, d, F, strm));
     HIP_TRY(mark(l, 9));
     HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, B, l, hidden_last,
                              w->final_norm, c->rms_eps, hn_a, hn_b, B, strm));
@@ -293,29 +315,39 @@ RKSC_EXPORT rksc_status rksc_asks_similarity(const float* hidden, int32_t n_laye
 
 // ------------------------------------------------------------------ kernel-level test entry points
 
-RKSC_EXPORT rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* W, float* P, int32_t M, int32_t N,
-                                       int32_t K, int32_t splits, int32_t* splits_used, void* stream) {
+RKSC_EXPORT rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P,
+                                       int32_t M, int32_t N, int32_t K, int32_t splits, int32_t* splits_used,
+                                       void* stream) {
   if (!A || !W || !P) return fail(RKSC_ERR_INVALID_ARGUMENT, "A, W and P must not be NULL");
+  if (dtype == RKSC_BF16 && !A_lo) return fail(RKSC_ERR_INVALID_ARGUMENT, "A_lo must not be NULL for bf16");
   if (dtype != RKSC_F32 && dtype != RKSC_BF16) return fail(RKSC_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
   if (M < 1 || N < 1 || K < 8 || K % 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "bad shape %d x %d x %d", M, N, K);
   if (splits < 0 || splits > 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "splits must be in [0, 8]");
   const DType dt = dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
   GemmPlan p = rksc::plan_gemm(dt, M, N, K);
   if (splits > 0) {
-    const int kstep = dt == DType::BF16 ? 64 : 16;
+    const int kstep = dt == DType::BF16 ? 32 : 16;
     const int ktiles = (K + kstep - 1) / kstep;
     p.k_per_split = (ktiles + splits - 1) / splits * kstep;
     p.splits = (K + p.k_per_split - 1) / p.k_per_split;
   }
   if (splits_used) *splits_used = p.splits;
-  HIP_TRY(rksc::launch_gemm(dt, p, A, W, P, (size_t)M * N, nullptr, 1, M, N, K, static_cast<hipStream_t>(stream)));
+  HIP_TRY(rksc::launch_gemm(dt, p, A, A_lo, W, P, (size_t)M * N, nullptr, 1, M, N, K,
+                            static_cast<hipStream_t>(stream)));
   return ok();
+}
+
+RKSC_EXPORT size_t rksc_test_attention_scratch_size(int32_t dtype, int32_t B, int32_t n, int32_t s, int32_t H,
+                                                   int32_t Hkv, int32_t hd) {
+  if (B < 1 || s < 1 || n < 0 || H < 1 || Hkv < 1 || H % Hkv || hd < 1) return 0;
+  const int nch = rksc::attention_chunks(dtype == RKSC_BF16 ? DType::BF16 : DType::F32, B, n, s, H, Hkv);
+  return 4096 + (nch > 1 ? (size_t)nch * B * s * H * (hd + 2) * 4 : 0);
 }
 
 RKSC_EXPORT rksc_status rksc_test_attention(int32_t dtype, const void* q, const void* prefix_k, const void* prefix_v,
                                             const void* k_own, const void* v_own, void* o, int32_t B, int32_t n,
                                             int32_t s, int32_t H, int32_t Hkv, int32_t hd, void* scratch,
-                                            void* stream) {
+                                            size_t scratch_bytes, void* stream) {
   if (!q || !k_own || !v_own || !o || !scratch) return fail(RKSC_ERR_INVALID_ARGUMENT, "NULL pointer");
   if (n > 0 && (!prefix_k || !prefix_v)) return fail(RKSC_ERR_INVALID_ARGUMENT, "NULL prefix with n > 0");
   if (dtype != RKSC_F32 && dtype != RKSC_BF16) return fail(RKSC_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
@@ -324,8 +356,16 @@ RKSC_EXPORT rksc_status rksc_test_attention(int32_t dtype, const void* q, const 
   if (hd != 64 && hd != 128) return fail(RKSC_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
   hipStream_t st = static_cast<hipStream_t>(stream);
   rksc::Ctrl* ctrl = static_cast<rksc::Ctrl*>(scratch);
+  const DType dt = dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
+  const int nch = rksc::attention_chunks(dt, B, n, s, H, Hkv);
+  const size_t need = 4096 + (nch > 1 ? (size_t)nch * B * s * H * (hd + 2) * 4 : 0);
+  if (scratch_bytes < need)
+    return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "scratch has %zu bytes, needs %zu", scratch_bytes, need);
+  char* sc = static_cast<char*>(scratch);
+  float* opart = reinterpret_cast<float*>(sc + 4096);
+  float* mlpart = opart + (nch > 1 ? (size_t)nch * B * s * H * hd : 0);
   HIP_TRY(rksc::launch_init(ctrl, B, 1, nullptr, nullptr, nullptr, 0, st));
-  HIP_TRY(rksc::launch_attention(dtype == RKSC_BF16 ? DType::BF16 : DType::F32, q, prefix_k, prefix_v, k_own, v_own,
-                                 o, ctrl, n, s, H, Hkv, hd, B, st));
+  HIP_TRY(rksc::launch_attention(dt, q, prefix_k, prefix_v, k_own, v_own, o, opart, mlpart, nch, ctrl, n, s, H, Hkv,
+                                 hd, B, st));
   return ok();
 }

@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
     assert "rksc_verify_forward" in names and "rksc_asks_similarity" in names
     for name in names:
         assert hasattr(lib, name), f"{name} declared in include/ but not exported"
-    assert rk.rksc_abi_version() == 1
+    assert rk.rksc_abi_version() == 2
 
 
 def test_status_strings(lib):
@@ -59,22 +59,24 @@ def _shape(**kw):
 ])
 def test_workspace_size_rejects_bad_shapes(lib, kw, needle):
     with pytest.raises(rk.RkscError) as e:
-        rk.rksc_verify_workspace_size(_shape(**kw), 4, 16)
+        rk.rksc_verify_workspace_size(_shape(**kw), 4, 16, 64)
     assert needle in str(e.value)
 
 
 @pytest.mark.parametrize("B,s", [(0, 16), (65, 16), (4, 0)])
 def test_workspace_size_rejects_bad_batch(lib, B, s):
     with pytest.raises(rk.RkscError):
-        rk.rksc_verify_workspace_size(workloads.get("tiny").model, B, s)
+        rk.rksc_verify_workspace_size(workloads.get("tiny").model, B, s, 64)
 
 
 def test_workspace_size_grows_with_batch(lib):
     shape = workloads.get("tiny").model
-    a = rk.rksc_verify_workspace_size(shape, 1, 16)
-    b = rk.rksc_verify_workspace_size(shape, 4, 16)
-    c = rk.rksc_verify_workspace_size(shape, 4, 64)
+    a = rk.rksc_verify_workspace_size(shape, 1, 16, 64)
+    b = rk.rksc_verify_workspace_size(shape, 4, 16, 64)
+    c = rk.rksc_verify_workspace_size(shape, 4, 64, 64)
     assert 0 < a < b < c
+    with pytest.raises(rk.RkscError):
+        rk.rksc_verify_workspace_size(shape, 4, 16, -1)
 
 
 def _call(lib, shape, B=4, s=16, tau=0.05, patience=1, ws_bytes=None, ws_ptr=0x10000, null=None, n_prefix=8):
@@ -86,7 +88,7 @@ def _call(lib, shape, B=4, s=16, tau=0.05, patience=1, ws_bytes=None, ws_ptr=0x1
         layers[shape.n_layers - 1] = rk.LayerWeights(FAKE, FAKE, None, FAKE, FAKE, FAKE)
     w = rk.Weights(cfg, FAKE, layers, FAKE, None if null == "lm_head" else FAKE)
     kv = rk.PrefixKV(n_prefix, None if null == "prefix" else FAKE, FAKE)
-    need = lib.rksc_verify_workspace_size(ctypes.byref(cfg), B, s) if 1 <= B <= 64 and s >= 1 else 0
+    need = lib.rksc_verify_workspace_size(ctypes.byref(cfg), B, s, n_prefix) if 1 <= B <= 64 and s >= 1 else 0
     size = need if ws_bytes is None else ws_bytes
     args = [ctypes.byref(w), ctypes.byref(kv), None if null == "tokens" else FAKE, B, s, tau, patience,
             None if null == "entropy" else FAKE, None if null == "exit" else FAKE, None,
@@ -110,7 +112,7 @@ def test_verify_rejects_bad_rule(lib, tau, patience):
 def test_verify_rejects_small_or_misaligned_workspace(lib):
     shape = workloads.get("tiny").model
     cfg = rk.model_config(shape)
-    need = lib.rksc_verify_workspace_size(ctypes.byref(cfg), 4, 16)
+    need = lib.rksc_verify_workspace_size(ctypes.byref(cfg), 4, 16, 8)
     assert _call(lib, shape, ws_bytes=need - 1) == rk.RKSC_ERR_WORKSPACE_TOO_SMALL
     assert str(need) in rk.rksc_last_error()
     assert _call(lib, shape, ws_ptr=0x10010) == rk.RKSC_ERR_INVALID_ARGUMENT
@@ -137,7 +139,9 @@ def test_asks_rejects_bad_arguments(lib):
 
 def test_testing_entry_points_reject_bad_shapes(lib):
     used = ctypes.c_int32(0)
-    assert lib.rksc_test_gemm(1, FAKE, FAKE, FAKE, 4, 4, 12, 0, ctypes.byref(used), None) == \
+    assert lib.rksc_test_gemm(1, FAKE, FAKE, FAKE, FAKE, 4, 4, 12, 0, ctypes.byref(used), None) == \
         rk.RKSC_ERR_INVALID_ARGUMENT
-    assert lib.rksc_test_attention(1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 4, 4, 4, 2, 32, FAKE, None) == \
+    assert lib.rksc_test_gemm(1, FAKE, None, FAKE, FAKE, 4, 4, 16, 0, ctypes.byref(used), None) == \
+        rk.RKSC_ERR_INVALID_ARGUMENT
+    assert lib.rksc_test_attention(1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 4, 4, 4, 2, 32, FAKE, 1 << 20, None) == \
         rk.RKSC_ERR_UNSUPPORTED

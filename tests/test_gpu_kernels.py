@@ -25,7 +25,14 @@ def test_gemm_matches_fp64(dtype, M, N, K, splits):
     log(f"gemm {dtype} M={M} N={N} K={K} splits={splits}")
     A = _rand((M, K), torch.float32, 1 + M, 0.5)     # activations are fp32 in every mode
     W = _rand((N, K), dtype, 2 + N, 0.05)
-    P = rk.rksc_test_gemm(A.to(DEV), W.to(DEV), splits=splits)
+    if dtype == torch.bfloat16:
+        # bf16 models feed the projection the hi/lo bf16 planes of the fp32 activation (RNE split).
+        a_hi = A.to(torch.bfloat16)
+        a_lo = (A - a_hi.float()).to(torch.bfloat16)
+        A = a_hi.float() + a_lo.float()                # the value the planes carry
+        P = rk.rksc_test_gemm((a_hi.to(DEV), a_lo.to(DEV)), W.to(DEV), splits=splits)
+    else:
+        P = rk.rksc_test_gemm(A.to(DEV), W.to(DEV), splits=splits)
     torch.cuda.synchronize()
     if splits:
         # a split never gets less than one K tile, so tiny K can use fewer splits than asked
