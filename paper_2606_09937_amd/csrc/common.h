@@ -27,6 +27,21 @@ __device__ __forceinline__ uint4 ldg16(const void* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Direct global->LDS DMA of 16 bytes per lane (global_load_lds_dwordx4): lane L's
+// bytes land at lds_base + 16 * L. lds_base must be uniform across the wave.
+// The transfer counts on the vector-memory counter like an ordinary load.
+__device__ __forceinline__ void dma16(const void* gsrc, void* lds_base) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)gsrc,
+                                   (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t u) {
   return __uint_as_float(static_cast<uint32_t>(u) << 16);
 }

@@ -92,7 +92,12 @@ def test_tiny_deep_fp32_prefill_prefix_and_exits():
     (dataclasses.replace(workloads.get("tiny_deep").model, dtype="bf16"), 3, 50, 21),
     (GQA_BF16, 5, 100, 40),
     (G7_BF16, 2, 129, 65),
-], ids=["tiny_bf16", "tiny_deep_bf16", "gqa_bf16", "g7_bf16"])
+    # wide batches: 17..32 and 33..64 live columns take the lm_head kernel's
+    # two- and four-block variants; 64 is the largest batch the ABI accepts
+    (dataclasses.replace(workloads.get("tiny_deep").model, dtype="bf16"), 20, 30, 5),
+    (G7_BF16, 37, 9, 2),
+    (GQA_BF16, 64, 16, 3),
+], ids=["tiny_bf16", "tiny_deep_bf16", "gqa_bf16", "g7_bf16", "tiny_deep_bf16_b20", "g7_bf16_b37", "gqa_bf16_b64"])
 def test_small_bf16(shape, B, n, s):
     mw, kv, toks = _inputs(shape, B, n, s, seed=3)
     for tau, pat in ((0.05, 1), (0.5, 1), (0.0, 1)):
