@@ -6,12 +6,12 @@
 // per workgroup and branch is written. Logits never reach HBM. A separate
 // single-workgroup kernel merges the per-workgroup triples: H = log s - t/s.
 //
-// bf16: the kernel streams W_lm [V, d] from HBM exactly once per layer. Each
-// wave owns 16*NT vocabulary rows and contracts them against the normalised
-// hidden rows with v_mfma_f32_16x16x32_bf16: W rows are the A operand, the
-// branches the B columns (NCB blocks of 16). The hidden row is supplied as a
-// bf16 hi + lo pair (two MFMAs into one fp32 accumulator), so the product keeps
-// ~2^-16 relative accuracy while W_lm stays in its bf16 storage format.
+// bf16: the kernel streams W_lm [V, d] from HBM exactly once per layer and
+// contracts it against the normalised hidden rows with
+// v_mfma_f32_16x16x32_bf16: W rows are the A operand, the branches the B
+// columns (NCB blocks of 16). The hidden row is supplied as a bf16 hi + lo
+// pair (two MFMAs into one fp32 accumulator), so the product keeps ~2^-16
+// relative accuracy while W_lm stays in its bf16 storage format.
 // fp32: a plain wave-per-row dot-product kernel (fp32 models).
 #include "common.h"
 #include "kernels.h"
@@ -46,198 +46,230 @@ __device__ __forceinline__ void stats_fold(EntStats& st, float mx, const float* 
   st.t = t_new;
 }
 
-// Wave triples -> block triple per column -> parts[block][col]. `red` is LDS
-// scratch of kEntWaves * 16 * NCB triples that no DMA is still writing.
-template <int NCB>
-__device__ __forceinline__ void write_block_stats(EntStats (&st)[NCB], int Bl, float* parts, EntStats* red) {
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+// Folds one MFMA output fragment into a lane's running triple: the lane holds
+// z[row0 + i], i = 0..3, of its column; rows at or past V are left out.
+__device__ __forceinline__ void fold4(EntStats& st, const floatx4& z, int row0, int V) {
+  float mx = -INFINITY;
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) {
-    EntStats v = st[cb];
+  for (int i = 0; i < 4; ++i)
+    if (row0 + i < V) mx = fmaxf(mx, z[i]);
+  if (mx == -INFINITY) return;
+  const float mn = fmaxf(st.m, mx);
+  float s_new = 0.f, t_new = 0.f;
+  if (st.m != -INFINITY) {
+    const float dm = st.m - mn, sc = __expf(dm);
+    s_new = st.s * sc;
+    t_new = (st.t + st.s * dm) * sc;
+  }
 #pragma unroll
-    for (int off = 16; off < 64; off <<= 1) {
-      EntStats o{__shfl_xor(v.m, off, 64), __shfl_xor(v.s, off, 64), __shfl_xor(v.t, off, 64)};
-      v = ent_merge(v, o);
+  for (int i = 0; i < 4; ++i)
+    if (row0 + i < V) {
+      const float dz = z[i] - mn, e = __expf(dz);
+      s_new += e;
+      t_new = fmaf(e, dz, t_new);
     }
-    if (lane < 16) red[wid * 16 * NCB + 16 * cb + lane] = v;
-  }
-  __syncthreads();
-  const int col = threadIdx.x;
-  if (col < 16 * NCB && col < Bl) {
-    EntStats v = red[col];
-    for (int w = 1; w < kEntWaves; ++w) v = ent_merge(v, red[w * 16 * NCB + col]);
-    float* p = parts + ((size_t)blockIdx.x * 64 + col) * 3;
-    p[0] = v.m;
-    p[1] = v.s;
-    p[2] = v.t;
-  }
+  st = EntStats{mn, s_new, t_new};
 }
 
 // lm_head stream through an R-deep LDS ring fed by direct DMA.
 //
-// A workgroup (4 waves) owns vocabulary tiles of 128 rows; the tiles of one
-// workgroup are blockIdx.x, blockIdx.x + gridDim.x, ... and its K steps of 64
-// run back to back across tiles, so the ring never drains between tiles. One
-// ring slot holds the W tile's 64-wide K slice (128 rows x 128 B) and the same
-// slice of the normalised hidden columns (NCB blocks of 16 columns, hi and lo
-// planes, 128 B per column). Every DMA instruction moves 8 rows x 128 B, eight
-// lanes per 128-byte line, so HBM reads are whole lines. Within a row the
-// 16-byte chunk c is stored at position c ^ (row & 7); the swizzle is applied
-// to the global address each lane fetches (the DMA writes lane L at 16 L), so
-// the MFMA fragment reads of 16 consecutive rows spread over the banks.
-// Wave w computes rows 32w .. 32w+31 of the tile (two 16-row MFMA tiles):
-// per K step two k-substeps of 32, each tile times the hi and the lo plane.
+// The unit of the ring is 16 rows x 1 KB: a 512-wide K slice of 16 vocabulary
+// rows of W, or of 16 hidden columns of one plane (hi or lo). Each DMA
+// instruction moves one 1 KB row segment, so HBM sees 1 KB contiguous runs:
+// runs of 128-512 B per row cost up to a fifth of the bandwidth on MI355X.
+// Within a row the 16-byte chunk c sits at position c ^ (row & 15) (the lanes
+// fetch permuted chunks of the same segment), so a 16-row fragment read hits
+// 16 distinct bank groups.
+//
+// A workgroup (8 waves) owns a contiguous range of 16-row vocabulary tiles
+// (the ranges of the grid differ by at most one tile) and walks it in groups
+// of G tiles. Wave w serves column block w % NCB, K half (w / NCB) % 2 of the
+// slice and owner group w / (2 NCB). For each 512-wide K slice of a group, the
+// 2*NCB hidden units come first: every wave copies its column block's K half
+// into registers (8 k-substeps x hi/lo). The group's G weight units follow;
+// unit i is contracted by the 2*NCB waves of owner group i mod (4 / NCB), each
+// over its K half (16 MFMAs), so a unit's work is spread over two SIMDs and
+// the barrier of the next unit waits for at most that. After the group the two
+// K halves of each tile are summed through LDS (one barrier per group) and
+// the first-half wave folds the logits into its running statistics.
+//
 // Chunks at or past d are fetched from the row start (valid memory) and the
-// hidden fragment is zeroed on read; rows past V are clamped and left out of
-// the statistics; hidden columns past the live count read column 0 and their
-// statistics are never written.
+// hidden fragment is zeroed; rows past V are clamped and left out of the
+// statistics; hidden columns past the live count read stale (allocated) rows
+// and their statistics are never written.
 // The explicit vmcnt wait + barrier is what orders the DMA writes before the
 // fragment reads. The reads are typed bf16x8 loads: the compiler then treats
 // them as not aliasing the untyped DMA stores and adds no wait of its own
 // (with untyped reads it waits for every outstanding DMA, draining the ring).
-constexpr int kEntRows = 128;
+constexpr int kUnitBytes = 16 * 1024;
+constexpr int kEntRing = 7;
+constexpr int kEntWaves8 = 8;                         // waves per workgroup
+constexpr int kEntRedTiles = 4;                       // tiles per wave per reduction round
+constexpr int kRedBytes = kEntWaves8 * kEntRedTiles * 1024;
+constexpr int kFinBytes = kEntWaves8 * 16 * 12;       // one triple per column per wave
 
-__device__ __forceinline__ int ent_swz(int row, int chunk) { return chunk ^ (row & 7); }
-
-template <int NCB, int R>
-__global__ __launch_bounds__(256) void k_entropy_bf16(const bf16* __restrict__ W, const bf16* __restrict__ hi,
+template <int NCB, int G, int R>
+__global__ __launch_bounds__(512) void k_entropy_bf16(const bf16* __restrict__ W, const bf16* __restrict__ hi,
                                                       const bf16* __restrict__ lo, const Ctrl* c, int V, int d,
                                                       float* __restrict__ parts) {
-  constexpr int W_BYTES = kEntRows * 128;          // 16 KB
-  constexpr int H_BYTES = NCB * 2 * 16 * 128;      // NCB x (hi, lo) x 16 columns x 128 B
-  constexpr int SLOT = W_BYTES + H_BYTES;
-  constexpr int W_INS = W_BYTES / 1024 / 4;        // DMA instructions per wave per step
-  constexpr int H_INS = H_BYTES / 1024 / 4;
-  constexpr int NDMA = W_INS + H_INS;
-  static_assert(H_BYTES % 4096 == 0, "hidden slice must split evenly over 4 waves");
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[R * SLOT];
+  constexpr int NW = kEntWaves8;
+  constexpr int IPW = 16 / NW;        // DMA instructions per wave per unit
+  constexpr int TPW = NW / (2 * NCB); // owner groups; unit i goes to group i % TPW
+  constexpr int LT = G / TPW;         // tiles per wave per group
+  constexpr int HU = 2 * NCB;         // hidden units per slice
+  static_assert(G % TPW == 0 && LT % kEntRedTiles == 0, "tile group must split over the waves and rounds");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[R * kUnitBytes + kRedBytes + kFinBytes];
 
   const int Bl = c->live_count;
   if (Bl == 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const int ntiles = (V + kEntRows - 1) / kEntRows;
-  const int nk = (d + 63) / 64;
-  const int my_tiles = blockIdx.x < ntiles ? (ntiles - 1 - blockIdx.x) / gridDim.x + 1 : 0;
-  const int total = my_tiles * nk;
+  const int cbw = wid % NCB, kh = (wid / NCB) & 1, own = wid / (2 * NCB);
+  const int T = (V + 15) / 16;
+  const int t0 = (int)((long long)blockIdx.x * T / gridDim.x);
+  const int t1 = (int)((long long)(blockIdx.x + 1) * T / gridDim.x);
+  const int ntile = t1 - t0;
+  const int ns = (d + 511) / 512;
+  const int ng = (ntile + G - 1) / G;
 
-  // DMA lane roles: lane L fills row/column (L >> 3) of its instruction's 8,
-  // physical chunk L & 7, i.e. logical chunk (L & 7) ^ (L >> 3).
-  const int sub = lane >> 3;
-  const int lchunk = (lane & 7) ^ sub;
-  const bf16* hsrc[H_INS];
-  int hdst[H_INS];
+  // Issue cursor (group, slice, unit) of the next ring unit; past the end the
+  // first unit is fetched again (never consumed) so every step has the same
+  // number of DMAs in flight.
+  int cg = 0, cs = 0, cu = 0;
+  auto issue = [&](int slot_idx) {
+    uint8_t* slot = smem + slot_idx * kUnitBytes;
+    const bool past = cg >= ng;
+    const int g_ = past ? 0 : cg, s_ = past ? 0 : cs, u_ = past ? 0 : cu;
 #pragma unroll
-  for (int j = 0; j < H_INS; ++j) {
-    const int ins = wid * H_INS + j;           // 0 .. NCB*4-1: (cb, plane, 8-column group)
-    const int cb = ins >> 2, plane = (ins >> 1) & 1, grp = ins & 1;
-    const int col = 16 * cb + 8 * grp + sub;
-    hsrc[j] = (plane ? lo : hi) + (size_t)(col < Bl ? col : 0) * d;
-    hdst[j] = W_BYTES + ins * 1024;
-  }
-  auto issue = [&](int q) {
-    uint8_t* slot = smem + (q % R) * SLOT;
-    // Steps past the end re-read the block's first step (valid memory, never
-    // used), which keeps every iteration's wait count the same.
-    if (q >= total) q = 0;
-    const int t = q / nk, ks = q - t * nk;
-    const int v0 = (blockIdx.x + t * gridDim.x) * kEntRows;
-    const int k = 64 * ks + 8 * lchunk;
-    const int kk = k < d ? k : 0;
-#pragma unroll
-    for (int j = 0; j < W_INS; ++j) {
-      const int ins = wid * W_INS + j;          // rows 8*ins .. 8*ins+7 of the tile
-      const int row = min(v0 + 8 * ins + sub, V - 1);
-      dma16(W + (size_t)row * d + kk, slot + ins * 1024);
+    for (int j = 0; j < IPW; ++j) {
+      const int r = IPW * wid + j;                // unit row filled by this instruction
+      const int k = 512 * s_ + 8 * (lane ^ r);    // logical chunk lane ^ r of the segment
+      const int kk = k < d ? k : 0;
+      const bf16* src;
+      if (u_ < HU) {
+        const int col = 16 * (u_ >> 1) + r;
+        src = ((u_ & 1) ? lo : hi) + (size_t)col * d + kk;   // rows past Bl: stale, never used
+      } else {
+        const int row = min(16 * (t0 + g_ * G + (u_ - HU)) + r, V - 1);
+        src = W + (size_t)row * d + kk;
+      }
+      dma16(src, slot + r * 1024);
     }
-#pragma unroll
-    for (int j = 0; j < H_INS; ++j) dma16(hsrc[j] + kk, slot + hdst[j]);
+    if (!past) {
+      const int gt = min(G, ntile - cg * G);
+      if (++cu == HU + gt) {
+        cu = 0;
+        if (++cs == ns) {
+          cs = 0;
+          ++cg;
+        }
+      }
+    }
   };
+  int qc = 0;   // ring units consumed
+  auto step = [&]() -> const uint8_t* {
+    // This thread's DMAs for unit qc have landed and its reads of unit qc-1
+    // are complete; after the barrier every wave's are.
+    wait_vmcnt_lds<IPW * (R - 2)>();
+    __builtin_amdgcn_s_barrier();
+    issue((qc + R - 1) % R);          // refills the slot unit qc-1 used
+    const uint8_t* slot = smem + (qc % R) * kUnitBytes;
+    ++qc;
+    return slot;
+  };
+#pragma unroll
+  for (int i = 0; i < R - 1; ++i) issue(i);
 
-  EntStats st[NCB];
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) st[cb] = ent_empty();
-  floatx4 acc[2][NCB];
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) acc[t][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
   const bf16x8 zero = {};
-
+  EntStats st = ent_empty();
+  bf16x8 hreg[2][8];
+  floatx4 acc[LT];
+  for (int gi = 0; gi < ng; ++gi) {
+    const int gt = min(G, ntile - gi * G);
 #pragma unroll
-  for (int q = 0; q < R - 1; ++q) issue(q);
-
-  for (int q = 0; q < total; ++q) {
-    wait_vmcnt<NDMA * (R - 2)>();     // this thread's DMAs for step q have landed
-    __builtin_amdgcn_s_barrier();     // every wave's DMAs for q landed; step q-1 fully consumed
-    issue(q + R - 1);   // refills the slot step q-1 used
-    const uint8_t* slot = smem + (q % R) * SLOT;
-    const int t_loc = q / nk, ks = q - t_loc * nk;
+    for (int m = 0; m < LT; ++m) acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < ns; ++s) {
 #pragma unroll
-    for (int kh = 0; kh < 2; ++kh) {
-      const int chunk = 4 * kh + g;
-      const bool kin = 64 * ks + 8 * chunk < d;
-      bf16x8 a[2];
+      for (int u = 0; u < HU; ++u) {
+        const uint8_t* slot = step();
+        if ((u >> 1) == cbw) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int row = 32 * wid + 16 * t + r16;
-        a[t] = *reinterpret_cast<const bf16x8*>(slot + row * 128 + ent_swz(row, chunk) * 16);
+          for (int j = 0; j < 8; ++j) {
+            const int lc = 4 * (8 * kh + j) + g;
+            const bf16x8 v = *reinterpret_cast<const bf16x8*>(slot + r16 * 1024 + (lc ^ r16) * 16);
+            hreg[u & 1][j] = 512 * s + 8 * lc < d ? v : zero;
+          }
+        }
       }
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) {
-        // Column r16 of block cb, plane p: instruction (cb, p, r16 >> 3), row r16 & 7.
-        const int hoff = cb * 4096 + (r16 >> 3) * 1024 + (r16 & 7) * 128 + ent_swz(r16, chunk) * 16;
-        const bf16x8 xh = *reinterpret_cast<const bf16x8*>(slot + W_BYTES + hoff);
-        const bf16x8 xl = *reinterpret_cast<const bf16x8*>(slot + W_BYTES + hoff + 2048);
-        const bf16x8 bh = kin ? xh : zero;
-        const bf16x8 bl = kin ? xl : zero;
+      for (int ii = 0; ii < G; ++ii) {
+        if (ii < gt) {
+          const uint8_t* slot = step();
+          if (ii % TPW == own) {
+            floatx4& ac = acc[ii / TPW];
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          acc[t][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[t], bh, acc[t][cb], 0, 0, 0);
-          acc[t][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[t], bl, acc[t][cb], 0, 0, 0);
+            for (int j = 0; j < 8; ++j) {
+              const int lc = 4 * (8 * kh + j) + g;
+              const bf16x8 a = *reinterpret_cast<const bf16x8*>(slot + r16 * 1024 + (lc ^ r16) * 16);
+              ac = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, hreg[0][j], ac, 0, 0, 0);
+              ac = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, hreg[1][j], ac, 0, 0, 0);
+            }
+          }
         }
       }
     }
-    if (ks == nk - 1) {
-      // Tile done: lane (r16, g) holds z[v0 + 32 wid + 16 t + 4 g + i] of column 16 cb + r16.
-      const int vb = (blockIdx.x + t_loc * gridDim.x) * kEntRows + 32 * wid + 4 * g;
+    // Lane (r16, g) holds, over its K half, z[16 tile + 4 g + i] of column
+    // 16 cbw + r16 for the wave's tiles ii = m * TPW + own. The second-half
+    // wave hands its partials to its partner (wave - NCB) through LDS, four
+    // tiles per round; after the last round the area is rewritten only at the
+    // end of the next group, many barriers on.
+    floatx4* red = reinterpret_cast<floatx4*>(smem + R * kUnitBytes);
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) {
-        float mx = -INFINITY;
+    for (int rr = 0; rr < LT / kEntRedTiles; ++rr) {
+      if (rr > 0) __builtin_amdgcn_s_barrier();   // the previous round is read
+      if (kh == 1) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int m = 0; m < kEntRedTiles; ++m)
+          red[((wid - NCB) * kEntRedTiles + m) * 64 + lane] = acc[rr * kEntRedTiles + m];
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the partials are in LDS
+      __builtin_amdgcn_s_barrier();
+      if (kh == 0) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (vb + 16 * t + i < V) mx = fmaxf(mx, acc[t][cb][i]);
-        if (mx != -INFINITY) {
-          const float mn = fmaxf(st[cb].m, mx);
-          float s_new = 0.f, t_new = 0.f;
-          if (st[cb].m != -INFINITY) {
-            const float dm = st[cb].m - mn, sc = __expf(dm);
-            s_new = st[cb].s * sc;
-            t_new = (st[cb].t + st[cb].s * dm) * sc;
+        for (int m = 0; m < kEntRedTiles; ++m) {
+          const int ii = (rr * kEntRedTiles + m) * TPW + own;
+          if (ii < gt) {
+            const floatx4 z = acc[rr * kEntRedTiles + m] + red[(wid * kEntRedTiles + m) * 64 + lane];
+            fold4(st, z, 16 * (t0 + gi * G + ii) + 4 * g, V);
           }
-#pragma unroll
-          for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              if (vb + 16 * t + i < V) {
-                const float dz = acc[t][cb][i] - mn, e = __expf(dz);
-                s_new += e;
-                t_new = fmaf(e, dz, t_new);
-              }
-          st[cb] = EntStats{mn, s_new, t_new};
         }
-#pragma unroll
-        for (int t = 0; t < 2; ++t) acc[t][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
     }
   }
-  // Drain the look-ahead DMAs and let every wave finish its reads, then reuse
-  // the ring for the cross-wave reduction.
-  wait_vmcnt<0>();
+  wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
+
+  // Column triples: merge the four lane groups, then the waves of each column
+  // block in a fixed order (second-half waves hold empty triples).
+#pragma unroll
+  for (int off = 16; off < 64; off <<= 1) {
+    EntStats o{__shfl_xor(st.m, off, 64), __shfl_xor(st.s, off, 64), __shfl_xor(st.t, off, 64)};
+    st = ent_merge(st, o);
+  }
+  EntStats* fin = reinterpret_cast<EntStats*>(smem + R * kUnitBytes + kRedBytes);
+  if (lane < 16) fin[wid * 16 + lane] = st;
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the triples are in LDS
   __builtin_amdgcn_s_barrier();
-  write_block_stats<NCB>(st, Bl, parts, reinterpret_cast<EntStats*>(smem));
+  const int col = tid;
+  if (col < 16 * NCB && col < Bl) {
+    const int cb = col >> 4;
+    EntStats v = fin[cb * 16 + (col & 15)];
+#pragma unroll
+    for (int p = 1; p < NW / NCB; ++p) v = ent_merge(v, fin[(p * NCB + cb) * 16 + (col & 15)]);
+    float* pp = parts + ((size_t)blockIdx.x * 64 + col) * 3;
+    pp[0] = v.m;
+    pp[1] = v.s;
+    pp[2] = v.t;
+  }
 }
 
 // fp32 models: each wave takes whole vocabulary rows, lanes stride over d.
@@ -275,11 +307,10 @@ __global__ __launch_bounds__(256) void k_entropy_f32(const float* __restrict__ W
   }
 }
 
-// Persistent grid: as many workgroups as are resident at once on MI355X's 256
-// compute units (LDS per workgroup: 60 KB for <= 16 columns, 72 KB for <= 32,
-// 96 KB for <= 64).
+// Persistent grid: one 8-wave workgroup (146 KB of LDS: a 7-unit ring keeps
+// 96 KB of the stream in flight) per compute unit on MI355X's 256 compute
+// units.
 constexpr int kComputeUnits = 256;
-constexpr int kEntRing = 3;
 
 int ent_ncb(int max_branches) { return max_branches <= 16 ? 1 : max_branches <= 32 ? 2 : 4; }
 
@@ -290,8 +321,8 @@ int entropy_parts(DType dt, int V, int max_branches) {
     const int b = (V + kEntWaves - 1) / kEntWaves;
     return b < 256 ? b : 256;
   }
-  const int tiles = (V + kEntRows - 1) / kEntRows;
-  const int grid = (ent_ncb(max_branches) <= 2 ? 2 : 1) * kComputeUnits;
+  const int tiles = (V + 15) / 16;
+  const int grid = kComputeUnits;
   return tiles < grid ? tiles : grid;
 }
 
@@ -308,13 +339,13 @@ hipError_t launch_entropy(DType dt, const void* W, const void* hn_a, const void*
   const bf16* b = static_cast<const bf16*>(hn_b);
   switch (ent_ncb(max_branches)) {
     case 1:
-      hipLaunchKernelGGL((k_entropy_bf16<1, kEntRing>), dim3(blocks), dim3(256), 0, st, w, a, b, c, V, d, parts);
+      hipLaunchKernelGGL((k_entropy_bf16<1, 32, kEntRing>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d, parts);
       break;
     case 2:
-      hipLaunchKernelGGL((k_entropy_bf16<2, kEntRing>), dim3(blocks), dim3(256), 0, st, w, a, b, c, V, d, parts);
+      hipLaunchKernelGGL((k_entropy_bf16<2, 32, kEntRing>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d, parts);
       break;
     default:
-      hipLaunchKernelGGL((k_entropy_bf16<4, kEntRing>), dim3(blocks), dim3(256), 0, st, w, a, b, c, V, d, parts);
+      hipLaunchKernelGGL((k_entropy_bf16<4, 16, kEntRing>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d, parts);
       break;
   }
   return hipGetLastError();
