@@ -95,6 +95,131 @@ def kernel_work(shape, B_live, n, s):
 
 EVENT_SLOTS = {"qkv_proj": 0, "attention": 2, "o_proj": 4, "gate_up_proj": 6, "down_proj": 8, "lm_head_entropy": 10}
 
+# Device code each timed kernel class is built from (hashed to tell whether a
+# stored counter measurement still describes the current kernel).
+KERNEL_SOURCES = {
+    "lm_head_entropy": ["k_entropy.hip", "common.h"],
+    "qkv_proj": ["k_gemm.hip", "common.h"], "o_proj": ["k_gemm.hip", "common.h"],
+    "gate_up_proj": ["k_gemm.hip", "common.h"], "down_proj": ["k_gemm.hip", "common.h"],
+    "attention": ["k_attn.hip", "common.h"],
+}
+# Name fragments of the device kernels behind each class in rocprofv3 output.
+KERNEL_NAMES = {"lm_head_entropy": "k_entropy_bf16", "attention": "k_attn_bf16", "qkv_proj": "k_gemm_dma",
+                "o_proj": "k_gemm_dma", "gate_up_proj": "k_gemm_dma", "down_proj": "k_gemm_dma"}
+COPY_BYTES = 1 << 29   # calibration copy: 512 MiB read + 512 MiB written
+
+
+def source_digest(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    for fn in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2606_09937_amd", "csrc", fn), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_record_path(kernel, workload):
+    return os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+
+
+def stored_traffic(kernel, workload):
+    """HBM bytes per launch from the committed counter runs, or None if absent or stale."""
+    path = traffic_record_path(kernel, workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha256") != source_digest(kernel):
+        return None
+    return rec["hbm_bytes_per_launch"]
+
+
+def _read_counter_csv(directory):
+    """(kernel name, counter name, value) rows of every *counter_collection.csv under directory."""
+    import csv
+    rows = []
+    for dp, _, files in os.walk(directory):
+        for fn in files:
+            if fn.endswith("counter_collection.csv"):
+                with open(os.path.join(dp, fn)) as f:
+                    for r in csv.DictReader(f):
+                        rows.append((r["Kernel_Name"], r["Counter_Name"], float(r["Counter_Value"]), r["Dispatch_Id"]))
+    return rows
+
+
+def _per_dispatch(rows, name_part, counter):
+    """Counter value per dispatch (summed over its per-agent/per-instance records)."""
+    per = {}
+    for kname, cname, val, disp in rows:
+        if name_part in kname and cname == counter:
+            per[disp] = per.get(disp, 0.0) + val
+    return list(per.values())
+
+
+def summarize_pmc(args):
+    """Writes the traffic record and prints a text summary from four rocprofv3 --pmc runs."""
+    import statistics
+    fetch, write = _read_counter_csv(args.pmc_fetch), _read_counter_csv(args.pmc_write)
+    cfetch, cwrite = _read_counter_csv(args.pmc_copy_fetch), _read_counter_csv(args.pmc_copy_write)
+    kname = KERNEL_NAMES[args.kernel]
+    k_f = _per_dispatch(fetch, kname, "FETCH_SIZE")
+    k_w = _per_dispatch(write, kname, "WRITE_SIZE")
+    c_f = _per_dispatch(cfetch, "neg_kernel", "FETCH_SIZE")
+    c_w = _per_dispatch(cwrite, "neg_kernel", "WRITE_SIZE")
+    if not (k_f and k_w and c_f and c_w):
+        raise SystemExit(f"missing dispatches: kernel fetch {len(k_f)} write {len(k_w)}, "
+                         f"copy fetch {len(c_f)} write {len(c_w)}")
+    # bytes per counter unit, from the copy of known size (counters read KiB nominally)
+    sf = COPY_BYTES / statistics.median(c_f)
+    sw = COPY_BYTES / statistics.median(c_w)
+    fb = statistics.median(k_f) * sf
+    wb = statistics.median(k_w) * sw
+    rec = {
+        "kernel": args.kernel, "workload": args.workload, "device_kernel": kname,
+        "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb, "hbm_bytes_per_launch": fb + wb,
+        "fetch_scale_bytes_per_unit": sf, "write_scale_bytes_per_unit": sw,
+        "dispatches": {"kernel_fetch": len(k_f), "kernel_write": len(k_w), "copy_fetch": len(c_f),
+                       "copy_write": len(c_w)},
+        "source_sha256": source_digest(args.kernel),
+    }
+    with open(traffic_record_path(args.kernel, args.workload), "w") as f:
+        json.dump(rec, f, indent=1)
+    print(f"{args.kernel} ({kname}) at {args.workload}: FETCH_SIZE median {statistics.median(k_f):.0f} over "
+          f"{len(k_f)} dispatches, WRITE_SIZE median {statistics.median(k_w):.0f} over {len(k_w)}")
+    print(f"copy calibration ({COPY_BYTES} B read + written): FETCH_SIZE {statistics.median(c_f):.0f}, "
+          f"WRITE_SIZE {statistics.median(c_w):.0f} -> {sf:.1f} / {sw:.1f} bytes per counter unit")
+    print(f"HBM traffic per launch: read {fb / 1e6:.1f} MB + write {wb / 1e6:.3f} MB = {(fb + wb) / 1e6:.1f} MB")
+
+
+def summarize_stats(args):
+    """Prints the per-kernel table of a rocprofv3 --stats run (kernel_stats.csv)."""
+    import csv
+    path = None
+    for dp, _, files in os.walk(args.stats):
+        for fn in files:
+            if fn.endswith("kernel_stats.csv"):
+                path = os.path.join(dp, fn)
+    if path is None:
+        raise SystemExit(f"no kernel_stats.csv under {args.stats}")
+    with open(path) as f:
+        rows = list(csv.DictReader(f))
+    print(f"{'calls':>6} {'avg us':>9} {'min us':>9} {'max us':>9} {'total %':>8}  kernel")
+    for r in rows:
+        print(f"{int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:9.2f} {float(r['MinNs']) / 1e3:9.2f} "
+              f"{float(r['MaxNs']) / 1e3:9.2f} {float(r['Percentage']):8.2f}  {r['Name'][:110]}")
+
+
+def copy_calibration():
+    """One plain copy kernel (dst = -src, fp32) of COPY_BYTES, three times, for counter scaling."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": COPY_BYTES, "copy_bytes_written": COPY_BYTES, "launches": 3}))
+
 
 def cpu_baseline(mw, kv, toks, wl, layers):
     """Float64 oracle on the first `layers` layers of the same workload; time scaled to all layers."""
@@ -142,13 +267,31 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=4, help="layers in the oracle's bounded sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-depth", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run the plain copy kernel used to scale HBM counters")
+    ap.add_argument("--summarize-stats", dest="stats", metavar="DIR",
+                    help="print the kernel table of a rocprofv3 --stats output directory and exit")
+    ap.add_argument("--summarize-pmc", action="store_true",
+                    help="write profiles/<kernel>_<workload>_traffic.json from four --pmc output directories")
+    ap.add_argument("--kernel", default="lm_head_entropy")
+    ap.add_argument("--pmc-fetch")
+    ap.add_argument("--pmc-write")
+    ap.add_argument("--pmc-copy-fetch")
+    ap.add_argument("--pmc-copy-write")
     args = ap.parse_args()
+    if args.stats:
+        return summarize_stats(args)
+    if args.summarize_pmc:
+        return summarize_pmc(args)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the verify pass runs on a single MI355X (no multi-GPU path); "
               "run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        return copy_calibration()
 
     import torch
 
@@ -260,7 +403,7 @@ def main():
         "achieved": dk["tflops"] if gemm_like else dk["hbm_gbs"],
         "peak": BF16_PEAK_TFLOPS if gemm_like else HBM_PEAK_GBS,
         "unit": "TFLOP/s" if gemm_like else "GB/s",
-        "traffic": None,
+        "traffic": stored_traffic(dom, wl.name),
         "avg_launch_us": dk["avg_us"],
         "algorithmic_bytes_per_launch": work[dom]["bytes"],
     }

@@ -3,9 +3,9 @@
  *
  * RKSC (arXiv 2606.09937) verifies B reasoning branches that share one prefix.
  * This library implements the verify pass of its layer-level early exit
- * (Sec. 3.3 "Layer-level entropy exit", Alg. VerifyWithEntropyExit) over a
+ * (Sec. 2.3 "Layer-level entropy exit", Alg. VerifyWithEntropyExit) over a
  * prefix KV cache that is computed once and read by every branch
- * (Sec. 3.2 "KV broadcast and batched decode"), and the layer-weighted cosine
+ * (Sec. 2.2 "KV broadcast and batched decode"), and the layer-weighted cosine
  * similarity of the ASKS gate (Eq. asks_sim, Alg. AsksGate).
  *
  * Conventions shared by every entry point:
@@ -106,11 +106,11 @@ size_t rksc_verify_workspace_size(const rksc_model_config* cfg, int32_t n_branch
  *
  * Every branch b's tokens branch_tokens[b, 0..s-1] sit at positions n..n+s-1;
  * each attends to the whole shared prefix and, causally, to its own earlier
- * tokens (Sec. 3.2). After every layer l (1-based) the last token's hidden row
+ * tokens (Sec. 2.2). After every layer l (1-based) the last token's hidden row
  * h goes through the final RMSNorm and the lm_head, and its softmax entropy in
  * nats H_l[b] is taken (Eq. entropy; the final norm is applied before the
  * projection so that layer L gives the model's real output distribution).
- * Exit rule (Sec. 3.3, condition (iii) with the entropy-stabilisation
+ * Exit rule (Sec. 2.3, condition (iii) with the entropy-stabilisation
  * tolerance tau and a patience): with H_0 = +inf, a layer counts toward the
  * streak when |H_l - H_{l-1}| < tau (strict) and resets it otherwise; branch b
  * exits at the first layer whose streak reaches `patience` and is not

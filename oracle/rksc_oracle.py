@@ -9,7 +9,7 @@ the only library primitive. Weights and KV arrive in their storage precision
 (fp32, or bf16 already widened exactly to fp32) and are widened to float64 on
 use. No blocking, fusion or reordering beyond what each definition states.
 
-Model (RKSC paper, Sec. 3 "Problem Setting"; the decoder itself is the standard
+Model (RKSC paper, Sec. 2.1 "Problem Setting"; the decoder itself is the standard
 pre-norm Llama-style block the paper runs through HF Transformers, Appendix
 "Implementation Details"):
   x_0 = E[token]
@@ -18,12 +18,12 @@ pre-norm Llama-style block the paper runs through HF Transformers, Appendix
              grouped-query attention (query head h reads KV head floor(h/G)),
              scale 1/sqrt(hd); x += o W_o^T;
              w = RMSNorm(x; g_ffn); x += (silu(w W_g^T) * (w W_u^T)) W_d^T.
-Verify pass (Sec. 3.2 "KV broadcast and batched decode", Eq. prefix_fwd):
+Verify pass (Sec. 2.2 "KV broadcast and batched decode", Eq. prefix_fwd):
   every branch's tokens sit at positions n..n+s-1 and attend to the one shared
   prefix cache plus their own earlier tokens.
 Layer entropy (Eq. entropy, Alg. VerifyWithEntropyExit): last token of the
   branch, final RMSNorm, lm_head, softmax entropy in nats.
-Exit rule (Sec. 3.3 "Layer-level entropy exit"), as (tau, patience): the layer
+Exit rule (Sec. 2.3 "Layer-level entropy exit"), as (tau, patience): the layer
   delta is |H_l - H_{l-1}| with H_0 = +inf; a streak counts consecutive layers
   with delta < tau (strict); the branch exits at the first layer whose streak
   reaches patience, else at L.

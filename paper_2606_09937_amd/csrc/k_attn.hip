@@ -2,7 +2,7 @@
 //
 // Query row (branch b, token i, head h) reads every key of the ONE shared prefix
 // cache of KV head floor(h/G) (positions 0..n-1) and, causally, its own branch's
-// keys 0..i (Sec. 3.2 "KV broadcast and batched decode": the cache is read by
+// keys 0..i (Sec. 2.2 "KV broadcast and batched decode": the cache is read by
 // all branches, never copied per branch). Softmax uses the scale 1/sqrt(hd).
 //
 // bf16 kernel: one workgroup per (live slot, KV head, 64 query rows); the rows

@@ -58,7 +58,7 @@ def test_entropy_matches_scipy_and_invariances():
     np.testing.assert_allclose(oracle.softmax_entropy(z[:, perm] + 9.0), H, rtol=0, atol=1e-10)
 
 
-# ----------------------------------------------------------------- exit rule (Sec. 3.3)
+# ----------------------------------------------------------------- exit rule (Sec. 2.3)
 
 def test_exit_tau_zero_never_exits():
     H = np.linspace(5.0, 5.0, 12)          # constant: every delta is 0, still not < 0
