@@ -326,7 +326,7 @@ RKSC_EXPORT rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void*
   const DType dt = dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
   GemmPlan p = rksc::plan_gemm(dt, M, N, K);
   if (splits > 0) {
-    const int kstep = dt == DType::BF16 ? 32 : 16;
+    const int kstep = dt == DType::BF16 ? 64 : 16;   // K elements per pipeline stage
     const int ktiles = (K + kstep - 1) / kstep;
     p.k_per_split = (ktiles + splits - 1) / splits * kstep;
     p.splits = (K + p.k_per_split - 1) / p.k_per_split;
