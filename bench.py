@@ -12,9 +12,13 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   value        verify tokens/s = n_branches * branch_len / step time
   roofline     the dominant kernel (fused lm_head-entropy at the default
                workload) against the HBM peak, timed with HIP events recorded
-               around its launches inside the timed steps
-  kernels      the same measurement for the projections and the attention
+               around its launches inside the timed steps (the only events in
+               that region: every recorded event opens a gap in the stream)
+  kernels      every kernel class timed the same way in a separate breakdown
+               pass before the timed region ("pass" says which)
+  exit_histogram, live_layer_fraction   exit layers of the timed calls
   full_depth   the same workload with tau = 0 (no exit)
+  tau_sweep    exit layers and call time at tau in {0.02, 0.05, 0.1, 0.2}
   cpu_baseline the float64 CPU oracle on a bounded sample of the workload
 
     python bench.py [--steps K] [--warmup W] [--workload 7b_single]
@@ -44,17 +48,26 @@ def log(msg):
 class HipEvents:
     """hipEvent_t handles through the HIP runtime (events recorded by librksc on the call's stream)."""
 
+    # Timing-only events: no system-scope fence on record. A fenced record writes
+    # back and invalidates the caches, which opens a ~5 us gap in the stream and
+    # leaves the next kernel cold.
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
     def __init__(self):
         self.lib = ctypes.CDLL("libamdhip64.so")
         self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
         self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
         self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
 
-    def create(self, n):
+    def create(self, n, fenced=True):
         evs = []
         for _ in range(n):
             e = ctypes.c_void_p()
-            rc = self.lib.hipEventCreate(ctypes.byref(e))
+            if fenced:
+                rc = self.lib.hipEventCreate(ctypes.byref(e))
+            else:
+                rc = self.lib.hipEventCreateWithFlags(ctypes.byref(e), self.DISABLE_SYSTEM_FENCE)
             if rc != 0:
                 raise RuntimeError(f"hipEventCreate failed ({rc})")
             evs.append(e.value)
@@ -267,6 +280,7 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=4, help="layers in the oracle's bounded sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-depth", action="store_true")
+    ap.add_argument("--no-tau-sweep", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the plain copy kernel used to scale HBM counters")
     ap.add_argument("--summarize-stats", dest="stats", metavar="DIR",
@@ -344,45 +358,69 @@ def main():
     log(f"warmup done ({args.warmup} steps)")
 
     hip = HipEvents()
+    hip.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
     per_step = 12 * L
-    ev = hip.create(per_step * args.steps)
-    ev_arrays = [(ctypes.c_void_p * per_step)(*ev[k * per_step:(k + 1) * per_step]) for k in range(args.steps)]
-    ev_ptrs = [ctypes.cast(a, ctypes.c_void_p) for a in ev_arrays]
+    tokens = B * s
+
+    def profiled_steps(k_steps, slots):
+        """Runs k_steps calls with timing events at the given per-layer slots;
+        returns durs[name] = per-(step, layer) milliseconds for each slot pair."""
+        evs = hip.create(per_step * k_steps, fenced=False)
+        arrays = []
+        for k in range(k_steps):
+            arr = (ctypes.c_void_p * per_step)()
+            for l in range(L):
+                for sl in slots:
+                    arr[12 * l + sl] = evs[k * per_step + 12 * l + sl]
+            arrays.append(arr)
+        ptrs = [ctypes.cast(a, ctypes.c_void_p) for a in arrays]
+        return evs, ptrs
+
+    def durations(evs, k_steps, slot, layers):
+        return [hip.elapsed_ms(evs[k * per_step + 12 * l + slot], evs[k * per_step + 12 * l + slot + 1])
+                for k in range(k_steps) for l in range(layers)]
+
+    # 1) Breakdown pass (untimed): events around every kernel class. Each recorded
+    #    event opens a few-microsecond gap in the stream, so these steps are not
+    #    the ones the headline is measured on.
+    kb_steps = max(2, min(args.steps, 5))
+    evs_b, ptrs_b = profiled_steps(kb_steps, sorted(set(v for s0 in EVENT_SLOTS.values() for v in (s0, s0 + 1))))
+    for k in range(kb_steps):
+        step(wl.tau, wl.patience, ptrs_b[k])
+    torch.cuda.synchronize()
+    exits = ex.cpu().tolist()
+    live_layers = max(exits)   # layers past every branch's exit run kernels that return at once
+    kernels = {}
+    for name, slot in EVENT_SLOTS.items():
+        d = durations(evs_b, kb_steps, slot, live_layers)
+        kernels[name] = {"avg_us": sum(d) / len(d) * 1e3, "launches_timed": len(d), "pass": "breakdown"}
+    hip.destroy(evs_b)
+    live_per_layer = [sum(1 for e in exits if e >= l + 1) for l in range(L)]
+    mean_live = sum(live_per_layer[:live_layers]) / live_layers
+    work = kernel_work(shape, max(1, round(mean_live)), n, s)
+    shares = {k: v["avg_us"] for k, v in kernels.items()}
+    dom = "lm_head_entropy" if shares["lm_head_entropy"] >= max(shares.values()) * 0.999 else max(shares, key=shares.get)
+
+    # 2) Timed region: K calls, events only around the dominant kernel class.
+    evs_t, ptrs_t = profiled_steps(args.steps, [EVENT_SLOTS[dom], EVENT_SLOTS[dom] + 1])
     start, stop = hip.create(2)
     torch.cuda.synchronize()
-    hip.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
     hip.lib.hipEventRecord(ctypes.c_void_p(start), sp)
     t_wall = time.perf_counter()
     for k in range(args.steps):
-        step(wl.tau, wl.patience, ev_ptrs[k])
+        step(wl.tau, wl.patience, ptrs_t[k])
     hip.lib.hipEventRecord(ctypes.c_void_p(stop), sp)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
     total_ms = hip.elapsed_ms(start, stop)
     ms_per_step = total_ms / args.steps
-    exits = ex.cpu().tolist()
-    tokens = B * s
     value = tokens / (ms_per_step / 1e3)
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall / args.steps * 1e3:.3f} ms), "
         f"{value:.1f} tokens/s, exit layers {exits}")
+    d = durations(evs_t, args.steps, EVENT_SLOTS[dom], live_layers)
+    kernels[dom].update({"avg_us": sum(d) / len(d) * 1e3, "launches_timed": len(d), "pass": "timed"})
+    hip.destroy(evs_t + [start, stop])
 
-    # Per-kernel durations inside the timed steps. Layers past every branch's exit
-    # run kernels that return at once; the roofline averages the layers still live.
-    live_layers = max(exits)
-    ent_cpu = ent.cpu()
-    kernels = {}
-    for name, slot in EVENT_SLOTS.items():
-        durs_live = []
-        for k in range(args.steps):
-            base = k * per_step
-            for l in range(live_layers):
-                durs_live.append(hip.elapsed_ms(ev[base + 12 * l + slot], ev[base + 12 * l + slot + 1]))
-        avg_ms = sum(durs_live) / len(durs_live)
-        kernels[name] = {"avg_us": avg_ms * 1e3, "launches_timed": len(durs_live)}
-    # live branches per layer (all branches are live up to the first exit)
-    live_per_layer = [sum(1 for e in exits if e >= l + 1) for l in range(L)]
-    mean_live = sum(live_per_layer[:live_layers]) / live_layers
-    work = kernel_work(shape, max(1, round(mean_live)), n, s)
     for name, rec in kernels.items():
         wk = work[name]
         sec = rec["avg_us"] * 1e-6
@@ -393,8 +431,6 @@ def main():
         rec["mfma_frac"] = rec["tflops"] / peak
         rec["algorithmic_bytes"] = wk["bytes"]
         rec["algorithmic_flops"] = wk["flops"]
-    shares = {k: v["avg_us"] * live_layers for k, v in kernels.items()}
-    dom = "lm_head_entropy" if shares["lm_head_entropy"] >= max(shares.values()) * 0.999 else max(shares, key=shares.get)
     dk = kernels[dom]
     gemm_like = dom.endswith("_proj") and work[dom]["flops"] / work[dom]["bytes"] > 315
     roofline = {
@@ -408,7 +444,8 @@ def main():
         "algorithmic_bytes_per_launch": work[dom]["bytes"],
     }
     roofline["frac"] = roofline["achieved"] / roofline["peak"]
-    hip.destroy(ev + [start, stop])
+    exit_hist = {str(l): exits.count(l) for l in sorted(set(exits))}
+    live_fraction = sum(min(e, L) for e in exits) / (L * B)
 
     full_depth = None
     if not args.no_full_depth:
@@ -425,6 +462,27 @@ def main():
         hip.destroy([a, b])
         full_depth = {"tau": 0.0, "ms_per_step": fd_ms, "value": tokens / (fd_ms / 1e3), "unit": "tokens/s"}
         log(f"full depth (tau=0): {fd_ms:.3f} ms/step, {full_depth['value']:.1f} tokens/s")
+
+    # Functional sweep of the exit threshold (same inputs): random-init weights
+    # rarely stabilise within tau = 0.02, so larger taus show the exit path at work.
+    tau_sweep = None
+    if not args.no_tau_sweep:
+        tau_sweep = []
+        for tau in (0.02, 0.05, 0.1, 0.2):
+            step(tau, wl.patience)
+            torch.cuda.synchronize()
+            a, b = hip.create(2)
+            hip.lib.hipEventRecord(ctypes.c_void_p(a), sp)
+            for _ in range(3):
+                step(tau, wl.patience)
+            hip.lib.hipEventRecord(ctypes.c_void_p(b), sp)
+            torch.cuda.synchronize()
+            t_ms = hip.elapsed_ms(a, b) / 3
+            hip.destroy([a, b])
+            ex_t = ex.cpu().tolist()
+            tau_sweep.append({"tau": tau, "patience": wl.patience, "exit_layers": ex_t, "ms_per_step": t_ms,
+                              "value": tokens / (t_ms / 1e3)})
+            log(f"tau {tau}: exit layers {ex_t}, {t_ms:.3f} ms/step")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -454,8 +512,11 @@ def main():
             "exit_layers": exits, "parallelism": "single GPU",
         },
         "roofline": roofline,
+        "exit_histogram": exit_hist,
+        "live_layer_fraction": live_fraction,
         "kernels": kernels,
         "full_depth": full_depth,
+        "tau_sweep": tau_sweep,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
