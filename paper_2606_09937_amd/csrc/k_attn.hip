@@ -23,15 +23,28 @@ namespace rksc {
 
 namespace {
 
+// a if c, else zero; component-wise so that no address is selected (a select
+// of struct lvalues keeps register arrays in scratch memory).
+__device__ __forceinline__ uint4 keep_if(bool c, const uint4& a) {
+  return make_uint4(c ? a.x : 0u, c ? a.y : 0u, c ? a.z : 0u, c ? a.w : 0u);
+}
+
 // V^T tile layout: row = head dimension, column = key. The 4-key group of a
 // row is XOR-swizzled by the row's 8-dimension block so that the packed stores
 // (4 keys of one dimension) and the fragment reads are bank-conflict free.
 __device__ __forceinline__ int vt_col(int dim, int key) { return key ^ (((dim >> 3) & 15) << 2); }
 
-// Split-KV work unit: chunk `chunk` of `nchunks` covers prefix tiles
-// [t0, t1); with nchunks > 1 the last chunk covers the own-span tiles only.
+// Split-KV: the key tiles of a query tile -- the prefix tiles, then the own-span
+// tiles up to its last query -- are divided evenly over `nchunks` workgroups,
+// each writing an unnormalised partial output with its (max, sum) for
+// k_attn_combine. (A merge by the last chunk to finish, found with an atomic
+// ticket, needs device-scope release fences; on MI355X those write back the
+// whole L2 and cost far more than the separate combine launch.)
+// Tile loads are software-pipelined: the next tile's K/V (own-span tiles: K)
+// are fetched into registers while the current tile is contracted; the masking
+// and the hi/lo split happen when they are stored to LDS.
 template <int HD>
-__global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, const bf16* __restrict__ pk,
+__global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ q, const bf16* __restrict__ pk,
                                                    const bf16* __restrict__ pv, const float* __restrict__ ko,
                                                    const float* __restrict__ vo, void* __restrict__ o,
                                                    float* __restrict__ opart, float* __restrict__ mlpart,
@@ -42,6 +55,16 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
   constexpr int LDV = KT + 8;     // V^T row stride (elements)
   constexpr int NC = HD / 32;     // 32-dim chunks of the QK^T contraction
   constexpr int ND = HD / 16;     // 16-dim tiles of the output
+  // Register staging per thread: prefix tile (bf16) K in 16-byte row chunks and
+  // V in units of 4 keys x 8 dimensions; own-span tile (fp32) K in 16-byte
+  // chunks (4 dimensions); own-span V goes in units of 4 keys x 4 dimensions.
+  constexpr int PK = KT * HD / 8 / 256;                  // K chunks per thread, prefix
+  constexpr int PVU = (KT * HD / 32 + 255) / 256;        // V units per thread, prefix
+  constexpr int OK = KT * HD / 4 / 256;                  // K chunks per thread, own span
+  constexpr int OVU = (KT * HD / 16 + 255) / 256;        // V units per thread, own span
+  // Own-span V is loaded when the tile is stored (2 of the ~n/64 + 2 tiles), which
+  // keeps the staging at 8 registers x 16 B.
+  constexpr int NSTAGE = (PK + 4 * PVU) > OK ? (PK + 4 * PVU) : OK;
   static_assert(KT * HD / 8 % 256 == 0 && KT * HD / 4 % 256 == 0, "tile staging assumes 256 threads");
   // [0]: the prefix tile (exact bf16) or the hi part of an own-span tile; [1]: its lo part.
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * LDK];
@@ -61,18 +84,8 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
 
   const int i_max = min(s - 1, (min(row0 + 63, rows - 1)) / G);
   const int n_ptiles = (n + KT - 1) / KT;
-  const int n_otiles = i_max / KT + 1;
-  int t_begin, t_end;   // tile range, prefix tiles first, then own-span tiles
-  if (nchunks == 1) {
-    t_begin = 0;
-    t_end = n_ptiles + n_otiles;
-  } else if (chunk == nchunks - 1) {
-    t_begin = n_ptiles;
-    t_end = n_ptiles + n_otiles;
-  } else {
-    t_begin = chunk * n_ptiles / (nchunks - 1);
-    t_end = (chunk + 1) * n_ptiles / (nchunks - 1);
-  }
+  const int n_tiles = n_ptiles + i_max / KT + 1;
+  const int t_begin = chunk * n_tiles / nchunks, t_end = (chunk + 1) * n_tiles / nchunks;
 
   // The query this lane owns as an MFMA column. Rows past the end compute a
   // duplicate of the last row and are not stored.
@@ -105,79 +118,118 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
   const float* Ko = ko + ((size_t)slot * Hkv + kvh) * s * HD;
   const float* Vo = vo + ((size_t)slot * Hkv + kvh) * s * HD;
 
-  for (int t = t_begin; t < t_end; ++t) {
-    const bool own = t >= n_ptiles;
-    const int kbase = own ? (t - n_ptiles) * KT : t * KT;
-    if (!own) {
-      // Prefix tile (exact bf16). K: 16-byte row chunks. V: each thread takes 4
-      // consecutive keys of 8 dimensions and stores 4-key words per dimension.
+  // Fetch of tile t into registers (addresses clamped in bounds; out-of-range
+  // keys are zeroed when stored).
+  uint4 stg[NSTAGE];
+  auto fetch = [&](int t) {
+    if (t < n_ptiles) {
+      const int kbase = t * KT;
 #pragma unroll
-      for (int j = 0; j < KT * HD / 8 / 256; ++j) {
-        const int idx = tid + 256 * j, key = idx / (HD / 8), dc = idx % (HD / 8);
-        const int kk = kbase + key < n ? kbase + key : 0;
-        uint4 kv = ldg16(Kp + (size_t)kk * HD + dc * 8);
-        if (kbase + key >= n) kv = make_uint4(0, 0, 0, 0);
-        *reinterpret_cast<uint4*>(&Ks[0][key * LDK + dc * 8]) = kv;
+      for (int j = 0; j < PK; ++j) {
+        const int idx = tid + 256 * j, key = kbase + idx / (HD / 8), dc = idx % (HD / 8);
+        stg[j] = ldg16(Kp + (size_t)(key < n ? key : 0) * HD + dc * 8);
       }
-      // KT * HD / 32 units of 4 keys x 8 dimensions (128 for HD = 64: half the threads idle).
-      for (int idx = tid; idx < KT * HD / 32; idx += 256) {
-        const int dc = idx % (HD / 8), kg = idx / (HD / 8);
-        uint4 v4[4];
+#pragma unroll
+      for (int u = 0; u < PVU; ++u) {
+        const int idx = tid + 256 * u;
+        const int dc = idx % (HD / 8), kg = (idx < KT * HD / 32 ? idx : 0) / (HD / 8);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int key = kbase + 4 * kg + e;
-          v4[e] = ldg16(Vp + (size_t)(key < n ? key : 0) * HD + dc * 8);
-          if (key >= n) v4[e] = make_uint4(0, 0, 0, 0);
-        }
-        const uint16_t* ve0 = reinterpret_cast<const uint16_t*>(&v4[0]);
-        const uint16_t* ve1 = reinterpret_cast<const uint16_t*>(&v4[1]);
-        const uint16_t* ve2 = reinterpret_cast<const uint16_t*>(&v4[2]);
-        const uint16_t* ve3 = reinterpret_cast<const uint16_t*>(&v4[3]);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int dim = dc * 8 + e;
-          *reinterpret_cast<uint2*>(&Vt[0][dim * LDV + vt_col(dim, 4 * kg)]) =
-              make_uint2(pack2(ve0[e], ve1[e]), pack2(ve2[e], ve3[e]));
+          stg[PK + 4 * u + e] = ldg16(Vp + (size_t)(key < n ? key : 0) * HD + dc * 8);
         }
       }
     } else {
-      // Own-span tile: fp32 keys/values of the branch, split into hi/lo.
+      const int kbase = (t - n_ptiles) * KT;
 #pragma unroll
-      for (int j = 0; j < KT * HD / 4 / 256; ++j) {
+      for (int j = 0; j < OK; ++j) {
+        const int idx = tid + 256 * j, key = kbase + idx / (HD / 4), dq = idx % (HD / 4);
+        stg[j] = ldg16(Ko + (size_t)(key < s ? key : 0) * HD + dq * 4);
+      }
+    }
+  };
+  // Store of the fetched tile t to LDS: K rows and V^T, own-span tiles split into hi/lo.
+  auto store = [&](int t) {
+    if (t < n_ptiles) {
+      const int kbase = t * KT;
+#pragma unroll
+      for (int j = 0; j < PK; ++j) {
+        const int idx = tid + 256 * j, key = idx / (HD / 8), dc = idx % (HD / 8);
+        *reinterpret_cast<uint4*>(&Ks[0][key * LDK + dc * 8]) = keep_if(kbase + key < n, stg[j]);
+      }
+#pragma unroll
+      for (int u = 0; u < PVU; ++u) {
+        const int idx = tid + 256 * u;
+        if (idx < KT * HD / 32) {
+          const int dc = idx % (HD / 8), kg = idx / (HD / 8);
+          uint32_t w[4][4];   // w[e][j]: word j (elements 2j, 2j+1) of key 4kg + e
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint4 v = keep_if(kbase + 4 * kg + e < n, stg[PK + 4 * u + e]);
+            w[e][0] = v.x; w[e][1] = v.y; w[e][2] = v.z; w[e][3] = v.w;
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            // elements 2j (low halves) and 2j+1 (high halves) of the four keys
+            const uint32_t lo01 = (w[0][j] & 0xffffu) | (w[1][j] << 16);
+            const uint32_t lo23 = (w[2][j] & 0xffffu) | (w[3][j] << 16);
+            const uint32_t hi01 = (w[0][j] >> 16) | (w[1][j] & 0xffff0000u);
+            const uint32_t hi23 = (w[2][j] >> 16) | (w[3][j] & 0xffff0000u);
+            const int d0 = dc * 8 + 2 * j, d1 = d0 + 1;
+            *reinterpret_cast<uint2*>(&Vt[0][d0 * LDV + vt_col(d0, 4 * kg)]) = make_uint2(lo01, lo23);
+            *reinterpret_cast<uint2*>(&Vt[0][d1 * LDV + vt_col(d1, 4 * kg)]) = make_uint2(hi01, hi23);
+          }
+        }
+      }
+    } else {
+      const int kbase = (t - n_ptiles) * KT;
+#pragma unroll
+      for (int j = 0; j < OK; ++j) {
         const int idx = tid + 256 * j, key = idx / (HD / 4), dq = idx % (HD / 4);
-        const int kk = kbase + key < s ? kbase + key : 0;
-        float4 kf = __builtin_bit_cast(float4, ldg16(Ko + (size_t)kk * HD + dq * 4));
-        if (kbase + key >= s) kf = make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 kf = __builtin_bit_cast(float4, keep_if(kbase + key < s, stg[j]));
         uint16_t kh[4], kl[4];
         split2(kf.x, kh[0], kl[0]); split2(kf.y, kh[1], kl[1]); split2(kf.z, kh[2], kl[2]); split2(kf.w, kh[3], kl[3]);
         *reinterpret_cast<uint2*>(&Ks[0][key * LDK + dq * 4]) = make_uint2(pack2(kh[0], kh[1]), pack2(kh[2], kh[3]));
         *reinterpret_cast<uint2*>(&Ks[1][key * LDK + dq * 4]) = make_uint2(pack2(kl[0], kl[1]), pack2(kl[2], kl[3]));
       }
-      for (int idx = tid; idx < KT * HD / 16; idx += 256) {
-        const int dq = idx % (HD / 4), kg = idx / (HD / 4);
-        float4 v4[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = kbase + 4 * kg + e;
-          v4[e] = __builtin_bit_cast(float4, ldg16(Vo + (size_t)(key < s ? key : 0) * HD + dq * 4));
-          if (key >= s) v4[e] = make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+      for (int u = 0; u < OVU; ++u) {
+        const int idx = tid + 256 * u;
+        if (idx < KT * HD / 16) {
+          const int dq = idx % (HD / 4), kg = idx / (HD / 4);
+          float x[4][4];   // x[e][k]: dimension 4dq + k of key 4kg + e
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int dim = dq * 4 + e;
-          uint16_t hh[4], lw[4];
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4) {
-            const float x = e == 0 ? v4[q4].x : (e == 1 ? v4[q4].y : (e == 2 ? v4[q4].z : v4[q4].w));
-            split2(x, hh[q4], lw[q4]);
+          for (int e = 0; e < 4; ++e) {
+            const int key = kbase + 4 * kg + e;
+            const bool ok = key < s;
+            const uint4 v = ldg16(Vo + (size_t)(ok ? key : 0) * HD + dq * 4);
+            x[e][0] = ok ? __uint_as_float(v.x) : 0.f;
+            x[e][1] = ok ? __uint_as_float(v.y) : 0.f;
+            x[e][2] = ok ? __uint_as_float(v.z) : 0.f;
+            x[e][3] = ok ? __uint_as_float(v.w) : 0.f;
           }
-          const int col = vt_col(dim, 4 * kg);
-          *reinterpret_cast<uint2*>(&Vt[0][dim * LDV + col]) = make_uint2(pack2(hh[0], hh[1]), pack2(hh[2], hh[3]));
-          *reinterpret_cast<uint2*>(&Vt[1][dim * LDV + col]) = make_uint2(pack2(lw[0], lw[1]), pack2(lw[2], lw[3]));
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int dim = dq * 4 + k;
+            uint16_t hh[4], lw[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) split2(x[e][k], hh[e], lw[e]);
+            const int col = vt_col(dim, 4 * kg);
+            *reinterpret_cast<uint2*>(&Vt[0][dim * LDV + col]) = make_uint2(pack2(hh[0], hh[1]), pack2(hh[2], hh[3]));
+            *reinterpret_cast<uint2*>(&Vt[1][dim * LDV + col]) = make_uint2(pack2(lw[0], lw[1]), pack2(lw[2], lw[3]));
+          }
         }
       }
     }
+  };
+
+  if (t_begin < t_end) fetch(t_begin);
+  for (int t = t_begin; t < t_end; ++t) {
+    const bool own = t >= n_ptiles;
+    const int kbase = own ? (t - n_ptiles) * KT : t * KT;
+    store(t);
     __syncthreads();
+    if (t + 1 < t_end) fetch(t + 1);   // in flight while this tile is contracted
 
     // S^T: lane holds scores of keys 16*kt + 4g + i for its query.
     floatx4 sc[4];
@@ -208,11 +260,10 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
       }
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    // A tile can be fully masked for a query only after an earlier tile of the same
-    // chunk gave it a finite maximum (prefix tiles are never fully masked; own tile
-    // 0 always holds key 0), so mn is finite whenever scores are used.
+    // A query may see no key in this chunk so far (an own-span tile past it):
+    // then mn = -inf and everything stays zero.
     const float mn = fmaxf(m, mt);
-    const float alpha = exp2f((m - mn) * sl2);
+    const float alpha = m == -INFINITY ? 0.f : exp2f((m - mn) * sl2);
     m = mn;
     l *= alpha;
 #pragma unroll
@@ -222,7 +273,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        p[kt][i] = exp2f((sc[kt][i] - mn) * sl2);
+        p[kt][i] = mn == -INFINITY ? 0.f : exp2f((sc[kt][i] - mn) * sl2);
         l += p[kt][i];
       }
     // O^T += V^T P^T over two 32-key blocks; lane group g supplies keys
@@ -262,11 +313,11 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
 
   l += __shfl_xor(l, 16, 64);
   l += __shfl_xor(l, 32, 64);
-  if (!qvalid) return;
+  const size_t plane = (size_t)max_rows * H * HD;
   if (nchunks == 1) {
+    if (!qvalid) return;
     // The output feeds the O projection: bf16 hi/lo planes [max_rows, H*hd] each.
     const float inv = 1.f / l;
-    const size_t plane = (size_t)max_rows * H * HD;
     bf16* ob = reinterpret_cast<bf16*>(o);
 #pragma unroll
     for (int dt = 0; dt < ND; ++dt) {
@@ -277,16 +328,16 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const float* __restrict__ q, 
       *reinterpret_cast<uint2*>(ob + idx) = make_uint2(pack2(h4[0], h4[1]), pack2(h4[2], h4[3]));
       *reinterpret_cast<uint2*>(ob + plane + idx) = make_uint2(pack2(l4[0], l4[1]), pack2(l4[2], l4[3]));
     }
-  } else {
-    // Unnormalised partial output and its (max, sum) for the combine kernel.
-    const size_t prow = ((size_t)chunk * max_rows + qrow) * H + h;
-    float* orow = opart + prow * HD;
-#pragma unroll
-    for (int dt = 0; dt < ND; ++dt)
-      *reinterpret_cast<float4*>(orow + 16 * dt + 4 * g) =
-          make_float4(oacc[dt][0], oacc[dt][1], oacc[dt][2], oacc[dt][3]);
-    if (g == 0) *reinterpret_cast<float2*>(mlpart + prow * 2) = make_float2(m, l);
+    return;
   }
+  // Unnormalised partial output and its (max, sum) for the combine kernel.
+  if (!qvalid) return;
+  const size_t prow = ((size_t)chunk * max_rows + qrow) * H + h;
+  float* orow = opart + prow * HD;
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt)
+    *reinterpret_cast<float4*>(orow + 16 * dt + 4 * g) = make_float4(oacc[dt][0], oacc[dt][1], oacc[dt][2], oacc[dt][3]);
+  if (g == 0) *reinterpret_cast<float2*>(mlpart + prow * 2) = make_float2(m, l);
 }
 
 // Merges the split-KV partials of each (row, head):
@@ -367,11 +418,11 @@ __global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ q, c
 int attention_chunks(DType dt, int B, int n, int s, int H, int Hkv) {
   if (dt != DType::BF16 || n == 0) return 1;
   const int base = ((H / Hkv) * s + 63) / 64 * Hkv * B;
-  const int n_ptiles = (n + 63) / 64;
+  // Tiles of the smallest query tile: every chunk gets at least one.
+  const int min_tiles = (n + 63) / 64 + 1;
   int chunks = 1;
-  // Split the prefix until the launch has about two workgroups per CU.
-  while (base * chunks < 512 && chunks - 1 < n_ptiles) chunks = chunks == 1 ? 3 : chunks + 1;
-  if (chunks > 1 && chunks - 1 > n_ptiles) chunks = n_ptiles + 1;
+  // Split the keys until the launch has about two workgroups per CU.
+  while (base * chunks < 512 && chunks < min_tiles) ++chunks;
   return chunks;
 }
 

@@ -231,13 +231,25 @@ GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
     p.splits = cdiv(K, p.k_per_split);
     return p;
   }
-  // bf16: one 8-wave workgroup per compute unit at a time (144 KB of LDS); split
-  // K until the launch covers ~192 workgroups, keeping at least 256 K per split.
+  // bf16: one 8-wave workgroup per compute unit at a time. Take the widest weight
+  // tile (256, 192 or 128 columns: wider tiles read fewer activation bytes from
+  // LDS per MFMA) whose launch still reaches ~224 workgroups with at most 8
+  // K splits; split K until it does, keeping at least 256 K per split.
   p.bm = 128;
+  const int mt = cdiv(max_rows, p.bm);
+  auto splits_for = [&](int bn) {
+    int sp = 1;
+    while (cdiv(N, bn) * mt * sp < 224 && K / (sp * 2) >= 256 && sp < kMaxSplitsGemm) sp *= 2;
+    return sp;
+  };
   p.bn = 128;
-  const int tiles = cdiv(N, p.bn) * cdiv(max_rows, p.bm);
-  int splits = 1;
-  while (tiles * splits < 192 && K / (splits * 2) >= 256 && splits < kMaxSplitsGemm) splits *= 2;
+  for (int bn : {256, 192}) {
+    if (cdiv(N, bn) * mt * splits_for(bn) >= 224) {
+      p.bn = bn;
+      break;
+    }
+  }
+  const int splits = splits_for(p.bn);
   p.k_per_split = cdiv(cdiv(K, 64), splits) * 64;
   p.splits = cdiv(K, p.k_per_split);
   return p;
@@ -250,9 +262,18 @@ hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* 
     hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, st, static_cast<const float*>(A0),
                        static_cast<const float*>(W), P, split_stride, c, s, max_rows, N, K, p.k_per_split);
   } else {
-    hipLaunchKernelGGL((k_gemm_dma<128, 3>), grid, dim3(kGemmWaves * 64), 0, st, static_cast<const bf16*>(A0),
-                       static_cast<const bf16*>(A1), static_cast<const bf16*>(W), P, split_stride, c, s, max_rows,
-                       N, K, p.k_per_split);
+    const bf16 *a0 = static_cast<const bf16*>(A0), *a1 = static_cast<const bf16*>(A1);
+    const bf16* w = static_cast<const bf16*>(W);
+    // LDS: 144 KB (128 columns, 3 slots), 112 KB (192, 2), 128 KB (256, 2).
+    if (p.bn == 256)
+      hipLaunchKernelGGL((k_gemm_dma<256, 2>), grid, dim3(kGemmWaves * 64), 0, st, a0, a1, w, P, split_stride, c, s,
+                         max_rows, N, K, p.k_per_split);
+    else if (p.bn == 192)
+      hipLaunchKernelGGL((k_gemm_dma<192, 2>), grid, dim3(kGemmWaves * 64), 0, st, a0, a1, w, P, split_stride, c, s,
+                         max_rows, N, K, p.k_per_split);
+    else
+      hipLaunchKernelGGL((k_gemm_dma<128, 3>), grid, dim3(kGemmWaves * 64), 0, st, a0, a1, w, P, split_stride, c, s,
+                         max_rows, N, K, p.k_per_split);
   }
   return hipGetLastError();
 }
