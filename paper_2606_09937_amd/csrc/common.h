@@ -53,12 +53,10 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t u) {
   return __uint_as_float(static_cast<uint32_t>(u) << 16);
 }
 
-// Round-to-nearest-even fp32 -> bf16 bits (finite inputs; NaN stays NaN).
+// Round-to-nearest-even fp32 -> bf16 bits (NaN stays NaN): gfx950's
+// v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 
 // Split of an fp32 value into bf16 hi + lo (hi = RNE(x), lo = RNE(x - hi); x - hi
@@ -66,8 +64,9 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
 // times each part is exact in the MFMA's fp32 products, so two bf16 MFMAs give
 // an fp32-accurate product with a bf16 operand.
 __device__ __forceinline__ void split2(float x, uint16_t& hi, uint16_t& lo) {
-  hi = f32_to_bf16_bits(x);
-  lo = f32_to_bf16_bits(x - bf16_to_f32(hi));
+  const __bf16 h = static_cast<__bf16>(x);
+  hi = __builtin_bit_cast(uint16_t, h);
+  lo = __builtin_bit_cast(uint16_t, static_cast<__bf16>(x - static_cast<float>(h)));
 }
 
 __device__ __forceinline__ uint32_t pack2(uint16_t a, uint16_t b) {
