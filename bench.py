@@ -262,9 +262,10 @@ def cpu_baseline(mw, kv, toks, wl, layers):
     tokens = wl.n_branches * wl.branch_len
     return {
         "value": tokens / per_step, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-        "sample": (f"float64 oracle verify pass over the first {layers} of {shape.n_layers} layers of the same "
-                   f"workload ({wl.n_branches} branch(es) x {wl.branch_len} tokens, {kv.k.shape[2]}-token prefix), "
-                   f"{dt:.1f} s, time scaled by {shape.n_layers}/{layers}"),
+        "sample": (f"float64 oracle verify pass over {'all' if layers == shape.n_layers else f'the first {layers} of'} "
+                   f"{shape.n_layers} layers of the same workload ({wl.n_branches} branch(es) x {wl.branch_len} tokens, "
+                   f"{kv.k.shape[2]}-token prefix), {dt:.1f} s"
+                   + ("" if layers == shape.n_layers else f", time scaled by {shape.n_layers}/{layers}")),
     }
 
 
@@ -277,7 +278,8 @@ def main():
     ap.add_argument("--tau", type=float, default=None)
     ap.add_argument("--patience", type=int, default=None)
     ap.add_argument("--seed", type=int, default=42)
-    ap.add_argument("--cpu-layers", type=int, default=4, help="layers in the oracle's bounded sample")
+    ap.add_argument("--cpu-layers", type=int, default=0,
+                    help="layers in the oracle's sample (0: all layers, the whole verify pass)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-depth", action="store_true")
     ap.add_argument("--no-tau-sweep", action="store_true")
@@ -486,8 +488,9 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        log(f"cpu baseline: oracle on {args.cpu_layers} layer(s)")
-        cpu = cpu_baseline(mw, kv, toks, wl, min(args.cpu_layers, L))
+        cpu_layers = L if args.cpu_layers <= 0 else min(args.cpu_layers, L)
+        log(f"cpu baseline: oracle on {cpu_layers} layer(s)")
+        cpu = cpu_baseline(mw, kv, toks, wl, cpu_layers)
         log(f"cpu baseline: {cpu['value']:.3f} tokens/s on {cpu['cores']} threads")
 
     out = {
