@@ -19,6 +19,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace rksc {
 
 namespace {
@@ -29,10 +31,17 @@ __device__ __forceinline__ uint4 keep_if(bool c, const uint4& a) {
   return make_uint4(c ? a.x : 0u, c ? a.y : 0u, c ? a.z : 0u, c ? a.w : 0u);
 }
 
-// V^T tile layout: row = head dimension, column = key. The 4-key group of a
-// row is XOR-swizzled by the row's 8-dimension block so that the packed stores
-// (4 keys of one dimension) and the fragment reads are bank-conflict free.
-__device__ __forceinline__ int vt_col(int dim, int key) { return key ^ (((dim >> 3) & 15) << 2); }
+// V^T tile layout: row = head dimension, column = key position. Within each
+// 32-key block the eight keys that one lane group feeds to a P.V MFMA
+// ({4g..4g+3} and {16+4g..16+4g+3}, the keys whose probabilities the lane
+// holds) are made adjacent, so a fragment is one 16-byte read; the 8-key groups
+// are XOR-swizzled by the row's 8-dimension block so that the 4-key stores of
+// neighbouring dimension blocks land in different banks.
+__device__ __forceinline__ int vt_col(int dim, int key) {
+  const int k = key & 31;
+  const int pos = (key & 32) + ((k & 15) >> 2) * 8 + (k >> 4) * 4 + (k & 3);
+  return pos ^ (((dim >> 3) & 7) << 3);
+}
 
 // Split-KV: the key tiles of a query tile -- the prefix tiles, then the own-span
 // tiles up to its last query -- are divided evenly over `nchunks` workgroups,
@@ -42,7 +51,13 @@ __device__ __forceinline__ int vt_col(int dim, int key) { return key ^ (((dim >>
 // whole L2 and cost far more than the separate combine launch.)
 // Tile loads are software-pipelined: the next tile's K/V (own-span tiles: K)
 // are fetched into registers while the current tile is contracted; the masking
-// and the hi/lo split happen when they are stored to LDS.
+// and the hi/lo split happen when they are stored to LDS. The contraction is
+// instantiated per tile kind (full prefix tile, last partial prefix tile,
+// own-span tile), so the MFMA sequences carry no branches and full prefix
+// tiles no masking.
+// Scores are formed in log2 units: the queries are pre-multiplied by
+// log2(e)/sqrt(hd) before their hi/lo split, and the partial maxima in mlpart
+// are in the same units.
 template <int HD>
 __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ q, const bf16* __restrict__ pk,
                                                    const bf16* __restrict__ pv, const float* __restrict__ ko,
@@ -84,6 +99,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
 
   const int i_max = min(s - 1, (min(row0 + 63, rows - 1)) / G);
   const int n_ptiles = (n + KT - 1) / KT;
+  const int n_full = n / KT;      // prefix tiles with no key past n - 1
   const int n_tiles = n_ptiles + i_max / KT + 1;
   const int t_begin = chunk * n_tiles / nchunks, t_end = (chunk + 1) * n_tiles / nchunks;
 
@@ -99,9 +115,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
   for (int cc = 0; cc < NC; ++cc) {
     const float* qp = q + (qrow * H + h) * HD + 32 * cc + 8 * g;
     const float4 a = *reinterpret_cast<const float4*>(qp), b = *reinterpret_cast<const float4*>(qp + 4);
+    const float x[8] = {a.x * sl2, a.y * sl2, a.z * sl2, a.w * sl2, b.x * sl2, b.y * sl2, b.z * sl2, b.w * sl2};
     uint16_t hh[8], ll[8];
-    split2(a.x, hh[0], ll[0]); split2(a.y, hh[1], ll[1]); split2(a.z, hh[2], ll[2]); split2(a.w, hh[3], ll[3]);
-    split2(b.x, hh[4], ll[4]); split2(b.y, hh[5], ll[5]); split2(b.z, hh[6], ll[6]); split2(b.w, hh[7], ll[7]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) split2(x[e], hh[e], ll[e]);
     qh[cc] = __builtin_bit_cast(bf16x8, make_uint4(pack2(hh[0], hh[1]), pack2(hh[2], hh[3]), pack2(hh[4], hh[5]),
                                                    pack2(hh[6], hh[7])));
     ql[cc] = __builtin_bit_cast(bf16x8, make_uint4(pack2(ll[0], ll[1]), pack2(ll[2], ll[3]), pack2(ll[4], ll[5]),
@@ -124,10 +141,13 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
   auto fetch = [&](int t) {
     if (t < n_ptiles) {
       const int kbase = t * KT;
+      const bf16* kt = Kp + (size_t)kbase * HD;
+      const bf16* vt = Vp + (size_t)kbase * HD;
+      const int kmax = n - 1 - kbase;   // last valid key of the tile
 #pragma unroll
       for (int j = 0; j < PK; ++j) {
-        const int idx = tid + 256 * j, key = kbase + idx / (HD / 8), dc = idx % (HD / 8);
-        stg[j] = ldg16(Kp + (size_t)(key < n ? key : 0) * HD + dc * 8);
+        const int idx = tid + 256 * j, key = idx / (HD / 8), dc = idx % (HD / 8);
+        stg[j] = ldg16(kt + (key <= kmax ? key : kmax) * HD + dc * 8);
       }
 #pragma unroll
       for (int u = 0; u < PVU; ++u) {
@@ -135,102 +155,103 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
         const int dc = idx % (HD / 8), kg = (idx < KT * HD / 32 ? idx : 0) / (HD / 8);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int key = kbase + 4 * kg + e;
-          stg[PK + 4 * u + e] = ldg16(Vp + (size_t)(key < n ? key : 0) * HD + dc * 8);
+          const int key = 4 * kg + e;
+          stg[PK + 4 * u + e] = ldg16(vt + (key <= kmax ? key : kmax) * HD + dc * 8);
         }
       }
     } else {
       const int kbase = (t - n_ptiles) * KT;
-#pragma unroll
-      for (int j = 0; j < OK; ++j) {
-        const int idx = tid + 256 * j, key = kbase + idx / (HD / 4), dq = idx % (HD / 4);
-        stg[j] = ldg16(Ko + (size_t)(key < s ? key : 0) * HD + dq * 4);
-      }
-    }
-  };
-  // Store of the fetched tile t to LDS: K rows and V^T, own-span tiles split into hi/lo.
-  auto store = [&](int t) {
-    if (t < n_ptiles) {
-      const int kbase = t * KT;
-#pragma unroll
-      for (int j = 0; j < PK; ++j) {
-        const int idx = tid + 256 * j, key = idx / (HD / 8), dc = idx % (HD / 8);
-        *reinterpret_cast<uint4*>(&Ks[0][key * LDK + dc * 8]) = keep_if(kbase + key < n, stg[j]);
-      }
-#pragma unroll
-      for (int u = 0; u < PVU; ++u) {
-        const int idx = tid + 256 * u;
-        if (idx < KT * HD / 32) {
-          const int dc = idx % (HD / 8), kg = idx / (HD / 8);
-          uint32_t w[4][4];   // w[e][j]: word j (elements 2j, 2j+1) of key 4kg + e
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const uint4 v = keep_if(kbase + 4 * kg + e < n, stg[PK + 4 * u + e]);
-            w[e][0] = v.x; w[e][1] = v.y; w[e][2] = v.z; w[e][3] = v.w;
-          }
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            // elements 2j (low halves) and 2j+1 (high halves) of the four keys
-            const uint32_t lo01 = (w[0][j] & 0xffffu) | (w[1][j] << 16);
-            const uint32_t lo23 = (w[2][j] & 0xffffu) | (w[3][j] << 16);
-            const uint32_t hi01 = (w[0][j] >> 16) | (w[1][j] & 0xffff0000u);
-            const uint32_t hi23 = (w[2][j] >> 16) | (w[3][j] & 0xffff0000u);
-            const int d0 = dc * 8 + 2 * j, d1 = d0 + 1;
-            *reinterpret_cast<uint2*>(&Vt[0][d0 * LDV + vt_col(d0, 4 * kg)]) = make_uint2(lo01, lo23);
-            *reinterpret_cast<uint2*>(&Vt[0][d1 * LDV + vt_col(d1, 4 * kg)]) = make_uint2(hi01, hi23);
-          }
-        }
-      }
-    } else {
-      const int kbase = (t - n_ptiles) * KT;
+      const float* kt = Ko + (size_t)kbase * HD;
+      const int kmax = s - 1 - kbase;
 #pragma unroll
       for (int j = 0; j < OK; ++j) {
         const int idx = tid + 256 * j, key = idx / (HD / 4), dq = idx % (HD / 4);
-        const float4 kf = __builtin_bit_cast(float4, keep_if(kbase + key < s, stg[j]));
-        uint16_t kh[4], kl[4];
-        split2(kf.x, kh[0], kl[0]); split2(kf.y, kh[1], kl[1]); split2(kf.z, kh[2], kl[2]); split2(kf.w, kh[3], kl[3]);
-        *reinterpret_cast<uint2*>(&Ks[0][key * LDK + dq * 4]) = make_uint2(pack2(kh[0], kh[1]), pack2(kh[2], kh[3]));
-        *reinterpret_cast<uint2*>(&Ks[1][key * LDK + dq * 4]) = make_uint2(pack2(kl[0], kl[1]), pack2(kl[2], kl[3]));
+        stg[j] = ldg16(kt + (key <= kmax ? key : kmax) * HD + dq * 4);
       }
+    }
+  };
+  // Store of a fetched prefix tile to LDS (K rows and V^T); PARTIAL zeroes the
+  // keys past n - 1.
+  auto store_prefix = [&](auto partial, int kbase) {
+    constexpr bool PARTIAL = decltype(partial)::value;
 #pragma unroll
-      for (int u = 0; u < OVU; ++u) {
-        const int idx = tid + 256 * u;
-        if (idx < KT * HD / 16) {
-          const int dq = idx % (HD / 4), kg = idx / (HD / 4);
-          float x[4][4];   // x[e][k]: dimension 4dq + k of key 4kg + e
+    for (int j = 0; j < PK; ++j) {
+      const int idx = tid + 256 * j, key = idx / (HD / 8), dc = idx % (HD / 8);
+      *reinterpret_cast<uint4*>(&Ks[0][key * LDK + dc * 8]) = PARTIAL ? keep_if(kbase + key < n, stg[j]) : stg[j];
+    }
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int key = kbase + 4 * kg + e;
-            const bool ok = key < s;
-            const uint4 v = ldg16(Vo + (size_t)(ok ? key : 0) * HD + dq * 4);
-            x[e][0] = ok ? __uint_as_float(v.x) : 0.f;
-            x[e][1] = ok ? __uint_as_float(v.y) : 0.f;
-            x[e][2] = ok ? __uint_as_float(v.z) : 0.f;
-            x[e][3] = ok ? __uint_as_float(v.w) : 0.f;
-          }
+    for (int u = 0; u < PVU; ++u) {
+      const int idx = tid + 256 * u;
+      if (idx < KT * HD / 32) {
+        const int dc = idx % (HD / 8), kg = idx / (HD / 8);
+        uint32_t w[4][4];   // w[e][j]: word j (elements 2j, 2j+1) of key 4kg + e
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            const int dim = dq * 4 + k;
-            uint16_t hh[4], lw[4];
+        for (int e = 0; e < 4; ++e) {
+          const uint4 v = PARTIAL ? keep_if(kbase + 4 * kg + e < n, stg[PK + 4 * u + e]) : stg[PK + 4 * u + e];
+          w[e][0] = v.x; w[e][1] = v.y; w[e][2] = v.z; w[e][3] = v.w;
+        }
 #pragma unroll
-            for (int e = 0; e < 4; ++e) split2(x[e][k], hh[e], lw[e]);
-            const int col = vt_col(dim, 4 * kg);
-            *reinterpret_cast<uint2*>(&Vt[0][dim * LDV + col]) = make_uint2(pack2(hh[0], hh[1]), pack2(hh[2], hh[3]));
-            *reinterpret_cast<uint2*>(&Vt[1][dim * LDV + col]) = make_uint2(pack2(lw[0], lw[1]), pack2(lw[2], lw[3]));
-          }
+        for (int j = 0; j < 4; ++j) {
+          // elements 2j (low halves) and 2j+1 (high halves) of the four keys
+          const uint32_t lo01 = (w[0][j] & 0xffffu) | (w[1][j] << 16);
+          const uint32_t lo23 = (w[2][j] & 0xffffu) | (w[3][j] << 16);
+          const uint32_t hi01 = (w[0][j] >> 16) | (w[1][j] & 0xffff0000u);
+          const uint32_t hi23 = (w[2][j] >> 16) | (w[3][j] & 0xffff0000u);
+          const int d0 = dc * 8 + 2 * j, d1 = d0 + 1;
+          *reinterpret_cast<uint2*>(&Vt[0][d0 * LDV + vt_col(d0, 4 * kg)]) = make_uint2(lo01, lo23);
+          *reinterpret_cast<uint2*>(&Vt[0][d1 * LDV + vt_col(d1, 4 * kg)]) = make_uint2(hi01, hi23);
+        }
+      }
+    }
+  };
+  // Store of a fetched own-span tile: K and V split into hi/lo; keys past s - 1 zeroed.
+  auto store_own = [&](int kbase) {
+#pragma unroll
+    for (int j = 0; j < OK; ++j) {
+      const int idx = tid + 256 * j, key = idx / (HD / 4), dq = idx % (HD / 4);
+      const float4 kf = __builtin_bit_cast(float4, keep_if(kbase + key < s, stg[j]));
+      uint16_t kh[4], kl[4];
+      split2(kf.x, kh[0], kl[0]); split2(kf.y, kh[1], kl[1]); split2(kf.z, kh[2], kl[2]); split2(kf.w, kh[3], kl[3]);
+      *reinterpret_cast<uint2*>(&Ks[0][key * LDK + dq * 4]) = make_uint2(pack2(kh[0], kh[1]), pack2(kh[2], kh[3]));
+      *reinterpret_cast<uint2*>(&Ks[1][key * LDK + dq * 4]) = make_uint2(pack2(kl[0], kl[1]), pack2(kl[2], kl[3]));
+    }
+#pragma unroll
+    for (int u = 0; u < OVU; ++u) {
+      const int idx = tid + 256 * u;
+      if (idx < KT * HD / 16) {
+        const int dq = idx % (HD / 4), kg = idx / (HD / 4);
+        float x[4][4];   // x[e][k]: dimension 4dq + k of key 4kg + e
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int key = kbase + 4 * kg + e;
+          const bool ok = key < s;
+          const uint4 v = ldg16(Vo + (size_t)(ok ? key : 0) * HD + dq * 4);
+          x[e][0] = ok ? __uint_as_float(v.x) : 0.f;
+          x[e][1] = ok ? __uint_as_float(v.y) : 0.f;
+          x[e][2] = ok ? __uint_as_float(v.z) : 0.f;
+          x[e][3] = ok ? __uint_as_float(v.w) : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int dim = dq * 4 + k;
+          uint16_t hh[4], lw[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) split2(x[e][k], hh[e], lw[e]);
+          const int col = vt_col(dim, 4 * kg);
+          *reinterpret_cast<uint2*>(&Vt[0][dim * LDV + col]) = make_uint2(pack2(hh[0], hh[1]), pack2(hh[2], hh[3]));
+          *reinterpret_cast<uint2*>(&Vt[1][dim * LDV + col]) = make_uint2(pack2(lw[0], lw[1]), pack2(lw[2], lw[3]));
         }
       }
     }
   };
 
-  if (t_begin < t_end) fetch(t_begin);
-  for (int t = t_begin; t < t_end; ++t) {
-    const bool own = t >= n_ptiles;
-    const int kbase = own ? (t - n_ptiles) * KT : t * KT;
-    store(t);
-    __syncthreads();
-    if (t + 1 < t_end) fetch(t + 1);   // in flight while this tile is contracted
-
+  // Contraction of the tile in LDS with this lane's query: S^T = K Q^T, online
+  // softmax in log2 units, O^T += V^T P^T. OWN: the keys and values are hi/lo
+  // pairs (three MFMAs per product) and the causal mask applies; MASKED: some
+  // keys of the tile are invalid for some query.
+  auto contract = [&](auto own_c, auto masked_c, int kbase) {
+    constexpr bool OWN = decltype(own_c)::value;
+    constexpr bool MASKED = decltype(masked_c)::value;
     // S^T: lane holds scores of keys 16*kt + 4g + i for its query.
     floatx4 sc[4];
 #pragma unroll
@@ -242,38 +263,45 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
         const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&Ks[0][off]);
         sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qh[cc], sc[kt], 0, 0, 0);
         sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, ql[cc], sc[kt], 0, 0, 0);
-        if (own) {
+        if constexpr (OWN) {
           const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&Ks[1][off]);
           sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qh[cc], sc[kt], 0, 0, 0);
         }
       }
     }
-    float mt = -INFINITY;
+    if constexpr (MASKED) {
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+      for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = kbase + 16 * kt + 4 * g + i;
-        const bool ok = own ? (key <= qi) : (key < n);
-        if (!ok) sc[kt][i] = -INFINITY;
-        mt = fmaxf(mt, sc[kt][i]);
-      }
+        for (int i = 0; i < 4; ++i) {
+          const int key = kbase + 16 * kt + 4 * g + i;
+          if (!(OWN ? key <= qi : key < n)) sc[kt][i] = -INFINITY;
+        }
+    }
+    float mt = fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3]));
+#pragma unroll
+    for (int kt = 1; kt < 4; ++kt) mt = fmaxf(mt, fmaxf(fmaxf(sc[kt][0], sc[kt][1]), fmaxf(sc[kt][2], sc[kt][3])));
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    // A query may see no key in this chunk so far (an own-span tile past it):
-    // then mn = -inf and everything stays zero.
     const float mn = fmaxf(m, mt);
-    const float alpha = m == -INFINITY ? 0.f : exp2f((m - mn) * sl2);
+    // A fully masked tile for this query (an own-span tile past it, possible
+    // only when MASKED) leaves mn = -inf: then nothing is accumulated.
+    const bool none = MASKED && mn == -INFINITY;
+    const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m - mn);   // m = -inf gives 0
+    const float msub = none ? 0.f : mn;
     m = mn;
-    l *= alpha;
+    // Rescale only when some query's maximum moved (rare after the first tiles).
+    if (__ballot(alpha != 1.f)) {
+      l *= alpha;
 #pragma unroll
-    for (int dt = 0; dt < ND; ++dt) oacc[dt] *= alpha;
+      for (int dt = 0; dt < ND; ++dt) oacc[dt] *= alpha;
+    }
     float p[4][4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        p[kt][i] = mn == -INFINITY ? 0.f : exp2f((sc[kt][i] - mn) * sl2);
+        p[kt][i] = __builtin_amdgcn_exp2f(sc[kt][i] - msub);   // masked: exp2(-inf) = 0
         l += p[kt][i];
       }
     // O^T += V^T P^T over two 32-key blocks; lane group g supplies keys
@@ -293,21 +321,28 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt) {
         const int dim = 16 * dt + r16;
-        const int off0 = dim * LDV + vt_col(dim, 32 * kb + 4 * g);
-        const int off1 = dim * LDV + vt_col(dim, 32 * kb + 16 + 4 * g);
-        const uint2 a0 = *reinterpret_cast<const uint2*>(&Vt[0][off0]);
-        const uint2 a1 = *reinterpret_cast<const uint2*>(&Vt[0][off1]);
-        const bf16x8 v0 = __builtin_bit_cast(bf16x8, make_uint4(a0.x, a0.y, a1.x, a1.y));
+        const int off = dim * LDV + vt_col(dim, 32 * kb + 4 * g);
+        const bf16x8 v0 = *reinterpret_cast<const bf16x8*>(&Vt[0][off]);
         oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, pbh, oacc[dt], 0, 0, 0);
         oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, pbl, oacc[dt], 0, 0, 0);
-        if (own) {
-          const uint2 b0 = *reinterpret_cast<const uint2*>(&Vt[1][off0]);
-          const uint2 b1 = *reinterpret_cast<const uint2*>(&Vt[1][off1]);
-          const bf16x8 v1 = __builtin_bit_cast(bf16x8, make_uint4(b0.x, b0.y, b1.x, b1.y));
+        if constexpr (OWN) {
+          const bf16x8 v1 = *reinterpret_cast<const bf16x8*>(&Vt[1][off]);
           oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, pbh, oacc[dt], 0, 0, 0);
         }
       }
     }
+  };
+
+  if (t_begin < t_end) fetch(t_begin);
+  for (int t = t_begin; t < t_end; ++t) {
+    if (t < n_full) store_prefix(std::false_type{}, t * KT);
+    else if (t < n_ptiles) store_prefix(std::true_type{}, t * KT);
+    else store_own((t - n_ptiles) * KT);
+    __syncthreads();
+    if (t + 1 < t_end) fetch(t + 1);   // in flight while this tile is contracted
+    if (t < n_full) contract(std::false_type{}, std::false_type{}, t * KT);
+    else if (t < n_ptiles) contract(std::false_type{}, std::true_type{}, t * KT);
+    else contract(std::true_type{}, std::true_type{}, (t - n_ptiles) * KT);
     __syncthreads();
   }
 
@@ -340,30 +375,68 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
   if (g == 0) *reinterpret_cast<float2*>(mlpart + prow * 2) = make_float2(m, l);
 }
 
-// Merges the split-KV partials of each (row, head):
-// o = sum_c e^{(m_c - M) sl} o_c / sum_c e^{(m_c - M) sl} l_c, M = max_c m_c.
-// A chunk that saw no key for a query (m = -inf) contributes nothing.
+// Merges the split-KV partials of each (row, head), with maxima in log2 units:
+// o = sum_c 2^{m_c - M} o_c / sum_c 2^{m_c - M} l_c, M = max_c m_c.
+// A chunk that saw no key for a query (m = -inf) contributes nothing. One wave
+// per (row, head): lane c < nchunks reads chunk c's (m, l), the wave reduces
+// the maximum, and each lane then sums its HD/64 dimensions over the chunks.
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_combine(const float* __restrict__ opart, const float* __restrict__ mlpart,
-                                                      void* __restrict__ o, const Ctrl* c, int s, int H, float sl2,
+                                                      void* __restrict__ o, const Ctrl* c, int s, int H,
                                                       int nchunks, int max_rows) {
   const int rows = c->live_count * s * H;
   const int wid = (blockIdx.x * blockDim.x + threadIdx.x) >> 6, lane = threadIdx.x & 63;
   if (wid >= rows) return;    // one wave per (row, head)
-  float M = -INFINITY;
-  for (int ch = 0; ch < nchunks; ++ch) M = fmaxf(M, mlpart[((size_t)ch * max_rows * H + wid) * 2]);
-  float den = 0.f;
+  const size_t cstride = (size_t)max_rows * H;
   float acc[HD / 64];
 #pragma unroll
   for (int j = 0; j < HD / 64; ++j) acc[j] = 0.f;
-  for (int ch = 0; ch < nchunks; ++ch) {
-    const float2 ml = *reinterpret_cast<const float2*>(mlpart + ((size_t)ch * max_rows * H + wid) * 2);
-    if (ml.x == -INFINITY) continue;
-    const float w = exp2f((ml.x - M) * sl2);
-    den += w * ml.y;
-    const float* op = opart + ((size_t)ch * max_rows * H + wid) * HD;
+  float den = 0.f;
+  float Mx = -INFINITY;
+  for (int c0 = 0; c0 < nchunks; c0 += 64) {
+    const int ch = c0 + lane;
+    const float mc = ch < nchunks ? mlpart[(ch * cstride + wid) * 2] : -INFINITY;
+    float M = mc;
 #pragma unroll
-    for (int j = 0; j < HD / 64; ++j) acc[j] += w * op[lane + 64 * j];
+    for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+    Mx = fmaxf(Mx, M);
+  }
+  for (int c0 = 0; c0 < nchunks; c0 += 64) {
+    const int ch = c0 + lane;
+    float w = 0.f, wl = 0.f;
+    if (ch < nchunks) {
+      const float2 ml = *reinterpret_cast<const float2*>(mlpart + (ch * cstride + wid) * 2);
+      w = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - Mx);
+      wl = w * ml.y;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) wl += __shfl_xor(wl, off, 64);
+    den += wl;
+    // Every chunk wrote its partial (zeros where it saw no key), so the loads
+    // are independent of the weights and can all be in flight.
+    const int cn = min(64, nchunks - c0);
+    int k = 0;
+    for (; k + 4 <= cn; k += 4) {
+      float v[4][HD / 64];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float* op = opart + ((size_t)(c0 + k + u) * cstride + wid) * HD;
+#pragma unroll
+        for (int j = 0; j < HD / 64; ++j) v[u][j] = op[lane + 64 * j];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float wk = __shfl(w, k + u, 64);
+#pragma unroll
+        for (int j = 0; j < HD / 64; ++j) acc[j] += wk * v[u][j];
+      }
+    }
+    for (; k < cn; ++k) {
+      const float wk = __shfl(w, k, 64);
+      const float* op = opart + ((size_t)(c0 + k) * cstride + wid) * HD;
+#pragma unroll
+      for (int j = 0; j < HD / 64; ++j) acc[j] += wk * op[lane + 64 * j];
+    }
   }
   // bf16 hi/lo planes of the output, as in the single-chunk path.
   const float inv = 1.f / den;
@@ -418,11 +491,12 @@ __global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ q, c
 int attention_chunks(DType dt, int B, int n, int s, int H, int Hkv) {
   if (dt != DType::BF16 || n == 0) return 1;
   const int base = ((H / Hkv) * s + 63) / 64 * Hkv * B;
-  // Tiles of the smallest query tile: every chunk gets at least one.
+  // Tiles of the smallest query tile.
   const int min_tiles = (n + 63) / 64 + 1;
   int chunks = 1;
-  // Split the keys until the launch has about two workgroups per CU.
-  while (base * chunks < 512 && chunks < min_tiles) ++chunks;
+  // Split the keys until the launch has about two workgroups per CU, keeping at
+  // least 4 tiles per chunk (shorter chunks are all prologue and partial traffic).
+  while (base * chunks < 512 && (chunks + 1) * 4 <= min_tiles) ++chunks;
   return chunks;
 }
 
@@ -447,10 +521,10 @@ hipError_t launch_attention(DType dt, const void* q, const void* pk, const void*
       const int waves = max_rows * H;
       const dim3 cgrid((waves * 64 + 255) / 256);
       if (hd == 128)
-        hipLaunchKernelGGL(k_attn_combine<128>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, sl2, nchunks,
+        hipLaunchKernelGGL(k_attn_combine<128>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, nchunks,
                            max_rows);
       else
-        hipLaunchKernelGGL(k_attn_combine<64>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, sl2, nchunks,
+        hipLaunchKernelGGL(k_attn_combine<64>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, nchunks,
                            max_rows);
     }
   } else {
