@@ -58,7 +58,7 @@ __device__ __forceinline__ int vt_col(int dim, int key) {
 // Scores are formed in log2 units: the queries are pre-multiplied by
 // log2(e)/sqrt(hd) before their hi/lo split, and the partial maxima in mlpart
 // are in the same units.
-template <int HD>
+template <int HD, bool XB>
 __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ q, const bf16* __restrict__ pk,
                                                    const bf16* __restrict__ pv, const float* __restrict__ ko,
                                                    const float* __restrict__ vo, void* __restrict__ o,
@@ -85,13 +85,15 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * LDK];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[2][HD * LDV];
 
-  const int B_slots = gridDim.z / nchunks;
-  const int slot = blockIdx.z % B_slots;
+  // Fused mode: blockIdx.z = chunk * slots + slot, rows of one branch.
+  // XB mode: blockIdx.z = chunk, rows of all live branches, prefix tiles only.
+  const int B_slots = XB ? 1 : gridDim.z / nchunks;
   const int chunk = blockIdx.z / B_slots;
-  if (slot >= c->live_count) return;
+  const int bslot = blockIdx.z % B_slots;
+  if (!XB && bslot >= c->live_count) return;
   const int kvh = blockIdx.y;
   const int G = H / Hkv;
-  const int rows = G * s;
+  const int rows = XB ? c->live_count * s * G : G * s;
   const int row0 = blockIdx.x * 64;
   if (row0 >= rows) return;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -100,7 +102,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
   const int i_max = min(s - 1, (min(row0 + 63, rows - 1)) / G);
   const int n_ptiles = (n + KT - 1) / KT;
   const int n_full = n / KT;      // prefix tiles with no key past n - 1
-  const int n_tiles = n_ptiles + i_max / KT + 1;
+  const int n_tiles = XB ? n_ptiles : n_ptiles + i_max / KT + 1;
   const int t_begin = chunk * n_tiles / nchunks, t_end = (chunk + 1) * n_tiles / nchunks;
 
   // The query this lane owns as an MFMA column. Rows past the end compute a
@@ -108,7 +110,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
   const int rho_raw = row0 + 16 * wid + r16;
   const bool qvalid = rho_raw < rows;
   const int rho = qvalid ? rho_raw : rows - 1;
-  const int qi = rho / G, h = kvh * G + rho % G;
+  const int slot = XB ? rho / (s * G) : bslot;
+  const int rin = XB ? rho - slot * s * G : rho;
+  const int qi = rin / G, h = kvh * G + rin % G;
   const size_t qrow = (size_t)slot * s + qi;
   bf16x8 qh[NC], ql[NC];
 #pragma unroll
@@ -349,7 +353,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
   l += __shfl_xor(l, 16, 64);
   l += __shfl_xor(l, 32, 64);
   const size_t plane = (size_t)max_rows * H * HD;
-  if (nchunks == 1) {
+  if (!XB && nchunks == 1) {
     if (!qvalid) return;
     // The output feeds the O projection: bf16 hi/lo planes [max_rows, H*hd] each.
     const float inv = 1.f / l;
@@ -416,16 +420,16 @@ __global__ __launch_bounds__(256) void k_attn_combine(const float* __restrict__ 
     // are independent of the weights and can all be in flight.
     const int cn = min(64, nchunks - c0);
     int k = 0;
-    for (; k + 4 <= cn; k += 4) {
-      float v[4][HD / 64];
+    for (; k + 8 <= cn; k += 8) {
+      float v[8][HD / 64];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 8; ++u) {
         const float* op = opart + ((size_t)(c0 + k + u) * cstride + wid) * HD;
 #pragma unroll
         for (int j = 0; j < HD / 64; ++j) v[u][j] = op[lane + 64 * j];
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 8; ++u) {
         const float wk = __shfl(w, k + u, 64);
 #pragma unroll
         for (int j = 0; j < HD / 64; ++j) acc[j] += wk * v[u][j];
@@ -448,6 +452,106 @@ __global__ __launch_bounds__(256) void k_attn_combine(const float* __restrict__ 
     split2(acc[j] * inv, hb, lb);
     ob[(size_t)wid * HD + lane + 64 * j] = hb;
     ob[plane + (size_t)wid * HD + lane + 64 * j] = lb;
+  }
+}
+
+// XB-mode merge: the prefix partials of each (row, head) plus the row's own
+// causal span, whose few keys (G * s < 64, so s < 64) are scored here in fp32:
+// o = (sum_c 2^{m_c - M} o_c + sum_{j <= i} 2^{t_j - M} v_j) / (sum_c 2^{m_c - M} l_c + sum_j 2^{t_j - M}),
+// t_j = log2(e)/sqrt(hd) q.k_j, M the maximum of all m_c and t_j. One wave per (row, head).
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_combine_own(const float* __restrict__ opart,
+                                                          const float* __restrict__ mlpart,
+                                                          const float* __restrict__ q, const float* __restrict__ ko,
+                                                          const float* __restrict__ vo, void* __restrict__ o,
+                                                          const Ctrl* c, int s, int H, int Hkv, float sl2,
+                                                          int nchunks, int max_rows) {
+  constexpr int E = HD / 64;   // dimensions per lane
+  const int rows = c->live_count * s * H;
+  const int wid = (blockIdx.x * blockDim.x + threadIdx.x) >> 6, lane = threadIdx.x & 63;
+  if (wid >= rows) return;
+  const int qrow = wid / H, h = wid - qrow * H;
+  const int slot = qrow / s, qi = qrow - slot * s, kvh = h / (H / Hkv);
+  const size_t cstride = (size_t)max_rows * H;
+  float Mx = -INFINITY;
+  for (int c0 = 0; c0 < nchunks; c0 += 64) {
+    const int ch = c0 + lane;
+    float M = ch < nchunks ? mlpart[(ch * cstride + wid) * 2] : -INFINITY;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+    Mx = fmaxf(Mx, M);
+  }
+  float qv[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) qv[e] = q[(size_t)wid * HD + lane + 64 * e] * sl2;
+  const float* kb = ko + ((size_t)slot * Hkv + kvh) * s * HD;
+  const float* vb = vo + ((size_t)slot * Hkv + kvh) * s * HD;
+  float my_t = -INFINITY;   // lane j keeps the score of own key j
+  for (int j = 0; j <= qi; ++j) {
+    float part = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) part = fmaf(qv[e], kb[(size_t)j * HD + lane + 64 * e], part);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
+    if (lane == j) my_t = part;
+    Mx = fmaxf(Mx, part);
+  }
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  float den = 0.f;
+  for (int c0 = 0; c0 < nchunks; c0 += 64) {
+    const int ch = c0 + lane;
+    float w = 0.f, wl = 0.f;
+    if (ch < nchunks) {
+      const float2 ml = *reinterpret_cast<const float2*>(mlpart + (ch * cstride + wid) * 2);
+      w = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - Mx);
+      wl = w * ml.y;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) wl += __shfl_xor(wl, off, 64);
+    den += wl;
+    // Every chunk wrote its partial (zeros where it saw no key), so the loads
+    // do not depend on the weights and can all be in flight.
+    const int cn = min(64, nchunks - c0);
+    int k = 0;
+    for (; k + 8 <= cn; k += 8) {
+      float v[8][E];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float* op = opart + ((size_t)(c0 + k + u) * cstride + wid) * HD;
+#pragma unroll
+        for (int e = 0; e < E; ++e) v[u][e] = op[lane + 64 * e];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float wk = __shfl(w, k + u, 64);
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] += wk * v[u][e];
+      }
+    }
+    for (; k < cn; ++k) {
+      const float wk = __shfl(w, k, 64);
+      const float* op = opart + ((size_t)(c0 + k) * cstride + wid) * HD;
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] += wk * op[lane + 64 * e];
+    }
+  }
+  for (int j = 0; j <= qi; ++j) {
+    const float p = __builtin_amdgcn_exp2f(__shfl(my_t, j, 64) - Mx);
+    den += p;
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] += p * vb[(size_t)j * HD + lane + 64 * e];
+  }
+  const float inv = 1.f / den;
+  const size_t plane = (size_t)max_rows * H * HD;
+  uint16_t* ob = reinterpret_cast<uint16_t*>(o);
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    uint16_t hb, lb;
+    split2(acc[e] * inv, hb, lb);
+    ob[(size_t)wid * HD + lane + 64 * e] = hb;
+    ob[plane + (size_t)wid * HD + lane + 64 * e] = lb;
   }
 }
 
@@ -488,43 +592,74 @@ __global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ q, c
 
 }  // namespace
 
-int attention_chunks(DType dt, int B, int n, int s, int H, int Hkv) {
-  if (dt != DType::BF16 || n == 0) return 1;
-  const int base = ((H / Hkv) * s + 63) / 64 * Hkv * B;
-  // Tiles of the smallest query tile.
-  const int min_tiles = (n + 63) / 64 + 1;
-  int chunks = 1;
+AttnPlan plan_attention(DType dt, int B, int n, int s, int H, int Hkv) {
+  AttnPlan p{1, 0, false};
+  if (dt != DType::BF16) return p;
+  const int G = H / Hkv;
+  const int n_ptiles = (n + 63) / 64;
+  // A branch with fewer than 64 query rows per KV head (G * s < 64, e.g. decode
+  // or short verify spans) would leave most of a 64-row tile empty and make every
+  // branch stream the prefix on its own: its rows are packed with other
+  // branches' into shared tiles that see only the prefix, and the short own span
+  // is merged in the combine.
+  p.cross = G * s < 64;
+  const int base = p.cross ? (B * s * G + 63) / 64 * Hkv : (G * s + 63) / 64 * Hkv * B;
+  const int min_tiles = p.cross ? n_ptiles : n_ptiles + 1;   // key tiles of the smallest query tile
+  if (p.cross && n == 0) {
+    p.chunks = 0;
+    return p;
+  }
   // Split the keys until the launch has about two workgroups per CU, keeping at
   // least 4 tiles per chunk (shorter chunks are all prologue and partial traffic).
-  while (base * chunks < 512 && (chunks + 1) * 4 <= min_tiles) ++chunks;
-  return chunks;
+  while (base * p.chunks < 512 && (p.chunks + 1) * 4 <= min_tiles) ++p.chunks;
+  p.partials = (p.cross || p.chunks > 1) ? p.chunks : 0;
+  return p;
 }
 
-hipError_t launch_attention(DType dt, const void* q, const void* pk, const void* pv, const void* k_own,
-                            const void* v_own, void* o, float* opart, float* mlpart, int nchunks, const Ctrl* c,
-                            int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st) {
+hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,
+                            const void* k_own, const void* v_own, void* o, float* opart, float* mlpart,
+                            const Ctrl* c, int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st) {
   if (dt == DType::BF16) {
     const float sl2 = 1.4426950408889634f / sqrtf((float)hd);
-    const dim3 grid(((H / Hkv) * s + 63) / 64, Hkv, max_branches * nchunks);
+    const int G = H / Hkv;
     const int max_rows = max_branches * s;
     const float* qq = static_cast<const float*>(q);
     const bf16 *kk = static_cast<const bf16*>(pk), *vv = static_cast<const bf16*>(pv);
     const float *ko = static_cast<const float*>(k_own), *vo = static_cast<const float*>(v_own);
     void* oo = o;
-    if (hd == 128)
-      hipLaunchKernelGGL(k_attn_bf16<128>, grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c, n, s, H,
-                         Hkv, sl2, nchunks, max_rows);
-    else
-      hipLaunchKernelGGL(k_attn_bf16<64>, grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c, n, s, H,
-                         Hkv, sl2, nchunks, max_rows);
-    if (nchunks > 1) {
-      const int waves = max_rows * H;
-      const dim3 cgrid((waves * 64 + 255) / 256);
+    const int waves = max_rows * H;
+    const dim3 cgrid((waves * 64 + 255) / 256);
+    if (p.cross) {
+      const dim3 grid((max_rows * G + 63) / 64, Hkv, p.chunks);
+      if (p.chunks > 0) {
+        if (hd == 128)
+          hipLaunchKernelGGL((k_attn_bf16<128, true>), grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
+                             c, n, s, H, Hkv, sl2, p.chunks, max_rows);
+        else
+          hipLaunchKernelGGL((k_attn_bf16<64, true>), grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
+                             c, n, s, H, Hkv, sl2, p.chunks, max_rows);
+      }
       if (hd == 128)
-        hipLaunchKernelGGL(k_attn_combine<128>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, nchunks,
+        hipLaunchKernelGGL(k_attn_combine_own<128>, cgrid, dim3(256), 0, st, opart, mlpart, qq, ko, vo, oo, c, s, H,
+                           Hkv, sl2, p.chunks, max_rows);
+      else
+        hipLaunchKernelGGL(k_attn_combine_own<64>, cgrid, dim3(256), 0, st, opart, mlpart, qq, ko, vo, oo, c, s, H,
+                           Hkv, sl2, p.chunks, max_rows);
+      return hipGetLastError();
+    }
+    const dim3 grid((G * s + 63) / 64, Hkv, max_branches * p.chunks);
+    if (hd == 128)
+      hipLaunchKernelGGL((k_attn_bf16<128, false>), grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
+                         n, s, H, Hkv, sl2, p.chunks, max_rows);
+    else
+      hipLaunchKernelGGL((k_attn_bf16<64, false>), grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
+                         n, s, H, Hkv, sl2, p.chunks, max_rows);
+    if (p.chunks > 1) {
+      if (hd == 128)
+        hipLaunchKernelGGL(k_attn_combine<128>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, p.chunks,
                            max_rows);
       else
-        hipLaunchKernelGGL(k_attn_combine<64>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, nchunks,
+        hipLaunchKernelGGL(k_attn_combine<64>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, p.chunks,
                            max_rows);
     }
   } else {

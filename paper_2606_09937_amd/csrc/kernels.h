@@ -66,12 +66,19 @@ hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* 
 
 // ---- attention over [shared prefix ; own causal span]: q, k_own, v_own fp32; prefix of the
 // model dtype; o is the projection input (bf16 hi/lo planes for BF16 models, fp32 otherwise).
-// With nchunks > 1 the prefix is split across workgroups (split-KV); opart
-// [nchunks, B*s, H, hd] and mlpart [nchunks, B*s, H, 2] hold the partials.
-int attention_chunks(DType dt, int B, int n, int s, int H, int Hkv);
-hipError_t launch_attention(DType dt, const void* q, const void* pk, const void* pv, const void* k_own,
-                            const void* v_own, void* o, float* opart, float* mlpart, int nchunks, const Ctrl* c,
-                            int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st);
+// Split-KV plan: `chunks` workgroups share the keys of a query tile and write
+// partials opart [partials, B*s, H, hd] and mlpart [partials, B*s, H, 2] that a
+// combine kernel merges. `cross`: branches with G*s < 64 query rows per KV head
+// are packed together into prefix-only tiles and their own spans are merged in
+// the combine.
+struct AttnPlan {
+  int chunks, partials;
+  bool cross;
+};
+AttnPlan plan_attention(DType dt, int B, int n, int s, int H, int Hkv);
+hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,
+                            const void* k_own, const void* v_own, void* o, float* opart, float* mlpart,
+                            const Ctrl* c, int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st);
 
 // ---- entropy of the live branches' last-token logits
 int entropy_parts(DType dt, int V, int max_branches);

@@ -42,7 +42,7 @@ struct Layout {
   size_t ctrl, x0, x1, act, ffn, q, kown, vown, pbig, pres, hn_a, hn_b, parts, rope, opart, mlpart, total;
   GemmPlan qkv, o, gu, down;
   int nparts;
-  int attn_chunks;
+  rksc::AttnPlan attn;
   int max_rows;
 };
 
@@ -112,8 +112,8 @@ rksc_status make_layout(const rksc_model_config* c, int B, int s, int n_prefix, 
   lay->hn_b = take((size_t)RKSC_MAX_BRANCHES * d * 2);
   lay->parts = take((size_t)lay->nparts * 64 * 3 * 4);
   lay->rope = take((size_t)s * (hd / 2) * 8);
-  lay->attn_chunks = rksc::attention_chunks(dt, B, n_prefix, s, H, Hkv);
-  const size_t nch = lay->attn_chunks > 1 ? (size_t)lay->attn_chunks : 0;
+  lay->attn = rksc::plan_attention(dt, B, n_prefix, s, H, Hkv);
+  const size_t nch = (size_t)lay->attn.partials;
   lay->opart = take(nch * Ms * H * hd * 4);
   lay->mlpart = take(nch * Ms * H * 2 * 4);
   lay->total = off;
@@ -250,8 +250,8 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     const void* pk = n > 0 ? pk_base + l * kv_layer : nullptr;
     const void* pv = n > 0 ? pv_base + l * kv_layer : nullptr;
     HIP_TRY(mark(l, 2));
-    HIP_TRY(rksc::launch_attention(dt, qb, pk, pv, kown, vown, act, opart, mlpart, lay.attn_chunks, ctrl, n, s, H,
-                                   Hkv, hd, B, strm));
+    HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, pk, pv, kown, vown, act, opart, mlpart, ctrl, n, s, H, Hkv, hd,
+                                   B, strm));
     HIP_TRY(mark(l, 3));
     HIP_TRY(mark(l, 4));
     HIP_TRY(rksc::launch_gemm(dt, lay.o, act, plane_lo(act, (size_t)M * H * hd), lw.w_o, pres, res_stride, ctrl, s,
@@ -340,8 +340,8 @@ RKSC_EXPORT rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void*
 RKSC_EXPORT size_t rksc_test_attention_scratch_size(int32_t dtype, int32_t B, int32_t n, int32_t s, int32_t H,
                                                    int32_t Hkv, int32_t hd) {
   if (B < 1 || s < 1 || n < 0 || H < 1 || Hkv < 1 || H % Hkv || hd < 1) return 0;
-  const int nch = rksc::attention_chunks(dtype == RKSC_BF16 ? DType::BF16 : DType::F32, B, n, s, H, Hkv);
-  return 4096 + (nch > 1 ? (size_t)nch * B * s * H * (hd + 2) * 4 : 0);
+  const rksc::AttnPlan p = rksc::plan_attention(dtype == RKSC_BF16 ? DType::BF16 : DType::F32, B, n, s, H, Hkv);
+  return 4096 + (size_t)p.partials * B * s * H * (hd + 2) * 4;
 }
 
 RKSC_EXPORT rksc_status rksc_test_attention(int32_t dtype, const void* q, const void* prefix_k, const void* prefix_v,
@@ -357,15 +357,15 @@ RKSC_EXPORT rksc_status rksc_test_attention(int32_t dtype, const void* q, const 
   hipStream_t st = static_cast<hipStream_t>(stream);
   rksc::Ctrl* ctrl = static_cast<rksc::Ctrl*>(scratch);
   const DType dt = dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
-  const int nch = rksc::attention_chunks(dt, B, n, s, H, Hkv);
-  const size_t need = 4096 + (nch > 1 ? (size_t)nch * B * s * H * (hd + 2) * 4 : 0);
+  const rksc::AttnPlan plan = rksc::plan_attention(dt, B, n, s, H, Hkv);
+  const size_t need = 4096 + (size_t)plan.partials * B * s * H * (hd + 2) * 4;
   if (scratch_bytes < need)
     return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "scratch has %zu bytes, needs %zu", scratch_bytes, need);
   char* sc = static_cast<char*>(scratch);
   float* opart = reinterpret_cast<float*>(sc + 4096);
-  float* mlpart = opart + (nch > 1 ? (size_t)nch * B * s * H * hd : 0);
+  float* mlpart = opart + (size_t)plan.partials * B * s * H * hd;
   HIP_TRY(rksc::launch_init(ctrl, B, 1, nullptr, nullptr, nullptr, 0, st));
-  HIP_TRY(rksc::launch_attention(dt, q, prefix_k, prefix_v, k_own, v_own, o, opart, mlpart, nch, ctrl, n, s, H, Hkv,
-                                 hd, B, st));
+  HIP_TRY(rksc::launch_attention(dt, plan, q, prefix_k, prefix_v, k_own, v_own, o, opart, mlpart, ctrl, n, s, H,
+                                 Hkv, hd, B, st));
   return ok();
 }

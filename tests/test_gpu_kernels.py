@@ -53,6 +53,9 @@ def test_gemm_matches_fp64(dtype, M, N, K, splits):
 @pytest.mark.parametrize("B,n,s,H,Hkv,hd", [
     (1, 0, 1, 4, 4, 64), (2, 37, 16, 8, 2, 64), (3, 130, 70, 28, 4, 128),
     (1, 1024, 128, 32, 8, 128), (2, 64, 200, 4, 4, 128), (4, 64, 16, 4, 4, 64),
+    # fewer than 64 query rows per branch and KV head: branches share prefix tiles
+    (5, 300, 1, 8, 2, 128), (3, 64, 3, 4, 4, 64), (8, 1000, 2, 32, 8, 128), (4, 0, 5, 8, 2, 64),
+    (2, 130, 15, 8, 2, 128), (32, 2100, 1, 32, 8, 128), (64, 64, 1, 4, 1, 64),
 ])
 def test_attention_matches_oracle(dtype, B, n, s, H, Hkv, hd):
     if dtype == torch.float32 and n * s * H > 1024 * 128 * 8:

@@ -151,7 +151,8 @@ def test_7b_single_full():
     _parity(mw, kv, toks, wl.tau, wl.patience, "7b_single")
 
 
-@pytest.mark.parametrize("name,layers", [("7b_tot", 2), ("7b_large_vocab", 2), ("10b_long", 2)])
+@pytest.mark.parametrize("name,layers", [("7b_tot", 2), ("7b_large_vocab", 2), ("10b_long", 2), ("10b_decode", 2),
+                                         ("7b_paper_verify", 2)])
 def test_large_shapes_sampled_branches(name, layers):
     """Full model width, branch count, prefix and span; first layers only; oracle on two branches."""
     wl = workloads.get(name)

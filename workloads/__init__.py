@@ -111,6 +111,18 @@ WORKLOADS = {
     "10b_long": Workload("10b_long", _B10, n_branches=32, prefix_len=16384, branch_len=256,
                          tau=0.02, patience=3, alpha=0.1,
                          description="48-layer 10B shape, vocab 256000, 32 branches, 16384-token prefix"),
+    # Supplemental points (not headline configs).
+    # One verify token per branch over the long prefix: the decode regime, in
+    # which the shared-prefix attention reads 67 MB of K/V per layer for only
+    # G * B = 128 query rows per KV head and is HBM-bound.
+    "10b_decode": Workload("10b_decode", _B10, n_branches=32, prefix_len=16384, branch_len=1,
+                           tau=0.02, patience=3, alpha=0.1,
+                           description="48-layer 10B shape, 32 branches x 1 token over a 16384-token prefix"),
+    # The paper's own verify shape on the large-vocab model: 8 branches x 128
+    # tokens over a 1024-token prefix.
+    "7b_paper_verify": Workload("7b_paper_verify", _Q7B, n_branches=8, prefix_len=1024, branch_len=128,
+                                tau=0.02, patience=2, alpha=0.1,
+                                description="28-layer 28Q/4KV shape, 8 branches x 128 tokens, 1024-token prefix"),
 }
 
 
