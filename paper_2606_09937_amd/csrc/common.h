@@ -116,6 +116,9 @@ struct EntStats {
 
 __device__ __forceinline__ EntStats ent_empty() { return {-INFINITY, 0.f, 0.f}; }
 
+// Compute units of an MI355X (8 XCDs x 32): the size of a one-wave-of-workgroups grid.
+constexpr int kComputeUnits = 256;
+
 // Merge of two statistic triples (associative up to rounding).
 __device__ __forceinline__ EntStats ent_merge(EntStats a, EntStats b) {
   if (b.m == -INFINITY) return a;

@@ -25,6 +25,9 @@ namespace rksc {
 
 namespace {
 
+constexpr int kAttnWaves = 8;    // waves per attention workgroup (16 query rows each)
+constexpr int kAttnRing = 4;     // prefix K/V tiles in the LDS ring
+
 // a if c, else zero; component-wise so that no address is selected (a select
 // of struct lvalues keeps register arrays in scratch memory).
 __device__ __forceinline__ uint4 keep_if(bool c, const uint4& a) {
@@ -43,47 +46,93 @@ __device__ __forceinline__ int vt_col(int dim, int key) {
   return pos ^ (((dim >> 3) & 7) << 3);
 }
 
+// Prefix K/V tiles are moved by DMA (global_load_lds) in their natural
+// [key][dim] layout into an R-slot LDS ring, several tiles ahead of the
+// contraction. The 16-byte chunks of a key row are XOR-swizzled by the key:
+// K by key & (CPR - 1), so that the 16 rows of a fragment read hit distinct
+// banks; V by (key & (CPR/2 - 1)) << 1, which keeps chunk pairs together for
+// the transposing reads. V^T fragments for O^T += V^T P^T come from
+// ds_read_b64_tr_b16: within each 16-lane group, result lane i, element t is
+// element (i mod 4) of source lane 4t + i/4, so a group whose lane j points at
+// dims 4(j mod 4)..+3 of key k0 + j/4 receives dim i of keys k0..k0+3.
+__device__ __forceinline__ int swz_k(int key, int cpr) { return key & (cpr - 1); }
+__device__ __forceinline__ int swz_v(int key, int cpr) { return (key & (cpr / 2 - 1)) << 1; }
+
+// The transposing reads are issued as inline assembly: the compiler cannot
+// tell that the builtin's LDS read does not alias the ring's in-flight DMA
+// writes and would drain the whole ring (vmcnt(0)) before every such read. The
+// kernel's own wait + barrier already guarantee that the tile has landed; the
+// results are made valid by an explicit lgkmcnt(0) that takes the fragments as
+// operands, so no use of them can be scheduled before it.
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+template <int OFF>
+__device__ __forceinline__ void lds_read_tr16_pair(uint32_t addr, shortx4& a, shortx4& b) {
+  // Early-clobber outputs: the first read's destination must not share a
+  // register with the address that the second read still uses.
+  asm volatile("ds_read_b64_tr_b16 %0, %2\n\tds_read_b64_tr_b16 %1, %2 offset:%3"
+               : "=&v"(a), "=&v"(b)
+               : "v"(addr), "i"(OFF));
+}
+template <int ND>
+__device__ __forceinline__ void lds_wait_pairs(shortx4 (&a)[ND], shortx4 (&b)[ND]) {
+  static_assert(ND == 4 || ND == 8, "head_dim 64 or 128");
+  if constexpr (ND == 8)
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(a[0]), "+v"(b[0]), "+v"(a[1]), "+v"(b[1]), "+v"(a[2]), "+v"(b[2]), "+v"(a[3]), "+v"(b[3]),
+                   "+v"(a[4]), "+v"(b[4]), "+v"(a[5]), "+v"(b[5]), "+v"(a[6]), "+v"(b[6]), "+v"(a[7]), "+v"(b[7]));
+  else
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(a[0]), "+v"(b[0]), "+v"(a[1]), "+v"(b[1]), "+v"(a[2]), "+v"(b[2]), "+v"(a[3]), "+v"(b[3]));
+}
+
 // Split-KV: the key tiles of a query tile -- the prefix tiles, then the own-span
 // tiles up to its last query -- are divided evenly over `nchunks` workgroups,
-// each writing an unnormalised partial output with its (max, sum) for
-// k_attn_combine. (A merge by the last chunk to finish, found with an atomic
-// ticket, needs device-scope release fences; on MI355X those write back the
-// whole L2 and cost far more than the separate combine launch.)
-// Tile loads are software-pipelined: the next tile's K/V (own-span tiles: K)
-// are fetched into registers while the current tile is contracted; the masking
-// and the hi/lo split happen when they are stored to LDS. The contraction is
-// instantiated per tile kind (full prefix tile, last partial prefix tile,
-// own-span tile), so the MFMA sequences carry no branches and full prefix
-// tiles no masking.
+// each writing an unnormalised partial output with its (max, sum) for the
+// combine. (A merge by the last chunk to finish, found with an atomic ticket,
+// needs device-scope release fences; on MI355X those write back the whole L2
+// and cost far more than the separate combine launch.)
+// Own-span tiles (fp32 keys/values of the branch itself) are staged through
+// registers, split into bf16 hi/lo and stored to padded LDS tiles that reuse
+// the ring's memory once the prefix tiles of the chunk are done; the next own
+// tile is fetched while the current one is contracted.
+// The contraction is instantiated per tile kind (full prefix tile, last
+// partial prefix tile, own-span tile), so the MFMA sequences carry no branches
+// and full prefix tiles no masking.
 // Scores are formed in log2 units: the queries are pre-multiplied by
 // log2(e)/sqrt(hd) before their hi/lo split, and the partial maxima in mlpart
 // are in the same units.
+// 8 waves x 16 query columns = 128 query rows per workgroup.
 template <int HD, bool XB>
-__global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ q, const bf16* __restrict__ pk,
+__global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, const bf16* __restrict__ pk,
                                                    const bf16* __restrict__ pv, const float* __restrict__ ko,
                                                    const float* __restrict__ vo, void* __restrict__ o,
                                                    float* __restrict__ opart, float* __restrict__ mlpart,
                                                    const Ctrl* c, int n, int s, int H, int Hkv, float sl2,
                                                    int nchunks, int max_rows) {
-  constexpr int KT = 64;          // keys per tile
-  constexpr int LDK = HD + 8;     // K tile row stride (elements)
-  constexpr int LDV = KT + 8;     // V^T row stride (elements)
-  constexpr int NC = HD / 32;     // 32-dim chunks of the QK^T contraction
-  constexpr int ND = HD / 16;     // 16-dim tiles of the output
-  // Register staging per thread: prefix tile (bf16) K in 16-byte row chunks and
-  // V in units of 4 keys x 8 dimensions; own-span tile (fp32) K in 16-byte
-  // chunks (4 dimensions); own-span V goes in units of 4 keys x 4 dimensions.
-  constexpr int PK = KT * HD / 8 / 256;                  // K chunks per thread, prefix
-  constexpr int PVU = (KT * HD / 32 + 255) / 256;        // V units per thread, prefix
-  constexpr int OK = KT * HD / 4 / 256;                  // K chunks per thread, own span
-  constexpr int OVU = (KT * HD / 16 + 255) / 256;        // V units per thread, own span
-  // Own-span V is loaded when the tile is stored (2 of the ~n/64 + 2 tiles), which
-  // keeps the staging at 8 registers x 16 B.
-  constexpr int NSTAGE = (PK + 4 * PVU) > OK ? (PK + 4 * PVU) : OK;
-  static_assert(KT * HD / 8 % 256 == 0 && KT * HD / 4 % 256 == 0, "tile staging assumes 256 threads");
-  // [0]: the prefix tile (exact bf16) or the hi part of an own-span tile; [1]: its lo part.
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][HD * LDV];
+  constexpr int NW = kAttnWaves, NT = NW * 64, QT = 16 * NW;
+  constexpr int KT = 64;                   // keys per tile
+  constexpr int CPR = HD / 8;              // 16-byte chunks per key row
+  constexpr int ROW = HD * 2;              // bytes per key row
+  constexpr int TB = KT * ROW;             // bytes of a K (or V) tile
+  constexpr int SLOT = 2 * TB;             // ring slot: K tile, then V tile
+  constexpr int R = kAttnRing;
+  constexpr int IPT = SLOT / 1024;         // 1 KB DMA instructions per tile
+  static_assert(IPT % NW == 0, "every wave issues the same number of DMA instructions");
+  constexpr int IPW = IPT / NW;
+  constexpr int RPI = 1024 / ROW;          // key rows per DMA instruction
+  constexpr int LDK = HD + 8;              // own-span K tile row stride (elements)
+  constexpr int LDV = KT + 8;              // own-span V^T row stride (elements)
+  constexpr int NC = HD / 32;              // 32-dim chunks of the QK^T contraction
+  constexpr int ND = HD / 16;              // 16-dim tiles of the output
+  constexpr int OK = KT * HD / 4 / NT;     // own-span K: 16-byte chunks (4 fp32) per thread
+  constexpr int OVU = (KT * HD / 16 + NT - 1) / NT;   // own-span V: units of 4 keys x 4 dims
+  static_assert(OK >= 1 && KT * HD / 4 % NT == 0, "own-span staging");
+  static_assert((2 * KT * LDK + 2 * HD * LDV) * 2 <= R * SLOT, "own-span tiles fit in the ring");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[R * SLOT];
+  uint16_t* const Ks0 = reinterpret_cast<uint16_t*>(smem);   // own span: K hi [KT][LDK]
+  uint16_t* const Ks1 = Ks0 + KT * LDK;                        //            K lo
+  uint16_t* const Vt0 = Ks1 + KT * LDK;                        //            V^T hi [HD][LDV]
+  uint16_t* const Vt1 = Vt0 + HD * LDV;                        //            V^T lo
 
   // Fused mode: blockIdx.z = chunk * slots + slot, rows of one branch.
   // XB mode: blockIdx.z = chunk, rows of all live branches, prefix tiles only.
@@ -94,12 +143,12 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
   const int kvh = blockIdx.y;
   const int G = H / Hkv;
   const int rows = XB ? c->live_count * s * G : G * s;
-  const int row0 = blockIdx.x * 64;
+  const int row0 = blockIdx.x * QT;
   if (row0 >= rows) return;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
 
-  const int i_max = min(s - 1, (min(row0 + 63, rows - 1)) / G);
+  const int i_max = min(s - 1, (min(row0 + QT - 1, rows - 1)) / G);
   const int n_ptiles = (n + KT - 1) / KT;
   const int n_full = n / KT;      // prefix tiles with no key past n - 1
   const int n_tiles = XB ? n_ptiles : n_ptiles + i_max / KT + 1;
@@ -139,89 +188,71 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
   const float* Ko = ko + ((size_t)slot * Hkv + kvh) * s * HD;
   const float* Vo = vo + ((size_t)slot * Hkv + kvh) * s * HD;
 
-  // Fetch of tile t into registers (addresses clamped in bounds; out-of-range
-  // keys are zeroed when stored).
-  uint4 stg[NSTAGE];
-  auto fetch = [&](int t) {
-    if (t < n_ptiles) {
-      const int kbase = t * KT;
-      const bf16* kt = Kp + (size_t)kbase * HD;
-      const bf16* vt = Vp + (size_t)kbase * HD;
-      const int kmax = n - 1 - kbase;   // last valid key of the tile
+  // ---- prefix DMA: instruction ins = j * NW + wid of a tile moves RPI key rows
+  // of K (ins < IPT/2) or V; lane L fills physical chunk L % CPR of row L / CPR.
+  int dkey[IPW], dsrc[IPW], ddst[IPW];
+  bool dv[IPW];
 #pragma unroll
-      for (int j = 0; j < PK; ++j) {
-        const int idx = tid + 256 * j, key = idx / (HD / 8), dc = idx % (HD / 8);
-        stg[j] = ldg16(kt + (key <= kmax ? key : kmax) * HD + dc * 8);
-      }
+  for (int j = 0; j < IPW; ++j) {
+    const int ins = j * NW + wid;
+    dv[j] = ins >= IPT / 2;
+    const int i_in = dv[j] ? ins - IPT / 2 : ins;
+    const int key = i_in * RPI + lane / CPR;
+    const int ph = lane % CPR;
+    const int lc = ph ^ (dv[j] ? swz_v(key, CPR) : swz_k(key, CPR));
+    dkey[j] = key;
+    dsrc[j] = lc * 8;
+    ddst[j] = (dv[j] ? TB : 0) + i_in * 1024;
+  }
+  // Transposing V reads: this lane points at key 4g + r16/4 of each 32-key
+  // block (and 16 keys further, an immediate offset), dims 16dt + 4 (r16 % 4)
+  // .. +3, i.e. logical 16-byte chunk 2dt + (r16 % 4)/2, half r16 % 2; with the
+  // V swizzle 2m, m = key & (CPR/2 - 1) (the same for key + 16 and key + 32),
+  // the physical chunk is 2 (dt ^ m) + (r16 % 4)/2.
+  uint32_t voff[ND];
+  {
+    const int vk = 4 * g + (r16 >> 2);
+    const int mv = swz_v(vk, CPR) >> 1;
 #pragma unroll
-      for (int u = 0; u < PVU; ++u) {
-        const int idx = tid + 256 * u;
-        const int dc = idx % (HD / 8), kg = (idx < KT * HD / 32 ? idx : 0) / (HD / 8);
+    for (int dt = 0; dt < ND; ++dt)
+      voff[dt] = vk * ROW + 32 * (dt ^ mv) + 16 * ((r16 & 3) >> 1) + 8 * (r16 & 1);
+  }
+  const uint32_t smem_lds = (uint32_t)reinterpret_cast<uintptr_t>(smem);   // LDS byte offset of the ring
+
+  auto issue = [&](int pt, int sl) {
+    const int kbase = pt * KT;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = 4 * kg + e;
-          stg[PK + 4 * u + e] = ldg16(vt + (key <= kmax ? key : kmax) * HD + dc * 8);
-        }
-      }
-    } else {
-      const int kbase = (t - n_ptiles) * KT;
-      const float* kt = Ko + (size_t)kbase * HD;
-      const int kmax = s - 1 - kbase;
-#pragma unroll
-      for (int j = 0; j < OK; ++j) {
-        const int idx = tid + 256 * j, key = idx / (HD / 4), dq = idx % (HD / 4);
-        stg[j] = ldg16(kt + (key <= kmax ? key : kmax) * HD + dq * 4);
-      }
+    for (int j = 0; j < IPW; ++j) {
+      const int key = min(kbase + dkey[j], n - 1);   // rows past n - 1 are masked in the contraction
+      const bf16* src = (dv[j] ? Vp : Kp) + (size_t)key * HD + dsrc[j];
+      dma16(src, smem + sl * SLOT + ddst[j]);
     }
   };
-  // Store of a fetched prefix tile to LDS (K rows and V^T); PARTIAL zeroes the
-  // keys past n - 1.
-  auto store_prefix = [&](auto partial, int kbase) {
-    constexpr bool PARTIAL = decltype(partial)::value;
+
+  // ---- own-span staging (fused mode)
+  uint4 stg[OK];
+  auto fetch_own = [&](int kbase) {
+    const float* kt = Ko + (size_t)kbase * HD;
+    const int kmax = s - 1 - kbase;
 #pragma unroll
-    for (int j = 0; j < PK; ++j) {
-      const int idx = tid + 256 * j, key = idx / (HD / 8), dc = idx % (HD / 8);
-      *reinterpret_cast<uint4*>(&Ks[0][key * LDK + dc * 8]) = PARTIAL ? keep_if(kbase + key < n, stg[j]) : stg[j];
-    }
-#pragma unroll
-    for (int u = 0; u < PVU; ++u) {
-      const int idx = tid + 256 * u;
-      if (idx < KT * HD / 32) {
-        const int dc = idx % (HD / 8), kg = idx / (HD / 8);
-        uint32_t w[4][4];   // w[e][j]: word j (elements 2j, 2j+1) of key 4kg + e
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const uint4 v = PARTIAL ? keep_if(kbase + 4 * kg + e < n, stg[PK + 4 * u + e]) : stg[PK + 4 * u + e];
-          w[e][0] = v.x; w[e][1] = v.y; w[e][2] = v.z; w[e][3] = v.w;
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          // elements 2j (low halves) and 2j+1 (high halves) of the four keys
-          const uint32_t lo01 = (w[0][j] & 0xffffu) | (w[1][j] << 16);
-          const uint32_t lo23 = (w[2][j] & 0xffffu) | (w[3][j] << 16);
-          const uint32_t hi01 = (w[0][j] >> 16) | (w[1][j] & 0xffff0000u);
-          const uint32_t hi23 = (w[2][j] >> 16) | (w[3][j] & 0xffff0000u);
-          const int d0 = dc * 8 + 2 * j, d1 = d0 + 1;
-          *reinterpret_cast<uint2*>(&Vt[0][d0 * LDV + vt_col(d0, 4 * kg)]) = make_uint2(lo01, lo23);
-          *reinterpret_cast<uint2*>(&Vt[0][d1 * LDV + vt_col(d1, 4 * kg)]) = make_uint2(hi01, hi23);
-        }
-      }
+    for (int j = 0; j < OK; ++j) {
+      const int idx = tid + NT * j, key = idx / (HD / 4), dq = idx % (HD / 4);
+      stg[j] = ldg16(kt + (key <= kmax ? key : kmax) * HD + dq * 4);
     }
   };
-  // Store of a fetched own-span tile: K and V split into hi/lo; keys past s - 1 zeroed.
   auto store_own = [&](int kbase) {
 #pragma unroll
     for (int j = 0; j < OK; ++j) {
-      const int idx = tid + 256 * j, key = idx / (HD / 4), dq = idx % (HD / 4);
+      const int idx = tid + NT * j, key = idx / (HD / 4), dq = idx % (HD / 4);
       const float4 kf = __builtin_bit_cast(float4, keep_if(kbase + key < s, stg[j]));
       uint16_t kh[4], kl[4];
       split2(kf.x, kh[0], kl[0]); split2(kf.y, kh[1], kl[1]); split2(kf.z, kh[2], kl[2]); split2(kf.w, kh[3], kl[3]);
-      *reinterpret_cast<uint2*>(&Ks[0][key * LDK + dq * 4]) = make_uint2(pack2(kh[0], kh[1]), pack2(kh[2], kh[3]));
-      *reinterpret_cast<uint2*>(&Ks[1][key * LDK + dq * 4]) = make_uint2(pack2(kl[0], kl[1]), pack2(kl[2], kl[3]));
+      *reinterpret_cast<uint2*>(&Ks0[key * LDK + dq * 4]) = make_uint2(pack2(kh[0], kh[1]), pack2(kh[2], kh[3]));
+      *reinterpret_cast<uint2*>(&Ks1[key * LDK + dq * 4]) = make_uint2(pack2(kl[0], kl[1]), pack2(kl[2], kl[3]));
     }
 #pragma unroll
     for (int u = 0; u < OVU; ++u) {
-      const int idx = tid + 256 * u;
+      const int idx = tid + NT * u;
       if (idx < KT * HD / 16) {
         const int dq = idx % (HD / 4), kg = idx / (HD / 4);
         float x[4][4];   // x[e][k]: dimension 4dq + k of key 4kg + e
@@ -242,34 +273,41 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
 #pragma unroll
           for (int e = 0; e < 4; ++e) split2(x[e][k], hh[e], lw[e]);
           const int col = vt_col(dim, 4 * kg);
-          *reinterpret_cast<uint2*>(&Vt[0][dim * LDV + col]) = make_uint2(pack2(hh[0], hh[1]), pack2(hh[2], hh[3]));
-          *reinterpret_cast<uint2*>(&Vt[1][dim * LDV + col]) = make_uint2(pack2(lw[0], lw[1]), pack2(lw[2], lw[3]));
+          *reinterpret_cast<uint2*>(&Vt0[dim * LDV + col]) = make_uint2(pack2(hh[0], hh[1]), pack2(hh[2], hh[3]));
+          *reinterpret_cast<uint2*>(&Vt1[dim * LDV + col]) = make_uint2(pack2(lw[0], lw[1]), pack2(lw[2], lw[3]));
         }
       }
     }
   };
 
-  // Contraction of the tile in LDS with this lane's query: S^T = K Q^T, online
-  // softmax in log2 units, O^T += V^T P^T. OWN: the keys and values are hi/lo
-  // pairs (three MFMAs per product) and the causal mask applies; MASKED: some
-  // keys of the tile are invalid for some query.
-  auto contract = [&](auto own_c, auto masked_c, int kbase) {
+  // Contraction of one tile with this lane's query: S^T = K Q^T, online softmax
+  // in log2 units, O^T += V^T P^T. OWN: a padded own-span tile whose keys and
+  // values are hi/lo pairs (three MFMAs per product), causal mask; otherwise the
+  // prefix tile in ring slot `sl`. MASKED: some keys of the tile are invalid for
+  // some query.
+  auto contract = [&](auto own_c, auto masked_c, int sl, int kbase) {
     constexpr bool OWN = decltype(own_c)::value;
     constexpr bool MASKED = decltype(masked_c)::value;
+    const uint8_t* Kt = smem + sl * SLOT;
     // S^T: lane holds scores of keys 16*kt + 4g + i for its query.
     floatx4 sc[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
       sc[kt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      const int key = 16 * kt + r16;
 #pragma unroll
       for (int cc = 0; cc < NC; ++cc) {
-        const int off = (16 * kt + r16) * LDK + 32 * cc + 8 * g;
-        const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&Ks[0][off]);
-        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qh[cc], sc[kt], 0, 0, 0);
-        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, ql[cc], sc[kt], 0, 0, 0);
         if constexpr (OWN) {
-          const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&Ks[1][off]);
+          const int off = key * LDK + 32 * cc + 8 * g;
+          const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&Ks0[off]);
+          const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&Ks1[off]);
+          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qh[cc], sc[kt], 0, 0, 0);
+          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, ql[cc], sc[kt], 0, 0, 0);
           sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qh[cc], sc[kt], 0, 0, 0);
+        } else {
+          const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(Kt + key * ROW + ((4 * cc + g) ^ swz_k(key, CPR)) * 16);
+          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qh[cc], sc[kt], 0, 0, 0);
+          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, ql[cc], sc[kt], 0, 0, 0);
         }
       }
     }
@@ -322,32 +360,68 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const float* __restrict__ 
                                                                pack2(ph[4], ph[5]), pack2(ph[6], ph[7])));
       const bf16x8 pbl = __builtin_bit_cast(bf16x8, make_uint4(pack2(pl[0], pl[1]), pack2(pl[2], pl[3]),
                                                                pack2(pl[4], pl[5]), pack2(pl[6], pl[7])));
+      shortx4 vlo[ND], vhi[ND];
+      if constexpr (!OWN) {
+        const uint32_t vb = smem_lds + sl * SLOT + TB + kb * 32 * ROW;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) lds_read_tr16_pair<16 * ROW>(vb + voff[dt], vlo[dt], vhi[dt]);
+        lds_wait_pairs<ND>(vlo, vhi);
+      }
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt) {
-        const int dim = 16 * dt + r16;
-        const int off = dim * LDV + vt_col(dim, 32 * kb + 4 * g);
-        const bf16x8 v0 = *reinterpret_cast<const bf16x8*>(&Vt[0][off]);
+        bf16x8 v0;
+        if constexpr (OWN) {
+          const int dim = 16 * dt + r16;
+          v0 = *reinterpret_cast<const bf16x8*>(&Vt0[dim * LDV + vt_col(dim, 32 * kb + 4 * g)]);
+        } else {
+          v0 = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vlo[dt], vhi[dt], 0, 1, 2, 3, 4, 5, 6, 7));
+        }
         oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, pbh, oacc[dt], 0, 0, 0);
         oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, pbl, oacc[dt], 0, 0, 0);
         if constexpr (OWN) {
-          const bf16x8 v1 = *reinterpret_cast<const bf16x8*>(&Vt[1][off]);
+          const int dim = 16 * dt + r16;
+          const bf16x8 v1 = *reinterpret_cast<const bf16x8*>(&Vt1[dim * LDV + vt_col(dim, 32 * kb + 4 * g)]);
           oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, pbh, oacc[dt], 0, 0, 0);
         }
       }
     }
   };
 
-  if (t_begin < t_end) fetch(t_begin);
-  for (int t = t_begin; t < t_end; ++t) {
-    if (t < n_full) store_prefix(std::false_type{}, t * KT);
-    else if (t < n_ptiles) store_prefix(std::true_type{}, t * KT);
-    else store_own((t - n_ptiles) * KT);
+  // ---- prefix tiles of this chunk through the ring. Every step issues one
+  // tile (past the end: a harmless re-fetch of the first), so the number of
+  // DMA instructions behind the tile being waited for is always IPW * (R - 2).
+  const int p_end = min(t_end, n_ptiles);
+  const int np = p_end - t_begin;
+  if (np > 0) {
+#pragma unroll
+    for (int u = 0; u < R - 1; ++u) issue(t_begin + (u < np ? u : 0), u);
+    for (int i = 0; i < np; ++i) {
+      wait_vmcnt_lds<IPW * (R - 2)>();
+      __builtin_amdgcn_s_barrier();
+      const int nx = i + R - 1;
+      issue(t_begin + (nx < np ? nx : 0), nx % R);
+      const int pt = t_begin + i;
+      if (pt < n_full) contract(std::false_type{}, std::false_type{}, i % R, pt * KT);
+      else contract(std::false_type{}, std::true_type{}, i % R, pt * KT);
+    }
+    // The trailing re-fetches must land before the ring memory is reused or the
+    // workgroup ends.
+    wait_vmcnt<0>();
     __syncthreads();
-    if (t + 1 < t_end) fetch(t + 1);   // in flight while this tile is contracted
-    if (t < n_full) contract(std::false_type{}, std::false_type{}, t * KT);
-    else if (t < n_ptiles) contract(std::false_type{}, std::true_type{}, t * KT);
-    else contract(std::true_type{}, std::true_type{}, (t - n_ptiles) * KT);
-    __syncthreads();
+  }
+
+  // ---- own-span tiles of this chunk (fused mode)
+  const int o_begin = max(t_begin, n_ptiles);
+  if (!XB && o_begin < t_end) {
+    fetch_own((o_begin - n_ptiles) * KT);
+    for (int t = o_begin; t < t_end; ++t) {
+      const int kbase = (t - n_ptiles) * KT;
+      store_own(kbase);
+      __syncthreads();
+      if (t + 1 < t_end) fetch_own(kbase + KT);   // in flight while this tile is contracted
+      contract(std::true_type{}, std::true_type{}, 0, kbase);
+      __syncthreads();
+    }
   }
 
   l += __shfl_xor(l, 16, 64);
@@ -603,15 +677,16 @@ AttnPlan plan_attention(DType dt, int B, int n, int s, int H, int Hkv) {
   // branches' into shared tiles that see only the prefix, and the short own span
   // is merged in the combine.
   p.cross = G * s < 64;
-  const int base = p.cross ? (B * s * G + 63) / 64 * Hkv : (G * s + 63) / 64 * Hkv * B;
+  constexpr int QT = 16 * kAttnWaves;   // query rows per workgroup
+  const int base = p.cross ? (B * s * G + QT - 1) / QT * Hkv : (G * s + QT - 1) / QT * Hkv * B;
   const int min_tiles = p.cross ? n_ptiles : n_ptiles + 1;   // key tiles of the smallest query tile
   if (p.cross && n == 0) {
     p.chunks = 0;
     return p;
   }
-  // Split the keys until the launch has about two workgroups per CU, keeping at
-  // least 4 tiles per chunk (shorter chunks are all prologue and partial traffic).
-  while (base * p.chunks < 512 && (p.chunks + 1) * 4 <= min_tiles) ++p.chunks;
+  // Split the keys until the launch has a workgroup per CU (one fits per CU),
+  // keeping at least 2 tiles per chunk.
+  while (base * p.chunks < kComputeUnits && (p.chunks + 1) * 2 <= min_tiles) ++p.chunks;
   p.partials = (p.cross || p.chunks > 1) ? p.chunks : 0;
   return p;
 }
@@ -630,13 +705,13 @@ hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const vo
     const int waves = max_rows * H;
     const dim3 cgrid((waves * 64 + 255) / 256);
     if (p.cross) {
-      const dim3 grid((max_rows * G + 63) / 64, Hkv, p.chunks);
+      const dim3 grid((max_rows * G + 16 * kAttnWaves - 1) / (16 * kAttnWaves), Hkv, p.chunks);
       if (p.chunks > 0) {
         if (hd == 128)
-          hipLaunchKernelGGL((k_attn_bf16<128, true>), grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
+          hipLaunchKernelGGL((k_attn_bf16<128, true>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
                              c, n, s, H, Hkv, sl2, p.chunks, max_rows);
         else
-          hipLaunchKernelGGL((k_attn_bf16<64, true>), grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
+          hipLaunchKernelGGL((k_attn_bf16<64, true>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
                              c, n, s, H, Hkv, sl2, p.chunks, max_rows);
       }
       if (hd == 128)
@@ -647,12 +722,12 @@ hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const vo
                            Hkv, sl2, p.chunks, max_rows);
       return hipGetLastError();
     }
-    const dim3 grid((G * s + 63) / 64, Hkv, max_branches * p.chunks);
+    const dim3 grid((G * s + 16 * kAttnWaves - 1) / (16 * kAttnWaves), Hkv, max_branches * p.chunks);
     if (hd == 128)
-      hipLaunchKernelGGL((k_attn_bf16<128, false>), grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
+      hipLaunchKernelGGL((k_attn_bf16<128, false>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
                          n, s, H, Hkv, sl2, p.chunks, max_rows);
     else
-      hipLaunchKernelGGL((k_attn_bf16<64, false>), grid, dim3(256), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
+      hipLaunchKernelGGL((k_attn_bf16<64, false>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
                          n, s, H, Hkv, sl2, p.chunks, max_rows);
     if (p.chunks > 1) {
       if (hd == 128)

@@ -308,9 +308,7 @@ __global__ __launch_bounds__(256) void k_entropy_f32(const float* __restrict__ W
 }
 
 // Persistent grid: one 8-wave workgroup (146 KB of LDS: a 7-unit ring keeps
-// 96 KB of the stream in flight) per compute unit on MI355X's 256 compute
-// units.
-constexpr int kComputeUnits = 256;
+// 96 KB of the stream in flight) per compute unit (kComputeUnits).
 
 int ent_ncb(int max_branches) { return max_branches <= 16 ? 1 : max_branches <= 32 ? 2 : 4; }
 

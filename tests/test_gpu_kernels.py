@@ -56,6 +56,9 @@ def test_gemm_matches_fp64(dtype, M, N, K, splits):
     # fewer than 64 query rows per branch and KV head: branches share prefix tiles
     (5, 300, 1, 8, 2, 128), (3, 64, 3, 4, 4, 64), (8, 1000, 2, 32, 8, 128), (4, 0, 5, 8, 2, 64),
     (2, 130, 15, 8, 2, 128), (32, 2100, 1, 32, 8, 128), (64, 64, 1, 4, 1, 64),
+    # full-size decode and long-prefix verify tiles: many prefix tiles per chunk
+    # stream through the LDS ring (slots reused while others are in flight)
+    (32, 16384, 1, 32, 8, 128), (4, 16384, 32, 32, 8, 128), (64, 1024, 32, 8, 2, 128),
 ])
 def test_attention_matches_oracle(dtype, B, n, s, H, Hkv, hd):
     if dtype == torch.float32 and n * s * H > 1024 * 128 * 8:
