@@ -69,6 +69,17 @@ __device__ __forceinline__ void split2(float x, uint16_t& hi, uint16_t& lo) {
   lo = __builtin_bit_cast(uint16_t, static_cast<__bf16>(x - static_cast<float>(h)));
 }
 
+// split2 of two values at once, packed: hi2 = (bf16(x1) << 16) | bf16(x0), lo2
+// likewise for the residuals (one v_cvt_pk_bf16_f32 each).
+__device__ __forceinline__ void split2x2(float x0, float x1, uint32_t& hi2, uint32_t& lo2) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float floatx2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t h = __builtin_convertvector(floatx2_t{x0, x1}, bf16x2_t);
+  hi2 = __builtin_bit_cast(uint32_t, h);
+  const float h0 = __uint_as_float(hi2 << 16), h1 = __uint_as_float(hi2 & 0xffff0000u);
+  lo2 = __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2_t{x0 - h0, x1 - h1}, bf16x2_t));
+}
+
 __device__ __forceinline__ uint32_t pack2(uint16_t a, uint16_t b) {
   return static_cast<uint32_t>(a) | (static_cast<uint32_t>(b) << 16);
 }

@@ -280,17 +280,17 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     }
   };
 
-  // Contraction of one tile with this lane's query: S^T = K Q^T, online softmax
-  // in log2 units, O^T += V^T P^T. OWN: a padded own-span tile whose keys and
-  // values are hi/lo pairs (three MFMAs per product), causal mask; otherwise the
-  // prefix tile in ring slot `sl`. MASKED: some keys of the tile are invalid for
-  // some query.
-  auto contract = [&](auto own_c, auto masked_c, int sl, int kbase) {
+  // Contraction of one tile with this lane's query, in two parts so that the
+  // prefix loop can overlap them across tiles:
+  // - scores: S^T = K Q^T (lane holds the scores of keys 16*kt + 4g + i of its
+  //   query);
+  // - softmax_pv: online softmax in log2 units, then O^T += V^T P^T.
+  // OWN: a padded own-span tile whose keys and values are hi/lo pairs (three
+  // MFMAs per product), causal mask; otherwise the prefix tile in ring slot
+  // `sl`. MASKED: some keys of the tile are invalid for some query.
+  auto scores = [&](auto own_c, int sl, floatx4 (&sc)[4]) {
     constexpr bool OWN = decltype(own_c)::value;
-    constexpr bool MASKED = decltype(masked_c)::value;
     const uint8_t* Kt = smem + sl * SLOT;
-    // S^T: lane holds scores of keys 16*kt + 4g + i for its query.
-    floatx4 sc[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
       sc[kt] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -311,6 +311,10 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
         }
       }
     }
+  };
+  auto softmax_pv = [&](auto own_c, auto masked_c, int sl, int kbase, floatx4 (&sc)[4]) {
+    constexpr bool OWN = decltype(own_c)::value;
+    constexpr bool MASKED = decltype(masked_c)::value;
     if constexpr (MASKED) {
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
@@ -332,12 +336,10 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m - mn);   // m = -inf gives 0
     const float msub = none ? 0.f : mn;
     m = mn;
-    // Rescale only when some query's maximum moved (rare after the first tiles).
-    if (__ballot(alpha != 1.f)) {
-      l *= alpha;
+    // Branch-free rescale, so the whole contraction stays one scheduling region.
+    l *= alpha;
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) oacc[dt] *= alpha;
-    }
+    for (int dt = 0; dt < ND; ++dt) oacc[dt] *= alpha;
     float p[4][4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
@@ -350,16 +352,16 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     // {32kb + 4g + e, 32kb + 16 + 4g + e}, e = 0..3, in both operands.
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      uint16_t ph[8], pl[8];
+      // hi/lo split of the probabilities, two at a time: hi = bf16(p) packed
+      // by one conversion, lo = bf16(p - hi) likewise.
+      uint32_t ph[4], pl[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        split2(p[2 * kb][e], ph[e], pl[e]);
-        split2(p[2 * kb + 1][e], ph[4 + e], pl[4 + e]);
+      for (int e2 = 0; e2 < 4; ++e2) {
+        const float p0 = p[2 * kb + (e2 >> 1)][2 * (e2 & 1)], p1 = p[2 * kb + (e2 >> 1)][2 * (e2 & 1) + 1];
+        split2x2(p0, p1, ph[e2], pl[e2]);
       }
-      const bf16x8 pbh = __builtin_bit_cast(bf16x8, make_uint4(pack2(ph[0], ph[1]), pack2(ph[2], ph[3]),
-                                                               pack2(ph[4], ph[5]), pack2(ph[6], ph[7])));
-      const bf16x8 pbl = __builtin_bit_cast(bf16x8, make_uint4(pack2(pl[0], pl[1]), pack2(pl[2], pl[3]),
-                                                               pack2(pl[4], pl[5]), pack2(pl[6], pl[7])));
+      const bf16x8 pbh = __builtin_bit_cast(bf16x8, make_uint4(ph[0], ph[1], ph[2], ph[3]));
+      const bf16x8 pbl = __builtin_bit_cast(bf16x8, make_uint4(pl[0], pl[1], pl[2], pl[3]));
       shortx4 vlo[ND], vhi[ND];
       if constexpr (!OWN) {
         const uint32_t vb = smem_lds + sl * SLOT + TB + kb * 32 * ROW;
@@ -386,24 +388,43 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
       }
     }
   };
+  auto contract = [&](auto own_c, auto masked_c, int sl, int kbase) {
+    floatx4 sc[4];
+    scores(own_c, sl, sc);
+    softmax_pv(own_c, masked_c, sl, kbase, sc);
+  };
 
-  // ---- prefix tiles of this chunk through the ring. Every step issues one
-  // tile (past the end: a harmless re-fetch of the first), so the number of
-  // DMA instructions behind the tile being waited for is always IPW * (R - 2).
+  // ---- prefix tiles of this chunk through the ring, software-pipelined: the
+  // scores of tile i+1 (MFMA) are formed in the same scheduling region as the
+  // softmax of tile i (VALU), so the two overlap on the SIMD. Every step issues
+  // one tile (past the end: a harmless re-fetch of the first); at step i the
+  // DMA instructions behind tile i+1 are those of tiles i+2 .. i+R-2.
   const int p_end = min(t_end, n_ptiles);
   const int np = p_end - t_begin;
   if (np > 0) {
+    static_assert(R >= 3, "the pipelined loop needs a slot for tile i+1 and one being refilled");
 #pragma unroll
     for (int u = 0; u < R - 1; ++u) issue(t_begin + (u < np ? u : 0), u);
-    for (int i = 0; i < np; ++i) {
-      wait_vmcnt_lds<IPW * (R - 2)>();
+    wait_vmcnt_lds<IPW * (R - 2)>();   // tile 0
+    __builtin_amdgcn_s_barrier();
+    floatx4 sc_cur[4];
+    scores(std::false_type{}, 0, sc_cur);
+    // Tiles before the chunk's last are never partial (only the prefix's last
+    // tile can be, and it is the last of its chunk).
+    for (int i = 0; i + 1 < np; ++i) {
+      wait_vmcnt_lds<IPW * (R - 3)>();   // tile i+1 has landed; every wave is done with slot (i-1) % R
       __builtin_amdgcn_s_barrier();
       const int nx = i + R - 1;
       issue(t_begin + (nx < np ? nx : 0), nx % R);
-      const int pt = t_begin + i;
-      if (pt < n_full) contract(std::false_type{}, std::false_type{}, i % R, pt * KT);
-      else contract(std::false_type{}, std::true_type{}, i % R, pt * KT);
+      floatx4 sc_nxt[4];
+      scores(std::false_type{}, (i + 1) % R, sc_nxt);
+      softmax_pv(std::false_type{}, std::false_type{}, i % R, (t_begin + i) * KT, sc_cur);
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) sc_cur[kt] = sc_nxt[kt];
     }
+    const int pl = t_begin + np - 1;
+    if (pl < n_full) softmax_pv(std::false_type{}, std::false_type{}, (np - 1) % R, pl * KT, sc_cur);
+    else softmax_pv(std::false_type{}, std::true_type{}, (np - 1) % R, pl * KT, sc_cur);
     // The trailing re-fetches must land before the ring memory is reused or the
     // workgroup ends.
     wait_vmcnt<0>();
