@@ -26,6 +26,14 @@ extern "C" {
 rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P, int32_t M,
                            int32_t N, int32_t K, int32_t splits, int32_t* splits_used, void* stream);
 
+/* rksc_test_gemm with the kernel chosen by the caller: kind = -1 the
+ * library's own choice for this shape, 0 the 128-row-tile kernel, 1 the
+ * 256 x 256-tile kernel (bf16 only; RKSC_ERR_UNSUPPORTED otherwise). The
+ * verify pass picks kind 1 for projections with many rows. */
+rksc_status rksc_test_gemm_kind(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P,
+                                int32_t M, int32_t N, int32_t K, int32_t splits, int32_t kind,
+                                int32_t* splits_used, void* stream);
+
 /* Shared-prefix attention of one layer for B branches of s tokens, with the
  * same split of the prefix across workgroups as the verify pass:
  * q [B*s, H, hd], k_own/v_own [B, Hkv, s, hd] are fp32 and prefix_k/prefix_v

@@ -21,7 +21,7 @@ __all__ = [
     "RkscError", "load_library", "library_path",
     "rksc_abi_version", "rksc_verify_workspace_size", "rksc_verify_forward",
     "rksc_asks_similarity", "rksc_status_string", "rksc_last_error",
-    "rksc_test_gemm", "rksc_test_attention",
+    "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_attention",
     "verify_forward", "asks_similarity", "model_config",
     "RKSC_OK", "RKSC_ERR_INVALID_ARGUMENT", "RKSC_ERR_UNSUPPORTED",
     "RKSC_ERR_WORKSPACE_TOO_SMALL", "RKSC_ERR_HIP", "RKSC_F32", "RKSC_BF16", "RKSC_MAX_BRANCHES",
@@ -106,6 +106,8 @@ def load_library():
     lib.rksc_last_error.argtypes = []
     lib.rksc_test_gemm.restype = i32
     lib.rksc_test_gemm.argtypes = [i32, vp, vp, vp, vp, i32, i32, i32, i32, ctypes.POINTER(i32), vp]
+    lib.rksc_test_gemm_kind.restype = i32
+    lib.rksc_test_gemm_kind.argtypes = [i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, ctypes.POINTER(i32), vp]
     lib.rksc_test_attention.restype = i32
     lib.rksc_test_attention_scratch_size.restype = sz
     lib.rksc_test_attention_scratch_size.argtypes = [i32, i32, i32, i32, i32, i32, i32]
@@ -203,10 +205,11 @@ def rksc_asks_similarity(hidden: torch.Tensor, alpha: float, S: torch.Tensor, st
                                                _stream(stream)))
 
 
-def rksc_test_gemm(A, W: torch.Tensor, splits: int = 0, stream=None):
+def rksc_test_gemm(A, W: torch.Tensor, splits: int = 0, stream=None, kind: int = -1):
     """Kernel-level GEMM: returns the fp32 split partials [splits_used, M, N].
 
     bf16 W: A is the pair (A_hi, A_lo) of bf16 [M, K] planes; fp32 W: A is an fp32 [M, K] tensor.
+    kind: -1 the library's choice, 0 the 128-row-tile kernel, 1 the 256 x 256-tile kernel (bf16).
     """
     if W.dtype == torch.bfloat16:
         a_hi, a_lo = A
@@ -218,8 +221,8 @@ def rksc_test_gemm(A, W: torch.Tensor, splits: int = 0, stream=None):
     N = W.shape[0]
     P = torch.empty((8, M, N), dtype=torch.float32, device=a_hi.device)
     used = ctypes.c_int32(0)
-    _check(load_library().rksc_test_gemm(dt, _ptr(a_hi), _ptr(a_lo), _ptr(W), _ptr(P), M, N, K, splits,
-                                         ctypes.byref(used), _stream(stream)))
+    _check(load_library().rksc_test_gemm_kind(dt, _ptr(a_hi), _ptr(a_lo), _ptr(W), _ptr(P), M, N, K, splits,
+                                              kind, ctypes.byref(used), _stream(stream)))
     return P[: used.value]
 
 

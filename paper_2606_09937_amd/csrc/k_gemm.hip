@@ -43,6 +43,27 @@ __device__ __forceinline__ int gswz(int row, int chunk) { return chunk ^ ((row >
 
 constexpr int kGemmWaves = 8;
 
+// XCD-aware grouped raster for grids with several row tiles. Workgroups are
+// dealt to the 8 XCDs round robin (id % 8), and each XCD has its own L2. Each
+// XCD is given a contiguous range of "virtual" tile ids, and virtual ids walk
+// GM row tiles x all column tiles per group, so the ~32 workgroups resident on
+// one XCD cover a compact GM-row block of tiles and re-read their activation
+// and weight tiles from that XCD's L2 instead of from HBM/MALL.
+template <int GM>
+__device__ __forceinline__ void xcd_raster(int& tx, int& ty, int& tz) {
+  const int NX = gridDim.x, NY = gridDim.y, T = NX * NY * gridDim.z;
+  const int id = blockIdx.x + NX * (blockIdx.y + NY * blockIdx.z);
+  const int x = id % 8, q = id / 8;
+  const int v = x * (T / 8) + min(x, T % 8) + q;   // XCD x holds ids x, x+8, ...: T/8 (+1 for x < T%8)
+  const int per_split = NX * NY;
+  tz = v / per_split;
+  const int r = v - tz * per_split;
+  const int grp = r / (GM * NX), first_m = grp * GM, gm = min(GM, NY - first_m);
+  const int rr = r - grp * GM * NX;
+  ty = first_m + rr % gm;
+  tx = rr / gm;
+}
+
 template <int BN, int R>
 __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __restrict__ Ahi,
                                                               const bf16* __restrict__ Alo,
@@ -58,10 +79,12 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
   __shared__ __attribute__((aligned(1024))) uint8_t smem[R * SLOT];
 
   const int Ml = c ? min(c->live_count * s, max_rows) : max_rows;
-  const int m0 = blockIdx.y * BM;
+  int tx = blockIdx.x, ty = blockIdx.y, tz = blockIdx.z;
+  if (gridDim.y > 1) xcd_raster<4>(tx, ty, tz);
+  const int m0 = ty * BM;
   if (m0 >= Ml) return;
-  const int n0 = blockIdx.x * BN;
-  const int kb = blockIdx.z * kps;
+  const int n0 = tx * BN;
+  const int kb = tz * kps;
   const int ke = min(K, kb + kps);
   const int nsteps = (ke - kb + KEL - 1) / KEL;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -160,7 +183,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
   }
   wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
 
-  float* out = P + blockIdx.z * split_stride;
+  float* out = P + tz * split_stride;
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
@@ -169,6 +192,126 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = m0 + wm0 + 16 * tm + 4 * g + i;
+        if (row < Ml && col < N) out[(size_t)row * N + col] = acc[tm][tn][i];
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 256 x 256 tiles for large row counts (MFMA-bound projections).
+//
+// 8 waves as a 4 (rows) x 2 (columns) grid of 64 x 128 wave tiles: each wave
+// reads 64 x 32 activation and 128 x 32 weight elements from LDS per 32-wide
+// K step for 64 MFMAs, a third fewer LDS bytes per MFMA than the 128-row
+// kernel's 64 x 64 wave tiles. A stage is a 32-wide K slice (64 bytes per row)
+// of three 16 KB sub-tiles (A hi, A lo, W), so three stages fit the LDS and two
+// are in flight while one is contracted. Each DMA instruction moves 16 rows x
+// 64 bytes; within a row the 16-byte chunk c sits at c ^ ((row >> 2) & 3), which
+// spreads the 16 rows of a fragment read over the banks.
+__device__ __forceinline__ int wswz(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
+
+template <int R>
+__global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __restrict__ Ahi,
+                                                               const bf16* __restrict__ Alo,
+                                                               const bf16* __restrict__ W, float* __restrict__ P,
+                                                               size_t split_stride, const Ctrl* c, int s,
+                                                               int max_rows, int N, int K, int kps) {
+  constexpr int BM = 256, BN = 256, KEL = 32, RB = KEL * 2;
+  constexpr int SUB = BM * RB, SLOT = 3 * SUB;
+  constexpr int IPW = SLOT / 1024 / kGemmWaves;   // 6 DMA instructions per wave per stage
+  constexpr int TM = 4, TN = 8;                   // 64 x 128 wave tile
+  static_assert(SUB / 1024 % kGemmWaves == 0, "every instruction of a wave stays in one sub-tile");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[R * SLOT];
+
+  const int Ml = c ? min(c->live_count * s, max_rows) : max_rows;
+  int tx, ty, tz;
+  xcd_raster<4>(tx, ty, tz);
+  const int m0 = ty * BM;
+  if (m0 >= Ml) return;
+  const int n0 = tx * BN;
+  const int kb = tz * kps, ke = min(K, kb + kps);
+  const int nsteps = (ke - kb + KEL - 1) / KEL;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int wm = wid & 3, wn = wid >> 2;
+  const bool wave_live = m0 + 64 * wm < Ml;
+
+  // DMA instruction j of this wave (ins = 8j + wid) fills rows 16 (ins % 16) ..
+  // +15 of sub-tile ins / 16 = j / 2; lane L fills physical chunk L & 3 of row
+  // L >> 2, i.e. logical chunk (L & 3) ^ ((L >> 4) & 3), the same for every j.
+  int rowoff[IPW];
+#pragma unroll
+  for (int j = 0; j < IPW; ++j) {
+    const int row = ((j * kGemmWaves + wid) % 16) * 16 + (lane >> 2);
+    rowoff[j] = (j / 2 < 2 ? min(m0 + row, max_rows - 1) : min(n0 + row, N - 1)) * K;
+  }
+  const int ccol = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
+  auto issue = [&](int step) {
+    // Steps past the end re-read the split's first step (valid memory, never used);
+    // chunks at or past the split's end read its first chunk and are zeroed in compute.
+    const int k = kb + (step < nsteps ? step : 0) * KEL;
+    const int col = k + ccol < ke ? k + ccol : kb;
+    uint8_t* slot = smem + (step % R) * SLOT;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const bf16* base = j / 2 == 0 ? Ahi : (j / 2 == 1 ? Alo : W);
+      dma16(base + rowoff[j] + col, slot + (j * kGemmWaves + wid) * 1024);
+    }
+  };
+
+  floatx4 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const bf16x8 zero = {};
+  auto compute = [&](const uint8_t* slot, bool kin) {
+    bf16x8 bw[TN];
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int row = wn * 128 + 16 * tn + r16;
+      bw[tn] = *reinterpret_cast<const bf16x8*>(slot + 2 * SUB + row * RB + wswz(row, g) * 16);
+    }
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      const int row = wm * 64 + 16 * tm + r16;
+      const int off = row * RB + wswz(row, g) * 16;
+      bf16x8 ah = *reinterpret_cast<const bf16x8*>(slot + off);
+      bf16x8 al = *reinterpret_cast<const bf16x8*>(slot + SUB + off);
+      ah = kin ? ah : zero;
+      al = kin ? al : zero;
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+        acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw[tn], acc[tm][tn], 0, 0, 0);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+        acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw[tn], acc[tm][tn], 0, 0, 0);
+    }
+  };
+
+#pragma unroll
+  for (int st = 0; st < R - 1; ++st) issue(st);
+  for (int st = 0; st < nsteps; ++st) {
+    // This thread's DMAs for step st have landed and its reads of step st-1 are
+    // complete; after the barrier every wave's are.
+    wait_vmcnt_lds<IPW * (R - 2)>();
+    __builtin_amdgcn_s_barrier();
+    issue(st + R - 1);   // refills the slot step st-1 used
+    // The lane's 8-element K chunk lies wholly inside or outside the split (K % 8 == 0).
+    if (wave_live) compute(smem + (st % R) * SLOT, kb + st * KEL + 8 * g < ke);
+  }
+  wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
+  if (!wave_live) return;
+
+  float* out = P + tz * split_stride;
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int col = n0 + wn * 128 + 16 * tn + r16;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = m0 + wm * 64 + 16 * tm + 4 * g + i;
         if (row < Ml && col < N) out[(size_t)row * N + col] = acc[tm][tn][i];
       }
     }
@@ -221,6 +364,7 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
   GemmPlan p;
+  p.kind = 0;
   if (dt == DType::F32) {
     p.bm = 64;
     p.bn = 64;
@@ -252,13 +396,51 @@ GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
   const int splits = splits_for(p.bn);
   p.k_per_split = cdiv(cdiv(K, 64), splits) * 64;
   p.splits = cdiv(K, p.k_per_split);
+  // 256 x 256 tiles when they fill at least one full round of workgroups without
+  // splitting K and, counted in rounds of 256 workgroups, finish sooner: measured
+  // on MI355X (split MFMA work, 4096 rows) the 256 x 256 kernel issues MFMAs at
+  // ~50% of peak and the 128 x 256 kernel at ~45%.
+  const int wide_wgs = cdiv(N, 256) * cdiv(max_rows, 256);
+  if (p.splits == 1 && p.bn == 256 && wide_wgs >= kComputeUnits) {
+    const double t_wide = cdiv(wide_wgs, kComputeUnits) * 2.0 / 0.50;
+    const double t_dma = cdiv(cdiv(N, 256) * mt, kComputeUnits) * 1.0 / 0.45;
+    if (t_wide < t_dma) {
+      p.kind = 1;
+      p.bm = 256;
+      p.k_per_split = cdiv(K, 32) * 32;
+    }
+  }
+  return p;
+}
+
+GemmPlan plan_gemm_kind(DType dt, int max_rows, int N, int K, int kind, int splits) {
+  GemmPlan p = plan_gemm(dt, max_rows, N, K);
+  if (dt == DType::BF16 && kind == 1) {
+    p.kind = 1;
+    p.bm = 256;
+    p.bn = 256;
+  } else if (dt == DType::BF16 && kind == 0 && p.kind == 1) {
+    p.kind = 0;
+    p.bm = 128;
+    p.k_per_split = cdiv(cdiv(K, 64), p.splits) * 64;
+  }
+  if (splits > 0 || p.kind == 1) {
+    const int sp = splits > 0 ? splits : p.splits;
+    const int kstep = dt == DType::F32 ? 16 : (p.kind == 1 ? 32 : 64);   // K elements per pipeline stage
+    p.k_per_split = cdiv(cdiv(K, kstep), sp) * kstep;
+    p.splits = cdiv(K, p.k_per_split);
+  }
   return p;
 }
 
 hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W, float* P,
                        size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st) {
   const dim3 grid(cdiv(N, p.bn), cdiv(max_rows, p.bm), p.splits);
-  if (dt == DType::F32) {
+  if (dt == DType::BF16 && p.kind == 1) {
+    hipLaunchKernelGGL((k_gemm_wide<3>), grid, dim3(kGemmWaves * 64), 0, st, static_cast<const bf16*>(A0),
+                       static_cast<const bf16*>(A1), static_cast<const bf16*>(W), P, split_stride, c, s, max_rows, N,
+                       K, p.k_per_split);
+  } else if (dt == DType::F32) {
     hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, st, static_cast<const float*>(A0),
                        static_cast<const float*>(W), P, split_stride, c, s, max_rows, N, K, p.k_per_split);
   } else {

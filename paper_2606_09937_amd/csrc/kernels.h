@@ -57,10 +57,14 @@ hipError_t launch_tap(DType dt, const float* x, const float* P, int nsplit, size
 // BF16 models: A0/A1 are the bf16 hi/lo planes of the activation, W bf16.
 // F32 models: A0 is the fp32 activation (A1 unused), W fp32.
 constexpr int kMaxSplitsGemm = 8;   // the consumers of split partials sum at most this many
+// kind: 0 = 128-row tiles (bn columns; HBM-bound skinny projections and mid
+// sizes), 1 = 256 x 256 tiles (MFMA-bound projections with many rows).
 struct GemmPlan {
-  int bm, bn, splits, k_per_split;
+  int kind, bm, bn, splits, k_per_split;
 };
 GemmPlan plan_gemm(DType dt, int max_rows, int N, int K);
+// Test hook: kind -1 = the planner's choice, 0/1 = that kernel; splits > 0 forces the split count.
+GemmPlan plan_gemm_kind(DType dt, int max_rows, int N, int K, int kind, int splits);
 hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W, float* P,
                        size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st);
 

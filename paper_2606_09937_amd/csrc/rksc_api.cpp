@@ -315,26 +315,28 @@ RKSC_EXPORT rksc_status rksc_asks_similarity(const float* hidden, int32_t n_laye
 
 // ------------------------------------------------------------------ kernel-level test entry points
 
-RKSC_EXPORT rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P,
-                                       int32_t M, int32_t N, int32_t K, int32_t splits, int32_t* splits_used,
-                                       void* stream) {
+RKSC_EXPORT rksc_status rksc_test_gemm_kind(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P,
+                                            int32_t M, int32_t N, int32_t K, int32_t splits, int32_t kind,
+                                            int32_t* splits_used, void* stream) {
   if (!A || !W || !P) return fail(RKSC_ERR_INVALID_ARGUMENT, "A, W and P must not be NULL");
   if (dtype == RKSC_BF16 && !A_lo) return fail(RKSC_ERR_INVALID_ARGUMENT, "A_lo must not be NULL for bf16");
   if (dtype != RKSC_F32 && dtype != RKSC_BF16) return fail(RKSC_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
   if (M < 1 || N < 1 || K < 8 || K % 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "bad shape %d x %d x %d", M, N, K);
   if (splits < 0 || splits > 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "splits must be in [0, 8]");
+  if (kind < -1 || kind > 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "kind must be -1, 0 or 1 (got %d)", kind);
+  if (kind == 1 && dtype != RKSC_BF16) return fail(RKSC_ERR_UNSUPPORTED, "kind 1 needs bf16 weights");
   const DType dt = dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
-  GemmPlan p = rksc::plan_gemm(dt, M, N, K);
-  if (splits > 0) {
-    const int kstep = dt == DType::BF16 ? 64 : 16;   // K elements per pipeline stage
-    const int ktiles = (K + kstep - 1) / kstep;
-    p.k_per_split = (ktiles + splits - 1) / splits * kstep;
-    p.splits = (K + p.k_per_split - 1) / p.k_per_split;
-  }
+  const GemmPlan p = rksc::plan_gemm_kind(dt, M, N, K, kind, splits);
   if (splits_used) *splits_used = p.splits;
   HIP_TRY(rksc::launch_gemm(dt, p, A, A_lo, W, P, (size_t)M * N, nullptr, 1, M, N, K,
                             static_cast<hipStream_t>(stream)));
   return ok();
+}
+
+RKSC_EXPORT rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P,
+                                       int32_t M, int32_t N, int32_t K, int32_t splits, int32_t* splits_used,
+                                       void* stream) {
+  return rksc_test_gemm_kind(dtype, A, A_lo, W, P, M, N, K, splits, -1, splits_used, stream);
 }
 
 RKSC_EXPORT size_t rksc_test_attention_scratch_size(int32_t dtype, int32_t B, int32_t n, int32_t s, int32_t H,

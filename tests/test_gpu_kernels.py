@@ -51,6 +51,30 @@ def test_gemm_matches_fp64(dtype, M, N, K, splits):
     assert (err <= bound).all(), f"max err {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}"
 
 
+@pytest.mark.parametrize("M,N,K,splits", [
+    (1, 16, 32, 0), (100, 200, 256, 0), (300, 700, 1000, 0), (256, 256, 8, 0), (513, 260, 4104, 3),
+    (777, 513, 1000, 5), (1024, 1024, 2048, 0), (260, 1030, 3000, 8),
+])
+def test_gemm_wide_tiles_match_fp64(M, N, K, splits):
+    """The 256 x 256-tile kernel (the verify pass's choice for projections with many rows), forced on
+    ragged rows, columns and K (K % 32 != 0 included) and on forced K splits."""
+    log(f"gemm wide M={M} N={N} K={K} splits={splits}")
+    A = _rand((M, K), torch.float32, 11 + M, 0.5)
+    W = _rand((N, K), torch.bfloat16, 12 + N, 0.05)
+    a_hi = A.to(torch.bfloat16)
+    a_lo = (A - a_hi.float()).to(torch.bfloat16)
+    A = a_hi.float() + a_lo.float()
+    P = rk.rksc_test_gemm((a_hi.to(DEV), a_lo.to(DEV)), W.to(DEV), splits=splits, kind=1)
+    torch.cuda.synchronize()
+    if splits:
+        assert 1 <= P.shape[0] <= splits
+    got = P.double().sum(0).cpu().numpy()
+    a, w = A.double().numpy(), W.double().numpy()
+    bound = 1e-5 * (np.abs(a) @ np.abs(w).T) + 1e-7
+    err = np.abs(got - a @ w.T)
+    assert (err <= bound).all(), f"max err {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}"
+
+
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
 @pytest.mark.parametrize("B,n,s,H,Hkv,hd", [
     (1, 0, 1, 4, 4, 64), (2, 37, 16, 8, 2, 64), (3, 130, 70, 28, 4, 128),
