@@ -283,6 +283,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-depth", action="store_true")
     ap.add_argument("--no-tau-sweep", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the root-forward (prefill) timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the plain copy kernel used to scale HBM counters")
     ap.add_argument("--summarize-stats", dest="stats", metavar="DIR",
@@ -486,6 +487,40 @@ def main():
                               "value": tokens / (t_ms / 1e3)})
             log(f"tau {tau}: exit layers {ex_t}, {t_ms:.3f} ms/step")
 
+    # Root forward over the same prefix length (Eq. prefix_fwd): the step before
+    # the verify pass, which writes the cache the verify pass reads.
+    prefill = None
+    if not args.no_prefill:
+        ptoks = workloads.make_tokens(n, shape.vocab, seed=args.seed, name="prefix", device=dev)
+        pws = torch.empty(rk.rksc_prefill_workspace_size(shape, n), dtype=torch.uint8, device=dev)
+        dt_kv = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+        pk = torch.empty((L, shape.n_kv_heads, n, shape.head_dim), dtype=dt_kv, device=dev)
+        pv = torch.empty_like(pk)
+        hr = torch.empty((L, shape.d_model), dtype=torch.float32, device=dev)
+        pstep = lambda: rk.rksc_prefill(mw, ptoks, pk, pv, hr, pws, stream)   # noqa: E731
+        for _ in range(max(1, args.warmup)):
+            pstep()
+        torch.cuda.synchronize()
+        k_p = max(1, min(args.steps, 10))
+        a, b = hip.create(2)
+        hip.lib.hipEventRecord(ctypes.c_void_p(a), sp)
+        for _ in range(k_p):
+            pstep()
+        hip.lib.hipEventRecord(ctypes.c_void_p(b), sp)
+        torch.cuda.synchronize()
+        p_ms = hip.elapsed_ms(a, b) / k_p
+        hip.destroy([a, b])
+        d_, H_, Hkv_, hd_, F_ = shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.d_ff
+        P_ = d_ * (H_ + 2 * Hkv_) * hd_ + H_ * hd_ * d_ + 3 * d_ * F_
+        p_flops = L * (2.0 * n * P_ + 4.0 * hd_ * H_ * n * (n + 1) / 2)
+        peak = BF16_PEAK_TFLOPS if shape.dtype == "bf16" else FP32_PEAK_TFLOPS
+        prefill = {"n_prefix": n, "ms_per_call": p_ms, "tokens_per_s": n / (p_ms / 1e3), "calls_timed": k_p,
+                   "algorithmic_tflops": p_flops / (p_ms / 1e3) / 1e12,
+                   "mfma_frac": p_flops / (p_ms / 1e3) / 1e12 / peak}
+        log(f"prefill n={n}: {p_ms:.3f} ms/call, {prefill['tokens_per_s']:.0f} tokens/s, "
+            f"{prefill['algorithmic_tflops']:.1f} TFLOP/s algorithmic")
+        del pws, pk, pv, hr
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu_layers = L if args.cpu_layers <= 0 else min(args.cpu_layers, L)
@@ -520,6 +555,7 @@ def main():
         "kernels": kernels,
         "full_depth": full_depth,
         "tau_sweep": tau_sweep,
+        "prefill": prefill,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

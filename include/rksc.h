@@ -5,8 +5,10 @@
  * This library implements the verify pass of its layer-level early exit
  * (Sec. 2.3 "Layer-level entropy exit", Alg. VerifyWithEntropyExit) over a
  * prefix KV cache that is computed once and read by every branch
- * (Sec. 2.2 "KV broadcast and batched decode"), and the layer-weighted cosine
- * similarity of the ASKS gate (Eq. asks_sim, Alg. AsksGate).
+ * (Sec. 2.2 "KV broadcast and batched decode"), the root forward that computes
+ * that cache and the root hidden states (Eq. prefix_fwd), and the
+ * layer-weighted cosine similarity of the ASKS gate (Eq. asks_sim,
+ * Alg. AsksGate).
  *
  * Conventions shared by every entry point:
  *   - Tensor arguments are DEVICE pointers to dense row-major arrays.
@@ -132,13 +134,39 @@ rksc_status rksc_verify_forward(const rksc_weights* weights, const rksc_prefix_k
                                 float* entropy, int32_t* exit_layer, float* hidden_last,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of workspace rksc_prefill needs for an n_prefix-token prefix; 0 if the
+ * shape is invalid (rksc_last_error() says why). */
+size_t rksc_prefill_workspace_size(const rksc_model_config* cfg, int32_t n_prefix);
+
+/*
+ * Root forward over the shared prefix (Eq. prefix_fwd; the first step of
+ * Alg. RKSC): one causal pass of the n prefix tokens at positions 0..n-1
+ * through all L layers. It writes the prefix cache C = {(K^(l), V^(l))} that
+ * rksc_verify_forward reads (pass k_out/v_out as rksc_prefix_kv.k/.v with
+ * n_prefix = n), and the root hidden states H_root = {h_root^(l)}: the layer-l
+ * output row of the last prefix token, normalised to unit length once here as
+ * the paper stores them (Sec. 2.2; a zero row stays zero).
+ *
+ * tokens     [n] int32 device, ids in [0, V) (not checked; an id outside gives
+ *            NaN rows); n_prefix = n >= 1.
+ * k_out      [L, Hkv, n, hd] device out, the model's storage type (bf16 by
+ *            round-to-nearest-even for RKSC_BF16): keys after RoPE.
+ * v_out      [L, Hkv, n, hd] device out, same type: values.
+ * h_root     [L, d] fp32 device out: unit-normalised root hidden states.
+ * workspace  device buffer of at least rksc_prefill_workspace_size() bytes,
+ *            256-byte aligned; its contents on entry do not matter.
+ */
+rksc_status rksc_prefill(const rksc_weights* weights, const int32_t* tokens, int32_t n_prefix, void* k_out,
+                         void* v_out, float* h_root, void* workspace, size_t workspace_bytes, void* stream);
+
 /*
  * ASKS similarity (Eq. asks_sim with the weights of Alg. AsksGate, generalised
  * from branch-vs-root to all branch pairs):
  *   w_l = exp(alpha*l/L) / sum_{l'=1..L} exp(alpha*l'/L),  l = 1..L
  *   S[i][j] = sum_l w_l * <h_i^(l), h_j^(l)> / (|h_i^(l)| |h_j^(l)|)
  * A zero row has cosine 0 with everything. To get the paper's sigma_b against
- * the root, append the root's rows as one more "branch".
+ * the root, append the root's rows (h_root of rksc_prefill) as one more
+ * "branch".
  * hidden [L, B, d] fp32 device; S [B, B] fp32 device out.
  * L >= 1, B >= 1, d >= 1, alpha finite.
  */

@@ -38,7 +38,7 @@ __all__ = [
     "f64", "rmsnorm", "rope_inv_freq", "apply_rope", "silu", "attention",
     "decoder_stack", "prefill", "forward_full", "softmax_entropy",
     "layer_entropies", "exit_layer", "verify_forward", "asks_weights",
-    "asks_similarity",
+    "asks_similarity", "unit_rows", "root_similarity",
 ]
 
 
@@ -178,6 +178,25 @@ def prefill(weights, cfg, prefix_tokens):
     """
     hidden, ks, vs = decoder_stack(weights, cfg, np.asarray(prefix_tokens)[None, :], 0)
     return ks[:, 0], vs[:, 0], hidden[:, 0, -1, :]
+
+
+def unit_rows(h) -> np.ndarray:
+    """Rows scaled to unit Euclidean length; a zero row stays zero.
+
+    The root hidden states of Eq. prefix_fwd are stored in this normalised form
+    (Sec. 2.2, paragraph "Prefix forward pass").
+    """
+    h = f64(h)
+    nrm = np.sqrt((h * h).sum(axis=-1, keepdims=True))
+    return np.where(nrm > 0, h / np.where(nrm > 0, nrm, 1.0), 0.0)
+
+
+def root_similarity(hidden, h_root_unit, alpha: float) -> np.ndarray:
+    """sigma_b of Eq. asks_sim: sum_l w_l <h_b^(l) / |h_b^(l)|, h_root^(l)> for hidden [L, B, d]
+    and pre-normalised root rows h_root_unit [L, d] (Alg. AsksGate); a zero branch row contributes 0."""
+    hb = unit_rows(hidden)
+    w = asks_weights(alpha, hb.shape[0])
+    return np.einsum("l,lbd,ld->b", w, hb, f64(h_root_unit))
 
 
 def forward_full(weights, cfg, tokens):

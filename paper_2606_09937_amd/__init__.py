@@ -22,7 +22,7 @@ __all__ = [
     "rksc_abi_version", "rksc_verify_workspace_size", "rksc_verify_forward",
     "rksc_asks_similarity", "rksc_status_string", "rksc_last_error",
     "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_attention",
-    "verify_forward", "asks_similarity", "model_config",
+    "verify_forward", "asks_similarity", "prefill", "rksc_prefill", "rksc_prefill_workspace_size", "model_config",
     "RKSC_OK", "RKSC_ERR_INVALID_ARGUMENT", "RKSC_ERR_UNSUPPORTED",
     "RKSC_ERR_WORKSPACE_TOO_SMALL", "RKSC_ERR_HIP", "RKSC_F32", "RKSC_BF16", "RKSC_MAX_BRANCHES",
 ]
@@ -98,6 +98,10 @@ def load_library():
     lib.rksc_verify_forward.restype = i32
     lib.rksc_verify_forward.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32, i32,
                                         vp, vp, vp, vp, sz, vp]
+    lib.rksc_prefill_workspace_size.restype = sz
+    lib.rksc_prefill_workspace_size.argtypes = [ctypes.POINTER(ModelConfig), i32]
+    lib.rksc_prefill.restype = i32
+    lib.rksc_prefill.argtypes = [ctypes.POINTER(Weights), vp, i32, vp, vp, vp, vp, sz, vp]
     lib.rksc_asks_similarity.restype = i32
     lib.rksc_asks_similarity.argtypes = [vp, i32, i32, i32, f32, vp, vp]
     lib.rksc_status_string.restype = ctypes.c_char_p
@@ -198,6 +202,29 @@ def rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, 
     _check(st)
 
 
+def rksc_prefill_workspace_size(shape, n_prefix: int) -> int:
+    cfg = model_config(shape)
+    n = int(load_library().rksc_prefill_workspace_size(ctypes.byref(cfg), n_prefix))
+    if n == 0:
+        raise RkscError(RKSC_ERR_INVALID_ARGUMENT, rksc_last_error())
+    return n
+
+
+def rksc_prefill(weights, tokens: torch.Tensor, k_out: torch.Tensor, v_out: torch.Tensor, h_root: torch.Tensor,
+                 workspace: torch.Tensor, stream=None) -> None:
+    """Marshal torch device tensors into rksc_prefill (asynchronous on `stream`).
+
+    tokens [n] int32 device; k_out/v_out [L, Hkv, n, hd] of the model dtype; h_root [L, d] fp32.
+    """
+    lib = load_library()
+    w, layers_keepalive = _weights_struct(weights)
+    st = lib.rksc_prefill(ctypes.byref(w), _ptr(tokens), int(tokens.numel()), _ptr(k_out), _ptr(v_out),
+                          _ptr(h_root), _ptr(workspace), int(workspace.numel() * workspace.element_size()),
+                          _stream(stream))
+    del layers_keepalive
+    _check(st)
+
+
 def rksc_asks_similarity(hidden: torch.Tensor, alpha: float, S: torch.Tensor, stream=None) -> None:
     """Marshal hidden [L, B, d] fp32 and S [B, B] fp32 device tensors into rksc_asks_similarity."""
     L, B, d = hidden.shape
@@ -265,6 +292,25 @@ def verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, patie
     rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau, patience, entropy, exit_layer, hidden,
                         workspace, stream)
     return (entropy, exit_layer, hidden) if return_hidden else (entropy, exit_layer)
+
+
+def prefill(weights, tokens: torch.Tensor, workspace: Optional[torch.Tensor] = None, stream=None):
+    """Allocate the cache and root rows (and the workspace unless given) and run the root forward.
+
+    Returns (k [L, Hkv, n, hd], v [L, Hkv, n, hd] of the model dtype, h_root [L, d] fp32 unit rows).
+    """
+    shape = weights.shape
+    n = int(tokens.numel())
+    dev = tokens.device
+    L = len(weights.layers)
+    dtype = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    if workspace is None:
+        workspace = torch.empty(rksc_prefill_workspace_size(shape, n), dtype=torch.uint8, device=dev)
+    k = torch.empty((L, shape.n_kv_heads, n, shape.head_dim), dtype=dtype, device=dev)
+    v = torch.empty_like(k)
+    h_root = torch.empty((L, shape.d_model), dtype=torch.float32, device=dev)
+    rksc_prefill(weights, tokens.contiguous(), k, v, h_root, workspace, stream)
+    return k, v, h_root
 
 
 def asks_similarity(hidden: torch.Tensor, alpha: float, stream=None) -> torch.Tensor:

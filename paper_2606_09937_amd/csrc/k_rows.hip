@@ -313,7 +313,50 @@ __global__ __launch_bounds__(256) void k_finalize_exit(const float* parts, int n
   }
 }
 
+// ------------------------------------------------------------------ root forward
+
+// The prefix cache in the model's storage type from the fp32 keys/values of the
+// root's own span (keys already rotated): 4 elements per thread.
+template <typename T>
+__global__ __launch_bounds__(256) void k_store_kv(const float* __restrict__ k_own, const float* __restrict__ v_own,
+                                                  T* __restrict__ k_dst, T* __restrict__ v_dst, size_t elems) {
+  const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= elems) return;
+  const float4 a = *reinterpret_cast<const float4*>(k_own + i);
+  const float4 b = *reinterpret_cast<const float4*>(v_own + i);
+  store4(k_dst + i, a.x, a.y, a.z, a.w);
+  store4(v_dst + i, b.x, b.y, b.z, b.w);
+}
+
+// Unit-normalises each row (the root hidden states are stored normalised).
+__global__ __launch_bounds__(256) void k_unit_rows(float* __restrict__ x, int d) {
+  __shared__ float red[16];
+  float* row = x + (size_t)blockIdx.x * d;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) ss += row[c] * row[c];
+  const float tot = block_sum(ss, red);
+  const float inv = tot > 0.f ? rsqrtf(tot) : 0.f;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) row[c] *= inv;
+}
+
 }  // namespace
+
+hipError_t launch_store_kv(DType dt, const float* k_own, const float* v_own, void* k_dst, void* v_dst,
+                           size_t elems, hipStream_t st) {
+  const dim3 grid((unsigned)((elems / 4 + 255) / 256));
+  if (dt == DType::BF16)
+    hipLaunchKernelGGL(k_store_kv<bf16>, grid, dim3(256), 0, st, k_own, v_own, static_cast<bf16*>(k_dst),
+                       static_cast<bf16*>(v_dst), elems);
+  else
+    hipLaunchKernelGGL(k_store_kv<float>, grid, dim3(256), 0, st, k_own, v_own, static_cast<float*>(k_dst),
+                       static_cast<float*>(v_dst), elems);
+  return hipGetLastError();
+}
+
+hipError_t launch_unit_rows(float* x, int rows, int d, hipStream_t st) {
+  hipLaunchKernelGGL(k_unit_rows, dim3(rows), dim3(256), 0, st, x, d);
+  return hipGetLastError();
+}
 
 hipError_t launch_init(Ctrl* c, int B, int L, float* entropy, int* exit_layer, float* hidden_last,
                        size_t hidden_elems, hipStream_t st) {

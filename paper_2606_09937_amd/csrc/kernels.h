@@ -93,6 +93,13 @@ hipError_t launch_entropy(DType dt, const void* W, const void* hn_a, const void*
 hipError_t launch_finalize_exit(const float* parts, int nparts, Ctrl* c, int layer1, int L, int B,
                                 float tau, int patience, float* entropy, int* exit_layer, hipStream_t st);
 
+// ---- root forward (prefill)
+// k_dst/v_dst [Hkv, n, hd] of the model dtype from the fp32 k_own/v_own of one branch.
+hipError_t launch_store_kv(DType dt, const float* k_own, const float* v_own, void* k_dst, void* v_dst,
+                           size_t elems, hipStream_t st);
+// x[r] /= |x[r]| for rows r < rows of d floats (zero rows stay zero).
+hipError_t launch_unit_rows(float* x, int rows, int d, hipStream_t st);
+
 // ---- ASKS similarity
 hipError_t launch_asks(const float* hidden, int L, int B, int d, float alpha, float* S, hipStream_t st);
 

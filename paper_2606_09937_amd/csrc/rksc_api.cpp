@@ -301,6 +301,106 @@ RKSC_EXPORT rksc_status rksc_verify_forward_profiled(const rksc_weights* w, cons
                      hidden_last, workspace, workspace_bytes, stream, events);
 }
 
+RKSC_EXPORT size_t rksc_prefill_workspace_size(const rksc_model_config* cfg, int32_t n_prefix) {
+  if (n_prefix < 1) {
+    fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 1 (got %d)", n_prefix);
+    return 0;
+  }
+  Layout lay;
+  if (make_layout(cfg, 1, n_prefix, 0, &lay) != RKSC_OK) return 0;
+  return lay.total;
+}
+
+// Root forward (Eq. prefix_fwd): the verify pass's layer sequence for one
+// "branch" of n tokens over an empty prefix, causal within itself, with the
+// post-RoPE keys and the values of every layer stored as the prefix cache and
+// the last token's layer outputs as the root hidden states. No entropy probe.
+RKSC_EXPORT rksc_status rksc_prefill(const rksc_weights* w, const int32_t* tokens, int32_t n_prefix, void* k_out,
+                                     void* v_out, float* h_root, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
+  if (!w) return fail(RKSC_ERR_INVALID_ARGUMENT, "weights is NULL");
+  if (!tokens) return fail(RKSC_ERR_INVALID_ARGUMENT, "tokens is NULL");
+  if (!k_out || !v_out) return fail(RKSC_ERR_INVALID_ARGUMENT, "k_out and v_out must not be NULL");
+  if (!h_root) return fail(RKSC_ERR_INVALID_ARGUMENT, "h_root is NULL");
+  if (!workspace) return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  if (n_prefix < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 1 (got %d)", n_prefix);
+  const rksc_model_config* c = &w->cfg;
+  Layout lay;
+  rksc_status st = make_layout(c, 1, n_prefix, 0, &lay);
+  if (st != RKSC_OK) return st;
+  if (workspace_bytes < lay.total)
+    return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
+  if (!w->embed || !w->final_norm || !w->layers)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "embed, final_norm and layers must not be NULL");
+  for (int l = 0; l < c->n_layers; ++l) {
+    const rksc_layer_weights& lw = w->layers[l];
+    if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
+      return fail(RKSC_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
+  }
+
+  const DType dt = c->dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
+  const size_t T = dt == DType::BF16 ? 2 : 4;
+  const int L = c->n_layers, d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, hd = c->head_dim;
+  const int F = c->d_ff, V = c->vocab, s = n_prefix;
+  const int M = lay.max_rows;
+  const int Nqkv = (H + 2 * Hkv) * hd;
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  rksc::Ctrl* ctrl = reinterpret_cast<rksc::Ctrl*>(ws + lay.ctrl);
+  float* x0 = reinterpret_cast<float*>(ws + lay.x0);
+  float* x1 = reinterpret_cast<float*>(ws + lay.x1);
+  float* act = reinterpret_cast<float*>(ws + lay.act);
+  float* ffn = reinterpret_cast<float*>(ws + lay.ffn);
+  float* qb = reinterpret_cast<float*>(ws + lay.q);
+  float* kown = reinterpret_cast<float*>(ws + lay.kown);
+  float* vown = reinterpret_cast<float*>(ws + lay.vown);
+  float* pbig = reinterpret_cast<float*>(ws + lay.pbig);
+  float* pres = reinterpret_cast<float*>(ws + lay.pres);
+  float2* rope = reinterpret_cast<float2*>(ws + lay.rope);
+  float* opart = reinterpret_cast<float*>(ws + lay.opart);
+  float* mlpart = reinterpret_cast<float*>(ws + lay.mlpart);
+  const size_t res_stride = (size_t)M * d;
+  const size_t kv_layer = (size_t)Hkv * s * hd;
+  auto plane_lo = [&](float* buf, size_t elems) -> const void* {
+    return dt == DType::BF16 ? static_cast<const void*>(reinterpret_cast<const uint16_t*>(buf) + elems) : nullptr;
+  };
+
+  // One live "branch": h_root takes the tap's rows (hidden_last with B = 1).
+  HIP_TRY(rksc::launch_init(ctrl, 1, L, nullptr, nullptr, h_root, (size_t)L * d, strm));
+  HIP_TRY(rksc::launch_rope_table(rope, s, 0, hd, (double)c->rope_base, strm));
+  HIP_TRY(rksc::launch_embed(dt, w->embed, tokens, V, x0, M, d, strm));
+  for (int l = 0; l < L; ++l) {
+    const rksc_layer_weights& lw = w->layers[l];
+    float* x_prev = (l % 2 == 0) ? x0 : x1;
+    float* x_cur = (l % 2 == 0) ? x1 : x0;
+    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, true, ctrl, s,
+                                  x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
+                              s, M, Nqkv, d, strm));
+    HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
+                                  vown, M, strm));
+    HIP_TRY(rksc::launch_store_kv(dt, kown, vown, static_cast<char*>(k_out) + l * kv_layer * T,
+                                  static_cast<char*>(v_out) + l * kv_layer * T, kv_layer, strm));
+    HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, nullptr, nullptr, kown, vown, act, opart, mlpart, ctrl, 0, s, H,
+                                   Hkv, hd, 1, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.o, act, plane_lo(act, (size_t)M * H * hd), lw.w_o, pres, res_stride, ctrl, s,
+                              M, d, H * hd, strm));
+    HIP_TRY(rksc::launch_add_norm(dt, x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
+                                  lw.ffn_norm, d, c->rms_eps, M, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig, (size_t)M * 2 * F,
+                              ctrl, s, M, 2 * F, d, strm));
+    HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
+                              M, d, F, strm));
+    HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, 1, l, h_root, w->final_norm,
+                             c->rms_eps, ws + lay.hn_a, ws + lay.hn_b, 1, strm));
+  }
+  HIP_TRY(rksc::launch_unit_rows(h_root, L, d, strm));
+  return ok();
+}
+
 RKSC_EXPORT rksc_status rksc_asks_similarity(const float* hidden, int32_t n_layers, int32_t n_branches,
                                              int32_t d_model, float alpha, float* S, void* stream) {
   if (!hidden || !S) return fail(RKSC_ERR_INVALID_ARGUMENT, "hidden and S must not be NULL");

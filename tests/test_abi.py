@@ -149,3 +149,26 @@ def test_testing_entry_points_reject_bad_shapes(lib):
         rk.RKSC_ERR_UNSUPPORTED
     assert lib.rksc_test_attention(1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 4, 4, 4, 2, 32, FAKE, 1 << 20, None) == \
         rk.RKSC_ERR_UNSUPPORTED
+
+
+def test_prefill_rejects_bad_arguments(lib):
+    shape = workloads.get("tiny").model
+    cfg = rk.model_config(shape)
+    assert lib.rksc_prefill_workspace_size(ctypes.byref(cfg), 0) == 0
+    assert lib.rksc_prefill_workspace_size(ctypes.byref(cfg), 64) > 0
+    layers = (rk.LayerWeights * shape.n_layers)()
+    for i in range(shape.n_layers):
+        layers[i] = rk.LayerWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    w = rk.Weights(cfg, FAKE, layers, FAKE, FAKE)
+    ws = lib.rksc_prefill_workspace_size(ctypes.byref(cfg), 64)
+    ok_ws = ctypes.c_void_p(0x100000)   # 256-byte aligned, never touched
+    assert lib.rksc_prefill(ctypes.byref(w), None, 64, FAKE, FAKE, FAKE, ok_ws, ws, None) == \
+        rk.RKSC_ERR_INVALID_ARGUMENT
+    assert lib.rksc_prefill(ctypes.byref(w), FAKE, 0, FAKE, FAKE, FAKE, ok_ws, ws, None) == \
+        rk.RKSC_ERR_INVALID_ARGUMENT
+    assert lib.rksc_prefill(ctypes.byref(w), FAKE, 64, FAKE, FAKE, None, ok_ws, ws, None) == \
+        rk.RKSC_ERR_INVALID_ARGUMENT
+    assert lib.rksc_prefill(ctypes.byref(w), FAKE, 64, FAKE, FAKE, FAKE, ok_ws, ws - 1, None) == \
+        rk.RKSC_ERR_WORKSPACE_TOO_SMALL
+    assert lib.rksc_prefill(ctypes.byref(w), FAKE, 64, FAKE, FAKE, FAKE, ctypes.c_void_p(0x100010), ws, None) == \
+        rk.RKSC_ERR_INVALID_ARGUMENT

@@ -409,3 +409,36 @@ def test_zero_lm_head_gives_log_vocab_every_layer():
     # Every delta is 0 after layer 1, so any tau > 0 exits at 1 + patience.
     _, ex, _, _, _ = oracle.verify_forward(mw, shape, pk, pv, toks, 1e-9, 2)
     assert np.all(ex == 3)
+
+
+# ----------------------------------------------------------------- root rows (Eq. prefix_fwd, Alg. AsksGate)
+
+def test_unit_rows_norm_direction_and_zero():
+    rng = np.random.default_rng(11)
+    h = rng.standard_normal((5, 3, 40)) * rng.uniform(0.01, 100.0, (5, 3, 1))
+    h[2, 1] = 0.0
+    u = oracle.unit_rows(h)
+    nrm = np.linalg.norm(u, axis=-1)
+    nz = np.linalg.norm(h, axis=-1) > 0
+    np.testing.assert_allclose(nrm[nz], 1.0, rtol=1e-14)
+    assert np.all(u[2, 1] == 0.0)
+    # same direction: h = |h| u
+    np.testing.assert_allclose(h, np.linalg.norm(h, axis=-1, keepdims=True) * u, rtol=1e-12, atol=1e-14)
+
+
+def test_root_similarity_equals_appended_root_row():
+    """sigma_b against pre-normalised root rows equals the pairwise S with the root as one more branch."""
+    rng = np.random.default_rng(12)
+    L, B, d = 7, 4, 24
+    hb = rng.standard_normal((L, B, d))
+    root = rng.standard_normal((L, d)) * 5.0
+    hb[:, 1] = 2.5 * root                        # a branch on the root's direction: sigma = 1
+    hb[:, 2] = -root                             # antipodal: sigma = -1
+    sig = oracle.root_similarity(hb, oracle.unit_rows(root), 1.5)
+    S = oracle.asks_similarity(np.concatenate([hb, root[:, None, :]], axis=1), 1.5)
+    np.testing.assert_allclose(sig, S[:B, B], atol=1e-13)
+    assert abs(sig[1] - 1.0) < 1e-13 and abs(sig[2] + 1.0) < 1e-13
+    # L = 1: plain cosine
+    s1 = oracle.root_similarity(hb[:1], oracle.unit_rows(root[:1]), 0.3)
+    for b in range(B):
+        assert abs(s1[b] - (1 - scipy.spatial.distance.cosine(hb[0, b], root[0]))) < 1e-12
