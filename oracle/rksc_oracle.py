@@ -29,6 +29,11 @@ Exit rule (Sec. 2.3 "Layer-level entropy exit"), as (tau, patience): the layer
   reaches patience, else at L.
 ASKS (Eq. asks_sim with its exponential layer weights): S_ij = sum_l w_l *
   cos(h_i^(l), h_j^(l)), w_l = exp(alpha l/L) / sum_l' exp(alpha l'/L).
+Batched decode (Sec. 2.2; the stepwise loop of the implementation notes): a
+  suffix prefill of every branch over the shared prefix, then one token per
+  branch per step attending to the prefix, the branch's own earlier tokens and
+  itself; each step's top-1 probability max_v softmax(z)_v feeds the generation
+  confidence p_b (Eq. gen_conf), and Eq. cgee_gate decides on the p_b.
 """
 from __future__ import annotations
 
@@ -39,6 +44,7 @@ __all__ = [
     "decoder_stack", "prefill", "forward_full", "softmax_entropy",
     "layer_entropies", "exit_layer", "verify_forward", "asks_weights",
     "asks_similarity", "unit_rows", "root_similarity",
+    "final_logits", "top1", "decode_suffix", "decode_step", "gen_confidence", "cgee_gate",
 ]
 
 
@@ -284,3 +290,85 @@ def asks_similarity(hidden, alpha: float) -> np.ndarray:
         hat[nz] = h[l][nz] / norms[nz, None]
         S += w[l] * (hat @ hat.T)
     return S
+
+
+def final_logits(weights, cfg, h) -> np.ndarray:
+    """z = RMSNorm(h; g_final) W_lm^T for rows h [..., d]: the model's output logits."""
+    return rmsnorm(f64(h), weights.final_norm, cfg.rms_eps) @ f64(weights.lm_head).T
+
+
+def top1(z):
+    """(argmax_v z_v, max_v softmax(z)_v) per row of z [..., V]: the next token and
+    the term max_v Pr[y_j = v] of Eq. gen_conf. np.argmax takes the first maximum."""
+    z = f64(z)
+    m = z.max(axis=-1, keepdims=True)
+    p = np.exp(z - m)
+    p = p / p.sum(axis=-1, keepdims=True)
+    return np.argmax(z, axis=-1).astype(np.int64), p.max(axis=-1)
+
+
+def decode_suffix(weights, cfg, prefix_k, prefix_v, suffix_tokens):
+    """Suffix prefill of B branches over the shared prefix (Sec. 2.2): branch b's
+    tokens at positions n..n+s-1. Returns (k [L, B, Hkv, s, hd] post-RoPE,
+    v [L, B, Hkv, s, hd], z [B, V] logits of each branch's last token)."""
+    tokens = np.asarray(suffix_tokens, dtype=np.int64)
+    n = 0 if prefix_k is None else int(prefix_k.shape[2])
+    hidden, ks, vs = decoder_stack(weights, cfg, tokens, n, prefix_k, prefix_v)
+    return ks, vs, final_logits(weights, cfg, hidden[-1, :, -1, :])
+
+
+def decode_step(weights, cfg, prefix_k, prefix_v, past_k, past_v, tokens):
+    """One decode step: token tokens[b] of branch b at position n + len attends to
+    the prefix, to the branch's past entries past_k/past_v [L, B, Hkv, len, hd]
+    (post-RoPE keys and values of its tokens at n..n+len-1) and to itself.
+    Returns (k [L, B, Hkv, 1, hd], v [L, B, Hkv, 1, hd], z [B, V])."""
+    tokens = np.asarray(tokens, dtype=np.int64).reshape(-1)
+    B = tokens.shape[0]
+    n = 0 if prefix_k is None else int(prefix_k.shape[2])
+    length = int(past_k.shape[3])
+    L, Hkv, hd = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim
+    ks = np.empty((L, B, Hkv, 1, hd))
+    vs = np.empty((L, B, Hkv, 1, hd))
+    z = np.empty((B, weights.lm_head.shape[0]))
+    for b in range(B):
+        if n:
+            pk = np.concatenate([f64(prefix_k), f64(past_k[:, b])], axis=2)
+            pv = np.concatenate([f64(prefix_v), f64(past_v[:, b])], axis=2)
+        else:
+            pk, pv = f64(past_k[:, b]), f64(past_v[:, b])
+        if pk.shape[2] == 0:
+            pk = pv = None
+        hidden, kb, vb = decoder_stack(weights, cfg, tokens[b:b + 1, None], n + length, pk, pv)
+        ks[:, b], vs[:, b] = kb[:, 0], vb[:, 0]
+        z[b] = final_logits(weights, cfg, hidden[-1, 0, -1, :])
+    return ks, vs, z
+
+
+def gen_confidence(p_top) -> np.ndarray:
+    """Eq. gen_conf: p_b = (1/t) sum_{j=1..t} max_v Pr[y_j^(b) = v] for p_top [t, B]."""
+    p_top = f64(p_top)
+    return p_top.sum(axis=0) / p_top.shape[0]
+
+
+def cgee_gate(p, tau_conf: float, r_gap: float) -> dict:
+    """Eq. cgee_gate on the generation confidences p [B]: fires iff
+    max_b p >= tau_conf and (max_b p - 2nd-max_b p) / max_b p >= r_gap.
+
+    Readings: the winner is the first index holding the maximum; the 2nd max is
+    the largest p among the other branches, 0 when there is none; a zero
+    maximum gives a gap ratio of 0. NaN entries are left out.
+    """
+    p = f64(p).reshape(-1)
+    idx = [b for b in range(p.shape[0]) if not np.isnan(p[b])]
+    if not idx:
+        return {"fired": False, "winner": -1, "max": float("nan"), "second": 0.0, "gap": 0.0}
+    winner = idx[0]
+    for b in idx:
+        if p[b] > p[winner]:
+            winner = b
+    others = [p[b] for b in idx if b != winner]
+    top = float(p[winner])
+    second = float(max(others)) if others else 0.0
+    gap = (top - second) / top if top > 0 else 0.0
+    return {"fired": bool(top >= tau_conf and gap >= r_gap), "winner": winner, "max": top, "second": second,
+            "gap": gap}

@@ -442,3 +442,170 @@ def test_root_similarity_equals_appended_root_row():
     s1 = oracle.root_similarity(hb[:1], oracle.unit_rows(root[:1]), 0.3)
     for b in range(B):
         assert abs(s1[b] - (1 - scipy.spatial.distance.cosine(hb[0, b], root[0]))) < 1e-12
+
+
+# ----------------------------------------------------------------- decode, Eq. gen_conf, Eq. cgee_gate
+
+def _gate_examples():
+    with open(os.path.join(GOLDEN, "cgee_gate_examples.json")) as f:
+        return json.load(f)
+
+
+def _confidences(top, second, B, seed):
+    """B confidences whose maximum is `top` and whose second maximum is `second` (the rest below)."""
+    rng = np.random.default_rng(seed)
+    p = np.concatenate([[top, second], rng.uniform(0.0, second, B - 2)])
+    return p[rng.permutation(B)]
+
+
+def test_cgee_gate_paper_examples():
+    g = _gate_examples()
+    for ex in g["examples"]:
+        for seed in range(5):
+            p = _confidences(ex["max"], ex["second"], g["n_branches"], seed)
+            r = oracle.cgee_gate(p, g["tau_conf"], g["r_gap"])
+            assert r["fired"] == ex["fires"], ex["name"]
+            assert r["max"] == ex["max"] and r["second"] == ex["second"]
+            assert round(r["gap"], 2) == ex["printed_gap_ratio"]
+            assert p[r["winner"]] == ex["max"]
+    # The deferred example fails on the absolute threshold, not on the gap.
+    d = g["examples"][1]
+    r = oracle.cgee_gate(_confidences(d["max"], d["second"], 8, 0), d["max"], g["r_gap"])
+    assert r["fired"] and r["gap"] >= g["r_gap"]
+    # Under the stricter decode-level thresholds the first example still fires.
+    e = g["examples"][0]
+    assert oracle.cgee_gate(_confidences(e["max"], e["second"], 8, 1), g["theta_dec"], g["r_dec"])["fired"]
+
+
+def test_cgee_gate_two_failure_modes():
+    """Sec. 2.3: (a) a confident branch with a close competitor and (b) a large relative gap
+    between two unconfident branches must both defer; each condition alone would fire."""
+    a = np.array([0.80, 0.79, 0.3])
+    r = oracle.cgee_gate(a, 0.70, 0.06)
+    assert not r["fired"] and r["max"] >= 0.70 and oracle.cgee_gate(a, 0.70, 0.0)["fired"]
+    b = np.array([0.10, 0.40, 0.05])
+    r = oracle.cgee_gate(b, 0.70, 0.06)
+    assert not r["fired"] and r["gap"] >= 0.06 and r["winner"] == 1
+    assert oracle.cgee_gate(b, 0.40, 0.06)["fired"]
+
+
+def test_cgee_gate_brute_force_sorted():
+    rng = np.random.default_rng(5)
+    for _ in range(300):
+        B = int(rng.integers(2, 65))
+        p = rng.uniform(0, 1, B)
+        if rng.uniform() < 0.3:
+            p[rng.integers(0, B)] = p.max()   # a tie at the maximum
+        srt = np.sort(p)
+        tau, rg = rng.uniform(0.3, 0.9), rng.uniform(0.0, 0.3)
+        gap = (srt[-1] - srt[-2]) / srt[-1]
+        r = oracle.cgee_gate(p, tau, rg)
+        assert r["max"] == srt[-1] and r["second"] == srt[-2]
+        assert abs(r["gap"] - gap) < 1e-15
+        assert r["fired"] == (srt[-1] >= tau and gap >= rg)
+        assert r["winner"] == int(np.flatnonzero(p == srt[-1])[0])
+
+
+def test_cgee_gate_single_branch_nan_and_zero():
+    r = oracle.cgee_gate([0.75], 0.70, 0.06)
+    assert r["fired"] and r["second"] == 0.0 and r["gap"] == 1.0
+    assert not oracle.cgee_gate([0.65], 0.70, 0.06)["fired"]
+    r = oracle.cgee_gate([np.nan, 0.9, np.nan, 0.5], 0.70, 0.06)
+    assert r["winner"] == 1 and r["second"] == 0.5
+    r = oracle.cgee_gate([np.nan, np.nan], 0.0, 0.0)
+    assert not r["fired"] and r["winner"] == -1
+    r = oracle.cgee_gate([0.0, 0.0], 0.0, 0.0)
+    assert r["gap"] == 0.0 and r["winner"] == 0 and r["fired"]
+
+
+def test_gen_confidence_is_the_step_mean():
+    rng = np.random.default_rng(6)
+    pt = rng.uniform(0.1, 1.0, (9, 5))
+    for t in (1, 4, 9):
+        np.testing.assert_allclose(oracle.gen_confidence(pt[:t]), [sum(pt[j, b] for j in range(t)) / t
+                                                                   for b in range(5)], rtol=1e-15)
+    np.testing.assert_allclose(oracle.gen_confidence(np.full((7, 3), 0.35)), 0.35, rtol=1e-15)
+
+
+@pytest.mark.parametrize("a", [-3.0, 0.0, 2.5, 30.0])
+def test_top1_two_level_closed_form(a):
+    V = 1000
+    z = np.zeros((2, V))
+    z[0, 17] = a
+    z[1, 999] = a
+    tok, p = oracle.top1(z)
+    ref = math.exp(a) / (math.exp(a) + V - 1)
+    if a > 0:
+        assert list(tok) == [17, 999]
+        np.testing.assert_allclose(p, ref, rtol=1e-13)
+    elif a == 0:
+        assert list(tok) == [0, 0]          # first of the tied maxima
+        np.testing.assert_allclose(p, 1.0 / V, rtol=1e-13)
+    else:
+        assert list(tok) == [0, 0]
+        np.testing.assert_allclose(p, 1.0 / (V - 1 + math.exp(a)), rtol=1e-13)
+
+
+def test_decode_equals_full_causal_forward():
+    """Prefill + suffix + stepwise decode with the branch caches equals one causal forward of
+    the concatenated sequence, for every branch: logits of each step and its cached K/V."""
+    shape = GQA_SHAPE
+    mw = _randomise_gains(workloads.make_model(shape, seed=8))
+    n, s, B, steps = 10, 4, 3, 3
+    prefix = workloads.make_tokens(n, shape.vocab, seed=8, name="prefix").numpy()
+    suffix = workloads.make_tokens(B * s, shape.vocab, seed=8).numpy().reshape(B, s)
+    gen = workloads.make_tokens(B * steps, shape.vocab, seed=8, name="decode").numpy().reshape(steps, B)
+    pk, pv, _ = oracle.prefill(mw, shape, prefix)
+    ck, cv, z = oracle.decode_suffix(mw, shape, pk, pv, suffix)
+    zs = [z]
+    for j in range(steps):
+        k1, v1, z = oracle.decode_step(mw, shape, pk, pv, ck, cv, gen[j])
+        ck, cv = np.concatenate([ck, k1], axis=3), np.concatenate([cv, v1], axis=3)
+        zs.append(z)
+    lm = oracle.f64(mw.lm_head)
+    for b in range(B):
+        seq = np.concatenate([prefix, suffix[b], gen[:, b]])
+        hid, ks, vs = oracle.decoder_stack(mw, shape, seq[None, :], 0)
+        zf = oracle.rmsnorm(hid[-1, 0], mw.final_norm, shape.rms_eps) @ lm.T
+        for j in range(steps + 1):
+            np.testing.assert_allclose(zs[j][b], zf[n + s - 1 + j], rtol=1e-10, atol=1e-10)
+        np.testing.assert_allclose(ck[:, b], ks[:, 0, :, n:], rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(cv[:, b], vs[:, 0, :, n:], rtol=1e-10, atol=1e-12)
+
+
+def test_decode_matches_hf_kv_cache_generation():
+    """Suffix prefill and teacher-forced decode steps vs HF's own KV-cache path."""
+    pytest.importorskip("transformers")
+    import copy
+    shape = GQA_SHAPE
+    mw = _randomise_gains(workloads.make_model(shape, seed=9))
+    n, s, B, steps = 12, 5, 2, 3
+    prefix = workloads.make_tokens(n, shape.vocab, seed=9, name="prefix").numpy()
+    suffix = workloads.make_tokens(B * s, shape.vocab, seed=9).numpy().reshape(B, s)
+    gen = workloads.make_tokens(B * steps, shape.vocab, seed=9, name="decode").numpy().reshape(steps, B)
+    pk, pv, _ = oracle.prefill(mw, shape, prefix)
+    ck, cv, z = oracle.decode_suffix(mw, shape, pk, pv, suffix)
+    zs, tops = [z], [oracle.top1(z)[1]]
+    for j in range(steps):
+        k1, v1, z = oracle.decode_step(mw, shape, pk, pv, ck, cv, gen[j])
+        ck, cv = np.concatenate([ck, k1], axis=3), np.concatenate([cv, v1], axis=3)
+        zs.append(z)
+        tops.append(oracle.top1(z)[1])
+    m = _hf_model(mw, shape)
+    with torch.no_grad():
+        pre = m(torch.from_numpy(prefix.astype(np.int64))[None], use_cache=True)
+        for b in range(B):
+            out = m(torch.from_numpy(suffix[b].astype(np.int64))[None],
+                    past_key_values=copy.deepcopy(pre.past_key_values), use_cache=True)
+            hf_z = [out.logits[0, -1].numpy()]
+            cache = out.past_key_values
+            for j in range(steps):
+                out = m(torch.tensor([[int(gen[j, b])]]), past_key_values=cache, use_cache=True)
+                cache = out.past_key_values
+                hf_z.append(out.logits[0, -1].numpy())
+            for j in range(steps + 1):
+                _close(zs[j][b], hf_z[j])
+                p_hf = torch.softmax(torch.from_numpy(hf_z[j]), -1).max().item()
+                assert abs(p_hf - tops[j][b]) < 1e-6
+    conf = oracle.gen_confidence(np.stack(tops))
+    assert conf.shape == (B,) and np.all((conf > 0) & (conf <= 1))
