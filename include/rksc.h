@@ -6,9 +6,10 @@
  * (Sec. 2.3 "Layer-level entropy exit", Alg. VerifyWithEntropyExit) over a
  * prefix KV cache that is computed once and read by every branch
  * (Sec. 2.2 "KV broadcast and batched decode"), the root forward that computes
- * that cache and the root hidden states (Eq. prefix_fwd), and the
- * layer-weighted cosine similarity of the ASKS gate (Eq. asks_sim,
- * Alg. AsksGate).
+ * that cache and the root hidden states (Eq. prefix_fwd), the batched decode
+ * of the branches over it with the generation confidence (Eq. gen_conf) and
+ * the CGEE verify-skip gate (Eq. cgee_gate), and the layer-weighted cosine
+ * similarity of the ASKS gate (Eq. asks_sim, Alg. AsksGate).
  *
  * Conventions shared by every entry point:
  *   - Tensor arguments are DEVICE pointers to dense row-major arrays.
@@ -35,7 +36,7 @@
 extern "C" {
 #endif
 
-#define RKSC_ABI_VERSION 2
+#define RKSC_ABI_VERSION 3
 
 /* Largest number of branches one verify call accepts. */
 #define RKSC_MAX_BRANCHES 64
@@ -94,6 +95,18 @@ typedef struct {
   const void* k;      /* [L, Hkv, n, hd], keys after RoPE at positions 0..n-1 */
   const void* v;      /* [L, Hkv, n, hd] */
 } rksc_prefix_kv;
+
+/* One branch set's own K/V cache for the decode loop (Sec. 2.2 "KV broadcast
+ * and batched decode"): entry j of branch b holds the key (after RoPE) and the
+ * value of the branch's token at position n_prefix + j. Allocated by the
+ * caller for a fixed number of branches B; the decode calls append to it and
+ * advance `length` (host field) on success. */
+typedef struct {
+  int32_t capacity;   /* entries allocated per (layer, branch, kv head) */
+  int32_t length;     /* entries filled; 0 before rksc_decode_suffix */
+  void* k;            /* [L, B, Hkv, capacity, hd] device, storage type */
+  void* v;            /* [L, B, Hkv, capacity, hd] device, storage type */
+} rksc_branch_kv;
 
 int32_t rksc_abi_version(void);
 
@@ -158,6 +171,75 @@ size_t rksc_prefill_workspace_size(const rksc_model_config* cfg, int32_t n_prefi
  */
 rksc_status rksc_prefill(const rksc_weights* weights, const int32_t* tokens, int32_t n_prefix, void* k_out,
                          void* v_out, float* h_root, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace that rksc_decode_suffix (suffix_len tokens per branch)
+ * and rksc_decode_step (one token per branch) need for n_branches branches over
+ * an n_prefix-token prefix cache; one buffer of this size serves both. 0 if the
+ * shape is invalid (rksc_last_error() says why). */
+size_t rksc_decode_workspace_size(const rksc_model_config* cfg, int32_t n_branches, int32_t suffix_len,
+                                  int32_t n_prefix);
+
+/*
+ * Batched suffix prefill, the first step of the stepwise decode loop
+ * (Sec. 2.2: every branch decodes over the shared cache C_B in one batched
+ * call; implementation notes, "Stepwise Batched Decode" (1)). Branch b's
+ * tokens suffix_tokens[b, 0..s-1] sit at positions n..n+s-1, attend to the
+ * whole prefix and causally to each other, and their keys and values of every
+ * layer are written to branch_kv entries 0..s-1 (storage type; bf16 by
+ * round-to-nearest-even). From the last token's logits
+ * z = lm_head . RMSNorm_final(h_L):
+ *   next_token[b] = argmax_v z_v (smallest index among equal maxima),
+ *   p_top[b]      = max_v softmax(z)_v, the step's term of Eq. gen_conf,
+ *   conf[b]       = p_top[b]  (the running sum of Eq. gen_conf, t = 1).
+ * A branch whose logits have no finite maximum gets next_token -1, p_top NaN.
+ *
+ * branch_kv      length must be 0 and capacity >= s; length becomes s.
+ * suffix_tokens  [B, s] int32 device, ids in [0, V) (not checked).
+ * n_branches     B in [1, RKSC_MAX_BRANCHES]; suffix_len s >= 1.
+ * next_token     [B] int32 device out; p_top, conf [B] fp32 device out.
+ * workspace      at least rksc_decode_workspace_size() bytes, 256-byte aligned.
+ */
+rksc_status rksc_decode_suffix(const rksc_weights* weights, const rksc_prefix_kv* prefix_kv,
+                               rksc_branch_kv* branch_kv, const int32_t* suffix_tokens, int32_t n_branches,
+                               int32_t suffix_len, int32_t* next_token, float* p_top, float* conf, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/*
+ * One token-by-token decode step (implementation notes, "Stepwise Batched
+ * Decode" (2)): tokens[b] at position n + len (len = branch_kv->length) attends
+ * to the prefix, to the branch's cached entries 0..len-1 and to itself; its key
+ * and value are written to entry len. Outputs as rksc_decode_suffix, except
+ * conf[b] += p_top[b] (the running sum of Eq. gen_conf over the steps).
+ * tokens and next_token may be the same buffer (feeding the argmax back).
+ *
+ * branch_kv  capacity >= len + 1; length becomes len + 1.
+ * tokens     [B] int32 device, ids in [0, V) (not checked).
+ */
+rksc_status rksc_decode_step(const rksc_weights* weights, const rksc_prefix_kv* prefix_kv, rksc_branch_kv* branch_kv,
+                             const int32_t* tokens, int32_t n_branches, int32_t* next_token, float* p_top,
+                             float* conf, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * CGEE gate (Eq. cgee_gate) over the generation confidences
+ * p_b = conf[b] / n_steps (Eq. gen_conf, conf being the running sums of the
+ * decode calls and n_steps = t the tokens generated): fires when
+ *   max_b p_b >= tau_conf  and  (max_b p_b - 2nd-max_b p_b) / max_b p_b >= r_gap.
+ * With (tau_conf, r_gap) = (0.70, 0.06) it is the Level-1 verify-skip gate
+ * after decoding; with (0.72, 0.10) the decode-level early-termination gate
+ * between steps (Sec. 2.3; implementation notes (3)). The 2nd max is the
+ * largest p among the branches other than the winner (the smallest index
+ * holding the maximum), 0 for a single branch; NaN entries are ignored. The
+ * decision is taken in fp32.
+ *
+ * conf      [B] fp32 device; B in [1, RKSC_MAX_BRANCHES]; n_steps >= 1;
+ *           tau_conf, r_gap not NaN.
+ * p_mean    [B] fp32 device out or NULL: p_b.
+ * fired     [1] int32 device out: 1 if the gate fires, else 0.
+ * winner    [1] int32 device out: argmax_b p_b, -1 if every p_b is NaN.
+ * stats     [3] fp32 device out or NULL: max, 2nd max, gap ratio.
+ */
+rksc_status rksc_cgee_gate(const float* conf, int32_t n_branches, int32_t n_steps, float tau_conf, float r_gap,
+                           float* p_mean, int32_t* fired, int32_t* winner, float* stats, void* stream);
 
 /*
  * ASKS similarity (Eq. asks_sim with the weights of Alg. AsksGate, generalised

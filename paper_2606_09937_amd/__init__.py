@@ -23,6 +23,8 @@ __all__ = [
     "rksc_asks_similarity", "rksc_status_string", "rksc_last_error",
     "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_attention",
     "verify_forward", "asks_similarity", "prefill", "rksc_prefill", "rksc_prefill_workspace_size", "model_config",
+    "BranchCache", "Decoder", "rksc_decode_workspace_size", "rksc_decode_suffix", "rksc_decode_step",
+    "rksc_cgee_gate", "cgee_gate", "RKSC_ABI_VERSION",
     "RKSC_OK", "RKSC_ERR_INVALID_ARGUMENT", "RKSC_ERR_UNSUPPORTED",
     "RKSC_ERR_WORKSPACE_TOO_SMALL", "RKSC_ERR_HIP", "RKSC_F32", "RKSC_BF16", "RKSC_MAX_BRANCHES",
 ]
@@ -35,6 +37,7 @@ RKSC_ERR_HIP = -4
 RKSC_F32 = 0
 RKSC_BF16 = 1
 RKSC_MAX_BRANCHES = 64
+RKSC_ABI_VERSION = 3
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 
@@ -76,6 +79,11 @@ class PrefixKV(ctypes.Structure):
     _fields_ = [("n_prefix", ctypes.c_int32), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p)]
 
 
+class BranchKVStruct(ctypes.Structure):
+    _fields_ = [("capacity", ctypes.c_int32), ("length", ctypes.c_int32), ("k", ctypes.c_void_p),
+                ("v", ctypes.c_void_p)]
+
+
 _lib = None
 
 
@@ -102,6 +110,16 @@ def load_library():
     lib.rksc_prefill_workspace_size.argtypes = [ctypes.POINTER(ModelConfig), i32]
     lib.rksc_prefill.restype = i32
     lib.rksc_prefill.argtypes = [ctypes.POINTER(Weights), vp, i32, vp, vp, vp, vp, sz, vp]
+    lib.rksc_decode_workspace_size.restype = sz
+    lib.rksc_decode_workspace_size.argtypes = [ctypes.POINTER(ModelConfig), i32, i32, i32]
+    lib.rksc_decode_suffix.restype = i32
+    lib.rksc_decode_suffix.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV),
+                                       ctypes.POINTER(BranchKVStruct), vp, i32, i32, vp, vp, vp, vp, sz, vp]
+    lib.rksc_decode_step.restype = i32
+    lib.rksc_decode_step.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV),
+                                     ctypes.POINTER(BranchKVStruct), vp, i32, vp, vp, vp, vp, sz, vp]
+    lib.rksc_cgee_gate.restype = i32
+    lib.rksc_cgee_gate.argtypes = [vp, i32, i32, f32, f32, vp, vp, vp, vp, vp]
     lib.rksc_asks_similarity.restype = i32
     lib.rksc_asks_similarity.argtypes = [vp, i32, i32, i32, f32, vp, vp]
     lib.rksc_status_string.restype = ctypes.c_char_p
@@ -318,3 +336,118 @@ def asks_similarity(hidden: torch.Tensor, alpha: float, stream=None) -> torch.Te
     S = torch.empty((B, B), dtype=torch.float32, device=hidden.device)
     rksc_asks_similarity(hidden, alpha, S, stream)
     return S
+
+
+class BranchCache:
+    """A branch set's own K/V cache ([L, B, Hkv, capacity, hd] device tensors of the
+    model dtype) and the rksc_branch_kv struct whose `length` the decode calls advance."""
+
+    def __init__(self, shape, n_layers: int, n_branches: int, capacity: int, device):
+        dtype = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+        dims = (n_layers, n_branches, shape.n_kv_heads, capacity, shape.head_dim)
+        self.k = torch.zeros(dims, dtype=dtype, device=device)
+        self.v = torch.zeros(dims, dtype=dtype, device=device)
+        self.n_branches = n_branches
+        self.struct = BranchKVStruct(int(capacity), 0, _ptr(self.k), _ptr(self.v))
+
+    @property
+    def length(self) -> int:
+        return int(self.struct.length)
+
+    @property
+    def capacity(self) -> int:
+        return int(self.struct.capacity)
+
+
+def rksc_decode_workspace_size(shape, n_branches: int, suffix_len: int, n_prefix: int) -> int:
+    cfg = model_config(shape)
+    n = int(load_library().rksc_decode_workspace_size(ctypes.byref(cfg), n_branches, suffix_len, n_prefix))
+    if n == 0:
+        raise RkscError(RKSC_ERR_INVALID_ARGUMENT, rksc_last_error())
+    return n
+
+
+def rksc_decode_suffix(weights, prefix_k, prefix_v, cache: BranchCache, suffix_tokens: torch.Tensor,
+                       next_token: torch.Tensor, p_top: torch.Tensor, conf: torch.Tensor, workspace: torch.Tensor,
+                       stream=None) -> None:
+    """Marshal torch device tensors into rksc_decode_suffix (asynchronous on `stream`)."""
+    lib = load_library()
+    w, layers_keepalive = _weights_struct(weights)
+    B, s = suffix_tokens.shape
+    n = int(prefix_k.shape[2]) if prefix_k is not None else 0
+    kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
+    st = lib.rksc_decode_suffix(ctypes.byref(w), ctypes.byref(kv), ctypes.byref(cache.struct), _ptr(suffix_tokens),
+                                int(B), int(s), _ptr(next_token), _ptr(p_top), _ptr(conf), _ptr(workspace),
+                                int(workspace.numel() * workspace.element_size()), _stream(stream))
+    del layers_keepalive
+    _check(st)
+
+
+def rksc_decode_step(weights, prefix_k, prefix_v, cache: BranchCache, tokens: torch.Tensor,
+                     next_token: torch.Tensor, p_top: torch.Tensor, conf: torch.Tensor, workspace: torch.Tensor,
+                     stream=None) -> None:
+    """Marshal torch device tensors into rksc_decode_step (asynchronous on `stream`)."""
+    lib = load_library()
+    w, layers_keepalive = _weights_struct(weights)
+    n = int(prefix_k.shape[2]) if prefix_k is not None else 0
+    kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
+    st = lib.rksc_decode_step(ctypes.byref(w), ctypes.byref(kv), ctypes.byref(cache.struct), _ptr(tokens),
+                              int(tokens.numel()), _ptr(next_token), _ptr(p_top), _ptr(conf), _ptr(workspace),
+                              int(workspace.numel() * workspace.element_size()), _stream(stream))
+    del layers_keepalive
+    _check(st)
+
+
+def rksc_cgee_gate(conf: torch.Tensor, n_steps: int, tau_conf: float, r_gap: float, p_mean: Optional[torch.Tensor],
+                   fired: torch.Tensor, winner: torch.Tensor, stats: Optional[torch.Tensor], stream=None) -> None:
+    """Marshal torch device tensors into rksc_cgee_gate (asynchronous on `stream`)."""
+    st = load_library().rksc_cgee_gate(_ptr(conf), int(conf.numel()), int(n_steps), float(tau_conf), float(r_gap),
+                                       _ptr(p_mean), _ptr(fired), _ptr(winner), _ptr(stats), _stream(stream))
+    _check(st)
+
+
+def cgee_gate(conf: torch.Tensor, n_steps: int, tau_conf: float = 0.70, r_gap: float = 0.06, stream=None):
+    """Eq. cgee_gate on the device: returns (fired [1] int32, winner [1] int32, p_mean [B], stats [3]) tensors."""
+    dev = conf.device
+    fired = torch.empty((1,), dtype=torch.int32, device=dev)
+    winner = torch.empty((1,), dtype=torch.int32, device=dev)
+    p_mean = torch.empty_like(conf)
+    stats = torch.empty((3,), dtype=torch.float32, device=dev)
+    rksc_cgee_gate(conf, n_steps, tau_conf, r_gap, p_mean, fired, winner, stats, stream)
+    return fired, winner, p_mean, stats
+
+
+class Decoder:
+    """The stepwise batched decode loop over a shared prefix cache: allocates the
+    branch cache, the workspace and the running confidence once, then
+    `suffix(tokens [B, s])` and `step(tokens [B])` run rksc_decode_suffix /
+    rksc_decode_step; `n_steps` counts the tokens generated (the t of Eq. gen_conf)."""
+
+    def __init__(self, weights, prefix_k, prefix_v, n_branches: int, suffix_len: int, capacity: int, device):
+        shape = weights.shape
+        self.weights, self.prefix_k, self.prefix_v = weights, prefix_k, prefix_v
+        n = int(prefix_k.shape[2]) if prefix_k is not None else 0
+        self.cache = BranchCache(shape, len(weights.layers), n_branches, capacity, device)
+        self.workspace = torch.empty(rksc_decode_workspace_size(shape, n_branches, suffix_len, n),
+                                     dtype=torch.uint8, device=device)
+        self.next_token = torch.empty((n_branches,), dtype=torch.int32, device=device)
+        self.p_top = torch.empty((n_branches,), dtype=torch.float32, device=device)
+        self.conf = torch.zeros((n_branches,), dtype=torch.float32, device=device)
+        self.n_steps = 0
+
+    def suffix(self, suffix_tokens: torch.Tensor, stream=None):
+        rksc_decode_suffix(self.weights, self.prefix_k, self.prefix_v, self.cache, suffix_tokens.contiguous(),
+                           self.next_token, self.p_top, self.conf, self.workspace, stream)
+        self.n_steps = 1
+        return self.next_token, self.p_top
+
+    def step(self, tokens: Optional[torch.Tensor] = None, stream=None):
+        """One decode step; tokens defaults to the previous step's next_token (greedy)."""
+        tok = self.next_token if tokens is None else tokens.contiguous()
+        rksc_decode_step(self.weights, self.prefix_k, self.prefix_v, self.cache, tok, self.next_token,
+                         self.p_top, self.conf, self.workspace, stream)
+        self.n_steps += 1
+        return self.next_token, self.p_top
+
+    def gate(self, tau_conf: float = 0.70, r_gap: float = 0.06, stream=None):
+        return cgee_gate(self.conf, self.n_steps, tau_conf, r_gap, stream)

@@ -650,6 +650,171 @@ __global__ __launch_bounds__(256) void k_attn_combine_own(const float* __restric
   }
 }
 
+// Decode merge: one new token per branch (s = 1). One wave per (branch, head)
+// combines the prefix partials of the split-KV chunks with the branch's own
+// keys -- its cached entries 0..len-1 (bf16) and the new token's own key
+// (fp32, entry len) -- in log2 units:
+// o = (sum_c 2^{m_c - M} o_c + sum_j 2^{t_j - M} v_j) / (sum_c 2^{m_c - M} l_c + sum_j 2^{t_j - M}),
+// t_j = log2(e)/sqrt(hd) q.k_j. The own keys are scored 64 at a time, one per
+// lane (16-byte loads of the key row; the query address is wave-uniform), with
+// an online maximum across the blocks of 64.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_combine_dec(const float* __restrict__ opart,
+                                                          const float* __restrict__ mlpart,
+                                                          const float* __restrict__ q, const bf16* __restrict__ ck,
+                                                          const bf16* __restrict__ cv, int len, int cap,
+                                                          const float* __restrict__ ko, const float* __restrict__ vo,
+                                                          void* __restrict__ o, const Ctrl* c, int H, int Hkv,
+                                                          float sl2, int nchunks, int max_rows) {
+  constexpr int E = HD / 64;   // dimensions per lane
+  const int rows = c->live_count * H;
+  const int wid = (blockIdx.x * blockDim.x + threadIdx.x) >> 6, lane = threadIdx.x & 63;
+  if (wid >= rows) return;
+  const int b = wid / H, h = wid - b * H, kvh = h / (H / Hkv);
+  const float* qr = q + (size_t)wid * HD;
+  const bf16* kb = ck + ((size_t)b * Hkv + kvh) * cap * HD;
+  const bf16* vb = cv + ((size_t)b * Hkv + kvh) * cap * HD;
+  const float* kc = ko + ((size_t)b * Hkv + kvh) * HD;   // the new token's own key (s = 1)
+  const float* vc = vo + ((size_t)b * Hkv + kvh) * HD;
+  float Mr = -INFINITY, den = 0.f, acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  const int nkeys = len + 1;
+  for (int j0 = 0; j0 < nkeys; j0 += 64) {
+    const int j = j0 + lane;
+    float t = -INFINITY;
+    if (j < len) {
+      const uint4* kr = reinterpret_cast<const uint4*>(kb + (size_t)j * HD);
+      float dot = 0.f;
+#pragma unroll
+      for (int u = 0; u < HD / 8; ++u) {
+        const uint4 w = kr[u];
+        const float4 qa = *reinterpret_cast<const float4*>(qr + 8 * u);
+        const float4 qb = *reinterpret_cast<const float4*>(qr + 8 * u + 4);
+        dot = fmaf(qa.x, __uint_as_float(w.x << 16), dot);
+        dot = fmaf(qa.y, __uint_as_float(w.x & 0xffff0000u), dot);
+        dot = fmaf(qa.z, __uint_as_float(w.y << 16), dot);
+        dot = fmaf(qa.w, __uint_as_float(w.y & 0xffff0000u), dot);
+        dot = fmaf(qb.x, __uint_as_float(w.z << 16), dot);
+        dot = fmaf(qb.y, __uint_as_float(w.z & 0xffff0000u), dot);
+        dot = fmaf(qb.z, __uint_as_float(w.w << 16), dot);
+        dot = fmaf(qb.w, __uint_as_float(w.w & 0xffff0000u), dot);
+      }
+      t = dot * sl2;
+    } else if (j == len) {
+      float dot = 0.f;
+#pragma unroll 8
+      for (int dd = 0; dd < HD; ++dd) dot = fmaf(qr[dd], kc[dd], dot);
+      t = dot * sl2;
+    }
+    float bm = t;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) bm = fmaxf(bm, __shfl_xor(bm, off, 64));
+    const float Mn = fmaxf(Mr, bm);   // finite: every block holds at least one key
+    const float alpha = __builtin_amdgcn_exp2f(Mr - Mn);   // Mr = -inf gives 0
+    const float p = j < nkeys ? __builtin_amdgcn_exp2f(t - Mn) : 0.f;
+    float ps = p;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) ps += __shfl_xor(ps, off, 64);
+    den = den * alpha + ps;
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] *= alpha;
+    const int cnt = min(64, nkeys - j0);
+    for (int u = 0; u < cnt; ++u) {
+      const float pu = __shfl(p, u, 64);
+      const int ju = j0 + u;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const float v = ju < len ? __uint_as_float((uint32_t)__builtin_bit_cast(uint16_t, vb[(size_t)ju * HD + lane + 64 * e]) << 16)
+                                 : vc[lane + 64 * e];
+        acc[e] = fmaf(pu, v, acc[e]);
+      }
+    }
+    Mr = Mn;
+  }
+  // The prefix chunks' partials (zeros where a chunk saw no key).
+  const size_t cstride = (size_t)max_rows * H;
+  float Mx = Mr;
+  for (int c0 = 0; c0 < nchunks; c0 += 64) {
+    const int ch = c0 + lane;
+    float M = ch < nchunks ? mlpart[(ch * cstride + wid) * 2] : -INFINITY;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+    Mx = fmaxf(Mx, M);
+  }
+  const float own_w = __builtin_amdgcn_exp2f(Mr - Mx);
+  den *= own_w;
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] *= own_w;
+  for (int c0 = 0; c0 < nchunks; c0 += 64) {
+    const int ch = c0 + lane;
+    float w = 0.f, wl = 0.f;
+    if (ch < nchunks) {
+      const float2 ml = *reinterpret_cast<const float2*>(mlpart + (ch * cstride + wid) * 2);
+      w = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - Mx);
+      wl = w * ml.y;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) wl += __shfl_xor(wl, off, 64);
+    den += wl;
+    const int cn = min(64, nchunks - c0);
+    for (int k = 0; k < cn; ++k) {
+      const float wk = __shfl(w, k, 64);
+      const float* op = opart + ((size_t)(c0 + k) * cstride + wid) * HD;
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] = fmaf(wk, op[lane + 64 * e], acc[e]);
+    }
+  }
+  const float inv = 1.f / den;
+  const size_t plane = (size_t)max_rows * H * HD;
+  uint16_t* ob = reinterpret_cast<uint16_t*>(o);
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    uint16_t hb, lb;
+    split2(acc[e] * inv, hb, lb);
+    ob[(size_t)wid * HD + lane + 64 * e] = hb;
+    ob[plane + (size_t)wid * HD + lane + 64 * e] = lb;
+  }
+}
+
+// fp32 models, decode: one thread per (branch, head) over the prefix, the
+// branch's cached entries 0..len-1 and its own new key.
+template <int HD>
+__global__ __launch_bounds__(128) void k_attn_f32_dec(const float* __restrict__ q, const float* __restrict__ pk,
+                                                      const float* __restrict__ pv, const float* __restrict__ ck,
+                                                      const float* __restrict__ cv, int len, int cap,
+                                                      const float* __restrict__ ko, const float* __restrict__ vo,
+                                                      float* __restrict__ o, const Ctrl* c, int n, int H, int Hkv,
+                                                      float scale) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= c->live_count * H) return;
+  const int b = idx / H, h = idx % H;
+  const int kvh = h / (H / Hkv);
+  const float* qr = q + (size_t)idx * HD;
+  float acc[HD];
+  for (int d = 0; d < HD; ++d) acc[d] = 0.f;
+  float m = -INFINITY, l = 0.f;
+  auto visit = [&](const float* kr, const float* vr) {
+    float sc = 0.f;
+    for (int d = 0; d < HD; ++d) sc = fmaf(qr[d], kr[d], sc);
+    sc *= scale;
+    const float mn = fmaxf(m, sc);
+    const float a = expf(m - mn), p = expf(sc - mn);
+    l = l * a + p;
+    for (int d = 0; d < HD; ++d) acc[d] = acc[d] * a + p * vr[d];
+    m = mn;
+  };
+  const float* Kp = pk + (size_t)kvh * n * HD;
+  const float* Vp = pv + (size_t)kvh * n * HD;
+  for (int j = 0; j < n; ++j) visit(Kp + (size_t)j * HD, Vp + (size_t)j * HD);
+  const float* Kc = ck + ((size_t)b * Hkv + kvh) * cap * HD;
+  const float* Vc = cv + ((size_t)b * Hkv + kvh) * cap * HD;
+  for (int j = 0; j < len; ++j) visit(Kc + (size_t)j * HD, Vc + (size_t)j * HD);
+  visit(ko + ((size_t)b * Hkv + kvh) * HD, vo + ((size_t)b * Hkv + kvh) * HD);
+  float* orow = o + (size_t)idx * HD;
+  for (int d = 0; d < HD; ++d) orow[d] = acc[d] / l;
+}
+
 // fp32 models: one thread per (query row, head), plain online softmax.
 template <int HD>
 __global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ q, const float* __restrict__ pk,
@@ -710,6 +875,49 @@ AttnPlan plan_attention(DType dt, int B, int n, int s, int H, int Hkv) {
   while (base * p.chunks < kComputeUnits && (p.chunks + 1) * 2 <= min_tiles) ++p.chunks;
   p.partials = (p.cross || p.chunks > 1) ? p.chunks : 0;
   return p;
+}
+
+hipError_t launch_attention_decode(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,
+                                   const void* ck, const void* cv, int len, int cap, const void* k_own,
+                                   const void* v_own, void* o, float* opart, float* mlpart, const Ctrl* c, int n,
+                                   int H, int Hkv, int hd, int B, hipStream_t st) {
+  const float* qq = static_cast<const float*>(q);
+  const float *ko = static_cast<const float*>(k_own), *vo = static_cast<const float*>(v_own);
+  if (dt == DType::BF16) {
+    const float sl2 = 1.4426950408889634f / sqrtf((float)hd);
+    const int G = H / Hkv;
+    const int max_rows = B;   // one token per branch
+    const bf16 *kk = static_cast<const bf16*>(pk), *vv = static_cast<const bf16*>(pv);
+    const bf16 *cka = static_cast<const bf16*>(ck), *cva = static_cast<const bf16*>(cv);
+    if (p.chunks > 0) {
+      const dim3 grid((max_rows * G + 16 * kAttnWaves - 1) / (16 * kAttnWaves), Hkv, p.chunks);
+      if (hd == 128)
+        hipLaunchKernelGGL((k_attn_bf16<128, true>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, o, opart,
+                           mlpart, c, n, 1, H, Hkv, sl2, p.chunks, max_rows);
+      else
+        hipLaunchKernelGGL((k_attn_bf16<64, true>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, o, opart,
+                           mlpart, c, n, 1, H, Hkv, sl2, p.chunks, max_rows);
+    }
+    const dim3 cgrid((B * H * 64 + 255) / 256);
+    if (hd == 128)
+      hipLaunchKernelGGL(k_attn_combine_dec<128>, cgrid, dim3(256), 0, st, opart, mlpart, qq, cka, cva, len,
+                         cap, ko, vo, o, c, H, Hkv, sl2, p.chunks, max_rows);
+    else
+      hipLaunchKernelGGL(k_attn_combine_dec<64>, cgrid, dim3(256), 0, st, opart, mlpart, qq, cka, cva, len,
+                         cap, ko, vo, o, c, H, Hkv, sl2, p.chunks, max_rows);
+  } else {
+    const float scale = 1.f / sqrtf((float)hd);
+    const dim3 grid((B * H + 127) / 128);
+    const float *kk = static_cast<const float*>(pk), *vv = static_cast<const float*>(pv);
+    const float *cka = static_cast<const float*>(ck), *cva = static_cast<const float*>(cv);
+    if (hd == 128)
+      hipLaunchKernelGGL(k_attn_f32_dec<128>, grid, dim3(128), 0, st, qq, kk, vv, cka, cva, len, cap, ko, vo,
+                         static_cast<float*>(o), c, n, H, Hkv, scale);
+    else
+      hipLaunchKernelGGL(k_attn_f32_dec<64>, grid, dim3(128), 0, st, qq, kk, vv, cka, cva, len, cap, ko, vo,
+                         static_cast<float*>(o), c, n, H, Hkv, scale);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,

@@ -71,6 +71,32 @@ __device__ __forceinline__ void fold4(EntStats& st, const floatx4& z, int row0, 
   st = EntStats{mn, s_new, t_new};
 }
 
+// fold4 that also keeps the vocabulary index of the running maximum (the
+// greedy token): the first row among equal maxima wins, as rows are visited in
+// increasing order within a lane and merges keep the smaller index on ties.
+__device__ __forceinline__ void fold4_am(EntStats& st, int& am, const floatx4& z, int row0, int V) {
+  float mx = -INFINITY;
+  int ix = 0x7fffffff;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (row0 + i < V && z[i] > mx) {
+      mx = z[i];
+      ix = row0 + i;
+    }
+  if (mx == -INFINITY) return;
+  if (mx > st.m) am = ix;
+  else if (mx == st.m) am = min(am, ix);
+  fold4(st, z, row0, V);
+}
+
+// Index of the larger maximum of two (statistics, index) pairs; the smaller
+// index on equal maxima; an empty side (m = -inf) has no index.
+__device__ __forceinline__ int merge_am(const EntStats& a, int ia, const EntStats& b, int ib) {
+  if (b.m > a.m) return ib;
+  if (b.m < a.m) return ia;
+  return min(ia, ib);
+}
+
 // lm_head stream through an R-deep LDS ring fed by direct DMA.
 //
 // The unit of the ring is 16 rows x 1 KB: a 512-wide K slice of 16 vocabulary
@@ -106,9 +132,11 @@ constexpr int kEntRing = 7;
 constexpr int kEntWaves8 = 8;                         // waves per workgroup
 constexpr int kEntRedTiles = 4;                       // tiles per wave per reduction round
 constexpr int kRedBytes = kEntWaves8 * kEntRedTiles * 1024;
-constexpr int kFinBytes = kEntWaves8 * 16 * 12;       // one triple per column per wave
+constexpr int kFinBytes = kEntWaves8 * 16 * 16;       // one triple (+ argmax) per column per wave
 
-template <int NCB, int G, int R>
+// AM: also track the argmax (greedy token) and write (m, s, t, index) per
+// column instead of the triple.
+template <int NCB, int G, int R, bool AM>
 __global__ __launch_bounds__(512) void k_entropy_bf16(const bf16* __restrict__ W, const bf16* __restrict__ hi,
                                                       const bf16* __restrict__ lo, const Ctrl* c, int V, int d,
                                                       float* __restrict__ parts) {
@@ -182,6 +210,7 @@ __global__ __launch_bounds__(512) void k_entropy_bf16(const bf16* __restrict__ W
 
   const bf16x8 zero = {};
   EntStats st = ent_empty();
+  int am = 0x7fffffff;
   bf16x8 hreg[2][8];
   floatx4 acc[LT];
   for (int gi = 0; gi < ng; ++gi) {
@@ -240,7 +269,8 @@ __global__ __launch_bounds__(512) void k_entropy_bf16(const bf16* __restrict__ W
           const int ii = (rr * kEntRedTiles + m) * TPW + own;
           if (ii < gt) {
             const floatx4 z = acc[rr * kEntRedTiles + m] + red[(wid * kEntRedTiles + m) * 64 + lane];
-            fold4(st, z, 16 * (t0 + gi * G + ii) + 4 * g, V);
+            if constexpr (AM) fold4_am(st, am, z, 16 * (t0 + gi * G + ii) + 4 * g, V);
+            else fold4(st, z, 16 * (t0 + gi * G + ii) + 4 * g, V);
           }
         }
       }
@@ -253,26 +283,45 @@ __global__ __launch_bounds__(512) void k_entropy_bf16(const bf16* __restrict__ W
 #pragma unroll
   for (int off = 16; off < 64; off <<= 1) {
     EntStats o{__shfl_xor(st.m, off, 64), __shfl_xor(st.s, off, 64), __shfl_xor(st.t, off, 64)};
+    if constexpr (AM) am = merge_am(st, am, o, __shfl_xor(am, off, 64));
     st = ent_merge(st, o);
   }
   EntStats* fin = reinterpret_cast<EntStats*>(smem + R * kUnitBytes + kRedBytes);
-  if (lane < 16) fin[wid * 16 + lane] = st;
+  int* fin_am = reinterpret_cast<int*>(fin + NW * 16);
+  if (lane < 16) {
+    fin[wid * 16 + lane] = st;
+    if constexpr (AM) fin_am[wid * 16 + lane] = am;
+  }
   __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the triples are in LDS
   __builtin_amdgcn_s_barrier();
   const int col = tid;
   if (col < 16 * NCB && col < Bl) {
     const int cb = col >> 4;
     EntStats v = fin[cb * 16 + (col & 15)];
+    int va = AM ? fin_am[cb * 16 + (col & 15)] : 0;
 #pragma unroll
-    for (int p = 1; p < NW / NCB; ++p) v = ent_merge(v, fin[(p * NCB + cb) * 16 + (col & 15)]);
-    float* pp = parts + ((size_t)blockIdx.x * 64 + col) * 3;
-    pp[0] = v.m;
-    pp[1] = v.s;
-    pp[2] = v.t;
+    for (int p = 1; p < NW / NCB; ++p) {
+      const EntStats o = fin[(p * NCB + cb) * 16 + (col & 15)];
+      if constexpr (AM) va = merge_am(v, va, o, fin_am[(p * NCB + cb) * 16 + (col & 15)]);
+      v = ent_merge(v, o);
+    }
+    if constexpr (AM) {
+      float* pp = parts + ((size_t)blockIdx.x * 64 + col) * 4;
+      pp[0] = v.m;
+      pp[1] = v.s;
+      pp[2] = v.t;
+      pp[3] = __int_as_float(va);
+    } else {
+      float* pp = parts + ((size_t)blockIdx.x * 64 + col) * 3;
+      pp[0] = v.m;
+      pp[1] = v.s;
+      pp[2] = v.t;
+    }
   }
 }
 
 // fp32 models: each wave takes whole vocabulary rows, lanes stride over d.
+template <bool AM>
 __global__ __launch_bounds__(256) void k_entropy_f32(const float* __restrict__ W, const float* __restrict__ hn,
                                                      const Ctrl* c, int V, int d, float* __restrict__ parts) {
   const int Bl = c->live_count;
@@ -280,6 +329,7 @@ __global__ __launch_bounds__(256) void k_entropy_f32(const float* __restrict__ W
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   // Branch column `col` is owned by lane `col` (at most 64 branches).
   EntStats own = ent_empty();
+  int own_am = 0x7fffffff;
   for (int row = blockIdx.x * kEntWaves + wid; row < V; row += gridDim.x * kEntWaves) {
     const float* wr = W + (size_t)row * d;
     for (int col = 0; col < Bl; ++col) {
@@ -289,21 +339,36 @@ __global__ __launch_bounds__(256) void k_entropy_f32(const float* __restrict__ W
       acc = wave_sum(acc);
       if (lane == col) {
         float z = acc;
+        if (AM && z > own.m) own_am = row;   // rows ascend within a wave: the first maximum is kept
         stats_fold(own, z, &z, 1);
       }
     }
   }
   __shared__ EntStats red[kEntWaves][64];
+  __shared__ int red_am[kEntWaves][64];
   red[wid][lane] = own;
+  red_am[wid][lane] = own_am;
   __syncthreads();
   const int col = threadIdx.x;
   if (col < Bl) {
     EntStats v = red[0][col];
-    for (int w = 1; w < kEntWaves; ++w) v = ent_merge(v, red[w][col]);
-    float* p = parts + ((size_t)blockIdx.x * 64 + col) * 3;
-    p[0] = v.m;
-    p[1] = v.s;
-    p[2] = v.t;
+    int va = red_am[0][col];
+    for (int w = 1; w < kEntWaves; ++w) {
+      if (AM) va = merge_am(v, va, red[w][col], red_am[w][col]);
+      v = ent_merge(v, red[w][col]);
+    }
+    if (AM) {
+      float* p = parts + ((size_t)blockIdx.x * 64 + col) * 4;
+      p[0] = v.m;
+      p[1] = v.s;
+      p[2] = v.t;
+      p[3] = __int_as_float(va);
+    } else {
+      float* p = parts + ((size_t)blockIdx.x * 64 + col) * 3;
+      p[0] = v.m;
+      p[1] = v.s;
+      p[2] = v.t;
+    }
   }
 }
 
@@ -324,11 +389,13 @@ int entropy_parts(DType dt, int V, int max_branches) {
   return tiles < grid ? tiles : grid;
 }
 
-hipError_t launch_entropy(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c, int V, int d,
-                          int max_branches, float* parts, hipStream_t st) {
+namespace {
+template <bool AM>
+hipError_t launch_entropy_t(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c, int V,
+                            int d, int max_branches, float* parts, hipStream_t st) {
   const int blocks = entropy_parts(dt, V, max_branches);
   if (dt == DType::F32) {
-    hipLaunchKernelGGL(k_entropy_f32, dim3(blocks), dim3(256), 0, st, static_cast<const float*>(W),
+    hipLaunchKernelGGL(k_entropy_f32<AM>, dim3(blocks), dim3(256), 0, st, static_cast<const float*>(W),
                        static_cast<const float*>(hn_a), c, V, d, parts);
     return hipGetLastError();
   }
@@ -337,16 +404,30 @@ hipError_t launch_entropy(DType dt, const void* W, const void* hn_a, const void*
   const bf16* b = static_cast<const bf16*>(hn_b);
   switch (ent_ncb(max_branches)) {
     case 1:
-      hipLaunchKernelGGL((k_entropy_bf16<1, 32, kEntRing>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d, parts);
+      hipLaunchKernelGGL((k_entropy_bf16<1, 32, kEntRing, AM>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d,
+                         parts);
       break;
     case 2:
-      hipLaunchKernelGGL((k_entropy_bf16<2, 32, kEntRing>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d, parts);
+      hipLaunchKernelGGL((k_entropy_bf16<2, 32, kEntRing, AM>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d,
+                         parts);
       break;
     default:
-      hipLaunchKernelGGL((k_entropy_bf16<4, 16, kEntRing>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d, parts);
+      hipLaunchKernelGGL((k_entropy_bf16<4, 16, kEntRing, AM>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d,
+                         parts);
       break;
   }
   return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_entropy(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c, int V, int d,
+                          int max_branches, float* parts, hipStream_t st) {
+  return launch_entropy_t<false>(dt, W, hn_a, hn_b, c, V, d, max_branches, parts, st);
+}
+
+hipError_t launch_entropy_argmax(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c, int V,
+                                 int d, int max_branches, float* parts, hipStream_t st) {
+  return launch_entropy_t<true>(dt, W, hn_a, hn_b, c, V, d, max_branches, parts, st);
 }
 
 }  // namespace rksc

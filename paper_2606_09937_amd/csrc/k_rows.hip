@@ -313,6 +313,72 @@ __global__ __launch_bounds__(256) void k_finalize_exit(const float* parts, int n
   }
 }
 
+// ------------------------------------------------------------------ batched decode
+
+// Index of the larger maximum of two (statistics, index) pairs; the smaller
+// index on equal maxima.
+__device__ __forceinline__ int merge_argmax(const EntStats& a, int ia, const EntStats& b, int ib) {
+  if (b.m > a.m) return ib;
+  if (b.m < a.m) return ia;
+  return min(ia, ib);
+}
+
+// Greedy token and top-1 probability of each branch's logits from the
+// per-workgroup (m, s, t, argmax) of the lm_head stream (Eq. gen_conf's
+// max_v Pr[y = v] = e^(z_max - LSE) = 1 / s). Fixed reduction order.
+__global__ __launch_bounds__(256) void k_finalize_decode(const float* parts, int nparts, int B, int* next_token,
+                                                         float* p_top, float* conf, int accumulate) {
+  __shared__ EntStats red[256];
+  __shared__ int red_am[256];
+  const int tid = threadIdx.x;
+  for (int col = 0; col < B; ++col) {
+    EntStats st = ent_empty();
+    int am = 0x7fffffff;
+    for (int p = tid; p < nparts; p += blockDim.x) {
+      const float* q = parts + ((size_t)p * 64 + col) * 4;
+      const EntStats o{q[0], q[1], q[2]};
+      am = merge_argmax(st, am, o, __float_as_int(q[3]));
+      st = ent_merge(st, o);
+    }
+    red[tid] = st;
+    red_am[tid] = am;
+    __syncthreads();
+    for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+      if (tid < off) {
+        red_am[tid] = merge_argmax(red[tid], red_am[tid], red[tid + off], red_am[tid + off]);
+        red[tid] = ent_merge(red[tid], red[tid + off]);
+      }
+      __syncthreads();
+    }
+    if (tid == 0) {
+      const bool ok = red[0].m != -INFINITY && red_am[0] != 0x7fffffff;
+      const float p = ok ? 1.f / red[0].s : __builtin_nanf("");
+      next_token[col] = ok ? red_am[0] : -1;
+      p_top[col] = p;
+      if (conf) conf[col] = accumulate ? conf[col] + p : p;
+    }
+    __syncthreads();
+  }
+}
+
+// Branch cache entries off..off+s-1 of one layer from the branches' fp32 keys
+// (already rotated) and values: 4 elements per thread.
+template <typename T>
+__global__ __launch_bounds__(256) void k_store_branch_kv(const float* __restrict__ k_own,
+                                                         const float* __restrict__ v_own, T* __restrict__ k_dst,
+                                                         T* __restrict__ v_dst, int s, int hd, int cap, int off,
+                                                         size_t elems) {
+  const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= elems) return;
+  const size_t bh = i / ((size_t)s * hd);           // branch * Hkv + kv head
+  const size_t rem = i - bh * s * hd;
+  const size_t dst = (bh * cap + off) * hd + rem;   // entry off + rem / hd, element rem % hd
+  const float4 a = *reinterpret_cast<const float4*>(k_own + i);
+  const float4 b = *reinterpret_cast<const float4*>(v_own + i);
+  store4(k_dst + dst, a.x, a.y, a.z, a.w);
+  store4(v_dst + dst, b.x, b.y, b.z, b.w);
+}
+
 // ------------------------------------------------------------------ root forward
 
 // The prefix cache in the model's storage type from the fp32 keys/values of the
@@ -339,7 +405,74 @@ __global__ __launch_bounds__(256) void k_unit_rows(float* __restrict__ x, int d)
   for (int c = threadIdx.x; c < d; c += blockDim.x) row[c] *= inv;
 }
 
+// Eq. cgee_gate over the generation confidences p_b = conf_b / n_steps
+// (Eq. gen_conf), one lane per branch: fires when max_b p >= tau_conf and
+// (max - 2nd max) / max >= r_gap. The winner is the smallest index holding the
+// maximum; the 2nd max is the largest p among the other branches (0 when there
+// is none, so one branch is gated by tau_conf alone). NaN entries are ignored;
+// with no valid entry the gate does not fire and winner = -1.
+__global__ __launch_bounds__(64) void k_cgee_gate(const float* conf, int B, int n_steps, float tau_conf, float r_gap,
+                                                  float* p_mean, int* fired, int* winner, float* stats) {
+  const int lane = threadIdx.x;
+  const float p = lane < B ? conf[lane] / (float)n_steps : __builtin_nanf("");
+  if (p_mean && lane < B) p_mean[lane] = p;
+  const bool valid = p == p;
+  float m = valid ? p : -INFINITY;
+  int idx = valid ? lane : 0x7fffffff;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float om = __shfl_xor(m, off, 64);
+    const int oi = __shfl_xor(idx, off, 64);
+    if (om > m || (om == m && oi < idx)) {
+      m = om;
+      idx = oi;
+    }
+  }
+  float q = valid && lane != idx ? p : -INFINITY;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) q = fmaxf(q, __shfl_xor(q, off, 64));
+  if (lane == 0) {
+    const bool any = idx != 0x7fffffff;
+    const float second = q == -INFINITY ? 0.f : q;
+    const float gap = any && m > 0.f ? (m - second) / m : 0.f;
+    fired[0] = any && m >= tau_conf && gap >= r_gap ? 1 : 0;
+    winner[0] = any ? idx : -1;
+    if (stats) {
+      stats[0] = any ? m : __builtin_nanf("");
+      stats[1] = second;
+      stats[2] = gap;
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_finalize_decode(const float* parts, int nparts, int B, int* next_token, float* p_top, float* conf,
+                                  int accumulate, hipStream_t st) {
+  hipLaunchKernelGGL(k_finalize_decode, dim3(1), dim3(256), 0, st, parts, nparts, B, next_token, p_top, conf,
+                     accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_cgee_gate(const float* conf, int B, int n_steps, float tau_conf, float r_gap, float* p_mean,
+                            int* fired, int* winner, float* stats, hipStream_t st) {
+  hipLaunchKernelGGL(k_cgee_gate, dim3(1), dim3(64), 0, st, conf, B, n_steps, tau_conf, r_gap, p_mean, fired, winner,
+                     stats);
+  return hipGetLastError();
+}
+
+hipError_t launch_store_branch_kv(DType dt, const float* k_own, const float* v_own, void* k_dst, void* v_dst, int B,
+                                  int Hkv, int s, int hd, int cap, int off, hipStream_t st) {
+  const size_t elems = (size_t)B * Hkv * s * hd;
+  const dim3 grid((unsigned)((elems / 4 + 255) / 256));
+  if (dt == DType::BF16)
+    hipLaunchKernelGGL(k_store_branch_kv<bf16>, grid, dim3(256), 0, st, k_own, v_own, static_cast<bf16*>(k_dst),
+                       static_cast<bf16*>(v_dst), s, hd, cap, off, elems);
+  else
+    hipLaunchKernelGGL(k_store_branch_kv<float>, grid, dim3(256), 0, st, k_own, v_own, static_cast<float*>(k_dst),
+                       static_cast<float*>(v_dst), s, hd, cap, off, elems);
+  return hipGetLastError();
+}
 
 hipError_t launch_store_kv(DType dt, const float* k_own, const float* v_own, void* k_dst, void* v_dst,
                            size_t elems, hipStream_t st) {

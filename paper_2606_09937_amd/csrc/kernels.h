@@ -88,10 +88,37 @@ hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const vo
 int entropy_parts(DType dt, int V, int max_branches);
 hipError_t launch_entropy(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c,
                           int V, int d, int max_branches, float* parts, hipStream_t st);
+// As launch_entropy, plus the vocabulary index of each column's maximum logit:
+// parts become [grid, 64, 4] = (m, s, t, argmax as int bits).
+hipError_t launch_entropy_argmax(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c, int V,
+                                 int d, int max_branches, float* parts, hipStream_t st);
+// Merges [nparts, 64, 4] statistics of B columns: next_token = argmax (smallest
+// index among equal maxima; -1 if no finite logit), p_top = 1 / sum e^(z - max)
+// (the top-1 softmax probability); conf = p_top (accumulate = 0) or conf + p_top.
+hipError_t launch_finalize_decode(const float* parts, int nparts, int B, int* next_token, float* p_top, float* conf,
+                                  int accumulate, hipStream_t st);
 // Merges the partial statistics, writes entropy[l-1][branch], applies the exit
 // rule and compacts the live list.
 hipError_t launch_finalize_exit(const float* parts, int nparts, Ctrl* c, int layer1, int L, int B,
                                 float tau, int patience, float* entropy, int* exit_layer, hipStream_t st);
+
+// ---- batched decode
+// Branch cache of one layer [B, Hkv, cap, hd] (model dtype): entries off..off+s-1
+// from the fp32 k_own/v_own [B, Hkv, s, hd].
+hipError_t launch_store_branch_kv(DType dt, const float* k_own, const float* v_own, void* k_dst, void* v_dst, int B,
+                                  int Hkv, int s, int hd, int cap, int off, hipStream_t st);
+// Attention of one new token per branch (s = 1) over the shared prefix (split-KV
+// plan p, cross mode), the branch's cached entries 0..len-1 (model dtype, layer
+// base [B, Hkv, cap, hd]) and its own key/value (fp32 k_own/v_own [B, Hkv, 1, hd]).
+hipError_t launch_attention_decode(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,
+                                   const void* ck, const void* cv, int len, int cap, const void* k_own,
+                                   const void* v_own, void* o, float* opart, float* mlpart, const Ctrl* c, int n,
+                                   int H, int Hkv, int hd, int B, hipStream_t st);
+
+// Level-1 / decode-level gate of Eq. cgee_gate over p = conf / n_steps of B <= 64
+// branches; stats = (max, 2nd max, gap ratio) when not NULL.
+hipError_t launch_cgee_gate(const float* conf, int B, int n_steps, float tau_conf, float r_gap, float* p_mean,
+                            int* fired, int* winner, float* stats, hipStream_t st);
 
 // ---- root forward (prefill)
 // k_dst/v_dst [Hkv, n, hd] of the model dtype from the fp32 k_own/v_own of one branch.

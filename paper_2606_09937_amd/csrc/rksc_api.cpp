@@ -110,7 +110,7 @@ rksc_status make_layout(const rksc_model_config* c, int B, int s, int n_prefix, 
   lay->pres = take((size_t)sres * Ms * d * 4);
   lay->hn_a = take((size_t)RKSC_MAX_BRANCHES * d * (dt == DType::BF16 ? 2 : 4));
   lay->hn_b = take((size_t)RKSC_MAX_BRANCHES * d * 2);
-  lay->parts = take((size_t)lay->nparts * 64 * 3 * 4);
+  lay->parts = take((size_t)lay->nparts * 64 * 4 * 4);   // (m, s, t[, argmax]) per column
   lay->rope = take((size_t)s * (hd / 2) * 8);
   lay->attn = rksc::plan_attention(dt, B, n_prefix, s, H, Hkv);
   const size_t nch = (size_t)lay->attn.partials;
@@ -398,6 +398,173 @@ RKSC_EXPORT rksc_status rksc_prefill(const rksc_weights* w, const int32_t* token
                              c->rms_eps, ws + lay.hn_a, ws + lay.hn_b, 1, strm));
   }
   HIP_TRY(rksc::launch_unit_rows(h_root, L, d, strm));
+  return ok();
+}
+
+RKSC_EXPORT size_t rksc_decode_workspace_size(const rksc_model_config* cfg, int32_t n_branches, int32_t suffix_len,
+                                             int32_t n_prefix) {
+  if (n_prefix < 0) {
+    fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", n_prefix);
+    return 0;
+  }
+  Layout a, b;
+  if (make_layout(cfg, n_branches, suffix_len, n_prefix, &a) != RKSC_OK) return 0;
+  if (make_layout(cfg, n_branches, 1, n_prefix, &b) != RKSC_OK) return 0;
+  return a.total > b.total ? a.total : b.total;
+}
+
+namespace {
+
+// Batched decode over the shared prefix (Sec. 2.2, "KV broadcast and batched
+// decode"; the stepwise loop of the implementation notes): s tokens per branch
+// at positions n + len .. n + len + s - 1 through all L layers, each attending
+// to the prefix cache, to the branch's cached entries 0..len-1 and, causally, to
+// its own new tokens, whose keys and values are appended to the branch cache.
+// After the last layer the last token's logits give the next token (argmax)
+// and its top-1 probability, summed into conf for Eq. gen_conf. `step` selects
+// the one-token kernels (s = 1, any len); otherwise len must be 0.
+rksc_status decode_impl(const rksc_weights* w, const rksc_prefix_kv* kv, rksc_branch_kv* bkv, const int32_t* tokens,
+                        int32_t n_branches, int32_t s, bool step, int32_t* next_token, float* p_top, float* conf,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  if (!w) return fail(RKSC_ERR_INVALID_ARGUMENT, "weights is NULL");
+  if (!kv) return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix_kv is NULL");
+  if (!bkv) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_kv is NULL");
+  if (!bkv->k || !bkv->v) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_kv k/v are NULL");
+  if (!tokens) return fail(RKSC_ERR_INVALID_ARGUMENT, "tokens is NULL");
+  if (!next_token || !p_top || !conf)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "next_token, p_top and conf must not be NULL");
+  if (!workspace) return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  if (kv->n_prefix < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", kv->n_prefix);
+  if (kv->n_prefix > 0 && (!kv->k || !kv->v))
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix k/v are NULL with n_prefix = %d", kv->n_prefix);
+  if (bkv->length < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_kv length must be >= 0 (got %d)", bkv->length);
+  if (!step && bkv->length != 0)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "the suffix needs an empty branch cache (length %d)", bkv->length);
+  if (s < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "suffix_len must be >= 1 (got %d)", s);
+  if ((long long)bkv->length + s > bkv->capacity)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "branch cache full: length %d + %d > capacity %d", bkv->length, s,
+                bkv->capacity);
+  if ((long long)kv->n_prefix + bkv->length + s > (1LL << 30))
+    return fail(RKSC_ERR_UNSUPPORTED, "positions above 2^30");
+  const rksc_model_config* c = &w->cfg;
+  Layout lay;
+  rksc_status st = make_layout(c, n_branches, s, kv->n_prefix, &lay);
+  if (st != RKSC_OK) return st;
+  if (workspace_bytes < lay.total)
+    return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
+  if (!w->embed || !w->final_norm || !w->lm_head || !w->layers)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "embed, final_norm, lm_head and layers must not be NULL");
+  for (int l = 0; l < c->n_layers; ++l) {
+    const rksc_layer_weights& lw = w->layers[l];
+    if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
+      return fail(RKSC_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
+  }
+
+  const DType dt = c->dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
+  const size_t T = dt == DType::BF16 ? 2 : 4;
+  const int L = c->n_layers, d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, hd = c->head_dim;
+  const int F = c->d_ff, V = c->vocab, B = n_branches, n = kv->n_prefix, len = bkv->length, cap = bkv->capacity;
+  const int M = lay.max_rows;
+  const int Nqkv = (H + 2 * Hkv) * hd;
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  rksc::Ctrl* ctrl = reinterpret_cast<rksc::Ctrl*>(ws + lay.ctrl);
+  float* x0 = reinterpret_cast<float*>(ws + lay.x0);
+  float* x1 = reinterpret_cast<float*>(ws + lay.x1);
+  float* act = reinterpret_cast<float*>(ws + lay.act);
+  float* ffn = reinterpret_cast<float*>(ws + lay.ffn);
+  float* qb = reinterpret_cast<float*>(ws + lay.q);
+  float* kown = reinterpret_cast<float*>(ws + lay.kown);
+  float* vown = reinterpret_cast<float*>(ws + lay.vown);
+  float* pbig = reinterpret_cast<float*>(ws + lay.pbig);
+  float* pres = reinterpret_cast<float*>(ws + lay.pres);
+  float* parts = reinterpret_cast<float*>(ws + lay.parts);
+  float2* rope = reinterpret_cast<float2*>(ws + lay.rope);
+  float* opart = reinterpret_cast<float*>(ws + lay.opart);
+  float* mlpart = reinterpret_cast<float*>(ws + lay.mlpart);
+  const size_t res_stride = (size_t)M * d;
+  const size_t kv_layer = (size_t)Hkv * n * hd * T;
+  const size_t bkv_layer = (size_t)B * Hkv * cap * hd * T;
+  auto plane_lo = [&](float* buf, size_t elems) -> const void* {
+    return dt == DType::BF16 ? static_cast<const void*>(reinterpret_cast<const uint16_t*>(buf) + elems) : nullptr;
+  };
+
+  HIP_TRY(rksc::launch_init(ctrl, B, L, nullptr, nullptr, nullptr, 0, strm));
+  HIP_TRY(rksc::launch_rope_table(rope, s, n + len, hd, (double)c->rope_base, strm));
+  HIP_TRY(rksc::launch_embed(dt, w->embed, tokens, V, x0, M, d, strm));
+  const char* pk_base = static_cast<const char*>(kv->k);
+  const char* pv_base = static_cast<const char*>(kv->v);
+  for (int l = 0; l < L; ++l) {
+    const rksc_layer_weights& lw = w->layers[l];
+    float* x_prev = (l % 2 == 0) ? x0 : x1;
+    float* x_cur = (l % 2 == 0) ? x1 : x0;
+    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, true, ctrl, s,
+                                  x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
+                              s, M, Nqkv, d, strm));
+    HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
+                                  vown, M, strm));
+    char* bk = static_cast<char*>(bkv->k) + l * bkv_layer;
+    char* bv = static_cast<char*>(bkv->v) + l * bkv_layer;
+    HIP_TRY(rksc::launch_store_branch_kv(dt, kown, vown, bk, bv, B, Hkv, s, hd, cap, len, strm));
+    const void* pk = n > 0 ? pk_base + l * kv_layer : nullptr;
+    const void* pv = n > 0 ? pv_base + l * kv_layer : nullptr;
+    if (step)
+      HIP_TRY(rksc::launch_attention_decode(dt, lay.attn, qb, pk, pv, bk, bv, len, cap, kown, vown, act, opart,
+                                            mlpart, ctrl, n, H, Hkv, hd, B, strm));
+    else
+      HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, pk, pv, kown, vown, act, opart, mlpart, ctrl, n, s, H, Hkv,
+                                     hd, B, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.o, act, plane_lo(act, (size_t)M * H * hd), lw.w_o, pres, res_stride, ctrl, s,
+                              M, d, H * hd, strm));
+    HIP_TRY(rksc::launch_add_norm(dt, x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
+                                  lw.ffn_norm, d, c->rms_eps, M, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig, (size_t)M * 2 * F,
+                              ctrl, s, M, 2 * F, d, strm));
+    HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
+    HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
+                              M, d, F, strm));
+  }
+  float* x_last = (L % 2 == 1) ? x1 : x0;
+  HIP_TRY(rksc::launch_tap(dt, x_last, pres, lay.down.splits, res_stride, ctrl, s, d, B, L - 1, nullptr,
+                           w->final_norm, c->rms_eps, ws + lay.hn_a, ws + lay.hn_b, B, strm));
+  HIP_TRY(rksc::launch_entropy_argmax(dt, w->lm_head, ws + lay.hn_a, ws + lay.hn_b, ctrl, V, d, B, parts, strm));
+  HIP_TRY(rksc::launch_finalize_decode(parts, lay.nparts, B, next_token, p_top, conf, step ? 1 : 0, strm));
+  bkv->length = len + s;
+  return ok();
+}
+
+}  // namespace
+
+RKSC_EXPORT rksc_status rksc_decode_suffix(const rksc_weights* w, const rksc_prefix_kv* kv, rksc_branch_kv* branch_kv,
+                                           const int32_t* suffix_tokens, int32_t n_branches, int32_t suffix_len,
+                                           int32_t* next_token, float* p_top, float* conf, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+  return decode_impl(w, kv, branch_kv, suffix_tokens, n_branches, suffix_len, false, next_token, p_top, conf,
+                     workspace, workspace_bytes, stream);
+}
+
+RKSC_EXPORT rksc_status rksc_decode_step(const rksc_weights* w, const rksc_prefix_kv* kv, rksc_branch_kv* branch_kv,
+                                         const int32_t* tokens, int32_t n_branches, int32_t* next_token, float* p_top,
+                                         float* conf, void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_impl(w, kv, branch_kv, tokens, n_branches, 1, true, next_token, p_top, conf, workspace,
+                     workspace_bytes, stream);
+}
+
+RKSC_EXPORT rksc_status rksc_cgee_gate(const float* conf, int32_t n_branches, int32_t n_steps, float tau_conf,
+                                       float r_gap, float* p_mean, int32_t* fired, int32_t* winner, float* stats,
+                                       void* stream) {
+  if (!conf) return fail(RKSC_ERR_INVALID_ARGUMENT, "conf is NULL");
+  if (!fired || !winner) return fail(RKSC_ERR_INVALID_ARGUMENT, "fired and winner must not be NULL");
+  if (n_branches < 1 || n_branches > RKSC_MAX_BRANCHES)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "n_branches must be in [1, %d] (got %d)", RKSC_MAX_BRANCHES, n_branches);
+  if (n_steps < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_steps must be >= 1 (got %d)", n_steps);
+  if (std::isnan(tau_conf) || std::isnan(r_gap))
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "tau_conf and r_gap must not be NaN");
+  HIP_TRY(rksc::launch_cgee_gate(conf, n_branches, n_steps, tau_conf, r_gap, p_mean, fired, winner, stats,
+                                 static_cast<hipStream_t>(stream)));
   return ok();
 }
 

@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
     assert "rksc_verify_forward" in names and "rksc_asks_similarity" in names
     for name in names:
         assert hasattr(lib, name), f"{name} declared in include/ but not exported"
-    assert rk.rksc_abi_version() == 2
+    assert rk.rksc_abi_version() == 3
 
 
 def test_status_strings(lib):
@@ -172,3 +172,67 @@ def test_prefill_rejects_bad_arguments(lib):
         rk.RKSC_ERR_WORKSPACE_TOO_SMALL
     assert lib.rksc_prefill(ctypes.byref(w), FAKE, 64, FAKE, FAKE, FAKE, ctypes.c_void_p(0x100010), ws, None) == \
         rk.RKSC_ERR_INVALID_ARGUMENT
+
+
+def _fake_weights(shape):
+    cfg = rk.model_config(shape)
+    layers = (rk.LayerWeights * shape.n_layers)()
+    for i in range(shape.n_layers):
+        layers[i] = rk.LayerWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    return rk.Weights(cfg, FAKE, layers, FAKE, FAKE), layers, cfg
+
+
+def test_decode_rejects_bad_arguments(lib):
+    shape = workloads.get("tiny").model
+    w, _keep, cfg = _fake_weights(shape)
+    assert lib.rksc_decode_workspace_size(ctypes.byref(cfg), 4, 16, -1) == 0
+    assert lib.rksc_decode_workspace_size(ctypes.byref(cfg), 0, 16, 8) == 0
+    assert lib.rksc_decode_workspace_size(ctypes.byref(cfg), 4, 0, 8) == 0
+    ws = lib.rksc_decode_workspace_size(ctypes.byref(cfg), 4, 16, 8)
+    assert ws >= lib.rksc_verify_workspace_size(ctypes.byref(cfg), 4, 16, 8)
+    assert ws >= lib.rksc_verify_workspace_size(ctypes.byref(cfg), 4, 1, 8)
+    ok_ws = ctypes.c_void_p(0x100000)
+    kv = rk.PrefixKV(8, FAKE, FAKE)
+    I = rk.RKSC_ERR_INVALID_ARGUMENT
+
+    def suffix(bkv, s=16, B=4, tokens=FAKE, outs=(FAKE, FAKE, FAKE), wsb=ws, wsp=ok_ws, kvp=kv):
+        return lib.rksc_decode_suffix(ctypes.byref(w), ctypes.byref(kvp) if kvp else None,
+                                      ctypes.byref(bkv) if bkv else None, tokens, B, s, *outs, wsp, wsb, None)
+
+    def step(bkv, B=4, wsb=ws):
+        return lib.rksc_decode_step(ctypes.byref(w), ctypes.byref(kv), ctypes.byref(bkv), FAKE, B, FAKE, FAKE, FAKE,
+                                    ok_ws, wsb, None)
+
+    good = rk.BranchKVStruct(32, 0, FAKE, FAKE)
+    assert suffix(None) == I
+    assert suffix(good, kvp=None) == I
+    assert suffix(rk.BranchKVStruct(32, 0, None, FAKE)) == I
+    assert suffix(good, tokens=None) == I
+    assert suffix(good, outs=(FAKE, None, FAKE)) == I
+    assert suffix(good, outs=(FAKE, FAKE, None)) == I
+    assert suffix(good, s=0) == I
+    assert suffix(good, B=0) == I and suffix(good, B=65) == I
+    assert suffix(rk.BranchKVStruct(15, 0, FAKE, FAKE)) == I              # capacity < s
+    assert suffix(rk.BranchKVStruct(32, 3, FAKE, FAKE)) == I              # suffix needs an empty cache
+    assert suffix(good, wsb=ws - 1) == rk.RKSC_ERR_WORKSPACE_TOO_SMALL
+    assert suffix(good, wsp=ctypes.c_void_p(0x100040)) == I
+    assert suffix(good, kvp=rk.PrefixKV(-1, FAKE, FAKE)) == I
+    assert suffix(good, kvp=rk.PrefixKV(8, None, FAKE)) == I
+    full = rk.BranchKVStruct(32, 32, FAKE, FAKE)
+    assert step(full) == I                                                 # no free entry
+    assert full.length == 32
+    assert step(rk.BranchKVStruct(32, -1, FAKE, FAKE)) == I
+    assert step(rk.BranchKVStruct(32, 5, FAKE, FAKE), wsb=16) == rk.RKSC_ERR_WORKSPACE_TOO_SMALL
+    assert "workspace" in rk.rksc_last_error()
+
+
+def test_cgee_gate_rejects_bad_arguments(lib):
+    I = rk.RKSC_ERR_INVALID_ARGUMENT
+    assert lib.rksc_cgee_gate(None, 4, 3, 0.7, 0.06, None, FAKE, FAKE, None, None) == I
+    assert lib.rksc_cgee_gate(FAKE, 4, 3, 0.7, 0.06, None, None, FAKE, None, None) == I
+    assert lib.rksc_cgee_gate(FAKE, 4, 3, 0.7, 0.06, None, FAKE, None, None, None) == I
+    assert lib.rksc_cgee_gate(FAKE, 0, 3, 0.7, 0.06, None, FAKE, FAKE, None, None) == I
+    assert lib.rksc_cgee_gate(FAKE, 65, 3, 0.7, 0.06, None, FAKE, FAKE, None, None) == I
+    assert lib.rksc_cgee_gate(FAKE, 4, 0, 0.7, 0.06, None, FAKE, FAKE, None, None) == I
+    assert lib.rksc_cgee_gate(FAKE, 4, 3, math.nan, 0.06, None, FAKE, FAKE, None, None) == I
+    assert lib.rksc_cgee_gate(FAKE, 4, 3, 0.7, math.nan, None, FAKE, FAKE, None, None) == I
