@@ -19,6 +19,10 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   exit_histogram, live_layer_fraction   exit layers of the timed calls
   full_depth   the same workload with tau = 0 (no exit)
   tau_sweep    exit layers and call time at tau in {0.02, 0.05, 0.1, 0.2}
+  prefill      the root forward (Eq. prefix_fwd) over the workload's prefix
+  decode       batched greedy decode of 8 branches over the same prefix cache
+               (suffix prefill, one-token steps, the CGEE gate), per step
+               against the HBM bytes it must stream (weights, lm_head, prefix KV)
   cpu_baseline the float64 CPU oracle on a bounded sample of the workload
 
     python bench.py [--steps K] [--warmup W] [--workload 7b_single]
@@ -119,6 +123,9 @@ KERNEL_SOURCES = {
 # Name fragments of the device kernels behind each class in rocprofv3 output.
 KERNEL_NAMES = {"lm_head_entropy": "k_entropy_bf16", "attention": "k_attn_bf16", "qkv_proj": "k_gemm_dma",
                 "o_proj": "k_gemm_dma", "gate_up_proj": "k_gemm_dma", "down_proj": "k_gemm_dma"}
+# The decode measurement: the paper's B = 8 branches and t = 32 decode steps of
+# its throughput table, after a 32-token suffix per branch.
+DECODE_BRANCHES, DECODE_SUFFIX, DECODE_TOKENS = 8, 32, 32
 COPY_BYTES = 1 << 29   # calibration copy: 512 MiB read + 512 MiB written
 
 
@@ -269,6 +276,71 @@ def cpu_baseline(mw, kv, toks, wl, layers):
     }
 
 
+def measure_decode(mw, kv, shape, n, args, hip, sp, stream, dev):
+    """Batched decode over the prefix cache (Sec. 2.2; Eq. gen_conf, Eq. cgee_gate):
+    DECODE_BRANCHES branches, a DECODE_SUFFIX-token suffix prefill, then greedy
+    one-token steps (each feeds its argmax back) until DECODE_TOKENS tokens per
+    branch are generated, then the Level-1 gate. The steps are timed with HIP
+    events on `stream`; the solve time spans the suffix, the steps and the gate."""
+    import torch
+
+    import paper_2606_09937_amd as rk
+    import workloads
+
+    L = shape.n_layers
+    Bd, sd, td = DECODE_BRANCHES, DECODE_SUFFIX, DECODE_TOKENS
+    stoks = workloads.make_tokens(Bd * sd, shape.vocab, seed=args.seed, name="suffix",
+                                  device=dev).reshape(Bd, sd).contiguous()
+    dec = rk.Decoder(mw, kv.k, kv.v, Bd, sd, capacity=sd + td, device=dev)
+
+    def run_decode(ev=None):
+        dec.cache.struct.length = 0
+        dec.suffix(stoks, stream)
+        if ev:
+            hip.lib.hipEventRecord(ctypes.c_void_p(ev[0]), sp)
+        for _ in range(td - 1):
+            dec.step(None, stream)
+        if ev:
+            hip.lib.hipEventRecord(ctypes.c_void_p(ev[1]), sp)
+        return dec.gate(0.70, 0.06, stream)
+
+    run_decode()
+    torch.cuda.synchronize()
+    k_d = max(1, min(args.steps, 3))
+    a, b = hip.create(2)
+    tot = []
+    steps_ms = []
+    for _ in range(k_d):
+        m0, m1 = hip.create(2)
+        hip.lib.hipEventRecord(ctypes.c_void_p(a), sp)
+        fired, winner, p_mean, _ = run_decode((m0, m1))
+        hip.lib.hipEventRecord(ctypes.c_void_p(b), sp)
+        torch.cuda.synchronize()
+        tot.append(hip.elapsed_ms(a, b))
+        steps_ms.append(hip.elapsed_ms(m0, m1))
+        hip.destroy([m0, m1])
+    hip.destroy([a, b])
+    d_, H_, Hkv_, hd_, F_ = shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.d_ff
+    T_ = 2 if shape.dtype == "bf16" else 4
+    P_ = d_ * (H_ + 2 * Hkv_) * hd_ + H_ * hd_ * d_ + 3 * d_ * F_
+    step_bytes = T_ * (L * P_ + shape.vocab * d_ + L * 2 * Hkv_ * n * hd_)
+    step_ms = float(sorted(steps_ms)[len(steps_ms) // 2]) / (td - 1)
+    total_ms = float(sorted(tot)[len(tot) // 2])
+    decode = {"n_branches": Bd, "suffix_len": sd, "tokens_per_branch": td, "prefix_len": n,
+              "ms_per_solve": total_ms, "suffix_and_gate_ms": total_ms - step_ms * (td - 1),
+              "ms_per_step": step_ms, "step_tokens_per_s": Bd / (step_ms / 1e3),
+              "solve_tokens_per_s": Bd * td / (total_ms / 1e3),
+              "step_algorithmic_bytes": step_bytes, "step_hbm_gbs": step_bytes / (step_ms / 1e3) / 1e9,
+              "step_hbm_frac": step_bytes / (step_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+              "gate": {"tau_conf": 0.70, "r_gap": 0.06, "fired": int(fired.item()),
+                       "winner": int(winner.item()), "p_mean": [round(x, 4) for x in p_mean.tolist()]},
+              "runs_timed": k_d}
+    log(f"decode B={Bd} suffix={sd} tokens={td}: {total_ms:.2f} ms/solve, {step_ms:.3f} ms/step "
+        f"({decode['step_hbm_gbs']:.0f} GB/s weight+KV stream), gate fired={decode['gate']['fired']}")
+    del dec
+    return decode
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -284,6 +356,9 @@ def main():
     ap.add_argument("--no-full-depth", action="store_true")
     ap.add_argument("--no-tau-sweep", action="store_true")
     ap.add_argument("--no-prefill", action="store_true", help="skip the root-forward (prefill) timing")
+    ap.add_argument("--no-decode", action="store_true", help="skip the batched-decode timing")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="time only the batched decode (for a kernel trace of it) and print its JSON")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the plain copy kernel used to scale HBM counters")
     ap.add_argument("--summarize-stats", dest="stats", metavar="DIR",
@@ -351,6 +426,15 @@ def main():
                                                   None, rk._ptr(ws), ws.numel(), sp, events)
         if st != 0:
             raise RuntimeError(f"rksc_verify_forward failed: {rk.rksc_last_error()}")
+
+    if args.decode_only:
+        hip = HipEvents()
+        hip.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        decode = measure_decode(mw, kv, shape, n, args, hip, sp, stream, dev)
+        print(json.dumps({"metric": "batched decode (8 branches, greedy) at 7B shape", "unit": "tokens/s",
+                          "value": decode["step_tokens_per_s"], "dtype": shape.dtype, "data": "synthetic",
+                          "config": {"workload": wl.name, "prefix_len": n}, "decode": decode}), flush=True)
+        return
 
     lib.rksc_verify_forward_profiled.restype = ctypes.c_int32
     lib.rksc_verify_forward_profiled.argtypes = list(lib.rksc_verify_forward.argtypes) + [ctypes.c_void_p]
@@ -521,6 +605,8 @@ def main():
             f"{prefill['algorithmic_tflops']:.1f} TFLOP/s algorithmic")
         del pws, pk, pv, hr
 
+    decode = None if args.no_decode else measure_decode(mw, kv, shape, n, args, hip, sp, stream, dev)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu_layers = L if args.cpu_layers <= 0 else min(args.cpu_layers, L)
@@ -556,6 +642,7 @@ def main():
         "full_depth": full_depth,
         "tau_sweep": tau_sweep,
         "prefill": prefill,
+        "decode": decode,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

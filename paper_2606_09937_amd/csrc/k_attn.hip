@@ -655,9 +655,13 @@ __global__ __launch_bounds__(256) void k_attn_combine_own(const float* __restric
 // keys -- its cached entries 0..len-1 (bf16) and the new token's own key
 // (fp32, entry len) -- in log2 units:
 // o = (sum_c 2^{m_c - M} o_c + sum_j 2^{t_j - M} v_j) / (sum_c 2^{m_c - M} l_c + sum_j 2^{t_j - M}),
-// t_j = log2(e)/sqrt(hd) q.k_j. The own keys are scored 64 at a time, one per
-// lane (16-byte loads of the key row; the query address is wave-uniform), with
-// an online maximum across the blocks of 64.
+// t_j = log2(e)/sqrt(hd) q.k_j. The cached keys are scored 64 at a time, one
+// per lane (16-byte loads of the key row; the query address is wave-uniform),
+// with an online maximum across the blocks of 64; the own key is scored by the
+// whole wave. Value rows and chunk partials are loaded DEC_BATCH at a time so
+// that their loads are in flight together.
+constexpr int kDecBatch = 16;
+
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_combine_dec(const float* __restrict__ opart,
                                                           const float* __restrict__ mlpart,
@@ -672,10 +676,19 @@ __global__ __launch_bounds__(256) void k_attn_combine_dec(const float* __restric
   if (wid >= rows) return;
   const int b = wid / H, h = wid - b * H, kvh = h / (H / Hkv);
   const float* qr = q + (size_t)wid * HD;
-  const bf16* kb = ck + ((size_t)b * Hkv + kvh) * cap * HD;
-  const bf16* vb = cv + ((size_t)b * Hkv + kvh) * cap * HD;
+  const uint16_t* kb = reinterpret_cast<const uint16_t*>(ck) + ((size_t)b * Hkv + kvh) * cap * HD;
+  const uint16_t* vb = reinterpret_cast<const uint16_t*>(cv) + ((size_t)b * Hkv + kvh) * cap * HD;
   const float* kc = ko + ((size_t)b * Hkv + kvh) * HD;   // the new token's own key (s = 1)
   const float* vc = vo + ((size_t)b * Hkv + kvh) * HD;
+
+  // The own key's score, reduced over the wave.
+  float t_own = 0.f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) t_own = fmaf(qr[lane + 64 * e], kc[lane + 64 * e], t_own);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) t_own += __shfl_xor(t_own, off, 64);
+  t_own *= sl2;
+
   float Mr = -INFINITY, den = 0.f, acc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
@@ -685,27 +698,26 @@ __global__ __launch_bounds__(256) void k_attn_combine_dec(const float* __restric
     float t = -INFINITY;
     if (j < len) {
       const uint4* kr = reinterpret_cast<const uint4*>(kb + (size_t)j * HD);
+      uint4 w[HD / 8];
+#pragma unroll
+      for (int u = 0; u < HD / 8; ++u) w[u] = kr[u];
       float dot = 0.f;
 #pragma unroll
       for (int u = 0; u < HD / 8; ++u) {
-        const uint4 w = kr[u];
         const float4 qa = *reinterpret_cast<const float4*>(qr + 8 * u);
         const float4 qb = *reinterpret_cast<const float4*>(qr + 8 * u + 4);
-        dot = fmaf(qa.x, __uint_as_float(w.x << 16), dot);
-        dot = fmaf(qa.y, __uint_as_float(w.x & 0xffff0000u), dot);
-        dot = fmaf(qa.z, __uint_as_float(w.y << 16), dot);
-        dot = fmaf(qa.w, __uint_as_float(w.y & 0xffff0000u), dot);
-        dot = fmaf(qb.x, __uint_as_float(w.z << 16), dot);
-        dot = fmaf(qb.y, __uint_as_float(w.z & 0xffff0000u), dot);
-        dot = fmaf(qb.z, __uint_as_float(w.w << 16), dot);
-        dot = fmaf(qb.w, __uint_as_float(w.w & 0xffff0000u), dot);
+        dot = fmaf(qa.x, __uint_as_float(w[u].x << 16), dot);
+        dot = fmaf(qa.y, __uint_as_float(w[u].x & 0xffff0000u), dot);
+        dot = fmaf(qa.z, __uint_as_float(w[u].y << 16), dot);
+        dot = fmaf(qa.w, __uint_as_float(w[u].y & 0xffff0000u), dot);
+        dot = fmaf(qb.x, __uint_as_float(w[u].z << 16), dot);
+        dot = fmaf(qb.y, __uint_as_float(w[u].z & 0xffff0000u), dot);
+        dot = fmaf(qb.z, __uint_as_float(w[u].w << 16), dot);
+        dot = fmaf(qb.w, __uint_as_float(w[u].w & 0xffff0000u), dot);
       }
       t = dot * sl2;
     } else if (j == len) {
-      float dot = 0.f;
-#pragma unroll 8
-      for (int dd = 0; dd < HD; ++dd) dot = fmaf(qr[dd], kc[dd], dot);
-      t = dot * sl2;
+      t = t_own;
     }
     float bm = t;
 #pragma unroll
@@ -719,16 +731,29 @@ __global__ __launch_bounds__(256) void k_attn_combine_dec(const float* __restric
     den = den * alpha + ps;
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] *= alpha;
-    const int cnt = min(64, nkeys - j0);
-    for (int u = 0; u < cnt; ++u) {
-      const float pu = __shfl(p, u, 64);
-      const int ju = j0 + u;
+    // Cached values of the block: one load path (rows clamped to len - 1, weight 0
+    // past the block), so a batch's loads are all in flight together.
+    const int cnt = min(64, len - j0);
+    for (int u0 = 0; u0 < cnt; u0 += kDecBatch) {
+      float v[kDecBatch][E];
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const float v = ju < len ? __uint_as_float((uint32_t)__builtin_bit_cast(uint16_t, vb[(size_t)ju * HD + lane + 64 * e]) << 16)
-                                 : vc[lane + 64 * e];
-        acc[e] = fmaf(pu, v, acc[e]);
+      for (int uu = 0; uu < kDecBatch; ++uu) {
+        const size_t row = (size_t)min(j0 + u0 + uu, len - 1) * HD;
+#pragma unroll
+        for (int e = 0; e < E; ++e) v[uu][e] = __uint_as_float((uint32_t)vb[row + lane + 64 * e] << 16);
       }
+#pragma unroll
+      for (int uu = 0; uu < kDecBatch; ++uu) {
+        const float pu = __shfl(p, (u0 + uu) & 63, 64);
+        const float pv = u0 + uu < cnt ? pu : 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = fmaf(pv, v[uu][e], acc[e]);
+      }
+    }
+    if (len - j0 < 64) {   // the own key is in this block, at lane len - j0
+      const float po = __shfl(p, len - j0, 64);
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] = fmaf(po, vc[lane + 64 * e], acc[e]);
     }
     Mr = Mn;
   }
@@ -758,11 +783,21 @@ __global__ __launch_bounds__(256) void k_attn_combine_dec(const float* __restric
     for (int off = 32; off >= 1; off >>= 1) wl += __shfl_xor(wl, off, 64);
     den += wl;
     const int cn = min(64, nchunks - c0);
-    for (int k = 0; k < cn; ++k) {
-      const float wk = __shfl(w, k, 64);
-      const float* op = opart + ((size_t)(c0 + k) * cstride + wid) * HD;
+    for (int k0 = 0; k0 < cn; k0 += kDecBatch) {
+      float v[kDecBatch][E];
 #pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = fmaf(wk, op[lane + 64 * e], acc[e]);
+      for (int kk = 0; kk < kDecBatch; ++kk) {
+        const float* op = opart + ((size_t)(c0 + min(k0 + kk, cn - 1)) * cstride + wid) * HD;
+#pragma unroll
+        for (int e = 0; e < E; ++e) v[kk][e] = op[lane + 64 * e];
+      }
+#pragma unroll
+      for (int kk = 0; kk < kDecBatch; ++kk) {
+        const float wk = __shfl(w, (k0 + kk) & 63, 64);
+        const float wv = k0 + kk < cn ? wk : 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = fmaf(wv, v[kk][e], acc[e]);
+      }
     }
   }
   const float inv = 1.f / den;

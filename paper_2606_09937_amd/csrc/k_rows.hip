@@ -138,11 +138,16 @@ __global__ __launch_bounds__(1024) void k_add_norm(const float* __restrict__ x_i
 
 // Thread (unit u, row r): unit u covers columns (hh*hd + j, hh*hd + j + hd/2)
 // of head hh of the [q | k | v] output; q and k pairs are rotated by RoPE.
-template <typename T>
+// When kc is not NULL, the rotated keys and the values are also stored, in the
+// cache type CT, as entries off..off+s-1 of the cache layer kc/vc
+// [slots, Hkv, cap, hd] (the prefix cache of the root forward, or a branch
+// cache of the decode).
+template <typename T, typename CT>
 __global__ __launch_bounds__(256) void k_qkv_post(const float* __restrict__ P, int nsplit, size_t split_stride,
                                                   const Ctrl* c, int s, int H, int Hkv, int hd,
                                                   const float2* __restrict__ rope, T* __restrict__ q,
-                                                  T* __restrict__ k_own, T* __restrict__ v_own) {
+                                                  T* __restrict__ k_own, T* __restrict__ v_own,
+                                                  CT* __restrict__ kc, CT* __restrict__ vc, int cap, int off) {
   const int r = blockIdx.y;
   if (r >= c->live_count * s) return;
   const int half = hd / 2;
@@ -170,15 +175,22 @@ __global__ __launch_bounds__(256) void k_qkv_post(const float* __restrict__ P, i
     x2 = y2;
   }
   T* dst;
+  CT* cdst = nullptr;
   if (hh < H) {
     dst = q + ((size_t)r * H + hh) * hd;
   } else if (hh < H + Hkv) {
     dst = k_own + (((size_t)slot * Hkv + (hh - H)) * s + i) * hd;
+    if (kc) cdst = kc + (((size_t)slot * Hkv + (hh - H)) * cap + off + i) * hd;
   } else {
     dst = v_own + (((size_t)slot * Hkv + (hh - H - Hkv)) * s + i) * hd;
+    if (kc) cdst = vc + (((size_t)slot * Hkv + (hh - H - Hkv)) * cap + off + i) * hd;
   }
   dst[j] = from_f32<T>(x1);
   dst[j + half] = from_f32<T>(x2);
+  if (cdst) {
+    cdst[j] = from_f32<CT>(x1);
+    cdst[j + half] = from_f32<CT>(x2);
+  }
 }
 
 // ------------------------------------------------------------------ SwiGLU epilogue
@@ -331,68 +343,35 @@ __global__ __launch_bounds__(256) void k_finalize_decode(const float* parts, int
   __shared__ EntStats red[256];
   __shared__ int red_am[256];
   const int tid = threadIdx.x;
-  for (int col = 0; col < B; ++col) {
-    EntStats st = ent_empty();
-    int am = 0x7fffffff;
-    for (int p = tid; p < nparts; p += blockDim.x) {
-      const float* q = parts + ((size_t)p * 64 + col) * 4;
-      const EntStats o{q[0], q[1], q[2]};
-      am = merge_argmax(st, am, o, __float_as_int(q[3]));
-      st = ent_merge(st, o);
-    }
-    red[tid] = st;
-    red_am[tid] = am;
-    __syncthreads();
-    for (int off = blockDim.x / 2; off > 0; off >>= 1) {
-      if (tid < off) {
-        red_am[tid] = merge_argmax(red[tid], red_am[tid], red[tid + off], red_am[tid + off]);
-        red[tid] = ent_merge(red[tid], red[tid + off]);
-      }
-      __syncthreads();
-    }
-    if (tid == 0) {
-      const bool ok = red[0].m != -INFINITY && red_am[0] != 0x7fffffff;
-      const float p = ok ? 1.f / red[0].s : __builtin_nanf("");
-      next_token[col] = ok ? red_am[0] : -1;
-      p_top[col] = p;
-      if (conf) conf[col] = accumulate ? conf[col] + p : p;
+  const int col = blockIdx.x;   // one workgroup per branch column
+  EntStats st = ent_empty();
+  int am = 0x7fffffff;
+  for (int p = tid; p < nparts; p += blockDim.x) {
+    const float* q = parts + ((size_t)p * 64 + col) * 4;
+    const EntStats o{q[0], q[1], q[2]};
+    am = merge_argmax(st, am, o, __float_as_int(q[3]));
+    st = ent_merge(st, o);
+  }
+  red[tid] = st;
+  red_am[tid] = am;
+  __syncthreads();
+  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+    if (tid < off) {
+      red_am[tid] = merge_argmax(red[tid], red_am[tid], red[tid + off], red_am[tid + off]);
+      red[tid] = ent_merge(red[tid], red[tid + off]);
     }
     __syncthreads();
   }
-}
-
-// Branch cache entries off..off+s-1 of one layer from the branches' fp32 keys
-// (already rotated) and values: 4 elements per thread.
-template <typename T>
-__global__ __launch_bounds__(256) void k_store_branch_kv(const float* __restrict__ k_own,
-                                                         const float* __restrict__ v_own, T* __restrict__ k_dst,
-                                                         T* __restrict__ v_dst, int s, int hd, int cap, int off,
-                                                         size_t elems) {
-  const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (i >= elems) return;
-  const size_t bh = i / ((size_t)s * hd);           // branch * Hkv + kv head
-  const size_t rem = i - bh * s * hd;
-  const size_t dst = (bh * cap + off) * hd + rem;   // entry off + rem / hd, element rem % hd
-  const float4 a = *reinterpret_cast<const float4*>(k_own + i);
-  const float4 b = *reinterpret_cast<const float4*>(v_own + i);
-  store4(k_dst + dst, a.x, a.y, a.z, a.w);
-  store4(v_dst + dst, b.x, b.y, b.z, b.w);
+  if (tid == 0) {
+    const bool ok = red[0].m != -INFINITY && red_am[0] != 0x7fffffff;
+    const float p = ok ? 1.f / red[0].s : __builtin_nanf("");
+    next_token[col] = ok ? red_am[0] : -1;
+    p_top[col] = p;
+    if (conf) conf[col] = accumulate ? conf[col] + p : p;
+  }
 }
 
 // ------------------------------------------------------------------ root forward
-
-// The prefix cache in the model's storage type from the fp32 keys/values of the
-// root's own span (keys already rotated): 4 elements per thread.
-template <typename T>
-__global__ __launch_bounds__(256) void k_store_kv(const float* __restrict__ k_own, const float* __restrict__ v_own,
-                                                  T* __restrict__ k_dst, T* __restrict__ v_dst, size_t elems) {
-  const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (i >= elems) return;
-  const float4 a = *reinterpret_cast<const float4*>(k_own + i);
-  const float4 b = *reinterpret_cast<const float4*>(v_own + i);
-  store4(k_dst + i, a.x, a.y, a.z, a.w);
-  store4(v_dst + i, b.x, b.y, b.z, b.w);
-}
 
 // Unit-normalises each row (the root hidden states are stored normalised).
 __global__ __launch_bounds__(256) void k_unit_rows(float* __restrict__ x, int d) {
@@ -449,7 +428,7 @@ __global__ __launch_bounds__(64) void k_cgee_gate(const float* conf, int B, int 
 
 hipError_t launch_finalize_decode(const float* parts, int nparts, int B, int* next_token, float* p_top, float* conf,
                                   int accumulate, hipStream_t st) {
-  hipLaunchKernelGGL(k_finalize_decode, dim3(1), dim3(256), 0, st, parts, nparts, B, next_token, p_top, conf,
+  hipLaunchKernelGGL(k_finalize_decode, dim3(B), dim3(256), 0, st, parts, nparts, B, next_token, p_top, conf,
                      accumulate);
   return hipGetLastError();
 }
@@ -458,31 +437,6 @@ hipError_t launch_cgee_gate(const float* conf, int B, int n_steps, float tau_con
                             int* fired, int* winner, float* stats, hipStream_t st) {
   hipLaunchKernelGGL(k_cgee_gate, dim3(1), dim3(64), 0, st, conf, B, n_steps, tau_conf, r_gap, p_mean, fired, winner,
                      stats);
-  return hipGetLastError();
-}
-
-hipError_t launch_store_branch_kv(DType dt, const float* k_own, const float* v_own, void* k_dst, void* v_dst, int B,
-                                  int Hkv, int s, int hd, int cap, int off, hipStream_t st) {
-  const size_t elems = (size_t)B * Hkv * s * hd;
-  const dim3 grid((unsigned)((elems / 4 + 255) / 256));
-  if (dt == DType::BF16)
-    hipLaunchKernelGGL(k_store_branch_kv<bf16>, grid, dim3(256), 0, st, k_own, v_own, static_cast<bf16*>(k_dst),
-                       static_cast<bf16*>(v_dst), s, hd, cap, off, elems);
-  else
-    hipLaunchKernelGGL(k_store_branch_kv<float>, grid, dim3(256), 0, st, k_own, v_own, static_cast<float*>(k_dst),
-                       static_cast<float*>(v_dst), s, hd, cap, off, elems);
-  return hipGetLastError();
-}
-
-hipError_t launch_store_kv(DType dt, const float* k_own, const float* v_own, void* k_dst, void* v_dst,
-                           size_t elems, hipStream_t st) {
-  const dim3 grid((unsigned)((elems / 4 + 255) / 256));
-  if (dt == DType::BF16)
-    hipLaunchKernelGGL(k_store_kv<bf16>, grid, dim3(256), 0, st, k_own, v_own, static_cast<bf16*>(k_dst),
-                       static_cast<bf16*>(v_dst), elems);
-  else
-    hipLaunchKernelGGL(k_store_kv<float>, grid, dim3(256), 0, st, k_own, v_own, static_cast<float*>(k_dst),
-                       static_cast<float*>(v_dst), elems);
   return hipGetLastError();
 }
 
@@ -533,10 +487,17 @@ hipError_t launch_add_norm(DType dt, const float* x_in, const float* P, int nspl
 
 hipError_t launch_qkv_post(const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s, int H,
                            int Hkv, int hd, const float2* rope, float* q, float* k_own, float* v_own,
-                           int max_rows, hipStream_t st) {
+                           int max_rows, hipStream_t st, DType cache_dt, void* k_cache, void* v_cache, int cap,
+                           int off) {
   const int units = (H + 2 * Hkv) * hd / 2;
-  hipLaunchKernelGGL(k_qkv_post<float>, dim3((units + 255) / 256, max_rows), dim3(256), 0, st, P, nsplit,
-                     split_stride, c, s, H, Hkv, hd, rope, q, k_own, v_own);
+  const dim3 grid((units + 255) / 256, max_rows);
+  if (k_cache && cache_dt == DType::BF16)
+    hipLaunchKernelGGL((k_qkv_post<float, bf16>), grid, dim3(256), 0, st, P, nsplit, split_stride, c, s, H, Hkv, hd,
+                       rope, q, k_own, v_own, static_cast<bf16*>(k_cache), static_cast<bf16*>(v_cache), cap, off);
+  else
+    hipLaunchKernelGGL((k_qkv_post<float, float>), grid, dim3(256), 0, st, P, nsplit, split_stride, c, s, H, Hkv,
+                       hd, rope, q, k_own, v_own, static_cast<float*>(k_cache), static_cast<float*>(v_cache), cap,
+                       off);
   return hipGetLastError();
 }
 

@@ -40,9 +40,12 @@ hipError_t launch_add_norm(DType dt, const float* x_in, const float* P, int nspl
                            bool gather, const Ctrl* c, int s, float* x_out, void* xn, const float* gamma, int d,
                            float eps, int max_rows, hipStream_t st);
 // q [rows, H, hd], k_own/v_own [B, Hkv, s, hd] from the summed QKV partials, RoPE on q and k.
+// With k_cache/v_cache, the keys and values are also stored (type cache_dt) as
+// entries off..off+s-1 of a cache layer [B, Hkv, cap, hd].
 hipError_t launch_qkv_post(const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s, int H,
                            int Hkv, int hd, const float2* rope, float* q, float* k_own, float* v_own,
-                           int max_rows, hipStream_t st);
+                           int max_rows, hipStream_t st, DType cache_dt = DType::F32, void* k_cache = nullptr,
+                           void* v_cache = nullptr, int cap = 0, int off = 0);
 // a = silu(gate) * up from the summed gate|up partials.
 hipError_t launch_swiglu_post(DType dt, const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s,
                               int F, void* a, int max_rows, hipStream_t st);
@@ -103,10 +106,6 @@ hipError_t launch_finalize_exit(const float* parts, int nparts, Ctrl* c, int lay
                                 float tau, int patience, float* entropy, int* exit_layer, hipStream_t st);
 
 // ---- batched decode
-// Branch cache of one layer [B, Hkv, cap, hd] (model dtype): entries off..off+s-1
-// from the fp32 k_own/v_own [B, Hkv, s, hd].
-hipError_t launch_store_branch_kv(DType dt, const float* k_own, const float* v_own, void* k_dst, void* v_dst, int B,
-                                  int Hkv, int s, int hd, int cap, int off, hipStream_t st);
 // Attention of one new token per branch (s = 1) over the shared prefix (split-KV
 // plan p, cross mode), the branch's cached entries 0..len-1 (model dtype, layer
 // base [B, Hkv, cap, hd]) and its own key/value (fp32 k_own/v_own [B, Hkv, 1, hd]).
@@ -121,9 +120,6 @@ hipError_t launch_cgee_gate(const float* conf, int B, int n_steps, float tau_con
                             int* fired, int* winner, float* stats, hipStream_t st);
 
 // ---- root forward (prefill)
-// k_dst/v_dst [Hkv, n, hd] of the model dtype from the fp32 k_own/v_own of one branch.
-hipError_t launch_store_kv(DType dt, const float* k_own, const float* v_own, void* k_dst, void* v_dst,
-                           size_t elems, hipStream_t st);
 // x[r] /= |x[r]| for rows r < rows of d floats (zero rows stay zero).
 hipError_t launch_unit_rows(float* x, int rows, int d, hipStream_t st);
 

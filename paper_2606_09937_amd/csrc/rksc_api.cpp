@@ -379,10 +379,10 @@ RKSC_EXPORT rksc_status rksc_prefill(const rksc_weights* w, const int32_t* token
                                   x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
                               s, M, Nqkv, d, strm));
+    // The cache layer [Hkv, n, hd] is the branch-cache layout with one slot, cap = n.
     HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
-                                  vown, M, strm));
-    HIP_TRY(rksc::launch_store_kv(dt, kown, vown, static_cast<char*>(k_out) + l * kv_layer * T,
-                                  static_cast<char*>(v_out) + l * kv_layer * T, kv_layer, strm));
+                                  vown, M, strm, dt, static_cast<char*>(k_out) + l * kv_layer * T,
+                                  static_cast<char*>(v_out) + l * kv_layer * T, s, 0));
     HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, nullptr, nullptr, kown, vown, act, opart, mlpart, ctrl, 0, s, H,
                                    Hkv, hd, 1, strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.o, act, plane_lo(act, (size_t)M * H * hd), lw.w_o, pres, res_stride, ctrl, s,
@@ -504,11 +504,10 @@ rksc_status decode_impl(const rksc_weights* w, const rksc_prefix_kv* kv, rksc_br
                                   x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
                               s, M, Nqkv, d, strm));
-    HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
-                                  vown, M, strm));
     char* bk = static_cast<char*>(bkv->k) + l * bkv_layer;
     char* bv = static_cast<char*>(bkv->v) + l * bkv_layer;
-    HIP_TRY(rksc::launch_store_branch_kv(dt, kown, vown, bk, bv, B, Hkv, s, hd, cap, len, strm));
+    HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
+                                  vown, M, strm, dt, bk, bv, cap, len));
     const void* pk = n > 0 ? pk_base + l * kv_layer : nullptr;
     const void* pv = n > 0 ? pv_base + l * kv_layer : nullptr;
     if (step)
