@@ -254,7 +254,8 @@ def rksc_test_gemm(A, W: torch.Tensor, splits: int = 0, stream=None, kind: int =
     """Kernel-level GEMM: returns the fp32 split partials [splits_used, M, N].
 
     bf16 W: A is the pair (A_hi, A_lo) of bf16 [M, K] planes; fp32 W: A is an fp32 [M, K] tensor.
-    kind: -1 the library's choice, 0 the 128-row-tile kernel, 1 the 256 x 256-tile kernel (bf16).
+    kind: -1 the library's choice, 0 the 128-row-tile kernel, 1 the 256 x 256-tile kernel, 2 the
+    weight-streaming kernel for at most 16 rows (kinds 1 and 2 bf16 only).
     """
     if W.dtype == torch.bfloat16:
         a_hi, a_lo = A

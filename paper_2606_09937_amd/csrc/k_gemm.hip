@@ -8,6 +8,7 @@
 // fp32 accumulation, so the product keeps fp32-level accuracy at twice the
 // bf16 MFMA work. Operands stream through an LDS ring by direct DMA.
 // fp32 weights: a plain LDS-tiled FMA kernel on fp32 activations.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -362,6 +363,161 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
 
+// ---------------------------------------------------------------- skinny GEMM
+//
+// At most 16 activation rows (one decode token per branch): the product is a
+// stream of the weight matrix, and the kernel is laid out like the lm_head
+// stream. The weights pass through an R-deep LDS ring of 16 KB units (16 rows x
+// 512 K, one 1 KB row segment per DMA instruction, chunk c of row r at position
+// c ^ r), while the activation stays in registers: a workgroup covers a K range
+// of 2048 * KH (one split of the output) and wave w holds the hi and lo bf16
+// fragments of the 16 rows over its KH half-slices of 256 K, loaded once. A unit
+// (tile t, slice s) is contracted by the owners of the slice's two halves (8
+// k-substeps x 2 MFMAs each); after every kSkGroup tiles the waves' partial
+// tiles are summed through LDS and stored as fp32 partials P[split][row][n].
+// Workgroup (split, j) takes a contiguous range of the 16-row weight tiles.
+// Rows past N are clamped (fetched, never stored); activation rows past the
+// live rows are zero; chunks past K read the row start and meet zero fragments.
+constexpr int kSkUnit = 16 * 1024;
+constexpr int kSkRing = 7;
+constexpr int kSkGroup = 4;
+constexpr int kSkRedBytes = kGemmWaves * kSkGroup * 1024;
+constexpr int kSkMaxRows = 16;
+
+template <int KH>
+__global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_skinny(const bf16* __restrict__ Ahi,
+                                                                 const bf16* __restrict__ Alo,
+                                                                 const bf16* __restrict__ W, float* __restrict__ P,
+                                                                 size_t split_stride, const Ctrl* c, int s,
+                                                                 int max_rows, int N, int K, int wgps) {
+  constexpr int NW = kGemmWaves, R = kSkRing, IPW = 16 / NW;
+  constexpr int KSPLIT = 2048 * KH;
+  static_assert(16 % NW == 0, "a unit's 16 rows split evenly over the waves");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[R * kSkUnit + kSkRedBytes];
+
+  const int Ml = c ? min(c->live_count * s, max_rows) : max_rows;
+  const int sp = blockIdx.x / wgps, jw = blockIdx.x - sp * wgps;
+  const int k0 = sp * KSPLIT;
+  const int ns = min(4 * KH, (K - k0 + 511) / 512);   // 512-wide slices of this split
+  const int T = (N + 15) / 16;
+  const int t0 = (int)((long long)jw * T / wgps), t1 = (int)((long long)(jw + 1) * T / wgps);
+  const int ntile = t1 - t0, nunits = ntile * ns;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+
+  int iu = 0;   // next unit to issue; past the end unit 0 is fetched again (never consumed)
+  auto issue = [&](int slot_idx) {
+    uint8_t* slot = smem + slot_idx * kSkUnit;
+    const int u = iu < nunits ? iu : 0;
+    const int tq = u / ns;
+    const int t = t0 + tq, sl = u - tq * ns;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const int r = IPW * wid + j;
+      const int k = k0 + 512 * sl + 8 * (lane ^ r);
+      const int row = min(16 * t + r, N - 1);
+      dma16(W + (size_t)row * K + (k < K ? k : 0), slot + r * 1024);
+    }
+    ++iu;
+  };
+#pragma unroll
+  for (int i = 0; i < R - 1; ++i) issue(i);
+
+  // The activation fragments (after the ring's first units, so that both are in
+  // flight together); the empty asm makes the compiler wait for them here, once.
+  const bf16x8 zero = {};
+  bf16x8 ah[KH][8], al[KH][8];
+  const int arow = min(r16, max_rows - 1);
+#pragma unroll
+  for (int q = 0; q < KH; ++q) {
+    const int kb = k0 + 256 * (wid * KH + q);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = kb + 32 * j + 8 * g;
+      const bool ok = k < K && r16 < Ml;
+      const size_t off = (size_t)arow * K + (ok ? k : 0);
+      const bf16x8 h = *reinterpret_cast<const bf16x8*>(Ahi + off);
+      const bf16x8 l = *reinterpret_cast<const bf16x8*>(Alo + off);
+      ah[q][j] = ok ? h : zero;
+      al[q][j] = ok ? l : zero;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < KH; ++q)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const u32x4 hv = __builtin_bit_cast(u32x4, ah[q][j]), lv = __builtin_bit_cast(u32x4, al[q][j]);
+      asm volatile("" ::"v"(hv), "v"(lv));
+    }
+
+  int qc = 0;   // ring units consumed
+  auto step = [&]() -> const uint8_t* {
+    wait_vmcnt_lds<IPW * (R - 2)>();
+    __builtin_amdgcn_s_barrier();
+    issue((qc + R - 1) % R);   // refills the slot unit qc-1 used
+    const uint8_t* slot = smem + (qc % R) * kSkUnit;
+    ++qc;
+    return slot;
+  };
+
+  floatx4* red = reinterpret_cast<floatx4*>(smem + R * kSkUnit);
+  for (int gi = 0; gi < ntile; gi += kSkGroup) {
+    const int gt = min(kSkGroup, ntile - gi);
+    floatx4 acc[kSkGroup];
+#pragma unroll
+    for (int m = 0; m < kSkGroup; ++m) acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int m = 0; m < kSkGroup; ++m) {
+      if (m < gt) {
+        for (int sl = 0; sl < ns; ++sl) {
+          const uint8_t* slot = step();
+#pragma unroll
+          for (int q = 0; q < KH; ++q) {
+            const int hs = wid * KH + q;   // half-slice: slice hs / 2, K half hs % 2
+            if ((hs >> 1) == sl) {
+              const int kh = hs & 1;
+#pragma unroll
+              for (int j = 0; j < 8; ++j) {
+                const int lc = 4 * (8 * kh + j) + g;
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(slot + r16 * 1024 + (lc ^ r16) * 16);
+                acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, ah[q][j], acc[m], 0, 0, 0);
+                acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, al[q][j], acc[m], 0, 0, 0);
+              }
+            }
+          }
+        }
+      }
+    }
+    // Lane (r16, g) of every wave holds, for activation row r16, its K part of
+    // weight rows 16 t + 4 g + i. The group's partial tiles meet in LDS; the
+    // area is rewritten only after the next group's first ring barrier.
+#pragma unroll
+    for (int m = 0; m < kSkGroup; ++m) red[(wid * kSkGroup + m) * 64 + lane] = acc[m];
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the partials are in LDS
+    __builtin_amdgcn_s_barrier();
+    if (tid < gt * 64) {
+      const int m = tid >> 6, l = tid & 63;
+      floatx4 z = red[m * 64 + l];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) z += red[(w * kSkGroup + m) * 64 + l];
+      const int row = l & 15, n = 16 * (t0 + gi + m) + 4 * (l >> 4);
+      if (row < Ml && n < N)
+        *reinterpret_cast<float4*>(P + sp * split_stride + (size_t)row * N + n) = make_float4(z[0], z[1], z[2], z[3]);
+    }
+  }
+  wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
+}
+
+namespace {
+// Half-slices per wave of the skinny kernel: the K range of a split is 2048 * KH
+// and the consumers sum at most kMaxSplitsGemm splits.
+int skinny_kh(int K) { return cdiv(K, 2048) <= kMaxSplitsGemm ? 1 : 2; }
+bool skinny_fits(DType dt, int max_rows, int N, int K) {
+  return dt == DType::BF16 && max_rows <= kSkMaxRows && N % 4 == 0 && K % 8 == 0 &&
+         cdiv(K, 2048 * skinny_kh(K)) <= kMaxSplitsGemm;
+}
+}  // namespace
+
 GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
   GemmPlan p;
   p.kind = 0;
@@ -372,6 +528,15 @@ GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
     int splits = 1;
     while (tiles * splits < 384 && K / (splits * 2) >= 256 && splits < kMaxSplitsGemm) splits *= 2;
     p.k_per_split = cdiv(cdiv(K, 16), splits) * 16;
+    p.splits = cdiv(K, p.k_per_split);
+    return p;
+  }
+  // bf16 with at most 16 rows (a decode step): the weight stream.
+  if (skinny_fits(dt, max_rows, N, K)) {
+    p.kind = 2;
+    p.bm = kSkMaxRows;
+    p.bn = 16;
+    p.k_per_split = 2048 * skinny_kh(K);
     p.splits = cdiv(K, p.k_per_split);
     return p;
   }
@@ -414,7 +579,22 @@ GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
 }
 
 GemmPlan plan_gemm_kind(DType dt, int max_rows, int N, int K, int kind, int splits) {
+  if (kind == 2) {   // the skinny kernel fixes its own splits (callers check skinny_fits)
+    GemmPlan p{2, kSkMaxRows, 16, 1, 2048 * skinny_kh(K)};
+    p.splits = cdiv(K, p.k_per_split);
+    return p;
+  }
   GemmPlan p = plan_gemm(dt, max_rows, N, K);
+  if (p.kind == 2 && kind < 0) return p;   // the planner's weight stream keeps its own splits
+  if (p.kind == 2) {   // a forced dense kernel for a shape the planner streams
+    p.kind = 0;
+    p.bm = 128;
+    p.bn = 128;
+    int sp = 1;
+    while (cdiv(N, 128) * sp < 224 && K / (sp * 2) >= 256 && sp < kMaxSplitsGemm) sp *= 2;
+    p.k_per_split = cdiv(cdiv(K, 64), sp) * 64;
+    p.splits = cdiv(K, p.k_per_split);
+  }
   if (dt == DType::BF16 && kind == 1) {
     p.kind = 1;
     p.bm = 256;
@@ -435,6 +615,19 @@ GemmPlan plan_gemm_kind(DType dt, int max_rows, int N, int K, int kind, int spli
 
 hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W, float* P,
                        size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st) {
+  if (dt == DType::BF16 && p.kind == 2) {
+    const int wgps = std::max(1, std::min(cdiv(N, 16), kComputeUnits / p.splits));
+    const dim3 sgrid(p.splits * wgps);
+    const bf16 *a0 = static_cast<const bf16*>(A0), *a1 = static_cast<const bf16*>(A1);
+    if (p.k_per_split != 2048 && p.k_per_split != 4096) return hipErrorInvalidValue;
+    if (p.k_per_split == 2048)
+      hipLaunchKernelGGL(k_gemm_skinny<1>, sgrid, dim3(kGemmWaves * 64), 0, st, a0, a1, static_cast<const bf16*>(W),
+                         P, split_stride, c, s, max_rows, N, K, wgps);
+    else
+      hipLaunchKernelGGL(k_gemm_skinny<2>, sgrid, dim3(kGemmWaves * 64), 0, st, a0, a1, static_cast<const bf16*>(W),
+                         P, split_stride, c, s, max_rows, N, K, wgps);
+    return hipGetLastError();
+  }
   const dim3 grid(cdiv(N, p.bn), cdiv(max_rows, p.bm), p.splits);
   if (dt == DType::BF16 && p.kind == 1) {
     hipLaunchKernelGGL((k_gemm_wide<3>), grid, dim3(kGemmWaves * 64), 0, st, static_cast<const bf16*>(A0),

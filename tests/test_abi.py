@@ -143,8 +143,14 @@ def test_testing_entry_points_reject_bad_shapes(lib):
         rk.RKSC_ERR_INVALID_ARGUMENT
     assert lib.rksc_test_gemm(1, FAKE, None, FAKE, FAKE, 4, 4, 16, 0, ctypes.byref(used), None) == \
         rk.RKSC_ERR_INVALID_ARGUMENT
-    assert lib.rksc_test_gemm_kind(1, FAKE, FAKE, FAKE, FAKE, 4, 4, 16, 0, 2, ctypes.byref(used), None) == \
+    assert lib.rksc_test_gemm_kind(1, FAKE, FAKE, FAKE, FAKE, 4, 4, 16, 0, 3, ctypes.byref(used), None) == \
         rk.RKSC_ERR_INVALID_ARGUMENT
+    assert lib.rksc_test_gemm_kind(1, FAKE, FAKE, FAKE, FAKE, 17, 4, 16, 0, 2, ctypes.byref(used), None) == \
+        rk.RKSC_ERR_UNSUPPORTED
+    assert lib.rksc_test_gemm_kind(1, FAKE, FAKE, FAKE, FAKE, 4, 6, 16, 0, 2, ctypes.byref(used), None) == \
+        rk.RKSC_ERR_UNSUPPORTED
+    assert lib.rksc_test_gemm_kind(0, FAKE, None, FAKE, FAKE, 4, 4, 16, 0, 2, ctypes.byref(used), None) == \
+        rk.RKSC_ERR_UNSUPPORTED
     assert lib.rksc_test_gemm_kind(0, FAKE, None, FAKE, FAKE, 4, 4, 16, 0, 1, ctypes.byref(used), None) == \
         rk.RKSC_ERR_UNSUPPORTED
     assert lib.rksc_test_attention(1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 4, 4, 4, 2, 32, FAKE, 1 << 20, None) == \

@@ -75,6 +75,31 @@ def test_gemm_wide_tiles_match_fp64(M, N, K, splits):
     assert (err <= bound).all(), f"max err {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}"
 
 
+@pytest.mark.parametrize("M,N,K,kind", [
+    (1, 16, 32, 2), (3, 4, 8, 2), (8, 260, 504, 2), (16, 1000, 2048, 2), (5, 6144, 4096, 2),
+    (8, 4096, 14336, 2), (13, 1028, 4104, 2), (16, 200, 20000, 2), (8, 28672, 4096, -1), (7, 4096, 14336, -1),
+])
+def test_gemm_skinny_matches_fp64(M, N, K, kind):
+    """The weight-streaming kernel for at most 16 rows (a decode step's projections), forced and as
+    the planner's choice: ragged N (a partial last 16-row weight tile), K not a multiple of 512, one
+    to eight K splits of 2048 and the 4096-wide splits of a K above 16384."""
+    log(f"gemm skinny M={M} N={N} K={K} kind={kind}")
+    A = _rand((M, K), torch.float32, 21 + M, 0.5)
+    W = _rand((N, K), torch.bfloat16, 22 + N, 0.05)
+    a_hi = A.to(torch.bfloat16)
+    a_lo = (A - a_hi.float()).to(torch.bfloat16)
+    A = a_hi.float() + a_lo.float()
+    P = rk.rksc_test_gemm((a_hi.to(DEV), a_lo.to(DEV)), W.to(DEV), kind=kind)
+    torch.cuda.synchronize()
+    per_split = 2048 if -(-K // 2048) <= 8 else 4096
+    assert P.shape[0] == -(-K // per_split)
+    got = P.double().sum(0).cpu().numpy()
+    a, w = A.double().numpy(), W.double().numpy()
+    bound = 1e-5 * (np.abs(a) @ np.abs(w).T) + 1e-7
+    err = np.abs(got - a @ w.T)
+    assert (err <= bound).all(), f"max err {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}"
+
+
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
 @pytest.mark.parametrize("B,n,s,H,Hkv,hd", [
     (1, 0, 1, 4, 4, 64), (2, 37, 16, 8, 2, 64), (3, 130, 70, 28, 4, 128),
