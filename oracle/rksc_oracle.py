@@ -34,6 +34,10 @@ Batched decode (Sec. 2.2; the stepwise loop of the implementation notes): a
   branch per step attending to the prefix, the branch's own earlier tokens and
   itself; each step's top-1 probability max_v softmax(z)_v feeds the generation
   confidence p_b (Eq. gen_conf), and Eq. cgee_gate decides on the p_b.
+RSBCM (Sec. 2.4, Alg. RsbcmEvict): while the block table holds more than
+  N_max blocks, evict the block of least omega = score / (depth + 1).
+KV probe (Sec. 2.2, paragraph "KV probe"): per 64-token prefix bucket, share
+  the prefix cache iff t(root forward) + t(suffix decode) < t(full recompute).
 """
 from __future__ import annotations
 
@@ -45,6 +49,7 @@ __all__ = [
     "layer_entropies", "exit_layer", "verify_forward", "asks_weights",
     "asks_similarity", "unit_rows", "root_similarity",
     "final_logits", "top1", "decode_suffix", "decode_step", "gen_confidence", "cgee_gate",
+    "rsbcm_omega", "rsbcm_evict", "kv_probe_bucket", "kv_probe_share",
 ]
 
 
@@ -372,3 +377,37 @@ def cgee_gate(p, tau_conf: float, r_gap: float) -> dict:
     gap = (top - second) / top if top > 0 else 0.0
     return {"fired": bool(top >= tau_conf and gap >= r_gap), "winner": winner, "max": top, "second": second,
             "gap": gap}
+
+
+def rsbcm_omega(score, depth) -> float:
+    """Importance of a cached block (Sec. 2.4): omega = score / (depth + 1), in double."""
+    return float(np.float32(score)) / (float(depth) + 1.0)
+
+
+def rsbcm_evict(blocks, n_max: int):
+    """Alg. RsbcmEvict on a block table given as a list of (id, score, depth) in
+    insertion order. While the table holds more than n_max blocks, recompute every
+    omega, take the first index of the least one, evict it. Returns (remaining
+    table, evicted ids in eviction order)."""
+    table = list(blocks)
+    evicted = []
+    while len(table) > n_max:
+        omegas = [rsbcm_omega(score, depth) for _, score, depth in table]
+        least = 0
+        for i in range(1, len(table)):
+            if omegas[i] < omegas[least]:
+                least = i
+        evicted.append(table[least][0])
+        del table[least]
+    return table, evicted
+
+
+def kv_probe_bucket(n_prefix: int) -> int:
+    """The probe's prefix-length bucket k = floor(n / 64) (Sec. 2.2, "KV probe")."""
+    return int(n_prefix) // 64
+
+
+def kv_probe_share(t_full: float, t_prefix: float, t_suffix: float) -> bool:
+    """Sharing is beneficial iff t(ii) + t(iii) < t(i): root forward plus batched
+    suffix decode against batched full recompute (Sec. 2.2, "KV probe")."""
+    return t_prefix + t_suffix < t_full

@@ -609,3 +609,64 @@ def test_decode_matches_hf_kv_cache_generation():
                 assert abs(p_hf - tops[j][b]) < 1e-6
     conf = oracle.gen_confidence(np.stack(tops))
     assert conf.shape == (B,) and np.all((conf > 0) & (conf <= 1))
+
+
+# ----------------------------------------------------------------- RSBCM (Alg. RsbcmEvict), KV probe
+
+def test_rsbcm_stress_test_eviction_count():
+    """App. RSBCM validation: capacity 4, B = 8 branch blocks per solve, 20 solves: exactly
+    B - N_max = 4 evictions per solve and 80 in total, whatever the scores."""
+    rng = np.random.default_rng(12)
+    total = 0
+    for problem in range(20):
+        blocks = [(b, float(rng.uniform(0, 1)), int(rng.integers(0, 3))) for b in range(8)]
+        kept, ev = oracle.rsbcm_evict(blocks, 4)
+        assert len(ev) == 4 and len(kept) == 4
+        total += len(ev)
+        # the evicted blocks are the four of least omega
+        om = sorted(oracle.rsbcm_omega(s, d) for _, s, d in blocks)
+        assert max(oracle.rsbcm_omega(s, d) for i, s, d in blocks if i in ev) <= om[4]
+    assert total == 20 * (8 - 4) == 80
+
+
+def test_rsbcm_order_depth_ties_and_capacity():
+    # omega = score / (depth + 1): a deep high-score block goes before a shallow low-score one
+    blocks = [(10, 0.9, 8), (11, 0.2, 0), (12, 0.5, 1), (13, 0.5, 1), (14, 0.05, 0)]
+    kept, ev = oracle.rsbcm_evict(blocks, 2)
+    # omegas: 0.1, 0.2, 0.25, 0.25, 0.05 -> 14, 10, 11 ; ties (12, 13) keep both
+    assert ev == [14, 10, 11] and [b[0] for b in kept] == [12, 13]
+    _, ev = oracle.rsbcm_evict(blocks, 3)
+    assert ev == [14, 10]
+    _, ev = oracle.rsbcm_evict(blocks, 4)
+    assert ev == [14]
+    # equal omegas go in insertion order
+    _, ev = oracle.rsbcm_evict([(1, 0.5, 1), (2, 0.25, 0), (3, 1.0, 3), (4, 0.25, 0)], 1)
+    assert ev == [1, 2, 3]
+    assert oracle.rsbcm_evict(blocks, 0)[1] == [14, 10, 11, 12, 13]
+    assert oracle.rsbcm_evict(blocks, 5)[1] == [] and oracle.rsbcm_evict([], 0) == ([], [])
+
+
+def test_rsbcm_brute_force_sorted():
+    """Evicting the argmin one at a time equals taking the size - N_max least (omega, insertion) keys."""
+    rng = np.random.default_rng(13)
+    for _ in range(200):
+        n = int(rng.integers(0, 40))
+        blocks = [(i, float(np.float32(rng.choice([0.25, 0.5, rng.uniform(-1, 2)]))), int(rng.integers(0, 5)))
+                  for i in range(n)]
+        cap = int(rng.integers(0, 45))
+        kept, ev = oracle.rsbcm_evict(blocks, cap)
+        keys = sorted(range(n), key=lambda i: (blocks[i][1] / (blocks[i][2] + 1), i))
+        assert ev == [blocks[i][0] for i in keys[: max(0, n - cap)]]
+        assert sorted(b[0] for b in kept) == sorted(blocks[i][0] for i in keys[max(0, n - cap):])
+
+
+def test_kv_probe_paper_cost_table():
+    with open(os.path.join(GOLDEN, "kv_probe_cost_constants.json")) as f:
+        g = json.load(f)
+    for row in g["rows"]:
+        net = row["batch_full"] - row["prefix_fwd"] - row["sfx_kv"]
+        assert abs(net - row["net_saved"]) <= 0.1 + 1e-9, row["model"]
+        assert oracle.kv_probe_share(row["batch_full"], row["prefix_fwd"], row["sfx_kv"])
+        # sharing stops paying once root forward + suffix decode cost what the recompute costs
+        assert not oracle.kv_probe_share(row["batch_full"], row["batch_full"] - row["sfx_kv"], row["sfx_kv"])
+    assert [oracle.kv_probe_bucket(n) for n in (0, 63, 64, 1023, 1024, 1087, 1088)] == [0, 0, 1, 15, 16, 16, 17]
