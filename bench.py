@@ -23,6 +23,9 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   decode       batched greedy decode of 8 branches over the same prefix cache
                (suffix prefill, one-token steps, the CGEE gate), per step
                against the HBM bytes it must stream (weights, lm_head, prefix KV)
+  kv_probe     the library's KV probe at 8 branches over the same prefix: the
+               batched full recompute, the root forward and the batched suffix
+               decode over the shared cache (min of 3 each), and its verdict
   cpu_baseline the float64 CPU oracle on a bounded sample of the workload
 
     python bench.py [--steps K] [--warmup W] [--workload 7b_single]
@@ -341,6 +344,27 @@ def measure_decode(mw, kv, shape, n, args, hip, sp, stream, dev):
     return decode
 
 
+def measure_kv_probe(mw, shape, n, args, stream, dev):
+    """The KV probe (Sec. 2.2) at the paper's cost-constants setting: B = 8 branches
+    over the workload's prefix with a DECODE_SUFFIX-token suffix; the three paths
+    are timed as the minimum of 3 runs each by the library's probe."""
+    import paper_2606_09937_amd as rk
+    import workloads
+
+    Bd, sd = DECODE_BRANCHES, DECODE_SUFFIX
+    ptoks = workloads.make_tokens(n, shape.vocab, seed=args.seed, name="prefix", device=dev)
+    stoks = workloads.make_tokens(Bd * sd, shape.vocab, seed=args.seed, name="suffix",
+                                  device=dev).reshape(Bd, sd).contiguous()
+    probe = rk.KVProbe(3)
+    share, t, _ = probe.decide(mw, ptoks, stoks, stream=stream)
+    out = {"n_branches": Bd, "prefix_len": n, "suffix_len": sd, "reps": 3,
+           "batch_full_ms": t[0], "prefix_fwd_ms": t[1], "sfx_kv_ms": t[2], "net_saved_ms": t[0] - t[1] - t[2],
+           "share": share}
+    log(f"kv probe B={Bd} n={n} s={sd}: full {t[0]:.1f} ms, prefix {t[1]:.1f} ms, suffix {t[2]:.1f} ms, "
+        f"net saved {t[0] - t[1] - t[2]:.1f} ms, share={share}")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -357,6 +381,7 @@ def main():
     ap.add_argument("--no-tau-sweep", action="store_true")
     ap.add_argument("--no-prefill", action="store_true", help="skip the root-forward (prefill) timing")
     ap.add_argument("--no-decode", action="store_true", help="skip the batched-decode timing")
+    ap.add_argument("--no-probe", action="store_true", help="skip the KV probe timing")
     ap.add_argument("--decode-only", action="store_true",
                     help="time only the batched decode (for a kernel trace of it) and print its JSON")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -606,6 +631,7 @@ def main():
         del pws, pk, pv, hr
 
     decode = None if args.no_decode else measure_decode(mw, kv, shape, n, args, hip, sp, stream, dev)
+    kv_probe = None if args.no_probe else measure_kv_probe(mw, shape, n, args, stream, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -643,6 +669,7 @@ def main():
         "tau_sweep": tau_sweep,
         "prefill": prefill,
         "decode": decode,
+        "kv_probe": kv_probe,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

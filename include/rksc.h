@@ -8,8 +8,10 @@
  * (Sec. 2.2 "KV broadcast and batched decode"), the root forward that computes
  * that cache and the root hidden states (Eq. prefix_fwd), the batched decode
  * of the branches over it with the generation confidence (Eq. gen_conf) and
- * the CGEE verify-skip gate (Eq. cgee_gate), and the layer-weighted cosine
- * similarity of the ASKS gate (Eq. asks_sim, Alg. AsksGate).
+ * the CGEE verify-skip gate (Eq. cgee_gate), the layer-weighted cosine
+ * similarity of the ASKS gate (Eq. asks_sim, Alg. AsksGate), and the host
+ * runtime around them: the RSBCM block table (Alg. RsbcmEvict) and the KV
+ * probe.
  *
  * Conventions shared by every entry point:
  *   - Tensor arguments are DEVICE pointers to dense row-major arrays.
@@ -36,7 +38,7 @@
 extern "C" {
 #endif
 
-#define RKSC_ABI_VERSION 3
+#define RKSC_ABI_VERSION 4
 
 /* Largest number of branches one verify call accepts. */
 #define RKSC_MAX_BRANCHES 64
@@ -254,6 +256,73 @@ rksc_status rksc_cgee_gate(const float* conf, int32_t n_branches, int32_t n_step
  */
 rksc_status rksc_asks_similarity(const float* hidden, int32_t n_layers, int32_t n_branches,
                                  int32_t d_model, float alpha, float* S, void* stream);
+
+/*
+ * RSBCM block table (Sec. 2.4 "RSBCM"; Alg. RsbcmEvict): host-side
+ * bookkeeping of cached KV blocks under tree search. Each block carries an
+ * importance omega = score / (depth + 1), with score the owning branch's score
+ * (e.g. its generation confidence) and depth its depth in the search tree.
+ * rksc_block_table_evict runs the algorithm: while the table holds more than
+ * `capacity` blocks, it removes the block of smallest omega (the earliest
+ * inserted among equal omegas, omega evaluated in double). The ids are the
+ * caller's (a KV block, a branch-cache slot); the caller releases the memory
+ * of the evicted ids. A table is not thread-safe.
+ */
+typedef struct rksc_block_table rksc_block_table;
+
+/* New empty table (capacity N_max >= 0; the paper's default is 2000); NULL on
+ * a bad argument. Destroy with rksc_block_table_destroy. */
+rksc_block_table* rksc_block_table_create(int32_t capacity);
+void rksc_block_table_destroy(rksc_block_table* table);
+/* Adds block_id (not yet in the table) with a finite score and depth >= 0. */
+rksc_status rksc_block_table_insert(rksc_block_table* table, int64_t block_id, float score, int32_t depth);
+/* Replaces the score of a block in the table (its omega changes with it). */
+rksc_status rksc_block_table_set_score(rksc_block_table* table, int64_t block_id, float score);
+/* Removes a block without counting an eviction (the caller freed it). */
+rksc_status rksc_block_table_remove(rksc_block_table* table, int64_t block_id);
+/* Alg. RsbcmEvict: evicts size - capacity blocks (if positive) in ascending
+ * omega order, writing their ids to evicted[0 .. *n_evicted) (host array of
+ * max_evicted entries; RKSC_ERR_INVALID_ARGUMENT, with nothing evicted, if it
+ * is shorter than needed). */
+rksc_status rksc_block_table_evict(rksc_block_table* table, int64_t* evicted, int32_t max_evicted,
+                                   int32_t* n_evicted);
+/* Blocks in the table; evictions so far (-1 for a NULL table). */
+int32_t rksc_block_table_size(const rksc_block_table* table);
+int64_t rksc_block_table_evicted_total(const rksc_block_table* table);
+
+/*
+ * KV probe (Sec. 2.2, paragraph "KV probe"): decides per 64-token
+ * prefix-length bucket k = floor(n / 64) whether sharing the prefix cache pays
+ * off. At the first decide call of a bucket it times, each as the minimum of
+ * `reps` runs (the paper uses 3) with HIP events on `stream`:
+ *   (i)   the batched full recompute: every branch's prefix and suffix as one
+ *         sequence (rksc_decode_suffix over an empty prefix, B x (n + s) tokens);
+ *   (ii)  one root forward over the prefix (rksc_prefill);
+ *   (iii) the batched suffix decode over that shared cache (rksc_decode_suffix);
+ * and stores share = 1 iff t(ii) + t(iii) < t(i). Later calls in the bucket
+ * return the stored verdict and run nothing. A timing call blocks until the
+ * stream has run the paths. A probe is not thread-safe.
+ */
+typedef struct rksc_kv_probe rksc_kv_probe;
+
+rksc_kv_probe* rksc_kv_probe_create(int32_t reps);
+void rksc_kv_probe_destroy(rksc_kv_probe* probe);
+/* Device workspace the timing runs need (0 if the shape is invalid). */
+size_t rksc_kv_probe_workspace_size(const rksc_model_config* cfg, int32_t n_prefix, int32_t n_branches,
+                                    int32_t suffix_len);
+/*
+ * prefix_tokens  [n] int32 device; suffix_tokens [B, s] int32 device.
+ * share          host out: 1 share the prefix cache, 0 recompute.
+ * times_ms       host out [3] or NULL: t(i), t(ii), t(iii) of the bucket's probe.
+ * probed         host out or NULL: 1 if this call ran the timing, 0 if the
+ *                bucket's verdict was stored.
+ */
+rksc_status rksc_kv_probe_decide(rksc_kv_probe* probe, const rksc_weights* weights, const int32_t* prefix_tokens,
+                                 int32_t n_prefix, const int32_t* suffix_tokens, int32_t n_branches,
+                                 int32_t suffix_len, void* workspace, size_t workspace_bytes, void* stream,
+                                 int32_t* share, float* times_ms, int32_t* probed);
+/* The stored verdict of n_prefix's bucket: share = -1 if it was never probed. */
+rksc_status rksc_kv_probe_lookup(const rksc_kv_probe* probe, int32_t n_prefix, int32_t* share, float* times_ms);
 
 const char* rksc_status_string(rksc_status status);
 

@@ -24,7 +24,7 @@ __all__ = [
     "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_attention",
     "verify_forward", "asks_similarity", "prefill", "rksc_prefill", "rksc_prefill_workspace_size", "model_config",
     "BranchCache", "Decoder", "rksc_decode_workspace_size", "rksc_decode_suffix", "rksc_decode_step",
-    "rksc_cgee_gate", "cgee_gate", "RKSC_ABI_VERSION",
+    "rksc_cgee_gate", "cgee_gate", "RKSC_ABI_VERSION", "BlockTable", "KVProbe",
     "RKSC_OK", "RKSC_ERR_INVALID_ARGUMENT", "RKSC_ERR_UNSUPPORTED",
     "RKSC_ERR_WORKSPACE_TOO_SMALL", "RKSC_ERR_HIP", "RKSC_F32", "RKSC_BF16", "RKSC_MAX_BRANCHES",
 ]
@@ -37,7 +37,7 @@ RKSC_ERR_HIP = -4
 RKSC_F32 = 0
 RKSC_BF16 = 1
 RKSC_MAX_BRANCHES = 64
-RKSC_ABI_VERSION = 3
+RKSC_ABI_VERSION = 4
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 
@@ -120,6 +120,34 @@ def load_library():
                                      ctypes.POINTER(BranchKVStruct), vp, i32, vp, vp, vp, vp, sz, vp]
     lib.rksc_cgee_gate.restype = i32
     lib.rksc_cgee_gate.argtypes = [vp, i32, i32, f32, f32, vp, vp, vp, vp, vp]
+    i64 = ctypes.c_int64
+    lib.rksc_block_table_create.restype = vp
+    lib.rksc_block_table_create.argtypes = [i32]
+    lib.rksc_block_table_destroy.restype = None
+    lib.rksc_block_table_destroy.argtypes = [vp]
+    lib.rksc_block_table_insert.restype = i32
+    lib.rksc_block_table_insert.argtypes = [vp, i64, f32, i32]
+    lib.rksc_block_table_set_score.restype = i32
+    lib.rksc_block_table_set_score.argtypes = [vp, i64, f32]
+    lib.rksc_block_table_remove.restype = i32
+    lib.rksc_block_table_remove.argtypes = [vp, i64]
+    lib.rksc_block_table_evict.restype = i32
+    lib.rksc_block_table_evict.argtypes = [vp, ctypes.POINTER(i64), i32, ctypes.POINTER(i32)]
+    lib.rksc_block_table_size.restype = i32
+    lib.rksc_block_table_size.argtypes = [vp]
+    lib.rksc_block_table_evicted_total.restype = i64
+    lib.rksc_block_table_evicted_total.argtypes = [vp]
+    lib.rksc_kv_probe_create.restype = vp
+    lib.rksc_kv_probe_create.argtypes = [i32]
+    lib.rksc_kv_probe_destroy.restype = None
+    lib.rksc_kv_probe_destroy.argtypes = [vp]
+    lib.rksc_kv_probe_workspace_size.restype = sz
+    lib.rksc_kv_probe_workspace_size.argtypes = [ctypes.POINTER(ModelConfig), i32, i32, i32]
+    lib.rksc_kv_probe_decide.restype = i32
+    lib.rksc_kv_probe_decide.argtypes = [vp, ctypes.POINTER(Weights), vp, i32, vp, i32, i32, vp, sz, vp,
+                                         ctypes.POINTER(i32), ctypes.POINTER(f32), ctypes.POINTER(i32)]
+    lib.rksc_kv_probe_lookup.restype = i32
+    lib.rksc_kv_probe_lookup.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(f32)]
     lib.rksc_asks_similarity.restype = i32
     lib.rksc_asks_similarity.argtypes = [vp, i32, i32, i32, f32, vp, vp]
     lib.rksc_status_string.restype = ctypes.c_char_p
@@ -452,3 +480,96 @@ class Decoder:
 
     def gate(self, tau_conf: float = 0.70, r_gap: float = 0.06, stream=None):
         return cgee_gate(self.conf, self.n_steps, tau_conf, r_gap, stream)
+
+
+class BlockTable:
+    """The RSBCM block table (rksc_block_table_*): host-side, no GPU needed."""
+
+    def __init__(self, capacity: int):
+        lib = load_library()
+        self._lib = lib
+        self.capacity = int(capacity)
+        self._t = lib.rksc_block_table_create(int(capacity))
+        if not self._t:
+            raise RkscError(RKSC_ERR_INVALID_ARGUMENT, rksc_last_error())
+
+    def __del__(self):
+        if getattr(self, "_t", None):
+            self._lib.rksc_block_table_destroy(self._t)
+            self._t = None
+
+    def insert(self, block_id: int, score: float, depth: int) -> None:
+        _check(self._lib.rksc_block_table_insert(self._t, int(block_id), float(score), int(depth)))
+
+    def set_score(self, block_id: int, score: float) -> None:
+        _check(self._lib.rksc_block_table_set_score(self._t, int(block_id), float(score)))
+
+    def remove(self, block_id: int) -> None:
+        _check(self._lib.rksc_block_table_remove(self._t, int(block_id)))
+
+    def evict(self) -> list:
+        """Alg. RsbcmEvict: the evicted ids, in eviction order."""
+        need = max(0, len(self) - self.capacity)
+        buf = (ctypes.c_int64 * max(1, need))()
+        n = ctypes.c_int32(0)
+        _check(self._lib.rksc_block_table_evict(self._t, buf, max(1, need), ctypes.byref(n)))
+        return [int(buf[i]) for i in range(n.value)]
+
+    def __len__(self) -> int:
+        return int(self._lib.rksc_block_table_size(self._t))
+
+    @property
+    def evicted_total(self) -> int:
+        return int(self._lib.rksc_block_table_evicted_total(self._t))
+
+
+class KVProbe:
+    """The KV probe (rksc_kv_probe_*): per 64-token prefix bucket, times the three paths once
+    and keeps the verdict."""
+
+    def __init__(self, reps: int = 3):
+        lib = load_library()
+        self._lib = lib
+        self._p = lib.rksc_kv_probe_create(int(reps))
+        if not self._p:
+            raise RkscError(RKSC_ERR_INVALID_ARGUMENT, rksc_last_error())
+
+    def __del__(self):
+        if getattr(self, "_p", None):
+            self._lib.rksc_kv_probe_destroy(self._p)
+            self._p = None
+
+    @staticmethod
+    def workspace_size(shape, n_prefix: int, n_branches: int, suffix_len: int) -> int:
+        cfg = model_config(shape)
+        n = int(load_library().rksc_kv_probe_workspace_size(ctypes.byref(cfg), n_prefix, n_branches, suffix_len))
+        if n == 0:
+            raise RkscError(RKSC_ERR_INVALID_ARGUMENT, rksc_last_error())
+        return n
+
+    def decide(self, weights, prefix_tokens: torch.Tensor, suffix_tokens: torch.Tensor,
+               workspace: Optional[torch.Tensor] = None, stream=None):
+        """Returns (share: bool, times_ms [full, prefix, suffix], probed: bool)."""
+        B, s = suffix_tokens.shape
+        n = int(prefix_tokens.numel())
+        if workspace is None:
+            workspace = torch.empty(self.workspace_size(weights.shape, n, B, s), dtype=torch.uint8,
+                                    device=prefix_tokens.device)
+        w, keep = _weights_struct(weights)
+        share = ctypes.c_int32(0)
+        probed = ctypes.c_int32(0)
+        times = (ctypes.c_float * 3)()
+        st = self._lib.rksc_kv_probe_decide(self._p, ctypes.byref(w), _ptr(prefix_tokens), n, _ptr(suffix_tokens),
+                                            int(B), int(s), _ptr(workspace),
+                                            int(workspace.numel() * workspace.element_size()), _stream(stream),
+                                            ctypes.byref(share), times, ctypes.byref(probed))
+        del keep
+        _check(st)
+        return bool(share.value), [float(t) for t in times], bool(probed.value)
+
+    def lookup(self, n_prefix: int):
+        """The stored verdict of n_prefix's bucket: None if never probed, else (share, times_ms)."""
+        share = ctypes.c_int32(0)
+        times = (ctypes.c_float * 3)()
+        _check(self._lib.rksc_kv_probe_lookup(self._p, int(n_prefix), ctypes.byref(share), times))
+        return None if share.value < 0 else (bool(share.value), [float(t) for t in times])

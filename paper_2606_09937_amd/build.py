@@ -19,7 +19,8 @@ BUILD_DIR = os.path.join(os.path.dirname(PKG_DIR), "_build", "rksc")
 LIB_PATH = os.path.join(PKG_DIR, "librksc.so")
 ARCH = "gfx950"
 
-SOURCES = ["k_rows.hip", "k_gemm.hip", "k_attn.hip", "k_entropy.hip", "k_asks.hip", "rksc_api.cpp"]
+SOURCES = ["k_rows.hip", "k_gemm.hip", "k_attn.hip", "k_entropy.hip", "k_asks.hip", "rksc_api.cpp",
+           "rksc_runtime.cpp"]
 
 COMMON_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",

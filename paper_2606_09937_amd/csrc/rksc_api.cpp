@@ -11,12 +11,16 @@
 #include "../../include/rksc.h"
 #include "../../include/rksc_testing.h"
 #include "kernels.h"
+#include "status.h"
 
 #define RKSC_EXPORT extern "C" __attribute__((visibility("default")))
 
-namespace {
+namespace rksc {
 
-thread_local std::string g_last_error;
+std::string& last_error() {
+  thread_local std::string text;
+  return text;
+}
 
 rksc_status fail(rksc_status st, const char* fmt, ...) {
   char buf[512];
@@ -24,14 +28,21 @@ rksc_status fail(rksc_status st, const char* fmt, ...) {
   va_start(ap, fmt);
   vsnprintf(buf, sizeof buf, fmt, ap);
   va_end(ap);
-  g_last_error = buf;
+  last_error() = buf;
   return st;
 }
 
 rksc_status ok() {
-  g_last_error.clear();
+  last_error().clear();
   return RKSC_OK;
 }
+
+}  // namespace rksc
+
+namespace {
+
+using rksc::fail;
+using rksc::ok;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -142,7 +153,7 @@ RKSC_EXPORT const char* rksc_status_string(rksc_status s) {
   return "unknown status";
 }
 
-RKSC_EXPORT const char* rksc_last_error(void) { return g_last_error.c_str(); }
+RKSC_EXPORT const char* rksc_last_error(void) { return rksc::last_error().c_str(); }
 
 RKSC_EXPORT size_t rksc_verify_workspace_size(const rksc_model_config* cfg, int32_t n_branches,
                                               int32_t branch_len, int32_t n_prefix) {
