@@ -36,6 +36,9 @@ Batched decode (Sec. 2.2; the stepwise loop of the implementation notes): a
   confidence p_b (Eq. gen_conf), and Eq. cgee_gate decides on the p_b.
 RSBCM (Sec. 2.4, Alg. RsbcmEvict): while the block table holds more than
   N_max blocks, evict the block of least omega = score / (depth + 1).
+Tree sharing: a search-tree node's tokens are run once over its parent's cache
+  and the resulting cache serves all of its children.
+ASKS gate (Alg. AsksGate): a branch receives the shared cache iff sigma_b >= tau.
 KV probe (Sec. 2.2, paragraph "KV probe"): per 64-token prefix bucket, share
   the prefix cache iff t(root forward) + t(suffix decode) < t(full recompute).
 """
@@ -49,7 +52,7 @@ __all__ = [
     "layer_entropies", "exit_layer", "verify_forward", "asks_weights",
     "asks_similarity", "unit_rows", "root_similarity",
     "final_logits", "top1", "decode_suffix", "decode_step", "gen_confidence", "cgee_gate",
-    "rsbcm_omega", "rsbcm_evict", "kv_probe_bucket", "kv_probe_share",
+    "rsbcm_omega", "rsbcm_evict", "kv_probe_bucket", "kv_probe_share", "prefix_extend", "asks_gate",
 ]
 
 
@@ -411,3 +414,26 @@ def kv_probe_share(t_full: float, t_prefix: float, t_suffix: float) -> bool:
     """Sharing is beneficial iff t(ii) + t(iii) < t(i): root forward plus batched
     suffix decode against batched full recompute (Sec. 2.2, "KV probe")."""
     return t_prefix + t_suffix < t_full
+
+
+def prefix_extend(weights, cfg, parent_k, parent_v, tokens):
+    """A tree node's cache: its m tokens at positions n..n+m-1 attend to the
+    parent's n cached entries and causally to each other. Returns (k [L, Hkv, n+m,
+    hd], v, h_node [L, d]): the parent's entries followed by the node's, and the
+    last node token's layer outputs (not normalised)."""
+    tokens = np.asarray(tokens, dtype=np.int64).reshape(1, -1)
+    n = 0 if parent_k is None else int(parent_k.shape[2])
+    hidden, ks, vs = decoder_stack(weights, cfg, tokens, n, parent_k if n else None, parent_v if n else None)
+    if n:
+        k = np.concatenate([f64(parent_k), ks[:, 0]], axis=2)
+        v = np.concatenate([f64(parent_v), vs[:, 0]], axis=2)
+    else:
+        k, v = ks[:, 0], vs[:, 0]
+    return k, v, hidden[:, 0, -1, :]
+
+
+def asks_gate(hidden, h_root_unit, alpha: float, tau: float):
+    """Alg. AsksGate: sigma_b of Eq. asks_sim against the unit root rows and the
+    shared set {b : sigma_b >= tau}, for branch rows hidden [L, B, d]."""
+    sigma = root_similarity(hidden, h_root_unit, alpha)
+    return sigma, sigma >= tau

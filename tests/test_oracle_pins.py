@@ -670,3 +670,43 @@ def test_kv_probe_paper_cost_table():
         # sharing stops paying once root forward + suffix decode cost what the recompute costs
         assert not oracle.kv_probe_share(row["batch_full"], row["batch_full"] - row["sfx_kv"], row["sfx_kv"])
     assert [oracle.kv_probe_bucket(n) for n in (0, 63, 64, 1023, 1024, 1087, 1088)] == [0, 0, 1, 15, 16, 16, 17]
+
+
+# ----------------------------------------------------------------- tree sharing, ASKS gate (Alg. AsksGate)
+
+def test_prefix_extend_equals_prefill_of_the_concatenation():
+    """A node's cache built on its parent's equals one causal prefill of [root; node] (and two levels
+    [root; a; b]); h_node is the last token's rows of that prefill."""
+    shape = GQA_SHAPE
+    mw = _randomise_gains(workloads.make_model(shape, seed=14))
+    root = workloads.make_tokens(11, shape.vocab, seed=14, name="prefix").numpy()
+    a = workloads.make_tokens(6, shape.vocab, seed=14, name="node_a").numpy()
+    b = workloads.make_tokens(4, shape.vocab, seed=14, name="node_b").numpy()
+    pk, pv, _ = oracle.prefill(mw, shape, root)
+    ka, va, ha = oracle.prefix_extend(mw, shape, pk, pv, a)
+    rk_, rv_, rh_ = oracle.prefill(mw, shape, np.concatenate([root, a]))
+    np.testing.assert_allclose(ka, rk_, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(va, rv_, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(ha, rh_, rtol=1e-10, atol=1e-12)
+    kb, vb, hb = oracle.prefix_extend(mw, shape, ka, va, b)
+    rk2, rv2, rh2 = oracle.prefill(mw, shape, np.concatenate([root, a, b]))
+    np.testing.assert_allclose(kb, rk2, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(hb, rh2, rtol=1e-10, atol=1e-12)
+    # an empty parent is a plain prefill
+    k0, v0, h0 = oracle.prefix_extend(mw, shape, None, None, root)
+    np.testing.assert_allclose(k0, pk, rtol=1e-12, atol=1e-14)
+
+
+def test_asks_gate_threshold_and_identity():
+    rng = np.random.default_rng(15)
+    L, d = 6, 48
+    root = oracle.unit_rows(rng.standard_normal((L, d)))
+    same = np.stack([root * 3.0, -root, rng.standard_normal((L, d)), np.zeros((L, d))], axis=1)   # [L, 4, d]
+    sigma, shared = oracle.asks_gate(same, root, 1.5, 0.82)
+    assert abs(sigma[0] - 1.0) < 1e-12 and abs(sigma[1] + 1.0) < 1e-12 and sigma[3] == 0.0
+    assert list(shared) == [True, False, bool(sigma[2] >= 0.82), False]
+    # the threshold is inclusive (Alg. AsksGate shares at sigma_b >= tau)
+    assert oracle.asks_gate(same, root, 1.5, float(sigma[2]))[1][2]
+    # tau = -1 shares everything with a finite sigma, tau above 1 nothing
+    assert oracle.asks_gate(same, root, 1.5, -1.0)[1].all()
+    assert not oracle.asks_gate(same, root, 1.5, 1.0 + 1e-9)[1].any()
