@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define RKSC_ABI_VERSION 4
+#define RKSC_ABI_VERSION 5
 
 /* Largest number of branches one verify call accepts. */
 #define RKSC_MAX_BRANCHES 64
@@ -220,6 +220,51 @@ rksc_status rksc_decode_suffix(const rksc_weights* weights, const rksc_prefix_kv
 rksc_status rksc_decode_step(const rksc_weights* weights, const rksc_prefix_kv* prefix_kv, rksc_branch_kv* branch_kv,
                              const int32_t* tokens, int32_t n_branches, int32_t* next_token, float* p_top,
                              float* conf, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace rksc_prefix_extend needs for n_new tokens on top of an
+ * n_parent-entry cache (0 if the shape is invalid). */
+size_t rksc_prefix_extend_workspace_size(const rksc_model_config* cfg, int32_t n_parent, int32_t n_new);
+
+/*
+ * Tree sharing (Sec. 1: siblings share an intermediate node; the same
+ * "compute once, broadcast" of Sec. 2.2 one level down): the cache of a
+ * search-tree node whose m tokens follow its parent's n cached entries. The
+ * child cache receives the parent's entries 0..n-1 (copied) and the entries
+ * n..n+m-1 of the node's tokens, computed in one causal pass at positions
+ * n..n+m-1 over the parent cache; every child of the node then uses it as its
+ * rksc_prefix_kv (n_prefix = n + m) in rksc_verify_forward / rksc_decode_*.
+ * h_node receives the node's own "root" rows for the next level's ASKS gate:
+ * the last new token's layer outputs, unit-normalised (as h_root of
+ * rksc_prefill; with n = 0 this call is rksc_prefill).
+ *
+ * parent     the parent cache, n >= 0 entries [L, Hkv, n, hd]; it must not
+ *            overlap k_out / v_out.
+ * tokens     [m] int32 device (m = n_new >= 1).
+ * k_out      [L, Hkv, n + m, hd] device out, storage type; v_out likewise.
+ * h_node     [L, d] fp32 device out, or NULL.
+ * workspace  at least rksc_prefix_extend_workspace_size() bytes, 256-byte aligned.
+ */
+rksc_status rksc_prefix_extend(const rksc_weights* weights, const rksc_prefix_kv* parent, const int32_t* tokens,
+                               int32_t n_new, void* k_out, void* v_out, float* h_node, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/*
+ * ASKS gate (Alg. AsksGate; Eq. asks_sim against the root): for each branch b
+ *   sigma_b = sum_l w_l < h_b^(l) / |h_b^(l)| , h_root^(l) >,
+ *   w_l = exp(alpha l / L) / sum_{l'} exp(alpha l' / L),
+ * with h_root the unit rows of rksc_prefill (not normalised again), and
+ * shared[b] = 1 iff sigma_b >= tau: the branch receives the shared cache;
+ * below tau it falls back to its own recomputation (Sec. 2.2). A zero branch
+ * row contributes 0. The decision is taken in fp32.
+ *
+ * hidden  [L, B, d] fp32 device: the branches' per-layer rows (e.g. the unit
+ *         root rows of each branch's own rksc_prefill, or hidden_last of a
+ *         verify pass); h_root [L, d] fp32 device.
+ * sigma   [B] fp32 device out; shared [B] int32 device out.
+ * L, B, d >= 1; alpha finite; tau not NaN.
+ */
+rksc_status rksc_asks_gate(const float* hidden, const float* h_root, int32_t n_layers, int32_t n_branches,
+                           int32_t d_model, float alpha, float tau, float* sigma, int32_t* shared, void* stream);
 
 /*
  * CGEE gate (Eq. cgee_gate) over the generation confidences

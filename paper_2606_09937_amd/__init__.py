@@ -25,6 +25,7 @@ __all__ = [
     "verify_forward", "asks_similarity", "prefill", "rksc_prefill", "rksc_prefill_workspace_size", "model_config",
     "BranchCache", "Decoder", "rksc_decode_workspace_size", "rksc_decode_suffix", "rksc_decode_step",
     "rksc_cgee_gate", "cgee_gate", "RKSC_ABI_VERSION", "BlockTable", "KVProbe",
+    "rksc_prefix_extend", "rksc_prefix_extend_workspace_size", "prefix_extend", "rksc_asks_gate", "asks_gate",
     "RKSC_OK", "RKSC_ERR_INVALID_ARGUMENT", "RKSC_ERR_UNSUPPORTED",
     "RKSC_ERR_WORKSPACE_TOO_SMALL", "RKSC_ERR_HIP", "RKSC_F32", "RKSC_BF16", "RKSC_MAX_BRANCHES",
 ]
@@ -37,7 +38,7 @@ RKSC_ERR_HIP = -4
 RKSC_F32 = 0
 RKSC_BF16 = 1
 RKSC_MAX_BRANCHES = 64
-RKSC_ABI_VERSION = 4
+RKSC_ABI_VERSION = 5
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 
@@ -118,6 +119,13 @@ def load_library():
     lib.rksc_decode_step.restype = i32
     lib.rksc_decode_step.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV),
                                      ctypes.POINTER(BranchKVStruct), vp, i32, vp, vp, vp, vp, sz, vp]
+    lib.rksc_prefix_extend_workspace_size.restype = sz
+    lib.rksc_prefix_extend_workspace_size.argtypes = [ctypes.POINTER(ModelConfig), i32, i32]
+    lib.rksc_prefix_extend.restype = i32
+    lib.rksc_prefix_extend.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, vp, vp, vp, vp,
+                                       sz, vp]
+    lib.rksc_asks_gate.restype = i32
+    lib.rksc_asks_gate.argtypes = [vp, vp, i32, i32, i32, f32, f32, vp, vp, vp]
     lib.rksc_cgee_gate.restype = i32
     lib.rksc_cgee_gate.argtypes = [vp, i32, i32, f32, f32, vp, vp, vp, vp, vp]
     i64 = ctypes.c_int64
@@ -573,3 +581,58 @@ class KVProbe:
         times = (ctypes.c_float * 3)()
         _check(self._lib.rksc_kv_probe_lookup(self._p, int(n_prefix), ctypes.byref(share), times))
         return None if share.value < 0 else (bool(share.value), [float(t) for t in times])
+
+
+def rksc_prefix_extend_workspace_size(shape, n_parent: int, n_new: int) -> int:
+    cfg = model_config(shape)
+    n = int(load_library().rksc_prefix_extend_workspace_size(ctypes.byref(cfg), n_parent, n_new))
+    if n == 0:
+        raise RkscError(RKSC_ERR_INVALID_ARGUMENT, rksc_last_error())
+    return n
+
+
+def rksc_prefix_extend(weights, parent_k, parent_v, tokens: torch.Tensor, k_out: torch.Tensor, v_out: torch.Tensor,
+                       h_node: Optional[torch.Tensor], workspace: torch.Tensor, stream=None) -> None:
+    """Marshal torch device tensors into rksc_prefix_extend (asynchronous on `stream`)."""
+    lib = load_library()
+    w, keep = _weights_struct(weights)
+    n = int(parent_k.shape[2]) if parent_k is not None else 0
+    kv = PrefixKV(n, _ptr(parent_k), _ptr(parent_v))
+    st = lib.rksc_prefix_extend(ctypes.byref(w), ctypes.byref(kv), _ptr(tokens), int(tokens.numel()), _ptr(k_out),
+                                _ptr(v_out), _ptr(h_node), _ptr(workspace),
+                                int(workspace.numel() * workspace.element_size()), _stream(stream))
+    del keep
+    _check(st)
+
+
+def prefix_extend(weights, parent_k, parent_v, tokens: torch.Tensor, stream=None):
+    """A tree node's cache on top of its parent's: returns (k [L, Hkv, n+m, hd], v, h_node [L, d] unit rows)."""
+    shape = weights.shape
+    n = int(parent_k.shape[2]) if parent_k is not None else 0
+    m = int(tokens.numel())
+    dev = tokens.device
+    L = len(weights.layers)
+    dtype = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    ws = torch.empty(rksc_prefix_extend_workspace_size(shape, n, m), dtype=torch.uint8, device=dev)
+    k = torch.empty((L, shape.n_kv_heads, n + m, shape.head_dim), dtype=dtype, device=dev)
+    v = torch.empty_like(k)
+    h = torch.empty((L, shape.d_model), dtype=torch.float32, device=dev)
+    rksc_prefix_extend(weights, parent_k, parent_v, tokens.contiguous(), k, v, h, ws, stream)
+    return k, v, h
+
+
+def rksc_asks_gate(hidden: torch.Tensor, h_root: torch.Tensor, alpha: float, tau: float, sigma: torch.Tensor,
+                   shared: torch.Tensor, stream=None) -> None:
+    """Marshal torch device tensors into rksc_asks_gate (asynchronous on `stream`)."""
+    L, B, d = hidden.shape
+    _check(load_library().rksc_asks_gate(_ptr(hidden), _ptr(h_root), L, B, d, float(alpha), float(tau), _ptr(sigma),
+                                         _ptr(shared), _stream(stream)))
+
+
+def asks_gate(hidden: torch.Tensor, h_root: torch.Tensor, alpha: float = 1.5, tau: float = 0.82, stream=None):
+    """Alg. AsksGate on the device: returns (sigma [B] fp32, shared [B] int32)."""
+    L, B, d = hidden.shape
+    sigma = torch.empty((B,), dtype=torch.float32, device=hidden.device)
+    shared = torch.empty((B,), dtype=torch.int32, device=hidden.device)
+    rksc_asks_gate(hidden.contiguous(), h_root.contiguous(), alpha, tau, sigma, shared, stream)
+    return sigma, shared

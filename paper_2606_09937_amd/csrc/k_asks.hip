@@ -54,10 +54,60 @@ __global__ __launch_bounds__(256) void k_asks(const float* __restrict__ hidden, 
   if (tid == 0) S[(size_t)i * B + j] = acc;
 }
 
+// Alg. AsksGate against the root: sigma_b = sum_l w_l <h_b^l / |h_b^l|, r^l>
+// with the root rows r^l stored unit-normalised (Eq. prefix_fwd; they are not
+// normalised again), shared[b] = sigma_b >= tau. One workgroup per branch; a
+// zero branch row contributes 0.
+__global__ __launch_bounds__(256) void k_asks_gate(const float* __restrict__ hidden, const float* __restrict__ root,
+                                                   int L, int B, int d, float alpha, float tau,
+                                                   float* __restrict__ sigma, int* __restrict__ shared) {
+  __shared__ float red[2][4];
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const double a = (double)alpha;
+  const double top = a >= 0.0 ? a : a / (double)L;
+  double wsum = 0.0;
+  for (int l = 1; l <= L; ++l) wsum += exp(a * (double)l / (double)L - top);
+  float acc = 0.f;
+  for (int l = 0; l < L; ++l) {
+    const float* hb = hidden + ((size_t)l * B + b) * d;
+    const float* r = root + (size_t)l * d;
+    float dot = 0.f, nb = 0.f;
+    for (int k = tid; k < d; k += 256) {
+      const float x = hb[k];
+      dot = fmaf(x, r[k], dot);
+      nb = fmaf(x, x, nb);
+    }
+    dot = wave_sum(dot);
+    nb = wave_sum(nb);
+    if (lane == 0) {
+      red[0][wid] = dot;
+      red[1][wid] = nb;
+    }
+    __syncthreads();
+    dot = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    nb = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    __syncthreads();
+    const float cosv = nb > 0.f ? dot / sqrtf(nb) : 0.f;
+    const float w = (float)(exp(a * (double)(l + 1) / (double)L - top) / wsum);
+    acc = fmaf(w, cosv, acc);
+  }
+  if (tid == 0) {
+    sigma[b] = acc;
+    shared[b] = acc >= tau ? 1 : 0;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_asks(const float* hidden, int L, int B, int d, float alpha, float* S, hipStream_t st) {
   hipLaunchKernelGGL(k_asks, dim3(B, B), dim3(256), 0, st, hidden, L, B, d, alpha, S);
+  return hipGetLastError();
+}
+
+hipError_t launch_asks_gate(const float* hidden, const float* root, int L, int B, int d, float alpha, float tau,
+                            float* sigma, int* shared, hipStream_t st) {
+  hipLaunchKernelGGL(k_asks_gate, dim3(B), dim3(256), 0, st, hidden, root, L, B, d, alpha, tau, sigma, shared);
   return hipGetLastError();
 }
 

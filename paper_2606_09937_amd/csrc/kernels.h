@@ -125,5 +125,8 @@ hipError_t launch_unit_rows(float* x, int rows, int d, hipStream_t st);
 
 // ---- ASKS similarity
 hipError_t launch_asks(const float* hidden, int L, int B, int d, float alpha, float* S, hipStream_t st);
+// Alg. AsksGate against unit root rows: sigma [B], shared [B] = sigma >= tau.
+hipError_t launch_asks_gate(const float* hidden, const float* root, int L, int B, int d, float alpha, float tau,
+                            float* sigma, int* shared, hipStream_t st);
 
 }  // namespace rksc

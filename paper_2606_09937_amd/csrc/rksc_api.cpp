@@ -426,46 +426,45 @@ RKSC_EXPORT size_t rksc_decode_workspace_size(const rksc_model_config* cfg, int3
 
 namespace {
 
-// Batched decode over the shared prefix (Sec. 2.2, "KV broadcast and batched
-// decode"; the stepwise loop of the implementation notes): s tokens per branch
-// at positions n + len .. n + len + s - 1 through all L layers, each attending
-// to the prefix cache, to the branch's cached entries 0..len-1 and, causally, to
-// its own new tokens, whose keys and values are appended to the branch cache.
-// After the last layer the last token's logits give the next token (argmax)
-// and its top-1 probability, summed into conf for Eq. gen_conf. `step` selects
-// the one-token kernels (s = 1, any len); otherwise len must be 0.
-rksc_status decode_impl(const rksc_weights* w, const rksc_prefix_kv* kv, rksc_branch_kv* bkv, const int32_t* tokens,
-                        int32_t n_branches, int32_t s, bool step, int32_t* next_token, float* p_top, float* conf,
+// Outputs of a branch pass; NULL members are not produced.
+struct PassOut {
+  int32_t* next_token;   // with p_top and conf: the last token's argmax and top-1 probability
+  float* p_top;
+  float* conf;
+  float* h_out;          // [L, B, d]: every layer's output row of each branch's last token
+};
+
+// One pass of B branches of s tokens through all L layers (Sec. 2.2, "KV
+// broadcast and batched decode"): the tokens sit at positions
+// n + pos .. n + pos + s - 1, attend to the prefix cache `kv` and causally to
+// each other, and their keys and values are written as entries off..off+s-1 of
+// the per-branch cache layers ck/cv [L][B, Hkv, cap, hd]. `step` (s = 1, a
+// decode step, pos = off) also attends to the cached entries 0..off-1;
+// otherwise those entries are not read (a tree node's cache holds its parent's
+// n entries first: off = n, pos = 0). With out.next_token, the last token's logits give the
+// next token and its top-1 probability, summed into conf for Eq. gen_conf
+// (set when off == 0 and not a step, else accumulated).
+rksc_status branch_pass(const rksc_weights* w, const rksc_prefix_kv* kv, void* ck, void* cv, int cap, int off,
+                        int pos, const int32_t* tokens, int32_t n_branches, int32_t s, bool step, const PassOut& out,
                         void* workspace, size_t workspace_bytes, void* stream) {
   if (!w) return fail(RKSC_ERR_INVALID_ARGUMENT, "weights is NULL");
   if (!kv) return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix_kv is NULL");
-  if (!bkv) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_kv is NULL");
-  if (!bkv->k || !bkv->v) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_kv k/v are NULL");
   if (!tokens) return fail(RKSC_ERR_INVALID_ARGUMENT, "tokens is NULL");
-  if (!next_token || !p_top || !conf)
-    return fail(RKSC_ERR_INVALID_ARGUMENT, "next_token, p_top and conf must not be NULL");
   if (!workspace) return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) % 256)
     return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
   if (kv->n_prefix < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", kv->n_prefix);
   if (kv->n_prefix > 0 && (!kv->k || !kv->v))
     return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix k/v are NULL with n_prefix = %d", kv->n_prefix);
-  if (bkv->length < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_kv length must be >= 0 (got %d)", bkv->length);
-  if (!step && bkv->length != 0)
-    return fail(RKSC_ERR_INVALID_ARGUMENT, "the suffix needs an empty branch cache (length %d)", bkv->length);
   if (s < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "suffix_len must be >= 1 (got %d)", s);
-  if ((long long)bkv->length + s > bkv->capacity)
-    return fail(RKSC_ERR_INVALID_ARGUMENT, "branch cache full: length %d + %d > capacity %d", bkv->length, s,
-                bkv->capacity);
-  if ((long long)kv->n_prefix + bkv->length + s > (1LL << 30))
-    return fail(RKSC_ERR_UNSUPPORTED, "positions above 2^30");
+  if ((long long)kv->n_prefix + pos + s > (1LL << 30)) return fail(RKSC_ERR_UNSUPPORTED, "positions above 2^30");
   const rksc_model_config* c = &w->cfg;
   Layout lay;
   rksc_status st = make_layout(c, n_branches, s, kv->n_prefix, &lay);
   if (st != RKSC_OK) return st;
   if (workspace_bytes < lay.total)
     return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
-  if (!w->embed || !w->final_norm || !w->lm_head || !w->layers)
+  if (!w->embed || !w->final_norm || !w->layers || (out.next_token && !w->lm_head))
     return fail(RKSC_ERR_INVALID_ARGUMENT, "embed, final_norm, lm_head and layers must not be NULL");
   for (int l = 0; l < c->n_layers; ++l) {
     const rksc_layer_weights& lw = w->layers[l];
@@ -476,7 +475,7 @@ rksc_status decode_impl(const rksc_weights* w, const rksc_prefix_kv* kv, rksc_br
   const DType dt = c->dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
   const size_t T = dt == DType::BF16 ? 2 : 4;
   const int L = c->n_layers, d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, hd = c->head_dim;
-  const int F = c->d_ff, V = c->vocab, B = n_branches, n = kv->n_prefix, len = bkv->length, cap = bkv->capacity;
+  const int F = c->d_ff, V = c->vocab, B = n_branches, n = kv->n_prefix, len = off;
   const int M = lay.max_rows;
   const int Nqkv = (H + 2 * Hkv) * hd;
   hipStream_t strm = static_cast<hipStream_t>(stream);
@@ -502,8 +501,8 @@ rksc_status decode_impl(const rksc_weights* w, const rksc_prefix_kv* kv, rksc_br
     return dt == DType::BF16 ? static_cast<const void*>(reinterpret_cast<const uint16_t*>(buf) + elems) : nullptr;
   };
 
-  HIP_TRY(rksc::launch_init(ctrl, B, L, nullptr, nullptr, nullptr, 0, strm));
-  HIP_TRY(rksc::launch_rope_table(rope, s, n + len, hd, (double)c->rope_base, strm));
+  HIP_TRY(rksc::launch_init(ctrl, B, L, nullptr, nullptr, out.h_out, (size_t)L * B * d, strm));
+  HIP_TRY(rksc::launch_rope_table(rope, s, n + pos, hd, (double)c->rope_base, strm));
   HIP_TRY(rksc::launch_embed(dt, w->embed, tokens, V, x0, M, d, strm));
   const char* pk_base = static_cast<const char*>(kv->k);
   const char* pv_base = static_cast<const char*>(kv->v);
@@ -515,8 +514,8 @@ rksc_status decode_impl(const rksc_weights* w, const rksc_prefix_kv* kv, rksc_br
                                   x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
                               s, M, Nqkv, d, strm));
-    char* bk = static_cast<char*>(bkv->k) + l * bkv_layer;
-    char* bv = static_cast<char*>(bkv->v) + l * bkv_layer;
+    char* bk = static_cast<char*>(ck) + l * bkv_layer;
+    char* bv = static_cast<char*>(cv) + l * bkv_layer;
     HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
                                   vown, M, strm, dt, bk, bv, cap, len));
     const void* pk = n > 0 ? pk_base + l * kv_layer : nullptr;
@@ -536,14 +535,36 @@ rksc_status decode_impl(const rksc_weights* w, const rksc_prefix_kv* kv, rksc_br
     HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
                               M, d, F, strm));
+    if (out.h_out || (out.next_token && l == L - 1))
+      HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, B, l, out.h_out,
+                               w->final_norm, c->rms_eps, ws + lay.hn_a, ws + lay.hn_b, B, strm));
   }
-  float* x_last = (L % 2 == 1) ? x1 : x0;
-  HIP_TRY(rksc::launch_tap(dt, x_last, pres, lay.down.splits, res_stride, ctrl, s, d, B, L - 1, nullptr,
-                           w->final_norm, c->rms_eps, ws + lay.hn_a, ws + lay.hn_b, B, strm));
-  HIP_TRY(rksc::launch_entropy_argmax(dt, w->lm_head, ws + lay.hn_a, ws + lay.hn_b, ctrl, V, d, B, parts, strm));
-  HIP_TRY(rksc::launch_finalize_decode(parts, lay.nparts, B, next_token, p_top, conf, step ? 1 : 0, strm));
-  bkv->length = len + s;
+  if (out.next_token) {
+    HIP_TRY(rksc::launch_entropy_argmax(dt, w->lm_head, ws + lay.hn_a, ws + lay.hn_b, ctrl, V, d, B, parts, strm));
+    HIP_TRY(rksc::launch_finalize_decode(parts, lay.nparts, B, out.next_token, out.p_top, out.conf,
+                                         step || off > 0 ? 1 : 0, strm));
+  }
   return ok();
+}
+
+rksc_status decode_impl(const rksc_weights* w, const rksc_prefix_kv* kv, rksc_branch_kv* bkv, const int32_t* tokens,
+                        int32_t n_branches, int32_t s, bool step, int32_t* next_token, float* p_top, float* conf,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  if (!bkv) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_kv is NULL");
+  if (!bkv->k || !bkv->v) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_kv k/v are NULL");
+  if (!next_token || !p_top || !conf)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "next_token, p_top and conf must not be NULL");
+  if (bkv->length < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_kv length must be >= 0 (got %d)", bkv->length);
+  if (!step && bkv->length != 0)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "the suffix needs an empty branch cache (length %d)", bkv->length);
+  if (s >= 1 && (long long)bkv->length + s > bkv->capacity)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "branch cache full: length %d + %d > capacity %d", bkv->length, s,
+                bkv->capacity);
+  const rksc_status st = branch_pass(w, kv, bkv->k, bkv->v, bkv->capacity, bkv->length, bkv->length, tokens,
+                                     n_branches, s, step,
+                                     PassOut{next_token, p_top, conf, nullptr}, workspace, workspace_bytes, stream);
+  if (st == RKSC_OK) bkv->length += s;
+  return st;
 }
 
 }  // namespace
@@ -561,6 +582,94 @@ RKSC_EXPORT rksc_status rksc_decode_step(const rksc_weights* w, const rksc_prefi
                                          float* conf, void* workspace, size_t workspace_bytes, void* stream) {
   return decode_impl(w, kv, branch_kv, tokens, n_branches, 1, true, next_token, p_top, conf, workspace,
                      workspace_bytes, stream);
+}
+
+RKSC_EXPORT size_t rksc_prefix_extend_workspace_size(const rksc_model_config* cfg, int32_t n_parent,
+                                                    int32_t n_new) {
+  if (n_parent < 0) {
+    fail(RKSC_ERR_INVALID_ARGUMENT, "n_parent must be >= 0 (got %d)", n_parent);
+    return 0;
+  }
+  Layout lay;
+  if (make_layout(cfg, 1, n_new, n_parent, &lay) != RKSC_OK) return 0;
+  return lay.total;
+}
+
+// Tree sharing (a node's tokens on top of its parent's cache): the child cache
+// holds the parent's n entries followed by the m new tokens' entries, computed
+// once over the parent cache and shared by every child of the node.
+RKSC_EXPORT rksc_status rksc_prefix_extend(const rksc_weights* w, const rksc_prefix_kv* parent, const int32_t* tokens,
+                                           int32_t n_new, void* k_out, void* v_out, float* h_node, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+  if (!w) return fail(RKSC_ERR_INVALID_ARGUMENT, "weights is NULL");
+  if (!parent) return fail(RKSC_ERR_INVALID_ARGUMENT, "parent is NULL");
+  if (!k_out || !v_out) return fail(RKSC_ERR_INVALID_ARGUMENT, "k_out and v_out must not be NULL");
+  if (n_new < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_new must be >= 1 (got %d)", n_new);
+  const rksc_model_config* c = &w->cfg;
+  rksc_status st = check_config(c);
+  if (st != RKSC_OK) return st;
+  const int n = parent->n_prefix;
+  if (n < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", n);
+  if ((long long)n + n_new > (1 << 30)) return fail(RKSC_ERR_UNSUPPORTED, "positions above 2^30");
+  const size_t T = c->dtype == RKSC_BF16 ? 2 : 4;
+  const size_t row_new = (size_t)(n + n_new) * c->head_dim * T, row_old = (size_t)n * c->head_dim * T;
+  const size_t rows = (size_t)c->n_layers * c->n_kv_heads;
+  // The parent cache must not overlap the child cache (the copy reads it while rows are written).
+  if (n > 0 && parent->k && parent->v) {
+    auto overlap = [&](const void* a, size_t na, const void* b, size_t nb) {
+      const char *pa = static_cast<const char*>(a), *pb = static_cast<const char*>(b);
+      return pa < pb + nb && pb < pa + na;
+    };
+    const size_t child = rows * row_new, par = rows * row_old;
+    if (overlap(parent->k, par, k_out, child) || overlap(parent->v, par, v_out, child) ||
+        overlap(parent->k, par, v_out, child) || overlap(parent->v, par, k_out, child))
+      return fail(RKSC_ERR_INVALID_ARGUMENT, "the parent cache overlaps the child cache");
+  }
+  // Validate the pass before copying anything.
+  Layout lay;
+  st = make_layout(c, 1, n_new, n, &lay);
+  if (st != RKSC_OK) return st;
+  if (workspace && workspace_bytes < lay.total)
+    return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
+  if (n > 0 && (!parent->k || !parent->v))
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "parent k/v are NULL with n_prefix = %d", n);
+  if (!tokens) return fail(RKSC_ERR_INVALID_ARGUMENT, "tokens is NULL");
+  if (!workspace) return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  if (!w->embed || !w->final_norm || !w->layers)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "embed, final_norm and layers must not be NULL");
+  for (int l = 0; l < c->n_layers; ++l) {
+    const rksc_layer_weights& lw = w->layers[l];
+    if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
+      return fail(RKSC_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
+  }
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  if (n > 0) {
+    HIP_TRY(hipMemcpy2DAsync(k_out, row_new, parent->k, row_old, row_old, rows, hipMemcpyDeviceToDevice, strm));
+    HIP_TRY(hipMemcpy2DAsync(v_out, row_new, parent->v, row_old, row_old, rows, hipMemcpyDeviceToDevice, strm));
+  }
+  st = branch_pass(w, parent, k_out, v_out, n + n_new, n, 0, tokens, 1, n_new, false,
+                   PassOut{nullptr, nullptr, nullptr, h_node}, workspace, workspace_bytes, stream);
+  if (st != RKSC_OK) return st;
+  if (h_node) HIP_TRY(rksc::launch_unit_rows(h_node, c->n_layers, c->d_model, strm));
+  return ok();
+}
+
+RKSC_EXPORT rksc_status rksc_asks_gate(const float* hidden, const float* h_root, int32_t n_layers, int32_t n_branches,
+                                       int32_t d_model, float alpha, float tau, float* sigma, int32_t* shared,
+                                       void* stream) {
+  if (!hidden || !h_root || !sigma || !shared)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "hidden, h_root, sigma and shared must not be NULL");
+  if (n_layers < 1 || n_branches < 1 || d_model < 1)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "L, B and d must be >= 1 (got %d, %d, %d)", n_layers, n_branches,
+                d_model);
+  if (n_branches > 65535) return fail(RKSC_ERR_UNSUPPORTED, "n_branches above 65535 (got %d)", n_branches);
+  if (!std::isfinite(alpha)) return fail(RKSC_ERR_INVALID_ARGUMENT, "alpha must be finite");
+  if (std::isnan(tau)) return fail(RKSC_ERR_INVALID_ARGUMENT, "tau must not be NaN");
+  HIP_TRY(rksc::launch_asks_gate(hidden, h_root, n_layers, n_branches, d_model, alpha, tau, sigma, shared,
+                                 static_cast<hipStream_t>(stream)));
+  return ok();
 }
 
 RKSC_EXPORT rksc_status rksc_cgee_gate(const float* conf, int32_t n_branches, int32_t n_steps, float tau_conf,

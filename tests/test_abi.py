@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
     assert "rksc_verify_forward" in names and "rksc_asks_similarity" in names
     for name in names:
         assert hasattr(lib, name), f"{name} declared in include/ but not exported"
-    assert rk.rksc_abi_version() == 4
+    assert rk.rksc_abi_version() == 5
 
 
 def test_status_strings(lib):
@@ -242,3 +242,39 @@ def test_cgee_gate_rejects_bad_arguments(lib):
     assert lib.rksc_cgee_gate(FAKE, 4, 0, 0.7, 0.06, None, FAKE, FAKE, None, None) == I
     assert lib.rksc_cgee_gate(FAKE, 4, 3, math.nan, 0.06, None, FAKE, FAKE, None, None) == I
     assert lib.rksc_cgee_gate(FAKE, 4, 3, 0.7, math.nan, None, FAKE, FAKE, None, None) == I
+
+
+def test_prefix_extend_and_asks_gate_reject_bad_arguments(lib):
+    shape = workloads.get("tiny").model
+    w, _keep, cfg = _fake_weights(shape)
+    assert lib.rksc_prefix_extend_workspace_size(ctypes.byref(cfg), -1, 4) == 0
+    assert lib.rksc_prefix_extend_workspace_size(ctypes.byref(cfg), 8, 0) == 0
+    ws = lib.rksc_prefix_extend_workspace_size(ctypes.byref(cfg), 8, 4)
+    assert ws > 0
+    ok_ws = ctypes.c_void_p(0x100000)
+    I = rk.RKSC_ERR_INVALID_ARGUMENT
+    par = rk.PrefixKV(8, ctypes.c_void_p(0x2000000), ctypes.c_void_p(0x3000000))
+
+    def ext(parent=par, tokens=FAKE, m=4, k=ctypes.c_void_p(0x5000000), v=ctypes.c_void_p(0x6000000), wsp=ok_ws,
+            wsb=ws):
+        return lib.rksc_prefix_extend(ctypes.byref(w), ctypes.byref(parent) if parent else None, tokens, m, k, v,
+                                      None, wsp, wsb, None)
+
+    assert ext(parent=None) == I
+    assert ext(tokens=None) == I
+    assert ext(m=0) == I
+    assert ext(k=None) == I
+    assert ext(wsp=None) == I
+    assert ext(wsp=ctypes.c_void_p(0x100010)) == I
+    assert ext(wsb=ws - 1) == rk.RKSC_ERR_WORKSPACE_TOO_SMALL
+    assert ext(parent=rk.PrefixKV(8, None, FAKE)) == I
+    assert ext(parent=rk.PrefixKV(-1, FAKE, FAKE)) == I
+    # the child cache may not overlap the parent's
+    assert ext(k=ctypes.c_void_p(0x2000000 + 64)) == I
+    assert "overlap" in rk.rksc_last_error()
+    G = lib.rksc_asks_gate
+    assert G(None, FAKE, 2, 4, 8, 1.5, 0.8, FAKE, FAKE, None) == I
+    assert G(FAKE, FAKE, 2, 4, 8, 1.5, 0.8, FAKE, None, None) == I
+    assert G(FAKE, FAKE, 0, 4, 8, 1.5, 0.8, FAKE, FAKE, None) == I
+    assert G(FAKE, FAKE, 2, 4, 8, math.inf, 0.8, FAKE, FAKE, None) == I
+    assert G(FAKE, FAKE, 2, 4, 8, 1.5, math.nan, FAKE, FAKE, None) == I
