@@ -26,6 +26,9 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   kv_probe     the library's KV probe at 8 branches over the same prefix: the
                batched full recompute, the root forward and the batched suffix
                decode over the shared cache (min of 3 each), and its verdict
+  tree         a 64-token search-tree node built once over the prefix cache
+               (rksc_prefix_extend) against 8 children recomputing it, and the
+               device ASKS gate over 8 branches
   cpu_baseline the float64 CPU oracle on a bounded sample of the workload
 
     python bench.py [--steps K] [--warmup W] [--workload 7b_single]
@@ -129,6 +132,7 @@ KERNEL_NAMES = {"lm_head_entropy": "k_entropy_bf16", "attention": "k_attn_bf16",
 # The decode measurement: the paper's B = 8 branches and t = 32 decode steps of
 # its throughput table, after a 32-token suffix per branch.
 DECODE_BRANCHES, DECODE_SUFFIX, DECODE_TOKENS = 8, 32, 32
+TREE_NODE = 64   # tokens of a search-tree node (one reasoning step) in the tree-sharing measurement
 COPY_BYTES = 1 << 29   # calibration copy: 512 MiB read + 512 MiB written
 
 
@@ -365,6 +369,57 @@ def measure_kv_probe(mw, shape, n, args, stream, dev):
     return out
 
 
+def measure_tree(mw, kv, shape, n, args, hip, sp, stream, dev):
+    """Tree sharing and the ASKS gate at the workload's prefix: one search-tree node
+    of TREE_NODE tokens built once over the root cache (rksc_prefix_extend), against
+    its DECODE_BRANCHES children each recomputing the node's tokens over the root cache
+    (one batched suffix pass); and the device ASKS gate over DECODE_BRANCHES rows."""
+    import torch
+
+    import paper_2606_09937_amd as rk
+    import workloads
+
+    m, Bd = TREE_NODE, DECODE_BRANCHES
+    L = shape.n_layers
+    node = workloads.make_tokens(m, shape.vocab, seed=args.seed, name="node", device=dev)
+    dtype = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    ws = torch.empty(rk.rksc_prefix_extend_workspace_size(shape, n, m), dtype=torch.uint8, device=dev)
+    ck = torch.empty((L, shape.n_kv_heads, n + m, shape.head_dim), dtype=dtype, device=dev)
+    cv = torch.empty_like(ck)
+    hn = torch.empty((L, shape.d_model), dtype=torch.float32, device=dev)
+    dec = rk.Decoder(mw, kv.k, kv.v, Bd, m, capacity=m, device=dev)
+    rows = node.repeat(Bd, 1).contiguous()
+
+    def timed(fn, reps=3):
+        fn()
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(reps):
+            a, b = hip.create(2)
+            hip.lib.hipEventRecord(ctypes.c_void_p(a), sp)
+            fn()
+            hip.lib.hipEventRecord(ctypes.c_void_p(b), sp)
+            torch.cuda.synchronize()
+            best = min(best, hip.elapsed_ms(a, b))
+            hip.destroy([a, b])
+        return best
+
+    def unshared():
+        dec.cache.struct.length = 0
+        dec.suffix(rows, stream)
+
+    t_ext = timed(lambda: rk.rksc_prefix_extend(mw, kv.k, kv.v, node, ck, cv, hn, ws, stream))
+    t_all = timed(unshared)
+    hid = workloads.make_hidden(L, Bd, shape.d_model, seed=args.seed, device=dev)
+    t_gate = timed(lambda: rk.asks_gate(hid, hn, 1.5, 0.82, stream))
+    out = {"parent_len": n, "node_tokens": m, "children": Bd, "extend_ms": t_ext,
+           "children_recompute_ms": t_all, "asks_gate_us": t_gate * 1e3}
+    log(f"tree: node of {m} tokens over {n}: extend {t_ext:.2f} ms once vs {t_all:.2f} ms for {Bd} children "
+        f"recomputing it; ASKS gate {t_gate * 1e3:.1f} us")
+    del dec, ws, ck, cv
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -382,6 +437,7 @@ def main():
     ap.add_argument("--no-prefill", action="store_true", help="skip the root-forward (prefill) timing")
     ap.add_argument("--no-decode", action="store_true", help="skip the batched-decode timing")
     ap.add_argument("--no-probe", action="store_true", help="skip the KV probe timing")
+    ap.add_argument("--no-tree", action="store_true", help="skip the tree-sharing and ASKS-gate timing")
     ap.add_argument("--decode-only", action="store_true",
                     help="time only the batched decode (for a kernel trace of it) and print its JSON")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -632,6 +688,7 @@ def main():
 
     decode = None if args.no_decode else measure_decode(mw, kv, shape, n, args, hip, sp, stream, dev)
     kv_probe = None if args.no_probe else measure_kv_probe(mw, shape, n, args, stream, dev)
+    tree = None if args.no_tree else measure_tree(mw, kv, shape, n, args, hip, sp, stream, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -670,6 +727,7 @@ def main():
         "prefill": prefill,
         "decode": decode,
         "kv_probe": kv_probe,
+        "tree": tree,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
