@@ -3,17 +3,18 @@
 
 One step = one rksc_verify_forward call over the whole workload: every layer of
 the multi-branch forward over the shared prefix cache, the fused
-lm_head-entropy probe after every layer and the exit rule (branches that exit
-stop being computed). Inputs (random-init bf16 weights, synthetic prefix K/V,
+lm_head-entropy probe of every layer (one stream per exit window of layers)
+and the exit rule (branches that exit stop being computed). Inputs (random-init bf16 weights, synthetic prefix K/V,
 uniform tokens) are generated on the GPU and are resident in HBM before the
 timed region; the workspace and outputs are allocated once.
 
 Prints ONE JSON line on stdout (progress goes to stderr):
   value        verify tokens/s = n_branches * branch_len / step time
-  roofline     the dominant kernel (fused lm_head-entropy at the default
-               workload) against the HBM peak, timed with HIP events recorded
-               around its launches inside the timed steps (the only events in
-               that region: every recorded event opens a gap in the stream)
+  roofline     the dominant kernel class (most time per call; the gate|up
+               projection at the default workload) against its roof, timed
+               with HIP events recorded around its launches inside the timed
+               steps (the only events in that region: every recorded event
+               opens a gap in the stream)
   kernels      every kernel class timed the same way in a separate breakdown
                pass before the timed region ("pass" says which)
   exit_histogram, live_layer_fraction   exit layers of the timed calls
@@ -95,8 +96,9 @@ class HipEvents:
             self.lib.hipEventDestroy(ctypes.c_void_p(e))
 
 
-def kernel_work(shape, B_live, n, s):
-    """Algorithmic bytes and flops per launch of each timed kernel class at B_live live branches."""
+def kernel_work(shape, B_live, n, s, win=1):
+    """Algorithmic bytes and flops per launch of each timed kernel class at B_live live branches
+    (the lm_head stream serves an exit window of `win` layers: B_live * win columns)."""
     d, H, Hkv, hd, F, V = shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.d_ff, shape.vocab
     T = 2 if shape.dtype == "bf16" else 4
     M = B_live * s
@@ -112,7 +114,7 @@ def kernel_work(shape, B_live, n, s):
         "qkv_proj": gemm(Nqkv, d), "o_proj": gemm(d, H * hd), "gate_up_proj": gemm(2 * F, d),
         "down_proj": gemm(d, F), "attention": {"bytes": attn_bytes, "flops": attn_flops},
         # W_lm once, the hi+lo bf16 normalised rows, the per-workgroup statistics
-        "lm_head_entropy": {"bytes": V * d * T + B_live * d * 4, "flops": 2.0 * B_live * V * d},
+        "lm_head_entropy": {"bytes": V * d * T + B_live * win * d * 4, "flops": 2.0 * B_live * win * V * d},
     }
 
 
@@ -127,8 +129,9 @@ KERNEL_SOURCES = {
     "attention": ["k_attn.hip", "common.h"],
 }
 # Name fragments of the device kernels behind each class in rocprofv3 output.
-KERNEL_NAMES = {"lm_head_entropy": "k_entropy_bf16", "attention": "k_attn_bf16", "qkv_proj": "k_gemm_dma",
-                "o_proj": "k_gemm_dma", "gate_up_proj": "k_gemm_dma", "down_proj": "k_gemm_dma"}
+# At 7b_single: QKV uses 192-column tiles, gate|up 256, O and down 128.
+KERNEL_NAMES = {"lm_head_entropy": "k_entropy_bf16", "attention": "k_attn_bf16", "qkv_proj": "k_gemm_dmaILi192",
+                "o_proj": "k_gemm_dmaILi128", "gate_up_proj": "k_gemm_dmaILi256", "down_proj": "k_gemm_dmaILi128"}
 # The decode measurement: the paper's B = 8 branches and t = 32 decode steps of
 # its throughput table, after a 32-token suffix per branch.
 DECODE_BRANCHES, DECODE_SUFFIX, DECODE_TOKENS = 8, 32, 32
@@ -539,14 +542,22 @@ def main():
             arr = (ctypes.c_void_p * per_step)()
             for l in range(L):
                 for sl in slots:
+                    if sl in (EVENT_SLOTS["lm_head_entropy"], EVENT_SLOTS["lm_head_entropy"] + 1) and \
+                            l not in stream_layers:
+                        continue   # no stream at this layer: the library records nothing there
                     arr[12 * l + sl] = evs[k * per_step + 12 * l + sl]
             arrays.append(arr)
         ptrs = [ctypes.cast(a, ctypes.c_void_p) for a in arrays]
         return evs, ptrs
 
+    # The probe's lm_head stream runs once per exit window, at the window's last layer.
+    win = rk.rksc_verify_window(B)
+    stream_layers = [l for l in range(L) if l % win == win - 1 or l == L - 1]
+
     def durations(evs, k_steps, slot, layers):
+        ls = [l for l in stream_layers if l < layers] if slot == EVENT_SLOTS["lm_head_entropy"] else range(layers)
         return [hip.elapsed_ms(evs[k * per_step + 12 * l + slot], evs[k * per_step + 12 * l + slot + 1])
-                for k in range(k_steps) for l in range(layers)]
+                for k in range(k_steps) for l in ls]
 
     # 1) Breakdown pass (untimed): events around every kernel class. Each recorded
     #    event opens a few-microsecond gap in the stream, so these steps are not
@@ -565,9 +576,15 @@ def main():
     hip.destroy(evs_b)
     live_per_layer = [sum(1 for e in exits if e >= l + 1) for l in range(L)]
     mean_live = sum(live_per_layer[:live_layers]) / live_layers
-    work = kernel_work(shape, max(1, round(mean_live)), n, s)
-    shares = {k: v["avg_us"] for k, v in kernels.items()}
-    dom = "lm_head_entropy" if shares["lm_head_entropy"] >= max(shares.values()) * 0.999 else max(shares, key=shares.get)
+    work = kernel_work(shape, max(1, round(mean_live)), n, s, win)
+    # Dominant class: the most time per call (per-launch time x launches per call).
+    launches = {k: (len([l for l in stream_layers if l < live_layers]) if k == "lm_head_entropy" else live_layers)
+                for k in kernels}
+    shares = {k: v["avg_us"] * launches[k] for k, v in kernels.items()}
+    for k, v in kernels.items():
+        v["launches_per_call"] = launches[k]
+        v["us_per_call"] = shares[k]
+    dom = max(shares, key=shares.get)
 
     # 2) Timed region: K calls, events only around the dominant kernel class.
     evs_t, ptrs_t = profiled_steps(args.steps, [EVENT_SLOTS[dom], EVENT_SLOTS[dom] + 1])

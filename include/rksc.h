@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define RKSC_ABI_VERSION 5
+#define RKSC_ABI_VERSION 6
 
 /* Largest number of branches one verify call accepts. */
 #define RKSC_MAX_BRANCHES 64
@@ -142,12 +142,32 @@ size_t rksc_verify_workspace_size(const rksc_model_config* cfg, int32_t n_branch
  *                branch's last token (before the final norm), NaN rows after exit.
  * workspace      device buffer of at least rksc_verify_workspace_size() bytes,
  *                256-byte aligned; its contents on entry do not matter.
+ *
+ * Schedule: the probe's lm_head stream is shared by an exit window of
+ * rksc_verify_window(B) consecutive layers (their rows are extra columns of
+ * one read of W_lm). The rule still runs layer by layer, at the window's end;
+ * a branch that exits inside a window has its later layers of that window
+ * computed and discarded (NaN in the outputs), so every output equals that of
+ * a layer-by-layer schedule.
  */
 rksc_status rksc_verify_forward(const rksc_weights* weights, const rksc_prefix_kv* prefix_kv,
                                 const int32_t* branch_tokens, int32_t n_branches,
                                 int32_t branch_len, float tau, int32_t patience,
                                 float* entropy, int32_t* exit_layer, float* hidden_last,
                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* The exit window rksc_verify_forward uses for n_branches branches: 4 up to 8
+ * branches, 2 up to 16, else 1. */
+int32_t rksc_verify_window(int32_t n_branches);
+
+/* rksc_verify_forward with the exit window chosen by the caller: window = 1 is
+ * the layer-by-layer schedule (a branch stops at its exit layer); window in
+ * [1, 8] with window * n_branches <= 64. Outputs do not depend on it. */
+rksc_status rksc_verify_forward_window(const rksc_weights* weights, const rksc_prefix_kv* prefix_kv,
+                                       const int32_t* branch_tokens, int32_t n_branches, int32_t branch_len,
+                                       float tau, int32_t patience, float* entropy, int32_t* exit_layer,
+                                       float* hidden_last, void* workspace, size_t workspace_bytes, void* stream,
+                                       int32_t window);
 
 /* Bytes of workspace rksc_prefill needs for an n_prefix-token prefix; 0 if the
  * shape is invalid (rksc_last_error() says why). */

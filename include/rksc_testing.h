@@ -61,8 +61,9 @@ rksc_status rksc_test_attention(int32_t dtype, const void* q, const void* prefix
  * l * RKSC_PROFILE_EVENTS_PER_LAYER + k are, for k =
  *   0/1 QKV projection, 2/3 attention, 4/5 O projection, 6/7 gate|up
  *   projection, 8/9 down projection, 10/11 fused lm_head-entropy.
- * Events of layers a branch set never reaches are recorded too (their kernels
- * exit at once). */
+ * The lm_head-entropy events are recorded only at the last layer of each exit
+ * window (rksc_verify_window), where the stream runs. Events of layers a
+ * branch set never reaches are recorded too (their kernels exit at once). */
 #define RKSC_PROFILE_EVENTS_PER_LAYER 12
 rksc_status rksc_verify_forward_profiled(const rksc_weights* weights, const rksc_prefix_kv* prefix_kv,
                                          const int32_t* branch_tokens, int32_t n_branches, int32_t branch_len,

@@ -19,7 +19,7 @@ import torch
 
 __all__ = [
     "RkscError", "load_library", "library_path",
-    "rksc_abi_version", "rksc_verify_workspace_size", "rksc_verify_forward",
+    "rksc_abi_version", "rksc_verify_workspace_size", "rksc_verify_forward", "rksc_verify_window",
     "rksc_asks_similarity", "rksc_status_string", "rksc_last_error",
     "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_attention",
     "verify_forward", "asks_similarity", "prefill", "rksc_prefill", "rksc_prefill_workspace_size", "model_config",
@@ -38,7 +38,7 @@ RKSC_ERR_HIP = -4
 RKSC_F32 = 0
 RKSC_BF16 = 1
 RKSC_MAX_BRANCHES = 64
-RKSC_ABI_VERSION = 5
+RKSC_ABI_VERSION = 6
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 
@@ -107,6 +107,11 @@ def load_library():
     lib.rksc_verify_forward.restype = i32
     lib.rksc_verify_forward.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32, i32,
                                         vp, vp, vp, vp, sz, vp]
+    lib.rksc_verify_window.restype = i32
+    lib.rksc_verify_window.argtypes = [i32]
+    lib.rksc_verify_forward_window.restype = i32
+    lib.rksc_verify_forward_window.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32,
+                                               i32, vp, vp, vp, vp, sz, vp, i32]
     lib.rksc_prefill_workspace_size.restype = sz
     lib.rksc_prefill_workspace_size.argtypes = [ctypes.POINTER(ModelConfig), i32]
     lib.rksc_prefill.restype = i32
@@ -235,10 +240,15 @@ def _weights_struct(weights):
     return w, layers
 
 
+def rksc_verify_window(n_branches: int) -> int:
+    return int(load_library().rksc_verify_window(int(n_branches)))
+
+
 def rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, patience: int,
                         entropy: torch.Tensor, exit_layer: torch.Tensor, hidden_last: Optional[torch.Tensor],
-                        workspace: torch.Tensor, stream=None) -> None:
-    """Marshal torch device tensors into rksc_verify_forward (asynchronous on `stream`).
+                        workspace: torch.Tensor, stream=None, window: Optional[int] = None) -> None:
+    """Marshal torch device tensors into rksc_verify_forward (asynchronous on `stream`);
+    with `window`, into rksc_verify_forward_window.
 
     weights: object with .shape (decoder shape), .embed, .layers (dicts of tensors), .final_norm, .lm_head.
     prefix_k/prefix_v: [L, Hkv, n, hd] device tensors. branch_tokens: [B, s] int32 device.
@@ -248,10 +258,13 @@ def rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, 
     B, s = branch_tokens.shape
     n = int(prefix_k.shape[2]) if prefix_k is not None else 0
     kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
-    st = lib.rksc_verify_forward(ctypes.byref(w), ctypes.byref(kv), _ptr(branch_tokens), int(B), int(s),
-                                 float(tau), int(patience), _ptr(entropy), _ptr(exit_layer), _ptr(hidden_last),
-                                 _ptr(workspace), int(workspace.numel() * workspace.element_size()),
-                                 _stream(stream))
+    args = (ctypes.byref(w), ctypes.byref(kv), _ptr(branch_tokens), int(B), int(s), float(tau), int(patience),
+            _ptr(entropy), _ptr(exit_layer), _ptr(hidden_last), _ptr(workspace),
+            int(workspace.numel() * workspace.element_size()), _stream(stream))
+    if window is None:
+        st = lib.rksc_verify_forward(*args)
+    else:
+        st = lib.rksc_verify_forward_window(*args, int(window))
     del layers_keepalive
     _check(st)
 
@@ -329,7 +342,8 @@ def rksc_test_attention(q, prefix_k, prefix_v, k_own, v_own, dtype, stream=None)
 
 
 def verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, patience: int,
-                   return_hidden: bool = False, workspace: Optional[torch.Tensor] = None, stream=None):
+                   return_hidden: bool = False, workspace: Optional[torch.Tensor] = None, stream=None,
+                   window: Optional[int] = None):
     """Allocate outputs (and the workspace unless given) and run the verify pass.
 
     Returns (entropy [L, B] fp32, exit_layer [B] int32[, hidden_last [L, B, d] fp32]) on the device.
@@ -345,7 +359,7 @@ def verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, patie
     exit_layer = torch.empty((B,), dtype=torch.int32, device=dev)
     hidden = torch.empty((L, B, shape.d_model), dtype=torch.float32, device=dev) if return_hidden else None
     rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau, patience, entropy, exit_layer, hidden,
-                        workspace, stream)
+                        workspace, stream, window)
     return (entropy, exit_layer, hidden) if return_hidden else (entropy, exit_layer)
 
 

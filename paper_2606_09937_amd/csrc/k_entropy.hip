@@ -139,7 +139,7 @@ constexpr int kFinBytes = kEntWaves8 * 16 * 16;       // one triple (+ argmax) p
 template <int NCB, int G, int R, bool AM>
 __global__ __launch_bounds__(512) void k_entropy_bf16(const bf16* __restrict__ W, const bf16* __restrict__ hi,
                                                       const bf16* __restrict__ lo, const Ctrl* c, int V, int d,
-                                                      float* __restrict__ parts) {
+                                                      int kmul, float* __restrict__ parts) {
   constexpr int NW = kEntWaves8;
   constexpr int IPW = 16 / NW;        // DMA instructions per wave per unit
   constexpr int TPW = NW / (2 * NCB); // owner groups; unit i goes to group i % TPW
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(512) void k_entropy_bf16(const bf16* __restrict__ W
   static_assert(G % TPW == 0 && LT % kEntRedTiles == 0, "tile group must split over the waves and rounds");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[R * kUnitBytes + kRedBytes + kFinBytes];
 
-  const int Bl = c->live_count;
+  const int Bl = c->live_count * kmul;   // columns: kmul layers' rows of every live branch
   if (Bl == 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
@@ -323,8 +323,9 @@ __global__ __launch_bounds__(512) void k_entropy_bf16(const bf16* __restrict__ W
 // fp32 models: each wave takes whole vocabulary rows, lanes stride over d.
 template <bool AM>
 __global__ __launch_bounds__(256) void k_entropy_f32(const float* __restrict__ W, const float* __restrict__ hn,
-                                                     const Ctrl* c, int V, int d, float* __restrict__ parts) {
-  const int Bl = c->live_count;
+                                                     const Ctrl* c, int V, int d, int kmul,
+                                                     float* __restrict__ parts) {
+  const int Bl = c->live_count * kmul;
   if (Bl == 0) return;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   // Branch column `col` is owned by lane `col` (at most 64 branches).
@@ -392,11 +393,11 @@ int entropy_parts(DType dt, int V, int max_branches) {
 namespace {
 template <bool AM>
 hipError_t launch_entropy_t(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c, int V,
-                            int d, int max_branches, float* parts, hipStream_t st) {
+                            int d, int max_branches, int kmul, float* parts, hipStream_t st) {
   const int blocks = entropy_parts(dt, V, max_branches);
   if (dt == DType::F32) {
     hipLaunchKernelGGL(k_entropy_f32<AM>, dim3(blocks), dim3(256), 0, st, static_cast<const float*>(W),
-                       static_cast<const float*>(hn_a), c, V, d, parts);
+                       static_cast<const float*>(hn_a), c, V, d, kmul, parts);
     return hipGetLastError();
   }
   const bf16* w = static_cast<const bf16*>(W);
@@ -405,15 +406,15 @@ hipError_t launch_entropy_t(DType dt, const void* W, const void* hn_a, const voi
   switch (ent_ncb(max_branches)) {
     case 1:
       hipLaunchKernelGGL((k_entropy_bf16<1, 32, kEntRing, AM>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d,
-                         parts);
+                         kmul, parts);
       break;
     case 2:
       hipLaunchKernelGGL((k_entropy_bf16<2, 32, kEntRing, AM>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d,
-                         parts);
+                         kmul, parts);
       break;
     default:
       hipLaunchKernelGGL((k_entropy_bf16<4, 16, kEntRing, AM>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d,
-                         parts);
+                         kmul, parts);
       break;
   }
   return hipGetLastError();
@@ -421,13 +422,13 @@ hipError_t launch_entropy_t(DType dt, const void* W, const void* hn_a, const voi
 }  // namespace
 
 hipError_t launch_entropy(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c, int V, int d,
-                          int max_branches, float* parts, hipStream_t st) {
-  return launch_entropy_t<false>(dt, W, hn_a, hn_b, c, V, d, max_branches, parts, st);
+                          int max_branches, float* parts, hipStream_t st, int kmul) {
+  return launch_entropy_t<false>(dt, W, hn_a, hn_b, c, V, d, max_branches * kmul, kmul, parts, st);
 }
 
 hipError_t launch_entropy_argmax(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c, int V,
                                  int d, int max_branches, float* parts, hipStream_t st) {
-  return launch_entropy_t<true>(dt, W, hn_a, hn_b, c, V, d, max_branches, parts, st);
+  return launch_entropy_t<true>(dt, W, hn_a, hn_b, c, V, d, max_branches, 1, parts, st);
 }
 
 }  // namespace rksc

@@ -224,10 +224,11 @@ template <bool kSplitBf16, int MAXC>
 __global__ __launch_bounds__(1024) void k_tap(const float* __restrict__ x, const float* __restrict__ P, int nsplit,
                                               size_t split_stride, const Ctrl* c, int s, int d, int B, int layer0,
                                               float* __restrict__ hidden_last, const float* __restrict__ gamma,
-                                              float eps, void* hn_a, void* hn_b) {
+                                              float eps, void* hn_a, void* hn_b, int jrow) {
   __shared__ float red[16];
   const int slot = blockIdx.x;
   if (slot >= c->live_count) return;
+  const size_t hrow = (size_t)jrow * c->live_count + slot;   // row of the normalised rows (layer jrow of a window)
   const int branch = c->live_idx[slot];
   const size_t row = (size_t)slot * s + (s - 1);
   float4 v[MAXC];
@@ -266,24 +267,32 @@ __global__ __launch_bounds__(1024) void k_tap(const float* __restrict__ x, const
       split2(h1, b1, l1);
       split2(h2, b2, l2);
       split2(h3, b3, l3);
-      *reinterpret_cast<uint2*>(static_cast<bf16*>(hn_a) + (size_t)slot * d + col) = make_uint2(pack2(b0, b1), pack2(b2, b3));
-      *reinterpret_cast<uint2*>(static_cast<bf16*>(hn_b) + (size_t)slot * d + col) = make_uint2(pack2(l0, l1), pack2(l2, l3));
+      *reinterpret_cast<uint2*>(static_cast<bf16*>(hn_a) + hrow * d + col) = make_uint2(pack2(b0, b1), pack2(b2, b3));
+      *reinterpret_cast<uint2*>(static_cast<bf16*>(hn_b) + hrow * d + col) = make_uint2(pack2(l0, l1), pack2(l2, l3));
     } else {
-      *reinterpret_cast<float4*>(static_cast<float*>(hn_a) + (size_t)slot * d + col) = make_float4(h0, h1, h2, h3);
+      *reinterpret_cast<float4*>(static_cast<float*>(hn_a) + hrow * d + col) = make_float4(h0, h1, h2, h3);
     }
   }
 }
 
 // ------------------------------------------------------------------ entropy merge + exit rule
 
-__global__ __launch_bounds__(256) void k_finalize_exit(const float* parts, int nparts, Ctrl* c, int layer1,
+// The exit rule over a window of kw layers layer1 .. layer1 + kw - 1 (1-based),
+// whose entropies were streamed together: column j * Bl + slot holds layer
+// layer1 + j of live slot `slot`. Each branch walks its layers in order; at an
+// exit the later layers of the window (computed on the same live set) are
+// discarded: their entropies stay NaN and their hidden rows are set back to
+// NaN, so the outputs are those of a layer-by-layer schedule. Then the live
+// list is compacted.
+__global__ __launch_bounds__(256) void k_finalize_exit(const float* parts, int nparts, Ctrl* c, int layer1, int kw,
                                                        int L, int B, float tau, int patience, float* entropy,
-                                                       int* exit_layer) {
+                                                       int* exit_layer, float* hidden_last, int d) {
   __shared__ EntStats red[256];
+  __shared__ int exit_j[64], branch_of[64];
   const int Bl = c->live_count;
   if (Bl == 0) return;
   const int tid = threadIdx.x;
-  for (int col = 0; col < Bl; ++col) {
+  for (int col = 0; col < Bl * kw; ++col) {
     EntStats st = ent_empty();
     for (int p = tid; p < nparts; p += blockDim.x) {
       const float* q = parts + ((size_t)p * 64 + col) * 3;
@@ -301,20 +310,29 @@ __global__ __launch_bounds__(256) void k_finalize_exit(const float* parts, int n
   if (tid < 64) {
     const int slot = tid;
     const bool live = slot < Bl;
-    int branch = -1;
+    int branch = -1, ej = kw;
     bool keep = false;
     if (live) {
       branch = c->live_idx[slot];
-      const float H = c->h_cur[slot];
-      const float delta = fabsf(H - c->h_prev[branch]);      // H_0 = +inf
-      const int streak = (delta < tau) ? c->streak[branch] + 1 : 0;
+      int streak = c->streak[branch];
+      float prev = c->h_prev[branch];   // H_0 = +inf
+      for (int j = 0; j < kw; ++j) {
+        const float H = c->h_cur[j * Bl + slot];
+        streak = fabsf(H - prev) < tau ? streak + 1 : 0;
+        prev = H;
+        entropy[(size_t)(layer1 - 1 + j) * B + branch] = H;
+        if (streak >= patience) {
+          exit_layer[branch] = layer1 + j;
+          ej = j;
+          break;
+        }
+      }
       c->streak[branch] = streak;
-      c->h_prev[branch] = H;
-      entropy[(size_t)(layer1 - 1) * B + branch] = H;
-      const bool exits = streak >= patience;
-      if (exits) exit_layer[branch] = layer1;
-      keep = !exits && layer1 < L;
+      c->h_prev[branch] = prev;
+      keep = ej == kw && layer1 + kw - 1 < L;
     }
+    exit_j[slot] = ej;
+    branch_of[slot] = branch;
     const unsigned long long mask = __ballot(keep);
     if (keep) {
       const int ns = __popcll(mask & ((1ull << slot) - 1ull));
@@ -322,6 +340,15 @@ __global__ __launch_bounds__(256) void k_finalize_exit(const float* parts, int n
       c->live_idx[ns] = branch;
     }
     if (slot == 0) c->live_count = __popcll(mask);
+  }
+  __syncthreads();
+  if (hidden_last) {
+    const float nan = __builtin_nanf("");
+    for (int slot = 0; slot < Bl; ++slot)
+      for (int j = exit_j[slot] + 1; j < kw; ++j) {
+        float* row = hidden_last + ((size_t)(layer1 - 1 + j) * B + branch_of[slot]) * d;
+        for (int e = tid; e < d; e += blockDim.x) row[e] = nan;
+      }
   }
 }
 
@@ -513,11 +540,11 @@ hipError_t launch_swiglu_post(DType dt, const float* P, int nsplit, size_t split
 
 hipError_t launch_tap(DType dt, const float* x, const float* P, int nsplit, size_t split_stride, const Ctrl* c,
                       int s, int d, int B, int layer0, float* hidden_last, const float* gamma, float eps,
-                      void* hn_a, void* hn_b, int max_branches, hipStream_t st) {
+                      void* hn_a, void* hn_b, int max_branches, hipStream_t st, int jrow) {
   const int chunks = (d / 4 + 1023) / 1024;
 #define RKSC_TAP(SPLIT, MAXC)                                                                                   \
   hipLaunchKernelGGL((k_tap<SPLIT, MAXC>), dim3(max_branches), dim3(1024), 0, st, x, P, nsplit, split_stride, c, \
-                     s, d, B, layer0, hidden_last, gamma, eps, hn_a, hn_b)
+                     s, d, B, layer0, hidden_last, gamma, eps, hn_a, hn_b, jrow)
   if (dt == DType::BF16) {
     if (chunks <= 1) RKSC_TAP(true, 1); else if (chunks <= 2) RKSC_TAP(true, 2); else RKSC_TAP(true, 4);
   } else {
@@ -527,10 +554,11 @@ hipError_t launch_tap(DType dt, const float* x, const float* P, int nsplit, size
   return hipGetLastError();
 }
 
-hipError_t launch_finalize_exit(const float* parts, int nparts, Ctrl* c, int layer1, int L, int B, float tau,
-                                int patience, float* entropy, int* exit_layer, hipStream_t st) {
-  hipLaunchKernelGGL(k_finalize_exit, dim3(1), dim3(256), 0, st, parts, nparts, c, layer1, L, B, tau, patience,
-                     entropy, exit_layer);
+hipError_t launch_finalize_exit(const float* parts, int nparts, Ctrl* c, int layer1, int kw, int L, int B, float tau,
+                                int patience, float* entropy, int* exit_layer, float* hidden_last, int d,
+                                hipStream_t st) {
+  hipLaunchKernelGGL(k_finalize_exit, dim3(1), dim3(256), 0, st, parts, nparts, c, layer1, kw, L, B, tau, patience,
+                     entropy, exit_layer, hidden_last, d);
   return hipGetLastError();
 }
 

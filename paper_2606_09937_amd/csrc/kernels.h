@@ -50,11 +50,12 @@ hipError_t launch_qkv_post(const float* P, int nsplit, size_t split_stride, cons
 hipError_t launch_swiglu_post(DType dt, const float* P, int nsplit, size_t split_stride, const Ctrl* c, int s,
                               int F, void* a, int max_rows, hipStream_t st);
 // Last token of each live branch: h = x + sum_sp P; hidden_last[l][branch] = h;
-// hn = RMSNorm(h; final_norm) as fp32 (F32) or as a bf16 hi+lo pair (BF16).
+// hn = RMSNorm(h; final_norm) as fp32 (F32) or as a bf16 hi+lo pair (BF16), at
+// row jrow * live_count + slot (jrow: the layer's place in an exit window).
 hipError_t launch_tap(DType dt, const float* x, const float* P, int nsplit, size_t split_stride,
                       const Ctrl* c, int s, int d, int B, int layer0, float* hidden_last,
                       const float* gamma, float eps, void* hn_a, void* hn_b, int max_branches,
-                      hipStream_t st);
+                      hipStream_t st, int jrow = 0);
 
 // ---- GEMM: P[split][m][n] = sum_{k in split} A[m][k] * W[n][k], rows m < live*s.
 // BF16 models: A0/A1 are the bf16 hi/lo planes of the activation, W bf16.
@@ -89,8 +90,9 @@ hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const vo
 
 // ---- entropy of the live branches' last-token logits
 int entropy_parts(DType dt, int V, int max_branches);
+// kmul: layers per exit window; the columns are kmul * live_count rows of hn.
 hipError_t launch_entropy(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c,
-                          int V, int d, int max_branches, float* parts, hipStream_t st);
+                          int V, int d, int max_branches, float* parts, hipStream_t st, int kmul = 1);
 // As launch_entropy, plus the vocabulary index of each column's maximum logit:
 // parts become [grid, 64, 4] = (m, s, t, argmax as int bits).
 hipError_t launch_entropy_argmax(DType dt, const void* W, const void* hn_a, const void* hn_b, const Ctrl* c, int V,
@@ -100,10 +102,13 @@ hipError_t launch_entropy_argmax(DType dt, const void* W, const void* hn_a, cons
 // (the top-1 softmax probability); conf = p_top (accumulate = 0) or conf + p_top.
 hipError_t launch_finalize_decode(const float* parts, int nparts, int B, int* next_token, float* p_top, float* conf,
                                   int accumulate, hipStream_t st);
-// Merges the partial statistics, writes entropy[l-1][branch], applies the exit
-// rule and compacts the live list.
-hipError_t launch_finalize_exit(const float* parts, int nparts, Ctrl* c, int layer1, int L, int B,
-                                float tau, int patience, float* entropy, int* exit_layer, hipStream_t st);
+// Merges the partial statistics of an exit window of kw layers from layer1
+// (1-based), writes entropy[l-1][branch], applies the exit rule layer by layer
+// (NaN for the window's layers after an exit, in entropy and hidden_last) and
+// compacts the live list.
+hipError_t launch_finalize_exit(const float* parts, int nparts, Ctrl* c, int layer1, int kw, int L, int B,
+                                float tau, int patience, float* entropy, int* exit_layer, float* hidden_last, int d,
+                                hipStream_t st);
 
 // ---- batched decode
 // Attention of one new token per branch (s = 1) over the shared prefix (split-KV

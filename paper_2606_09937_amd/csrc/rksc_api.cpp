@@ -131,6 +131,15 @@ rksc_status make_layout(const rksc_model_config* c, int B, int s, int n_prefix, 
   return RKSC_OK;
 }
 
+// Exit window: the lm_head-entropy stream of the probe (one read of W_lm) is
+// shared by `window` consecutive layers, whose rows become extra columns of the
+// same stream; the exit rule still runs layer by layer at the window's end (a
+// branch's layers after its exit inside the window are computed and discarded).
+// Up to 32 columns cost the same stream, so the window is 4 layers up to 8
+// branches, 2 up to 16, else 1.
+constexpr int kMaxWindow = 8;
+int exit_window(int B) { return B <= 8 ? 4 : B <= 16 ? 2 : 1; }
+
 #define HIP_TRY(expr)                                                                   \
   do {                                                                                  \
     hipError_t e_ = (expr);                                                             \
@@ -173,7 +182,7 @@ namespace {
 rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const int32_t* branch_tokens,
                         int32_t n_branches, int32_t branch_len, float tau, int32_t patience, float* entropy,
                         int32_t* exit_layer, float* hidden_last, void* workspace, size_t workspace_bytes,
-                        void* stream, void* const* events) {
+                        void* stream, void* const* events, int32_t window) {
   if (!w) return fail(RKSC_ERR_INVALID_ARGUMENT, "weights is NULL");
   if (!kv) return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix_kv is NULL");
   if (!branch_tokens) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_tokens is NULL");
@@ -184,6 +193,10 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
   if (std::isnan(tau) || tau < 0.f) return fail(RKSC_ERR_INVALID_ARGUMENT, "tau must be >= 0 and not NaN");
   if (patience < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "patience must be >= 1 (got %d)", patience);
+  if (window < 1 || window > kMaxWindow || (long long)window * n_branches > 64)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "window must be in [1, %d] with window * n_branches <= 64 (got %d, %d)",
+                kMaxWindow, window, n_branches);
+  const int win = window;
   const rksc_model_config* c = &w->cfg;
   if (kv->n_prefix < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", kv->n_prefix);
   Layout lay;
@@ -249,8 +262,9 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     float* x_prev = (l % 2 == 0) ? x0 : x1;
     float* x_cur = (l % 2 == 0) ? x1 : x0;
     // Residual stream of the live rows (gathered), plus the previous layer's FFN output.
-    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, true, ctrl, s,
-                                  x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
+    // The live set changes only at window ends: the survivors are gathered at a window's first layer.
+    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, l % win == 0, ctrl,
+                                  s, x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
     HIP_TRY(mark(l, 0));
     // Projection inputs: bf16 planes hi = act[0, M*K), lo = act[M*K, 2*M*K) for BF16 models.
     HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
@@ -280,12 +294,15 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
                               M, d, F, strm));
     HIP_TRY(mark(l, 9));
     HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, B, l, hidden_last,
-                             w->final_norm, c->rms_eps, hn_a, hn_b, B, strm));
-    HIP_TRY(mark(l, 10));
-    HIP_TRY(rksc::launch_entropy(dt, w->lm_head, hn_a, hn_b, ctrl, V, d, B, parts, strm));
-    HIP_TRY(mark(l, 11));
-    HIP_TRY(rksc::launch_finalize_exit(parts, lay.nparts, ctrl, l + 1, L, B, tau, patience, entropy, exit_layer,
-                                       strm));
+                             w->final_norm, c->rms_eps, hn_a, hn_b, B, strm, l % win));
+    if (l % win == win - 1 || l == L - 1) {   // window end: one lm_head stream for its layers
+      const int kw = l % win + 1, first = l + 1 - kw;
+      HIP_TRY(mark(l, 10));
+      HIP_TRY(rksc::launch_entropy(dt, w->lm_head, hn_a, hn_b, ctrl, V, d, B, parts, strm, kw));
+      HIP_TRY(mark(l, 11));
+      HIP_TRY(rksc::launch_finalize_exit(parts, lay.nparts, ctrl, first + 1, kw, L, B, tau, patience, entropy,
+                                         exit_layer, hidden_last, d, strm));
+    }
   }
   return ok();
 }
@@ -298,7 +315,18 @@ RKSC_EXPORT rksc_status rksc_verify_forward(const rksc_weights* w, const rksc_pr
                                             float* hidden_last, void* workspace, size_t workspace_bytes,
                                             void* stream) {
   return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
-                     hidden_last, workspace, workspace_bytes, stream, nullptr);
+                     hidden_last, workspace, workspace_bytes, stream, nullptr, exit_window(n_branches));
+}
+
+RKSC_EXPORT int32_t rksc_verify_window(int32_t n_branches) { return exit_window(n_branches); }
+
+RKSC_EXPORT rksc_status rksc_verify_forward_window(const rksc_weights* w, const rksc_prefix_kv* kv,
+                                                   const int32_t* branch_tokens, int32_t n_branches,
+                                                   int32_t branch_len, float tau, int32_t patience, float* entropy,
+                                                   int32_t* exit_layer, float* hidden_last, void* workspace,
+                                                   size_t workspace_bytes, void* stream, int32_t window) {
+  return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
+                     hidden_last, workspace, workspace_bytes, stream, nullptr, window);
 }
 
 RKSC_EXPORT rksc_status rksc_verify_forward_profiled(const rksc_weights* w, const rksc_prefix_kv* kv,
@@ -309,7 +337,7 @@ RKSC_EXPORT rksc_status rksc_verify_forward_profiled(const rksc_weights* w, cons
                                                      void* const* events) {
   if (!events) return fail(RKSC_ERR_INVALID_ARGUMENT, "events is NULL");
   return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
-                     hidden_last, workspace, workspace_bytes, stream, events);
+                     hidden_last, workspace, workspace_bytes, stream, events, exit_window(n_branches));
 }
 
 RKSC_EXPORT size_t rksc_prefill_workspace_size(const rksc_model_config* cfg, int32_t n_prefix) {

@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
     assert "rksc_verify_forward" in names and "rksc_asks_similarity" in names
     for name in names:
         assert hasattr(lib, name), f"{name} declared in include/ but not exported"
-    assert rk.rksc_abi_version() == 5
+    assert rk.rksc_abi_version() == 6
 
 
 def test_status_strings(lib):

@@ -159,3 +159,31 @@ def test_large_shapes_sampled_branches(name, layers):
     mw, kv, toks = _inputs(wl.model, wl.n_branches, wl.prefix_len, wl.branch_len, seed=42, n_layers=layers)
     branches = [0, wl.n_branches - 1]
     _parity(mw, kv, toks, wl.tau, wl.patience, name, branches=branches)
+
+
+@pytest.mark.parametrize("B,taus", [(1, (0.3, 0.6, 0.0)), (4, (0.3, 0.0)), (9, (0.3,)), (20, (0.3,))])
+def test_exit_window_does_not_change_outputs(B, taus):
+    """The exit window (layers sharing one lm_head stream) changes only the schedule: entropies,
+    exit layers and hidden rows (NaN after each exit, also inside a window) match the oracle
+    for every window, and windows of up to 32 columns reproduce the layer-by-layer outputs bit
+    for bit (the same stream kernel; each column is computed on its own)."""
+    shape = dataclasses.replace(workloads.get("tiny_deep").model, dtype="bf16")
+    mw, kv, toks = _inputs(shape, B, 64, 5, 91)
+    assert rk.rksc_verify_window(B) == (4 if B <= 8 else 2 if B <= 16 else 1)
+    for tau in taus:
+        ent_ref, hid_ref, ex_ref = _run_oracle(mw, kv, toks, tau, 1)
+        base = None
+        for win in (1, 2, 3, 4, 8):
+            if win * B > 64:
+                continue
+            ent, ex, hid = rk.verify_forward(mw, kv.k, kv.v, toks, tau, 1, return_hidden=True, window=win)
+            torch.cuda.synchronize()
+            ent, ex, hid = to_np(ent), to_np(ex), to_np(hid)
+            stats = compare_verify(ent, ex, hid, ent_ref, hid_ref, ex_ref, tau, label=f"B={B} tau={tau} win={win}")
+            log(f"[window B={B} tau={tau} win={win}] exits {ex.tolist()} {stats}")
+            if base is None:
+                base = (ent, ex, hid)
+            elif win * B <= 32:
+                np.testing.assert_array_equal(ex, base[1])
+                np.testing.assert_array_equal(ent, base[0])
+                np.testing.assert_array_equal(hid, base[2])
