@@ -281,7 +281,8 @@ rksc_status rksc_prefix_extend(const rksc_weights* weights, const rksc_prefix_kv
  *         root rows of each branch's own rksc_prefill, or hidden_last of a
  *         verify pass); h_root [L, d] fp32 device.
  * sigma   [B] fp32 device out; shared [B] int32 device out.
- * L, B, d >= 1; alpha finite; tau not NaN.
+ * L, B, d >= 1; L <= 256 and d % 4 == 0 (RKSC_ERR_UNSUPPORTED otherwise);
+ * alpha finite; tau not NaN.
  */
 rksc_status rksc_asks_gate(const float* hidden, const float* h_root, int32_t n_layers, int32_t n_branches,
                            int32_t d_model, float alpha, float tau, float* sigma, int32_t* shared, void* stream);

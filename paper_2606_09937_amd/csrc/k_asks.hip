@@ -56,43 +56,41 @@ __global__ __launch_bounds__(256) void k_asks(const float* __restrict__ hidden, 
 
 // Alg. AsksGate against the root: sigma_b = sum_l w_l <h_b^l / |h_b^l|, r^l>
 // with the root rows r^l stored unit-normalised (Eq. prefix_fwd; they are not
-// normalised again), shared[b] = sigma_b >= tau. One workgroup per branch; a
-// zero branch row contributes 0.
-__global__ __launch_bounds__(256) void k_asks_gate(const float* __restrict__ hidden, const float* __restrict__ root,
-                                                   int L, int B, int d, float alpha, float tau,
-                                                   float* __restrict__ sigma, int* __restrict__ shared) {
-  __shared__ float red[2][4];
+// normalised again), shared[b] = sigma_b >= tau. One workgroup per branch; wave
+// w reduces the layers l = w, w + 8, ... (float4 loads, d % 4 == 0) and the
+// weighted sum runs over the layers in order, so the result does not depend on
+// the wave schedule. A zero branch row contributes 0.
+constexpr int kGateWaves = 8;
+constexpr int kGateMaxLayers = 256;
+
+__global__ __launch_bounds__(kGateWaves * 64) void k_asks_gate(const float* __restrict__ hidden,
+                                                               const float* __restrict__ root, int L, int B, int d,
+                                                               float alpha, float tau, float* __restrict__ sigma,
+                                                               int* __restrict__ shared) {
+  __shared__ float cosl[kGateMaxLayers];
   const int b = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const double a = (double)alpha;
-  const double top = a >= 0.0 ? a : a / (double)L;
-  double wsum = 0.0;
-  for (int l = 1; l <= L; ++l) wsum += exp(a * (double)l / (double)L - top);
-  float acc = 0.f;
-  for (int l = 0; l < L; ++l) {
-    const float* hb = hidden + ((size_t)l * B + b) * d;
-    const float* r = root + (size_t)l * d;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  for (int l = wid; l < L; l += kGateWaves) {
+    const float4* hb = reinterpret_cast<const float4*>(hidden + ((size_t)l * B + b) * d);
+    const float4* r = reinterpret_cast<const float4*>(root + (size_t)l * d);
     float dot = 0.f, nb = 0.f;
-    for (int k = tid; k < d; k += 256) {
-      const float x = hb[k];
-      dot = fmaf(x, r[k], dot);
-      nb = fmaf(x, x, nb);
+    for (int k = lane; k < d / 4; k += 64) {
+      const float4 x = hb[k], y = r[k];
+      dot = fmaf(x.x, y.x, fmaf(x.y, y.y, fmaf(x.z, y.z, fmaf(x.w, y.w, dot))));
+      nb = fmaf(x.x, x.x, fmaf(x.y, x.y, fmaf(x.z, x.z, fmaf(x.w, x.w, nb))));
     }
     dot = wave_sum(dot);
     nb = wave_sum(nb);
-    if (lane == 0) {
-      red[0][wid] = dot;
-      red[1][wid] = nb;
-    }
-    __syncthreads();
-    dot = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
-    nb = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
-    __syncthreads();
-    const float cosv = nb > 0.f ? dot / sqrtf(nb) : 0.f;
-    const float w = (float)(exp(a * (double)(l + 1) / (double)L - top) / wsum);
-    acc = fmaf(w, cosv, acc);
+    if (lane == 0) cosl[l] = nb > 0.f ? dot / sqrtf(nb) : 0.f;
   }
-  if (tid == 0) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double a = (double)alpha;
+    const double top = a >= 0.0 ? a : a / (double)L;
+    double wsum = 0.0;
+    for (int l = 1; l <= L; ++l) wsum += exp(a * (double)l / (double)L - top);
+    float acc = 0.f;
+    for (int l = 0; l < L; ++l) acc = fmaf((float)(exp(a * (double)(l + 1) / (double)L - top) / wsum), cosl[l], acc);
     sigma[b] = acc;
     shared[b] = acc >= tau ? 1 : 0;
   }
@@ -107,7 +105,7 @@ hipError_t launch_asks(const float* hidden, int L, int B, int d, float alpha, fl
 
 hipError_t launch_asks_gate(const float* hidden, const float* root, int L, int B, int d, float alpha, float tau,
                             float* sigma, int* shared, hipStream_t st) {
-  hipLaunchKernelGGL(k_asks_gate, dim3(B), dim3(256), 0, st, hidden, root, L, B, d, alpha, tau, sigma, shared);
+  hipLaunchKernelGGL(k_asks_gate, dim3(B), dim3(kGateWaves * 64), 0, st, hidden, root, L, B, d, alpha, tau, sigma, shared);
   return hipGetLastError();
 }
 

@@ -693,6 +693,8 @@ RKSC_EXPORT rksc_status rksc_asks_gate(const float* hidden, const float* h_root,
     return fail(RKSC_ERR_INVALID_ARGUMENT, "L, B and d must be >= 1 (got %d, %d, %d)", n_layers, n_branches,
                 d_model);
   if (n_branches > 65535) return fail(RKSC_ERR_UNSUPPORTED, "n_branches above 65535 (got %d)", n_branches);
+  if (n_layers > 256 || d_model % 4)
+    return fail(RKSC_ERR_UNSUPPORTED, "the gate needs L <= 256 and d %% 4 == 0 (got %d, %d)", n_layers, d_model);
   if (!std::isfinite(alpha)) return fail(RKSC_ERR_INVALID_ARGUMENT, "alpha must be finite");
   if (std::isnan(tau)) return fail(RKSC_ERR_INVALID_ARGUMENT, "tau must not be NaN");
   HIP_TRY(rksc::launch_asks_gate(hidden, h_root, n_layers, n_branches, d_model, alpha, tau, sigma, shared,

@@ -278,3 +278,9 @@ def test_prefix_extend_and_asks_gate_reject_bad_arguments(lib):
     assert G(FAKE, FAKE, 0, 4, 8, 1.5, 0.8, FAKE, FAKE, None) == I
     assert G(FAKE, FAKE, 2, 4, 8, math.inf, 0.8, FAKE, FAKE, None) == I
     assert G(FAKE, FAKE, 2, 4, 8, 1.5, math.nan, FAKE, FAKE, None) == I
+
+
+def test_asks_gate_rejects_unsupported_shapes(lib):
+    U = rk.RKSC_ERR_UNSUPPORTED
+    assert lib.rksc_asks_gate(FAKE, FAKE, 257, 4, 8, 1.5, 0.8, FAKE, FAKE, None) == U
+    assert lib.rksc_asks_gate(FAKE, FAKE, 2, 4, 10, 1.5, 0.8, FAKE, FAKE, None) == U
