@@ -617,7 +617,10 @@ def main():
         rec["algorithmic_bytes"] = wk["bytes"]
         rec["algorithmic_flops"] = wk["flops"]
     dk = kernels[dom]
-    gemm_like = dom.endswith("_proj") and work[dom]["flops"] / work[dom]["bytes"] > 315
+    # Compute-bound when the class's arithmetic intensity is above the bf16 ridge
+    # (2.5 PFLOP/s / 8 TB/s = 312 flop/B): the projections at many rows, and the
+    # shared-prefix attention at long prefixes with many query rows.
+    gemm_like = work[dom]["flops"] / work[dom]["bytes"] > BF16_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3
     roofline = {
         "kernel": dom,
         "bound": "mfma" if gemm_like else "hbm",
