@@ -1,13 +1,15 @@
-"""Python binding of librksc, the MI355X (gfx950) RKSC verify-pass library.
+"""Python binding of librksc, the MI355X (gfx950) RKSC library.
 
-The functions named like the C ABI (rksc_verify_forward, rksc_asks_similarity,
-...) only marshal torch device tensors into pointers and call the library;
-every step of the verify pass runs in the library's HIP kernels. torch is used
+The functions named like the C ABI (rksc_verify_forward, rksc_prefill,
+rksc_decode_step, rksc_asks_gate, ...) only marshal torch device tensors into
+pointers and call the library; every step runs in the library's HIP kernels
+(the block table and the KV probe are the library's host C++). torch is used
 for device memory and streams only. If librksc.so is not built, every call
 raises: there is no fallback path.
 
-Convenience wrappers (verify_forward, asks_similarity) allocate the outputs and
-the workspace with torch and call the C ABI.
+Convenience wrappers (verify_forward, prefill, Decoder, prefix_extend,
+asks_similarity, asks_gate, cgee_gate, BlockTable, KVProbe) allocate outputs
+and workspaces with torch and call the C ABI.
 """
 from __future__ import annotations
 
