@@ -287,26 +287,26 @@ __global__ __launch_bounds__(1024) void k_tap(const float* __restrict__ x, const
 __global__ __launch_bounds__(256) void k_finalize_exit(const float* parts, int nparts, Ctrl* c, int layer1, int kw,
                                                        int L, int B, float tau, int patience, float* entropy,
                                                        int* exit_layer, float* hidden_last, int d) {
-  __shared__ EntStats red[256];
   __shared__ int exit_j[64], branch_of[64];
   const int Bl = c->live_count;
   if (Bl == 0) return;
-  const int tid = threadIdx.x;
-  for (int col = 0; col < Bl * kw; ++col) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  // One wave per column: lane p merges parts p, p + 64, ... in order, then a
+  // fixed shuffle tree merges the lanes.
+  for (int col = wid; col < Bl * kw; col += blockDim.x >> 6) {
     EntStats st = ent_empty();
-    for (int p = tid; p < nparts; p += blockDim.x) {
+    for (int p = lane; p < nparts; p += 64) {
       const float* q = parts + ((size_t)p * 64 + col) * 3;
       st = ent_merge(st, EntStats{q[0], q[1], q[2]});
     }
-    red[tid] = st;
-    __syncthreads();
-    for (int off = blockDim.x / 2; off > 0; off >>= 1) {
-      if (tid < off) red[tid] = ent_merge(red[tid], red[tid + off]);
-      __syncthreads();
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const EntStats o{__shfl_xor(st.m, off, 64), __shfl_xor(st.s, off, 64), __shfl_xor(st.t, off, 64)};
+      st = ent_merge(st, o);
     }
-    if (tid == 0) c->h_cur[col] = logf(red[0].s) - red[0].t / red[0].s;
-    __syncthreads();
+    if (lane == 0) c->h_cur[col] = logf(st.s) - st.t / st.s;
   }
+  __syncthreads();
   if (tid < 64) {
     const int slot = tid;
     const bool live = slot < Bl;

@@ -134,7 +134,8 @@ def test_decode_fp32(name):
     (GQA_BF16, 129, 1, 1, 2),      # one branch, one-token suffix
     (GQA_BF16, 0, 3, 5, 2),        # no prefix: own keys only
     (GQA_BF16, 700, 6, 9, 2),      # several split-KV chunks of the prefix
-], ids=["tiny_deep_bf16", "gqa_cross64", "gqa_single", "gqa_noprefix", "gqa_chunks"])
+    (GQA_BF16, 300, 20, 4, 2),     # more than 16 branches: the 128-row projections instead of the weight stream
+], ids=["tiny_deep_bf16", "gqa_cross64", "gqa_single", "gqa_noprefix", "gqa_chunks", "gqa_b20"])
 def test_decode_bf16(shape, n, B, s, steps):
     _decode_parity(shape, n, B, s, steps, 32, f"decode {shape.d_model}x{shape.n_layers} n={n} B={B} s={s}")
 
