@@ -30,6 +30,7 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   tree         a 64-token search-tree node built once over the prefix cache
                (rksc_prefix_extend) against 8 children recomputing it, and the
                device ASKS gate over 8 branches
+  asks_similarity  the pairwise ASKS similarity at B = 1, 8, 16, 32 (time only)
   cpu_baseline the float64 CPU oracle on a bounded sample of the workload
 
     python bench.py [--steps K] [--warmup W] [--workload 7b_single]
@@ -423,6 +424,36 @@ def measure_tree(mw, kv, shape, n, args, hip, sp, stream, dev):
     return out
 
 
+def measure_asks(shape, args, hip, sp, stream, dev):
+    """The ASKS pairwise similarity (Eq. asks_sim over all branch pairs) at the
+    workload's layer count and width for the branch counts of the configs
+    (1, 8, 16, 32): latency-bound, reported as time only."""
+    import torch
+
+    import paper_2606_09937_amd as rk
+    import workloads
+
+    L, d = shape.n_layers, shape.d_model
+    out = {}
+    for B in (1, 8, 16, 32):
+        hid = workloads.make_hidden(L, B, d, seed=args.seed, device=dev)
+        S = torch.empty((B, B), dtype=torch.float32, device=dev)
+        rk.rksc_asks_similarity(hid, 1.5, S, stream)
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(5):
+            a, b = hip.create(2)
+            hip.lib.hipEventRecord(ctypes.c_void_p(a), sp)
+            rk.rksc_asks_similarity(hid, 1.5, S, stream)
+            hip.lib.hipEventRecord(ctypes.c_void_p(b), sp)
+            torch.cuda.synchronize()
+            best = min(best, hip.elapsed_ms(a, b))
+            hip.destroy([a, b])
+        out[str(B)] = {"us": best * 1e3, "bytes": 4 * L * B * d}
+    log("asks similarity: " + ", ".join(f"B={k} {v['us']:.1f} us" for k, v in out.items()))
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -440,7 +471,8 @@ def main():
     ap.add_argument("--no-prefill", action="store_true", help="skip the root-forward (prefill) timing")
     ap.add_argument("--no-decode", action="store_true", help="skip the batched-decode timing")
     ap.add_argument("--no-probe", action="store_true", help="skip the KV probe timing")
-    ap.add_argument("--no-tree", action="store_true", help="skip the tree-sharing and ASKS-gate timing")
+    ap.add_argument("--no-tree", action="store_true",
+                    help="skip the tree-sharing, ASKS-gate and ASKS-similarity timings")
     ap.add_argument("--decode-only", action="store_true",
                     help="time only the batched decode (for a kernel trace of it) and print its JSON")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -709,6 +741,7 @@ def main():
     decode = None if args.no_decode else measure_decode(mw, kv, shape, n, args, hip, sp, stream, dev)
     kv_probe = None if args.no_probe else measure_kv_probe(mw, shape, n, args, stream, dev)
     tree = None if args.no_tree else measure_tree(mw, kv, shape, n, args, hip, sp, stream, dev)
+    asks = None if args.no_tree else measure_asks(shape, args, hip, sp, stream, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -748,6 +781,7 @@ def main():
         "decode": decode,
         "kv_probe": kv_probe,
         "tree": tree,
+        "asks_similarity": asks,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -318,7 +318,7 @@ rksc_status rksc_cgee_gate(const float* conf, int32_t n_branches, int32_t n_step
  * the root, append the root's rows (h_root of rksc_prefill) as one more
  * "branch".
  * hidden [L, B, d] fp32 device; S [B, B] fp32 device out.
- * L >= 1, B >= 1, d >= 1, alpha finite.
+ * L >= 1, B >= 1, d >= 1, alpha finite; L <= 256 (RKSC_ERR_UNSUPPORTED otherwise).
  */
 rksc_status rksc_asks_similarity(const float* hidden, int32_t n_layers, int32_t n_branches,
                                  int32_t d_model, float alpha, float* S, void* stream);

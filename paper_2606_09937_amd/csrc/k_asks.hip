@@ -2,8 +2,8 @@
 // Alg. AsksGate), for every pair of branches:
 //   S[i][j] = sum_l w_l <h_i^l, h_j^l> / (|h_i^l| |h_j^l|),
 //   w_l = exp(alpha l / L) / sum_l' exp(alpha l' / L), l = 1..L.
-// One workgroup per pair (i, j). For each layer it reduces the dot product and
-// both squared norms in one pass over d with a fixed reduction order, so
+// One workgroup per pair (i, j). Each layer's dot product and both squared
+// norms are reduced in one pass over d by one wave, in a fixed order, so
 // S[i][j] and S[j][i] are computed identically (S is exactly symmetric).
 #include "common.h"
 #include "kernels.h"
@@ -12,22 +12,21 @@ namespace rksc {
 
 namespace {
 
-__global__ __launch_bounds__(256) void k_asks(const float* __restrict__ hidden, int L, int B, int d, float alpha,
-                                              float* __restrict__ S) {
-  __shared__ float red[3][4];
+constexpr int kAsksWaves = 8;
+constexpr int kAsksMaxLayers = 256;
+
+__global__ __launch_bounds__(kAsksWaves * 64) void k_asks(const float* __restrict__ hidden, int L, int B, int d,
+                                                          float alpha, float* __restrict__ S) {
+  __shared__ float cosl[kAsksMaxLayers];
   const int i = blockIdx.x, j = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  // Weights in double with the largest exponent subtracted (no overflow for large |alpha|).
-  const double a = (double)alpha;
-  const double top = a >= 0.0 ? a : a / (double)L;
-  double wsum = 0.0;
-  for (int l = 1; l <= L; ++l) wsum += exp(a * (double)l / (double)L - top);
-  float acc = 0.f;
-  for (int l = 0; l < L; ++l) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  // Wave w takes the layers w, w + 8, ...; the weighted sum then runs over the
+  // layers in order, so S[i][j] and S[j][i] see the same operations.
+  for (int l = wid; l < L; l += kAsksWaves) {
     const float* hi = hidden + ((size_t)l * B + i) * d;
     const float* hj = hidden + ((size_t)l * B + j) * d;
     float dot = 0.f, ni = 0.f, nj = 0.f;
-    for (int k = tid; k < d; k += 256) {
+    for (int k = lane; k < d; k += 64) {
       const float x = hi[k], y = hj[k];
       dot = fmaf(x, y, dot);
       ni = fmaf(x, x, ni);
@@ -36,22 +35,20 @@ __global__ __launch_bounds__(256) void k_asks(const float* __restrict__ hidden, 
     dot = wave_sum(dot);
     ni = wave_sum(ni);
     nj = wave_sum(nj);
-    if (lane == 0) {
-      red[0][wid] = dot;
-      red[1][wid] = ni;
-      red[2][wid] = nj;
-    }
-    __syncthreads();
-    dot = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
-    ni = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
-    nj = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
-    __syncthreads();
     // The two norms enter symmetrically (ni*nj), so S[i][j] == S[j][i] bit for bit.
-    const float cosv = (ni > 0.f && nj > 0.f) ? dot / sqrtf(ni * nj) : 0.f;
-    const float w = (float)(exp(a * (double)(l + 1) / (double)L - top) / wsum);
-    acc = fmaf(w, cosv, acc);
+    if (lane == 0) cosl[l] = (ni > 0.f && nj > 0.f) ? dot / sqrtf(ni * nj) : 0.f;
   }
-  if (tid == 0) S[(size_t)i * B + j] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    // Weights in double with the largest exponent subtracted (no overflow for large |alpha|).
+    const double a = (double)alpha;
+    const double top = a >= 0.0 ? a : a / (double)L;
+    double wsum = 0.0;
+    for (int l = 1; l <= L; ++l) wsum += exp(a * (double)l / (double)L - top);
+    float acc = 0.f;
+    for (int l = 0; l < L; ++l) acc = fmaf((float)(exp(a * (double)(l + 1) / (double)L - top) / wsum), cosl[l], acc);
+    S[(size_t)i * B + j] = acc;
+  }
 }
 
 // Alg. AsksGate against the root: sigma_b = sum_l w_l <h_b^l / |h_b^l|, r^l>
@@ -99,7 +96,7 @@ __global__ __launch_bounds__(kGateWaves * 64) void k_asks_gate(const float* __re
 }  // namespace
 
 hipError_t launch_asks(const float* hidden, int L, int B, int d, float alpha, float* S, hipStream_t st) {
-  hipLaunchKernelGGL(k_asks, dim3(B, B), dim3(256), 0, st, hidden, L, B, d, alpha, S);
+  hipLaunchKernelGGL(k_asks, dim3(B, B), dim3(kAsksWaves * 64), 0, st, hidden, L, B, d, alpha, S);
   return hipGetLastError();
 }
 

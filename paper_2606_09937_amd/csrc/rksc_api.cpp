@@ -724,6 +724,7 @@ RKSC_EXPORT rksc_status rksc_asks_similarity(const float* hidden, int32_t n_laye
     return fail(RKSC_ERR_INVALID_ARGUMENT, "L, B and d must be >= 1 (got %d, %d, %d)", n_layers, n_branches,
                 d_model);
   if (n_branches > 65535) return fail(RKSC_ERR_UNSUPPORTED, "n_branches above 65535 (got %d)", n_branches);
+  if (n_layers > 256) return fail(RKSC_ERR_UNSUPPORTED, "n_layers above 256 (got %d)", n_layers);
   if (!std::isfinite(alpha)) return fail(RKSC_ERR_INVALID_ARGUMENT, "alpha must be finite");
   HIP_TRY(rksc::launch_asks(hidden, n_layers, n_branches, d_model, alpha, S, static_cast<hipStream_t>(stream)));
   return ok();
