@@ -156,8 +156,8 @@ rksc_status rksc_verify_forward(const rksc_weights* weights, const rksc_prefix_k
                                 float* entropy, int32_t* exit_layer, float* hidden_last,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
-/* The exit window rksc_verify_forward uses for n_branches branches: 4 up to 8
- * branches, 2 up to 16, else 1. */
+/* The exit window rksc_verify_forward uses for n_branches branches: 4 up to 16
+ * branches, 2 up to 32, else 1. */
 int32_t rksc_verify_window(int32_t n_branches);
 
 /* rksc_verify_forward with the exit window chosen by the caller: window = 1 is

@@ -183,7 +183,7 @@ __global__ __launch_bounds__(256) void k_qkv_post(const float* __restrict__ P, i
     if (kc) cdst = kc + (((size_t)slot * Hkv + (hh - H)) * cap + off + i) * hd;
   } else {
     dst = v_own + (((size_t)slot * Hkv + (hh - H - Hkv)) * s + i) * hd;
-    if (kc) cdst = vc + (((size_t)slot * Hkv + (hh - H - Hkv)) * cap + off + i) * hd;
+    if (vc) cdst = vc + (((size_t)slot * Hkv + (hh - H - Hkv)) * cap + off + i) * hd;
   }
   dst[j] = from_f32<T>(x1);
   dst[j + half] = from_f32<T>(x2);
