@@ -22,6 +22,8 @@ def _rand(shape, dtype, seed, std=1.0):
     (300, 136, 128, 3), (513, 260, 512, 0), (77, 64, 1000, 5),
     # 256 x 256 tiles (512 rows and more): ragged rows, columns and K, forced splits
     (777, 700, 1000, 3), (1024, 512, 2048, 0), (2048, 1536, 4104, 0),
+    # one row tile: the 7B projections at 128 rows with the planner's tile width and split count
+    (128, 4096, 14336, 0), (128, 4096, 4096, 0), (128, 6144, 4096, 0),
     # the planner's 256- and 192-column weight tiles (ragged N and K, two row tiles)
     (130, 14376, 1000, 0), (70, 6016, 4104, 0),
 ])
