@@ -64,6 +64,38 @@ __global__ void k_embed(const T* E, const int* tok, int V, float* x, int d) {
   for (int c = threadIdx.x; c < d; c += blockDim.x) xr[c] = to_f32(e[c]);
 }
 
+// ------------------------------------------------------------------ last-token tap
+
+// The tap of one residual row v (held as MAXC float4 chunks per thread of a
+// 1024-thread block) with rinv = 1 / RMS(v): the row itself to hl_row (when not
+// NULL) and RMSNorm(v; gamma) to row hrow of the normalised rows, as fp32
+// (hn_a) or as a bf16 hi + lo pair (hn_a, hn_b): hi = bf16(hn), lo =
+// bf16(hn - hi), so the lm_head product runs on bf16 MFMA with ~2^-16 relative
+// error on the activation.
+template <bool kSplitBf16, int MAXC>
+__device__ __forceinline__ void tap_store(const float4 (&v)[MAXC], float rinv, const float* __restrict__ gamma,
+                                          float* hl_row, void* hn_a, void* hn_b, size_t hrow, int d) {
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) {
+    const int col = (threadIdx.x + j * 1024) * 4;
+    if (col >= d) continue;
+    if (hl_row) *reinterpret_cast<float4*>(hl_row + col) = v[j];
+    const float4 g = *reinterpret_cast<const float4*>(gamma + col);
+    const float h0 = g.x * v[j].x * rinv, h1 = g.y * v[j].y * rinv, h2 = g.z * v[j].z * rinv, h3 = g.w * v[j].w * rinv;
+    if (kSplitBf16) {
+      uint16_t b0, b1, b2, b3, l0, l1, l2, l3;
+      split2(h0, b0, l0);
+      split2(h1, b1, l1);
+      split2(h2, b2, l2);
+      split2(h3, b3, l3);
+      *reinterpret_cast<uint2*>(static_cast<bf16*>(hn_a) + hrow * d + col) = make_uint2(pack2(b0, b1), pack2(b2, b3));
+      *reinterpret_cast<uint2*>(static_cast<bf16*>(hn_b) + hrow * d + col) = make_uint2(pack2(l0, l1), pack2(l2, l3));
+    } else {
+      *reinterpret_cast<float4*>(static_cast<float*>(hn_a) + hrow * d + col) = make_float4(h0, h1, h2, h3);
+    }
+  }
+}
+
 // ------------------------------------------------------------------ add + RMSNorm
 
 // One 1024-thread block per row; each thread keeps up to MAXC float4 chunks of
@@ -90,11 +122,13 @@ __device__ __forceinline__ void store_act4(void* base, size_t idx, size_t plane_
   }
 }
 
+// With tap.gamma set, the last row of each branch (r % s == s - 1) is also
+// tapped for the previous layer: x_out's row is that layer's output.
 template <int MAXC, bool kSplit>
 __global__ __launch_bounds__(1024) void k_add_norm(const float* __restrict__ x_in, const float* __restrict__ P,
                                                    int nsplit, size_t split_stride, int gather, const Ctrl* c,
                                                    int s, float* __restrict__ x_out, void* __restrict__ xn,
-                                                   const float* __restrict__ gamma, int d, float eps) {
+                                                   const float* __restrict__ gamma, int d, float eps, TapArgs tap) {
   __shared__ float red[16];
   const int r = blockIdx.x;
   if (r >= c->live_count * s) return;
@@ -131,6 +165,12 @@ __global__ __launch_bounds__(1024) void k_add_norm(const float* __restrict__ x_i
       store_act4<kSplit>(xn, (size_t)r * d + col, plane, g.x * v[j].x * rinv, g.y * v[j].y * rinv,
                          g.z * v[j].z * rinv, g.w * v[j].w * rinv);
     }
+  }
+  if (tap.gamma && r % s == s - 1) {
+    const int slot = r / s, branch = c->live_idx[slot];
+    tap_store<kSplit, MAXC>(v, rinv, tap.gamma,
+                            tap.hidden_last ? tap.hidden_last + ((size_t)tap.layer0 * tap.B + branch) * d : nullptr,
+                            tap.hn_a, tap.hn_b, (size_t)tap.jrow * c->live_count + slot, d);
   }
 }
 
@@ -218,7 +258,7 @@ __global__ __launch_bounds__(256) void k_swiglu_post(const float* __restrict__ P
                      g.y / (1.f + expf(-g.y)) * u.y, g.z / (1.f + expf(-g.z)) * u.z, g.w / (1.f + expf(-g.w)) * u.w);
 }
 
-// ------------------------------------------------------------------ last-token tap
+// ------------------------------------------------------------------ last-token tap kernel
 
 template <bool kSplitBf16, int MAXC>
 __global__ __launch_bounds__(1024) void k_tap(const float* __restrict__ x, const float* __restrict__ P, int nsplit,
@@ -251,28 +291,8 @@ __global__ __launch_bounds__(1024) void k_tap(const float* __restrict__ x, const
   }
   const float tot = block_sum(ss, red);
   const float rinv = rsqrtf(tot / (float)d + eps);
-#pragma unroll
-  for (int j = 0; j < MAXC; ++j) {
-    const int col = (threadIdx.x + j * 1024) * 4;
-    if (col >= d) continue;
-    if (hidden_last)
-      *reinterpret_cast<float4*>(hidden_last + ((size_t)layer0 * B + branch) * d + col) = v[j];
-    const float4 g = *reinterpret_cast<const float4*>(gamma + col);
-    const float h0 = g.x * v[j].x * rinv, h1 = g.y * v[j].y * rinv, h2 = g.z * v[j].z * rinv, h3 = g.w * v[j].w * rinv;
-    if (kSplitBf16) {
-      // hn = hi + lo with hi = bf16(hn) and lo = bf16(hn - hi): the lm_head product
-      // then runs on bf16 MFMA with ~2^-16 relative error on the activation.
-      uint16_t b0, b1, b2, b3, l0, l1, l2, l3;
-      split2(h0, b0, l0);
-      split2(h1, b1, l1);
-      split2(h2, b2, l2);
-      split2(h3, b3, l3);
-      *reinterpret_cast<uint2*>(static_cast<bf16*>(hn_a) + hrow * d + col) = make_uint2(pack2(b0, b1), pack2(b2, b3));
-      *reinterpret_cast<uint2*>(static_cast<bf16*>(hn_b) + hrow * d + col) = make_uint2(pack2(l0, l1), pack2(l2, l3));
-    } else {
-      *reinterpret_cast<float4*>(static_cast<float*>(hn_a) + hrow * d + col) = make_float4(h0, h1, h2, h3);
-    }
-  }
+  tap_store<kSplitBf16, MAXC>(v, rinv, gamma, hidden_last ? hidden_last + ((size_t)layer0 * B + branch) * d : nullptr,
+                              hn_a, hn_b, hrow, d);
 }
 
 // ------------------------------------------------------------------ entropy merge + exit rule
@@ -292,12 +312,24 @@ __global__ __launch_bounds__(256) void k_finalize_exit(const float* parts, int n
   if (Bl == 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   // One wave per column: lane p merges parts p, p + 64, ... in order, then a
-  // fixed shuffle tree merges the lanes.
+  // fixed shuffle tree merges the lanes. The loads of kBatch parts are issued
+  // together (one memory latency per batch, not per part).
+  constexpr int kBatch = 8;
   for (int col = wid; col < Bl * kw; col += blockDim.x >> 6) {
     EntStats st = ent_empty();
-    for (int p = lane; p < nparts; p += 64) {
-      const float* q = parts + ((size_t)p * 64 + col) * 3;
-      st = ent_merge(st, EntStats{q[0], q[1], q[2]});
+    for (int p0 = lane; p0 < nparts; p0 += 64 * kBatch) {
+      EntStats q[kBatch];
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const int p = p0 + 64 * i;
+        if (p < nparts) {
+          const float* e = parts + ((size_t)p * 64 + col) * 3;
+          q[i] = EntStats{e[0], e[1], e[2]};
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i)
+        if (p0 + 64 * i < nparts) st = ent_merge(st, q[i]);
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
@@ -499,11 +531,12 @@ hipError_t launch_embed(DType dt, const void* E, const int* tok, int V, float* x
 
 hipError_t launch_add_norm(DType dt, const float* x_in, const float* P, int nsplit, size_t split_stride,
                            bool gather, const Ctrl* c, int s, float* x_out, void* xn, const float* gamma, int d,
-                           float eps, int max_rows, hipStream_t st) {
+                           float eps, int max_rows, hipStream_t st, const TapArgs& tap) {
+  if (gather && tap.gamma) return hipErrorInvalidValue;   // the tap reads rows in place
   const int chunks = (d / 4 + 1023) / 1024;
 #define RKSC_NORM(MAXC, SPLIT)                                                                                   \
   hipLaunchKernelGGL((k_add_norm<MAXC, SPLIT>), dim3(max_rows), dim3(1024), 0, st, x_in, P, nsplit, split_stride, \
-                     (int)gather, c, s, x_out, xn, gamma, d, eps)
+                     (int)gather, c, s, x_out, xn, gamma, d, eps, tap)
   const bool sp = dt == DType::BF16;
   if (chunks <= 1) { if (sp) RKSC_NORM(1, true); else RKSC_NORM(1, false); }
   else if (chunks <= 2) { if (sp) RKSC_NORM(2, true); else RKSC_NORM(2, false); }

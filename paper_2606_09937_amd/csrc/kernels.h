@@ -34,11 +34,23 @@ hipError_t launch_embed(DType dt, const void* E, const int* tok, int V, float* x
 // Projection inputs (xn, attention output o, SwiGLU output a) are written as bf16
 // hi/lo planes for BF16 models (plane lo follows plane hi: max_rows rows each)
 // and as fp32 for F32 models; q, k_own, v_own and the residual stream are fp32.
+// The last-token tap of launch_tap, fused into launch_add_norm: layer layer0's
+// output rows go to hidden_last and their RMSNorm(final_norm = gamma) to row
+// jrow * live_count + slot of hn_a/hn_b. gamma NULL: no tap.
+struct TapArgs {
+  const float* gamma = nullptr;
+  float* hidden_last = nullptr;
+  int layer0 = 0, B = 0, jrow = 0;
+  void* hn_a = nullptr;
+  void* hn_b = nullptr;
+};
 // x_out[r] = x_in[src(r)] + sum_sp P[sp][src(r)] ; xn[r] = RMSNorm(x_out[r]; gamma).
 // gather: src(r) = gather_src[r / s] * s + r % s, else src(r) = r (x_in may equal x_out).
+// With tap.gamma set (no gather), each branch's last row x_out[slot * s + s - 1]
+// is also tapped as described for TapArgs.
 hipError_t launch_add_norm(DType dt, const float* x_in, const float* P, int nsplit, size_t split_stride,
                            bool gather, const Ctrl* c, int s, float* x_out, void* xn, const float* gamma, int d,
-                           float eps, int max_rows, hipStream_t st);
+                           float eps, int max_rows, hipStream_t st, const TapArgs& tap = TapArgs{});
 // q [rows, H, hd], k_own/v_own [B, Hkv, s, hd] from the summed QKV partials, RoPE on q and k.
 // With k_cache/v_cache, the keys and values are also stored (type cache_dt) as
 // entries off..off+s-1 of a cache layer [B, Hkv, cap, hd].

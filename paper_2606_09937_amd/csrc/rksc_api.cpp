@@ -265,8 +265,19 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     float* x_cur = (l % 2 == 0) ? x1 : x0;
     // Residual stream of the live rows (gathered), plus the previous layer's FFN output.
     // The live set changes only at window ends: the survivors are gathered at a window's first layer.
+    // Inside a window this kernel also taps the previous layer's last-token rows.
+    rksc::TapArgs tap;
+    if (l % win != 0) {
+      tap.gamma = w->final_norm;
+      tap.hidden_last = hidden_last;
+      tap.layer0 = l - 1;
+      tap.B = B;
+      tap.jrow = (l - 1) % win;
+      tap.hn_a = hn_a;
+      tap.hn_b = hn_b;
+    }
     HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, l % win == 0, ctrl,
-                                  s, x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
+                                  s, x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm, tap));
     HIP_TRY(mark(l, 0));
     // Projection inputs: bf16 planes hi = act[0, M*K), lo = act[M*K, 2*M*K) for BF16 models.
     HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
@@ -295,9 +306,9 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
                               M, d, F, strm));
     HIP_TRY(mark(l, 9));
-    HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, B, l, hidden_last,
-                             w->final_norm, c->rms_eps, hn_a, hn_b, B, strm, l % win));
     if (l % win == win - 1 || l == L - 1) {   // window end: one lm_head stream for its layers
+      HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, B, l, hidden_last,
+                               w->final_norm, c->rms_eps, hn_a, hn_b, B, strm, l % win));
       const int kw = l % win + 1, first = l + 1 - kw;
       HIP_TRY(mark(l, 10));
       HIP_TRY(rksc::launch_entropy(dt, w->lm_head, hn_a, hn_b, ctrl, V, d, B, parts, strm, kw));
@@ -416,8 +427,18 @@ RKSC_EXPORT rksc_status rksc_prefill(const rksc_weights* w, const int32_t* token
     const rksc_layer_weights& lw = w->layers[l];
     float* x_prev = (l % 2 == 0) ? x0 : x1;
     float* x_cur = (l % 2 == 0) ? x1 : x0;
-    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, true, ctrl, s,
-                                  x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
+    // Also taps the previous layer's last row (the root hidden state of that layer).
+    rksc::TapArgs tap;
+    if (l > 0) {
+      tap.gamma = w->final_norm;
+      tap.hidden_last = h_root;
+      tap.layer0 = l - 1;
+      tap.B = 1;
+      tap.hn_a = ws + lay.hn_a;
+      tap.hn_b = ws + lay.hn_b;
+    }
+    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, false, ctrl, s,
+                                  x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm, tap));
     HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
                               s, M, Nqkv, d, strm));
     // The cache layer [Hkv, n, hd] is the branch-cache layout with one slot, cap = n.
@@ -435,8 +456,9 @@ RKSC_EXPORT rksc_status rksc_prefill(const rksc_weights* w, const int32_t* token
     HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
                               M, d, F, strm));
-    HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, 1, l, h_root, w->final_norm,
-                             c->rms_eps, ws + lay.hn_a, ws + lay.hn_b, 1, strm));
+    if (l == L - 1)
+      HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, 1, l, h_root,
+                               w->final_norm, c->rms_eps, ws + lay.hn_a, ws + lay.hn_b, 1, strm));
   }
   HIP_TRY(rksc::launch_unit_rows(h_root, L, d, strm));
   return ok();
@@ -540,8 +562,18 @@ rksc_status branch_pass(const rksc_weights* w, const rksc_prefix_kv* kv, void* c
     const rksc_layer_weights& lw = w->layers[l];
     float* x_prev = (l % 2 == 0) ? x0 : x1;
     float* x_cur = (l % 2 == 0) ? x1 : x0;
-    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, true, ctrl, s,
-                                  x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm));
+    // With h_out, also taps the previous layer's last rows.
+    rksc::TapArgs tap;
+    if (l > 0 && out.h_out) {
+      tap.gamma = w->final_norm;
+      tap.hidden_last = out.h_out;
+      tap.layer0 = l - 1;
+      tap.B = B;
+      tap.hn_a = ws + lay.hn_a;
+      tap.hn_b = ws + lay.hn_b;
+    }
+    HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, false, ctrl, s,
+                                  x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm, tap));
     HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
                               s, M, Nqkv, d, strm));
     char* bk = static_cast<char*>(ck) + l * bkv_layer;
@@ -565,7 +597,7 @@ rksc_status branch_pass(const rksc_weights* w, const rksc_prefix_kv* kv, void* c
     HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
                               M, d, F, strm));
-    if (out.h_out || (out.next_token && l == L - 1))
+    if (l == L - 1 && (out.h_out || out.next_token))
       HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, B, l, out.h_out,
                                w->final_norm, c->rms_eps, ws + lay.hn_a, ws + lay.hn_b, B, strm));
   }
