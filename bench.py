@@ -352,6 +352,44 @@ def measure_decode(mw, kv, shape, n, args, hip, sp, stream, dev):
     return decode
 
 
+def measure_prefill(mw, shape, n, args, hip, sp, stream, dev):
+    """Root forward (Eq. prefix_fwd) over n tokens: ms per call and algorithmic TFLOP/s."""
+    import torch
+    import paper_2606_09937_amd as rk
+    import workloads
+    L = shape.n_layers
+    ptoks = workloads.make_tokens(n, shape.vocab, seed=args.seed, name="prefix", device=dev)
+    pws = torch.empty(rk.rksc_prefill_workspace_size(shape, n), dtype=torch.uint8, device=dev)
+    dt_kv = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    pk = torch.empty((L, shape.n_kv_heads, n, shape.head_dim), dtype=dt_kv, device=dev)
+    pv = torch.empty_like(pk)
+    hr = torch.empty((L, shape.d_model), dtype=torch.float32, device=dev)
+    pstep = lambda: rk.rksc_prefill(mw, ptoks, pk, pv, hr, pws, stream)   # noqa: E731
+    for _ in range(max(1, args.warmup)):
+        pstep()
+    torch.cuda.synchronize()
+    k_p = max(1, min(args.steps, 10))
+    a, b = hip.create(2)
+    hip.lib.hipEventRecord(ctypes.c_void_p(a), sp)
+    for _ in range(k_p):
+        pstep()
+    hip.lib.hipEventRecord(ctypes.c_void_p(b), sp)
+    torch.cuda.synchronize()
+    p_ms = hip.elapsed_ms(a, b) / k_p
+    hip.destroy([a, b])
+    d_, H_, Hkv_, hd_, F_ = shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.d_ff
+    P_ = d_ * (H_ + 2 * Hkv_) * hd_ + H_ * hd_ * d_ + 3 * d_ * F_
+    p_flops = L * (2.0 * n * P_ + 4.0 * hd_ * H_ * n * (n + 1) / 2)
+    peak = BF16_PEAK_TFLOPS if shape.dtype == "bf16" else FP32_PEAK_TFLOPS
+    prefill = {"n_prefix": n, "ms_per_call": p_ms, "tokens_per_s": n / (p_ms / 1e3), "calls_timed": k_p,
+               "algorithmic_tflops": p_flops / (p_ms / 1e3) / 1e12,
+               "mfma_frac": p_flops / (p_ms / 1e3) / 1e12 / peak}
+    log(f"prefill n={n}: {p_ms:.3f} ms/call, {prefill['tokens_per_s']:.0f} tokens/s, "
+        f"{prefill['algorithmic_tflops']:.1f} TFLOP/s algorithmic")
+    del pws, pk, pv, hr
+    return prefill
+
+
 def measure_kv_probe(mw, shape, n, args, stream, dev):
     """The KV probe (Sec. 2.2) at the paper's cost-constants setting: B = 8 branches
     over the workload's prefix with a DECODE_SUFFIX-token suffix; the three paths
@@ -475,6 +513,8 @@ def main():
                     help="skip the tree-sharing, ASKS-gate and ASKS-similarity timings")
     ap.add_argument("--decode-only", action="store_true",
                     help="time only the batched decode (for a kernel trace of it) and print its JSON")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="time only the root forward (for a kernel trace of it) and print its JSON")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the plain copy kernel used to scale HBM counters")
     ap.add_argument("--summarize-stats", dest="stats", metavar="DIR",
@@ -542,6 +582,15 @@ def main():
                                                   None, rk._ptr(ws), ws.numel(), sp, events)
         if st != 0:
             raise RuntimeError(f"rksc_verify_forward failed: {rk.rksc_last_error()}")
+
+    if args.prefill_only:
+        hip = HipEvents()
+        hip.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        prefill = measure_prefill(mw, shape, n, args, hip, sp, stream, dev)
+        print(json.dumps({"metric": "root forward (prefill) at 7B shape", "unit": "tokens/s",
+                          "value": prefill["tokens_per_s"], "dtype": shape.dtype, "data": "synthetic",
+                          "config": {"workload": wl.name, "prefix_len": n}, "prefill": prefill}), flush=True)
+        return
 
     if args.decode_only:
         hip = HipEvents()
@@ -708,35 +757,7 @@ def main():
     # the verify pass, which writes the cache the verify pass reads.
     prefill = None
     if not args.no_prefill:
-        ptoks = workloads.make_tokens(n, shape.vocab, seed=args.seed, name="prefix", device=dev)
-        pws = torch.empty(rk.rksc_prefill_workspace_size(shape, n), dtype=torch.uint8, device=dev)
-        dt_kv = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
-        pk = torch.empty((L, shape.n_kv_heads, n, shape.head_dim), dtype=dt_kv, device=dev)
-        pv = torch.empty_like(pk)
-        hr = torch.empty((L, shape.d_model), dtype=torch.float32, device=dev)
-        pstep = lambda: rk.rksc_prefill(mw, ptoks, pk, pv, hr, pws, stream)   # noqa: E731
-        for _ in range(max(1, args.warmup)):
-            pstep()
-        torch.cuda.synchronize()
-        k_p = max(1, min(args.steps, 10))
-        a, b = hip.create(2)
-        hip.lib.hipEventRecord(ctypes.c_void_p(a), sp)
-        for _ in range(k_p):
-            pstep()
-        hip.lib.hipEventRecord(ctypes.c_void_p(b), sp)
-        torch.cuda.synchronize()
-        p_ms = hip.elapsed_ms(a, b) / k_p
-        hip.destroy([a, b])
-        d_, H_, Hkv_, hd_, F_ = shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.d_ff
-        P_ = d_ * (H_ + 2 * Hkv_) * hd_ + H_ * hd_ * d_ + 3 * d_ * F_
-        p_flops = L * (2.0 * n * P_ + 4.0 * hd_ * H_ * n * (n + 1) / 2)
-        peak = BF16_PEAK_TFLOPS if shape.dtype == "bf16" else FP32_PEAK_TFLOPS
-        prefill = {"n_prefix": n, "ms_per_call": p_ms, "tokens_per_s": n / (p_ms / 1e3), "calls_timed": k_p,
-                   "algorithmic_tflops": p_flops / (p_ms / 1e3) / 1e12,
-                   "mfma_frac": p_flops / (p_ms / 1e3) / 1e12 / peak}
-        log(f"prefill n={n}: {p_ms:.3f} ms/call, {prefill['tokens_per_s']:.0f} tokens/s, "
-            f"{prefill['algorithmic_tflops']:.1f} TFLOP/s algorithmic")
-        del pws, pk, pv, hr
+        prefill = measure_prefill(mw, shape, n, args, hip, sp, stream, dev)
 
     decode = None if args.no_decode else measure_decode(mw, kv, shape, n, args, hip, sp, stream, dev)
     kv_probe = None if args.no_probe else measure_kv_probe(mw, shape, n, args, stream, dev)
