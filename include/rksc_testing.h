@@ -38,6 +38,14 @@ rksc_status rksc_test_gemm_kind(int32_t dtype, const void* A, const void* A_lo, 
                                 int32_t M, int32_t N, int32_t K, int32_t splits, int32_t kind,
                                 int32_t* splits_used, void* stream);
 
+/* The plan rksc_test_gemm_kind would launch for this shape, without launching
+ * anything (host only): plan[0..4] = kernel kind (0, 1 or 2 as above), rows
+ * and columns of a workgroup's output tile, number of K splits, K elements per
+ * split. The verify pass, the root forward and the decode use the plan of
+ * kind = -1, splits = 0 for each projection. */
+rksc_status rksc_test_gemm_plan(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t splits, int32_t kind,
+                                int32_t* plan);
+
 /* Shared-prefix attention of one layer for B branches of s tokens, with the
  * same split of the prefix across workgroups as the verify pass:
  * q [B*s, H, hd], k_own/v_own [B, Hkv, s, hd] are fp32 and prefix_k/prefix_v

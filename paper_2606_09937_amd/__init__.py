@@ -23,7 +23,7 @@ __all__ = [
     "RkscError", "load_library", "library_path",
     "rksc_abi_version", "rksc_verify_workspace_size", "rksc_verify_forward", "rksc_verify_window",
     "rksc_asks_similarity", "rksc_status_string", "rksc_last_error",
-    "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_attention",
+    "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_gemm_plan", "rksc_test_attention",
     "verify_forward", "asks_similarity", "prefill", "rksc_prefill", "rksc_prefill_workspace_size", "model_config",
     "BranchCache", "Decoder", "rksc_decode_workspace_size", "rksc_decode_suffix", "rksc_decode_step",
     "rksc_cgee_gate", "cgee_gate", "RKSC_ABI_VERSION", "BlockTable", "KVProbe",
@@ -173,6 +173,8 @@ def load_library():
     lib.rksc_test_gemm.argtypes = [i32, vp, vp, vp, vp, i32, i32, i32, i32, ctypes.POINTER(i32), vp]
     lib.rksc_test_gemm_kind.restype = i32
     lib.rksc_test_gemm_kind.argtypes = [i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, ctypes.POINTER(i32), vp]
+    lib.rksc_test_gemm_plan.restype = i32
+    lib.rksc_test_gemm_plan.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(i32)]
     lib.rksc_test_attention.restype = i32
     lib.rksc_test_attention_scratch_size.restype = sz
     lib.rksc_test_attention_scratch_size.argtypes = [i32, i32, i32, i32, i32, i32, i32]
@@ -299,6 +301,13 @@ def rksc_asks_similarity(hidden: torch.Tensor, alpha: float, S: torch.Tensor, st
     L, B, d = hidden.shape
     _check(load_library().rksc_asks_similarity(_ptr(hidden), int(L), int(B), int(d), float(alpha), _ptr(S),
                                                _stream(stream)))
+
+
+def rksc_test_gemm_plan(M: int, N: int, K: int, bf16: bool = True, splits: int = 0, kind: int = -1) -> dict:
+    """The GEMM plan of rksc_test_gemm for this shape (host only, nothing is launched)."""
+    plan = (ctypes.c_int32 * 5)()
+    _check(load_library().rksc_test_gemm_plan(RKSC_BF16 if bf16 else RKSC_F32, M, N, K, splits, kind, plan))
+    return dict(zip(("kind", "bm", "bn", "splits", "k_per_split"), list(plan)))
 
 
 def rksc_test_gemm(A, W: torch.Tensor, splits: int = 0, stream=None, kind: int = -1):

@@ -518,6 +518,40 @@ bool skinny_fits(DType dt, int max_rows, int N, int K) {
 }
 }  // namespace
 
+// From 512 rows the projections are MFMA-bound (2 * 128 = 256 flops per weight
+// byte with the hi/lo split), and what decides is how evenly the workgroups
+// fill whole rounds of the 256 CUs. Modelled time of a plan: rounds of
+// workgroups x one workgroup's MFMA work at the issue rate measured on MI355X
+// (~45% of peak for the 128-row tiles, ~50% for 256 x 256), plus the split
+// partials (written by the GEMM, about half of it hidden behind the MFMAs, and
+// read back by the row kernel after it, at ~6 TB/s). The 128-row plan `p0`
+// competes with 256 x 256 tiles over 1 to 8 K splits; the latter are taken
+// only if the model puts them at least 5% ahead. Measured at 1024 rows: the
+// 3584-wide QKV of the 28-layer shape went from 108 to 71 µs (3 splits), the
+// 7B down projection from 202 to 197 µs; at 512 rows the 7B gate|up from 259
+// to 224 µs.
+static GemmPlan plan_mfma_bound(GemmPlan p0, int max_rows, int N, int K) {
+  constexpr double kCuFlops = 2.5e15 / kComputeUnits;   // dense bf16 MFMA per CU
+  auto rounds = [](long long wgs) { return (double)((wgs + kComputeUnits - 1) / kComputeUnits); };
+  auto partials = [&](int sp) { return sp * (double)max_rows * N * 4.0 * 1.5 / 6e12; };
+  const int mt0 = cdiv(max_rows, p0.bm);
+  const double t0 = rounds((long long)cdiv(N, p0.bn) * mt0 * p0.splits) * 4.0 * p0.bm * p0.bn * p0.k_per_split /
+                        (kCuFlops * 0.45) + partials(p0.splits);
+  GemmPlan best = p0;
+  double t_best = t0;
+  for (int sp : {1, 2, 3, 4, 6, 8}) {
+    const int kps = cdiv(cdiv(K, 32), sp) * 32;
+    if (cdiv(K, kps) != sp || (sp > 1 && kps < 256)) continue;
+    const double t = rounds((long long)cdiv(N, 256) * cdiv(max_rows, 256) * sp) * 4.0 * 256 * 256 * kps /
+                         (kCuFlops * 0.50) + partials(sp);
+    if (t < t_best && t < 0.95 * t0) {
+      best = GemmPlan{1, 256, 256, sp, kps};
+      t_best = t;
+    }
+  }
+  return best;
+}
+
 GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
   GemmPlan p;
   p.kind = 0;
@@ -561,6 +595,7 @@ GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
   const int splits = splits_for(p.bn);
   p.k_per_split = cdiv(cdiv(K, 64), splits) * 64;
   p.splits = cdiv(K, p.k_per_split);
+  if (max_rows >= 512) return plan_mfma_bound(p, max_rows, N, K);
   // 256 x 256 tiles when they fill at least one full round of workgroups without
   // splitting K and, counted in rounds of 256 workgroups, finish sooner: measured
   // on MI355X (split MFMA work, 4096 rows) the 256 x 256 kernel issues MFMAs at

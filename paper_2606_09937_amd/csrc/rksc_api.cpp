@@ -786,6 +786,22 @@ RKSC_EXPORT rksc_status rksc_test_gemm_kind(int32_t dtype, const void* A, const 
   return ok();
 }
 
+RKSC_EXPORT rksc_status rksc_test_gemm_plan(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t splits,
+                                            int32_t kind, int32_t* plan) {
+  if (!plan) return fail(RKSC_ERR_INVALID_ARGUMENT, "plan must not be NULL");
+  if (dtype != RKSC_F32 && dtype != RKSC_BF16) return fail(RKSC_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (M < 1 || N < 1 || K < 8 || K % 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "bad shape %d x %d x %d", M, N, K);
+  if (splits < 0 || splits > 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "splits must be in [0, 8]");
+  if (kind < -1 || kind > 2) return fail(RKSC_ERR_INVALID_ARGUMENT, "kind must be -1, 0, 1 or 2 (got %d)", kind);
+  const GemmPlan p = rksc::plan_gemm_kind(dtype == RKSC_BF16 ? DType::BF16 : DType::F32, M, N, K, kind, splits);
+  plan[0] = p.kind;
+  plan[1] = p.bm;
+  plan[2] = p.bn;
+  plan[3] = p.splits;
+  plan[4] = p.k_per_split;
+  return ok();
+}
+
 RKSC_EXPORT rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P,
                                        int32_t M, int32_t N, int32_t K, int32_t splits, int32_t* splits_used,
                                        void* stream) {

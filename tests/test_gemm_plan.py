@@ -1,0 +1,57 @@
+"""Host-side pins of the projection planner (rksc_test_gemm_plan launches nothing)."""
+import pytest
+
+import paper_2606_09937_amd as rk
+
+# The 7B projections: (N, K) of QKV, O, gate|up, down.
+P7B = {"qkv": (6144, 4096), "o": (4096, 4096), "gu": (28672, 4096), "down": (4096, 14336)}
+
+
+@pytest.mark.parametrize("M", [17, 64, 128])
+def test_128_row_plans_at_the_headline_shape(M):
+    """Up to 128 rows: one row tile, the widest column tile that reaches ~224 workgroups with at most
+    8 K splits (the HBM-bound verify pass of one branch)."""
+    want = {"qkv": (192, 8), "o": (128, 8), "gu": (256, 2), "down": (128, 8)}
+    for name, (N, K) in P7B.items():
+        p = rk.rksc_test_gemm_plan(M, N, K)
+        assert (p["kind"], p["bm"]) == (0, 128), (name, p)
+        assert (p["bn"], p["splits"]) == want[name], (name, p)
+
+
+@pytest.mark.parametrize("M", [1, 8, 16])
+def test_weight_stream_for_decode_rows(M):
+    for name, (N, K) in P7B.items():
+        p = rk.rksc_test_gemm_plan(M, N, K)
+        assert p["kind"] == 2 and p["k_per_split"] == 2048 and p["splits"] == -(-K // 2048), (name, p)
+
+
+@pytest.mark.parametrize("M,N,K,want", [
+    # measured on MI355X: 108 -> 71 us with 256 x 256 tiles over 3 K splits (28-layer QKV, 1024 rows)
+    (1024, 4608, 3584, (1, 3)),
+    # 259 -> 224 us: one round of 224 wide workgroups instead of 448 128-row ones (7B gate|up, 512 rows)
+    (512, 28672, 4096, (1, 1)),
+    # equal within noise: the 128-row plan stays (7B O, 1024 rows)
+    (1024, 4096, 4096, (0, 2)),
+    # many rows: whole rounds of wide tiles without splitting K
+    (8192, 4096, 14336, (1, 1)),
+])
+def test_mfma_bound_plans(M, N, K, want):
+    p = rk.rksc_test_gemm_plan(M, N, K)
+    assert (p["kind"], p["splits"]) == want, p
+    assert p["bm"] == (256 if p["kind"] == 1 else 128)
+
+
+@pytest.mark.parametrize("M", [129, 256, 511, 512, 777, 1024, 2048, 4096, 8192])
+@pytest.mark.parametrize("N,K", list(P7B.values()) + [(4608, 3584), (3584, 18944), (37888, 3584), (260, 1000)])
+def test_plan_invariants(M, N, K):
+    """Every plan covers K exactly with at most 8 splits (the row kernels sum at most 8 partials), in
+    whole pipeline stages (64 K elements for 128-row tiles, 32 for 256 x 256), none of them empty."""
+    for bf16 in (True, False):
+        p = rk.rksc_test_gemm_plan(M, N, K, bf16=bf16)
+        sp, kps = p["splits"], p["k_per_split"]
+        assert 1 <= sp <= 8, p
+        assert (sp - 1) * kps < K <= sp * kps, p
+        if bf16:
+            assert kps % (32 if p["kind"] == 1 else 64) == 0 or sp == 1, p
+        else:
+            assert p["kind"] == 0, p

@@ -26,6 +26,8 @@ def _rand(shape, dtype, seed, std=1.0):
     (128, 4096, 14336, 0), (128, 4096, 4096, 0), (128, 6144, 4096, 0),
     # the planner's 256- and 192-column weight tiles (ragged N and K, two row tiles)
     (130, 14376, 1000, 0), (70, 6016, 4104, 0),
+    # the planner's 256 x 256 tiles over K splits at 512 and 1024 rows (3 and 4 splits)
+    (1024, 4608, 3584, 0), (512, 6144, 4096, 0),
 ])
 def test_gemm_matches_fp64(dtype, M, N, K, splits):
     log(f"gemm {dtype} M={M} N={N} K={K} splits={splits}")
