@@ -520,7 +520,9 @@ bool skinny_fits(DType dt, int max_rows, int N, int K) {
 
 // From 512 rows the projections are MFMA-bound (2 * 128 = 256 flops per weight
 // byte with the hi/lo split), and what decides is how evenly the workgroups
-// fill whole rounds of the 256 CUs. Modelled time of a plan: rounds of
+// fill whole rounds of the 256 CUs. (Used from 512 to 1024 rows, where it was
+// measured; with many rounds the 256 x 256 tiles' lead grows beyond the fixed
+// rates below, and the whole-round rule after this function decides.) Modelled time of a plan: rounds of
 // workgroups x one workgroup's MFMA work at the issue rate measured on MI355X
 // (~45% of peak for the 128-row tiles, ~50% for 256 x 256), plus the split
 // partials (written by the GEMM, about half of it hidden behind the MFMAs, and
@@ -595,7 +597,7 @@ GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
   const int splits = splits_for(p.bn);
   p.k_per_split = cdiv(cdiv(K, 64), splits) * 64;
   p.splits = cdiv(K, p.k_per_split);
-  if (max_rows >= 512) return plan_mfma_bound(p, max_rows, N, K);
+  if (max_rows >= 512 && max_rows <= 1024) return plan_mfma_bound(p, max_rows, N, K);
   // 256 x 256 tiles when they fill at least one full round of workgroups without
   // splitting K and, counted in rounds of 256 workgroups, finish sooner: measured
   // on MI355X (split MFMA work, 4096 rows) the 256 x 256 kernel issues MFMAs at

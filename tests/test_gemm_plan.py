@@ -33,7 +33,7 @@ def test_weight_stream_for_decode_rows(M):
     # equal within noise: the 128-row plan stays (7B O, 1024 rows)
     (1024, 4096, 4096, (0, 2)),
     # many rows: whole rounds of wide tiles without splitting K
-    (8192, 4096, 14336, (1, 1)),
+    (8192, 4096, 14336, (1, 1)), (4096, 37888, 3584, (1, 1)),
 ])
 def test_mfma_bound_plans(M, N, K, want):
     p = rk.rksc_test_gemm_plan(M, N, K)
