@@ -697,6 +697,11 @@ def main():
         rec["mfma_frac"] = rec["tflops"] / peak
         rec["algorithmic_bytes"] = wk["bytes"]
         rec["algorithmic_flops"] = wk["flops"]
+        # HBM bytes per launch from the committed rocprofv3 counter passes, where taken
+        traffic = stored_traffic(name, wl.name)
+        if traffic is not None:
+            rec["hbm_traffic_bytes"] = traffic
+            rec["hbm_traffic_gbs"] = traffic / sec / 1e9
     dk = kernels[dom]
     # Compute-bound when the class's arithmetic intensity is above the bf16 ridge
     # (2.5 PFLOP/s / 8 TB/s = 312 flop/B): the projections at many rows, and the
