@@ -21,19 +21,20 @@ extern "C" {
  * RKSC_BF16: the activation is given as its bf16 hi/lo planes A and A_lo
  * ([M, K] each, A = hi + lo). RKSC_F32: A is fp32 [M, K], A_lo unused.
  * P is fp32 and must hold 8 * M * N floats. splits = 0 uses the library's
- * own split-K plan for this shape (bf16 with M <= 16 always does: the
- * weight-streaming kernel fixes its splits); the number used is written to
+ * own split-K plan for this shape (bf16 with M <= 16, or M <= 32 and
+ * K <= 16384, always does: the weight-streaming kernel fixes its splits); the
+ * number used is written to
  * *splits_used (host pointer). K % 8 == 0. */
 rksc_status rksc_test_gemm(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P, int32_t M,
                            int32_t N, int32_t K, int32_t splits, int32_t* splits_used, void* stream);
 
 /* rksc_test_gemm with the kernel chosen by the caller: kind = -1 the
  * library's own choice for this shape, 0 the 128-row-tile kernel, 1 the
- * 256 x 256-tile kernel, 2 the weight-streaming kernel for at most 16 rows
- * (kinds 1 and 2 bf16 only; kind 2 needs M <= 16, N % 4 == 0 and K <= 32768,
- * and fixes its own splits; RKSC_ERR_UNSUPPORTED otherwise). The verify pass
- * picks kind 1 for projections with many rows and kind 2 for a decode step of
- * at most 16 branches. */
+ * 256 x 256-tile kernel, 2 the weight-streaming kernel for at most 32 rows
+ * (kinds 1 and 2 bf16 only; kind 2 needs M <= 32, N % 4 == 0, K <= 32768 and,
+ * above 16 rows, K <= 16384, and fixes its own splits; RKSC_ERR_UNSUPPORTED
+ * otherwise). The verify pass picks kind 1 for projections with many rows and
+ * kind 2 for a decode step of at most 32 branches. */
 rksc_status rksc_test_gemm_kind(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P,
                                 int32_t M, int32_t N, int32_t K, int32_t splits, int32_t kind,
                                 int32_t* splits_used, void* stream);

@@ -315,7 +315,7 @@ def rksc_test_gemm(A, W: torch.Tensor, splits: int = 0, stream=None, kind: int =
 
     bf16 W: A is the pair (A_hi, A_lo) of bf16 [M, K] planes; fp32 W: A is an fp32 [M, K] tensor.
     kind: -1 the library's choice, 0 the 128-row-tile kernel, 1 the 256 x 256-tile kernel, 2 the
-    weight-streaming kernel for at most 16 rows (kinds 1 and 2 bf16 only).
+    weight-streaming kernel for at most 32 rows (kinds 1 and 2 bf16 only).
     """
     if W.dtype == torch.bfloat16:
         a_hi, a_lo = A

@@ -365,9 +365,10 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 // ---------------------------------------------------------------- skinny GEMM
 //
-// At most 16 activation rows (one decode token per branch): the product is a
+// At most 32 activation rows (one decode token per branch): the product is a
 // stream of the weight matrix, and the kernel is laid out like the lm_head
-// stream. The weights pass through an R-deep LDS ring of 16 KB units (16 rows x
+// stream. RB blocks of 16 activation rows (RB = 2 from 17 rows) meet every
+// weight fragment read from LDS. The weights pass through an R-deep LDS ring of 16 KB units (16 rows x
 // 512 K, one 1 KB row segment per DMA instruction, chunk c of row r at position
 // c ^ r), while the activation stays in registers: a workgroup covers a K range
 // of 2048 * KH (one split of the output) and wave w holds the hi and lo bf16
@@ -378,22 +379,25 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 // Workgroup (split, j) takes a contiguous range of the 16-row weight tiles.
 // Rows past N are clamped (fetched, never stored); activation rows past the
 // live rows are zero; chunks past K read the row start and meet zero fragments.
+// With two row blocks the ring has 6 units, so that the doubled reduction area
+// still fits the 160 KB of LDS, and the K range of a split is 2048 (KH = 1).
 constexpr int kSkUnit = 16 * 1024;
-constexpr int kSkRing = 7;
 constexpr int kSkGroup = 4;
-constexpr int kSkRedBytes = kGemmWaves * kSkGroup * 1024;
-constexpr int kSkMaxRows = 16;
+constexpr int kSkRedBytes = kGemmWaves * kSkGroup * 1024;   // per row block
+constexpr int kSkMaxRows = 32;
 
-template <int KH>
+template <int KH, int RB>
 __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_skinny(const bf16* __restrict__ Ahi,
                                                                  const bf16* __restrict__ Alo,
                                                                  const bf16* __restrict__ W, float* __restrict__ P,
                                                                  size_t split_stride, const Ctrl* c, int s,
                                                                  int max_rows, int N, int K, int wgps) {
-  constexpr int NW = kGemmWaves, R = kSkRing, IPW = 16 / NW;
+  constexpr int NW = kGemmWaves, R = RB == 1 ? 7 : 6, IPW = 16 / NW;
   constexpr int KSPLIT = 2048 * KH;
   static_assert(16 % NW == 0, "a unit's 16 rows split evenly over the waves");
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[R * kSkUnit + kSkRedBytes];
+  static_assert(RB == 1 || (RB == 2 && KH == 1), "two row blocks with one half-slice per wave");
+  static_assert(NW * 64 == RB * kSkGroup * 64 || RB == 1, "one merging thread per (block, tile, lane)");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[R * kSkUnit + RB * kSkRedBytes];
 
   const int Ml = c ? min(c->live_count * s, max_rows) : max_rows;
   const int sp = blockIdx.x / wgps, jw = blockIdx.x - sp * wgps;
@@ -426,29 +430,35 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_skinny(const bf16* __r
   // The activation fragments (after the ring's first units, so that both are in
   // flight together); the empty asm makes the compiler wait for them here, once.
   const bf16x8 zero = {};
-  bf16x8 ah[KH][8], al[KH][8];
-  const int arow = min(r16, max_rows - 1);
+  bf16x8 ah[RB][KH][8], al[RB][KH][8];
 #pragma unroll
-  for (int q = 0; q < KH; ++q) {
-    const int kb = k0 + 256 * (wid * KH + q);
+  for (int rb = 0; rb < RB; ++rb) {
+    const int ar = 16 * rb + r16;
+    const int arow = min(ar, max_rows - 1);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int k = kb + 32 * j + 8 * g;
-      const bool ok = k < K && r16 < Ml;
-      const size_t off = (size_t)arow * K + (ok ? k : 0);
-      const bf16x8 h = *reinterpret_cast<const bf16x8*>(Ahi + off);
-      const bf16x8 l = *reinterpret_cast<const bf16x8*>(Alo + off);
-      ah[q][j] = ok ? h : zero;
-      al[q][j] = ok ? l : zero;
+    for (int q = 0; q < KH; ++q) {
+      const int kb = k0 + 256 * (wid * KH + q);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = kb + 32 * j + 8 * g;
+        const bool ok = k < K && ar < Ml;
+        const size_t off = (size_t)arow * K + (ok ? k : 0);
+        const bf16x8 h = *reinterpret_cast<const bf16x8*>(Ahi + off);
+        const bf16x8 l = *reinterpret_cast<const bf16x8*>(Alo + off);
+        ah[rb][q][j] = ok ? h : zero;
+        al[rb][q][j] = ok ? l : zero;
+      }
     }
   }
 #pragma unroll
-  for (int q = 0; q < KH; ++q)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const u32x4 hv = __builtin_bit_cast(u32x4, ah[q][j]), lv = __builtin_bit_cast(u32x4, al[q][j]);
-      asm volatile("" ::"v"(hv), "v"(lv));
-    }
+    for (int q = 0; q < KH; ++q)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const u32x4 hv = __builtin_bit_cast(u32x4, ah[rb][q][j]), lv = __builtin_bit_cast(u32x4, al[rb][q][j]);
+        asm volatile("" ::"v"(hv), "v"(lv));
+      }
 
   int qc = 0;   // ring units consumed
   auto step = [&]() -> const uint8_t* {
@@ -463,9 +473,11 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_skinny(const bf16* __r
   floatx4* red = reinterpret_cast<floatx4*>(smem + R * kSkUnit);
   for (int gi = 0; gi < ntile; gi += kSkGroup) {
     const int gt = min(kSkGroup, ntile - gi);
-    floatx4 acc[kSkGroup];
+    floatx4 acc[RB][kSkGroup];
 #pragma unroll
-    for (int m = 0; m < kSkGroup; ++m) acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int m = 0; m < kSkGroup; ++m) acc[rb][m] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int m = 0; m < kSkGroup; ++m) {
       if (m < gt) {
@@ -480,29 +492,37 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_skinny(const bf16* __r
               for (int j = 0; j < 8; ++j) {
                 const int lc = 4 * (8 * kh + j) + g;
                 const bf16x8 a = *reinterpret_cast<const bf16x8*>(slot + r16 * 1024 + (lc ^ r16) * 16);
-                acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, ah[q][j], acc[m], 0, 0, 0);
-                acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, al[q][j], acc[m], 0, 0, 0);
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb) {
+                  acc[rb][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, ah[rb][q][j], acc[rb][m], 0, 0, 0);
+                  acc[rb][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, al[rb][q][j], acc[rb][m], 0, 0, 0);
+                }
               }
             }
           }
         }
       }
     }
-    // Lane (r16, g) of every wave holds, for activation row r16, its K part of
-    // weight rows 16 t + 4 g + i. The group's partial tiles meet in LDS; the
-    // area is rewritten only after the next group's first ring barrier.
+    // Lane (r16, g) of every wave holds, for activation row 16 rb + r16, its K
+    // part of weight rows 16 t + 4 g + i. The group's partial tiles meet in LDS;
+    // the area is rewritten only after the next group's first ring barrier.
 #pragma unroll
-    for (int m = 0; m < kSkGroup; ++m) red[(wid * kSkGroup + m) * 64 + lane] = acc[m];
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int m = 0; m < kSkGroup; ++m) red[((rb * NW + wid) * kSkGroup + m) * 64 + lane] = acc[rb][m];
     __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the partials are in LDS
     __builtin_amdgcn_s_barrier();
-    if (tid < gt * 64) {
-      const int m = tid >> 6, l = tid & 63;
-      floatx4 z = red[m * 64 + l];
+    {
+      const int rb = tid / (kSkGroup * 64), m = (tid >> 6) % kSkGroup, l = tid & 63;
+      if (rb < RB && m < gt) {
+        floatx4 z = red[((rb * NW) * kSkGroup + m) * 64 + l];
 #pragma unroll
-      for (int w = 1; w < NW; ++w) z += red[(w * kSkGroup + m) * 64 + l];
-      const int row = l & 15, n = 16 * (t0 + gi + m) + 4 * (l >> 4);
-      if (row < Ml && n < N)
-        *reinterpret_cast<float4*>(P + sp * split_stride + (size_t)row * N + n) = make_float4(z[0], z[1], z[2], z[3]);
+        for (int w = 1; w < NW; ++w) z += red[((rb * NW + w) * kSkGroup + m) * 64 + l];
+        const int row = 16 * rb + (l & 15), n = 16 * (t0 + gi + m) + 4 * (l >> 4);
+        if (row < Ml && n < N)
+          *reinterpret_cast<float4*>(P + sp * split_stride + (size_t)row * N + n) =
+              make_float4(z[0], z[1], z[2], z[3]);
+      }
     }
   }
   wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
@@ -512,9 +532,13 @@ namespace {
 // Half-slices per wave of the skinny kernel: the K range of a split is 2048 * KH
 // and the consumers sum at most kMaxSplitsGemm splits.
 int skinny_kh(int K) { return cdiv(K, 2048) <= kMaxSplitsGemm ? 1 : 2; }
+// From 17 rows the two-block stream is taken only for wide projections: at 32
+// rows it beat the 128-row tiles on the 28672-column gate|up (71 -> 53 us) and
+// lost on the 4096- and 6144-column ones (15 -> 19 us for O), whose short
+// stream per workgroup does not amortise the ring's fill and the reductions.
 bool skinny_fits(DType dt, int max_rows, int N, int K) {
-  return dt == DType::BF16 && max_rows <= kSkMaxRows && N % 4 == 0 && K % 8 == 0 &&
-         cdiv(K, 2048 * skinny_kh(K)) <= kMaxSplitsGemm;
+  const bool rows_ok = max_rows <= 16 || (max_rows <= kSkMaxRows && skinny_kh(K) == 1 && N >= 16384);
+  return dt == DType::BF16 && rows_ok && N % 4 == 0 && K % 8 == 0 && cdiv(K, 2048 * skinny_kh(K)) <= kMaxSplitsGemm;
 }
 }  // namespace
 
@@ -570,7 +594,7 @@ GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
   // bf16 with at most 16 rows (a decode step): the weight stream.
   if (skinny_fits(dt, max_rows, N, K)) {
     p.kind = 2;
-    p.bm = kSkMaxRows;
+    p.bm = max_rows <= 16 ? 16 : 32;
     p.bn = 16;
     p.k_per_split = 2048 * skinny_kh(K);
     p.splits = cdiv(K, p.k_per_split);
@@ -617,7 +641,7 @@ GemmPlan plan_gemm(DType dt, int max_rows, int N, int K) {
 
 GemmPlan plan_gemm_kind(DType dt, int max_rows, int N, int K, int kind, int splits) {
   if (kind == 2) {   // the skinny kernel fixes its own splits (callers check skinny_fits)
-    GemmPlan p{2, kSkMaxRows, 16, 1, 2048 * skinny_kh(K)};
+    GemmPlan p{2, max_rows <= 16 ? 16 : 32, 16, 1, 2048 * skinny_kh(K)};
     p.splits = cdiv(K, p.k_per_split);
     return p;
   }
@@ -657,12 +681,17 @@ hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* 
     const dim3 sgrid(p.splits * wgps);
     const bf16 *a0 = static_cast<const bf16*>(A0), *a1 = static_cast<const bf16*>(A1);
     if (p.k_per_split != 2048 && p.k_per_split != 4096) return hipErrorInvalidValue;
-    if (p.k_per_split == 2048)
-      hipLaunchKernelGGL(k_gemm_skinny<1>, sgrid, dim3(kGemmWaves * 64), 0, st, a0, a1, static_cast<const bf16*>(W),
-                         P, split_stride, c, s, max_rows, N, K, wgps);
+    if (max_rows > kSkMaxRows || (max_rows > 16 && (p.bm != 32 || p.k_per_split != 2048)))
+      return hipErrorInvalidValue;
+    if (p.bm == 32)
+      hipLaunchKernelGGL((k_gemm_skinny<1, 2>), sgrid, dim3(kGemmWaves * 64), 0, st, a0, a1,
+                         static_cast<const bf16*>(W), P, split_stride, c, s, max_rows, N, K, wgps);
+    else if (p.k_per_split == 2048)
+      hipLaunchKernelGGL((k_gemm_skinny<1, 1>), sgrid, dim3(kGemmWaves * 64), 0, st, a0, a1,
+                         static_cast<const bf16*>(W), P, split_stride, c, s, max_rows, N, K, wgps);
     else
-      hipLaunchKernelGGL(k_gemm_skinny<2>, sgrid, dim3(kGemmWaves * 64), 0, st, a0, a1, static_cast<const bf16*>(W),
-                         P, split_stride, c, s, max_rows, N, K, wgps);
+      hipLaunchKernelGGL((k_gemm_skinny<2, 1>), sgrid, dim3(kGemmWaves * 64), 0, st, a0, a1,
+                         static_cast<const bf16*>(W), P, split_stride, c, s, max_rows, N, K, wgps);
     return hipGetLastError();
   }
   const dim3 grid(cdiv(N, p.bn), cdiv(max_rows, p.bm), p.splits);

@@ -776,8 +776,8 @@ RKSC_EXPORT rksc_status rksc_test_gemm_kind(int32_t dtype, const void* A, const 
   if (splits < 0 || splits > 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "splits must be in [0, 8]");
   if (kind < -1 || kind > 2) return fail(RKSC_ERR_INVALID_ARGUMENT, "kind must be -1, 0, 1 or 2 (got %d)", kind);
   if (kind >= 1 && dtype != RKSC_BF16) return fail(RKSC_ERR_UNSUPPORTED, "kind %d needs bf16 weights", kind);
-  if (kind == 2 && (M > 16 || N % 4 || K > 32768))
-    return fail(RKSC_ERR_UNSUPPORTED, "kind 2 needs M <= 16, N %% 4 == 0 and K <= 32768");
+  if (kind == 2 && (M > 32 || N % 4 || K > 32768 || (M > 16 && K > 16384)))
+    return fail(RKSC_ERR_UNSUPPORTED, "kind 2 needs M <= 32, N %% 4 == 0 and K <= 32768 (K <= 16384 above 16 rows)");
   const DType dt = dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
   const GemmPlan p = rksc::plan_gemm_kind(dt, M, N, K, kind, splits);
   if (splits_used) *splits_used = p.splits;

@@ -145,7 +145,9 @@ def test_testing_entry_points_reject_bad_shapes(lib):
         rk.RKSC_ERR_INVALID_ARGUMENT
     assert lib.rksc_test_gemm_kind(1, FAKE, FAKE, FAKE, FAKE, 4, 4, 16, 0, 3, ctypes.byref(used), None) == \
         rk.RKSC_ERR_INVALID_ARGUMENT
-    assert lib.rksc_test_gemm_kind(1, FAKE, FAKE, FAKE, FAKE, 17, 4, 16, 0, 2, ctypes.byref(used), None) == \
+    assert lib.rksc_test_gemm_kind(1, FAKE, FAKE, FAKE, FAKE, 33, 4, 16, 0, 2, ctypes.byref(used), None) == \
+        rk.RKSC_ERR_UNSUPPORTED
+    assert lib.rksc_test_gemm_kind(1, FAKE, FAKE, FAKE, FAKE, 17, 4, 16400, 0, 2, ctypes.byref(used), None) == \
         rk.RKSC_ERR_UNSUPPORTED
     assert lib.rksc_test_gemm_kind(1, FAKE, FAKE, FAKE, FAKE, 4, 6, 16, 0, 2, ctypes.byref(used), None) == \
         rk.RKSC_ERR_UNSUPPORTED

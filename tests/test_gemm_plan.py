@@ -7,7 +7,7 @@ import paper_2606_09937_amd as rk
 P7B = {"qkv": (6144, 4096), "o": (4096, 4096), "gu": (28672, 4096), "down": (4096, 14336)}
 
 
-@pytest.mark.parametrize("M", [17, 64, 128])
+@pytest.mark.parametrize("M", [33, 64, 128])
 def test_128_row_plans_at_the_headline_shape(M):
     """Up to 128 rows: one row tile, the widest column tile that reaches ~224 workgroups with at most
     8 K splits (the HBM-bound verify pass of one branch)."""
@@ -18,11 +18,27 @@ def test_128_row_plans_at_the_headline_shape(M):
         assert (p["bn"], p["splits"]) == want[name], (name, p)
 
 
-@pytest.mark.parametrize("M", [1, 8, 16])
+@pytest.mark.parametrize("M", [1, 8, 16, 17, 32])
 def test_weight_stream_for_decode_rows(M):
+    """Up to 16 rows every projection streams the weights; from 17 to 32 rows (two 16-row activation
+    blocks) only the wide gate|up does, the others keep the 128-row tiles."""
     for name, (N, K) in P7B.items():
         p = rk.rksc_test_gemm_plan(M, N, K)
-        assert p["kind"] == 2 and p["k_per_split"] == 2048 and p["splits"] == -(-K // 2048), (name, p)
+        if M <= 16 or name == "gu":
+            assert p["kind"] == 2 and p["k_per_split"] == 2048 and p["splits"] == -(-K // 2048), (name, p)
+            assert p["bm"] == (16 if M <= 16 else 32), (name, p)
+        else:
+            assert p["kind"] == 0 and p["bm"] == 128, (name, p)
+
+
+def test_two_row_blocks_need_one_half_slice():
+    """Two row blocks hold one 256-wide half-slice per wave: K above 16384 falls back to 128-row tiles
+    from 17 rows, while 16 rows take 4096-wide splits."""
+    assert rk.rksc_test_gemm_plan(16, 4096, 20000)["kind"] == 2
+    assert rk.rksc_test_gemm_plan(16, 4096, 20000)["k_per_split"] == 4096
+    assert rk.rksc_test_gemm_plan(17, 28672, 20000)["kind"] == 0
+    assert rk.rksc_test_gemm_plan(17, 28672, 4096)["kind"] == 2
+    assert rk.rksc_test_gemm_plan(33, 28672, 4096)["kind"] == 0
 
 
 @pytest.mark.parametrize("M,N,K,want", [

@@ -82,11 +82,15 @@ def test_gemm_wide_tiles_match_fp64(M, N, K, splits):
 @pytest.mark.parametrize("M,N,K,kind", [
     (1, 16, 32, 2), (3, 4, 8, 2), (8, 260, 504, 2), (16, 1000, 2048, 2), (5, 6144, 4096, 2),
     (8, 4096, 14336, 2), (13, 1028, 4104, 2), (16, 200, 20000, 2), (8, 28672, 4096, -1), (7, 4096, 14336, -1),
+    # two 16-row activation blocks (17 to 32 rows): ragged rows, N and K, the 7B shapes
+    (17, 1000, 2048, 2), (20, 260, 1000, 2), (24, 1028, 4104, 2), (32, 6144, 4096, 2), (32, 28672, 4096, -1),
+    (29, 4096, 14336, 2), (17, 16384, 1000, -1),
 ])
 def test_gemm_skinny_matches_fp64(M, N, K, kind):
-    """The weight-streaming kernel for at most 16 rows (a decode step's projections), forced and as
+    """The weight-streaming kernel for at most 32 rows (a decode step's projections), forced and as
     the planner's choice: ragged N (a partial last 16-row weight tile), K not a multiple of 512, one
-    to eight K splits of 2048 and the 4096-wide splits of a K above 16384."""
+    to eight K splits of 2048, the 4096-wide splits of a K above 16384 (at most 16 rows), and two
+    16-row activation blocks from 17 rows."""
     log(f"gemm skinny M={M} N={N} K={K} kind={kind}")
     A = _rand((M, K), torch.float32, 21 + M, 0.5)
     W = _rand((N, K), torch.bfloat16, 22 + N, 0.05)
