@@ -389,20 +389,16 @@ def rsbcm_omega(score, depth) -> float:
 
 def rsbcm_evict(blocks, n_max: int):
     """Alg. RsbcmEvict on a block table given as a list of (id, score, depth) in
-    insertion order. While the table holds more than n_max blocks, recompute every
-    omega, take the first index of the least one, evict it. Returns (remaining
-    table, evicted ids in eviction order)."""
+    insertion order, keeping at most n_max blocks. A block's omega depends only on
+    its own score and depth, so evicting one never changes another's: the evicted
+    blocks are the len - n_max smallest by (omega, insertion index), in that order
+    (the algorithm takes the first of equal minima). Returns (remaining table in
+    insertion order, evicted ids in eviction order)."""
     table = list(blocks)
-    evicted = []
-    while len(table) > n_max:
-        omegas = [rsbcm_omega(score, depth) for _, score, depth in table]
-        least = 0
-        for i in range(1, len(table)):
-            if omegas[i] < omegas[least]:
-                least = i
-        evicted.append(table[least][0])
-        del table[least]
-    return table, evicted
+    n_evict = max(0, len(table) - int(n_max))
+    order = sorted(range(len(table)), key=lambda i: (rsbcm_omega(table[i][1], table[i][2]), i))
+    gone = set(order[:n_evict])
+    return [b for i, b in enumerate(table) if i not in gone], [table[i][0] for i in order[:n_evict]]
 
 
 def kv_probe_bucket(n_prefix: int) -> int:

@@ -197,6 +197,69 @@ def _ptr(t: Optional[torch.Tensor]):
     return ctypes.c_void_p(t.data_ptr())
 
 
+class _Args:
+    """Argument checks before pointers are handed to the library: every tensor's
+    dtype and shape (None entries match any size) first, then, in done(), that
+    all of them live on a GPU. Raises ValueError naming the argument."""
+
+    def __init__(self):
+        self._seen = []
+
+    def __call__(self, t, name: str, dtype=None, shape=None, ndim: Optional[int] = None):
+        if not isinstance(t, torch.Tensor):
+            raise ValueError(f"{name} must be a torch tensor (got {type(t).__name__})")
+        if dtype is not None and t.dtype != dtype:
+            raise ValueError(f"{name} must be {dtype} (got {t.dtype})")
+        if ndim is not None and t.dim() != ndim:
+            raise ValueError(f"{name} must have {ndim} dimensions (got shape {tuple(t.shape)})")
+        if shape is not None:
+            if t.dim() != len(shape) or any(w is not None and int(g) != int(w) for g, w in zip(t.shape, shape)):
+                want = "[" + ", ".join("*" if w is None else str(w) for w in shape) + "]"
+                raise ValueError(f"{name} must have shape {want} (got {list(t.shape)})")
+        self._seen.append((name, t))
+        return t
+
+    def done(self):
+        for name, t in self._seen:
+            if not t.is_cuda:
+                raise ValueError(f"{name} must be a GPU tensor (got device {t.device})")
+
+
+def _model_dtype(shape):
+    return torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+
+
+def _check_weights(need, weights, need_lm_head: bool = True):
+    """Every weight tensor of the decoder: model dtype (fp32 gains), torch Linear shapes."""
+    shape = weights.shape
+    dt = _model_dtype(shape)
+    d, F, V = shape.d_model, shape.d_ff, shape.vocab
+    H, Hkv, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
+    need(weights.embed, "embed", dt, (V, d))
+    need(weights.final_norm, "final_norm", torch.float32, (d,))
+    if need_lm_head or weights.lm_head is not None:
+        need(weights.lm_head, "lm_head", dt, (V, d))
+    for i, lw in enumerate(weights.layers):
+        need(lw["attn_norm"], f"layer {i} attn_norm", torch.float32, (d,))
+        need(lw["ffn_norm"], f"layer {i} ffn_norm", torch.float32, (d,))
+        need(lw["w_qkv"], f"layer {i} w_qkv", dt, ((H + 2 * Hkv) * hd, d))
+        need(lw["w_o"], f"layer {i} w_o", dt, (d, H * hd))
+        need(lw["w_gate_up"], f"layer {i} w_gate_up", dt, (2 * F, d))
+        need(lw["w_down"], f"layer {i} w_down", dt, (d, F))
+
+
+def _check_prefix(need, weights, prefix_k, prefix_v, name="prefix"):
+    """The shared cache [L, Hkv, n, hd] in the model dtype (both None: an empty prefix). Returns n."""
+    if prefix_k is None and prefix_v is None:
+        return 0
+    shape = weights.shape
+    dims = (len(weights.layers), shape.n_kv_heads, None, shape.head_dim)
+    need(prefix_k, f"{name}_k", _model_dtype(shape), dims)
+    n = int(prefix_k.shape[2])
+    need(prefix_v, f"{name}_v", _model_dtype(shape), dims[:2] + (n, dims[3]))
+    return n
+
+
 def _stream(stream):
     if stream is None:
         return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
@@ -257,10 +320,20 @@ def rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, 
     weights: object with .shape (decoder shape), .embed, .layers (dicts of tensors), .final_norm, .lm_head.
     prefix_k/prefix_v: [L, Hkv, n, hd] device tensors. branch_tokens: [B, s] int32 device.
     """
+    need = _Args()
+    _check_weights(need, weights)
+    n = _check_prefix(need, weights, prefix_k, prefix_v)
+    need(branch_tokens, "branch_tokens", torch.int32, ndim=2)
+    B, s = branch_tokens.shape
+    L, d = len(weights.layers), weights.shape.d_model
+    need(entropy, "entropy", torch.float32, (L, B))
+    need(exit_layer, "exit_layer", torch.int32, (B,))
+    if hidden_last is not None:
+        need(hidden_last, "hidden_last", torch.float32, (L, B, d))
+    need(workspace, "workspace", torch.uint8, ndim=1)
+    need.done()
     lib = load_library()
     w, layers_keepalive = _weights_struct(weights)
-    B, s = branch_tokens.shape
-    n = int(prefix_k.shape[2]) if prefix_k is not None else 0
     kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
     args = (ctypes.byref(w), ctypes.byref(kv), _ptr(branch_tokens), int(B), int(s), float(tau), int(patience),
             _ptr(entropy), _ptr(exit_layer), _ptr(hidden_last), _ptr(workspace),
@@ -287,6 +360,17 @@ def rksc_prefill(weights, tokens: torch.Tensor, k_out: torch.Tensor, v_out: torc
 
     tokens [n] int32 device; k_out/v_out [L, Hkv, n, hd] of the model dtype; h_root [L, d] fp32.
     """
+    need = _Args()
+    _check_weights(need, weights, need_lm_head=False)
+    need(tokens, "tokens", torch.int32, ndim=1)
+    n, L = int(tokens.numel()), len(weights.layers)
+    shape = weights.shape
+    dims = (L, shape.n_kv_heads, n, shape.head_dim)
+    need(k_out, "k_out", _model_dtype(shape), dims)
+    need(v_out, "v_out", _model_dtype(shape), dims)
+    need(h_root, "h_root", torch.float32, (L, shape.d_model))
+    need(workspace, "workspace", torch.uint8, ndim=1)
+    need.done()
     lib = load_library()
     w, layers_keepalive = _weights_struct(weights)
     st = lib.rksc_prefill(ctypes.byref(w), _ptr(tokens), int(tokens.numel()), _ptr(k_out), _ptr(v_out),
@@ -298,7 +382,11 @@ def rksc_prefill(weights, tokens: torch.Tensor, k_out: torch.Tensor, v_out: torc
 
 def rksc_asks_similarity(hidden: torch.Tensor, alpha: float, S: torch.Tensor, stream=None) -> None:
     """Marshal hidden [L, B, d] fp32 and S [B, B] fp32 device tensors into rksc_asks_similarity."""
+    need = _Args()
+    need(hidden, "hidden", torch.float32, ndim=3)
     L, B, d = hidden.shape
+    need(S, "S", torch.float32, (B, B))
+    need.done()
     _check(load_library().rksc_asks_similarity(_ptr(hidden), int(L), int(B), int(d), float(alpha), _ptr(S),
                                                _stream(stream)))
 
@@ -323,7 +411,13 @@ def rksc_test_gemm(A, W: torch.Tensor, splits: int = 0, stream=None, kind: int =
     else:
         a_hi, a_lo = A, None
         dt = RKSC_F32
+    need = _Args()
+    need(a_hi, "A", W.dtype, ndim=2)
     M, K = a_hi.shape
+    if a_lo is not None:
+        need(a_lo, "A_lo", torch.bfloat16, (M, K))
+    need(W, "W", None, (None, K))
+    need.done()
     N = W.shape[0]
     P = torch.empty((8, M, N), dtype=torch.float32, device=a_hi.device)
     used = ctypes.c_int32(0)
@@ -336,9 +430,19 @@ def rksc_test_attention(q, prefix_k, prefix_v, k_own, v_own, dtype, stream=None)
     """Kernel-level shared-prefix attention: q [B*s, H, hd], own [B, Hkv, s, hd] fp32; prefix [Hkv, n, hd]
     of `dtype` (torch.bfloat16 or torch.float32). Returns o [B*s, H*hd] as fp32 (bf16 hi/lo planes are
     recombined here for the bf16 path)."""
+    need = _Args()
+    need(q, "q", torch.float32, ndim=3)
     Ms, H, hd = q.shape
+    need(k_own, "k_own", torch.float32, ndim=4)
     B, Hkv, s, _ = k_own.shape
-    n = int(prefix_k.shape[1]) if prefix_k is not None else 0
+    need(k_own, "k_own", torch.float32, (B, Hkv, s, hd))
+    need(v_own, "v_own", torch.float32, (B, Hkv, s, hd))
+    n = 0
+    if prefix_k is not None:
+        need(prefix_k, "prefix_k", dtype, (Hkv, None, hd))
+        n = int(prefix_k.shape[1])
+        need(prefix_v, "prefix_v", dtype, (Hkv, n, hd))
+    need.done()
     dt = RKSC_BF16 if dtype == torch.bfloat16 else RKSC_F32
     o = torch.empty((Ms, H * hd), dtype=torch.float32, device=q.device)
     lib = load_library()
@@ -429,14 +533,30 @@ def rksc_decode_workspace_size(shape, n_branches: int, suffix_len: int, n_prefix
     return n
 
 
+def _check_decode_outputs(need, weights, cache, B, next_token, p_top, conf, workspace):
+    shape = weights.shape
+    dims = (len(weights.layers), B, shape.n_kv_heads, cache.capacity, shape.head_dim)
+    need(cache.k, "branch cache k", _model_dtype(shape), dims)
+    need(cache.v, "branch cache v", _model_dtype(shape), dims)
+    need(next_token, "next_token", torch.int32, (B,))
+    need(p_top, "p_top", torch.float32, (B,))
+    need(conf, "conf", torch.float32, (B,))
+    need(workspace, "workspace", torch.uint8, ndim=1)
+    need.done()
+
+
 def rksc_decode_suffix(weights, prefix_k, prefix_v, cache: BranchCache, suffix_tokens: torch.Tensor,
                        next_token: torch.Tensor, p_top: torch.Tensor, conf: torch.Tensor, workspace: torch.Tensor,
                        stream=None) -> None:
     """Marshal torch device tensors into rksc_decode_suffix (asynchronous on `stream`)."""
+    need = _Args()
+    _check_weights(need, weights)
+    n = _check_prefix(need, weights, prefix_k, prefix_v)
+    need(suffix_tokens, "suffix_tokens", torch.int32, ndim=2)
+    B, s = suffix_tokens.shape
+    _check_decode_outputs(need, weights, cache, B, next_token, p_top, conf, workspace)
     lib = load_library()
     w, layers_keepalive = _weights_struct(weights)
-    B, s = suffix_tokens.shape
-    n = int(prefix_k.shape[2]) if prefix_k is not None else 0
     kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
     st = lib.rksc_decode_suffix(ctypes.byref(w), ctypes.byref(kv), ctypes.byref(cache.struct), _ptr(suffix_tokens),
                                 int(B), int(s), _ptr(next_token), _ptr(p_top), _ptr(conf), _ptr(workspace),
@@ -449,9 +569,13 @@ def rksc_decode_step(weights, prefix_k, prefix_v, cache: BranchCache, tokens: to
                      next_token: torch.Tensor, p_top: torch.Tensor, conf: torch.Tensor, workspace: torch.Tensor,
                      stream=None) -> None:
     """Marshal torch device tensors into rksc_decode_step (asynchronous on `stream`)."""
+    need = _Args()
+    _check_weights(need, weights)
+    n = _check_prefix(need, weights, prefix_k, prefix_v)
+    need(tokens, "tokens", torch.int32, ndim=1)
+    _check_decode_outputs(need, weights, cache, int(tokens.numel()), next_token, p_top, conf, workspace)
     lib = load_library()
     w, layers_keepalive = _weights_struct(weights)
-    n = int(prefix_k.shape[2]) if prefix_k is not None else 0
     kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
     st = lib.rksc_decode_step(ctypes.byref(w), ctypes.byref(kv), ctypes.byref(cache.struct), _ptr(tokens),
                               int(tokens.numel()), _ptr(next_token), _ptr(p_top), _ptr(conf), _ptr(workspace),
@@ -463,6 +587,16 @@ def rksc_decode_step(weights, prefix_k, prefix_v, cache: BranchCache, tokens: to
 def rksc_cgee_gate(conf: torch.Tensor, n_steps: int, tau_conf: float, r_gap: float, p_mean: Optional[torch.Tensor],
                    fired: torch.Tensor, winner: torch.Tensor, stats: Optional[torch.Tensor], stream=None) -> None:
     """Marshal torch device tensors into rksc_cgee_gate (asynchronous on `stream`)."""
+    need = _Args()
+    need(conf, "conf", torch.float32, ndim=1)
+    B = int(conf.numel())
+    if p_mean is not None:
+        need(p_mean, "p_mean", torch.float32, (B,))
+    need(fired, "fired", torch.int32, (1,))
+    need(winner, "winner", torch.int32, (1,))
+    if stats is not None:
+        need(stats, "stats", torch.float32, (3,))
+    need.done()
     st = load_library().rksc_cgee_gate(_ptr(conf), int(conf.numel()), int(n_steps), float(tau_conf), float(r_gap),
                                        _ptr(p_mean), _ptr(fired), _ptr(winner), _ptr(stats), _stream(stream))
     _check(st)
@@ -583,11 +717,17 @@ class KVProbe:
     def decide(self, weights, prefix_tokens: torch.Tensor, suffix_tokens: torch.Tensor,
                workspace: Optional[torch.Tensor] = None, stream=None):
         """Returns (share: bool, times_ms [full, prefix, suffix], probed: bool)."""
+        need = _Args()
+        _check_weights(need, weights)
+        need(prefix_tokens, "prefix_tokens", torch.int32, ndim=1)
+        need(suffix_tokens, "suffix_tokens", torch.int32, ndim=2)
         B, s = suffix_tokens.shape
         n = int(prefix_tokens.numel())
         if workspace is None:
             workspace = torch.empty(self.workspace_size(weights.shape, n, B, s), dtype=torch.uint8,
                                     device=prefix_tokens.device)
+        need(workspace, "workspace", torch.uint8, ndim=1)
+        need.done()
         w, keep = _weights_struct(weights)
         share = ctypes.c_int32(0)
         probed = ctypes.c_int32(0)
@@ -619,9 +759,20 @@ def rksc_prefix_extend_workspace_size(shape, n_parent: int, n_new: int) -> int:
 def rksc_prefix_extend(weights, parent_k, parent_v, tokens: torch.Tensor, k_out: torch.Tensor, v_out: torch.Tensor,
                        h_node: Optional[torch.Tensor], workspace: torch.Tensor, stream=None) -> None:
     """Marshal torch device tensors into rksc_prefix_extend (asynchronous on `stream`)."""
+    need = _Args()
+    _check_weights(need, weights, need_lm_head=False)
+    n = _check_prefix(need, weights, parent_k, parent_v, "parent")
+    need(tokens, "tokens", torch.int32, ndim=1)
+    shape, L = weights.shape, len(weights.layers)
+    dims = (L, shape.n_kv_heads, n + int(tokens.numel()), shape.head_dim)
+    need(k_out, "k_out", _model_dtype(shape), dims)
+    need(v_out, "v_out", _model_dtype(shape), dims)
+    if h_node is not None:
+        need(h_node, "h_node", torch.float32, (L, shape.d_model))
+    need(workspace, "workspace", torch.uint8, ndim=1)
+    need.done()
     lib = load_library()
     w, keep = _weights_struct(weights)
-    n = int(parent_k.shape[2]) if parent_k is not None else 0
     kv = PrefixKV(n, _ptr(parent_k), _ptr(parent_v))
     st = lib.rksc_prefix_extend(ctypes.byref(w), ctypes.byref(kv), _ptr(tokens), int(tokens.numel()), _ptr(k_out),
                                 _ptr(v_out), _ptr(h_node), _ptr(workspace),
@@ -649,7 +800,13 @@ def prefix_extend(weights, parent_k, parent_v, tokens: torch.Tensor, stream=None
 def rksc_asks_gate(hidden: torch.Tensor, h_root: torch.Tensor, alpha: float, tau: float, sigma: torch.Tensor,
                    shared: torch.Tensor, stream=None) -> None:
     """Marshal torch device tensors into rksc_asks_gate (asynchronous on `stream`)."""
+    need = _Args()
+    need(hidden, "hidden", torch.float32, ndim=3)
     L, B, d = hidden.shape
+    need(h_root, "h_root", torch.float32, (L, d))
+    need(sigma, "sigma", torch.float32, (B,))
+    need(shared, "shared", torch.int32, (B,))
+    need.done()
     _check(load_library().rksc_asks_gate(_ptr(hidden), _ptr(h_root), L, B, d, float(alpha), float(tau), _ptr(sigma),
                                          _ptr(shared), _stream(stream)))
 

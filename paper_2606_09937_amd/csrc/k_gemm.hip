@@ -240,11 +240,12 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
   // DMA instruction j of this wave (ins = 8j + wid) fills rows 16 (ins % 16) ..
   // +15 of sub-tile ins / 16 = j / 2; lane L fills physical chunk L & 3 of row
   // L >> 2, i.e. logical chunk (L & 3) ^ ((L >> 4) & 3), the same for every j.
-  int rowoff[IPW];
+  // Row offsets in elements as size_t: rows x K passes 2^31 at large row counts.
+  size_t rowoff[IPW];
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
     const int row = ((j * kGemmWaves + wid) % 16) * 16 + (lane >> 2);
-    rowoff[j] = (j / 2 < 2 ? min(m0 + row, max_rows - 1) : min(n0 + row, N - 1)) * K;
+    rowoff[j] = (size_t)(j / 2 < 2 ? min(m0 + row, max_rows - 1) : min(n0 + row, N - 1)) * K;
   }
   const int ccol = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
   auto issue = [&](int step) {

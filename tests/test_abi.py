@@ -286,3 +286,66 @@ def test_asks_gate_rejects_unsupported_shapes(lib):
     U = rk.RKSC_ERR_UNSUPPORTED
     assert lib.rksc_asks_gate(FAKE, FAKE, 257, 4, 8, 1.5, 0.8, FAKE, FAKE, None) == U
     assert lib.rksc_asks_gate(FAKE, FAKE, 2, 4, 10, 1.5, 0.8, FAKE, FAKE, None) == U
+
+
+# ---- the Python binding checks dtype, shape and device before it hands a pointer to the library
+
+def _bf16_tiny():
+    import dataclasses
+    return dataclasses.replace(workloads.get("tiny").model, dtype="bf16")
+
+
+def _meta(shape, dtype):
+    import torch
+    return torch.empty(shape, dtype=dtype, device="meta")
+
+
+def test_marshal_rejects_wrong_dtype_shape_and_host_tensors(lib):
+    import torch
+    shape = _bf16_tiny()
+    mw = workloads.make_model(shape, seed=1)          # host tensors: rejected before any call
+    L, d, Hkv, hd = shape.n_layers, shape.d_model, shape.n_kv_heads, shape.head_dim
+    pk = _meta((L, Hkv, 8, hd), torch.bfloat16)
+    tok = _meta((2, 4), torch.int32)
+    ent, ex, ws = _meta((L, 2), torch.float32), _meta((2,), torch.int32), _meta((1 << 20,), torch.uint8)
+
+    def verify(**kw):
+        a = dict(weights=mw, prefix_k=pk, prefix_v=pk, branch_tokens=tok, tau=0.1, patience=1, entropy=ent,
+                 exit_layer=ex, hidden_last=None, workspace=ws)
+        a.update(kw)
+        with pytest.raises(ValueError) as e:
+            rk.rksc_verify_forward(**a)
+        return str(e.value)
+
+    assert "GPU" in verify()                                                  # host weights
+    mw_meta = workloads.ModelWeights(shape, _meta(mw.embed.shape, torch.bfloat16),
+                                     [{k: _meta(v.shape, v.dtype) for k, v in lw.items()} for lw in mw.layers],
+                                     _meta((d,), torch.float32), _meta(mw.lm_head.shape, torch.bfloat16))
+    assert "embed" in verify(weights=workloads.ModelWeights(shape, mw_meta.embed.float(), mw_meta.layers,
+                                                            mw_meta.final_norm, mw_meta.lm_head))
+    assert "prefix_k" in verify(weights=mw_meta, prefix_k=_meta((L, Hkv, 8, hd), torch.float32))
+    assert "prefix_k" in verify(weights=mw_meta, prefix_k=_meta((L, Hkv + 1, 8, hd), torch.bfloat16))
+    assert "prefix_v" in verify(weights=mw_meta, prefix_v=_meta((L, Hkv, 9, hd), torch.bfloat16))
+    assert "branch_tokens" in verify(weights=mw_meta, branch_tokens=_meta((2, 4), torch.int64))
+    assert "entropy" in verify(weights=mw_meta, entropy=_meta((L, 3), torch.float32))
+    assert "hidden_last" in verify(weights=mw_meta, hidden_last=_meta((L, 2, d), torch.bfloat16))
+    assert "GPU" in verify(weights=mw_meta)                                   # meta is not a GPU either
+    bad = [dict(lw) for lw in mw_meta.layers]
+    bad[1]["w_down"] = _meta((d, shape.d_ff + 8), torch.bfloat16)
+    assert "layer 1 w_down" in verify(weights=workloads.ModelWeights(shape, mw_meta.embed, bad, mw_meta.final_norm,
+                                                                     mw_meta.lm_head))
+
+    with pytest.raises(ValueError, match="hidden must be torch.float32"):
+        rk.rksc_asks_similarity(_meta((2, 3, 8), torch.bfloat16), 0.5, _meta((3, 3), torch.float32))
+    with pytest.raises(ValueError, match="S must have shape"):
+        rk.rksc_asks_similarity(_meta((2, 3, 8), torch.float32), 0.5, _meta((2, 2), torch.float32))
+    with pytest.raises(ValueError, match="GPU"):
+        rk.rksc_asks_similarity(torch.zeros((2, 3, 8)), 0.5, torch.zeros((3, 3)))
+    with pytest.raises(ValueError, match="tokens must be torch.int32"):
+        rk.rksc_prefill(mw_meta, _meta((8,), torch.int64), pk, pk, _meta((L, d), torch.float32), ws)
+    with pytest.raises(ValueError, match="h_root"):
+        rk.rksc_asks_gate(_meta((L, 2, d), torch.float32), _meta((L + 1, d), torch.float32), 1.5, 0.8,
+                          _meta((2,), torch.float32), _meta((2,), torch.int32))
+    with pytest.raises(ValueError, match="fired"):
+        rk.rksc_cgee_gate(_meta((4,), torch.float32), 3, 0.7, 0.06, None, _meta((1,), torch.int64),
+                          _meta((1,), torch.int32), None)

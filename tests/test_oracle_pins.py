@@ -646,8 +646,17 @@ def test_rsbcm_order_depth_ties_and_capacity():
     assert oracle.rsbcm_evict(blocks, 5)[1] == [] and oracle.rsbcm_evict([], 0) == ([], [])
 
 
-def test_rsbcm_brute_force_sorted():
-    """Evicting the argmin one at a time equals taking the size - N_max least (omega, insertion) keys."""
+def test_rsbcm_matches_one_at_a_time_eviction():
+    """Brute force of the algorithm's loop: while over capacity, recompute every omega and evict the
+    first least one. Its sequence equals the oracle's (omega, insertion) order."""
+    def one_at_a_time(blocks, cap):
+        table, ev = list(blocks), []
+        while len(table) > cap:
+            om = [s / (d + 1.0) for _, s, d in table]
+            j = min(range(len(table)), key=lambda i: (om[i], i))
+            ev.append(table.pop(j)[0])
+        return table, ev
+
     rng = np.random.default_rng(13)
     for _ in range(200):
         n = int(rng.integers(0, 40))
@@ -655,9 +664,9 @@ def test_rsbcm_brute_force_sorted():
                   for i in range(n)]
         cap = int(rng.integers(0, 45))
         kept, ev = oracle.rsbcm_evict(blocks, cap)
-        keys = sorted(range(n), key=lambda i: (blocks[i][1] / (blocks[i][2] + 1), i))
-        assert ev == [blocks[i][0] for i in keys[: max(0, n - cap)]]
-        assert sorted(b[0] for b in kept) == sorted(blocks[i][0] for i in keys[max(0, n - cap):])
+        kept_bf, ev_bf = one_at_a_time(blocks, cap)
+        assert ev == ev_bf
+        assert kept == kept_bf
 
 
 def test_kv_probe_paper_cost_table():
