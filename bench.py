@@ -105,15 +105,19 @@ def kernel_work(shape, B_live, n, s, win=1):
     M = B_live * s
     Nqkv = (H + 2 * Hkv) * hd
 
-    def gemm(N, K):
-        # weights + activation in + fp32 result out
-        return {"bytes": N * K * T + M * K * T + M * N * 4, "flops": 2.0 * M * N * K}
+    def gemm(N, K, out_bytes):
+        # What the method moves (not this library's split partials): the weights, the
+        # activation once in the storage type, and the method's output of the step.
+        return {"bytes": N * K * T + M * K * T + out_bytes, "flops": 2.0 * M * N * K}
 
     attn_flops = 4.0 * hd * H * B_live * (s * n + s * (s + 1) / 2)
     attn_bytes = 2 * Hkv * n * hd * T + B_live * 2 * Hkv * s * hd * T + 2 * M * H * hd * T
     return {
-        "qkv_proj": gemm(Nqkv, d), "o_proj": gemm(d, H * hd), "gate_up_proj": gemm(2 * F, d),
-        "down_proj": gemm(d, F), "attention": {"bytes": attn_bytes, "flops": attn_flops},
+        # q, k, v in the storage type; the O and down outputs are added to the fp32 residual;
+        # the gate|up step's output is the SwiGLU product [M, F]
+        "qkv_proj": gemm(Nqkv, d, M * Nqkv * T), "o_proj": gemm(d, H * hd, M * d * 4),
+        "gate_up_proj": gemm(2 * F, d, M * F * T), "down_proj": gemm(d, F, M * d * 4),
+        "attention": {"bytes": attn_bytes, "flops": attn_flops},
         # W_lm once, the hi+lo bf16 normalised rows, the per-workgroup statistics
         "lm_head_entropy": {"bytes": V * d * T + B_live * win * d * 4, "flops": 2.0 * B_live * win * V * d},
     }
@@ -252,14 +256,40 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": COPY_BYTES, "copy_bytes_written": COPY_BYTES, "launches": 3}))
 
 
-def cpu_baseline(mw, kv, toks, wl, layers):
-    """Float64 oracle on the first `layers` layers of the same workload; time scaled to all layers."""
+def cpu_model():
+    """The host CPU's model name and the cores this process may run on."""
+    name = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    return name, avail
+
+
+def blas_threads():
+    from threadpoolctl import threadpool_info
+    return max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+
+
+def cpu_baseline(mw, kv, toks, wl, layers, branches=None):
+    """Float64 oracle on the first `layers` layers (and the first `branches` branches) of the
+    same workload; the time is scaled to all layers and all branches (branches are independent
+    given the prefix, and every layer costs the same)."""
     import dataclasses
 
     import oracle
-    from threadpoolctl import threadpool_info
 
     shape = mw.shape
+    B = wl.n_branches
+    nb = B if branches is None else min(branches, B)
     sub = dataclasses.replace(shape, n_layers=layers)
 
     class Host:
@@ -271,20 +301,47 @@ def cpu_baseline(mw, kv, toks, wl, layers):
     host.final_norm = mw.final_norm.cpu()
     host.lm_head = mw.lm_head.cpu()
     pk, pv = kv.k[:layers].cpu(), kv.v[:layers].cpu()
-    t_np = toks.cpu().numpy()
+    t_np = toks.cpu().numpy()[:nb]
     t0 = time.perf_counter()
     oracle.verify_forward(host, sub, pk, pv, t_np, wl.tau, wl.patience)
     dt = time.perf_counter() - t0
-    per_step = dt * shape.n_layers / layers
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    tokens = wl.n_branches * wl.branch_len
+    scale = (shape.n_layers / layers) * (B / nb)
+    per_step = dt * scale
+    tokens = B * wl.branch_len
+    exact = layers == shape.n_layers and nb == B
     return {
-        "value": tokens / per_step, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+        "value": tokens / per_step, "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
+        "extrapolated": not exact,
         "sample": (f"float64 oracle verify pass over {'all' if layers == shape.n_layers else f'the first {layers} of'} "
-                   f"{shape.n_layers} layers of the same workload ({wl.n_branches} branch(es) x {wl.branch_len} tokens, "
-                   f"{kv.k.shape[2]}-token prefix), {dt:.1f} s"
-                   + ("" if layers == shape.n_layers else f", time scaled by {shape.n_layers}/{layers}")),
+                   f"{shape.n_layers} layers and {'all' if nb == B else f'{nb} of the'} {B} branch(es) of "
+                   f"{wl.name} ({wl.branch_len} tokens each, {kv.k.shape[2]}-token prefix), {dt:.1f} s"
+                   + ("" if exact else f"; time scaled by {scale:g} (layers x branches)")),
+        "sample_seconds": dt,
     }
+
+
+def cpu_single_thread_tiny(seed):
+    """The oracle on the tiny workload (2 layers, 4 branches x 16 tokens over 64 prefix tokens)
+    with BLAS limited to one thread: tokens/s."""
+    import oracle
+    import workloads
+    from threadpoolctl import threadpool_limits
+
+    wl = workloads.get("tiny")
+    shape = wl.model
+    mw = workloads.make_model(shape, seed=seed)
+    kv = workloads.make_prefix_kv(shape, wl.prefix_len, seed=seed)
+    toks = workloads.make_tokens(wl.n_branches * wl.branch_len, shape.vocab, seed=seed).reshape(
+        wl.n_branches, wl.branch_len).numpy()
+    with threadpool_limits(1):
+        oracle.verify_forward(mw, shape, kv.k, kv.v, toks, wl.tau, wl.patience)   # warm
+        reps, t0 = 0, time.perf_counter()
+        while reps < 3 or time.perf_counter() - t0 < 1.0:
+            oracle.verify_forward(mw, shape, kv.k, kv.v, toks, wl.tau, wl.patience)
+            reps += 1
+        dt = (time.perf_counter() - t0) / reps
+    return {"workload": "tiny", "value": wl.n_branches * wl.branch_len / dt, "unit": "tokens/s", "cores": 1,
+            "ms_per_call": dt * 1e3, "calls": reps}
 
 
 def measure_decode(mw, kv, shape, n, args, hip, sp, stream, dev):
@@ -492,6 +549,152 @@ def measure_asks(shape, args, hip, sp, stream, dev):
     return out
 
 
+# The other configurations of the verify pass, each timed in the default run
+# after the headline (one record each): the tree of thoughts, the large
+# vocabulary, the long prefix and its one-token decode regime.
+CONFIG_RECORDS = ("7b_tot", "7b_large_vocab", "10b_long", "10b_decode")
+PROJECTIONS = ("qkv_proj", "o_proj", "gate_up_proj", "down_proj")
+
+
+def class_roof(work, avg_us, dtype):
+    """One kernel class against its binding roof: MFMA when its algorithmic intensity is
+    above the bf16 ridge (2.5 PFLOP/s / 8 TB/s = 312 flop/B), else HBM."""
+    sec = avg_us * 1e-6
+    gbs = work["bytes"] / sec / 1e9
+    tf = work["flops"] / sec / 1e12
+    peak = BF16_PEAK_TFLOPS if dtype == "bf16" else FP32_PEAK_TFLOPS
+    mfma = work["flops"] / work["bytes"] > BF16_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3
+    return {"avg_us": avg_us, "hbm_gbs": gbs, "hbm_frac": gbs / HBM_PEAK_GBS, "tflops": tf, "mfma_frac": tf / peak,
+            "bound": "mfma" if mfma else "hbm", "frac": tf / peak if mfma else gbs / HBM_PEAK_GBS,
+            "algorithmic_bytes": work["bytes"], "algorithmic_flops": work["flops"]}
+
+
+def event_arrays(hip, L, k_steps, slots, stream_layers):
+    """HIP events for k_steps profiled calls at the given per-layer slots (the lm_head slots only
+    at the layers where the stream runs). Returns (events, per-call host arrays)."""
+    per_step = 12 * L
+    evs = hip.create(per_step * k_steps, fenced=False)
+    ptrs = []
+    for k in range(k_steps):
+        arr = (ctypes.c_void_p * per_step)()
+        for l in range(L):
+            for sl in slots:
+                if sl in (EVENT_SLOTS["lm_head_entropy"], EVENT_SLOTS["lm_head_entropy"] + 1) and \
+                        l not in stream_layers:
+                    continue
+                arr[12 * l + sl] = evs[k * per_step + 12 * l + sl]
+        ptrs.append(ctypes.cast(arr, ctypes.c_void_p))
+        ptrs[-1]._keep = arr
+    return evs, ptrs
+
+
+def measure_workload(name, args, hip, dev):
+    """One configuration of the verify pass: ms per call at its (tau, patience) and at tau = 0
+    (full depth), each the median of `reps` calls timed with HIP events; the per-class kernel
+    times from a profiled full-depth call; each class against its binding roof; and the
+    projections' algorithmic MFMA fraction over their summed time."""
+    import torch
+
+    import paper_2606_09937_amd as rk
+    import workloads
+
+    wl = workloads.get(name)
+    shape = wl.model
+    B, n, s, L = wl.n_branches, wl.prefix_len, wl.branch_len, shape.n_layers
+    t0 = time.perf_counter()
+    mw = workloads.make_model(shape, seed=args.seed, device=dev)
+    kv = workloads.make_prefix_kv(shape, n, seed=args.seed, device=dev)
+    toks = workloads.make_tokens(B * s, shape.vocab, seed=args.seed, device=dev).reshape(B, s).contiguous()
+    ws = torch.empty(rk.rksc_verify_workspace_size(shape, B, s, n), dtype=torch.uint8, device=dev)
+    ent = torch.empty((L, B), dtype=torch.float32, device=dev)
+    ex = torch.empty((B,), dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    lib = rk.load_library()
+    w_struct, keep = rk._weights_struct(mw)
+    kv_struct = rk.PrefixKV(n, rk._ptr(kv.k), rk._ptr(kv.v))
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    common = (ctypes.byref(w_struct), ctypes.byref(kv_struct), rk._ptr(toks), B, s)
+
+    def call(tau, patience, events=None):
+        if events is None:
+            st = lib.rksc_verify_forward(*common, float(tau), int(patience), rk._ptr(ent), rk._ptr(ex), None,
+                                         rk._ptr(ws), ws.numel(), sp)
+        else:
+            st = lib.rksc_verify_forward_profiled(*common, float(tau), int(patience), rk._ptr(ent), rk._ptr(ex),
+                                                  None, rk._ptr(ws), ws.numel(), sp, events)
+        if st != 0:
+            raise RuntimeError(f"rksc_verify_forward failed at {name}: {rk.rksc_last_error()}")
+
+    call(wl.tau, wl.patience)
+    torch.cuda.synchronize()
+    reps = 3
+
+    def timed(tau, patience):
+        out = []
+        for _ in range(reps):
+            a, b = hip.create(2)
+            hip.lib.hipEventRecord(ctypes.c_void_p(a), sp)
+            call(tau, patience)
+            hip.lib.hipEventRecord(ctypes.c_void_p(b), sp)
+            torch.cuda.synchronize()
+            out.append(hip.elapsed_ms(a, b))
+            hip.destroy([a, b])
+        return sorted(out)[len(out) // 2]
+
+    ms_tau = timed(wl.tau, wl.patience)
+    exits = ex.cpu().tolist()
+    ms_full = timed(0.0, 1)
+
+    # Per-class times from one profiled full-depth call (every layer live).
+    win = rk.rksc_verify_window(B)
+    stream_layers = [l for l in range(L) if l % win == win - 1 or l == L - 1]
+    slots = sorted(set(v for s0 in EVENT_SLOTS.values() for v in (s0, s0 + 1)))
+    evs, ptrs = event_arrays(hip, L, 1, slots, stream_layers)
+    call(0.0, 1, ptrs[0])
+    torch.cuda.synchronize()
+    work = kernel_work(shape, B, n, s, win)
+    kernels = {}
+    for cls, slot in EVENT_SLOTS.items():
+        ls = stream_layers if cls == "lm_head_entropy" else range(L)
+        d = [hip.elapsed_ms(evs[12 * l + slot], evs[12 * l + slot + 1]) for l in ls]
+        rec = class_roof(work[cls], sum(d) / len(d) * 1e3, shape.dtype)
+        rec["launches_per_call"] = len(d)
+        rec["us_per_call"] = sum(d) * 1e3
+        kernels[cls] = rec
+    hip.destroy(evs)
+    g_us = sum(kernels[c]["us_per_call"] for c in PROJECTIONS)
+    g_flops = sum(work[c]["flops"] * kernels[c]["launches_per_call"] for c in PROJECTIONS)
+    peak = BF16_PEAK_TFLOPS if shape.dtype == "bf16" else FP32_PEAK_TFLOPS
+    dom = max(kernels, key=lambda k: kernels[k]["us_per_call"])
+    rec = {
+        "workload": name, "description": wl.description, "n_branches": B, "prefix_len": n, "branch_len": s,
+        "layers": L, "tau": wl.tau, "patience": wl.patience, "exit_window": win,
+        "ms_per_call": ms_tau, "tokens_per_s": B * s / (ms_tau / 1e3), "exit_layers": exits,
+        "full_depth": {"ms_per_call": ms_full, "tokens_per_s": B * s / (ms_full / 1e3)},
+        "calls_timed": reps,
+        "kernels": kernels,
+        "dominant": dom,
+        "roofline": {"kernel": dom, "bound": kernels[dom]["bound"], "frac": kernels[dom]["frac"]},
+        "projections": {"us_per_call": g_us, "algorithmic_tflops": g_flops / (g_us * 1e-6) / 1e12,
+                        "mfma_frac": g_flops / (g_us * 1e-6) / 1e12 / peak},
+    }
+    log(f"{name}: {ms_tau:.2f} ms/call ({rec['tokens_per_s']:.0f} tokens/s, exits {sorted(set(exits))}), full depth "
+        f"{ms_full:.2f} ms; projections {rec['projections']['mfma_frac']:.3f} of bf16 peak, attention "
+        f"{kernels['attention']['avg_us']:.0f} us/layer ({kernels['attention']['bound']} "
+        f"{kernels['attention']['frac']:.3f}), lm_head {kernels['lm_head_entropy']['hbm_frac']:.3f} of HBM "
+        f"[{time.perf_counter() - t0:.1f} s]")
+    cpu = None
+    if args.cpu_extrapolate:
+        cpu = cpu_baseline(mw, kv, toks, wl, min(2, L), branches=2)
+        log(f"{name}: cpu oracle {cpu['value']:.4f} tokens/s extrapolated ({cpu['sample_seconds']:.1f} s sample)")
+    rec["cpu_baseline"] = cpu
+    del mw, kv, toks, ws, ent, ex, keep
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -504,6 +707,12 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=0,
                     help="layers in the oracle's sample (0: all layers, the whole verify pass)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the records of the other configurations (7b_tot, 7b_large_vocab, 10b_long, 10b_decode)")
+    ap.add_argument("--configs", default=",".join(CONFIG_RECORDS),
+                    help="comma-separated configurations to record after the headline")
+    ap.add_argument("--no-cpu-extrapolate", dest="cpu_extrapolate", action="store_false",
+                    help="skip the oracle's 2-branch, 2-layer samples of the other configurations")
     ap.add_argument("--no-full-depth", action="store_true")
     ap.add_argument("--no-tau-sweep", action="store_true")
     ap.add_argument("--no-prefill", action="store_true", help="skip the root-forward (prefill) timing")
@@ -774,7 +983,26 @@ def main():
         cpu_layers = L if args.cpu_layers <= 0 else min(args.cpu_layers, L)
         log(f"cpu baseline: oracle on {cpu_layers} layer(s)")
         cpu = cpu_baseline(mw, kv, toks, wl, cpu_layers)
-        log(f"cpu baseline: {cpu['value']:.3f} tokens/s on {cpu['cores']} threads")
+        name_cpu, avail = cpu_model()
+        cpu["cpu_model"] = name_cpu
+        cpu["cores_available"] = avail
+        cpu["single_thread_tiny"] = cpu_single_thread_tiny(args.seed)
+        log(f"cpu baseline: {cpu['value']:.3f} tokens/s on {cpu['cores']} threads ({name_cpu}, {avail} cores "
+            f"available); tiny on one thread {cpu['single_thread_tiny']['value']:.0f} tokens/s")
+
+    # The other configurations, one record each (their models replace the headline's in HBM).
+    configs = None
+    if not args.no_configs and args.configs:
+        del mw, kv, toks, ws, keep, w_struct
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        configs = {}
+        for cname in [c for c in args.configs.split(",") if c]:
+            configs[cname] = measure_workload(cname, args, hip, dev)
+        if cpu is not None:
+            cpu["extrapolated_configs"] = {k: v["cpu_baseline"] for k, v in configs.items() if v["cpu_baseline"]}
+            for v in configs.values():
+                v.pop("cpu_baseline", None)
 
     out = {
         "metric": METRIC,
@@ -809,6 +1037,7 @@ def main():
         "tree": tree,
         "asks_similarity": asks,
         "cpu_baseline": cpu,
+        "configs": configs,
     }
     print(json.dumps(out), flush=True)
 

@@ -39,6 +39,18 @@ rksc_status rksc_test_gemm_kind(int32_t dtype, const void* A, const void* A_lo, 
                                 int32_t M, int32_t N, int32_t K, int32_t splits, int32_t kind,
                                 int32_t* splits_used, void* stream);
 
+/* rksc_test_gemm_kind with a shrunken live set, as after branch exits in the
+ * verify pass (Alg. VerifyWithEntropyExit; Sec. 2.3 "Layer-level entropy
+ * exit"): the kernels are launched for M rows (the plan of an M-row call), but
+ * a control block in `ctrl_scratch` (a device buffer of at least 4096 bytes,
+ * overwritten) says that only live_count branches of branch_len rows are live,
+ * so only rows m < live_count * branch_len of P are written; the other rows
+ * of P are left as they were. Requires 1 <= live_count <= RKSC_MAX_BRANCHES,
+ * branch_len >= 1 and live_count * branch_len <= M. */
+rksc_status rksc_test_gemm_live(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P, int32_t M,
+                                int32_t N, int32_t K, int32_t splits, int32_t kind, int32_t live_count,
+                                int32_t branch_len, void* ctrl_scratch, int32_t* splits_used, void* stream);
+
 /* The plan rksc_test_gemm_kind would launch for this shape, without launching
  * anything (host only): plan[0..4] = kernel kind (0, 1 or 2 as above), rows
  * and columns of a workgroup's output tile, number of K splits, K elements per
@@ -79,6 +91,37 @@ rksc_status rksc_verify_forward_profiled(const rksc_weights* weights, const rksc
                                          float tau, int32_t patience, float* entropy, int32_t* exit_layer,
                                          float* hidden_last, void* workspace, size_t workspace_bytes,
                                          void* stream, void* const* events);
+
+/* Precision ablation of the verify pass (Eq. entropy is the quantity the
+ * ablation is judged on): rksc_verify_forward with the fp32 value at chosen
+ * operand sites carried at bf16 precision instead of as a bf16 hi + lo pair.
+ * drop_mask is an OR of the RKSC_DROP_* bits:
+ *   QKV_LO, O_LO, GATE_UP_LO, DOWN_LO   the lo plane of that projection's
+ *                                       activation is zeroed (bf16 hi alone);
+ *   Q_LO, OWN_KV_LO                     the queries / the branch's own keys and
+ *                                       values are rounded to bf16 before the
+ *                                       attention;
+ *   P_LO                                the attention probabilities enter P.V
+ *                                       as bf16 alone;
+ *   LM_HEAD_LO                          the final-normed rows meet W_lm as bf16
+ *                                       alone.
+ * bf16 models only (RKSC_ERR_UNSUPPORTED otherwise); drop_mask = 0 is
+ * rksc_verify_forward. For measuring which sites the error bars need, not for
+ * production use. */
+#define RKSC_DROP_QKV_LO 0x01u
+#define RKSC_DROP_O_LO 0x02u
+#define RKSC_DROP_GATE_UP_LO 0x04u
+#define RKSC_DROP_DOWN_LO 0x08u
+#define RKSC_DROP_Q_LO 0x10u
+#define RKSC_DROP_OWN_KV_LO 0x20u
+#define RKSC_DROP_P_LO 0x40u
+#define RKSC_DROP_LM_HEAD_LO 0x80u
+#define RKSC_DROP_ALL 0xffu
+rksc_status rksc_test_verify_precision(const rksc_weights* weights, const rksc_prefix_kv* prefix_kv,
+                                       const int32_t* branch_tokens, int32_t n_branches, int32_t branch_len,
+                                       float tau, int32_t patience, float* entropy, int32_t* exit_layer,
+                                       float* hidden_last, void* workspace, size_t workspace_bytes, void* stream,
+                                       uint32_t drop_mask);
 
 #ifdef __cplusplus
 }

@@ -23,7 +23,7 @@ __all__ = [
     "RkscError", "load_library", "library_path",
     "rksc_abi_version", "rksc_verify_workspace_size", "rksc_verify_forward", "rksc_verify_window",
     "rksc_asks_similarity", "rksc_status_string", "rksc_last_error",
-    "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_gemm_plan", "rksc_test_attention",
+    "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_gemm_live", "rksc_test_gemm_plan", "rksc_test_attention",
     "verify_forward", "asks_similarity", "prefill", "rksc_prefill", "rksc_prefill_workspace_size", "model_config",
     "BranchCache", "Decoder", "rksc_decode_workspace_size", "rksc_decode_suffix", "rksc_decode_step",
     "rksc_cgee_gate", "cgee_gate", "RKSC_ABI_VERSION", "BlockTable", "KVProbe",
@@ -109,6 +109,9 @@ def load_library():
     lib.rksc_verify_forward.restype = i32
     lib.rksc_verify_forward.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32, i32,
                                         vp, vp, vp, vp, sz, vp]
+    lib.rksc_test_verify_precision.restype = i32
+    lib.rksc_test_verify_precision.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32,
+                                               i32, vp, vp, vp, vp, sz, vp, ctypes.c_uint32]
     lib.rksc_verify_window.restype = i32
     lib.rksc_verify_window.argtypes = [i32]
     lib.rksc_verify_forward_window.restype = i32
@@ -173,6 +176,9 @@ def load_library():
     lib.rksc_test_gemm.argtypes = [i32, vp, vp, vp, vp, i32, i32, i32, i32, ctypes.POINTER(i32), vp]
     lib.rksc_test_gemm_kind.restype = i32
     lib.rksc_test_gemm_kind.argtypes = [i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, ctypes.POINTER(i32), vp]
+    lib.rksc_test_gemm_live.restype = i32
+    lib.rksc_test_gemm_live.argtypes = [i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp,
+                                        ctypes.POINTER(i32), vp]
     lib.rksc_test_gemm_plan.restype = i32
     lib.rksc_test_gemm_plan.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(i32)]
     lib.rksc_test_attention.restype = i32
@@ -346,6 +352,36 @@ def rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, 
     _check(st)
 
 
+# Operand sites of the precision ablation (rksc_test_verify_precision).
+RKSC_DROP = {"qkv": 0x01, "o": 0x02, "gate_up": 0x04, "down": 0x08, "q": 0x10, "own_kv": 0x20, "p": 0x40,
+             "lm_head": 0x80}
+
+
+def rksc_test_verify_precision(weights, prefix_k, prefix_v, branch_tokens, tau: float, patience: int,
+                               drop_mask: int, stream=None):
+    """The verify pass with the chosen operand sites at bf16 precision (RKSC_DROP bits); returns
+    (entropy [L, B], exit_layer [B], hidden_last [L, B, d]) device tensors."""
+    need = _Args()
+    _check_weights(need, weights)
+    n = _check_prefix(need, weights, prefix_k, prefix_v)
+    need(branch_tokens, "branch_tokens", torch.int32, ndim=2)
+    need.done()
+    B, s = branch_tokens.shape
+    L, d, dev = len(weights.layers), weights.shape.d_model, branch_tokens.device
+    ws = torch.empty(rksc_verify_workspace_size(weights.shape, B, s, n), dtype=torch.uint8, device=dev)
+    ent = torch.empty((L, B), dtype=torch.float32, device=dev)
+    ex = torch.empty((B,), dtype=torch.int32, device=dev)
+    hid = torch.empty((L, B, d), dtype=torch.float32, device=dev)
+    w, keep = _weights_struct(weights)
+    kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
+    _check(load_library().rksc_test_verify_precision(ctypes.byref(w), ctypes.byref(kv), _ptr(branch_tokens), int(B),
+                                                     int(s), float(tau), int(patience), _ptr(ent), _ptr(ex),
+                                                     _ptr(hid), _ptr(ws), ws.numel(), _stream(stream),
+                                                     int(drop_mask)))
+    del keep
+    return ent, ex, hid
+
+
 def rksc_prefill_workspace_size(shape, n_prefix: int) -> int:
     cfg = model_config(shape)
     n = int(load_library().rksc_prefill_workspace_size(ctypes.byref(cfg), n_prefix))
@@ -424,6 +460,34 @@ def rksc_test_gemm(A, W: torch.Tensor, splits: int = 0, stream=None, kind: int =
     _check(load_library().rksc_test_gemm_kind(dt, _ptr(a_hi), _ptr(a_lo), _ptr(W), _ptr(P), M, N, K, splits,
                                               kind, ctypes.byref(used), _stream(stream)))
     return P[: used.value]
+
+
+def rksc_test_gemm_live(A, W: torch.Tensor, live_count: int, branch_len: int, P: torch.Tensor, splits: int = 0,
+                        kind: int = -1, stream=None) -> int:
+    """rksc_test_gemm_kind with only live_count * branch_len of the M rows live (a control block
+    as after branch exits). P [8, M, N] fp32 is written in the live rows only; returns the
+    number of splits used."""
+    if W.dtype == torch.bfloat16:
+        a_hi, a_lo = A
+        dt = RKSC_BF16
+    else:
+        a_hi, a_lo = A, None
+        dt = RKSC_F32
+    need = _Args()
+    need(a_hi, "A", W.dtype, ndim=2)
+    M, K = a_hi.shape
+    if a_lo is not None:
+        need(a_lo, "A_lo", torch.bfloat16, (M, K))
+    need(W, "W", None, (None, K))
+    N = W.shape[0]
+    need(P, "P", torch.float32, (8, M, N))
+    need.done()
+    ctrl = torch.empty(4096, dtype=torch.uint8, device=a_hi.device)
+    used = ctypes.c_int32(0)
+    _check(load_library().rksc_test_gemm_live(dt, _ptr(a_hi), _ptr(a_lo), _ptr(W), _ptr(P), M, N, K, splits, kind,
+                                              int(live_count), int(branch_len), _ptr(ctrl), ctypes.byref(used),
+                                              _stream(stream)))
+    return used.value
 
 
 def rksc_test_attention(q, prefix_k, prefix_v, k_own, v_own, dtype, stream=None):

@@ -102,7 +102,9 @@ __device__ __forceinline__ void lds_wait_pairs(shortx4 (&a)[ND], shortx4 (&b)[ND
 // log2(e)/sqrt(hd) before their hi/lo split, and the partial maxima in mlpart
 // are in the same units.
 // 8 waves x 16 query columns = 128 query rows per workgroup.
-template <int HD, bool XB>
+// PS: the probabilities meet V as a bf16 hi/lo pair (two MFMAs); without it, as
+// bf16(p) alone (one MFMA, ~2^-9 relative rounding of each weight).
+template <int HD, bool XB, bool PS = true>
 __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, const bf16* __restrict__ pk,
                                                    const bf16* __restrict__ pv, const float* __restrict__ ko,
                                                    const float* __restrict__ vo, void* __restrict__ o,
@@ -354,11 +356,17 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     for (int kb = 0; kb < 2; ++kb) {
       // hi/lo split of the probabilities, two at a time: hi = bf16(p) packed
       // by one conversion, lo = bf16(p - hi) likewise.
-      uint32_t ph[4], pl[4];
+      uint32_t ph[4], pl[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
       for (int e2 = 0; e2 < 4; ++e2) {
         const float p0 = p[2 * kb + (e2 >> 1)][2 * (e2 & 1)], p1 = p[2 * kb + (e2 >> 1)][2 * (e2 & 1) + 1];
-        split2x2(p0, p1, ph[e2], pl[e2]);
+        if constexpr (PS) {
+          split2x2(p0, p1, ph[e2], pl[e2]);
+        } else {
+          typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+          typedef float floatx2_t __attribute__((ext_vector_type(2)));
+          ph[e2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2_t{p0, p1}, bf16x2_t));
+        }
       }
       const bf16x8 pbh = __builtin_bit_cast(bf16x8, make_uint4(ph[0], ph[1], ph[2], ph[3]));
       const bf16x8 pbl = __builtin_bit_cast(bf16x8, make_uint4(pl[0], pl[1], pl[2], pl[3]));
@@ -379,7 +387,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
           v0 = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vlo[dt], vhi[dt], 0, 1, 2, 3, 4, 5, 6, 7));
         }
         oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, pbh, oacc[dt], 0, 0, 0);
-        oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, pbl, oacc[dt], 0, 0, 0);
+        if constexpr (PS) oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, pbl, oacc[dt], 0, 0, 0);
         if constexpr (OWN) {
           const int dim = 16 * dt + r16;
           const bf16x8 v1 = *reinterpret_cast<const bf16x8*>(&Vt1[dim * LDV + vt_col(dim, 32 * kb + 4 * g)]);
@@ -955,9 +963,21 @@ hipError_t launch_attention_decode(DType dt, const AttnPlan& p, const void* q, c
   return hipGetLastError();
 }
 
+namespace {
+// k_attn_bf16 with the probabilities split into hi/lo (p_split) or not.
+template <int HD, bool XB, typename... Args>
+void launch_attn_tiles(bool p_split, dim3 grid, hipStream_t st, Args... args) {
+  if (p_split)
+    hipLaunchKernelGGL((k_attn_bf16<HD, XB, true>), grid, dim3(64 * kAttnWaves), 0, st, args...);
+  else
+    hipLaunchKernelGGL((k_attn_bf16<HD, XB, false>), grid, dim3(64 * kAttnWaves), 0, st, args...);
+}
+}  // namespace
+
 hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,
                             const void* k_own, const void* v_own, void* o, float* opart, float* mlpart,
-                            const Ctrl* c, int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st) {
+                            const Ctrl* c, int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st,
+                            bool p_split) {
   if (dt == DType::BF16) {
     const float sl2 = 1.4426950408889634f / sqrtf((float)hd);
     const int G = H / Hkv;
@@ -972,10 +992,10 @@ hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const vo
       const dim3 grid((max_rows * G + 16 * kAttnWaves - 1) / (16 * kAttnWaves), Hkv, p.chunks);
       if (p.chunks > 0) {
         if (hd == 128)
-          hipLaunchKernelGGL((k_attn_bf16<128, true>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
+          launch_attn_tiles<128, true>(p_split, grid, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
                              c, n, s, H, Hkv, sl2, p.chunks, max_rows);
         else
-          hipLaunchKernelGGL((k_attn_bf16<64, true>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
+          launch_attn_tiles<64, true>(p_split, grid, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
                              c, n, s, H, Hkv, sl2, p.chunks, max_rows);
       }
       if (hd == 128)
@@ -988,10 +1008,10 @@ hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const vo
     }
     const dim3 grid((G * s + 16 * kAttnWaves - 1) / (16 * kAttnWaves), Hkv, max_branches * p.chunks);
     if (hd == 128)
-      hipLaunchKernelGGL((k_attn_bf16<128, false>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
+      launch_attn_tiles<128, false>(p_split, grid, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
                          n, s, H, Hkv, sl2, p.chunks, max_rows);
     else
-      hipLaunchKernelGGL((k_attn_bf16<64, false>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
+      launch_attn_tiles<64, false>(p_split, grid, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
                          n, s, H, Hkv, sl2, p.chunks, max_rows);
     if (p.chunks > 1) {
       if (hd == 128)

@@ -499,6 +499,19 @@ hipError_t launch_cgee_gate(const float* conf, int B, int n_steps, float tau_con
   return hipGetLastError();
 }
 
+namespace {
+__global__ void k_round_bf16(float* x, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    x[i] = bf16_to_f32(f32_to_bf16_bits(x[i]));
+}
+}  // namespace
+
+hipError_t launch_round_bf16(float* x, size_t n, hipStream_t st) {
+  const size_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(k_round_bf16, dim3(blocks < 4096 ? (blocks > 0 ? blocks : 1) : 4096), dim3(256), 0, st, x, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_unit_rows(float* x, int rows, int d, hipStream_t st) {
   hipLaunchKernelGGL(k_unit_rows, dim3(rows), dim3(256), 0, st, x, d);
   return hipGetLastError();

@@ -96,9 +96,13 @@ struct AttnPlan {
   bool cross;
 };
 AttnPlan plan_attention(DType dt, int B, int n, int s, int H, int Hkv);
+// p_split = false: the probabilities enter P.V as bf16 alone instead of a hi/lo pair.
 hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,
                             const void* k_own, const void* v_own, void* o, float* opart, float* mlpart,
-                            const Ctrl* c, int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st);
+                            const Ctrl* c, int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st,
+                            bool p_split = true);
+// x[i] = fp32(bf16(x[i])) for i < n: the value rounded to bf16 precision, kept in fp32.
+hipError_t launch_round_bf16(float* x, size_t n, hipStream_t st);
 
 // ---- entropy of the live branches' last-token logits
 int entropy_parts(DType dt, int V, int max_branches);

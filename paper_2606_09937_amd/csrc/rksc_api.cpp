@@ -184,7 +184,7 @@ namespace {
 rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const int32_t* branch_tokens,
                         int32_t n_branches, int32_t branch_len, float tau, int32_t patience, float* entropy,
                         int32_t* exit_layer, float* hidden_last, void* workspace, size_t workspace_bytes,
-                        void* stream, void* const* events, int32_t window) {
+                        void* stream, void* const* events, int32_t window, uint32_t drop = 0) {
   if (!w) return fail(RKSC_ERR_INVALID_ARGUMENT, "weights is NULL");
   if (!kv) return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix_kv is NULL");
   if (!branch_tokens) return fail(RKSC_ERR_INVALID_ARGUMENT, "branch_tokens is NULL");
@@ -246,6 +246,12 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
   auto plane_lo = [&](float* buf, size_t elems) -> const void* {
     return dt == DType::BF16 ? static_cast<const void*>(reinterpret_cast<const uint16_t*>(buf) + elems) : nullptr;
   };
+  // Precision ablation (test hook only): zero the lo plane of a projection input of
+  // `elems` elements per plane, so that the projection sees the bf16 hi part alone.
+  if (drop && dt != DType::BF16) return fail(RKSC_ERR_UNSUPPORTED, "the precision ablation needs a bf16 model");
+  auto drop_lo = [&](float* buf, size_t elems) -> hipError_t {
+    return hipMemsetAsync(reinterpret_cast<uint16_t*>(buf) + elems, 0, elems * 2, strm);
+  };
 
   HIP_TRY(rksc::launch_init(ctrl, B, L, entropy, exit_layer, hidden_last, (size_t)L * B * d, strm));
   HIP_TRY(rksc::launch_rope_table(rope, s, n, hd, (double)c->rope_base, strm));
@@ -278,6 +284,7 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     }
     HIP_TRY(rksc::launch_add_norm(dt, x_prev, pres, l == 0 ? 0 : lay.down.splits, res_stride, l % win == 0, ctrl,
                                   s, x_cur, act, lw.attn_norm, d, c->rms_eps, M, strm, tap));
+    if (drop & RKSC_DROP_QKV_LO) HIP_TRY(drop_lo(act, (size_t)M * d));
     HIP_TRY(mark(l, 0));
     // Projection inputs: bf16 planes hi = act[0, M*K), lo = act[M*K, 2*M*K) for BF16 models.
     HIP_TRY(rksc::launch_gemm(dt, lay.qkv, act, plane_lo(act, (size_t)M * d), lw.w_qkv, pbig, (size_t)M * Nqkv, ctrl,
@@ -285,11 +292,17 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     HIP_TRY(mark(l, 1));
     HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
                                   vown, M, strm));
+    if (drop & RKSC_DROP_Q_LO) HIP_TRY(rksc::launch_round_bf16(qb, (size_t)M * H * hd, strm));
+    if (drop & RKSC_DROP_OWN_KV_LO) {
+      HIP_TRY(rksc::launch_round_bf16(kown, (size_t)B * Hkv * s * hd, strm));
+      HIP_TRY(rksc::launch_round_bf16(vown, (size_t)B * Hkv * s * hd, strm));
+    }
     const void* pk = n > 0 ? pk_base + l * kv_layer : nullptr;
     const void* pv = n > 0 ? pv_base + l * kv_layer : nullptr;
     HIP_TRY(mark(l, 2));
     HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, pk, pv, kown, vown, act, opart, mlpart, ctrl, n, s, H, Hkv, hd,
-                                   B, strm));
+                                   B, strm, !(drop & RKSC_DROP_P_LO)));
+    if (drop & RKSC_DROP_O_LO) HIP_TRY(drop_lo(act, (size_t)M * H * hd));
     HIP_TRY(mark(l, 3));
     HIP_TRY(mark(l, 4));
     HIP_TRY(rksc::launch_gemm(dt, lay.o, act, plane_lo(act, (size_t)M * H * hd), lw.w_o, pres, res_stride, ctrl, s,
@@ -297,11 +310,13 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     HIP_TRY(mark(l, 5));
     HIP_TRY(rksc::launch_add_norm(dt, x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
                                   lw.ffn_norm, d, c->rms_eps, M, strm));
+    if (drop & RKSC_DROP_GATE_UP_LO) HIP_TRY(drop_lo(act, (size_t)M * d));
     HIP_TRY(mark(l, 6));
     HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig, (size_t)M * 2 * F,
                               ctrl, s, M, 2 * F, d, strm));
     HIP_TRY(mark(l, 7));
     HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
+    if (drop & RKSC_DROP_DOWN_LO) HIP_TRY(drop_lo(ffn, (size_t)M * F));
     HIP_TRY(mark(l, 8));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
                               M, d, F, strm));
@@ -310,6 +325,7 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
       HIP_TRY(rksc::launch_tap(dt, x_cur, pres, lay.down.splits, res_stride, ctrl, s, d, B, l, hidden_last,
                                w->final_norm, c->rms_eps, hn_a, hn_b, B, strm, l % win));
       const int kw = l % win + 1, first = l + 1 - kw;
+      if (drop & RKSC_DROP_LM_HEAD_LO) HIP_TRY(hipMemsetAsync(hn_b, 0, (size_t)RKSC_MAX_BRANCHES * d * 2, strm));
       HIP_TRY(mark(l, 10));
       HIP_TRY(rksc::launch_entropy(dt, w->lm_head, hn_a, hn_b, ctrl, V, d, B, parts, strm, kw));
       HIP_TRY(mark(l, 11));
@@ -332,6 +348,16 @@ RKSC_EXPORT rksc_status rksc_verify_forward(const rksc_weights* w, const rksc_pr
 }
 
 RKSC_EXPORT int32_t rksc_verify_window(int32_t n_branches) { return exit_window(n_branches); }
+
+RKSC_EXPORT rksc_status rksc_test_verify_precision(const rksc_weights* w, const rksc_prefix_kv* kv,
+                                                   const int32_t* branch_tokens, int32_t n_branches,
+                                                   int32_t branch_len, float tau, int32_t patience, float* entropy,
+                                                   int32_t* exit_layer, float* hidden_last, void* workspace,
+                                                   size_t workspace_bytes, void* stream, uint32_t drop_mask) {
+  if (drop_mask & ~(uint32_t)RKSC_DROP_ALL) return fail(RKSC_ERR_INVALID_ARGUMENT, "unknown drop bits 0x%x", drop_mask);
+  return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
+                     hidden_last, workspace, workspace_bytes, stream, nullptr, exit_window(n_branches), drop_mask);
+}
 
 RKSC_EXPORT rksc_status rksc_verify_forward_window(const rksc_weights* w, const rksc_prefix_kv* kv,
                                                    const int32_t* branch_tokens, int32_t n_branches,
@@ -783,6 +809,35 @@ RKSC_EXPORT rksc_status rksc_test_gemm_kind(int32_t dtype, const void* A, const 
   if (splits_used) *splits_used = p.splits;
   HIP_TRY(rksc::launch_gemm(dt, p, A, A_lo, W, P, (size_t)M * N, nullptr, 1, M, N, K,
                             static_cast<hipStream_t>(stream)));
+  return ok();
+}
+
+RKSC_EXPORT rksc_status rksc_test_gemm_live(int32_t dtype, const void* A, const void* A_lo, const void* W, float* P,
+                                            int32_t M, int32_t N, int32_t K, int32_t splits, int32_t kind,
+                                            int32_t live_count, int32_t branch_len, void* ctrl_scratch,
+                                            int32_t* splits_used, void* stream) {
+  if (!A || !W || !P || !ctrl_scratch) return fail(RKSC_ERR_INVALID_ARGUMENT, "A, W, P and ctrl_scratch must not be NULL");
+  if (dtype == RKSC_BF16 && !A_lo) return fail(RKSC_ERR_INVALID_ARGUMENT, "A_lo must not be NULL for bf16");
+  if (dtype != RKSC_F32 && dtype != RKSC_BF16) return fail(RKSC_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (M < 1 || N < 1 || K < 8 || K % 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "bad shape %d x %d x %d", M, N, K);
+  if (splits < 0 || splits > 8) return fail(RKSC_ERR_INVALID_ARGUMENT, "splits must be in [0, 8]");
+  if (kind < -1 || kind > 2) return fail(RKSC_ERR_INVALID_ARGUMENT, "kind must be -1, 0, 1 or 2 (got %d)", kind);
+  if (kind >= 1 && dtype != RKSC_BF16) return fail(RKSC_ERR_UNSUPPORTED, "kind %d needs bf16 weights", kind);
+  if (kind == 2 && (M > 32 || N % 4 || K > 32768 || (M > 16 && K > 16384)))
+    return fail(RKSC_ERR_UNSUPPORTED, "kind 2 needs M <= 32, N %% 4 == 0 and K <= 32768 (K <= 16384 above 16 rows)");
+  if (live_count < 1 || live_count > RKSC_MAX_BRANCHES || branch_len < 1 || (long long)live_count * branch_len > M)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "need 1 <= live_count <= %d, branch_len >= 1, live rows <= M",
+                RKSC_MAX_BRANCHES);
+  if (reinterpret_cast<uintptr_t>(ctrl_scratch) % 256)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "ctrl_scratch must be 256-byte aligned");
+  static_assert(sizeof(rksc::Ctrl) <= 4096, "the control block fits the documented scratch size");
+  const DType dt = dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
+  const GemmPlan p = rksc::plan_gemm_kind(dt, M, N, K, kind, splits);
+  if (splits_used) *splits_used = p.splits;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  rksc::Ctrl* ctrl = static_cast<rksc::Ctrl*>(ctrl_scratch);
+  HIP_TRY(rksc::launch_init(ctrl, live_count, 1, nullptr, nullptr, nullptr, 0, st));
+  HIP_TRY(rksc::launch_gemm(dt, p, A, A_lo, W, P, (size_t)M * N, ctrl, branch_len, M, N, K, st));
   return ok();
 }
 

@@ -349,3 +349,4 @@ def test_marshal_rejects_wrong_dtype_shape_and_host_tensors(lib):
     with pytest.raises(ValueError, match="fired"):
         rk.rksc_cgee_gate(_meta((4,), torch.float32), 3, 0.7, 0.06, None, _meta((1,), torch.int64),
                           _meta((1,), torch.int32), None)
+

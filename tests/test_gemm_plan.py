@@ -71,3 +71,10 @@ def test_plan_invariants(M, N, K):
             assert kps % (32 if p["kind"] == 1 else 64) == 0 or sp == 1, p
         else:
             assert p["kind"] == 0, p
+
+
+def test_large_row_counts_take_wide_tiles():
+    """Row counts where row * K passes 2^31 (a 150k-token root forward, 64 branches x 2400 tokens at
+    the 7B width) reach the 256 x 256-tile kernel through the planner; its row offsets are 64-bit."""
+    for M in (153600, 262144):
+        assert rk.rksc_test_gemm_plan(M, 4096, 14336)["kind"] == 1

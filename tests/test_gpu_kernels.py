@@ -108,20 +108,93 @@ def test_gemm_skinny_matches_fp64(M, N, K, kind):
     assert (err <= bound).all(), f"max err {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}"
 
 
-@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
-@pytest.mark.parametrize("B,n,s,H,Hkv,hd", [
-    (1, 0, 1, 4, 4, 64), (2, 37, 16, 8, 2, 64), (3, 130, 70, 28, 4, 128),
-    (1, 1024, 128, 32, 8, 128), (2, 64, 200, 4, 4, 128), (4, 64, 16, 4, 4, 64),
-    # fewer than 64 query rows per branch and KV head: branches share prefix tiles
-    (5, 300, 1, 8, 2, 128), (3, 64, 3, 4, 4, 64), (8, 1000, 2, 32, 8, 128), (4, 0, 5, 8, 2, 64),
-    (2, 130, 15, 8, 2, 128), (32, 2100, 1, 32, 8, 128), (64, 64, 1, 4, 1, 64),
-    # full-size decode and long-prefix verify tiles: many prefix tiles per chunk
-    # stream through the LDS ring (slots reused while others are in flight)
-    (32, 16384, 1, 32, 8, 128), (4, 16384, 32, 32, 8, 128), (64, 1024, 32, 8, 2, 128),
+@pytest.mark.parametrize("M,N,K,splits,kind,live,s", [
+    # 256 x 256 tiles: a live set that ends inside a row tile, inside a wave's 64 rows, on a tile edge
+    (1024, 700, 1000, 3, 1, 3, 128), (1024, 4608, 3584, 0, -1, 5, 128), (1024, 512, 2048, 0, 1, 1, 200),
+    (8192, 4096, 14336, 0, -1, 7, 256), (8192, 1024, 4096, 2, 1, 31, 256),
+    # 128-row tiles: partial waves and tiles
+    (1024, 512, 2048, 0, 0, 2, 128), (128, 4096, 4096, 0, -1, 3, 16), (128, 6144, 4096, 0, 0, 1, 5),
+    (2048, 1536, 4104, 0, 0, 9, 100),
+    # the weight stream of a decode step
+    (32, 28672, 4096, 0, -1, 5, 1), (16, 4096, 14336, 0, 2, 11, 1), (32, 1028, 4104, 0, 2, 17, 1),
 ])
+def test_gemm_live_rows_match_fp64(M, N, K, splits, kind, live, s):
+    """Projections after branch exits: the plan of an M-row call with only live * s rows live
+    (a control block in device memory, as the verify pass keeps it). Live rows match fp64
+    (sampled at the largest shapes); rows past the live ones are not written."""
+    log(f"gemm live M={M} N={N} K={K} splits={splits} kind={kind} live={live}x{s}")
+    A = _rand((M, K), torch.float32, 31 + M, 0.5)
+    W = _rand((N, K), torch.bfloat16, 32 + N, 0.05)
+    a_hi = A.to(torch.bfloat16)
+    a_lo = (A - a_hi.float()).to(torch.bfloat16)
+    A = a_hi.float() + a_lo.float()
+    P = torch.full((8, M, N), float("nan"), dtype=torch.float32, device=DEV)
+    used = rk.rksc_test_gemm_live((a_hi.to(DEV), a_lo.to(DEV)), W.to(DEV), live, s, P, splits=splits, kind=kind)
+    torch.cuda.synchronize()
+    rows = live * s
+    Pc = P[:used].cpu()
+    assert torch.isnan(Pc[:, rows:]).all(), "rows past the live set were written"
+    assert not torch.isnan(Pc[:, :rows]).any(), "a live row was not written"
+    sample = np.arange(rows) if rows * N * K <= 4e9 else np.unique(np.r_[np.arange(0, rows, 37), rows - 1])
+    got = Pc[:, sample].double().sum(0).numpy()
+    a, w = A[sample].double().numpy(), W.double().numpy()
+    bound = 1e-5 * (np.abs(a) @ np.abs(w).T) + 1e-7
+    err = np.abs(got - a @ w.T)
+    assert (err <= bound).all(), f"max err {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}"
+
+
+@pytest.mark.parametrize("kind", [1, 0])
+def test_gemm_row_offsets_past_2_31(kind):
+    """Both dense kernels where row * K passes 2^31 elements (150000 rows x 14336, the 7B down
+    projection's K; the planner takes the 256 x 256 tiles for such row counts at the full width):
+    sampled rows on both sides of the boundary match fp64."""
+    M, N, K = 150000, 256, 14336
+    assert (M - 1) * K >= 2 ** 31
+    assert rk.rksc_test_gemm_plan(153600, 4096, K)["kind"] == 1
+    assert rk.rksc_test_gemm_plan(M, N, K, kind=kind)["kind"] == kind
+    log(f"gemm offsets kind={kind} M={M} N={N} K={K}")
+    g = torch.Generator(device=DEV).manual_seed(5)
+    a_hi = torch.randn((M, K), generator=g, device=DEV, dtype=torch.bfloat16)
+    a_lo = torch.randn((M, K), generator=g, device=DEV, dtype=torch.bfloat16) * (2.0 ** -9)
+    W = (torch.randn((N, K), generator=g, device=DEV, dtype=torch.float32) * 0.05).to(torch.bfloat16)
+    P = rk.rksc_test_gemm((a_hi, a_lo), W, kind=kind)
+    torch.cuda.synchronize()
+    first_past = -(-(2 ** 31) // K)
+    rows = np.unique(np.r_[0, 1, 255, 256, first_past - 3, first_past - 1, first_past, first_past + 1,
+                           np.arange(first_past + 2, M, 97), M - 2, M - 1])
+    idx = torch.from_numpy(rows).to(DEV)
+    got = P[:, idx].double().sum(0).cpu().numpy()
+    a = (a_hi[idx].double() + a_lo[idx].double()).cpu().numpy()
+    w = W.double().cpu().numpy()
+    bound = 1e-5 * (np.abs(a) @ np.abs(w).T) + 1e-7
+    err = np.abs(got - a @ w.T)
+    assert (err <= bound).all(), f"max err {err.max():.3e} at row {rows[np.unravel_index(err.argmax(), err.shape)[0]]}"
+    del a_hi, a_lo, P
+
+
+def _attention_cases():
+    """bf16 at every shape; fp32 (the plain per-thread kernel) only where it finishes quickly."""
+    shapes = [
+        (1, 0, 1, 4, 4, 64), (2, 37, 16, 8, 2, 64), (3, 130, 70, 28, 4, 128),
+        (1, 1024, 128, 32, 8, 128), (2, 64, 200, 4, 4, 128), (4, 64, 16, 4, 4, 64),
+        # fewer than 64 query rows per branch and KV head: branches share prefix tiles
+        (5, 300, 1, 8, 2, 128), (3, 64, 3, 4, 4, 64), (8, 1000, 2, 32, 8, 128), (4, 0, 5, 8, 2, 64),
+        (2, 130, 15, 8, 2, 128), (32, 2100, 1, 32, 8, 128), (64, 64, 1, 4, 1, 64),
+        # full-size decode and long-prefix verify tiles: many prefix tiles per chunk
+        # stream through the LDS ring (slots reused while others are in flight)
+        (32, 16384, 1, 32, 8, 128), (4, 16384, 32, 32, 8, 128), (64, 1024, 32, 8, 2, 128),
+    ]
+    cases = []
+    for shp in shapes:
+        B, n, s, H, Hkv, hd = shp
+        cases.append(pytest.param(torch.bfloat16, *shp, id=f"bf16-{B}-{n}-{s}-{H}-{Hkv}-{hd}"))
+        if n * s * H <= 1024 * 128 * 8:
+            cases.append(pytest.param(torch.float32, *shp, id=f"f32-{B}-{n}-{s}-{H}-{Hkv}-{hd}"))
+    return cases
+
+
+@pytest.mark.parametrize("dtype,B,n,s,H,Hkv,hd", _attention_cases())
 def test_attention_matches_oracle(dtype, B, n, s, H, Hkv, hd):
-    if dtype == torch.float32 and n * s * H > 1024 * 128 * 8:
-        pytest.skip("fp32 kernel is the plain per-thread path; large shapes are covered in bf16")
     log(f"attention {dtype} B={B} n={n} s={s} H={H} Hkv={Hkv} hd={hd}")
     std = 1.28
     f32 = torch.float32

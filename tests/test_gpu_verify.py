@@ -188,3 +188,76 @@ def test_exit_window_does_not_change_outputs(B, taus):
                 np.testing.assert_array_equal(ex, base[1])
                 np.testing.assert_array_equal(ent, base[0])
                 np.testing.assert_array_equal(hid, base[2])
+
+
+def _pick_tau(ent_ref, patience, L, window):
+    """_pick_tau_margin with the widest margin (from 2.5e-2 down to just above the 1e-2 bar) that
+    admits a tau."""
+    for margin in (2.5e-2, 1.5e-2, 1.1e-2):
+        tau = _pick_tau_margin(ent_ref, patience, L, window, margin)
+        if tau is not None:
+            return tau
+    return None
+
+
+def _pick_tau_margin(ent_ref, patience, L, window, margin):
+    """A tau read off the oracle's full-depth entropies [L, Bo] of the sampled branches such that
+    (a) no sampled delta |H_l - H_{l-1}| lies within `margin` of it (so the exit layers must agree
+    exactly), (b) some sampled branch exits before layer L and some exits later than another
+    (different depths), preferring exits inside an exit window (layer % window != 0)."""
+    Bo = ent_ref.shape[1]
+    deltas = np.sort(np.unique(np.abs(np.diff(ent_ref, axis=0)).ravel()))
+    cands = [(a + b) / 2 for a, b in zip(deltas[:-1], deltas[1:]) if b - a > 2 * margin]
+    best, best_score = None, -1
+    for tau in cands:
+        ex = [oracle.exit_layer(ent_ref[:, j], tau, patience) for j in range(Bo)]
+        if min(ex) >= L or len(set(ex)) < 2:
+            continue
+        # distinct depths first, then a sampled branch that survives every layer after the others
+        # left (the survivors' rows are gathered), then exits inside a window
+        score = len(set(ex)) * 10 + 15 * (max(ex) == L) + sum(1 for e in ex if e < L and e % window)
+        if score > best_score:
+            best, best_score = tau, score
+    return best
+
+
+def _exit_path_case(name, n_layers, patience, sampled, window_expect):
+    """Full-size kernel plans with exits firing (Alg. VerifyWithEntropyExit; Sec. 2.3
+    "Layer-level entropy exit"): the workload's width, branch count, prefix and span over
+    n_layers layers; tau is read off the oracle's deltas of the sampled branches so that they
+    exit at different layers (some inside an exit window) while every other branch exits
+    wherever its own entropies take it, shrinking the live set under the wide GEMM tiles."""
+    wl = workloads.get(name)
+    mw, kv, toks = _inputs(wl.model, wl.n_branches, wl.prefix_len, wl.branch_len, seed=42, n_layers=n_layers)
+    L = n_layers
+    win = rk.rksc_verify_window(wl.n_branches)
+    assert win == window_expect
+    log(f"[{name} exit path] oracle on branches {sampled}")
+    ent_ref, hid_ref, _ = _run_oracle(mw, kv, toks, 0.0, 1, branches=sampled)
+    tau = _pick_tau(ent_ref, patience, L, win)
+    assert tau is not None, f"no separable tau in the oracle deltas {np.abs(np.diff(ent_ref, axis=0)).T}"
+    ex_ref = np.array([oracle.exit_layer(ent_ref[:, j], tau, patience) for j in range(len(sampled))])
+    log(f"[{name} exit path] tau={tau:.4f} patience={patience} oracle exits {ex_ref.tolist()}")
+    ent, ex, hid = _run_gpu(mw, kv, toks, tau, patience)
+    stats = compare_verify(ent, ex, hid, ent_ref, hid_ref, ex_ref, tau, branches=sampled,
+                           label=f"{name} L={L} tau={tau:.4f}")
+    log(f"[{name} exit path] gpu exits {ex.tolist()} {stats}")
+    assert stats["near_threshold"] == 0 and stats["exit_match"] == len(sampled)
+    assert (ex < L).sum() >= 1 and len(set(ex.tolist())) >= 2, "the live set must shrink during the call"
+    # the same call at tau = 0 runs every layer: entropies and hidden rows at all depths
+    ent0, ex0, hid0 = _run_gpu(mw, kv, toks, 0.0, 1)
+    assert (ex0 == L).all()
+    compare_verify(ent0, ex0, hid0, ent_ref, hid_ref, np.full(len(sampled), L), 0.0, branches=sampled,
+                   label=f"{name} L={L} tau=0")
+
+
+def test_exit_path_full_plans_paper_verify():
+    """28 layers of the large-vocab shape, 8 x 128 rows over 1024 prefix tokens: 1024-row
+    projections on the 256 x 256 tiles (with K splits), exit windows of 4 layers."""
+    _exit_path_case("7b_paper_verify", 28, 2, [0, 3, 6], 4)
+
+
+def test_exit_path_full_plans_10b_long():
+    """6 layers of the 10B long-prefix shape, 32 x 256 rows over 16384 prefix tokens, patience 1:
+    8192-row projections, exit windows of 2 layers at 32 live columns."""
+    _exit_path_case("10b_long", 6, 1, [1, 17, 30], 2)
