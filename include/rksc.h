@@ -156,6 +156,31 @@ rksc_status rksc_verify_forward(const rksc_weights* weights, const rksc_prefix_k
                                 float* entropy, int32_t* exit_layer, float* hidden_last,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * rksc_verify_forward without a workspace argument, for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid allocation). The pass runs on a device array of
+ * RKSC_NOALLOC_SCRATCH_BYTES held by the library: each GPU the library runs on
+ * gets its own copy, resolved on the first call on that GPU (with that GPU
+ * current) and kept until the process ends. The call itself allocates
+ * nothing. Arguments, outputs and results are those of rksc_verify_forward
+ * (the same kernels); the caller still provides the inputs and outputs.
+ *   - A pass whose workspace (rksc_verify_workspace_size) exceeds
+ *     RKSC_NOALLOC_SCRATCH_BYTES is refused with RKSC_ERR_WORKSPACE_TOO_SMALL
+ *     before anything is launched (use rksc_verify_forward for it).
+ *   - `stream` must belong to the current device (RKSC_ERR_INVALID_ARGUMENT
+ *     otherwise).
+ *   - Every call on one GPU shares that GPU's array, and the pass overwrites
+ *     it: calls that overlap on one GPU (other streams, other threads) race.
+ *     Serialise them, e.g. on one stream. The array keeps the last call's
+ *     contents; the pass initialises everything it reads.
+ */
+#define RKSC_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+rksc_status rksc_verify_forward_noalloc(const rksc_weights* weights, const rksc_prefix_kv* prefix_kv,
+                                        const int32_t* branch_tokens, int32_t n_branches, int32_t branch_len,
+                                        float tau, int32_t patience, float* entropy, int32_t* exit_layer,
+                                        float* hidden_last, void* stream);
+
 /* The exit window rksc_verify_forward uses for n_branches branches: 4 up to 16
  * branches, 2 up to 32, else 1. */
 int32_t rksc_verify_window(int32_t n_branches);

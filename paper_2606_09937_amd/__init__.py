@@ -109,6 +109,9 @@ def load_library():
     lib.rksc_verify_forward.restype = i32
     lib.rksc_verify_forward.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32, i32,
                                         vp, vp, vp, vp, sz, vp]
+    lib.rksc_verify_forward_noalloc.restype = i32
+    lib.rksc_verify_forward_noalloc.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32,
+                                                f32, i32, vp, vp, vp, vp]
     lib.rksc_test_verify_precision.restype = i32
     lib.rksc_test_verify_precision.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32,
                                                i32, vp, vp, vp, vp, sz, vp, ctypes.c_uint32]
@@ -348,6 +351,35 @@ def rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, 
         st = lib.rksc_verify_forward(*args)
     else:
         st = lib.rksc_verify_forward_window(*args, int(window))
+    del layers_keepalive
+    _check(st)
+
+
+RKSC_NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def rksc_verify_forward_noalloc(weights, prefix_k, prefix_v, branch_tokens, tau: float, patience: int,
+                                entropy: torch.Tensor, exit_layer: torch.Tensor,
+                                hidden_last: Optional[torch.Tensor], stream=None) -> None:
+    """Marshal torch device tensors into rksc_verify_forward_noalloc (the verify pass on the
+    library's own device array of RKSC_NOALLOC_SCRATCH_BYTES; no workspace argument)."""
+    need = _Args()
+    _check_weights(need, weights)
+    n = _check_prefix(need, weights, prefix_k, prefix_v)
+    need(branch_tokens, "branch_tokens", torch.int32, ndim=2)
+    B, s = branch_tokens.shape
+    L, d = len(weights.layers), weights.shape.d_model
+    need(entropy, "entropy", torch.float32, (L, B))
+    need(exit_layer, "exit_layer", torch.int32, (B,))
+    if hidden_last is not None:
+        need(hidden_last, "hidden_last", torch.float32, (L, B, d))
+    need.done()
+    lib = load_library()
+    w, layers_keepalive = _weights_struct(weights)
+    kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
+    st = lib.rksc_verify_forward_noalloc(ctypes.byref(w), ctypes.byref(kv), _ptr(branch_tokens), int(B), int(s),
+                                         float(tau), int(patience), _ptr(entropy), _ptr(exit_layer),
+                                         _ptr(hidden_last), _stream(stream))
     del layers_keepalive
     _check(st)
 

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(PKG_DIR, "librksc.so")
 ARCH = "gfx950"
 
 SOURCES = ["k_rows.hip", "k_gemm.hip", "k_attn.hip", "k_entropy.hip", "k_asks.hip", "rksc_api.cpp",
-           "rksc_runtime.cpp"]
+           "rksc_runtime.cpp", "rksc_noalloc.hip"]
 
 COMMON_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",

@@ -10,6 +10,7 @@
 
 #include "../../include/rksc.h"
 #include "../../include/rksc_testing.h"
+#include "api_internal.h"
 #include "kernels.h"
 #include "status.h"
 
@@ -343,6 +344,24 @@ RKSC_EXPORT rksc_status rksc_verify_forward(const rksc_weights* w, const rksc_pr
                                             float tau, int32_t patience, float* entropy, int32_t* exit_layer,
                                             float* hidden_last, void* workspace, size_t workspace_bytes,
                                             void* stream) {
+  return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
+                     hidden_last, workspace, workspace_bytes, stream, nullptr, exit_window(n_branches));
+}
+
+rksc_status rksc::verify_workspace(const rksc_model_config* cfg, int32_t n_branches, int32_t branch_len,
+                                   int32_t n_prefix, size_t* bytes) {
+  if (n_prefix < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", n_prefix);
+  Layout lay;
+  const rksc_status st = make_layout(cfg, n_branches, branch_len, n_prefix, &lay);
+  if (st != RKSC_OK) return st;
+  *bytes = lay.total;
+  return RKSC_OK;
+}
+
+rksc_status rksc::verify_call(const rksc_weights* w, const rksc_prefix_kv* kv, const int32_t* branch_tokens,
+                              int32_t n_branches, int32_t branch_len, float tau, int32_t patience, float* entropy,
+                              int32_t* exit_layer, float* hidden_last, void* workspace, size_t workspace_bytes,
+                              void* stream) {
   return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
                      hidden_last, workspace, workspace_bytes, stream, nullptr, exit_window(n_branches));
 }

@@ -1,6 +1,7 @@
 """The C ABI library loads, exports every declared symbol, and rejects bad
 arguments before touching the device. CPU only: no call here reaches a launch."""
 import ctypes
+import dataclasses
 import math
 import os
 import re
@@ -350,3 +351,26 @@ def test_marshal_rejects_wrong_dtype_shape_and_host_tensors(lib):
         rk.rksc_cgee_gate(_meta((4,), torch.float32), 3, 0.7, 0.06, None, _meta((1,), torch.int64),
                           _meta((1,), torch.int32), None)
 
+
+def test_noalloc_refuses_oversized_pass_before_any_hip_call(lib):
+    """rksc_verify_forward_noalloc checks the pass's workspace against its fixed array on the host
+    first: a larger pass is refused with RKSC_ERR_WORKSPACE_TOO_SMALL (no device is touched)."""
+    wl = workloads.get("7b_tot")
+    w, _keep, cfg = _fake_weights(wl.model)
+    kv = rk.PrefixKV(wl.prefix_len, FAKE, FAKE)
+    need = lib.rksc_verify_workspace_size(ctypes.byref(cfg), wl.n_branches, wl.branch_len, wl.prefix_len)
+    assert need > rk.RKSC_NOALLOC_SCRATCH_BYTES
+    st = lib.rksc_verify_forward_noalloc(ctypes.byref(w), ctypes.byref(kv), FAKE, wl.n_branches, wl.branch_len,
+                                         0.02, 2, FAKE, FAKE, None, None)
+    assert st == rk.RKSC_ERR_WORKSPACE_TOO_SMALL
+    assert str(need) in rk.rksc_last_error() and "allocation-free" in rk.rksc_last_error()
+    assert lib.rksc_verify_forward_noalloc(None, ctypes.byref(kv), FAKE, 1, 1, 0.02, 2, FAKE, FAKE, None,
+                                           None) == rk.RKSC_ERR_INVALID_ARGUMENT
+    bad = workloads.get("tiny").model
+    w2, _k2, _ = _fake_weights(dataclasses.replace(bad, head_dim=32))
+    assert lib.rksc_verify_forward_noalloc(ctypes.byref(w2), ctypes.byref(rk.PrefixKV(8, FAKE, FAKE)), FAKE, 4, 16,
+                                           0.02, 2, FAKE, FAKE, None, None) == rk.RKSC_ERR_UNSUPPORTED
+    # the header's limit is the binding's
+    text = open(os.path.join(ROOT, "include", "rksc.h")).read()
+    assert "#define RKSC_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)" in text
+    assert rk.RKSC_NOALLOC_SCRATCH_BYTES == 128 << 20
