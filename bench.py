@@ -226,6 +226,50 @@ def summarize_pmc(args):
     print(f"HBM traffic per launch: read {fb / 1e6:.1f} MB + write {wb / 1e6:.3f} MB = {(fb + wb) / 1e6:.1f} MB")
 
 
+def summarize_mfma(args):
+    """Prints the MFMA counters of a rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_BF16 run per
+    projection class: MfmaUtil (MFMA-busy cycles over active cycles x SIMDs, %) and the bf16 MFMA
+    flops issued (MOPS x 512) against the class's algorithmic flops (the hi/lo operand split issues
+    two products per algorithmic one). Dispatches are assigned to classes by their issued flops."""
+    import re
+    import statistics
+
+    import workloads
+    rows = _read_counter_csv(args.pmc_mfma)
+    per = {}
+    for kname, cname, val, disp in rows:
+        d = per.setdefault(disp, {"name": kname})
+        d[cname] = d.get(cname, 0.0) + val
+    wl = workloads.get(args.workload)
+    shape = wl.model
+    work = kernel_work(shape, wl.n_branches, wl.prefix_len, wl.branch_len, 1)
+    classes = {c: work[c]["flops"] for c in PROJECTIONS}
+    got = {c: [] for c in classes}
+    other = {}
+    for d in per.values():
+        if "MfmaUtil" not in d or "SQ_INSTS_VALU_MFMA_MOPS_BF16" not in d:
+            continue
+        issued = d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+        best = min(classes, key=lambda c: abs(issued / classes[c] - 2.0))
+        if "k_gemm" in d["name"] and abs(issued / classes[best] - 2.0) < 0.1:
+            got[best].append((d["MfmaUtil"], issued, d["name"]))
+        else:
+            m = re.search(r"(k_[a-z0-9_]+)", d["name"])
+            other.setdefault(m.group(1) if m else d["name"][:40], []).append((d["MfmaUtil"], issued))
+    print(f"MFMA counters at {wl.name} (M = {wl.n_branches * wl.branch_len} rows): per projection class")
+    print(f"{'class':14s} {'launches':>8s} {'MfmaUtil %':>11s} {'issued GFLOP':>13s} {'algorithmic GFLOP':>18s}  kernel")
+    for c, lst in got.items():
+        if not lst:
+            continue
+        u = statistics.median(x[0] for x in lst)
+        iss = statistics.median(x[1] for x in lst)
+        print(f"{c:14s} {len(lst):8d} {u:11.1f} {iss / 1e9:13.1f} {classes[c] / 1e9:18.1f}  {lst[0][2][:70]}")
+    for k, lst in sorted(other.items()):
+        u = statistics.median(x[0] for x in lst)
+        iss = statistics.median(x[1] for x in lst)
+        print(f"{'(other)':14s} {len(lst):8d} {u:11.1f} {iss / 1e9:13.2f} {'':>18s}  {k}")
+
+
 def summarize_stats(args):
     """Prints the per-kernel table of a rocprofv3 --stats run (kernel_stats.csv)."""
     import csv
@@ -470,7 +514,8 @@ def measure_kv_probe(mw, shape, n, args, stream, dev):
 
 def measure_tree(mw, kv, shape, n, args, hip, sp, stream, dev):
     """Tree sharing and the ASKS gate at the workload's prefix: one search-tree node
-    of TREE_NODE tokens built once over the root cache (rksc_prefix_extend), against
+    of TREE_NODE tokens built once over the root cache (rksc_prefix_extend: the root is
+    read in place and only the node's entries are written), against
     its DECODE_BRANCHES children each recomputing the node's tokens over the root cache
     (one batched suffix pass); and the device ASKS gate over DECODE_BRANCHES rows."""
     import torch
@@ -483,7 +528,7 @@ def measure_tree(mw, kv, shape, n, args, hip, sp, stream, dev):
     node = workloads.make_tokens(m, shape.vocab, seed=args.seed, name="node", device=dev)
     dtype = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
     ws = torch.empty(rk.rksc_prefix_extend_workspace_size(shape, n, m), dtype=torch.uint8, device=dev)
-    ck = torch.empty((L, shape.n_kv_heads, n + m, shape.head_dim), dtype=dtype, device=dev)
+    ck = torch.empty((L, shape.n_kv_heads, m, shape.head_dim), dtype=dtype, device=dev)
     cv = torch.empty_like(ck)
     hn = torch.empty((L, shape.d_model), dtype=torch.float32, device=dev)
     dec = rk.Decoder(mw, kv.k, kv.v, Bd, m, capacity=m, device=dev)
@@ -647,7 +692,7 @@ def measure_workload(name, args, hip, dev):
     ms_full = timed(0.0, 1)
 
     # Per-class times from one profiled full-depth call (every layer live).
-    win = rk.rksc_verify_window(B)
+    win = rk.rksc_verify_window(shape, B, s, n)
     stream_layers = [l for l in range(L) if l % win == win - 1 or l == L - 1]
     slots = sorted(set(v for s0 in EVENT_SLOTS.values() for v in (s0, s0 + 1)))
     evs, ptrs = event_arrays(hip, L, 1, slots, stream_layers)
@@ -735,11 +780,16 @@ def main():
     ap.add_argument("--pmc-write")
     ap.add_argument("--pmc-copy-fetch")
     ap.add_argument("--pmc-copy-write")
+    ap.add_argument("--summarize-mfma", dest="pmc_mfma", metavar="DIR",
+                    help="print the per-class MFMA counters of a rocprofv3 --pmc MfmaUtil "
+                         "SQ_INSTS_VALU_MFMA_MOPS_BF16 output directory (for --workload) and exit")
     args = ap.parse_args()
     if args.stats:
         return summarize_stats(args)
     if args.summarize_pmc:
         return summarize_pmc(args)
+    if args.pmc_mfma:
+        return summarize_mfma(args)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -841,7 +891,7 @@ def main():
         return evs, ptrs
 
     # The probe's lm_head stream runs once per exit window, at the window's last layer.
-    win = rk.rksc_verify_window(B)
+    win = rk.rksc_verify_window(shape, B, s, n)
     stream_layers = [l for l in range(L) if l % win == win - 1 or l == L - 1]
 
     def durations(evs, k_steps, slot, layers):

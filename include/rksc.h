@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define RKSC_ABI_VERSION 6
+#define RKSC_ABI_VERSION 7
 
 /* Largest number of branches one verify call accepts. */
 #define RKSC_MAX_BRANCHES 64
@@ -91,16 +91,27 @@ typedef struct {
 } rksc_weights;
 
 /* The shared prefix cache C = {(K^(l), V^(l))} of Eq. prefix_fwd, computed once
- * for the n_prefix prefix tokens and read (never copied) by every branch. */
-typedef struct {
-  int32_t n_prefix;   /* n >= 0 */
-  const void* k;      /* [L, Hkv, n, hd], keys after RoPE at positions 0..n-1 */
-  const void* v;      /* [L, Hkv, n, hd] */
+ * for the prefix tokens and read (never copied) by every branch. A cache may
+ * continue another one: a search-tree node's cache (rksc_prefix_extend) holds
+ * only the node's own entries and names its parent, so that the node's
+ * children read the chain root, ..., parent, node in place as one prefix
+ * (Sec. 2.2, sharing of intermediate tree nodes). The prefix of a call is the
+ * chain ending at the cache passed, in position order; n_prefix counts this
+ * cache's entries only, and "the prefix length" below means the chain's total.
+ * At most RKSC_MAX_PREFIX_SEGMENTS caches per chain (RKSC_ERR_UNSUPPORTED
+ * otherwise; empty caches do not count). */
+#define RKSC_MAX_PREFIX_SEGMENTS 8
+typedef struct rksc_prefix_kv {
+  int32_t n_prefix;   /* entries of this cache, >= 0 */
+  const void* k;      /* [L, Hkv, n_prefix, hd], keys after RoPE at positions base..base+n_prefix-1 */
+  const void* v;      /* [L, Hkv, n_prefix, hd] */
+  const struct rksc_prefix_kv* parent;   /* NULL for a root cache (base = 0), else the cache whose
+                                            entries come first (base = the prefix length up to it) */
 } rksc_prefix_kv;
 
 /* One branch set's own K/V cache for the decode loop (Sec. 2.2 "KV broadcast
  * and batched decode"): entry j of branch b holds the key (after RoPE) and the
- * value of the branch's token at position n_prefix + j. Allocated by the
+ * value of the branch's token at position n + j (n: the prefix length). Allocated by the
  * caller for a fixed number of branches B; the decode calls append to it and
  * advance `length` (host field) on success. */
 typedef struct {
@@ -113,7 +124,7 @@ typedef struct {
 int32_t rksc_abi_version(void);
 
 /* Bytes of workspace rksc_verify_forward needs for this shape (n_branches
- * branches of branch_len tokens over an n_prefix-token prefix cache); 0 if the
+ * branches of branch_len tokens over a prefix of n_prefix entries in all); 0 if the
  * shape is invalid (rksc_last_error() says why). */
 size_t rksc_verify_workspace_size(const rksc_model_config* cfg, int32_t n_branches,
                                   int32_t branch_len, int32_t n_prefix);
@@ -144,7 +155,7 @@ size_t rksc_verify_workspace_size(const rksc_model_config* cfg, int32_t n_branch
  *                256-byte aligned; its contents on entry do not matter.
  *
  * Schedule: the probe's lm_head stream is shared by an exit window of
- * rksc_verify_window(B) consecutive layers (their rows are extra columns of
+ * rksc_verify_window(cfg, B, s, n) consecutive layers (their rows are extra columns of
  * one read of W_lm). The rule still runs layer by layer, at the window's end;
  * a branch that exits inside a window has its later layers of that window
  * computed and discarded (NaN in the outputs), so every output equals that of
@@ -181,9 +192,16 @@ rksc_status rksc_verify_forward_noalloc(const rksc_weights* weights, const rksc_
                                         float tau, int32_t patience, float* entropy, int32_t* exit_layer,
                                         float* hidden_last, void* stream);
 
-/* The exit window rksc_verify_forward uses for n_branches branches: 4 up to 16
- * branches, 2 up to 32, else 1. */
-int32_t rksc_verify_window(int32_t n_branches);
+/* The exit window rksc_verify_forward uses for this pass (B = n_branches
+ * branches of s = branch_len tokens over an n_prefix-token cache): a power of
+ * two in [1, min(8, 64 / B)] from a cost model of the schedule. Over L layers
+ * the probe pays L / w streams of W_lm, and an exit, taken as uniformly placed
+ * within its window, wastes (w - 1) / 2 computed layers on average; the window
+ * nearest sqrt(2 L c_probe / c_layer) minimises the sum, with c_probe the
+ * W_lm stream and c_layer a layer's projections, attention and row kernels,
+ * both estimated from the shapes. Outputs do not depend on the window.
+ * Returns 0 for an invalid shape (rksc_last_error() says why). */
+int32_t rksc_verify_window(const rksc_model_config* cfg, int32_t n_branches, int32_t branch_len, int32_t n_prefix);
 
 /* rksc_verify_forward with the exit window chosen by the caller: window = 1 is
  * the layer-by-layer schedule (a branch stops at its exit layer); window in
@@ -266,28 +284,31 @@ rksc_status rksc_decode_step(const rksc_weights* weights, const rksc_prefix_kv* 
                              const int32_t* tokens, int32_t n_branches, int32_t* next_token, float* p_top,
                              float* conf, void* workspace, size_t workspace_bytes, void* stream);
 
-/* Bytes of workspace rksc_prefix_extend needs for n_new tokens on top of an
- * n_parent-entry cache (0 if the shape is invalid). */
+/* Bytes of workspace rksc_prefix_extend needs for n_new tokens on top of a
+ * parent prefix of n_parent entries in all (0 if the shape is invalid). */
 size_t rksc_prefix_extend_workspace_size(const rksc_model_config* cfg, int32_t n_parent, int32_t n_new);
 
 /*
  * Tree sharing (Sec. 1: siblings share an intermediate node; the same
  * "compute once, broadcast" of Sec. 2.2 one level down): the cache of a
- * search-tree node whose m tokens follow its parent's n cached entries. The
- * child cache receives the parent's entries 0..n-1 (copied) and the entries
- * n..n+m-1 of the node's tokens, computed in one causal pass at positions
- * n..n+m-1 over the parent cache; every child of the node then uses it as its
- * rksc_prefix_kv (n_prefix = n + m) in rksc_verify_forward / rksc_decode_*.
- * h_node receives the node's own "root" rows for the next level's ASKS gate:
- * the last new token's layer outputs, unit-normalised (as h_root of
+ * search-tree node whose m tokens follow its parent's prefix (the chain ending
+ * at `parent`, n entries in all). The node's tokens are computed in one causal
+ * pass at positions n..n+m-1 over that prefix, read in place, and k_out/v_out
+ * receive only their m entries. Every child of the node then passes
+ * {m, k_out, v_out, parent} as its rksc_prefix_kv in rksc_verify_forward /
+ * rksc_decode_* (the chain of its ancestors' caches plus the node's: nothing
+ * is copied). h_node receives the node's own "root" rows for the next level's
+ * ASKS gate: the last new token's layer outputs, unit-normalised (as h_root of
  * rksc_prefill; with n = 0 this call is rksc_prefill).
  *
- * parent     the parent cache, n >= 0 entries [L, Hkv, n, hd]; it must not
- *            overlap k_out / v_out.
+ * parent     the parent's prefix chain (n >= 0 entries in all, at most
+ *            RKSC_MAX_PREFIX_SEGMENTS - 1 caches, so that the children's chain
+ *            fits); no cache of it may overlap k_out / v_out.
  * tokens     [m] int32 device (m = n_new >= 1).
- * k_out      [L, Hkv, n + m, hd] device out, storage type; v_out likewise.
+ * k_out      [L, Hkv, m, hd] device out, storage type; v_out likewise.
  * h_node     [L, d] fp32 device out, or NULL.
- * workspace  at least rksc_prefix_extend_workspace_size() bytes, 256-byte aligned.
+ * workspace  at least rksc_prefix_extend_workspace_size(cfg, n, m) bytes,
+ *            256-byte aligned.
  */
 rksc_status rksc_prefix_extend(const rksc_weights* weights, const rksc_prefix_kv* parent, const int32_t* tokens,
                                int32_t n_new, void* k_out, void* v_out, float* h_node, void* workspace,

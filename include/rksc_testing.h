@@ -51,6 +51,18 @@ rksc_status rksc_test_gemm_live(int32_t dtype, const void* A, const void* A_lo, 
                                 int32_t N, int32_t K, int32_t splits, int32_t kind, int32_t live_count,
                                 int32_t branch_len, void* ctrl_scratch, int32_t* splits_used, void* stream);
 
+/* The gate|up projection with its SwiGLU (the down projection's input), bf16
+ * weights: a = silu(A W_gate^T) * (A W_up^T) for W [2F, K] (gate rows, then up
+ * rows), the activation given as bf16 hi/lo planes A, A_lo [M, K]. a_out
+ * receives a as bf16 hi/lo planes [M, F] (hi at a_out, lo M * F elements
+ * later). fused = 1: the 256 x 256 kernel over one K split with the SwiGLU in
+ * its epilogue (what the verify pass runs for projections with many rows;
+ * RKSC_ERR_UNSUPPORTED if the planner has no such plan for the shape);
+ * fused = 0: the 128-row kernel's split partials in P (8 * M * 2F floats)
+ * combined by the SwiGLU kernel. */
+rksc_status rksc_test_gate_up_swiglu(const void* A, const void* A_lo, const void* W, void* a_out, float* P,
+                                     int32_t M, int32_t F, int32_t K, int32_t fused, void* stream);
+
 /* The plan rksc_test_gemm_kind would launch for this shape, without launching
  * anything (host only): plan[0..4] = kernel kind (0, 1 or 2 as above), rows
  * and columns of a workgroup's output tile, number of K splits, K elements per

@@ -23,13 +23,14 @@ __all__ = [
     "RkscError", "load_library", "library_path",
     "rksc_abi_version", "rksc_verify_workspace_size", "rksc_verify_forward", "rksc_verify_window",
     "rksc_asks_similarity", "rksc_status_string", "rksc_last_error",
-    "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_gemm_live", "rksc_test_gemm_plan", "rksc_test_attention",
+    "rksc_test_gemm", "rksc_test_gemm_kind", "rksc_test_gemm_live", "rksc_test_gemm_plan", "rksc_test_gate_up_swiglu", "rksc_test_attention",
     "verify_forward", "asks_similarity", "prefill", "rksc_prefill", "rksc_prefill_workspace_size", "model_config",
     "BranchCache", "Decoder", "rksc_decode_workspace_size", "rksc_decode_suffix", "rksc_decode_step",
     "rksc_cgee_gate", "cgee_gate", "RKSC_ABI_VERSION", "BlockTable", "KVProbe",
     "rksc_prefix_extend", "rksc_prefix_extend_workspace_size", "prefix_extend", "rksc_asks_gate", "asks_gate",
     "RKSC_OK", "RKSC_ERR_INVALID_ARGUMENT", "RKSC_ERR_UNSUPPORTED",
     "RKSC_ERR_WORKSPACE_TOO_SMALL", "RKSC_ERR_HIP", "RKSC_F32", "RKSC_BF16", "RKSC_MAX_BRANCHES",
+    "RKSC_MAX_PREFIX_SEGMENTS", "PrefixCache", "PrefixKV",
 ]
 
 RKSC_OK = 0
@@ -40,7 +41,8 @@ RKSC_ERR_HIP = -4
 RKSC_F32 = 0
 RKSC_BF16 = 1
 RKSC_MAX_BRANCHES = 64
-RKSC_ABI_VERSION = 6
+RKSC_MAX_PREFIX_SEGMENTS = 8
+RKSC_ABI_VERSION = 7
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 
@@ -79,7 +81,29 @@ class Weights(ctypes.Structure):
 
 
 class PrefixKV(ctypes.Structure):
-    _fields_ = [("n_prefix", ctypes.c_int32), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p)]
+    pass
+
+
+PrefixKV._fields_ = [("n_prefix", ctypes.c_int32), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                     ("parent", ctypes.POINTER(PrefixKV))]
+
+
+class PrefixCache:
+    """A shared prefix made of caches in position order (tree sharing, Sec. 2.2): segments
+    [(k, v), ...], each [L, Hkv, n_i, hd] in the model dtype, the root's first. Pass it as
+    `prefix_k` (with prefix_v None) wherever a prefix cache is taken; the library reads the
+    segments in place as one prefix of n_prefix = sum n_i entries."""
+
+    def __init__(self, segments):
+        self.segments = [(k, v) for k, v in segments]
+
+    @property
+    def n_prefix(self) -> int:
+        return sum(int(k.shape[2]) for k, _ in self.segments)
+
+    def extend(self, k, v) -> "PrefixCache":
+        """The prefix of a search-tree node's children: these segments, then the node's own cache."""
+        return PrefixCache(self.segments + [(k, v)])
 
 
 class BranchKVStruct(ctypes.Structure):
@@ -116,7 +140,7 @@ def load_library():
     lib.rksc_test_verify_precision.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32,
                                                i32, vp, vp, vp, vp, sz, vp, ctypes.c_uint32]
     lib.rksc_verify_window.restype = i32
-    lib.rksc_verify_window.argtypes = [i32]
+    lib.rksc_verify_window.argtypes = [ctypes.POINTER(ModelConfig), i32, i32, i32]
     lib.rksc_verify_forward_window.restype = i32
     lib.rksc_verify_forward_window.argtypes = [ctypes.POINTER(Weights), ctypes.POINTER(PrefixKV), vp, i32, i32, f32,
                                                i32, vp, vp, vp, vp, sz, vp, i32]
@@ -182,6 +206,8 @@ def load_library():
     lib.rksc_test_gemm_live.restype = i32
     lib.rksc_test_gemm_live.argtypes = [i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp,
                                         ctypes.POINTER(i32), vp]
+    lib.rksc_test_gate_up_swiglu.restype = i32
+    lib.rksc_test_gate_up_swiglu.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, vp]
     lib.rksc_test_gemm_plan.restype = i32
     lib.rksc_test_gemm_plan.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(i32)]
     lib.rksc_test_attention.restype = i32
@@ -258,15 +284,50 @@ def _check_weights(need, weights, need_lm_head: bool = True):
 
 
 def _check_prefix(need, weights, prefix_k, prefix_v, name="prefix"):
-    """The shared cache [L, Hkv, n, hd] in the model dtype (both None: an empty prefix). Returns n."""
+    """The shared prefix: a cache [L, Hkv, n, hd] in the model dtype (k and v), a PrefixCache of such
+    segments (in prefix_k, prefix_v None), or nothing (both None). Returns the total n."""
     if prefix_k is None and prefix_v is None:
         return 0
+    if isinstance(prefix_k, PrefixCache):
+        if prefix_v is not None:
+            raise ValueError(f"{name}: pass a PrefixCache as {name}_k with {name}_v None")
+        if len(prefix_k.segments) > RKSC_MAX_PREFIX_SEGMENTS:
+            raise ValueError(f"{name}: at most {RKSC_MAX_PREFIX_SEGMENTS} segments")
+        return sum(_check_prefix(need, weights, k, v, f"{name} segment {i}")
+                   for i, (k, v) in enumerate(prefix_k.segments))
     shape = weights.shape
     dims = (len(weights.layers), shape.n_kv_heads, None, shape.head_dim)
     need(prefix_k, f"{name}_k", _model_dtype(shape), dims)
     n = int(prefix_k.shape[2])
     need(prefix_v, f"{name}_v", _model_dtype(shape), dims[:2] + (n, dims[3]))
     return n
+
+
+def _prefix_len(prefix_k) -> int:
+    """Entries of a prefix: a cache tensor, a PrefixCache or None."""
+    if prefix_k is None:
+        return 0
+    if isinstance(prefix_k, PrefixCache):
+        return prefix_k.n_prefix
+    return int(prefix_k.shape[2])
+
+
+def _prefix_struct(prefix_k, prefix_v):
+    """rksc_prefix_kv of the prefix (a chain for a PrefixCache); returns (struct, objects to keep)."""
+    if not isinstance(prefix_k, PrefixCache):
+        kv = PrefixKV(_prefix_len(prefix_k), _ptr(prefix_k), _ptr(prefix_v))
+        return kv, [kv]
+    keep, prev = [], None
+    for k, v in prefix_k.segments:
+        kv = PrefixKV(int(k.shape[2]), _ptr(k), _ptr(v))
+        if prev is not None:
+            kv.parent = ctypes.pointer(prev)
+        keep.append(kv)
+        prev = kv
+    if prev is None:
+        prev = PrefixKV(0, None, None)
+        keep.append(prev)
+    return prev, keep
 
 
 def _stream(stream):
@@ -316,8 +377,13 @@ def _weights_struct(weights):
     return w, layers
 
 
-def rksc_verify_window(n_branches: int) -> int:
-    return int(load_library().rksc_verify_window(int(n_branches)))
+def rksc_verify_window(shape, n_branches: int, branch_len: int, n_prefix: int) -> int:
+    """The exit window rksc_verify_forward takes for this pass (a cost model of the schedule)."""
+    cfg = model_config(shape)
+    w = int(load_library().rksc_verify_window(ctypes.byref(cfg), int(n_branches), int(branch_len), int(n_prefix)))
+    if w == 0:
+        raise RkscError(RKSC_ERR_INVALID_ARGUMENT, rksc_last_error())
+    return w
 
 
 def rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, patience: int,
@@ -343,7 +409,7 @@ def rksc_verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, 
     need.done()
     lib = load_library()
     w, layers_keepalive = _weights_struct(weights)
-    kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
+    kv, kv_keep = _prefix_struct(prefix_k, prefix_v)
     args = (ctypes.byref(w), ctypes.byref(kv), _ptr(branch_tokens), int(B), int(s), float(tau), int(patience),
             _ptr(entropy), _ptr(exit_layer), _ptr(hidden_last), _ptr(workspace),
             int(workspace.numel() * workspace.element_size()), _stream(stream))
@@ -376,7 +442,7 @@ def rksc_verify_forward_noalloc(weights, prefix_k, prefix_v, branch_tokens, tau:
     need.done()
     lib = load_library()
     w, layers_keepalive = _weights_struct(weights)
-    kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
+    kv, kv_keep = _prefix_struct(prefix_k, prefix_v)
     st = lib.rksc_verify_forward_noalloc(ctypes.byref(w), ctypes.byref(kv), _ptr(branch_tokens), int(B), int(s),
                                          float(tau), int(patience), _ptr(entropy), _ptr(exit_layer),
                                          _ptr(hidden_last), _stream(stream))
@@ -405,7 +471,7 @@ def rksc_test_verify_precision(weights, prefix_k, prefix_v, branch_tokens, tau: 
     ex = torch.empty((B,), dtype=torch.int32, device=dev)
     hid = torch.empty((L, B, d), dtype=torch.float32, device=dev)
     w, keep = _weights_struct(weights)
-    kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
+    kv, kv_keep = _prefix_struct(prefix_k, prefix_v)
     _check(load_library().rksc_test_verify_precision(ctypes.byref(w), ctypes.byref(kv), _ptr(branch_tokens), int(B),
                                                      int(s), float(tau), int(patience), _ptr(ent), _ptr(ex),
                                                      _ptr(hid), _ptr(ws), ws.numel(), _stream(stream),
@@ -522,6 +588,24 @@ def rksc_test_gemm_live(A, W: torch.Tensor, live_count: int, branch_len: int, P:
     return used.value
 
 
+def rksc_test_gate_up_swiglu(A, W: torch.Tensor, fused: bool, stream=None) -> torch.Tensor:
+    """The gate|up projection and its SwiGLU through the library's kernels: A = (hi, lo) bf16 planes
+    [M, K], W [2F, K] bf16. Returns a = silu(gate) * up [M, F] as fp32 (hi + lo of the output planes)."""
+    a_hi, a_lo = A
+    need = _Args()
+    need(a_hi, "A", torch.bfloat16, ndim=2)
+    M, K = a_hi.shape
+    need(a_lo, "A_lo", torch.bfloat16, (M, K))
+    need(W, "W", torch.bfloat16, (None, K))
+    need.done()
+    F = int(W.shape[0]) // 2
+    out = torch.empty((2, M, F), dtype=torch.bfloat16, device=a_hi.device)
+    P = torch.empty((8, M, 2 * F), dtype=torch.float32, device=a_hi.device)
+    _check(load_library().rksc_test_gate_up_swiglu(_ptr(a_hi), _ptr(a_lo), _ptr(W), _ptr(out), _ptr(P), M, F, K,
+                                                   1 if fused else 0, _stream(stream)))
+    return out[0].float() + out[1].float()
+
+
 def rksc_test_attention(q, prefix_k, prefix_v, k_own, v_own, dtype, stream=None):
     """Kernel-level shared-prefix attention: q [B*s, H, hd], own [B, Hkv, s, hd] fp32; prefix [Hkv, n, hd]
     of `dtype` (torch.bfloat16 or torch.float32). Returns o [B*s, H*hd] as fp32 (bf16 hi/lo planes are
@@ -564,7 +648,7 @@ def verify_forward(weights, prefix_k, prefix_v, branch_tokens, tau: float, patie
     dev = branch_tokens.device
     L = len(weights.layers)
     if workspace is None:
-        n_prefix = int(prefix_k.shape[2]) if prefix_k is not None else 0
+        n_prefix = _prefix_len(prefix_k)
         workspace = torch.empty(rksc_verify_workspace_size(shape, B, s, n_prefix), dtype=torch.uint8, device=dev)
     entropy = torch.empty((L, B), dtype=torch.float32, device=dev)
     exit_layer = torch.empty((B,), dtype=torch.int32, device=dev)
@@ -653,7 +737,7 @@ def rksc_decode_suffix(weights, prefix_k, prefix_v, cache: BranchCache, suffix_t
     _check_decode_outputs(need, weights, cache, B, next_token, p_top, conf, workspace)
     lib = load_library()
     w, layers_keepalive = _weights_struct(weights)
-    kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
+    kv, kv_keep = _prefix_struct(prefix_k, prefix_v)
     st = lib.rksc_decode_suffix(ctypes.byref(w), ctypes.byref(kv), ctypes.byref(cache.struct), _ptr(suffix_tokens),
                                 int(B), int(s), _ptr(next_token), _ptr(p_top), _ptr(conf), _ptr(workspace),
                                 int(workspace.numel() * workspace.element_size()), _stream(stream))
@@ -672,7 +756,7 @@ def rksc_decode_step(weights, prefix_k, prefix_v, cache: BranchCache, tokens: to
     _check_decode_outputs(need, weights, cache, int(tokens.numel()), next_token, p_top, conf, workspace)
     lib = load_library()
     w, layers_keepalive = _weights_struct(weights)
-    kv = PrefixKV(n, _ptr(prefix_k), _ptr(prefix_v))
+    kv, kv_keep = _prefix_struct(prefix_k, prefix_v)
     st = lib.rksc_decode_step(ctypes.byref(w), ctypes.byref(kv), ctypes.byref(cache.struct), _ptr(tokens),
                               int(tokens.numel()), _ptr(next_token), _ptr(p_top), _ptr(conf), _ptr(workspace),
                               int(workspace.numel() * workspace.element_size()), _stream(stream))
@@ -718,7 +802,7 @@ class Decoder:
     def __init__(self, weights, prefix_k, prefix_v, n_branches: int, suffix_len: int, capacity: int, device):
         shape = weights.shape
         self.weights, self.prefix_k, self.prefix_v = weights, prefix_k, prefix_v
-        n = int(prefix_k.shape[2]) if prefix_k is not None else 0
+        n = _prefix_len(prefix_k)
         self.cache = BranchCache(shape, len(weights.layers), n_branches, capacity, device)
         self.workspace = torch.empty(rksc_decode_workspace_size(shape, n_branches, suffix_len, n),
                                      dtype=torch.uint8, device=device)
@@ -860,7 +944,7 @@ def rksc_prefix_extend(weights, parent_k, parent_v, tokens: torch.Tensor, k_out:
     n = _check_prefix(need, weights, parent_k, parent_v, "parent")
     need(tokens, "tokens", torch.int32, ndim=1)
     shape, L = weights.shape, len(weights.layers)
-    dims = (L, shape.n_kv_heads, n + int(tokens.numel()), shape.head_dim)
+    dims = (L, shape.n_kv_heads, int(tokens.numel()), shape.head_dim)
     need(k_out, "k_out", _model_dtype(shape), dims)
     need(v_out, "v_out", _model_dtype(shape), dims)
     if h_node is not None:
@@ -869,7 +953,7 @@ def rksc_prefix_extend(weights, parent_k, parent_v, tokens: torch.Tensor, k_out:
     need.done()
     lib = load_library()
     w, keep = _weights_struct(weights)
-    kv = PrefixKV(n, _ptr(parent_k), _ptr(parent_v))
+    kv, kv_keep = _prefix_struct(parent_k, parent_v)
     st = lib.rksc_prefix_extend(ctypes.byref(w), ctypes.byref(kv), _ptr(tokens), int(tokens.numel()), _ptr(k_out),
                                 _ptr(v_out), _ptr(h_node), _ptr(workspace),
                                 int(workspace.numel() * workspace.element_size()), _stream(stream))
@@ -878,15 +962,17 @@ def rksc_prefix_extend(weights, parent_k, parent_v, tokens: torch.Tensor, k_out:
 
 
 def prefix_extend(weights, parent_k, parent_v, tokens: torch.Tensor, stream=None):
-    """A tree node's cache on top of its parent's: returns (k [L, Hkv, n+m, hd], v, h_node [L, d] unit rows)."""
+    """A tree node's cache on top of its parent's prefix (a cache, or a PrefixCache in parent_k):
+    returns (k [L, Hkv, m, hd], v, h_node [L, d] unit rows), the node's own m entries. The node's
+    children read PrefixCache(parent segments).extend(k, v) as their prefix."""
     shape = weights.shape
-    n = int(parent_k.shape[2]) if parent_k is not None else 0
+    n = _prefix_len(parent_k)
     m = int(tokens.numel())
     dev = tokens.device
     L = len(weights.layers)
     dtype = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
     ws = torch.empty(rksc_prefix_extend_workspace_size(shape, n, m), dtype=torch.uint8, device=dev)
-    k = torch.empty((L, shape.n_kv_heads, n + m, shape.head_dim), dtype=dtype, device=dev)
+    k = torch.empty((L, shape.n_kv_heads, m, shape.head_dim), dtype=dtype, device=dev)
     v = torch.empty_like(k)
     h = torch.empty((L, shape.d_model), dtype=torch.float32, device=dev)
     rksc_prefix_extend(weights, parent_k, parent_v, tokens.contiguous(), k, v, h, ws, stream)

@@ -34,6 +34,23 @@ __device__ __forceinline__ uint4 keep_if(bool c, const uint4& a) {
   return make_uint4(c ? a.x : 0u, c ? a.y : 0u, c ? a.z : 0u, c ? a.w : 0u);
 }
 
+// Row `key` (a position in the shared prefix) of KV head kvh: the segment that
+// holds the position (segments are in position order; the loop bound is uniform,
+// so with one segment it is a single compare) and the row within it.
+template <typename T, int HD>
+__device__ __forceinline__ const T* prefix_row(const PrefixView& P, bool isv, int kvh, int key) {
+  const void* base = isv ? P.v[0] : P.k[0];
+  int off = key, ln = P.len[0];
+  for (int j = 1; j < P.nseg; ++j) {
+    if (key >= P.start[j]) {
+      base = isv ? P.v[j] : P.k[j];
+      off = key - P.start[j];
+      ln = P.len[j];
+    }
+  }
+  return static_cast<const T*>(base) + ((size_t)kvh * ln + off) * HD;
+}
+
 // V^T tile layout: row = head dimension, column = key position. Within each
 // 32-key block the eight keys that one lane group feeds to a P.V MFMA
 // ({4g..4g+3} and {16+4g..16+4g+3}, the keys whose probabilities the lane
@@ -104,13 +121,14 @@ __device__ __forceinline__ void lds_wait_pairs(shortx4 (&a)[ND], shortx4 (&b)[ND
 // 8 waves x 16 query columns = 128 query rows per workgroup.
 // PS: the probabilities meet V as a bf16 hi/lo pair (two MFMAs); without it, as
 // bf16(p) alone (one MFMA, ~2^-9 relative rounding of each weight).
-template <int HD, bool XB, bool PS = true>
-__global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, const bf16* __restrict__ pk,
-                                                   const bf16* __restrict__ pv, const float* __restrict__ ko,
+template <int HD, bool XB, bool PS = true, bool MS = false>
+__global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, const PrefixView pre,
+                                                   const float* __restrict__ ko,
                                                    const float* __restrict__ vo, void* __restrict__ o,
                                                    float* __restrict__ opart, float* __restrict__ mlpart,
-                                                   const Ctrl* c, int n, int s, int H, int Hkv, float sl2,
+                                                   const Ctrl* c, int s, int H, int Hkv, float sl2,
                                                    int nchunks, int max_rows) {
+  const int n = pre.n;
   constexpr int NW = kAttnWaves, NT = NW * 64, QT = 16 * NW;
   constexpr int KT = 64;                   // keys per tile
   constexpr int CPR = HD / 8;              // 16-byte chunks per key row
@@ -136,16 +154,21 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   uint16_t* const Vt0 = Ks1 + KT * LDK;                        //            V^T hi [HD][LDV]
   uint16_t* const Vt1 = Vt0 + HD * LDV;                        //            V^T lo
 
-  // Fused mode: blockIdx.z = chunk * slots + slot, rows of one branch.
-  // XB mode: blockIdx.z = chunk, rows of all live branches, prefix tiles only.
+  // Work order: the hardware's (linear id round robin over the 8 XCDs). Mapping
+  // each KV head to one XCD fetched the head's prefix about once (at 16 branches
+  // x 256 tokens over 2048 prefix tokens, 126 instead of 573 MB per launch) but
+  // ran 7% slower, and rotating the tile order on top of it slower still.
+  const int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  // Fused mode: bz = chunk * slots + slot, rows of one branch.
+  // XB mode: bz = chunk, rows of all live branches, prefix tiles only.
   const int B_slots = XB ? 1 : gridDim.z / nchunks;
-  const int chunk = blockIdx.z / B_slots;
-  const int bslot = blockIdx.z % B_slots;
+  const int chunk = bz / B_slots;
+  const int bslot = bz % B_slots;
   if (!XB && bslot >= c->live_count) return;
-  const int kvh = blockIdx.y;
+  const int kvh = by;
   const int G = H / Hkv;
   const int rows = XB ? c->live_count * s * G : G * s;
-  const int row0 = blockIdx.x * QT;
+  const int row0 = bx * QT;
   if (row0 >= rows) return;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
@@ -153,8 +176,14 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   const int i_max = min(s - 1, (min(row0 + QT - 1, rows - 1)) / G);
   const int n_ptiles = (n + KT - 1) / KT;
   const int n_full = n / KT;      // prefix tiles with no key past n - 1
-  const int n_tiles = XB ? n_ptiles : n_ptiles + i_max / KT + 1;
-  const int t_begin = chunk * n_tiles / nchunks, t_end = (chunk + 1) * n_tiles / nchunks;
+  // Split-KV chunks by cost: an own-span tile (fp32 keys and values staged through
+  // registers, three MFMAs per product) counts as two prefix tiles, so that the
+  // chunk holding the own span is not the straggler. f(x) = tiles whose cost
+  // interval starts below x (prefix tile i at i, own tile j at n_ptiles + 2j).
+  const int n_own = XB ? 0 : i_max / KT + 1;
+  const int cost = n_ptiles + 2 * n_own;
+  auto tiles_below = [&](int x) { return min(n_ptiles, x) + min(n_own, max(0, (x - n_ptiles + 1) / 2)); };
+  const int t_begin = tiles_below(chunk * cost / nchunks), t_end = tiles_below((chunk + 1) * cost / nchunks);
 
   // The query this lane owns as an MFMA column. Rows past the end compute a
   // duplicate of the last row and are not stored.
@@ -185,8 +214,6 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   for (int dt = 0; dt < ND; ++dt) oacc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
 
-  const bf16* Kp = pk + (size_t)kvh * n * HD;
-  const bf16* Vp = pv + (size_t)kvh * n * HD;
   const float* Ko = ko + ((size_t)slot * Hkv + kvh) * s * HD;
   const float* Vo = vo + ((size_t)slot * Hkv + kvh) * s * HD;
 
@@ -221,13 +248,41 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   }
   const uint32_t smem_lds = (uint32_t)reinterpret_cast<uintptr_t>(smem);   // LDS byte offset of the ring
 
+  // One segment (MS = false): every row from the one base, straight-line code.
+  // Several (MS): a tile inside one segment addresses its rows from that
+  // segment's base, found once per tile with scalar compares; only a tile that
+  // straddles a segment boundary looks up each row. A per-row lookup in the
+  // one-segment kernel cost it 13-18% (branches between the DMAs of a tile).
+  const bf16* const Kp0 = static_cast<const bf16*>(pre.k[0]) + (size_t)kvh * pre.len[0] * HD;
+  const bf16* const Vp0 = static_cast<const bf16*>(pre.v[0]) + (size_t)kvh * pre.len[0] * HD;
   auto issue = [&](int pt, int sl) {
     const int kbase = pt * KT;
+    if constexpr (!MS) {
 #pragma unroll
-    for (int j = 0; j < IPW; ++j) {
-      const int key = min(kbase + dkey[j], n - 1);   // rows past n - 1 are masked in the contraction
-      const bf16* src = (dv[j] ? Vp : Kp) + (size_t)key * HD + dsrc[j];
-      dma16(src, smem + sl * SLOT + ddst[j]);
+      for (int j = 0; j < IPW; ++j) {
+        const int key = min(kbase + dkey[j], n - 1);   // rows past n - 1 are masked in the contraction
+        dma16((dv[j] ? Vp0 : Kp0) + (size_t)key * HD + dsrc[j], smem + sl * SLOT + ddst[j]);
+      }
+    } else {
+      int sg = 0;
+      for (int j = 1; j < pre.nseg; ++j) sg = kbase >= pre.start[j] ? j : sg;
+      const int klast = min(kbase + KT, n) - 1;
+      if (sg + 1 == pre.nseg || klast < pre.start[sg + 1]) {
+        const int kofs = kbase - pre.start[sg];   // row of the tile's first key within its segment
+        const bf16* Kt = static_cast<const bf16*>(pre.k[sg]) + ((size_t)kvh * pre.len[sg] + kofs) * HD;
+        const bf16* Vt = static_cast<const bf16*>(pre.v[sg]) + ((size_t)kvh * pre.len[sg] + kofs) * HD;
+#pragma unroll
+        for (int j = 0; j < IPW; ++j) {
+          const int key = min(kbase + dkey[j], n - 1);
+          dma16((dv[j] ? Vt : Kt) + (size_t)(key - kbase) * HD + dsrc[j], smem + sl * SLOT + ddst[j]);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < IPW; ++j) {
+          const int key = min(kbase + dkey[j], n - 1);
+          dma16(prefix_row<bf16, HD>(pre, dv[j], kvh, key) + dsrc[j], smem + sl * SLOT + ddst[j]);
+        }
+      }
     }
   };
 
@@ -823,11 +878,11 @@ __global__ __launch_bounds__(256) void k_attn_combine_dec(const float* __restric
 // fp32 models, decode: one thread per (branch, head) over the prefix, the
 // branch's cached entries 0..len-1 and its own new key.
 template <int HD>
-__global__ __launch_bounds__(128) void k_attn_f32_dec(const float* __restrict__ q, const float* __restrict__ pk,
-                                                      const float* __restrict__ pv, const float* __restrict__ ck,
+__global__ __launch_bounds__(128) void k_attn_f32_dec(const float* __restrict__ q, const PrefixView pre,
+                                                      const float* __restrict__ ck,
                                                       const float* __restrict__ cv, int len, int cap,
                                                       const float* __restrict__ ko, const float* __restrict__ vo,
-                                                      float* __restrict__ o, const Ctrl* c, int n, int H, int Hkv,
+                                                      float* __restrict__ o, const Ctrl* c, int H, int Hkv,
                                                       float scale) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= c->live_count * H) return;
@@ -847,9 +902,11 @@ __global__ __launch_bounds__(128) void k_attn_f32_dec(const float* __restrict__ 
     for (int d = 0; d < HD; ++d) acc[d] = acc[d] * a + p * vr[d];
     m = mn;
   };
-  const float* Kp = pk + (size_t)kvh * n * HD;
-  const float* Vp = pv + (size_t)kvh * n * HD;
-  for (int j = 0; j < n; ++j) visit(Kp + (size_t)j * HD, Vp + (size_t)j * HD);
+  for (int sg = 0; sg < pre.nseg; ++sg) {
+    const float* Kp = static_cast<const float*>(pre.k[sg]) + (size_t)kvh * pre.len[sg] * HD;
+    const float* Vp = static_cast<const float*>(pre.v[sg]) + (size_t)kvh * pre.len[sg] * HD;
+    for (int j = 0; j < pre.len[sg]; ++j) visit(Kp + (size_t)j * HD, Vp + (size_t)j * HD);
+  }
   const float* Kc = ck + ((size_t)b * Hkv + kvh) * cap * HD;
   const float* Vc = cv + ((size_t)b * Hkv + kvh) * cap * HD;
   for (int j = 0; j < len; ++j) visit(Kc + (size_t)j * HD, Vc + (size_t)j * HD);
@@ -860,10 +917,10 @@ __global__ __launch_bounds__(128) void k_attn_f32_dec(const float* __restrict__ 
 
 // fp32 models: one thread per (query row, head), plain online softmax.
 template <int HD>
-__global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ q, const float* __restrict__ pk,
-                                                  const float* __restrict__ pv, const float* __restrict__ ko,
+__global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ q, const PrefixView pre,
+                                                  const float* __restrict__ ko,
                                                   const float* __restrict__ vo, float* __restrict__ o,
-                                                  const Ctrl* c, int n, int s, int H, int Hkv, float scale) {
+                                                  const Ctrl* c, int s, int H, int Hkv, float scale) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= c->live_count * s * H) return;
   const int r = idx / H, h = idx % H;
@@ -883,9 +940,11 @@ __global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ q, c
     for (int d = 0; d < HD; ++d) acc[d] = acc[d] * a + p * vr[d];
     m = mn;
   };
-  const float* Kp = pk + (size_t)kvh * n * HD;
-  const float* Vp = pv + (size_t)kvh * n * HD;
-  for (int j = 0; j < n; ++j) visit(Kp + (size_t)j * HD, Vp + (size_t)j * HD);
+  for (int sg = 0; sg < pre.nseg; ++sg) {
+    const float* Kp = static_cast<const float*>(pre.k[sg]) + (size_t)kvh * pre.len[sg] * HD;
+    const float* Vp = static_cast<const float*>(pre.v[sg]) + (size_t)kvh * pre.len[sg] * HD;
+    for (int j = 0; j < pre.len[sg]; ++j) visit(Kp + (size_t)j * HD, Vp + (size_t)j * HD);
+  }
   const float* Ko = ko + ((size_t)slot * Hkv + kvh) * s * HD;
   const float* Vo = vo + ((size_t)slot * Hkv + kvh) * s * HD;
   for (int j = 0; j <= i; ++j) visit(Ko + (size_t)j * HD, Vo + (size_t)j * HD);
@@ -920,9 +979,22 @@ AttnPlan plan_attention(DType dt, int B, int n, int s, int H, int Hkv) {
   return p;
 }
 
-hipError_t launch_attention_decode(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,
+namespace {
+// k_attn_bf16 with the probabilities split into hi/lo (p_split) or not, over a
+// prefix of one segment or of several (multi_seg).
+template <int HD, bool XB, typename... Args>
+void launch_attn_tiles(bool p_split, bool multi_seg, dim3 grid, hipStream_t st, Args... args) {
+  const dim3 blk(64 * kAttnWaves);
+  if (p_split && !multi_seg) hipLaunchKernelGGL((k_attn_bf16<HD, XB, true, false>), grid, blk, 0, st, args...);
+  else if (p_split) hipLaunchKernelGGL((k_attn_bf16<HD, XB, true, true>), grid, blk, 0, st, args...);
+  else if (!multi_seg) hipLaunchKernelGGL((k_attn_bf16<HD, XB, false, false>), grid, blk, 0, st, args...);
+  else hipLaunchKernelGGL((k_attn_bf16<HD, XB, false, true>), grid, blk, 0, st, args...);
+}
+}  // namespace
+
+hipError_t launch_attention_decode(DType dt, const AttnPlan& p, const void* q, const PrefixView& pre,
                                    const void* ck, const void* cv, int len, int cap, const void* k_own,
-                                   const void* v_own, void* o, float* opart, float* mlpart, const Ctrl* c, int n,
+                                   const void* v_own, void* o, float* opart, float* mlpart, const Ctrl* c,
                                    int H, int Hkv, int hd, int B, hipStream_t st) {
   const float* qq = static_cast<const float*>(q);
   const float *ko = static_cast<const float*>(k_own), *vo = static_cast<const float*>(v_own);
@@ -930,16 +1002,15 @@ hipError_t launch_attention_decode(DType dt, const AttnPlan& p, const void* q, c
     const float sl2 = 1.4426950408889634f / sqrtf((float)hd);
     const int G = H / Hkv;
     const int max_rows = B;   // one token per branch
-    const bf16 *kk = static_cast<const bf16*>(pk), *vv = static_cast<const bf16*>(pv);
     const bf16 *cka = static_cast<const bf16*>(ck), *cva = static_cast<const bf16*>(cv);
     if (p.chunks > 0) {
       const dim3 grid((max_rows * G + 16 * kAttnWaves - 1) / (16 * kAttnWaves), Hkv, p.chunks);
       if (hd == 128)
-        hipLaunchKernelGGL((k_attn_bf16<128, true>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, o, opart,
-                           mlpart, c, n, 1, H, Hkv, sl2, p.chunks, max_rows);
+        launch_attn_tiles<128, true>(true, pre.nseg > 1, grid, st, qq, pre, ko, vo, o, opart, mlpart, c, 1, H, Hkv,
+                                     sl2, p.chunks, max_rows);
       else
-        hipLaunchKernelGGL((k_attn_bf16<64, true>), grid, dim3(64 * kAttnWaves), 0, st, qq, kk, vv, ko, vo, o, opart,
-                           mlpart, c, n, 1, H, Hkv, sl2, p.chunks, max_rows);
+        launch_attn_tiles<64, true>(true, pre.nseg > 1, grid, st, qq, pre, ko, vo, o, opart, mlpart, c, 1, H, Hkv,
+                                    sl2, p.chunks, max_rows);
     }
     const dim3 cgrid((B * H * 64 + 255) / 256);
     if (hd == 128)
@@ -951,52 +1022,40 @@ hipError_t launch_attention_decode(DType dt, const AttnPlan& p, const void* q, c
   } else {
     const float scale = 1.f / sqrtf((float)hd);
     const dim3 grid((B * H + 127) / 128);
-    const float *kk = static_cast<const float*>(pk), *vv = static_cast<const float*>(pv);
     const float *cka = static_cast<const float*>(ck), *cva = static_cast<const float*>(cv);
     if (hd == 128)
-      hipLaunchKernelGGL(k_attn_f32_dec<128>, grid, dim3(128), 0, st, qq, kk, vv, cka, cva, len, cap, ko, vo,
-                         static_cast<float*>(o), c, n, H, Hkv, scale);
+      hipLaunchKernelGGL(k_attn_f32_dec<128>, grid, dim3(128), 0, st, qq, pre, cka, cva, len, cap, ko, vo,
+                         static_cast<float*>(o), c, H, Hkv, scale);
     else
-      hipLaunchKernelGGL(k_attn_f32_dec<64>, grid, dim3(128), 0, st, qq, kk, vv, cka, cva, len, cap, ko, vo,
-                         static_cast<float*>(o), c, n, H, Hkv, scale);
+      hipLaunchKernelGGL(k_attn_f32_dec<64>, grid, dim3(128), 0, st, qq, pre, cka, cva, len, cap, ko, vo,
+                         static_cast<float*>(o), c, H, Hkv, scale);
   }
   return hipGetLastError();
 }
 
-namespace {
-// k_attn_bf16 with the probabilities split into hi/lo (p_split) or not.
-template <int HD, bool XB, typename... Args>
-void launch_attn_tiles(bool p_split, dim3 grid, hipStream_t st, Args... args) {
-  if (p_split)
-    hipLaunchKernelGGL((k_attn_bf16<HD, XB, true>), grid, dim3(64 * kAttnWaves), 0, st, args...);
-  else
-    hipLaunchKernelGGL((k_attn_bf16<HD, XB, false>), grid, dim3(64 * kAttnWaves), 0, st, args...);
-}
-}  // namespace
-
-hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,
+hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const PrefixView& pre,
                             const void* k_own, const void* v_own, void* o, float* opart, float* mlpart,
-                            const Ctrl* c, int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st,
+                            const Ctrl* c, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st,
                             bool p_split) {
   if (dt == DType::BF16) {
     const float sl2 = 1.4426950408889634f / sqrtf((float)hd);
     const int G = H / Hkv;
     const int max_rows = max_branches * s;
     const float* qq = static_cast<const float*>(q);
-    const bf16 *kk = static_cast<const bf16*>(pk), *vv = static_cast<const bf16*>(pv);
     const float *ko = static_cast<const float*>(k_own), *vo = static_cast<const float*>(v_own);
     void* oo = o;
     const int waves = max_rows * H;
     const dim3 cgrid((waves * 64 + 255) / 256);
+    const bool ms = pre.nseg > 1;
     if (p.cross) {
       const dim3 grid((max_rows * G + 16 * kAttnWaves - 1) / (16 * kAttnWaves), Hkv, p.chunks);
       if (p.chunks > 0) {
         if (hd == 128)
-          launch_attn_tiles<128, true>(p_split, grid, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
-                             c, n, s, H, Hkv, sl2, p.chunks, max_rows);
+          launch_attn_tiles<128, true>(p_split, ms, grid, st, qq, pre, ko, vo, oo, opart, mlpart, c, s, H, Hkv, sl2,
+                                       p.chunks, max_rows);
         else
-          launch_attn_tiles<64, true>(p_split, grid, st, qq, kk, vv, ko, vo, oo, opart, mlpart,
-                             c, n, s, H, Hkv, sl2, p.chunks, max_rows);
+          launch_attn_tiles<64, true>(p_split, ms, grid, st, qq, pre, ko, vo, oo, opart, mlpart, c, s, H, Hkv, sl2,
+                                      p.chunks, max_rows);
       }
       if (hd == 128)
         hipLaunchKernelGGL(k_attn_combine_own<128>, cgrid, dim3(256), 0, st, opart, mlpart, qq, ko, vo, oo, c, s, H,
@@ -1008,11 +1067,11 @@ hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const vo
     }
     const dim3 grid((G * s + 16 * kAttnWaves - 1) / (16 * kAttnWaves), Hkv, max_branches * p.chunks);
     if (hd == 128)
-      launch_attn_tiles<128, false>(p_split, grid, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
-                         n, s, H, Hkv, sl2, p.chunks, max_rows);
+      launch_attn_tiles<128, false>(p_split, ms, grid, st, qq, pre, ko, vo, oo, opart, mlpart, c, s, H, Hkv, sl2,
+                                    p.chunks, max_rows);
     else
-      launch_attn_tiles<64, false>(p_split, grid, st, qq, kk, vv, ko, vo, oo, opart, mlpart, c,
-                         n, s, H, Hkv, sl2, p.chunks, max_rows);
+      launch_attn_tiles<64, false>(p_split, ms, grid, st, qq, pre, ko, vo, oo, opart, mlpart, c, s, H, Hkv, sl2,
+                                   p.chunks, max_rows);
     if (p.chunks > 1) {
       if (hd == 128)
         hipLaunchKernelGGL(k_attn_combine<128>, cgrid, dim3(256), 0, st, opart, mlpart, oo, c, s, H, p.chunks,
@@ -1025,15 +1084,14 @@ hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const vo
     const float scale = 1.f / sqrtf((float)hd);
     const int total = max_branches * s * H;
     const dim3 grid((total + 127) / 128);
-    const float *qq = static_cast<const float*>(q), *kk = static_cast<const float*>(pk),
-                *vv = static_cast<const float*>(pv), *ko = static_cast<const float*>(k_own),
+    const float *qq = static_cast<const float*>(q), *ko = static_cast<const float*>(k_own),
                 *vo = static_cast<const float*>(v_own);
     if (hd == 128)
-      hipLaunchKernelGGL(k_attn_f32<128>, grid, dim3(128), 0, st, qq, kk, vv, ko, vo, static_cast<float*>(o), c,
-                         n, s, H, Hkv, scale);
+      hipLaunchKernelGGL(k_attn_f32<128>, grid, dim3(128), 0, st, qq, pre, ko, vo, static_cast<float*>(o), c, s, H,
+                         Hkv, scale);
     else
-      hipLaunchKernelGGL(k_attn_f32<64>, grid, dim3(128), 0, st, qq, kk, vv, ko, vo, static_cast<float*>(o), c, n,
-                         s, H, Hkv, scale);
+      hipLaunchKernelGGL(k_attn_f32<64>, grid, dim3(128), 0, st, qq, pre, ko, vo, static_cast<float*>(o), c, s, H,
+                         Hkv, scale);
   }
   return hipGetLastError();
 }

@@ -409,11 +409,11 @@ hipError_t launch_entropy_t(DType dt, const void* W, const void* hn_a, const voi
                          kmul, parts);
       break;
     case 2:
-      hipLaunchKernelGGL((k_entropy_bf16<2, 32, kEntRing, AM>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d,
+      hipLaunchKernelGGL((k_entropy_bf16<2, 64, kEntRing, AM>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d,
                          kmul, parts);
       break;
     default:
-      hipLaunchKernelGGL((k_entropy_bf16<4, 16, kEntRing, AM>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d,
+      hipLaunchKernelGGL((k_entropy_bf16<4, 32, kEntRing, AM>), dim3(blocks), dim3(512), 0, st, w, a, b, c, V, d,
                          kmul, parts);
       break;
   }

@@ -199,29 +199,47 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
 }
 
 // ---------------------------------------------------------------------------
-// 256 x 256 tiles for large row counts (MFMA-bound projections).
+// K-32 stage kernel: BM x BN tiles (256 x 256 for large row counts, 128 x 512
+// or 128 x 256 for 128-row calls), stages of a 32-wide K slice (64 bytes per
+// row), so that more stages fit the LDS and more bytes are in flight per CU.
 //
-// 8 waves as a 4 (rows) x 2 (columns) grid of 64 x 128 wave tiles: each wave
-// reads 64 x 32 activation and 128 x 32 weight elements from LDS per 32-wide
-// K step for 64 MFMAs, a third fewer LDS bytes per MFMA than the 128-row
-// kernel's 64 x 64 wave tiles. A stage is a 32-wide K slice (64 bytes per row)
-// of three 16 KB sub-tiles (A hi, A lo, W), so three stages fit the LDS and two
-// are in flight while one is contracted. Each DMA instruction moves 16 rows x
-// 64 bytes; within a row the 16-byte chunk c sits at c ^ ((row >> 2) & 3), which
-// spreads the 16 rows of a fragment read over the banks.
+// 8 waves as a (BM / 64) x (8 / (BM / 64)) grid of 64 x WN wave tiles. At
+// 256 x 256 each wave reads 64 x 32 activation and 128 x 32 weight elements
+// from LDS per 32-wide K step for 64 MFMAs, a third fewer LDS bytes per MFMA
+// than the 128-row kernel's 64 x 64 wave tiles. A stage holds three sub-tiles
+// (A hi, A lo: BM rows; W: BN rows) of 64-byte rows; R stages fit the LDS and
+// R - 1 are in flight while one is contracted. A 128-row call of the 64-wide
+// stage kernel keeps one 64 KB stage in flight per CU, which at the weight
+// stream's latency holds it near a third of HBM bandwidth; 128 x 512 tiles in
+// three 48 KB stages keep twice the weight bytes in flight. Each DMA
+// instruction moves 16 rows x 64 bytes; within a row the 16-byte chunk c sits
+// at c ^ ((row >> 2) & 3), which spreads the 16 rows of a fragment read over
+// the banks.
 __device__ __forceinline__ int wswz(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
 
-template <int R>
+// SWIGLU: the gate|up projection with its SwiGLU epilogue (one K split). W is
+// [2F, K] (gate rows, then up rows, N = 2F); a workgroup's BN weight rows are
+// gate rows n0..n0+BN/2-1 and the matching up rows F+n0.., so the waves of
+// the first half of the wave columns hold gate values and those of the second
+// half the up values of the same (row, column) in the same lanes. The up waves
+// pass their accumulators through LDS and the gate waves write
+// a = silu(gate) * up as the bf16 hi/lo planes [max_rows, F] at P (hi) and
+// P + max_rows * F (lo), the down projection's input.
+template <int BM, int BN, int R, bool SWIGLU = false>
 __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __restrict__ Ahi,
                                                                const bf16* __restrict__ Alo,
                                                                const bf16* __restrict__ W, float* __restrict__ P,
                                                                size_t split_stride, const Ctrl* c, int s,
                                                                int max_rows, int N, int K, int kps) {
-  constexpr int BM = 256, BN = 256, KEL = 32, RB = KEL * 2;
-  constexpr int SUB = BM * RB, SLOT = 3 * SUB;
-  constexpr int IPW = SLOT / 1024 / kGemmWaves;   // 6 DMA instructions per wave per stage
-  constexpr int TM = 4, TN = 8;                   // 64 x 128 wave tile
-  static_assert(SUB / 1024 % kGemmWaves == 0, "every instruction of a wave stays in one sub-tile");
+  constexpr int KEL = 32, RB = KEL * 2;
+  constexpr int SUB_A = BM * RB, SLOT = 2 * SUB_A + BN * RB;
+  constexpr int IPW = SLOT / 1024 / kGemmWaves;   // DMA instructions per wave per stage
+  constexpr int A_INS = SUB_A / 1024;             // instructions per activation plane
+  constexpr int WGM = BM / 64, WGN = kGemmWaves / WGM;   // wave grid
+  constexpr int WN = BN / WGN, TM = 4, TN = WN / 16;     // 64 x WN wave tile
+  static_assert(A_INS % kGemmWaves == 0 && (SLOT / 1024) % kGemmWaves == 0,
+                "every instruction of a wave stays in one sub-tile");
+  static_assert(WGM * WGN == kGemmWaves && TN >= 1 && (!SWIGLU || WGN % 2 == 0), "wave grid");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[R * SLOT];
 
   const int Ml = c ? min(c->live_count * s, max_rows) : max_rows;
@@ -229,23 +247,32 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
   xcd_raster<4>(tx, ty, tz);
   const int m0 = ty * BM;
   if (m0 >= Ml) return;
-  const int n0 = tx * BN;
+  const int F = N / 2;
+  const int n0 = tx * (SWIGLU ? BN / 2 : BN);
   const int kb = tz * kps, ke = min(K, kb + kps);
   const int nsteps = (ke - kb + KEL - 1) / KEL;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const int wm = wid & 3, wn = wid >> 2;
+  const int wm = wid % WGM, wn = wid / WGM;
   const bool wave_live = m0 + 64 * wm < Ml;
+  // Weight row of tile row `row` (0..255).
+  auto wrow = [&](int row) {
+    if (!SWIGLU) return min(n0 + row, N - 1);
+    return row < BN / 2 ? min(n0 + row, F - 1) : F + min(n0 + row - BN / 2, F - 1);
+  };
 
-  // DMA instruction j of this wave (ins = 8j + wid) fills rows 16 (ins % 16) ..
-  // +15 of sub-tile ins / 16 = j / 2; lane L fills physical chunk L & 3 of row
-  // L >> 2, i.e. logical chunk (L & 3) ^ ((L >> 4) & 3), the same for every j.
+  // DMA instruction j of this wave (ins = 8j + wid) fills 16 rows of sub-tile
+  // plane(j) (0 A hi, 1 A lo, 2 W; fixed by j as A_INS is a multiple of 8);
+  // lane L fills physical chunk L & 3 of row L >> 2 of them, i.e. logical chunk
+  // (L & 3) ^ ((L >> 4) & 3), the same for every j.
   // Row offsets in elements as size_t: rows x K passes 2^31 at large row counts.
+  auto plane = [](int j) { return j * kGemmWaves < A_INS ? 0 : (j * kGemmWaves < 2 * A_INS ? 1 : 2); };
   size_t rowoff[IPW];
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
-    const int row = ((j * kGemmWaves + wid) % 16) * 16 + (lane >> 2);
-    rowoff[j] = (size_t)(j / 2 < 2 ? min(m0 + row, max_rows - 1) : min(n0 + row, N - 1)) * K;
+    const int pl = plane(j);
+    const int row = (j * kGemmWaves + wid - pl * A_INS) * 16 + (lane >> 2);
+    rowoff[j] = (size_t)(pl < 2 ? min(m0 + row, max_rows - 1) : wrow(row)) * K;
   }
   const int ccol = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
   auto issue = [&](int step) {
@@ -256,7 +283,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
     uint8_t* slot = smem + (step % R) * SLOT;
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
-      const bf16* base = j / 2 == 0 ? Ahi : (j / 2 == 1 ? Alo : W);
+      const bf16* base = plane(j) == 0 ? Ahi : (plane(j) == 1 ? Alo : W);
       dma16(base + rowoff[j] + col, slot + (j * kGemmWaves + wid) * 1024);
     }
   };
@@ -271,15 +298,15 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
     bf16x8 bw[TN];
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
-      const int row = wn * 128 + 16 * tn + r16;
-      bw[tn] = *reinterpret_cast<const bf16x8*>(slot + 2 * SUB + row * RB + wswz(row, g) * 16);
+      const int row = wn * WN + 16 * tn + r16;
+      bw[tn] = *reinterpret_cast<const bf16x8*>(slot + 2 * SUB_A + row * RB + wswz(row, g) * 16);
     }
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
       const int row = wm * 64 + 16 * tm + r16;
       const int off = row * RB + wswz(row, g) * 16;
       bf16x8 ah = *reinterpret_cast<const bf16x8*>(slot + off);
-      bf16x8 al = *reinterpret_cast<const bf16x8*>(slot + SUB + off);
+      bf16x8 al = *reinterpret_cast<const bf16x8*>(slot + SUB_A + off);
       ah = kin ? ah : zero;
       al = kin ? al : zero;
 #pragma unroll
@@ -303,6 +330,47 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
     if (wave_live) compute(smem + (st % R) * SLOT, kb + st * KEL + 8 * g < ke);
   }
   wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
+  if constexpr (SWIGLU) {
+    // Up accumulators of wave (wm, wn) with wn >= WGN / 2 to LDS (the ring is
+    // free once every wave is past its last stage), read back by wave
+    // (wm, wn - WGN / 2) lane for lane.
+    constexpr int HG = WGN / 2;
+    __syncthreads();
+    floatx4* xch = reinterpret_cast<floatx4*>(smem);   // [WGM][HG][TM][TN][64 lanes]
+    static_assert(WGM * HG * TM * TN * 64 * 16 <= R * SLOT, "the exchange fits in the ring");
+    const int pair = wm * HG + wn % HG;
+    if (wn >= HG) {
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) xch[((pair * TM + tm) * TN + tn) * 64 + lane] = acc[tm][tn];
+    }
+    __syncthreads();
+    if (wn >= HG || !wave_live) return;
+    bf16* hi = reinterpret_cast<bf16*>(P);
+    bf16* lo = hi + (size_t)max_rows * F;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const floatx4 u = xch[((pair * TM + tm) * TN + tn) * 64 + lane];
+        const int col = n0 + wn * WN + 16 * tn + r16;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = m0 + wm * 64 + 16 * tm + 4 * g + i;
+          if (row < Ml && col < F) {
+            const float gt = acc[tm][tn][i];
+            const float a = gt / (1.f + expf(-gt)) * u[i];
+            uint16_t h, l;
+            split2(a, h, l);
+            const size_t idx = (size_t)row * F + col;
+            hi[idx] = __builtin_bit_cast(bf16, h);
+            lo[idx] = __builtin_bit_cast(bf16, l);
+          }
+        }
+      }
+    return;
+  }
   if (!wave_live) return;
 
   float* out = P + tz * split_stride;
@@ -310,7 +378,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
-      const int col = n0 + wn * 128 + 16 * tn + r16;
+      const int col = n0 + wn * WN + 16 * tn + r16;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = m0 + wm * 64 + 16 * tm + 4 * g + i;
@@ -675,6 +743,42 @@ GemmPlan plan_gemm_kind(DType dt, int max_rows, int N, int K, int kind, int spli
   return p;
 }
 
+namespace {
+// The K-32 stage kernel for the plan's tile: 256 x 256, 128 x 512 or 128 x 256.
+template <bool SWIGLU>
+void launch_wide(const GemmPlan& p, dim3 grid, hipStream_t st, const void* A0, const void* A1, const void* W,
+                 float* P, size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K) {
+  const bf16 *a0 = static_cast<const bf16*>(A0), *a1 = static_cast<const bf16*>(A1), *w = static_cast<const bf16*>(W);
+  const dim3 blk(kGemmWaves * 64);
+  if (p.bm == 256)
+    hipLaunchKernelGGL((k_gemm_wide<256, 256, 3, SWIGLU>), grid, blk, 0, st, a0, a1, w, P, split_stride, c, s,
+                       max_rows, N, K, p.k_per_split);
+  else if (p.bn == 512)
+    hipLaunchKernelGGL((k_gemm_wide<128, 512, 3, SWIGLU>), grid, blk, 0, st, a0, a1, w, P, split_stride, c, s,
+                       max_rows, N, K, p.k_per_split);
+  else
+    hipLaunchKernelGGL((k_gemm_wide<128, 256, 4, SWIGLU>), grid, blk, 0, st, a0, a1, w, P, split_stride, c, s,
+                       max_rows, N, K, p.k_per_split);
+}
+}  // namespace
+
+bool gate_up_fused(DType dt, const GemmPlan& p, int N) {
+  return dt == DType::BF16 && p.kind == 1 && p.splits == 1 && N % 2 == 0;
+}
+
+hipError_t launch_gate_up_swiglu(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W,
+                                 float* P, size_t split_stride, const Ctrl* c, int s, int max_rows, int F, int K,
+                                 void* a, hipStream_t st) {
+  if (!gate_up_fused(dt, p, 2 * F)) {
+    hipError_t e = launch_gemm(dt, p, A0, A1, W, P, split_stride, c, s, max_rows, 2 * F, K, st);
+    if (e != hipSuccess) return e;
+    return launch_swiglu_post(dt, P, p.splits, split_stride, c, s, F, a, max_rows, st);
+  }
+  const dim3 grid(cdiv(F, p.bn / 2), cdiv(max_rows, p.bm), 1);
+  launch_wide<true>(p, grid, st, A0, A1, W, static_cast<float*>(a), split_stride, c, s, max_rows, 2 * F, K);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W, float* P,
                        size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st) {
   if (dt == DType::BF16 && p.kind == 2) {
@@ -697,9 +801,7 @@ hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* 
   }
   const dim3 grid(cdiv(N, p.bn), cdiv(max_rows, p.bm), p.splits);
   if (dt == DType::BF16 && p.kind == 1) {
-    hipLaunchKernelGGL((k_gemm_wide<3>), grid, dim3(kGemmWaves * 64), 0, st, static_cast<const bf16*>(A0),
-                       static_cast<const bf16*>(A1), static_cast<const bf16*>(W), P, split_stride, c, s, max_rows, N,
-                       K, p.k_per_split);
+    launch_wide<false>(p, grid, st, A0, A1, W, P, split_stride, c, s, max_rows, N, K);
   } else if (dt == DType::F32) {
     hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, st, static_cast<const float*>(A0),
                        static_cast<const float*>(W), P, split_stride, c, s, max_rows, N, K, p.k_per_split);

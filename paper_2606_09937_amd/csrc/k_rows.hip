@@ -240,7 +240,7 @@ template <bool kSplit>
 __global__ __launch_bounds__(256) void k_swiglu_post(const float* __restrict__ P, int nsplit, size_t split_stride,
                                                      const Ctrl* c, int s, int F, void* __restrict__ a) {
   const int r = blockIdx.y;
-  if (r >= c->live_count * s) return;
+  if (c && r >= c->live_count * s) return;   // no control block: every row is live, as in the GEMMs
   const int f = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (f >= F) return;
   const float* pr = P + (size_t)r * 2 * F;

@@ -83,6 +83,28 @@ GemmPlan plan_gemm(DType dt, int max_rows, int N, int K);
 GemmPlan plan_gemm_kind(DType dt, int max_rows, int N, int K, int kind, int splits);
 hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W, float* P,
                        size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st);
+// The gate|up projection (W [2F, K]) and its SwiGLU: a = silu(gate) * up, written to `a`
+// as the down projection's input (bf16 hi/lo planes [max_rows, F] for BF16 models). With
+// the 256 x 256 kernel over one K split it is fused into the projection's epilogue (the
+// fp32 gate|up product never reaches memory); otherwise the split partials go to P and
+// launch_swiglu_post combines them.
+bool gate_up_fused(DType dt, const GemmPlan& p, int N);
+hipError_t launch_gate_up_swiglu(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W,
+                                 float* P, size_t split_stride, const Ctrl* c, int s, int max_rows, int F, int K,
+                                 void* a, hipStream_t st);
+
+// ---- the shared prefix of one layer
+// Up to kMaxPrefixSegs caches in position order (a tree node's own entries after
+// its ancestors'): segment i holds positions start[i] .. start[i] + len[i] - 1 as
+// [Hkv, len[i], hd] in the model's storage type at k[i] / v[i]; n is the total.
+constexpr int kMaxPrefixSegs = 8;
+struct PrefixView {
+  int n = 0, nseg = 0;
+  int start[kMaxPrefixSegs] = {};
+  int len[kMaxPrefixSegs] = {};
+  const void* k[kMaxPrefixSegs] = {};
+  const void* v[kMaxPrefixSegs] = {};
+};
 
 // ---- attention over [shared prefix ; own causal span]: q, k_own, v_own fp32; prefix of the
 // model dtype; o is the projection input (bf16 hi/lo planes for BF16 models, fp32 otherwise).
@@ -97,9 +119,9 @@ struct AttnPlan {
 };
 AttnPlan plan_attention(DType dt, int B, int n, int s, int H, int Hkv);
 // p_split = false: the probabilities enter P.V as bf16 alone instead of a hi/lo pair.
-hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,
+hipError_t launch_attention(DType dt, const AttnPlan& p, const void* q, const PrefixView& pre,
                             const void* k_own, const void* v_own, void* o, float* opart, float* mlpart,
-                            const Ctrl* c, int n, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st,
+                            const Ctrl* c, int s, int H, int Hkv, int hd, int max_branches, hipStream_t st,
                             bool p_split = true);
 // x[i] = fp32(bf16(x[i])) for i < n: the value rounded to bf16 precision, kept in fp32.
 hipError_t launch_round_bf16(float* x, size_t n, hipStream_t st);
@@ -130,9 +152,9 @@ hipError_t launch_finalize_exit(const float* parts, int nparts, Ctrl* c, int lay
 // Attention of one new token per branch (s = 1) over the shared prefix (split-KV
 // plan p, cross mode), the branch's cached entries 0..len-1 (model dtype, layer
 // base [B, Hkv, cap, hd]) and its own key/value (fp32 k_own/v_own [B, Hkv, 1, hd]).
-hipError_t launch_attention_decode(DType dt, const AttnPlan& p, const void* q, const void* pk, const void* pv,
+hipError_t launch_attention_decode(DType dt, const AttnPlan& p, const void* q, const PrefixView& pre,
                                    const void* ck, const void* cv, int len, int cap, const void* k_own,
-                                   const void* v_own, void* o, float* opart, float* mlpart, const Ctrl* c, int n,
+                                   const void* v_own, void* o, float* opart, float* mlpart, const Ctrl* c,
                                    int H, int Hkv, int hd, int B, hipStream_t st);
 
 // Level-1 / decode-level gate of Eq. cgee_gate over p = conf / n_steps of B <= 64

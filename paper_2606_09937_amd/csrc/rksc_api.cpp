@@ -3,6 +3,7 @@
 // allocated).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -82,6 +83,53 @@ rksc_status check_config(const rksc_model_config* c) {
   return RKSC_OK;
 }
 
+// The caches of a prefix chain in position order (root first); empty caches are
+// left out. Rejects more than kMaxPrefixSegs caches (which also ends a cycle).
+struct Chain {
+  int nseg = 0;
+  long long n = 0;
+  const rksc_prefix_kv* seg[rksc::kMaxPrefixSegs] = {};
+};
+
+rksc_status collect_chain(const rksc_prefix_kv* kv, Chain* ch) {
+  const rksc_prefix_kv* rev[rksc::kMaxPrefixSegs];
+  int cnt = 0;
+  for (const rksc_prefix_kv* p = kv; p; p = p->parent) {
+    if (cnt == rksc::kMaxPrefixSegs)
+      return fail(RKSC_ERR_UNSUPPORTED, "a prefix chain of more than %d caches (or a cycle)", rksc::kMaxPrefixSegs);
+    if (p->n_prefix < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", p->n_prefix);
+    if (p->n_prefix > 0 && (!p->k || !p->v))
+      return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix k/v are NULL with n_prefix = %d", p->n_prefix);
+    rev[cnt++] = p;
+  }
+  *ch = Chain{};
+  for (int i = cnt - 1; i >= 0; --i) {
+    if (rev[i]->n_prefix == 0) continue;
+    ch->seg[ch->nseg++] = rev[i];
+    ch->n += rev[i]->n_prefix;
+  }
+  if (ch->n > (1LL << 30)) return fail(RKSC_ERR_UNSUPPORTED, "a prefix of more than 2^30 entries");
+  return RKSC_OK;
+}
+
+// Layer l of the chain for the attention kernels (each cache is [L, Hkv, n_i, hd]).
+rksc::PrefixView layer_view(const Chain& ch, int l, int Hkv, int hd, size_t T) {
+  rksc::PrefixView v;
+  v.n = (int)ch.n;
+  v.nseg = ch.nseg;
+  int start = 0;
+  for (int i = 0; i < ch.nseg; ++i) {
+    const rksc_prefix_kv* p = ch.seg[i];
+    const size_t layer = (size_t)Hkv * p->n_prefix * hd * T;
+    v.start[i] = start;
+    v.len[i] = p->n_prefix;
+    v.k[i] = static_cast<const char*>(p->k) + (size_t)l * layer;
+    v.v[i] = static_cast<const char*>(p->v) + (size_t)l * layer;
+    start += p->n_prefix;
+  }
+  return v;
+}
+
 rksc_status make_layout(const rksc_model_config* c, int B, int s, int n_prefix, Layout* lay) {
   rksc_status st = check_config(c);
   if (st != RKSC_OK) return st;
@@ -136,12 +184,31 @@ rksc_status make_layout(const rksc_model_config* c, int B, int s, int n_prefix, 
 // shared by `window` consecutive layers, whose rows become extra columns of the
 // same stream; the exit rule still runs layer by layer at the window's end (a
 // branch's layers after its exit inside the window are computed and discarded).
-// The stream's cost grows slowly with its columns (measured on MI355X: at 32
-// branches of the 10B shape a 2-layer window of 64 columns takes the call from
-// 28.2 to 21.9 ms), so the window is 4 layers up to 16 branches, 2 up to 32,
-// else 1 (at most 64 columns).
+// The window is chosen by a cost model. A pass of L layers pays L / w streams of
+// W_lm, and an exit, whose layer is not known in advance and is taken as placed
+// uniformly within its window, wastes (w - 1) / 2 computed layers on average;
+// w* = sqrt(2 L c_probe / c_layer) minimises the sum. c_probe is the stream of
+// W_lm at 6 TB/s (measured on MI355X: its cost barely grows with the columns);
+// c_layer is the layer's projections (the larger of their weight bytes at
+// 3 TB/s and their hi/lo MFMA work at half the bf16 peak), its attention at
+// 0.8 PFLOP/s, and about 30 us of row kernels. w is w* rounded to a power of two
+// in [1, min(8, 64 / B)] (at most 64 stream columns).
 constexpr int kMaxWindow = 8;
-int exit_window(int B) { return B <= 16 ? 4 : B <= 32 ? 2 : 1; }
+constexpr int kAutoWindow = 0;   // verify_impl's window argument: take exit_window's
+int exit_window(const rksc_model_config* c, int B, int s, int n) {
+  const double d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, hd = c->head_dim, F = c->d_ff;
+  const double T = c->dtype == RKSC_BF16 ? 2.0 : 4.0;
+  const double P = d * (H + 2 * Hkv) * hd + H * hd * d + 3 * d * F;
+  const double M = (double)B * s;
+  const double c_probe = (double)c->vocab * d * T / 6e12;
+  const double t_gemm = std::max(P * T / 3e12, 4.0 * M * P / 1.25e15);
+  const double t_attn = 8.0 * hd * H * B * ((double)s * n + 0.5 * (double)s * s) / 0.8e15;
+  const double c_layer = t_gemm + t_attn + 30e-6;
+  const double w_star = std::sqrt(2.0 * c->n_layers * c_probe / c_layer);
+  int w = 1;
+  while (w * 2 <= kMaxWindow && w * 2 * B <= 64 && w_star >= w * 1.4142135623730951) w *= 2;
+  return w;
+}
 
 #define HIP_TRY(expr)                                                                   \
   do {                                                                                  \
@@ -196,14 +263,15 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
   if (std::isnan(tau) || tau < 0.f) return fail(RKSC_ERR_INVALID_ARGUMENT, "tau must be >= 0 and not NaN");
   if (patience < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "patience must be >= 1 (got %d)", patience);
-  if (window < 1 || window > kMaxWindow || (long long)window * n_branches > 64)
+  if (window != kAutoWindow && (window < 1 || window > kMaxWindow || (long long)window * n_branches > 64))
     return fail(RKSC_ERR_INVALID_ARGUMENT, "window must be in [1, %d] with window * n_branches <= 64 (got %d, %d)",
                 kMaxWindow, window, n_branches);
-  const int win = window;
   const rksc_model_config* c = &w->cfg;
-  if (kv->n_prefix < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", kv->n_prefix);
+  Chain chain;
+  rksc_status st = collect_chain(kv, &chain);
+  if (st != RKSC_OK) return st;
   Layout lay;
-  rksc_status st = make_layout(c, n_branches, branch_len, kv->n_prefix, &lay);
+  st = make_layout(c, n_branches, branch_len, (int)chain.n, &lay);
   if (st != RKSC_OK) return st;
   if (workspace_bytes < lay.total)
     return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
@@ -214,14 +282,12 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
       return fail(RKSC_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
   }
-  if (kv->n_prefix < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", kv->n_prefix);
-  if (kv->n_prefix > 0 && (!kv->k || !kv->v))
-    return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix k/v are NULL with n_prefix = %d", kv->n_prefix);
+  const int win = window == kAutoWindow ? exit_window(c, n_branches, branch_len, (int)chain.n) : window;
 
   const DType dt = c->dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
   const size_t T = dt == DType::BF16 ? 2 : 4;
   const int L = c->n_layers, d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, hd = c->head_dim;
-  const int F = c->d_ff, V = c->vocab, B = n_branches, s = branch_len, n = kv->n_prefix;
+  const int F = c->d_ff, V = c->vocab, B = n_branches, s = branch_len, n = (int)chain.n;
   const int M = lay.max_rows;
   const int Nqkv = (H + 2 * Hkv) * hd;
   hipStream_t strm = static_cast<hipStream_t>(stream);
@@ -263,9 +329,6 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     void* e = events[(size_t)l * RKSC_PROFILE_EVENTS_PER_LAYER + slot];
     return e ? hipEventRecord(static_cast<hipEvent_t>(e), strm) : hipSuccess;
   };
-  const char* pk_base = static_cast<const char*>(kv->k);
-  const char* pv_base = static_cast<const char*>(kv->v);
-  const size_t kv_layer = (size_t)Hkv * n * hd * T;
   for (int l = 0; l < L; ++l) {
     const rksc_layer_weights& lw = w->layers[l];
     float* x_prev = (l % 2 == 0) ? x0 : x1;
@@ -298,11 +361,9 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
       HIP_TRY(rksc::launch_round_bf16(kown, (size_t)B * Hkv * s * hd, strm));
       HIP_TRY(rksc::launch_round_bf16(vown, (size_t)B * Hkv * s * hd, strm));
     }
-    const void* pk = n > 0 ? pk_base + l * kv_layer : nullptr;
-    const void* pv = n > 0 ? pv_base + l * kv_layer : nullptr;
     HIP_TRY(mark(l, 2));
-    HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, pk, pv, kown, vown, act, opart, mlpart, ctrl, n, s, H, Hkv, hd,
-                                   B, strm, !(drop & RKSC_DROP_P_LO)));
+    HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, layer_view(chain, l, Hkv, hd, T), kown, vown, act, opart,
+                                   mlpart, ctrl, s, H, Hkv, hd, B, strm, !(drop & RKSC_DROP_P_LO)));
     if (drop & RKSC_DROP_O_LO) HIP_TRY(drop_lo(act, (size_t)M * H * hd));
     HIP_TRY(mark(l, 3));
     HIP_TRY(mark(l, 4));
@@ -313,10 +374,9 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
                                   lw.ffn_norm, d, c->rms_eps, M, strm));
     if (drop & RKSC_DROP_GATE_UP_LO) HIP_TRY(drop_lo(act, (size_t)M * d));
     HIP_TRY(mark(l, 6));
-    HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig, (size_t)M * 2 * F,
-                              ctrl, s, M, 2 * F, d, strm));
+    HIP_TRY(rksc::launch_gate_up_swiglu(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig,
+                                        (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm));
     HIP_TRY(mark(l, 7));
-    HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
     if (drop & RKSC_DROP_DOWN_LO) HIP_TRY(drop_lo(ffn, (size_t)M * F));
     HIP_TRY(mark(l, 8));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
@@ -345,7 +405,7 @@ RKSC_EXPORT rksc_status rksc_verify_forward(const rksc_weights* w, const rksc_pr
                                             float* hidden_last, void* workspace, size_t workspace_bytes,
                                             void* stream) {
   return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
-                     hidden_last, workspace, workspace_bytes, stream, nullptr, exit_window(n_branches));
+                     hidden_last, workspace, workspace_bytes, stream, nullptr, kAutoWindow);
 }
 
 rksc_status rksc::verify_workspace(const rksc_model_config* cfg, int32_t n_branches, int32_t branch_len,
@@ -363,10 +423,18 @@ rksc_status rksc::verify_call(const rksc_weights* w, const rksc_prefix_kv* kv, c
                               int32_t* exit_layer, float* hidden_last, void* workspace, size_t workspace_bytes,
                               void* stream) {
   return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
-                     hidden_last, workspace, workspace_bytes, stream, nullptr, exit_window(n_branches));
+                     hidden_last, workspace, workspace_bytes, stream, nullptr, kAutoWindow);
 }
 
-RKSC_EXPORT int32_t rksc_verify_window(int32_t n_branches) { return exit_window(n_branches); }
+RKSC_EXPORT int32_t rksc_verify_window(const rksc_model_config* cfg, int32_t n_branches, int32_t branch_len,
+                                       int32_t n_prefix) {
+  if (check_config(cfg) != RKSC_OK) return 0;
+  if (n_branches < 1 || n_branches > RKSC_MAX_BRANCHES || branch_len < 1 || n_prefix < 0) {
+    fail(RKSC_ERR_INVALID_ARGUMENT, "bad pass shape B = %d, s = %d, n = %d", n_branches, branch_len, n_prefix);
+    return 0;
+  }
+  return exit_window(cfg, n_branches, branch_len, n_prefix);
+}
 
 RKSC_EXPORT rksc_status rksc_test_verify_precision(const rksc_weights* w, const rksc_prefix_kv* kv,
                                                    const int32_t* branch_tokens, int32_t n_branches,
@@ -375,7 +443,7 @@ RKSC_EXPORT rksc_status rksc_test_verify_precision(const rksc_weights* w, const 
                                                    size_t workspace_bytes, void* stream, uint32_t drop_mask) {
   if (drop_mask & ~(uint32_t)RKSC_DROP_ALL) return fail(RKSC_ERR_INVALID_ARGUMENT, "unknown drop bits 0x%x", drop_mask);
   return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
-                     hidden_last, workspace, workspace_bytes, stream, nullptr, exit_window(n_branches), drop_mask);
+                     hidden_last, workspace, workspace_bytes, stream, nullptr, kAutoWindow, drop_mask);
 }
 
 RKSC_EXPORT rksc_status rksc_verify_forward_window(const rksc_weights* w, const rksc_prefix_kv* kv,
@@ -383,6 +451,9 @@ RKSC_EXPORT rksc_status rksc_verify_forward_window(const rksc_weights* w, const 
                                                    int32_t branch_len, float tau, int32_t patience, float* entropy,
                                                    int32_t* exit_layer, float* hidden_last, void* workspace,
                                                    size_t workspace_bytes, void* stream, int32_t window) {
+  if (window < 1)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "window must be in [1, %d] with window * n_branches <= 64 (got %d)",
+                kMaxWindow, window);
   return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
                      hidden_last, workspace, workspace_bytes, stream, nullptr, window);
 }
@@ -395,7 +466,7 @@ RKSC_EXPORT rksc_status rksc_verify_forward_profiled(const rksc_weights* w, cons
                                                      void* const* events) {
   if (!events) return fail(RKSC_ERR_INVALID_ARGUMENT, "events is NULL");
   return verify_impl(w, kv, branch_tokens, n_branches, branch_len, tau, patience, entropy, exit_layer,
-                     hidden_last, workspace, workspace_bytes, stream, events, exit_window(n_branches));
+                     hidden_last, workspace, workspace_bytes, stream, events, kAutoWindow);
 }
 
 RKSC_EXPORT size_t rksc_prefill_workspace_size(const rksc_model_config* cfg, int32_t n_prefix) {
@@ -490,15 +561,14 @@ RKSC_EXPORT rksc_status rksc_prefill(const rksc_weights* w, const int32_t* token
     HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
                                   vown, M, strm, dt, static_cast<char*>(k_out) + l * kv_layer * T,
                                   static_cast<char*>(v_out) + l * kv_layer * T, s, 0));
-    HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, nullptr, nullptr, kown, vown, act, opart, mlpart, ctrl, 0, s, H,
-                                   Hkv, hd, 1, strm));
+    HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, rksc::PrefixView{}, kown, vown, act, opart, mlpart, ctrl, s,
+                                   H, Hkv, hd, 1, strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.o, act, plane_lo(act, (size_t)M * H * hd), lw.w_o, pres, res_stride, ctrl, s,
                               M, d, H * hd, strm));
     HIP_TRY(rksc::launch_add_norm(dt, x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
                                   lw.ffn_norm, d, c->rms_eps, M, strm));
-    HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig, (size_t)M * 2 * F,
-                              ctrl, s, M, 2 * F, d, strm));
-    HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
+    HIP_TRY(rksc::launch_gate_up_swiglu(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig,
+                                        (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
                               M, d, F, strm));
     if (l == L - 1)
@@ -550,14 +620,14 @@ rksc_status branch_pass(const rksc_weights* w, const rksc_prefix_kv* kv, void* c
   if (!workspace) return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) % 256)
     return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
-  if (kv->n_prefix < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", kv->n_prefix);
-  if (kv->n_prefix > 0 && (!kv->k || !kv->v))
-    return fail(RKSC_ERR_INVALID_ARGUMENT, "prefix k/v are NULL with n_prefix = %d", kv->n_prefix);
+  Chain chain;
+  rksc_status st = collect_chain(kv, &chain);
+  if (st != RKSC_OK) return st;
   if (s < 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "suffix_len must be >= 1 (got %d)", s);
-  if ((long long)kv->n_prefix + pos + s > (1LL << 30)) return fail(RKSC_ERR_UNSUPPORTED, "positions above 2^30");
+  if (chain.n + pos + s > (1LL << 30)) return fail(RKSC_ERR_UNSUPPORTED, "positions above 2^30");
   const rksc_model_config* c = &w->cfg;
   Layout lay;
-  rksc_status st = make_layout(c, n_branches, s, kv->n_prefix, &lay);
+  st = make_layout(c, n_branches, s, (int)chain.n, &lay);
   if (st != RKSC_OK) return st;
   if (workspace_bytes < lay.total)
     return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
@@ -572,7 +642,7 @@ rksc_status branch_pass(const rksc_weights* w, const rksc_prefix_kv* kv, void* c
   const DType dt = c->dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
   const size_t T = dt == DType::BF16 ? 2 : 4;
   const int L = c->n_layers, d = c->d_model, H = c->n_heads, Hkv = c->n_kv_heads, hd = c->head_dim;
-  const int F = c->d_ff, V = c->vocab, B = n_branches, n = kv->n_prefix, len = off;
+  const int F = c->d_ff, V = c->vocab, B = n_branches, n = (int)chain.n, len = off;
   const int M = lay.max_rows;
   const int Nqkv = (H + 2 * Hkv) * hd;
   hipStream_t strm = static_cast<hipStream_t>(stream);
@@ -592,7 +662,6 @@ rksc_status branch_pass(const rksc_weights* w, const rksc_prefix_kv* kv, void* c
   float* opart = reinterpret_cast<float*>(ws + lay.opart);
   float* mlpart = reinterpret_cast<float*>(ws + lay.mlpart);
   const size_t res_stride = (size_t)M * d;
-  const size_t kv_layer = (size_t)Hkv * n * hd * T;
   const size_t bkv_layer = (size_t)B * Hkv * cap * hd * T;
   auto plane_lo = [&](float* buf, size_t elems) -> const void* {
     return dt == DType::BF16 ? static_cast<const void*>(reinterpret_cast<const uint16_t*>(buf) + elems) : nullptr;
@@ -601,8 +670,6 @@ rksc_status branch_pass(const rksc_weights* w, const rksc_prefix_kv* kv, void* c
   HIP_TRY(rksc::launch_init(ctrl, B, L, nullptr, nullptr, out.h_out, (size_t)L * B * d, strm));
   HIP_TRY(rksc::launch_rope_table(rope, s, n + pos, hd, (double)c->rope_base, strm));
   HIP_TRY(rksc::launch_embed(dt, w->embed, tokens, V, x0, M, d, strm));
-  const char* pk_base = static_cast<const char*>(kv->k);
-  const char* pv_base = static_cast<const char*>(kv->v);
   for (int l = 0; l < L; ++l) {
     const rksc_layer_weights& lw = w->layers[l];
     float* x_prev = (l % 2 == 0) ? x0 : x1;
@@ -625,21 +692,19 @@ rksc_status branch_pass(const rksc_weights* w, const rksc_prefix_kv* kv, void* c
     char* bv = static_cast<char*>(cv) + l * bkv_layer;
     HIP_TRY(rksc::launch_qkv_post(pbig, lay.qkv.splits, (size_t)M * Nqkv, ctrl, s, H, Hkv, hd, rope, qb, kown,
                                   vown, M, strm, dt, bk, bv, cap, len));
-    const void* pk = n > 0 ? pk_base + l * kv_layer : nullptr;
-    const void* pv = n > 0 ? pv_base + l * kv_layer : nullptr;
+    const rksc::PrefixView pre = layer_view(chain, l, Hkv, hd, T);
     if (step)
-      HIP_TRY(rksc::launch_attention_decode(dt, lay.attn, qb, pk, pv, bk, bv, len, cap, kown, vown, act, opart,
-                                            mlpart, ctrl, n, H, Hkv, hd, B, strm));
+      HIP_TRY(rksc::launch_attention_decode(dt, lay.attn, qb, pre, bk, bv, len, cap, kown, vown, act, opart,
+                                            mlpart, ctrl, H, Hkv, hd, B, strm));
     else
-      HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, pk, pv, kown, vown, act, opart, mlpart, ctrl, n, s, H, Hkv,
-                                     hd, B, strm));
+      HIP_TRY(rksc::launch_attention(dt, lay.attn, qb, pre, kown, vown, act, opart, mlpart, ctrl, s, H, Hkv, hd, B,
+                                     strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.o, act, plane_lo(act, (size_t)M * H * hd), lw.w_o, pres, res_stride, ctrl, s,
                               M, d, H * hd, strm));
     HIP_TRY(rksc::launch_add_norm(dt, x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
                                   lw.ffn_norm, d, c->rms_eps, M, strm));
-    HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig, (size_t)M * 2 * F,
-                              ctrl, s, M, 2 * F, d, strm));
-    HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
+    HIP_TRY(rksc::launch_gate_up_swiglu(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig,
+                                        (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
                               M, d, F, strm));
     if (l == L - 1 && (out.h_out || out.next_token))
@@ -702,9 +767,11 @@ RKSC_EXPORT size_t rksc_prefix_extend_workspace_size(const rksc_model_config* cf
   return lay.total;
 }
 
-// Tree sharing (a node's tokens on top of its parent's cache): the child cache
-// holds the parent's n entries followed by the m new tokens' entries, computed
-// once over the parent cache and shared by every child of the node.
+// Tree sharing (Sec. 2.2; the paper shares a search-tree node's step among its
+// children): the node's m tokens are run once over its ancestors' caches (the
+// parent chain, read in place) and the node's own cache [L, Hkv, m, hd] receives
+// their keys and values. Children read the chain root .. parent, node as their
+// prefix (rksc_prefix_kv.parent); nothing of the parent is copied.
 RKSC_EXPORT rksc_status rksc_prefix_extend(const rksc_weights* w, const rksc_prefix_kv* parent, const int32_t* tokens,
                                            int32_t n_new, void* k_out, void* v_out, float* h_node, void* workspace,
                                            size_t workspace_bytes, void* stream) {
@@ -715,51 +782,42 @@ RKSC_EXPORT rksc_status rksc_prefix_extend(const rksc_weights* w, const rksc_pre
   const rksc_model_config* c = &w->cfg;
   rksc_status st = check_config(c);
   if (st != RKSC_OK) return st;
-  const int n = parent->n_prefix;
-  if (n < 0) return fail(RKSC_ERR_INVALID_ARGUMENT, "n_prefix must be >= 0 (got %d)", n);
-  if ((long long)n + n_new > (1 << 30)) return fail(RKSC_ERR_UNSUPPORTED, "positions above 2^30");
+  Chain chain;
+  st = collect_chain(parent, &chain);
+  if (st != RKSC_OK) return st;
+  if (chain.nseg == rksc::kMaxPrefixSegs)
+    return fail(RKSC_ERR_UNSUPPORTED, "the node's children would read more than %d caches", rksc::kMaxPrefixSegs);
+  if (chain.n + n_new > (1LL << 30)) return fail(RKSC_ERR_UNSUPPORTED, "positions above 2^30");
   const size_t T = c->dtype == RKSC_BF16 ? 2 : 4;
-  const size_t row_new = (size_t)(n + n_new) * c->head_dim * T, row_old = (size_t)n * c->head_dim * T;
-  const size_t rows = (size_t)c->n_layers * c->n_kv_heads;
-  // The parent cache must not overlap the child cache (the copy reads it while rows are written).
-  if (n > 0 && parent->k && parent->v) {
-    auto overlap = [&](const void* a, size_t na, const void* b, size_t nb) {
-      const char *pa = static_cast<const char*>(a), *pb = static_cast<const char*>(b);
-      return pa < pb + nb && pb < pa + na;
-    };
-    const size_t child = rows * row_new, par = rows * row_old;
-    if (overlap(parent->k, par, k_out, child) || overlap(parent->v, par, v_out, child) ||
-        overlap(parent->k, par, v_out, child) || overlap(parent->v, par, k_out, child))
-      return fail(RKSC_ERR_INVALID_ARGUMENT, "the parent cache overlaps the child cache");
+  const size_t per_entry = (size_t)c->n_layers * c->n_kv_heads * c->head_dim * T;
+  const size_t child = per_entry * n_new;
+  // The new entries are written while every cache of the chain is read: no overlap.
+  auto overlap = [](const void* a, size_t na, const void* b, size_t nb) {
+    const char *pa = static_cast<const char*>(a), *pb = static_cast<const char*>(b);
+    return pa < pb + nb && pb < pa + na;
+  };
+  if (overlap(k_out, child, v_out, child)) return fail(RKSC_ERR_INVALID_ARGUMENT, "k_out overlaps v_out");
+  for (int i = 0; i < chain.nseg; ++i) {
+    const size_t par = per_entry * chain.seg[i]->n_prefix;
+    const void* pk = chain.seg[i]->k;
+    const void* pv = chain.seg[i]->v;
+    if (overlap(pk, par, k_out, child) || overlap(pv, par, v_out, child) || overlap(pk, par, v_out, child) ||
+        overlap(pv, par, k_out, child))
+      return fail(RKSC_ERR_INVALID_ARGUMENT, "a parent cache overlaps the node's cache");
   }
-  // Validate the pass before copying anything.
   Layout lay;
-  st = make_layout(c, 1, n_new, n, &lay);
+  st = make_layout(c, 1, n_new, (int)chain.n, &lay);
   if (st != RKSC_OK) return st;
   if (workspace && workspace_bytes < lay.total)
     return fail(RKSC_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, needs %zu", workspace_bytes, lay.total);
-  if (n > 0 && (!parent->k || !parent->v))
-    return fail(RKSC_ERR_INVALID_ARGUMENT, "parent k/v are NULL with n_prefix = %d", n);
   if (!tokens) return fail(RKSC_ERR_INVALID_ARGUMENT, "tokens is NULL");
   if (!workspace) return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(workspace) % 256)
-    return fail(RKSC_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
   if (!w->embed || !w->final_norm || !w->layers)
     return fail(RKSC_ERR_INVALID_ARGUMENT, "embed, final_norm and layers must not be NULL");
-  for (int l = 0; l < c->n_layers; ++l) {
-    const rksc_layer_weights& lw = w->layers[l];
-    if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
-      return fail(RKSC_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
-  }
-  hipStream_t strm = static_cast<hipStream_t>(stream);
-  if (n > 0) {
-    HIP_TRY(hipMemcpy2DAsync(k_out, row_new, parent->k, row_old, row_old, rows, hipMemcpyDeviceToDevice, strm));
-    HIP_TRY(hipMemcpy2DAsync(v_out, row_new, parent->v, row_old, row_old, rows, hipMemcpyDeviceToDevice, strm));
-  }
-  st = branch_pass(w, parent, k_out, v_out, n + n_new, n, 0, tokens, 1, n_new, false,
+  st = branch_pass(w, parent, k_out, v_out, n_new, 0, 0, tokens, 1, n_new, false,
                    PassOut{nullptr, nullptr, nullptr, h_node}, workspace, workspace_bytes, stream);
   if (st != RKSC_OK) return st;
-  if (h_node) HIP_TRY(rksc::launch_unit_rows(h_node, c->n_layers, c->d_model, strm));
+  if (h_node) HIP_TRY(rksc::launch_unit_rows(h_node, c->n_layers, c->d_model, static_cast<hipStream_t>(stream)));
   return ok();
 }
 
@@ -860,6 +918,26 @@ RKSC_EXPORT rksc_status rksc_test_gemm_live(int32_t dtype, const void* A, const 
   return ok();
 }
 
+RKSC_EXPORT rksc_status rksc_test_gate_up_swiglu(const void* A, const void* A_lo, const void* W, void* a_out,
+                                                 float* P, int32_t M, int32_t F, int32_t K, int32_t fused,
+                                                 void* stream) {
+  if (!A || !A_lo || !W || !a_out || !P) return fail(RKSC_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if (M < 1 || F < 8 || F % 8 || K < 8 || K % 8)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "bad shape %d x %d x %d", M, F, K);
+  if (fused != 0 && fused != 1) return fail(RKSC_ERR_INVALID_ARGUMENT, "fused must be 0 or 1");
+  GemmPlan p = rksc::plan_gemm_kind(DType::BF16, M, 2 * F, K, fused ? 1 : -1, fused ? 1 : 0);
+  if (fused && !rksc::gate_up_fused(DType::BF16, p, 2 * F))
+    return fail(RKSC_ERR_UNSUPPORTED, "no fused plan for this shape");
+  if (!fused && rksc::gate_up_fused(DType::BF16, p, 2 * F)) {   // the unfused path: partials + SwiGLU kernel
+    p.kind = 0;
+    p.bm = 128;
+    p.k_per_split = (K + 63) / 64 * 64;
+  }
+  HIP_TRY(rksc::launch_gate_up_swiglu(DType::BF16, p, A, A_lo, W, P, (size_t)M * 2 * F, nullptr, 1, M, F, K, a_out,
+                                      static_cast<hipStream_t>(stream)));
+  return ok();
+}
+
 RKSC_EXPORT rksc_status rksc_test_gemm_plan(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t splits,
                                             int32_t kind, int32_t* plan) {
   if (!plan) return fail(RKSC_ERR_INVALID_ARGUMENT, "plan must not be NULL");
@@ -910,7 +988,14 @@ RKSC_EXPORT rksc_status rksc_test_attention(int32_t dtype, const void* q, const 
   float* opart = reinterpret_cast<float*>(sc + 4096);
   float* mlpart = opart + (size_t)plan.partials * B * s * H * hd;
   HIP_TRY(rksc::launch_init(ctrl, B, 1, nullptr, nullptr, nullptr, 0, st));
-  HIP_TRY(rksc::launch_attention(dt, plan, q, prefix_k, prefix_v, k_own, v_own, o, opart, mlpart, ctrl, n, s, H,
-                                 Hkv, hd, B, st));
+  rksc::PrefixView pre;
+  if (n > 0) {
+    pre.n = n;
+    pre.nseg = 1;
+    pre.len[0] = n;
+    pre.k[0] = prefix_k;
+    pre.v[0] = prefix_v;
+  }
+  HIP_TRY(rksc::launch_attention(dt, plan, q, pre, k_own, v_own, o, opart, mlpart, ctrl, s, H, Hkv, hd, B, st));
   return ok();
 }

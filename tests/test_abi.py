@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
     assert "rksc_verify_forward" in names and "rksc_asks_similarity" in names
     for name in names:
         assert hasattr(lib, name), f"{name} declared in include/ but not exported"
-    assert rk.rksc_abi_version() == 6
+    assert rk.rksc_abi_version() == 7
 
 
 def test_status_strings(lib):
@@ -374,3 +374,58 @@ def test_noalloc_refuses_oversized_pass_before_any_hip_call(lib):
     text = open(os.path.join(ROOT, "include", "rksc.h")).read()
     assert "#define RKSC_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)" in text
     assert rk.RKSC_NOALLOC_SCRATCH_BYTES == 128 << 20
+
+
+def test_exit_window_cost_model(lib):
+    """The exit window of the default schedule (host only): a power of two with window * B <= 64, the
+    value the cost model gives at each workload, and no window at all for an invalid shape."""
+    expect = {"7b_single": 8, "7b_tot": 2, "7b_large_vocab": 4, "10b_long": 2, "10b_decode": 2,
+              "7b_paper_verify": 4, "tiny": 1, "tiny_deep": 1}
+    for name, w in expect.items():
+        wl = workloads.get(name)
+        got = rk.rksc_verify_window(wl.model, wl.n_branches, wl.branch_len, wl.prefix_len)
+        assert got == w, (name, got)
+    shape = workloads.get("7b_single").model
+    for B in (1, 2, 5, 8, 9, 16, 17, 32, 33, 64):
+        for s, n in ((1, 0), (16, 64), (128, 1024), (256, 16384)):
+            w = rk.rksc_verify_window(shape, B, s, n)
+            assert w in (1, 2, 4, 8) and w * B <= 64
+    # more work per layer never asks for a larger window (the probe is a smaller share)
+    ws = [rk.rksc_verify_window(shape, 1, s, 1024) for s in (1, 16, 128, 1024, 4096)]
+    assert ws == sorted(ws, reverse=True)
+    with pytest.raises(rk.RkscError):
+        rk.rksc_verify_window(shape, 0, 16, 64)
+    with pytest.raises(rk.RkscError):
+        rk.rksc_verify_window(_shape(head_dim=32), 4, 16, 64)
+
+
+def test_prefix_chain_limits_before_any_launch(lib):
+    """A prefix chain longer than RKSC_MAX_PREFIX_SEGMENTS caches, or a cycle, is refused during
+    validation; so is a tree node whose children's chain would be too long."""
+    shape = workloads.get("tiny").model
+    w, _keep, cfg = _fake_weights(shape)
+    ws = lib.rksc_verify_workspace_size(ctypes.byref(cfg), 4, 16, 9 * 8)
+    ok_ws = ctypes.c_void_p(0x100000)
+    segs = []
+    for i in range(rk.RKSC_MAX_PREFIX_SEGMENTS + 1):
+        seg = rk.PrefixKV(8, ctypes.c_void_p(0x1000000 * (i + 1)), ctypes.c_void_p(0x1000000 * (i + 1) + 0x800000))
+        if segs:
+            seg.parent = ctypes.pointer(segs[-1])
+        segs.append(seg)
+
+    def verify(kv):
+        return lib.rksc_verify_forward(ctypes.byref(w), ctypes.byref(kv), FAKE, 4, 16, 0.1, 1, FAKE, FAKE, None,
+                                       ok_ws, ws, None)
+
+    assert verify(segs[-1]) == rk.RKSC_ERR_UNSUPPORTED and "chain" in rk.rksc_last_error()
+    cyc = rk.PrefixKV(8, FAKE, FAKE)
+    cyc.parent = ctypes.pointer(cyc)
+    assert verify(cyc) == rk.RKSC_ERR_UNSUPPORTED
+    bad = rk.PrefixKV(8, FAKE, FAKE)
+    bad.parent = ctypes.pointer(rk.PrefixKV(4, None, FAKE))
+    assert verify(bad) == rk.RKSC_ERR_INVALID_ARGUMENT
+    ext_ws = lib.rksc_prefix_extend_workspace_size(ctypes.byref(cfg), 8 * 8, 4)
+    full = segs[rk.RKSC_MAX_PREFIX_SEGMENTS - 1]     # a chain of exactly the maximum
+    st = lib.rksc_prefix_extend(ctypes.byref(w), ctypes.byref(full), FAKE, 4, ctypes.c_void_p(0x70000000),
+                                ctypes.c_void_p(0x78000000), None, ok_ws, ext_ws, None)
+    assert st == rk.RKSC_ERR_UNSUPPORTED and "children" in rk.rksc_last_error()

@@ -19,7 +19,7 @@ def _rand(shape, dtype, seed, std=1.0):
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
 @pytest.mark.parametrize("M,N,K,splits", [
     (1, 64, 64, 0), (64, 100, 688, 0), (100, 200, 256, 1), (128, 192, 4096, 0),
-    (300, 136, 128, 3), (513, 260, 512, 0), (77, 64, 1000, 5),
+    (300, 136, 128, 3), (513, 264, 512, 0), (77, 64, 1000, 5),
     # 256 x 256 tiles (512 rows and more): ragged rows, columns and K, forced splits
     (777, 700, 1000, 3), (1024, 512, 2048, 0), (2048, 1536, 4104, 0),
     # one row tile: the 7B projections at 128 rows with the planner's tile width and split count
@@ -170,6 +170,34 @@ def test_gemm_row_offsets_past_2_31(kind):
     err = np.abs(got - a @ w.T)
     assert (err <= bound).all(), f"max err {err.max():.3e} at row {rows[np.unravel_index(err.argmax(), err.shape)[0]]}"
     del a_hi, a_lo, P
+
+
+@pytest.mark.parametrize("M,F,K,fused", [
+    (777, 712, 1000, 1), (1024, 2048, 1024, 1), (300, 136, 4104, 1), (4096, 1792, 4096, 1),
+    (513, 264, 512, 0), (128, 1024, 4096, 0),
+])
+def test_gate_up_swiglu_matches_fp64(M, F, K, fused):
+    """The gate|up projection with its SwiGLU: the 256 x 256 kernel with the SwiGLU in its epilogue
+    (ragged rows, F not a multiple of its 128-column half tiles, ragged K) and the split path."""
+    log(f"gate_up swiglu M={M} F={F} K={K} fused={fused}")
+    A = _rand((M, K), torch.float32, 41 + M, 0.5)
+    W = _rand((2 * F, K), torch.bfloat16, 42 + F, 0.05)
+    a_hi = A.to(torch.bfloat16)
+    a_lo = (A - a_hi.float()).to(torch.bfloat16)
+    A = a_hi.float() + a_lo.float()
+    got = rk.rksc_test_gate_up_swiglu((a_hi.to(DEV), a_lo.to(DEV)), W.to(DEV), bool(fused))
+    torch.cuda.synchronize()
+    got = got.double().cpu().numpy()
+    a, w = A.double().numpy(), W.double().numpy()
+    gu = a @ w.T
+    g, u = gu[:, :F], gu[:, F:]
+    sig = 1.0 / (1.0 + np.exp(-g))
+    ref = g * sig * u
+    eb = 1e-5 * (np.abs(a) @ np.abs(w).T) + 1e-7
+    dsilu = np.abs(sig * (1 + g * (1 - sig)))
+    bound = dsilu * eb[:, :F] * np.abs(u) + np.abs(g * sig) * eb[:, F:] + 1e-6 * np.abs(ref) + 1e-7
+    err = np.abs(got - ref)
+    assert (err <= bound).all(), f"max err {err.max():.3e} at {np.unravel_index(err.argmax(), err.shape)}"
 
 
 def _attention_cases():

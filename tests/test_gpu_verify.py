@@ -170,7 +170,7 @@ def test_exit_window_does_not_change_outputs(B, taus):
     for bit (the same stream kernel; each column is computed on its own)."""
     shape = dataclasses.replace(workloads.get("tiny_deep").model, dtype="bf16")
     mw, kv, toks = _inputs(shape, B, 64, 5, 91)
-    assert rk.rksc_verify_window(B) == (4 if B <= 16 else 2 if B <= 32 else 1)
+    auto = rk.rksc_verify_window(shape, B, 5, 64)
     for tau in taus:
         ent_ref, hid_ref, ex_ref = _run_oracle(mw, kv, toks, tau, 1)
         base = None
@@ -182,6 +182,12 @@ def test_exit_window_does_not_change_outputs(B, taus):
             ent, ex, hid = to_np(ent), to_np(ex), to_np(hid)
             stats = compare_verify(ent, ex, hid, ent_ref, hid_ref, ex_ref, tau, label=f"B={B} tau={tau} win={win}")
             log(f"[window B={B} tau={tau} win={win}] exits {ex.tolist()} {stats}")
+            if win == auto:   # the default call takes the cost model's window: the same outputs
+                d_ent, d_ex, d_hid = rk.verify_forward(mw, kv.k, kv.v, toks, tau, 1, return_hidden=True)
+                torch.cuda.synchronize()
+                np.testing.assert_array_equal(to_np(d_ex), ex)
+                np.testing.assert_array_equal(to_np(d_ent), ent)
+                np.testing.assert_array_equal(to_np(d_hid), hid)
             if base is None:
                 base = (ent, ex, hid)
             elif win * B <= 32:
@@ -221,7 +227,7 @@ def _pick_tau_margin(ent_ref, patience, L, window, margin):
     return best
 
 
-def _exit_path_case(name, n_layers, patience, sampled, window_expect):
+def _exit_path_case(name, n_layers, patience, sampled, window_expect, window=None):
     """Full-size kernel plans with exits firing (Alg. VerifyWithEntropyExit; Sec. 2.3
     "Layer-level entropy exit"): the workload's width, branch count, prefix and span over
     n_layers layers; tau is read off the oracle's deltas of the sampled branches so that they
@@ -230,7 +236,8 @@ def _exit_path_case(name, n_layers, patience, sampled, window_expect):
     wl = workloads.get(name)
     mw, kv, toks = _inputs(wl.model, wl.n_branches, wl.prefix_len, wl.branch_len, seed=42, n_layers=n_layers)
     L = n_layers
-    win = rk.rksc_verify_window(wl.n_branches)
+    win = window or rk.rksc_verify_window(dataclasses.replace(wl.model, n_layers=L), wl.n_branches, wl.branch_len,
+                                          wl.prefix_len)
     assert win == window_expect
     log(f"[{name} exit path] oracle on branches {sampled}")
     ent_ref, hid_ref, _ = _run_oracle(mw, kv, toks, 0.0, 1, branches=sampled)
@@ -238,9 +245,11 @@ def _exit_path_case(name, n_layers, patience, sampled, window_expect):
     assert tau is not None, f"no separable tau in the oracle deltas {np.abs(np.diff(ent_ref, axis=0)).T}"
     ex_ref = np.array([oracle.exit_layer(ent_ref[:, j], tau, patience) for j in range(len(sampled))])
     log(f"[{name} exit path] tau={tau:.4f} patience={patience} oracle exits {ex_ref.tolist()}")
-    ent, ex, hid = _run_gpu(mw, kv, toks, tau, patience)
+    ent, ex, hid = rk.verify_forward(mw, kv.k, kv.v, toks, tau, patience, return_hidden=True, window=window)
+    torch.cuda.synchronize()
+    ent, ex, hid = to_np(ent), to_np(ex), to_np(hid)
     stats = compare_verify(ent, ex, hid, ent_ref, hid_ref, ex_ref, tau, branches=sampled,
-                           label=f"{name} L={L} tau={tau:.4f}")
+                           label=f"{name} L={L} tau={tau:.4f} window={win}")
     log(f"[{name} exit path] gpu exits {ex.tolist()} {stats}")
     assert stats["near_threshold"] == 0 and stats["exit_match"] == len(sampled)
     assert (ex < L).sum() >= 1 and len(set(ex.tolist())) >= 2, "the live set must shrink during the call"
@@ -259,5 +268,40 @@ def test_exit_path_full_plans_paper_verify():
 
 def test_exit_path_full_plans_10b_long():
     """6 layers of the 10B long-prefix shape, 32 x 256 rows over 16384 prefix tokens, patience 1:
-    8192-row projections, exit windows of 2 layers at 32 live columns."""
-    _exit_path_case("10b_long", 6, 1, [1, 17, 30], 2)
+    8192-row projections, exit windows of 2 layers at 32 live columns (the window the cost model
+    takes for the full 48-layer pass; with 6 layers it would take 1, so it is set here)."""
+    _exit_path_case("10b_long", 6, 1, [1, 17, 30], 2, window=2)
+
+
+@pytest.mark.parametrize("shape,B,n,s,cuts", [
+    (GQA_BF16, 3, 200, 40, (70, 130)),                 # per-branch (fused) tiles, cuts inside key tiles
+    (GQA_BF16, 6, 300, 3, (64, 65, 250)),              # packed tiles (G * s < 64), a one-entry segment
+    (G7_BF16, 2, 129, 65, (1,)),
+    (workloads.get("tiny_deep").model, 4, 64, 16, (17, 40)),   # fp32 model: the plain kernel
+])
+def test_prefix_chain_equals_one_cache(shape, B, n, s, cuts):
+    """A prefix given as a chain of caches (tree sharing: the ancestors' caches read in place)
+    gives bit for bit the outputs of the same prefix as one cache, for the verify pass and for a
+    batched decode step over it."""
+    mw, kv, toks = _inputs(shape, B, n, s, seed=17)
+    bounds = [0, *cuts, n]
+    segs = [(kv.k[:, :, a:b].contiguous(), kv.v[:, :, a:b].contiguous()) for a, b in zip(bounds[:-1], bounds[1:])]
+    chain = rk.PrefixCache(segs)
+    assert chain.n_prefix == n
+    for tau in (0.3, 0.0):
+        one = rk.verify_forward(mw, kv.k, kv.v, toks, tau, 1, return_hidden=True)
+        many = rk.verify_forward(mw, chain, None, toks, tau, 1, return_hidden=True)
+        torch.cuda.synchronize()
+        for a, b, what in zip(one, many, ("entropy", "exit", "hidden")):
+            np.testing.assert_array_equal(to_np(a), to_np(b), err_msg=f"{what} differs (tau={tau})")
+    # batched decode: suffix then two steps, over one cache and over the chain
+    outs = []
+    for pre_k, pre_v in ((kv.k, kv.v), (chain, None)):
+        dec = rk.Decoder(mw, pre_k, pre_v, B, s, capacity=s + 2, device=DEV)
+        got = [t.clone() for t in dec.suffix(toks)]
+        for _ in range(2):
+            got += [t.clone() for t in dec.step()]
+        torch.cuda.synchronize()
+        outs.append([to_np(t) for t in got])
+    for a, b in zip(*outs):
+        np.testing.assert_array_equal(a, b)
