@@ -27,6 +27,7 @@ namespace {
 
 constexpr int kAttnWaves = 8;    // waves per attention workgroup (16 query rows each)
 constexpr int kAttnRing = 4;     // prefix K/V tiles in the LDS ring
+constexpr float kLazyLog2 = 8.f; // slack of the softmax reference (log2 units): p <= 2^8
 
 // a if c, else zero; component-wise so that no address is selected (a select
 // of struct lvalues keeps register arrays in scratch memory).
@@ -64,7 +65,7 @@ __device__ __forceinline__ int vt_col(int dim, int key) {
 }
 
 // Prefix K/V tiles are moved by DMA (global_load_lds) in their natural
-// [key][dim] layout into an R-slot LDS ring, several tiles ahead of the
+// [key][dim] layout into R-slot LDS rings (one for K, one for V), several tiles ahead of the
 // contraction. The 16-byte chunks of a key row are XOR-swizzled by the key:
 // K by key & (CPR - 1), so that the 16 rows of a fragment read hit distinct
 // banks; V by (key & (CPR/2 - 1)) << 1, which keeps chunk pairs together for
@@ -82,13 +83,14 @@ __device__ __forceinline__ int swz_v(int key, int cpr) { return (key & (cpr / 2 
 // results are made valid by an explicit lgkmcnt(0) that takes the fragments as
 // operands, so no use of them can be scheduled before it.
 typedef short shortx4 __attribute__((ext_vector_type(4)));
-template <int OFF>
+template <int OFF0, int OFF1>
 __device__ __forceinline__ void lds_read_tr16_pair(uint32_t addr, shortx4& a, shortx4& b) {
+  static_assert(OFF0 >= 0 && OFF1 < 65536, "ds offsets are 16-bit immediates");
   // Early-clobber outputs: the first read's destination must not share a
   // register with the address that the second read still uses.
-  asm volatile("ds_read_b64_tr_b16 %0, %2\n\tds_read_b64_tr_b16 %1, %2 offset:%3"
+  asm volatile("ds_read_b64_tr_b16 %0, %2 offset:%3\n\tds_read_b64_tr_b16 %1, %2 offset:%4"
                : "=&v"(a), "=&v"(b)
-               : "v"(addr), "i"(OFF));
+               : "v"(addr), "i"(OFF0), "i"(OFF1));
 }
 template <int ND>
 __device__ __forceinline__ void lds_wait_pairs(shortx4 (&a)[ND], shortx4 (&b)[ND]) {
@@ -134,7 +136,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   constexpr int CPR = HD / 8;              // 16-byte chunks per key row
   constexpr int ROW = HD * 2;              // bytes per key row
   constexpr int TB = KT * ROW;             // bytes of a K (or V) tile
-  constexpr int SLOT = 2 * TB;             // ring slot: K tile, then V tile
+  constexpr int SLOT = 2 * TB;             // one tile: K (in the K ring), V (in the V ring)
   constexpr int R = kAttnRing;
   constexpr int IPT = SLOT / 1024;         // 1 KB DMA instructions per tile
   static_assert(IPT % NW == 0, "every wave issues the same number of DMA instructions");
@@ -219,19 +221,25 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
 
   // ---- prefix DMA: instruction ins = j * NW + wid of a tile moves RPI key rows
   // of K (ins < IPT/2) or V; lane L fills physical chunk L % CPR of row L / CPR.
+  // The first half of a wave's instructions move K, the rest V (IPT/2 is a
+  // multiple of NW). The wave index is made uniform so that the LDS
+  // destinations are scalar (M0) values; a full tile is addressed as a scalar
+  // tile base plus this lane's fixed 32-bit byte offset dlane[j].
+  static_assert((IPT / 2) % NW == 0, "K and V instructions of a wave are fixed by j");
+  const int widu = __builtin_amdgcn_readfirstlane(wid);
   int dkey[IPW], dsrc[IPW], ddst[IPW];
-  bool dv[IPW];
+  uint32_t dlane[IPW];
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
-    const int ins = j * NW + wid;
-    dv[j] = ins >= IPT / 2;
-    const int i_in = dv[j] ? ins - IPT / 2 : ins;
-    const int key = i_in * RPI + lane / CPR;
+    const bool isv = j * NW >= IPT / 2;
+    const int i_in = j * NW + (isv ? widu - IPT / 2 : widu);
+    const int key = (j * NW + wid - (isv ? IPT / 2 : 0)) * RPI + lane / CPR;
     const int ph = lane % CPR;
-    const int lc = ph ^ (dv[j] ? swz_v(key, CPR) : swz_k(key, CPR));
+    const int lc = ph ^ (isv ? swz_v(key, CPR) : swz_k(key, CPR));
     dkey[j] = key;
     dsrc[j] = lc * 8;
-    ddst[j] = (dv[j] ? TB : 0) + i_in * 1024;
+    dlane[j] = (uint32_t)(key * ROW + lc * 16);
+    ddst[j] = (isv ? R * TB : 0) + i_in * 1024;
   }
   // Transposing V reads: this lane points at key 4g + r16/4 of each 32-key
   // block (and 16 keys further, an immediate offset), dims 16dt + 4 (r16 % 4)
@@ -246,7 +254,11 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     for (int dt = 0; dt < ND; ++dt)
       voff[dt] = vk * ROW + 32 * (dt ^ mv) + 16 * ((r16 & 3) >> 1) + 8 * (r16 & 1);
   }
-  const uint32_t smem_lds = (uint32_t)reinterpret_cast<uintptr_t>(smem);   // LDS byte offset of the ring
+  // LDS byte address of the V ring, and of this lane's reads in a V tile at slot 0.
+  const uint32_t vring = (uint32_t)reinterpret_cast<uintptr_t>(smem) + R * TB;
+  uint32_t vaddr[ND];
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt) vaddr[dt] = vring + voff[dt];
 
   // One segment (MS = false): every row from the one base, straight-line code.
   // Several (MS): a tile inside one segment addresses its rows from that
@@ -258,10 +270,17 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   auto issue = [&](int pt, int sl) {
     const int kbase = pt * KT;
     if constexpr (!MS) {
+      if (kbase + KT <= n) {
+        const char* const kt0 = reinterpret_cast<const char*>(Kp0 + (size_t)kbase * HD);
+        const char* const vt0 = reinterpret_cast<const char*>(Vp0 + (size_t)kbase * HD);
 #pragma unroll
-      for (int j = 0; j < IPW; ++j) {
-        const int key = min(kbase + dkey[j], n - 1);   // rows past n - 1 are masked in the contraction
-        dma16((dv[j] ? Vp0 : Kp0) + (size_t)key * HD + dsrc[j], smem + sl * SLOT + ddst[j]);
+        for (int j = 0; j < IPW; ++j) dma16((j * NW >= IPT / 2 ? vt0 : kt0) + dlane[j], smem + sl * TB + ddst[j]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < IPW; ++j) {
+          const int key = min(kbase + dkey[j], n - 1);   // rows past n - 1 are masked in the contraction
+          dma16((j * NW >= IPT / 2 ? Vp0 : Kp0) + (size_t)key * HD + dsrc[j], smem + sl * TB + ddst[j]);
+        }
       }
     } else {
       int sg = 0;
@@ -274,13 +293,13 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
 #pragma unroll
         for (int j = 0; j < IPW; ++j) {
           const int key = min(kbase + dkey[j], n - 1);
-          dma16((dv[j] ? Vt : Kt) + (size_t)(key - kbase) * HD + dsrc[j], smem + sl * SLOT + ddst[j]);
+          dma16((j * NW >= IPT / 2 ? Vt : Kt) + (size_t)(key - kbase) * HD + dsrc[j], smem + sl * TB + ddst[j]);
         }
       } else {
 #pragma unroll
         for (int j = 0; j < IPW; ++j) {
           const int key = min(kbase + dkey[j], n - 1);
-          dma16(prefix_row<bf16, HD>(pre, dv[j], kvh, key) + dsrc[j], smem + sl * SLOT + ddst[j]);
+          dma16(prefix_row<bf16, HD>(pre, j * NW >= IPT / 2, kvh, key) + dsrc[j], smem + sl * TB + ddst[j]);
         }
       }
     }
@@ -337,20 +356,25 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     }
   };
 
-  // Contraction of one tile with this lane's query, in two parts so that the
+  // Contraction of one tile with this lane's query, in three parts so that the
   // prefix loop can overlap them across tiles:
-  // - scores: S^T = K Q^T (lane holds the scores of keys 16*kt + 4g + i of its
-  //   query);
-  // - softmax_pv: online softmax in log2 units, then O^T += V^T P^T.
+  // - scores: S^T = K Q^T relative to the lane's softmax reference (the MFMA
+  //   accumulator starts at -m, or at 0 while no key has been seen), so the
+  //   lane holds score - m of keys 16*kt + 4g + i of its query;
+  // - stats: mask, tile maximum, reference update;
+  // - pv: p = 2^(score - m), then O^T += V^T P^T.
   // OWN: a padded own-span tile whose keys and values are hi/lo pairs (three
   // MFMAs per product), causal mask; otherwise the prefix tile in ring slot
-  // `sl`. MASKED: some keys of the tile are invalid for some query.
-  auto scores = [&](auto own_c, int sl, floatx4 (&sc)[4]) {
+  // `sl`: an int, or a std::integral_constant so that every LDS offset of the
+  // tile is an instruction immediate. MASKED: some keys of the tile are invalid
+  // for some query.
+  auto scores = [&](auto own_c, auto sl, floatx4 (&sc)[4]) {
     constexpr bool OWN = decltype(own_c)::value;
-    const uint8_t* Kt = smem + sl * SLOT;
+    const float bias = m == -INFINITY ? 0.f : -m;
+    const uint8_t* Kt = smem + (int)sl * TB;
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
-      sc[kt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      sc[kt] = floatx4{bias, bias, bias, bias};
       const int key = 16 * kt + r16;
 #pragma unroll
       for (int cc = 0; cc < NC; ++cc) {
@@ -369,7 +393,19 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
       }
     }
   };
-  auto softmax_pv = [&](auto own_c, auto masked_c, int sl, int kbase, floatx4 (&sc)[4]) {
+  // Online softmax with a lazily moved reference: the probabilities are
+  // p = 2^(score - m) for a per-query reference m that moves only when a tile's
+  // maximum exceeds it by more than kLazyLog2 (then to that maximum, rescaling
+  // l and the accumulator by 2^(m_old - m_new)). Otherwise p <= 2^kLazyLog2 and
+  // the tile needs no rescale: the accumulators are exact sums relative to m
+  // either way, and the final normalisation by l (or the combine's weights
+  // 2^(m_c - M)) cancels the choice of m. The move is decided per lane (the four
+  // lanes of a query see the same tile maximum), and the rescale runs behind a
+  // wave-uniform branch that, past the first tiles, is rarely taken. The
+  // scores arrive relative to the reference in force when they were formed,
+  // which is the current one (no update comes between a tile's scores and its
+  // stats); a move shifts them to the new reference.
+  auto stats = [&](auto own_c, auto masked_c, int kbase, floatx4 (&sc)[4]) {
     constexpr bool OWN = decltype(own_c)::value;
     constexpr bool MASKED = decltype(masked_c)::value;
     if constexpr (MASKED) {
@@ -386,29 +422,35 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     for (int kt = 1; kt < 4; ++kt) mt = fmaxf(mt, fmaxf(fmaxf(sc[kt][0], sc[kt][1]), fmaxf(sc[kt][2], sc[kt][3])));
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float mn = fmaxf(m, mt);
-    // A fully masked tile for this query (an own-span tile past it, possible
-    // only when MASKED) leaves mn = -inf: then nothing is accumulated.
-    const bool none = MASKED && mn == -INFINITY;
-    const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m - mn);   // m = -inf gives 0
-    const float msub = none ? 0.f : mn;
-    m = mn;
-    // Branch-free rescale, so the whole contraction stays one scheduling region.
-    l *= alpha;
+    // mt is relative to the scores' reference: m, or 0 while m = -inf (then any
+    // finite maximum moves it; a fully masked tile, mt = -inf, never does).
+    const bool fresh = m == -INFINITY;
+    const bool up = fresh ? mt > -INFINITY : mt > kLazyLog2;
+    if (__builtin_amdgcn_ballot_w64(up) != 0) {
+      const float shift = up ? mt : 0.f;                 // new reference - old, in score units
+      const float alpha = up && !fresh ? __builtin_amdgcn_exp2f(-mt) : (fresh ? 0.f : 1.f);
+      m = up ? (fresh ? mt : m + mt) : m;
+      l *= alpha;
 #pragma unroll
-    for (int dt = 0; dt < ND; ++dt) oacc[dt] *= alpha;
+      for (int dt = 0; dt < ND; ++dt) oacc[dt] *= alpha;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) sc[kt] -= shift;
+    }
+  };
+  auto pv = [&](auto own_c, auto sl, floatx4 (&sc)[4]) {
+    constexpr bool OWN = decltype(own_c)::value;
     float p[4][4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        p[kt][i] = __builtin_amdgcn_exp2f(sc[kt][i] - msub);   // masked: exp2(-inf) = 0
+        p[kt][i] = __builtin_amdgcn_exp2f(sc[kt][i]);   // masked (and no key yet): exp2(-inf) = 0
         l += p[kt][i];
       }
     // O^T += V^T P^T over two 32-key blocks; lane group g supplies keys
     // {32kb + 4g + e, 32kb + 16 + 4g + e}, e = 0..3, in both operands.
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    auto block = [&](auto kb_c) {
+      constexpr int kb = decltype(kb_c)::value;
       // hi/lo split of the probabilities, two at a time: hi = bf16(p) packed
       // by one conversion, lo = bf16(p - hi) likewise.
       uint32_t ph[4], pl[4] = {0u, 0u, 0u, 0u};
@@ -427,9 +469,15 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
       const bf16x8 pbl = __builtin_bit_cast(bf16x8, make_uint4(pl[0], pl[1], pl[2], pl[3]));
       shortx4 vlo[ND], vhi[ND];
       if constexpr (!OWN) {
-        const uint32_t vb = smem_lds + sl * SLOT + TB + kb * 32 * ROW;
+        if constexpr (std::is_integral_v<decltype(sl)>) {
+          const uint32_t vb = vring + sl * TB + kb * 32 * ROW;
 #pragma unroll
-        for (int dt = 0; dt < ND; ++dt) lds_read_tr16_pair<16 * ROW>(vb + voff[dt], vlo[dt], vhi[dt]);
+          for (int dt = 0; dt < ND; ++dt) lds_read_tr16_pair<0, 16 * ROW>(vb + voff[dt], vlo[dt], vhi[dt]);
+        } else {
+          constexpr int IMM = decltype(sl)::value * TB + kb * 32 * ROW;
+#pragma unroll
+          for (int dt = 0; dt < ND; ++dt) lds_read_tr16_pair<IMM, IMM + 16 * ROW>(vaddr[dt], vlo[dt], vhi[dt]);
+        }
         lds_wait_pairs<ND>(vlo, vhi);
       }
 #pragma unroll
@@ -449,45 +497,71 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
           oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, pbh, oacc[dt], 0, 0, 0);
         }
       }
-    }
+    };
+    block(std::integral_constant<int, 0>{});
+    block(std::integral_constant<int, 1>{});
   };
   auto contract = [&](auto own_c, auto masked_c, int sl, int kbase) {
     floatx4 sc[4];
     scores(own_c, sl, sc);
-    softmax_pv(own_c, masked_c, sl, kbase, sc);
+    stats(own_c, masked_c, kbase, sc);
+    pv(own_c, sl, sc);
   };
 
   // ---- prefix tiles of this chunk through the ring, software-pipelined: the
   // scores of tile i+1 (MFMA) are formed in the same scheduling region as the
   // softmax of tile i (VALU), so the two overlap on the SIMD. Every step issues
   // one tile (past the end: a harmless re-fetch of the first); at step i the
-  // DMA instructions behind tile i+1 are those of tiles i+2 .. i+R-2.
+  // DMA instructions behind tile i+1 are those of tiles i+2 .. i+R-2. The loop
+  // is unrolled R times so that tile i's slot, i % R, is a compile-time
+  // constant; the score arrays alternate between two register sets.
   const int p_end = min(t_end, n_ptiles);
   const int np = p_end - t_begin;
   if (np > 0) {
-    static_assert(R >= 3, "the pipelined loop needs a slot for tile i+1 and one being refilled");
+    static_assert(R >= 3 && R % 2 == 0, "the pipelined loop needs a slot for tile i+1 and one being refilled");
 #pragma unroll
     for (int u = 0; u < R - 1; ++u) issue(t_begin + (u < np ? u : 0), u);
     wait_vmcnt_lds<IPW * (R - 2)>();   // tile 0
     __builtin_amdgcn_s_barrier();
-    floatx4 sc_cur[4];
-    scores(std::false_type{}, 0, sc_cur);
+    floatx4 sca[4], scb[4];
+    scores(std::false_type{}, std::integral_constant<int, 0>{}, sca);
     // Tiles before the chunk's last are never partial (only the prefix's last
     // tile can be, and it is the last of its chunk).
-    for (int i = 0; i + 1 < np; ++i) {
+    int i = 0;
+    auto step = [&](auto sl_c) {
+      constexpr int SL = decltype(sl_c)::value;
       wait_vmcnt_lds<IPW * (R - 3)>();   // tile i+1 has landed; every wave is done with slot (i-1) % R
       __builtin_amdgcn_s_barrier();
       const int nx = i + R - 1;
-      issue(t_begin + (nx < np ? nx : 0), nx % R);
-      floatx4 sc_nxt[4];
-      scores(std::false_type{}, (i + 1) % R, sc_nxt);
-      softmax_pv(std::false_type{}, std::false_type{}, i % R, (t_begin + i) * KT, sc_cur);
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt) sc_cur[kt] = sc_nxt[kt];
+      issue(t_begin + (nx < np ? nx : 0), (SL + R - 1) % R);
+      auto body = [&](floatx4 (&cur)[4], floatx4 (&nxt)[4]) {
+        stats(std::false_type{}, std::false_type{}, (t_begin + i) * KT, cur);
+        scores(std::false_type{}, std::integral_constant<int, (SL + 1) % R>{}, nxt);
+        pv(std::false_type{}, sl_c, cur);
+      };
+      if constexpr (SL % 2 == 0) body(sca, scb);
+      else body(scb, sca);
+      ++i;
+    };
+    static_assert(R == 4, "the unrolled loop below has R steps");
+    while (true) {
+      if (i + 1 >= np) break;
+      step(std::integral_constant<int, 0>{});
+      if (i + 1 >= np) break;
+      step(std::integral_constant<int, 1>{});
+      if (i + 1 >= np) break;
+      step(std::integral_constant<int, 2>{});
+      if (i + 1 >= np) break;
+      step(std::integral_constant<int, 3>{});
     }
     const int pl = t_begin + np - 1;
-    if (pl < n_full) softmax_pv(std::false_type{}, std::false_type{}, (np - 1) % R, pl * KT, sc_cur);
-    else softmax_pv(std::false_type{}, std::true_type{}, (np - 1) % R, pl * KT, sc_cur);
+    auto finish = [&](floatx4 (&last)[4]) {
+      if (pl < n_full) stats(std::false_type{}, std::false_type{}, pl * KT, last);
+      else stats(std::false_type{}, std::true_type{}, pl * KT, last);
+      pv(std::false_type{}, (np - 1) % R, last);
+    };
+    if ((np - 1) % 2 == 0) finish(sca);   // two copies: register arrays cannot be selected at run time
+    else finish(scb);
     // The trailing re-fetches must land before the ring memory is reused or the
     // workgroup ends.
     wait_vmcnt<0>();
