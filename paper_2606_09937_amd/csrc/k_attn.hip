@@ -196,20 +196,25 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   const int rin = XB ? rho - slot * s * G : rho;
   const int qi = rin / G, h = kvh * G + rin % G;
   const size_t qrow = (size_t)slot * s + qi;
+  // The lane's query, scaled to log2 units and split into hi/lo, is loaded
+  // after the chunk's first tiles are requested, so that the two memory round
+  // trips overlap.
   bf16x8 qh[NC], ql[NC];
+  auto load_q = [&]() {
 #pragma unroll
-  for (int cc = 0; cc < NC; ++cc) {
-    const float* qp = q + (qrow * H + h) * HD + 32 * cc + 8 * g;
-    const float4 a = *reinterpret_cast<const float4*>(qp), b = *reinterpret_cast<const float4*>(qp + 4);
-    const float x[8] = {a.x * sl2, a.y * sl2, a.z * sl2, a.w * sl2, b.x * sl2, b.y * sl2, b.z * sl2, b.w * sl2};
-    uint16_t hh[8], ll[8];
+    for (int cc = 0; cc < NC; ++cc) {
+      const float* qp = q + (qrow * H + h) * HD + 32 * cc + 8 * g;
+      const float4 a = *reinterpret_cast<const float4*>(qp), b = *reinterpret_cast<const float4*>(qp + 4);
+      const float x[8] = {a.x * sl2, a.y * sl2, a.z * sl2, a.w * sl2, b.x * sl2, b.y * sl2, b.z * sl2, b.w * sl2};
+      uint16_t hh[8], ll[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) split2(x[e], hh[e], ll[e]);
-    qh[cc] = __builtin_bit_cast(bf16x8, make_uint4(pack2(hh[0], hh[1]), pack2(hh[2], hh[3]), pack2(hh[4], hh[5]),
-                                                   pack2(hh[6], hh[7])));
-    ql[cc] = __builtin_bit_cast(bf16x8, make_uint4(pack2(ll[0], ll[1]), pack2(ll[2], ll[3]), pack2(ll[4], ll[5]),
-                                                   pack2(ll[6], ll[7])));
-  }
+      for (int e = 0; e < 8; ++e) split2(x[e], hh[e], ll[e]);
+      qh[cc] = __builtin_bit_cast(bf16x8, make_uint4(pack2(hh[0], hh[1]), pack2(hh[2], hh[3]), pack2(hh[4], hh[5]),
+                                                     pack2(hh[6], hh[7])));
+      ql[cc] = __builtin_bit_cast(bf16x8, make_uint4(pack2(ll[0], ll[1]), pack2(ll[2], ll[3]), pack2(ll[4], ll[5]),
+                                                     pack2(ll[6], ll[7])));
+    }
+  };
 
   floatx4 oacc[ND];
 #pragma unroll
@@ -305,8 +310,11 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     }
   };
 
-  // ---- own-span staging (fused mode)
+  // ---- own-span staging (fused mode): fetch_own loads a tile's fp32 keys and
+  // values into registers (in flight while the previous tile is contracted),
+  // store_own splits them into hi/lo and stores the padded LDS tiles.
   uint4 stg[OK];
+  uint4 vstg[OVU][4];
   auto fetch_own = [&](int kbase) {
     const float* kt = Ko + (size_t)kbase * HD;
     const int kmax = s - 1 - kbase;
@@ -314,6 +322,16 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     for (int j = 0; j < OK; ++j) {
       const int idx = tid + NT * j, key = idx / (HD / 4), dq = idx % (HD / 4);
       stg[j] = ldg16(kt + (key <= kmax ? key : kmax) * HD + dq * 4);
+    }
+#pragma unroll
+    for (int u = 0; u < OVU; ++u) {
+      const int idx = min(tid + NT * u, KT * HD / 16 - 1);   // units past the tile repeat its last (unused)
+      const int dq = idx % (HD / 4), kg = idx / (HD / 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int key = kbase + 4 * kg + e;
+        vstg[u][e] = ldg16(Vo + (size_t)(key < s ? key : 0) * HD + dq * 4);
+      }
     }
   };
   auto store_own = [&](int kbase) {
@@ -334,13 +352,12 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
         float x[4][4];   // x[e][k]: dimension 4dq + k of key 4kg + e
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int key = kbase + 4 * kg + e;
-          const bool ok = key < s;
-          const uint4 v = ldg16(Vo + (size_t)(ok ? key : 0) * HD + dq * 4);
-          x[e][0] = ok ? __uint_as_float(v.x) : 0.f;
-          x[e][1] = ok ? __uint_as_float(v.y) : 0.f;
-          x[e][2] = ok ? __uint_as_float(v.z) : 0.f;
-          x[e][3] = ok ? __uint_as_float(v.w) : 0.f;
+          const bool ok = kbase + 4 * kg + e < s;
+          const uint4 v = keep_if(ok, vstg[u][e]);
+          x[e][0] = __uint_as_float(v.x);
+          x[e][1] = __uint_as_float(v.y);
+          x[e][2] = __uint_as_float(v.z);
+          x[e][3] = __uint_as_float(v.w);
         }
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -521,6 +538,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     static_assert(R >= 3 && R % 2 == 0, "the pipelined loop needs a slot for tile i+1 and one being refilled");
 #pragma unroll
     for (int u = 0; u < R - 1; ++u) issue(t_begin + (u < np ? u : 0), u);
+    load_q();   // loads complete in order: the wait for the query covers these tiles too
     wait_vmcnt_lds<IPW * (R - 2)>();   // tile 0
     __builtin_amdgcn_s_barrier();
     floatx4 sca[4], scb[4];
@@ -572,6 +590,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   const int o_begin = max(t_begin, n_ptiles);
   if (!XB && o_begin < t_end) {
     fetch_own((o_begin - n_ptiles) * KT);
+    if (np <= 0) load_q();   // a chunk of own-span tiles only
     for (int t = o_begin; t < t_end; ++t) {
       const int kbase = (t - n_ptiles) * KT;
       store_own(kbase);
