@@ -28,6 +28,9 @@ namespace {
 constexpr int kAttnWaves = 8;    // waves per attention workgroup (16 query rows each)
 constexpr int kAttnRing = 4;     // prefix K/V tiles in the LDS ring
 constexpr float kLazyLog2 = 8.f; // slack of the softmax reference (log2 units): p <= 2^8
+#ifndef RKSC_ATTN_XCD_ORDER
+#define RKSC_ATTN_XCD_ORDER 1
+#endif
 
 // a if c, else zero; component-wise so that no address is selected (a select
 // of struct lvalues keeps register arrays in scratch memory).
@@ -156,11 +159,26 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   uint16_t* const Vt0 = Ks1 + KT * LDK;                        //            V^T hi [HD][LDV]
   uint16_t* const Vt1 = Vt0 + HD * LDV;                        //            V^T lo
 
-  // Work order: the hardware's (linear id round robin over the 8 XCDs). Mapping
-  // each KV head to one XCD fetched the head's prefix about once (at 16 branches
-  // x 256 tokens over 2048 prefix tokens, 126 instead of 573 MB per launch) but
-  // ran 7% slower, and rotating the tile order on top of it slower still.
-  const int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  // Work order. The hardware deals workgroups to the 8 XCDs round robin by
+  // linear id, and each XCD has its own L2. In fused mode every branch's query
+  // tiles of a KV head walk the same prefix tiles, so the linear ids are
+  // re-dealt KV-head-major: XCD x takes a contiguous range of (head, branch,
+  // query tile) work items, i.e. the workgroups of one head (Hkv = 8) or of a
+  // part of one (fewer heads), and the head's prefix is fetched from HBM about
+  // once per XCD instead of once per branch.
+  int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+#if RKSC_ATTN_XCD_ORDER
+  if constexpr (!XB) {
+    const int NX = gridDim.x, NY = gridDim.y, NZ = gridDim.z, T = NX * NY * NZ;
+    const int id = bx + NX * (by + NY * bz);
+    const int x = id % 8, qq = id / 8;
+    const int v = x * (T / 8) + min(x, T % 8) + qq;   // XCD x holds ids x, x+8, ...: T/8 (+1 for x < T%8)
+    by = v / (NX * NZ);
+    const int rr = v - by * NX * NZ;
+    bx = rr % NX;
+    bz = rr / NX;
+  }
+#endif
   // Fused mode: bz = chunk * slots + slot, rows of one branch.
   // XB mode: bz = chunk, rows of all live branches, prefix tiles only.
   const int B_slots = XB ? 1 : gridDim.z / nchunks;
