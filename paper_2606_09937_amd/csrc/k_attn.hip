@@ -32,6 +32,23 @@ constexpr float kLazyLog2 = 8.f; // slack of the softmax reference (log2 units):
 #define RKSC_ATTN_XCD_ORDER 1
 #endif
 
+// Maximum and sum over the four 16-lane rows of a wave (lanes l, l ^ 16, l ^ 32,
+// l ^ 48), with the gfx950 row-swap moves instead of LDS permutes: with both
+// operands x, v_permlane16_swap yields x's rows (0, 0, 2, 2) and (1, 1, 3, 3),
+// and v_permlane32_swap its halves (lo, lo) and (hi, hi) (checked on the device).
+__device__ __forceinline__ float rows_max(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // a if c, else zero; component-wise so that no address is selected (a select
 // of struct lvalues keeps register arrays in scratch memory).
 __device__ __forceinline__ uint4 keep_if(bool c, const uint4& a) {
@@ -455,8 +472,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     float mt = fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3]));
 #pragma unroll
     for (int kt = 1; kt < 4; ++kt) mt = fmaxf(mt, fmaxf(fmaxf(sc[kt][0], sc[kt][1]), fmaxf(sc[kt][2], sc[kt][3])));
-    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    mt = rows_max(mt);
     // mt is relative to the scores' reference: m, or 0 while m = -inf (then any
     // finite maximum moves it; a fully masked tile, mt = -inf, never does).
     const bool fresh = m == -INFINITY;
@@ -619,8 +635,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     }
   }
 
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
+  l = rows_sum(l);
   const size_t plane = (size_t)max_rows * H * HD;
   if (!XB && nchunks == 1) {
     if (!qvalid) return;
