@@ -275,16 +275,18 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
     rowoff[j] = (size_t)(pl < 2 ? min(m0 + row, max_rows - 1) : wrow(row)) * K;
   }
   const int ccol = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
+  // The wave index made uniform, so that the LDS destinations are scalar (M0) values.
+  const int widu = __builtin_amdgcn_readfirstlane(wid);
   auto issue = [&](int step) {
     // Steps past the end re-read the split's first step (valid memory, never used);
     // chunks at or past the split's end read its first chunk and are zeroed in compute.
     const int k = kb + (step < nsteps ? step : 0) * KEL;
-    const int col = k + ccol < ke ? k + ccol : kb;
     uint8_t* slot = smem + (step % R) * SLOT;
+    const int col = k + ccol < ke ? k + ccol : kb;
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
       const bf16* base = plane(j) == 0 ? Ahi : (plane(j) == 1 ? Alo : W);
-      dma16(base + rowoff[j] + col, slot + (j * kGemmWaves + wid) * 1024);
+      dma16(base + rowoff[j] + col, slot + (j * kGemmWaves + widu) * 1024);
     }
   };
 
@@ -293,8 +295,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const bf16x8 zero = {};
-  auto compute = [&](const uint8_t* slot, bool kin) {
+  auto compute = [&](const uint8_t* slot) {
     bf16x8 bw[TN];
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
@@ -305,10 +306,8 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
     for (int tm = 0; tm < TM; ++tm) {
       const int row = wm * 64 + 16 * tm + r16;
       const int off = row * RB + wswz(row, g) * 16;
-      bf16x8 ah = *reinterpret_cast<const bf16x8*>(slot + off);
-      bf16x8 al = *reinterpret_cast<const bf16x8*>(slot + SUB_A + off);
-      ah = kin ? ah : zero;
-      al = kin ? al : zero;
+      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(slot + off);
+      const bf16x8 al = *reinterpret_cast<const bf16x8*>(slot + SUB_A + off);
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn)
         acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw[tn], acc[tm][tn], 0, 0, 0);
@@ -326,8 +325,21 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
     wait_vmcnt_lds<IPW * (R - 2)>();
     __builtin_amdgcn_s_barrier();
     issue(st + R - 1);   // refills the slot step st-1 used
-    // The lane's 8-element K chunk lies wholly inside or outside the split (K % 8 == 0).
-    if (wave_live) compute(smem + (st % R) * SLOT, kb + st * KEL + 8 * g < ke);
+    uint8_t* const slot = smem + (st % R) * SLOT;
+    const int kst = kb + st * KEL;
+    if (kst + KEL > ke) {
+      // The split's last, partial stage: the activation chunks at or past its
+      // end (8-element chunks lie wholly inside or outside, K % 8 == 0) hold
+      // the split's first chunk and are zeroed in LDS, so that every stage is
+      // contracted without a mask. No DMA targets this slot any more.
+      for (int idx = threadIdx.x; idx < 2 * BM * 4; idx += kGemmWaves * 64) {
+        const int c = idx & 3, row = (idx >> 2) % BM, pl = idx / (BM * 4);
+        if (kst + 8 * c >= ke)
+          *reinterpret_cast<uint4*>(slot + pl * SUB_A + row * RB + wswz(row, c) * 16) = make_uint4(0, 0, 0, 0);
+      }
+      __syncthreads();
+    }
+    if (wave_live) compute(slot);
   }
   wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
   if constexpr (SWIGLU) {
