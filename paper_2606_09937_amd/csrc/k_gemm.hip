@@ -94,7 +94,10 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
   const bool wave_live = m0 + wm0 < Ml;   // waves whose 64 rows are all past the live rows skip the MFMAs
 
   // DMA sources: instruction ins covers rows 8*ins'.. of its sub-tile; lane L fills
-  // physical chunk L & 7 of row L >> 3, i.e. logical chunk gswz(row, L & 7).
+  // physical chunk L & 7 of row L >> 3, i.e. logical chunk gswz(row, L & 7). src[j]
+  // points at the lane's chunk of its row (K offset 0); the LDS destinations are
+  // scalar (the wave index made uniform).
+  const int widu = __builtin_amdgcn_readfirstlane(wid);
   const bf16* src[IPW];
   int dst[IPW], coff[IPW];
 #pragma unroll
@@ -110,16 +113,19 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
       src[j] = W + (size_t)min(n0 + row, N - 1) * K;
     }
     coff[j] = 8 * gswz(row, lane & 7);
-    dst[j] = off;
+    src[j] += coff[j];
+    dst[j] = (widu * IPW + j) * 1024;
   }
   auto issue = [&](int step) {
     // Steps past the end re-read the split's first step (valid memory, never used).
     const int k = step < nsteps ? kb + step * KEL : kb;
     uint8_t* slot = smem + (step % R) * SLOT;
+    if (k + KEL <= ke) {   // a whole stage (the common case)
 #pragma unroll
-    for (int j = 0; j < IPW; ++j) {
-      const int col = k + coff[j];
-      dma16(src[j] + (col < ke ? col : kb), slot + dst[j]);
+      for (int j = 0; j < IPW; ++j) dma16(src[j] + k, slot + dst[j]);
+    } else {   // chunks at or past the split's end read the split's first chunk
+#pragma unroll
+      for (int j = 0; j < IPW; ++j) dma16(k + coff[j] < ke ? src[j] + k : src[j] - coff[j] + kb, slot + dst[j]);
     }
   };
 
