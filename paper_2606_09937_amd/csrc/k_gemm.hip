@@ -496,20 +496,42 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_skinny(const bf16* __r
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
 
-  int iu = 0;   // next unit to issue; past the end unit 0 is fetched again (never consumed)
+  // Issue cursor: unit iu = (tile t0 + it, slice isl); past the end unit 0 is
+  // fetched again (never consumed). A unit inside the matrix is addressed as a
+  // scalar base (its tile's first row, its slice) plus this lane's fixed offset
+  // wlane[j] (row r of the tile, chunk lane ^ r); only a tile past row N - 1 or a
+  // slice past K takes the clamped path.
+  const int widu = __builtin_amdgcn_readfirstlane(wid);
+  size_t wlane[IPW];
+#pragma unroll
+  for (int j = 0; j < IPW; ++j) {
+    const int r = IPW * wid + j;
+    wlane[j] = (size_t)r * K + 8 * (lane ^ r);
+  }
+  int iu = 0, it = 0, isl = 0;
   auto issue = [&](int slot_idx) {
     uint8_t* slot = smem + slot_idx * kSkUnit;
-    const int u = iu < nunits ? iu : 0;
-    const int tq = u / ns;
-    const int t = t0 + tq, sl = u - tq * ns;
+    const bool past = iu >= nunits;
+    const int t = t0 + (past ? 0 : it), sl = past ? 0 : isl;
+    const int kbase = k0 + 512 * sl;
+    if (16 * t + 15 < N && kbase + 512 <= K) {
+      const bf16* base = W + (size_t)(16 * t) * K + kbase;
 #pragma unroll
-    for (int j = 0; j < IPW; ++j) {
-      const int r = IPW * wid + j;
-      const int k = k0 + 512 * sl + 8 * (lane ^ r);
-      const int row = min(16 * t + r, N - 1);
-      dma16(W + (size_t)row * K + (k < K ? k : 0), slot + r * 1024);
+      for (int j = 0; j < IPW; ++j) dma16(base + wlane[j], slot + (IPW * widu + j) * 1024);
+    } else {
+#pragma unroll
+      for (int j = 0; j < IPW; ++j) {
+        const int r = IPW * wid + j;
+        const int k = kbase + 8 * (lane ^ r);
+        const int row = min(16 * t + r, N - 1);
+        dma16(W + (size_t)row * K + (k < K ? k : 0), slot + (IPW * widu + j) * 1024);
+      }
     }
     ++iu;
+    if (++isl == ns) {
+      isl = 0;
+      ++it;
+    }
   };
 #pragma unroll
   for (int i = 0; i < R - 1; ++i) issue(i);
@@ -547,13 +569,13 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_skinny(const bf16* __r
         asm volatile("" ::"v"(hv), "v"(lv));
       }
 
-  int qc = 0;   // ring units consumed
+  int qs = 0;   // ring slot of the next unit consumed (units consumed mod R)
   auto step = [&]() -> const uint8_t* {
     wait_vmcnt_lds<IPW * (R - 2)>();
     __builtin_amdgcn_s_barrier();
-    issue((qc + R - 1) % R);   // refills the slot unit qc-1 used
-    const uint8_t* slot = smem + (qc % R) * kSkUnit;
-    ++qc;
+    issue(qs == 0 ? R - 1 : qs - 1);   // refills the slot the previous unit used
+    const uint8_t* slot = smem + qs * kSkUnit;
+    qs = qs == R - 1 ? 0 : qs + 1;
     return slot;
   };
 
