@@ -92,8 +92,11 @@ rksc_status rksc_test_attention(int32_t dtype, const void* q, const void* prefix
  * RKSC_PROFILE_EVENTS_PER_LAYER * n_layers hipEvent_t handles created by the
  * caller; NULL entries are skipped. Per layer l the entries at
  * l * RKSC_PROFILE_EVENTS_PER_LAYER + k are, for k =
- *   0/1 QKV projection, 2/3 attention, 4/5 O projection, 6/7 gate|up
- *   projection, 8/9 down projection, 10/11 fused lm_head-entropy.
+ *   0/1 QKV projection, 2/3 attention (with its split-KV combine where the
+ *   plan splits the prefix), 4/5 O projection, 6/7 gate|up projection (7 is
+ *   recorded right after the projection kernel, before the separate SwiGLU /
+ *   split-K combine kernel of the 128-row plans), 8/9 down projection,
+ *   10/11 fused lm_head-entropy.
  * The lm_head-entropy events are recorded only at the last layer of each exit
  * window (rksc_verify_window), where the stream runs. Events of layers a
  * branch set never reaches are recorded too (their kernels exit at once). */

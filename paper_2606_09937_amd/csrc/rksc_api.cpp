@@ -324,10 +324,12 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
   HIP_TRY(rksc::launch_rope_table(rope, s, n, hd, (double)c->rope_base, strm));
   HIP_TRY(rksc::launch_embed(dt, w->embed, branch_tokens, V, x0, M, d, strm));
 
+  auto event_at = [&](int l, int slot) -> hipEvent_t {
+    return events ? static_cast<hipEvent_t>(events[(size_t)l * RKSC_PROFILE_EVENTS_PER_LAYER + slot]) : nullptr;
+  };
   auto mark = [&](int l, int slot) -> hipError_t {
-    if (!events) return hipSuccess;
-    void* e = events[(size_t)l * RKSC_PROFILE_EVENTS_PER_LAYER + slot];
-    return e ? hipEventRecord(static_cast<hipEvent_t>(e), strm) : hipSuccess;
+    hipEvent_t e = event_at(l, slot);
+    return e ? hipEventRecord(e, strm) : hipSuccess;
   };
   for (int l = 0; l < L; ++l) {
     const rksc_layer_weights& lw = w->layers[l];
@@ -374,9 +376,18 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
                                   lw.ffn_norm, d, c->rms_eps, M, strm));
     if (drop & RKSC_DROP_GATE_UP_LO) HIP_TRY(drop_lo(act, (size_t)M * d));
     HIP_TRY(mark(l, 6));
-    HIP_TRY(rksc::launch_gate_up_swiglu(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig,
-                                        (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm));
-    HIP_TRY(mark(l, 7));
+    if (event_at(l, 7) && !rksc::gate_up_fused(dt, lay.gu, 2 * F)) {
+      // Profiled call: the class's closing event goes between the projection kernel and
+      // its separate SwiGLU / split-K combine, so the pair brackets the projection alone.
+      HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig,
+                                (size_t)M * 2 * F, ctrl, s, M, 2 * F, d, strm));
+      HIP_TRY(mark(l, 7));
+      HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
+    } else {
+      HIP_TRY(rksc::launch_gate_up_swiglu(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig,
+                                          (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm));
+      HIP_TRY(mark(l, 7));
+    }
     if (drop & RKSC_DROP_DOWN_LO) HIP_TRY(drop_lo(ffn, (size_t)M * F));
     HIP_TRY(mark(l, 8));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
