@@ -681,6 +681,33 @@ __global__ __launch_bounds__(256) void k_attn_combine(const float* __restrict__ 
   for (int j = 0; j < HD / 64; ++j) acc[j] = 0.f;
   float den = 0.f;
   float Mx = -INFINITY;
+  if (nchunks <= 8) {
+    // Up to 8 chunks: every load (the partials and each chunk's (m, l)) is issued
+    // before the first wait, so the merge costs one memory round trip.
+    float v[8][HD / 64];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int j = 0; j < HD / 64; ++j)
+        v[u][j] = u < nchunks ? opart[((size_t)u * cstride + wid) * HD + lane + 64 * j] : 0.f;
+    float2 ml = make_float2(-INFINITY, 0.f);
+    if (lane < nchunks) ml = *reinterpret_cast<const float2*>(mlpart + (lane * cstride + wid) * 2);
+    float M = ml.x;
+#pragma unroll
+    for (int off = 4; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+    const float w = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M);
+    float wl = w * ml.y;
+#pragma unroll
+    for (int off = 4; off >= 1; off >>= 1) wl += __shfl_xor(wl, off, 64);
+    den = __shfl(wl, 0, 64);   // lanes 0..7 hold the chunks' sum
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float wk = __shfl(w, u, 64);
+#pragma unroll
+      for (int j = 0; j < HD / 64; ++j) acc[j] += wk * v[u][j];
+    }
+    nchunks = 0;   // skips the general loops below
+  }
   for (int c0 = 0; c0 < nchunks; c0 += 64) {
     const int ch = c0 + lane;
     const float mc = ch < nchunks ? mlpart[(ch * cstride + wid) * 2] : -INFINITY;

@@ -151,6 +151,40 @@ def test_7b_single_full():
     _parity(mw, kv, toks, wl.tau, wl.patience, "7b_single")
 
 
+def test_7b_single_exit_inside_window():
+    """The headline shape with its exit firing (Alg. VerifyWithEntropyExit): 32 layers, one branch
+    x 128 tokens over the 1024-token prefix, exit windows of 8 layers (the cost model's choice at
+    this shape). tau is read off the oracle's deltas so that the branch exits at a layer inside a
+    window, with every delta at least 1.1e-2 nats from tau; the exit layer, the entropies and the
+    hidden rows up to it match the oracle and the window's layers after it are NaN."""
+    wl = workloads.get("7b_single")
+    mw, kv, toks = _inputs(wl.model, 1, wl.prefix_len, wl.branch_len, seed=42)
+    L, patience = wl.model.n_layers, wl.patience
+    win = rk.rksc_verify_window(wl.model, 1, wl.branch_len, wl.prefix_len)
+    assert win == 8
+    ent_ref, hid_ref, _ = _run_oracle(mw, kv, toks, 0.0, 1)
+    deltas = np.sort(np.abs(np.diff(ent_ref[:, 0])))
+    tau = None
+    for margin in (2.5e-2, 1.5e-2, 1.1e-2):
+        for a, b in zip(deltas[:-1], deltas[1:]):
+            t = (a + b) / 2
+            e = oracle.exit_layer(ent_ref[:, 0], t, patience)
+            if b - a > 2 * margin and e < L and e % win:
+                tau = t
+                break
+        if tau is not None:
+            break
+    assert tau is not None, f"no separable tau in the oracle deltas {deltas}"
+    ex_ref = np.array([oracle.exit_layer(ent_ref[:, 0], tau, patience)])
+    log(f"[7b_single exit] tau={tau:.4f} oracle exit {ex_ref.tolist()}")
+    ent, ex, hid = rk.verify_forward(mw, kv.k, kv.v, toks, tau, patience, return_hidden=True)
+    torch.cuda.synchronize()
+    ent, ex, hid = to_np(ent), to_np(ex), to_np(hid)
+    stats = compare_verify(ent, ex, hid, ent_ref, hid_ref, ex_ref, tau, label=f"7b_single tau={tau:.4f}")
+    log(f"[7b_single exit] gpu exit {ex.tolist()} {stats}")
+    assert stats["near_threshold"] == 0 and stats["exit_match"] == 1 and ex[0] < L
+
+
 @pytest.mark.parametrize("name,layers", [("7b_tot", 2), ("7b_large_vocab", 2), ("10b_long", 2), ("10b_decode", 2),
                                          ("7b_paper_verify", 2)])
 def test_large_shapes_sampled_branches(name, layers):
