@@ -209,6 +209,10 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   if (row0 >= rows) return;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
+  // A wave whose 16 query rows all lie past the last row (a packed decode tile
+  // of few branches) still issues its share of every tile's DMA and meets every
+  // barrier, but forms no scores and contracts nothing.
+  const bool wave_live = row0 + 16 * __builtin_amdgcn_readfirstlane(wid) < rows;
 
   const int i_max = min(s - 1, (min(row0 + QT - 1, rows - 1)) / G);
   const int n_ptiles = (n + KT - 1) / KT;
@@ -572,11 +576,11 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     static_assert(R >= 3 && R % 2 == 0, "the pipelined loop needs a slot for tile i+1 and one being refilled");
 #pragma unroll
     for (int u = 0; u < R - 1; ++u) issue(t_begin + (u < np ? u : 0), u);
-    load_q();   // loads complete in order: the wait for the query covers these tiles too
+    if (wave_live) load_q();   // loads complete in order: the wait for the query covers these tiles too
     wait_vmcnt_lds<IPW * (R - 2)>();   // tile 0
     __builtin_amdgcn_s_barrier();
     floatx4 sca[4], scb[4];
-    scores(std::false_type{}, std::integral_constant<int, 0>{}, sca);
+    if (wave_live) scores(std::false_type{}, std::integral_constant<int, 0>{}, sca);
     // Tiles before the chunk's last are never partial (only the prefix's last
     // tile can be, and it is the last of its chunk).
     int i = 0;
@@ -587,6 +591,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
       const int nx = i + R - 1;
       issue(t_begin + (nx < np ? nx : 0), (SL + R - 1) % R);
       auto body = [&](floatx4 (&cur)[4], floatx4 (&nxt)[4]) {
+        if (!wave_live) return;
         stats(std::false_type{}, std::false_type{}, (t_begin + i) * KT, cur);
         scores(std::false_type{}, std::integral_constant<int, (SL + 1) % R>{}, nxt);
         pv(std::false_type{}, sl_c, cur);
@@ -608,6 +613,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
     }
     const int pl = t_begin + np - 1;
     auto finish = [&](floatx4 (&last)[4]) {
+      if (!wave_live) return;
       if (pl < n_full) stats(std::false_type{}, std::false_type{}, pl * KT, last);
       else stats(std::false_type{}, std::true_type{}, pl * KT, last);
       pv(std::false_type{}, (np - 1) % R, last);
@@ -624,13 +630,13 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const float* __restrict__ q, 
   const int o_begin = max(t_begin, n_ptiles);
   if (!XB && o_begin < t_end) {
     fetch_own((o_begin - n_ptiles) * KT);
-    if (np <= 0) load_q();   // a chunk of own-span tiles only
+    if (np <= 0 && wave_live) load_q();   // a chunk of own-span tiles only
     for (int t = o_begin; t < t_end; ++t) {
       const int kbase = (t - n_ptiles) * KT;
       store_own(kbase);
       __syncthreads();
       if (t + 1 < t_end) fetch_own(kbase + KT);   // in flight while this tile is contracted
-      contract(std::true_type{}, std::true_type{}, 0, kbase);
+      if (wave_live) contract(std::true_type{}, std::true_type{}, 0, kbase);
       __syncthreads();
     }
   }
