@@ -902,6 +902,20 @@ __global__ __launch_bounds__(256) void k_attn_combine_dec(const float* __restric
   const uint16_t* vb = reinterpret_cast<const uint16_t*>(cv) + ((size_t)b * Hkv + kvh) * cap * HD;
   const float* kc = ko + ((size_t)b * Hkv + kvh) * HD;   // the new token's own key (s = 1)
   const float* vc = vo + ((size_t)b * Hkv + kvh) * HD;
+  const size_t cstride = (size_t)max_rows * H;
+
+  // Up to 8 prefix chunks: their (m, l) and partials do not depend on the rest,
+  // so they are requested first and are in registers by the time they are merged.
+  const bool few = nchunks <= 8;
+  float2 ml8 = make_float2(-INFINITY, 0.f);
+  float op8[8][E];
+  if (few) {
+    if (lane < nchunks) ml8 = *reinterpret_cast<const float2*>(mlpart + (lane * cstride + wid) * 2);
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+#pragma unroll
+      for (int e = 0; e < E; ++e) op8[k][e] = k < nchunks ? opart[((size_t)k * cstride + wid) * HD + lane + 64 * e] : 0.f;
+  }
 
   // The own key's score, reduced over the wave.
   float t_own = 0.f;
@@ -980,8 +994,28 @@ __global__ __launch_bounds__(256) void k_attn_combine_dec(const float* __restric
     Mr = Mn;
   }
   // The prefix chunks' partials (zeros where a chunk saw no key).
-  const size_t cstride = (size_t)max_rows * H;
   float Mx = Mr;
+  if (few) {
+    float M = ml8.x;
+#pragma unroll
+    for (int off = 4; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+    Mx = fmaxf(Mx, __shfl(M, 0, 64));
+    const float own_w = __builtin_amdgcn_exp2f(Mr - Mx);
+    const float w = ml8.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml8.x - Mx);
+    float wl = w * ml8.y;
+#pragma unroll
+    for (int off = 4; off >= 1; off >>= 1) wl += __shfl_xor(wl, off, 64);
+    den = den * own_w + __shfl(wl, 0, 64);
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] *= own_w;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float wk = __shfl(w, k, 64);
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] = fmaf(wk, op8[k][e], acc[e]);
+    }
+    nchunks = 0;   // skips the general merge below
+  }
   for (int c0 = 0; c0 < nchunks; c0 += 64) {
     const int ch = c0 + lane;
     float M = ch < nchunks ? mlpart[(ch * cstride + wid) * 2] : -INFINITY;
@@ -989,10 +1023,12 @@ __global__ __launch_bounds__(256) void k_attn_combine_dec(const float* __restric
     for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
     Mx = fmaxf(Mx, M);
   }
-  const float own_w = __builtin_amdgcn_exp2f(Mr - Mx);
-  den *= own_w;
+  if (!few) {
+    const float own_w = __builtin_amdgcn_exp2f(Mr - Mx);
+    den *= own_w;
 #pragma unroll
-  for (int e = 0; e < E; ++e) acc[e] *= own_w;
+    for (int e = 0; e < E; ++e) acc[e] *= own_w;
+  }
   for (int c0 = 0; c0 < nchunks; c0 += 64) {
     const int ch = c0 + lane;
     float w = 0.f, wl = 0.f;
