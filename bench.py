@@ -13,8 +13,9 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   roofline     the dominant kernel class (most time per call; the gate|up
                projection at the default workload) against its roof, timed
                with HIP events recorded around its launches inside the timed
-               steps (the only events in that region: every recorded event
-               opens a gap in the stream)
+               steps, at every 4th layer for a per-layer class (the only
+               events in that region: every recorded event opens a gap in
+               the stream)
   kernels      every kernel class timed the same way in a separate breakdown
                pass before the timed region ("pass" says which)
   exit_histogram, live_layer_fraction   exit layers of the timed calls
