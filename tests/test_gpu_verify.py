@@ -339,3 +339,65 @@ def test_prefix_chain_equals_one_cache(shape, B, n, s, cuts):
         outs.append([to_np(t) for t in got])
     for a, b in zip(*outs):
         np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("case", ["gqa_128rows", "gqa_1024rows", "7b_tot_2layers"])
+def test_profiled_call_matches_plain_call(case):
+    """The measurement variant of the verify call (a HIP event recorded on the stream before and
+    after every kernel class at every layer; the gate|up pair closes between the projection and
+    a separate SwiGLU combine where the plan has one) leaves the outputs bit-identical to
+    rksc_verify_forward's: 128- and 1024-row plans with the separate combine, and 4096 rows of
+    the 7B tree shape with the SwiGLU in the projection's epilogue. Every branch exits at layer
+    2, so later layers run on no live rows; every recorded pair has a duration."""
+    import ctypes
+    if case == "7b_tot_2layers":
+        wl = workloads.get("7b_tot")
+        B, s, n = wl.n_branches, wl.branch_len, wl.prefix_len
+        mw, kv, toks = _inputs(wl.model, B, n, s, seed=17, n_layers=2)
+    else:
+        B, s, n = (1 if case == "gqa_128rows" else 8), 128, 200
+        mw, kv, toks = _inputs(GQA_BF16, B, n, s, seed=17)
+    shape = mw.shape
+    L, d = len(mw.layers), shape.d_model
+    tau, patience = 10.0, 1   # every branch exits at layer 2
+    ent0, ex0, hid0 = _run_gpu(mw, kv, toks, tau, patience)
+
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    per = 12
+    evs = []
+    for _ in range(per * L):
+        e = ctypes.c_void_p()
+        assert hip.hipEventCreateWithFlags(ctypes.byref(e), 0x20000000) == 0   # no system fence on record
+        evs.append(e.value)
+    arr = (ctypes.c_void_p * (per * L))(*evs)
+    lib = rk.load_library()
+    lib.rksc_verify_forward_profiled.restype = ctypes.c_int32
+    lib.rksc_verify_forward_profiled.argtypes = list(lib.rksc_verify_forward.argtypes) + [ctypes.c_void_p]
+    ws = torch.empty(rk.rksc_verify_workspace_size(shape, B, s, n), dtype=torch.uint8, device=DEV)
+    ent = torch.empty((L, B), dtype=torch.float32, device=DEV)
+    ex = torch.empty((B,), dtype=torch.int32, device=DEV)
+    hid = torch.empty((L, B, d), dtype=torch.float32, device=DEV)
+    w_struct, keep = rk._weights_struct(mw)
+    kv_struct = rk.PrefixKV(n, rk._ptr(kv.k), rk._ptr(kv.v))
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    st = lib.rksc_verify_forward_profiled(ctypes.byref(w_struct), ctypes.byref(kv_struct), rk._ptr(toks), B, s,
+                                          tau, patience, rk._ptr(ent), rk._ptr(ex), rk._ptr(hid), rk._ptr(ws),
+                                          ws.numel(), stream, ctypes.cast(arr, ctypes.c_void_p))
+    assert st == 0, rk.rksc_last_error()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_np(ex), ex0)
+    np.testing.assert_array_equal(to_np(ent), ent0)
+    np.testing.assert_array_equal(to_np(hid), hid0)
+    assert (ex0 == 2).all(), f"every branch should exit at layer 2 (got {ex0})"
+    for l in range(L):
+        for a in (0, 2, 4, 6, 8):   # QKV, attention, O, gate|up, down pairs are recorded at every layer
+            ms = ctypes.c_float()
+            assert hip.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(evs[per * l + a]),
+                                           ctypes.c_void_p(evs[per * l + a + 1])) == 0
+            assert ms.value >= 0.0
+    for e in evs:
+        hip.hipEventDestroy(ctypes.c_void_p(e))
+    del keep
