@@ -6,7 +6,10 @@ the multi-branch forward over the shared prefix cache, the fused
 lm_head-entropy probe of every layer (one stream per exit window of layers)
 and the exit rule (branches that exit stop being computed). Inputs (random-init bf16 weights, synthetic prefix K/V,
 uniform tokens) are generated on the GPU and are resident in HBM before the
-timed region; the workspace and outputs are allocated once.
+timed region, with the pre-tiled gate|up copy of every layer (rksc_tile_gate_up,
+built once with the weights: a storage layout the library reads where the
+gate|up projection runs on 128-row tiles); the workspace and outputs are
+allocated once.
 
 Prints ONE JSON line on stdout (progress goes to stderr):
   value        verify tokens/s = n_branches * branch_len / step time
@@ -342,7 +345,7 @@ def cpu_baseline(mw, kv, toks, wl, layers, branches=None):
 
     host = Host()
     host.embed = mw.embed.cpu()
-    host.layers = [{k: v.cpu() for k, v in mw.layers[i].items()} for i in range(layers)]
+    host.layers = [{k: v.cpu() for k, v in mw.layers[i].items() if k != "w_gate_up_tiled"} for i in range(layers)]
     host.final_norm = mw.final_norm.cpu()
     host.lm_head = mw.lm_head.cpu()
     pk, pv = kv.k[:layers].cpu(), kv.v[:layers].cpu()
@@ -649,6 +652,7 @@ def measure_workload(name, args, hip, dev):
     B, n, s, L = wl.n_branches, wl.prefix_len, wl.branch_len, shape.n_layers
     t0 = time.perf_counter()
     mw = workloads.make_model(shape, seed=args.seed, device=dev)
+    rk.tile_gate_up(mw)
     kv = workloads.make_prefix_kv(shape, n, seed=args.seed, device=dev)
     toks = workloads.make_tokens(B * s, shape.vocab, seed=args.seed, device=dev).reshape(B, s).contiguous()
     ws = torch.empty(rk.rksc_verify_workspace_size(shape, B, s, n), dtype=torch.uint8, device=dev)
@@ -818,6 +822,7 @@ def main():
     log(f"workload {wl.name}: {wl.description}; generating inputs on {torch.cuda.get_device_name(0)}")
     t0 = time.perf_counter()
     mw = workloads.make_model(shape, seed=args.seed, device=dev)
+    tiled = rk.tile_gate_up(mw)
     kv = workloads.make_prefix_kv(shape, n, seed=args.seed, device=dev)
     toks = workloads.make_tokens(B * s, shape.vocab, seed=args.seed, device=dev).reshape(B, s).contiguous()
     ws = torch.empty(rk.rksc_verify_workspace_size(shape, B, s, n), dtype=torch.uint8, device=dev)
@@ -1079,7 +1084,7 @@ def main():
             "layers": L, "d_model": shape.d_model, "heads": shape.n_heads, "kv_heads": shape.n_kv_heads,
             "head_dim": shape.head_dim, "d_ff": shape.d_ff, "vocab": shape.vocab,
             "n_branches": B, "prefix_len": n, "branch_len": s, "tau": wl.tau, "patience": wl.patience,
-            "exit_layers": exits, "parallelism": "single GPU",
+            "exit_layers": exits, "parallelism": "single GPU", "gate_up_tiled": tiled,
         },
         "roofline": roofline,
         "exit_histogram": exit_hist,

@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define RKSC_ABI_VERSION 7
+#define RKSC_ABI_VERSION 8
 
 /* Largest number of branches one verify call accepts. */
 #define RKSC_MAX_BRANCHES 64
@@ -80,6 +80,11 @@ typedef struct {
   const float* ffn_norm;    /* [d] RMSNorm gain before the FFN */
   const void* w_gate_up;    /* [2*F, d]: the gate rows, then the up rows */
   const void* w_down;       /* [d, F] */
+  const void* w_gate_up_tiled;   /* optional (NULL: none): w_gate_up as laid out by
+                                    rksc_tile_gate_up, read instead of it where the
+                                    gate|up projection runs on the 128-row tiles (the
+                                    smaller row counts); outputs are bitwise the same
+                                    with or without it */
 } rksc_layer_weights;
 
 typedef struct {
@@ -122,6 +127,25 @@ typedef struct {
 } rksc_branch_kv;
 
 int32_t rksc_abi_version(void);
+
+/*
+ * Pre-tiled copy of one layer's gate|up weight (a storage layout only; the
+ * FFN's gate/up projection in the verify pass of Sec. 2.3 computes the same
+ * products from it).
+ *
+ * out[((t * (d / 64) + kb) * 256 + r) * 64 + e] = w_gate_up[(256 t + r) * d + 64 kb + e]
+ * for t < 2F / 256, kb < d / 64, r < 256, e < 64: every 256-row x 64-column
+ * block of the weight becomes one contiguous run, which is how the 128-row
+ * projection kernel streams it (a block per pipeline stage). Set the result as
+ * the layer's w_gate_up_tiled. bf16 models with d % 64 == 0 and
+ * (2 d_ff) % 256 == 0 only (RKSC_ERR_UNSUPPORTED otherwise, and for fp32).
+ * w_gate_up and out: device, 2 F d elements of the model dtype each (out_bytes
+ * at least rksc_gate_up_tiled_bytes(cfg)), not overlapping. Asynchronous on
+ * `stream`; the copy must be complete before a call that reads it, on the same
+ * stream or after a synchronisation. */
+size_t rksc_gate_up_tiled_bytes(const rksc_model_config* cfg);
+rksc_status rksc_tile_gate_up(const rksc_model_config* cfg, const void* w_gate_up, void* out, size_t out_bytes,
+                              void* stream);
 
 /* Bytes of workspace rksc_verify_forward needs for this shape (n_branches
  * branches of branch_len tokens over a prefix of n_prefix entries in all); 0 if the

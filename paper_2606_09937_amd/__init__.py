@@ -28,6 +28,7 @@ __all__ = [
     "BranchCache", "Decoder", "rksc_decode_workspace_size", "rksc_decode_suffix", "rksc_decode_step",
     "rksc_cgee_gate", "cgee_gate", "RKSC_ABI_VERSION", "BlockTable", "KVProbe",
     "rksc_prefix_extend", "rksc_prefix_extend_workspace_size", "prefix_extend", "rksc_asks_gate", "asks_gate",
+    "rksc_gate_up_tiled_bytes", "rksc_tile_gate_up", "tile_gate_up",
     "RKSC_OK", "RKSC_ERR_INVALID_ARGUMENT", "RKSC_ERR_UNSUPPORTED",
     "RKSC_ERR_WORKSPACE_TOO_SMALL", "RKSC_ERR_HIP", "RKSC_F32", "RKSC_BF16", "RKSC_MAX_BRANCHES",
     "RKSC_MAX_PREFIX_SEGMENTS", "PrefixCache", "PrefixKV",
@@ -42,7 +43,7 @@ RKSC_F32 = 0
 RKSC_BF16 = 1
 RKSC_MAX_BRANCHES = 64
 RKSC_MAX_PREFIX_SEGMENTS = 8
-RKSC_ABI_VERSION = 7
+RKSC_ABI_VERSION = 8
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 
@@ -70,6 +71,7 @@ class LayerWeights(ctypes.Structure):
     _fields_ = [
         ("attn_norm", ctypes.c_void_p), ("w_qkv", ctypes.c_void_p), ("w_o", ctypes.c_void_p),
         ("ffn_norm", ctypes.c_void_p), ("w_gate_up", ctypes.c_void_p), ("w_down", ctypes.c_void_p),
+        ("w_gate_up_tiled", ctypes.c_void_p),
     ]
 
 
@@ -128,6 +130,10 @@ def load_library():
     vp, i32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
     lib.rksc_abi_version.restype = i32
     lib.rksc_abi_version.argtypes = []
+    lib.rksc_gate_up_tiled_bytes.restype = sz
+    lib.rksc_gate_up_tiled_bytes.argtypes = [ctypes.POINTER(ModelConfig)]
+    lib.rksc_tile_gate_up.restype = i32
+    lib.rksc_tile_gate_up.argtypes = [ctypes.POINTER(ModelConfig), vp, vp, sz, vp]
     lib.rksc_verify_workspace_size.restype = sz
     lib.rksc_verify_workspace_size.argtypes = [ctypes.POINTER(ModelConfig), i32, i32, i32]
     lib.rksc_verify_forward.restype = i32
@@ -281,6 +287,8 @@ def _check_weights(need, weights, need_lm_head: bool = True):
         need(lw["w_o"], f"layer {i} w_o", dt, (d, H * hd))
         need(lw["w_gate_up"], f"layer {i} w_gate_up", dt, (2 * F, d))
         need(lw["w_down"], f"layer {i} w_down", dt, (d, F))
+        if lw.get("w_gate_up_tiled") is not None:
+            need(lw["w_gate_up_tiled"], f"layer {i} w_gate_up_tiled", dt, (2 * F, d))
 
 
 def _check_prefix(need, weights, prefix_k, prefix_v, name="prefix"):
@@ -370,7 +378,7 @@ def _weights_struct(weights):
     layers = (LayerWeights * len(weights.layers))()
     for i, lw in enumerate(weights.layers):
         layers[i] = LayerWeights(_ptr(lw["attn_norm"]), _ptr(lw["w_qkv"]), _ptr(lw["w_o"]), _ptr(lw["ffn_norm"]),
-                                 _ptr(lw["w_gate_up"]), _ptr(lw["w_down"]))
+                                 _ptr(lw["w_gate_up"]), _ptr(lw["w_down"]), _ptr(lw.get("w_gate_up_tiled")))
     cfg = model_config(shape)
     cfg.n_layers = len(weights.layers)
     w = Weights(cfg, _ptr(weights.embed), layers, _ptr(weights.final_norm), _ptr(weights.lm_head))
@@ -675,6 +683,36 @@ def prefill(weights, tokens: torch.Tensor, workspace: Optional[torch.Tensor] = N
     h_root = torch.empty((L, shape.d_model), dtype=torch.float32, device=dev)
     rksc_prefill(weights, tokens.contiguous(), k, v, h_root, workspace, stream)
     return k, v, h_root
+
+
+def rksc_gate_up_tiled_bytes(shape) -> int:
+    """Bytes of one layer's tiled gate|up copy; 0 if the model has no tiled layout."""
+    return int(load_library().rksc_gate_up_tiled_bytes(ctypes.byref(model_config(shape))))
+
+
+def rksc_tile_gate_up(shape, w_gate_up: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+    """Marshal one layer's gate|up weight [2F, d] and an output tensor of the same shape and dtype
+    (device) into rksc_tile_gate_up."""
+    need = _Args()
+    dt = _model_dtype(shape)
+    need(w_gate_up, "w_gate_up", dt, (2 * shape.d_ff, shape.d_model))
+    need(out, "out", dt, (2 * shape.d_ff, shape.d_model))
+    need.done()
+    _check(load_library().rksc_tile_gate_up(ctypes.byref(model_config(shape)), _ptr(w_gate_up), _ptr(out),
+                                            int(out.numel() * out.element_size()), _stream(stream)))
+
+
+def tile_gate_up(weights, stream=None) -> bool:
+    """Give every layer of `weights` its tiled gate|up copy (layer dict key "w_gate_up_tiled"), which
+    the library then streams instead of w_gate_up where the 128-row projection tiles run; the outputs
+    do not change. Returns False (and changes nothing) for a model without a tiled layout."""
+    if rksc_gate_up_tiled_bytes(weights.shape) == 0:
+        return False
+    for lw in weights.layers:
+        out = torch.empty_like(lw["w_gate_up"])
+        rksc_tile_gate_up(weights.shape, lw["w_gate_up"], out, stream)
+        lw["w_gate_up_tiled"] = out
+    return True
 
 
 def asks_similarity(hidden: torch.Tensor, alpha: float, stream=None) -> torch.Tensor:

@@ -39,6 +39,12 @@ namespace {
 // K needs only to be a multiple of 8: a chunk at or past the end of the split
 // reads the split's first chunk instead (valid memory), and activation
 // fragments past the end are zeroed when the last, partial stage is consumed.
+//
+// TILED: the weight is read from its pre-tiled copy [N/BN][K/64][BN][64]
+// (launch_tile_rows), in which a stage's BN x 64 weight block is one
+// contiguous run of BN * 128 bytes instead of BN runs of 128 bytes at a K * 2
+// byte stride; the tile and the LDS layout are the same. The launcher takes
+// this form only when N % BN == 0 and the split's K range is whole stages.
 
 __device__ __forceinline__ int gswz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
@@ -65,7 +71,7 @@ __device__ __forceinline__ void xcd_raster(int& tx, int& ty, int& tz) {
   tx = rr / gm;
 }
 
-template <int BN, int R>
+template <int BN, int R, bool TILED = false>
 __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __restrict__ Ahi,
                                                               const bf16* __restrict__ Alo,
                                                               const bf16* __restrict__ W, float* __restrict__ P,
@@ -98,19 +104,27 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
   // points at the lane's chunk of its row (K offset 0); the LDS destinations are
   // scalar (the wave index made uniform).
   const int widu = __builtin_amdgcn_readfirstlane(wid);
+  // kstr[j]: elements from one stage's source to the next one's per K element
+  // (1 in the row-major operands, BN in the tiled weight).
   const bf16* src[IPW];
-  int dst[IPW], coff[IPW];
+  int dst[IPW], coff[IPW], kstr[IPW];
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
     const int off = (wid * IPW + j) * 1024;
     int row;
+    kstr[j] = 1;
     if (off < 2 * A_BYTES) {
       const int plane = off / A_BYTES;
       row = (off % A_BYTES) / CB + (lane >> 3);
       src[j] = (plane ? Alo : Ahi) + (size_t)min(m0 + row, max_rows - 1) * K;
     } else {
       row = (off - 2 * A_BYTES) / CB + (lane >> 3);
-      src[j] = W + (size_t)min(n0 + row, N - 1) * K;
+      if constexpr (TILED) {
+        src[j] = W + (size_t)tx * K * BN + (size_t)row * KEL;   // block row `row` of column tile tx
+        kstr[j] = BN;
+      } else {
+        src[j] = W + (size_t)min(n0 + row, N - 1) * K;
+      }
     }
     coff[j] = 8 * gswz(row, lane & 7);
     src[j] += coff[j];
@@ -120,9 +134,9 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
     // Steps past the end re-read the split's first step (valid memory, never used).
     const int k = step < nsteps ? kb + step * KEL : kb;
     uint8_t* slot = smem + (step % R) * SLOT;
-    if (k + KEL <= ke) {   // a whole stage (the common case)
+    if (TILED || k + KEL <= ke) {   // a whole stage (the common case; always, when tiled)
 #pragma unroll
-      for (int j = 0; j < IPW; ++j) dma16(src[j] + k, slot + dst[j]);
+      for (int j = 0; j < IPW; ++j) dma16(src[j] + (size_t)k * kstr[j], slot + dst[j]);
     } else {   // chunks at or past the split's end read the split's first chunk
 #pragma unroll
       for (int j = 0; j < IPW; ++j) dma16(k + coff[j] < ke ? src[j] + k : src[j] - coff[j] + kb, slot + dst[j]);
@@ -808,9 +822,9 @@ bool gate_up_fused(DType dt, const GemmPlan& p, int N) {
 
 hipError_t launch_gate_up_swiglu(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W,
                                  float* P, size_t split_stride, const Ctrl* c, int s, int max_rows, int F, int K,
-                                 void* a, hipStream_t st) {
+                                 void* a, hipStream_t st, const void* W_tiled) {
   if (!gate_up_fused(dt, p, 2 * F)) {
-    hipError_t e = launch_gemm(dt, p, A0, A1, W, P, split_stride, c, s, max_rows, 2 * F, K, st);
+    hipError_t e = launch_gemm(dt, p, A0, A1, W, P, split_stride, c, s, max_rows, 2 * F, K, st, W_tiled);
     if (e != hipSuccess) return e;
     return launch_swiglu_post(dt, P, p.splits, split_stride, c, s, F, a, max_rows, st);
   }
@@ -819,8 +833,36 @@ hipError_t launch_gate_up_swiglu(DType dt, const GemmPlan& p, const void* A0, co
   return hipGetLastError();
 }
 
+bool gemm_tiled(DType dt, const GemmPlan& p, const void* W_tiled, int N, int K) {
+  return W_tiled && dt == DType::BF16 && p.kind == 0 && p.bn == kTileRows && N % kTileRows == 0 && K % 64 == 0 &&
+         p.k_per_split % 64 == 0;
+}
+
+namespace {
+// Column tile tx, K block kb (64 wide), row r, element e of the tiled copy sits
+// at ((tx * (K / 64) + kb) * kTileRows + r) * 64 + e; one thread moves 16 bytes.
+__global__ __launch_bounds__(256) void k_tile_rows(const bf16* __restrict__ W, bf16* __restrict__ out, int N, int K) {
+  const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;   // 16-byte chunk of `out`
+  if (idx >= (size_t)N * K / 8) return;
+  const int e8 = (int)(idx % 8), r = (int)((idx / 8) % kTileRows);
+  const size_t blk = idx / (8 * kTileRows);
+  const int kb = (int)(blk % (size_t)(K / 64)), tx = (int)(blk / (size_t)(K / 64));
+  *reinterpret_cast<uint4*>(out + idx * 8) =
+      *reinterpret_cast<const uint4*>(W + ((size_t)tx * kTileRows + r) * K + (size_t)kb * 64 + e8 * 8);
+}
+}  // namespace
+
+hipError_t launch_tile_rows(const void* W, void* out, int N, int K, hipStream_t st) {
+  if (N % kTileRows || K % 64) return hipErrorInvalidValue;
+  const size_t chunks = (size_t)N * K / 8;
+  hipLaunchKernelGGL(k_tile_rows, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, st,
+                     static_cast<const bf16*>(W), static_cast<bf16*>(out), N, K);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W, float* P,
-                       size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st) {
+                       size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st,
+                       const void* W_tiled) {
   if (dt == DType::BF16 && p.kind == 2) {
     const int wgps = std::max(1, std::min(cdiv(N, 16), kComputeUnits / p.splits));
     const dim3 sgrid(p.splits * wgps);
@@ -849,7 +891,10 @@ hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* 
     const bf16 *a0 = static_cast<const bf16*>(A0), *a1 = static_cast<const bf16*>(A1);
     const bf16* w = static_cast<const bf16*>(W);
     // LDS: 144 KB (128 columns, 3 slots), 112 KB (192, 2), 128 KB (256, 2).
-    if (p.bn == 256)
+    if (gemm_tiled(dt, p, W_tiled, N, K))
+      hipLaunchKernelGGL((k_gemm_dma<256, 2, true>), grid, dim3(kGemmWaves * 64), 0, st, a0, a1,
+                         static_cast<const bf16*>(W_tiled), P, split_stride, c, s, max_rows, N, K, p.k_per_split);
+    else if (p.bn == 256)
       hipLaunchKernelGGL((k_gemm_dma<256, 2>), grid, dim3(kGemmWaves * 64), 0, st, a0, a1, w, P, split_stride, c, s,
                          max_rows, N, K, p.k_per_split);
     else if (p.bn == 192)

@@ -81,8 +81,17 @@ struct GemmPlan {
 GemmPlan plan_gemm(DType dt, int max_rows, int N, int K);
 // Test hook: kind -1 = the planner's choice, 0/1 = that kernel; splits > 0 forces the split count.
 GemmPlan plan_gemm_kind(DType dt, int max_rows, int N, int K, int kind, int splits);
+// W_tiled (may be null): the same weight pre-tiled by launch_tile_rows, read
+// instead of W by the 128-row kernel's 256-column tiles (gemm_tiled says when).
 hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W, float* P,
-                       size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st);
+                       size_t split_stride, const Ctrl* c, int s, int max_rows, int N, int K, hipStream_t st,
+                       const void* W_tiled = nullptr);
+// Rows per column tile of the pre-tiled weight layout [N/kTileRows][K/64][kTileRows][64].
+constexpr int kTileRows = 256;
+// Whether launch_gemm reads W_tiled for this plan and shape.
+bool gemm_tiled(DType dt, const GemmPlan& p, const void* W_tiled, int N, int K);
+// out = W [N, K] (bf16) re-laid as [N/kTileRows][K/64][kTileRows][64]; N % kTileRows == 0, K % 64 == 0.
+hipError_t launch_tile_rows(const void* W, void* out, int N, int K, hipStream_t st);
 // The gate|up projection (W [2F, K]) and its SwiGLU: a = silu(gate) * up, written to `a`
 // as the down projection's input (bf16 hi/lo planes [max_rows, F] for BF16 models). With
 // the 256 x 256 kernel over one K split it is fused into the projection's epilogue (the
@@ -91,7 +100,7 @@ hipError_t launch_gemm(DType dt, const GemmPlan& p, const void* A0, const void* 
 bool gate_up_fused(DType dt, const GemmPlan& p, int N);
 hipError_t launch_gate_up_swiglu(DType dt, const GemmPlan& p, const void* A0, const void* A1, const void* W,
                                  float* P, size_t split_stride, const Ctrl* c, int s, int max_rows, int F, int K,
-                                 void* a, hipStream_t st);
+                                 void* a, hipStream_t st, const void* W_tiled = nullptr);
 
 // ---- the shared prefix of one layer
 // Up to kMaxPrefixSegs caches in position order (a tree node's own entries after

@@ -83,6 +83,23 @@ rksc_status check_config(const rksc_model_config* c) {
   return RKSC_OK;
 }
 
+// Whether a model's gate|up weight has the tiled layout of rksc_tile_gate_up.
+bool gate_up_tileable(const rksc_model_config* c) {
+  return c->dtype == RKSC_BF16 && c->d_model % 64 == 0 && (2 * c->d_ff) % rksc::kTileRows == 0;
+}
+
+// The optional tiled gate|up copy of a layer: only where the layout exists, 16-byte aligned.
+rksc_status check_tiled(const rksc_model_config* c, const rksc_layer_weights& lw, int l) {
+  if (!lw.w_gate_up_tiled) return RKSC_OK;
+  if (!gate_up_tileable(c))
+    return fail(RKSC_ERR_UNSUPPORTED,
+                "layer %d: w_gate_up_tiled is set, but this model has no tiled gate|up layout "
+                "(bf16, d_model %% 64 == 0, 2 d_ff %% 256 == 0)", l);
+  if (reinterpret_cast<uintptr_t>(lw.w_gate_up_tiled) % 16)
+    return fail(RKSC_ERR_INVALID_ARGUMENT, "layer %d: w_gate_up_tiled must be 16-byte aligned", l);
+  return RKSC_OK;
+}
+
 // The caches of a prefix chain in position order (root first); empty caches are
 // left out. Rejects more than kMaxPrefixSegs caches (which also ends a cycle).
 struct Chain {
@@ -221,6 +238,37 @@ int exit_window(const rksc_model_config* c, int B, int s, int n) {
 
 RKSC_EXPORT int32_t rksc_abi_version(void) { return RKSC_ABI_VERSION; }
 
+RKSC_EXPORT size_t rksc_gate_up_tiled_bytes(const rksc_model_config* cfg) {
+  if (check_config(cfg) != RKSC_OK) return 0;
+  if (!gate_up_tileable(cfg)) {
+    fail(RKSC_ERR_UNSUPPORTED, "no tiled gate|up layout for this model (bf16, d_model %% 64 == 0, 2 d_ff %% 256 == 0)");
+    return 0;
+  }
+  return (size_t)2 * cfg->d_ff * cfg->d_model * 2;
+}
+
+// The 256-row x 64-column blocks of the gate|up weight made contiguous, in the
+// order the 128-row projection kernel streams them (a storage layout of the
+// FFN's gate|up weight; rksc_layer_weights.w_gate_up_tiled).
+RKSC_EXPORT rksc_status rksc_tile_gate_up(const rksc_model_config* cfg, const void* w_gate_up, void* out,
+                                          size_t out_bytes, void* stream) {
+  const rksc_status st = check_config(cfg);
+  if (st != RKSC_OK) return st;
+  if (!gate_up_tileable(cfg))
+    return fail(RKSC_ERR_UNSUPPORTED,
+                "no tiled gate|up layout for this model (bf16, d_model %% 64 == 0, 2 d_ff %% 256 == 0)");
+  if (!w_gate_up || !out) return fail(RKSC_ERR_INVALID_ARGUMENT, "w_gate_up and out must not be NULL");
+  const size_t bytes = (size_t)2 * cfg->d_ff * cfg->d_model * 2;
+  if (out_bytes < bytes) return fail(RKSC_ERR_INVALID_ARGUMENT, "out has %zu bytes, needs %zu", out_bytes, bytes);
+  const uintptr_t a = reinterpret_cast<uintptr_t>(w_gate_up), b = reinterpret_cast<uintptr_t>(out);
+  if (a % 16 || b % 16) return fail(RKSC_ERR_INVALID_ARGUMENT, "w_gate_up and out must be 16-byte aligned");
+  if (a < b + bytes && b < a + bytes) return fail(RKSC_ERR_INVALID_ARGUMENT, "w_gate_up and out overlap");
+  const hipError_t e = rksc::launch_tile_rows(w_gate_up, out, 2 * cfg->d_ff, cfg->d_model,
+                                              static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(RKSC_ERR_HIP, "tiling launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 RKSC_EXPORT const char* rksc_status_string(rksc_status s) {
   switch (s) {
     case RKSC_OK: return "ok";
@@ -281,6 +329,7 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
     const rksc_layer_weights& lw = w->layers[l];
     if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
       return fail(RKSC_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
+    if (const rksc_status e = check_tiled(c, lw, l); e != RKSC_OK) return e;
   }
   const int win = window == kAutoWindow ? exit_window(c, n_branches, branch_len, (int)chain.n) : window;
 
@@ -380,12 +429,12 @@ rksc_status verify_impl(const rksc_weights* w, const rksc_prefix_kv* kv, const i
       // Profiled call: the class's closing event goes between the projection kernel and
       // its separate SwiGLU / split-K combine, so the pair brackets the projection alone.
       HIP_TRY(rksc::launch_gemm(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig,
-                                (size_t)M * 2 * F, ctrl, s, M, 2 * F, d, strm));
+                                (size_t)M * 2 * F, ctrl, s, M, 2 * F, d, strm, lw.w_gate_up_tiled));
       HIP_TRY(mark(l, 7));
       HIP_TRY(rksc::launch_swiglu_post(dt, pbig, lay.gu.splits, (size_t)M * 2 * F, ctrl, s, F, ffn, M, strm));
     } else {
       HIP_TRY(rksc::launch_gate_up_swiglu(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig,
-                                          (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm));
+                                          (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm, lw.w_gate_up_tiled));
       HIP_TRY(mark(l, 7));
     }
     if (drop & RKSC_DROP_DOWN_LO) HIP_TRY(drop_lo(ffn, (size_t)M * F));
@@ -517,6 +566,7 @@ RKSC_EXPORT rksc_status rksc_prefill(const rksc_weights* w, const int32_t* token
     const rksc_layer_weights& lw = w->layers[l];
     if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
       return fail(RKSC_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
+    if (const rksc_status e = check_tiled(c, lw, l); e != RKSC_OK) return e;
   }
 
   const DType dt = c->dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
@@ -579,7 +629,7 @@ RKSC_EXPORT rksc_status rksc_prefill(const rksc_weights* w, const int32_t* token
     HIP_TRY(rksc::launch_add_norm(dt, x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
                                   lw.ffn_norm, d, c->rms_eps, M, strm));
     HIP_TRY(rksc::launch_gate_up_swiglu(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig,
-                                        (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm));
+                                        (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm, lw.w_gate_up_tiled));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
                               M, d, F, strm));
     if (l == L - 1)
@@ -648,6 +698,7 @@ rksc_status branch_pass(const rksc_weights* w, const rksc_prefix_kv* kv, void* c
     const rksc_layer_weights& lw = w->layers[l];
     if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
       return fail(RKSC_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
+    if (const rksc_status e = check_tiled(c, lw, l); e != RKSC_OK) return e;
   }
 
   const DType dt = c->dtype == RKSC_BF16 ? DType::BF16 : DType::F32;
@@ -715,7 +766,7 @@ rksc_status branch_pass(const rksc_weights* w, const rksc_prefix_kv* kv, void* c
     HIP_TRY(rksc::launch_add_norm(dt, x_cur, pres, lay.o.splits, res_stride, false, ctrl, s, x_cur, act,
                                   lw.ffn_norm, d, c->rms_eps, M, strm));
     HIP_TRY(rksc::launch_gate_up_swiglu(dt, lay.gu, act, plane_lo(act, (size_t)M * d), lw.w_gate_up, pbig,
-                                        (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm));
+                                        (size_t)M * 2 * F, ctrl, s, M, F, d, ffn, strm, lw.w_gate_up_tiled));
     HIP_TRY(rksc::launch_gemm(dt, lay.down, ffn, plane_lo(ffn, (size_t)M * F), lw.w_down, pres, res_stride, ctrl, s,
                               M, d, F, strm));
     if (l == L - 1 && (out.h_out || out.next_token))

@@ -23,7 +23,8 @@ def log(msg: str):
 
 
 class HostLayers:
-    """Lazy host copies of device layer weights (bf16 stays bf16; the oracle widens exactly)."""
+    """Lazy host copies of device layer weights (bf16 stays bf16; the oracle widens exactly). A tiled
+    gate|up copy is a device storage layout only and is left out."""
 
     def __init__(self, layers):
         self._layers = layers
@@ -32,7 +33,7 @@ class HostLayers:
         return len(self._layers)
 
     def __getitem__(self, i):
-        return {k: v.detach().cpu() for k, v in self._layers[i].items()}
+        return {k: v.detach().cpu() for k, v in self._layers[i].items() if k != "w_gate_up_tiled"}
 
 
 @dataclasses.dataclass

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
     assert "rksc_verify_forward" in names and "rksc_asks_similarity" in names
     for name in names:
         assert hasattr(lib, name), f"{name} declared in include/ but not exported"
-    assert rk.rksc_abi_version() == 7
+    assert rk.rksc_abi_version() == 8
 
 
 def test_status_strings(lib):
@@ -429,3 +429,57 @@ def test_prefix_chain_limits_before_any_launch(lib):
     st = lib.rksc_prefix_extend(ctypes.byref(w), ctypes.byref(full), FAKE, 4, ctypes.c_void_p(0x70000000),
                                 ctypes.c_void_p(0x78000000), None, ok_ws, ext_ws, None)
     assert st == rk.RKSC_ERR_UNSUPPORTED and "children" in rk.rksc_last_error()
+
+
+def test_tile_gate_up_rejects_bad_arguments(lib):
+    """rksc_tile_gate_up and rksc_gate_up_tiled_bytes validate on the host: an fp32 or untileable
+    model, NULL, short, misaligned or overlapping buffers are refused before any launch."""
+    shape = dataclasses.replace(_bf16_tiny(), d_ff=768)     # 2 d_ff = 6 x 256
+    cfg = rk.model_config(shape)
+    need = lib.rksc_gate_up_tiled_bytes(ctypes.byref(cfg))
+    assert need == 2 * shape.d_ff * shape.d_model * 2
+    I, U = rk.RKSC_ERR_INVALID_ARGUMENT, rk.RKSC_ERR_UNSUPPORTED
+    src, dst = ctypes.c_void_p(0x10000000), ctypes.c_void_p(0x20000000)
+    T = lib.rksc_tile_gate_up
+    assert T(ctypes.byref(cfg), None, dst, need, None) == I
+    assert T(ctypes.byref(cfg), src, None, need, None) == I
+    assert T(ctypes.byref(cfg), src, dst, need - 1, None) == I and str(need) in rk.rksc_last_error()
+    assert T(ctypes.byref(cfg), ctypes.c_void_p(0x10000008), dst, need, None) == I
+    assert T(ctypes.byref(cfg), src, ctypes.c_void_p(0x10000000 + need - 64), need, None) == I
+    assert "overlap" in rk.rksc_last_error()
+    for bad in (workloads.get("tiny").model, dataclasses.replace(shape, dtype="f32"), _bf16_tiny()):
+        c2 = rk.model_config(bad)
+        assert (2 * bad.d_ff) % 256 or bad.dtype != "bf16"
+        assert lib.rksc_gate_up_tiled_bytes(ctypes.byref(c2)) == 0
+        assert T(ctypes.byref(c2), src, dst, 1 << 30, None) == U
+    assert lib.rksc_gate_up_tiled_bytes(ctypes.byref(rk.model_config(_shape(head_dim=96)))) == 0
+
+
+def test_verify_rejects_misplaced_tiled_weight(lib):
+    """A layer's w_gate_up_tiled is read only where the layout exists: set on an fp32 model it is
+    refused as unsupported, and a misaligned pointer as invalid, before any launch."""
+    shape = workloads.get("tiny").model
+    assert shape.dtype != "bf16"
+    w, layers, cfg = _fake_weights(shape)
+    layers[1].w_gate_up_tiled = FAKE
+    ws = lib.rksc_verify_workspace_size(ctypes.byref(cfg), 4, 16, 8)
+    kv = rk.PrefixKV(8, FAKE, FAKE)
+    ok_ws = ctypes.c_void_p(0x100000)
+    st = lib.rksc_verify_forward(ctypes.byref(w), ctypes.byref(kv), FAKE, 4, 16, 0.1, 1, FAKE, FAKE, None, ok_ws,
+                                 ws, None)
+    assert st == rk.RKSC_ERR_UNSUPPORTED and "layer 1" in rk.rksc_last_error()
+    pw = lib.rksc_prefill_workspace_size(ctypes.byref(cfg), 8)
+    assert lib.rksc_prefill(ctypes.byref(w), FAKE, 8, FAKE, FAKE, FAKE, ok_ws, pw, None) == rk.RKSC_ERR_UNSUPPORTED
+    w2, layers2, cfg2 = _fake_weights(dataclasses.replace(_bf16_tiny(), d_ff=768))
+    layers2[0].w_gate_up_tiled = ctypes.c_void_p(0x1008)
+    ws2 = lib.rksc_verify_workspace_size(ctypes.byref(cfg2), 4, 16, 8)
+    st = lib.rksc_verify_forward(ctypes.byref(w2), ctypes.byref(kv), FAKE, 4, 16, 0.1, 1, FAKE, FAKE, None,
+                                 ok_ws, ws2, None)
+    assert st == rk.RKSC_ERR_INVALID_ARGUMENT and "aligned" in rk.rksc_last_error()
+    layers2[0].w_gate_up_tiled = None
+    w3, layers3, cfg3 = _fake_weights(_bf16_tiny())                # 2 d_ff = 1376: no tiled layout
+    layers3[1].w_gate_up_tiled = FAKE
+    ws3 = lib.rksc_verify_workspace_size(ctypes.byref(cfg3), 4, 16, 8)
+    st = lib.rksc_verify_forward(ctypes.byref(w3), ctypes.byref(kv), FAKE, 4, 16, 0.1, 1, FAKE, FAKE, None,
+                                 ok_ws, ws3, None)
+    assert st == rk.RKSC_ERR_UNSUPPORTED
