@@ -315,51 +315,106 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  auto compute = [&](const uint8_t* slot) {
-    bf16x8 bw[TN];
+  // Fragment reads of one stage: the weight fragments of the wave's columns,
+  // and the hi/lo activation fragments of row block tm.
+  auto load_w = [&](const uint8_t* slot, bf16x8 (&bw)[TN]) {
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
       const int row = wn * WN + 16 * tn + r16;
       bw[tn] = *reinterpret_cast<const bf16x8*>(slot + 2 * SUB_A + row * RB + wswz(row, g) * 16);
     }
+  };
+  auto load_a = [&](const uint8_t* slot, int tm, bf16x8& ah, bf16x8& al) {
+    const int row = wm * 64 + 16 * tm + r16;
+    const int off = row * RB + wswz(row, g) * 16;
+    ah = *reinterpret_cast<const bf16x8*>(slot + off);
+    al = *reinterpret_cast<const bf16x8*>(slot + SUB_A + off);
+  };
+  auto mma = [&](int tm, const bf16x8& ah, const bf16x8& al, const bf16x8 (&bw)[TN]) {
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm) {
-      const int row = wm * 64 + 16 * tm + r16;
-      const int off = row * RB + wswz(row, g) * 16;
-      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(slot + off);
-      const bf16x8 al = *reinterpret_cast<const bf16x8*>(slot + SUB_A + off);
+    for (int tn = 0; tn < TN; ++tn)
+      acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw[tn], acc[tm][tn], 0, 0, 0);
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
-        acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw[tn], acc[tm][tn], 0, 0, 0);
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
-        acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw[tn], acc[tm][tn], 0, 0, 0);
+    for (int tn = 0; tn < TN; ++tn)
+      acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw[tn], acc[tm][tn], 0, 0, 0);
+  };
+  // The split's last, partial stage: the activation chunks at or past its end
+  // (8-element chunks lie wholly inside or outside, K % 8 == 0) hold the split's
+  // first chunk and are zeroed in LDS once the stage has landed, so that every
+  // stage is contracted without a mask. Called by every thread.
+  auto zero_tail = [&](int step) {
+    const int kst = kb + step * KEL;
+    if (kst + KEL <= ke) return;
+    uint8_t* const slot = smem + (step % R) * SLOT;
+    for (int idx = threadIdx.x; idx < 2 * BM * 4; idx += kGemmWaves * 64) {
+      const int c = idx & 3, row = (idx >> 2) % BM, pl = idx / (BM * 4);
+      if (kst + 8 * c >= ke)
+        *reinterpret_cast<uint4*>(slot + pl * SUB_A + row * RB + wswz(row, c) * 16) = make_uint4(0, 0, 0, 0);
     }
+    __syncthreads();
   };
 
+  // Software pipeline over the R-slot ring (all R slots filled up front). In
+  // stage st a wave contracts row blocks 0..2 while reading the next block's
+  // fragments; then (barrier A: stage st+1 has landed for every thread) it
+  // reads stage st+1's weight and first activation fragments while contracting
+  // row block 3, so the LDS reads of one stage overlap the MFMAs of the last;
+  // then (barrier B: every wave is done reading slot st) slot st is refilled
+  // with stage st+R. Barriers sit outside the wave_live guards.
 #pragma unroll
-  for (int st = 0; st < R - 1; ++st) issue(st);
-  for (int st = 0; st < nsteps; ++st) {
-    // This thread's DMAs for step st have landed and its reads of step st-1 are
-    // complete; after the barrier every wave's are.
-    wait_vmcnt_lds<IPW * (R - 2)>();
-    __builtin_amdgcn_s_barrier();
-    issue(st + R - 1);   // refills the slot step st-1 used
-    uint8_t* const slot = smem + (st % R) * SLOT;
-    const int kst = kb + st * KEL;
-    if (kst + KEL > ke) {
-      // The split's last, partial stage: the activation chunks at or past its
-      // end (8-element chunks lie wholly inside or outside, K % 8 == 0) hold
-      // the split's first chunk and are zeroed in LDS, so that every stage is
-      // contracted without a mask. No DMA targets this slot any more.
-      for (int idx = threadIdx.x; idx < 2 * BM * 4; idx += kGemmWaves * 64) {
-        const int c = idx & 3, row = (idx >> 2) % BM, pl = idx / (BM * 4);
-        if (kst + 8 * c >= ke)
-          *reinterpret_cast<uint4*>(slot + pl * SUB_A + row * RB + wswz(row, c) * 16) = make_uint4(0, 0, 0, 0);
-      }
-      __syncthreads();
+  for (int st = 0; st < R; ++st) issue(st);
+  wait_vmcnt<IPW * (R - 1)>();
+  __builtin_amdgcn_s_barrier();
+  zero_tail(0);
+  // Two register sets for the weight fragments, used alternately by even and
+  // odd stages. The last stage also reads the next slot's fragments; those
+  // reads land in the ring (in bounds) and are never used.
+  bf16x8 bwa[TN], bwb[TN], h0, l0, h1, l1, h2, l2, h3, l3;
+  if (wave_live) {
+    load_w(smem, bwa);
+    load_a(smem, 0, h0, l0);
+  }
+  auto stage = [&](int st, const bf16x8 (&bwc)[TN], bf16x8 (&bwn)[TN]) {
+    const uint8_t* const slot = smem + (st % R) * SLOT;
+    const uint8_t* const nslot = smem + ((st + 1) % R) * SLOT;
+    // sched_barrier(0) keeps the compiler from hoisting a row block's MFMAs
+    // above the previous block's, which would wait on reads just issued.
+    if (wave_live) {
+      load_a(slot, 1, h1, l1);
+      mma(0, h0, l0, bwc);
+      __builtin_amdgcn_sched_barrier(0);
+      load_a(slot, 2, h2, l2);
+      mma(1, h1, l1, bwc);
+      __builtin_amdgcn_sched_barrier(0);
+      load_a(slot, 3, h3, l3);
+      mma(2, h2, l2, bwc);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (wave_live) compute(slot);
+    // A: this thread's DMAs of stage st+1 have landed; after the barrier every thread's have.
+    wait_vmcnt<IPW * (R - 2)>();
+    __builtin_amdgcn_s_barrier();
+    if (st + 1 < nsteps) zero_tail(st + 1);
+    if (wave_live) {
+      load_w(nslot, bwn);
+      load_a(nslot, 0, h0, l0);
+      mma(3, h3, l3, bwc);
+      // The next stage's TN + 2 reads spread over the first MFMAs of this block.
+#pragma unroll
+      for (int i = 0; i < (TN + 2) / 2; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // two LDS reads
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * TN - (TN + 2) / 2, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // B: this wave's reads of slot st are complete; after the barrier every wave's are.
+    wait_vmcnt_lds<63>();
+    __builtin_amdgcn_s_barrier();
+    issue(st + R);   // refills slot st
+  };
+  for (int st = 0; st < nsteps; st += 2) {
+    stage(st, bwa, bwb);
+    if (st + 1 < nsteps) stage(st + 1, bwb, bwa);
   }
   wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
   if constexpr (SWIGLU) {
