@@ -148,58 +148,94 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const bf16x8 zero = {};
-
-  // One stage: two 32-wide k substeps; `masked` zeroes activation chunks at k >= ke.
-  auto compute = [&](const uint8_t* slot, int kst, auto masked) {
+  // The fragments of one 32-wide k substep sb of a stage: the hi/lo activation
+  // fragments of the wave's row blocks and the weight fragments of its columns.
+  struct Frag {
+    bf16x8 ah[TM], al[TM], bw[TN];
+  };
+  auto load = [&](const uint8_t* slot, int sb, Frag& f) {
+    const int ch = 4 * sb + g;
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      const int ch = 4 * sb + g;
-      bool kin = true;
-      if constexpr (decltype(masked)::value) kin = kst + 8 * ch < ke;
-      bf16x8 ah[TM], al[TM], bw[TN];
+    for (int tm = 0; tm < TM; ++tm) {
+      const int row = wm0 + 16 * tm + r16;
+      const int off = row * CB + gswz(row, ch) * 16;
+      f.ah[tm] = *reinterpret_cast<const bf16x8*>(slot + off);
+      f.al[tm] = *reinterpret_cast<const bf16x8*>(slot + A_BYTES + off);
+    }
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
-        const int row = wm0 + 16 * tm + r16;
-        const int off = row * CB + gswz(row, ch) * 16;
-        ah[tm] = *reinterpret_cast<const bf16x8*>(slot + off);
-        al[tm] = *reinterpret_cast<const bf16x8*>(slot + A_BYTES + off);
-        if constexpr (decltype(masked)::value) {
-          ah[tm] = kin ? ah[tm] : zero;
-          al[tm] = kin ? al[tm] : zero;
-        }
-      }
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        const int row = wn0 + 16 * tn + r16;
-        bw[tn] = *reinterpret_cast<const bf16x8*>(slot + 2 * A_BYTES + row * CB + gswz(row, ch) * 16);
-      }
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-        for (int tn = 0; tn < TN; ++tn) {
-          acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[tm], bw[tn], acc[tm][tn], 0, 0, 0);
-          acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[tm], bw[tn], acc[tm][tn], 0, 0, 0);
-        }
+    for (int tn = 0; tn < TN; ++tn) {
+      const int row = wn0 + 16 * tn + r16;
+      f.bw[tn] = *reinterpret_cast<const bf16x8*>(slot + 2 * A_BYTES + row * CB + gswz(row, ch) * 16);
     }
   };
-
+  auto mma = [&](const Frag& f) {
 #pragma unroll
-  for (int st = 0; st < R - 1; ++st) issue(st);
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.ah[tm], f.bw[tn], acc[tm][tn], 0, 0, 0);
+        acc[tm][tn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.al[tm], f.bw[tn], acc[tm][tn], 0, 0, 0);
+      }
+  };
+  // The next substep's TM * 2 + TN reads spread over the first MFMAs of a substep.
+  constexpr int NRD = TM * 2 + TN, NMF = TM * TN * 2;
+  auto interleave = [&]() {
+#pragma unroll
+    for (int i = 0; i < NRD / 2; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // two LDS reads
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD / 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // The split's last, partial stage: the activation chunks at or past its end
+  // (8-element chunks lie wholly inside or outside, K % 8 == 0) hold the split's
+  // first chunk and are zeroed in LDS once the stage has landed, so that every
+  // stage is contracted without a mask. Called by every thread.
+  auto zero_tail = [&](int step) {
+    const int kst = kb + step * KEL;
+    if (TILED || kst + KEL <= ke) return;
+    uint8_t* const slot = smem + (step % R) * SLOT;
+    for (int idx = threadIdx.x; idx < 2 * BM * 8; idx += kGemmWaves * 64) {
+      const int c = idx & 7, row = (idx >> 3) % BM, pl = idx / (BM * 8);
+      if (kst + 8 * c >= ke)
+        *reinterpret_cast<uint4*>(slot + pl * A_BYTES + row * CB + gswz(row, c) * 16) = make_uint4(0, 0, 0, 0);
+    }
+    __syncthreads();
+  };
 
+  // Software pipeline over the R-slot ring (all R slots filled up front). A
+  // stage is two k substeps: the wave contracts substep 0 while it reads
+  // substep 1's fragments; then (one barrier: stage st+1 has landed for every
+  // thread, and every wave's reads of slot st are complete) slot st is refilled
+  // with stage st+R, and the wave reads stage st+1's substep 0 while it
+  // contracts substep 1. The barrier sits outside the wave_live guards. The
+  // last stage also reads the next slot's fragments (in the ring, never used).
+#pragma unroll
+  for (int st = 0; st < R; ++st) issue(st);
+  wait_vmcnt<IPW * (R - 1)>();
+  __builtin_amdgcn_s_barrier();
+  zero_tail(0);
+  Frag f0, f1;
+  if (wave_live) load(smem, 0, f0);
   for (int st = 0; st < nsteps; ++st) {
-    // This thread's DMAs for step st have landed and its reads of step st-1 are
-    // complete; after the barrier every wave's are.
+    const uint8_t* const slot = smem + (st % R) * SLOT;
+    const uint8_t* const nslot = smem + ((st + 1) % R) * SLOT;
+    if (wave_live) {
+      load(slot, 1, f1);
+      mma(f0);
+      interleave();
+    }
+    // This thread's DMAs of stage st+1 have landed and its reads of slot st are
+    // complete; after the barrier every thread's are.
     wait_vmcnt_lds<IPW * (R - 2)>();
     __builtin_amdgcn_s_barrier();
-    issue(st + R - 1);   // refills the slot step st-1 used
-    const uint8_t* slot = smem + (st % R) * SLOT;
-    const int kst = kb + st * KEL;
+    issue(st + R);   // refills slot st
+    if (st + 1 < nsteps) zero_tail(st + 1);
     if (wave_live) {
-      if (kst + KEL <= ke)
-        compute(slot, kst, std::false_type{});
-      else
-        compute(slot, kst, std::true_type{});
+      load(nslot, 0, f0);
+      mma(f1);
+      interleave();
     }
   }
   wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
