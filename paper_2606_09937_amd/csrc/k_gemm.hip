@@ -268,10 +268,21 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
 // stage kernel keeps one 64 KB stage in flight per CU, which at the weight
 // stream's latency holds it near a third of HBM bandwidth; 128 x 512 tiles in
 // three 48 KB stages keep twice the weight bytes in flight. Each DMA
-// instruction moves 16 rows x 64 bytes; within a row the 16-byte chunk c sits
-// at c ^ ((row >> 2) & 3), which spreads the 16 rows of a fragment read over
-// the banks.
-__device__ __forceinline__ int wswz(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
+// instruction moves 16 rows x 64 bytes.
+//
+// LDS layout of a sub-tile: rows 2q and 2q + 1 form the 128-byte line q, row r
+// holding 16-byte slots 4 (r & 1) .. 4 (r & 1) + 3 of its line before the
+// swizzle, and slot t of line q sits at t ^ (q & 7). A fragment read has lane
+// (r16, g) read chunk g of row r16 of a 16-row block; a 128-bit LDS read is
+// served eight lanes at a time (the even, then the odd lanes of each 16), and
+// the eight even rows 0, 2, .., 14 lie on lines q = 0..7, so their chunks fall
+// on eight distinct slots, i.e. all 32 banks. (With each row on its own 64-byte
+// line, the even rows met only four distinct slots: a two-way bank conflict on
+// every read.)
+__device__ __forceinline__ int wlds(int row, int chunk) {
+  const int q = row >> 1;
+  return q * 128 + (((row & 1) * 4 + chunk) ^ (q & 7)) * 16;
+}
 
 // SWIGLU: the gate|up projection with its SwiGLU epilogue (one K split). W is
 // [2F, K] (gate rows, then up rows, N = 2F); a workgroup's BN weight rows are
@@ -317,20 +328,22 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
     return row < BN / 2 ? min(n0 + row, F - 1) : F + min(n0 + row - BN / 2, F - 1);
   };
 
-  // DMA instruction j of this wave (ins = 8j + wid) fills 16 rows of sub-tile
-  // plane(j) (0 A hi, 1 A lo, 2 W; fixed by j as A_INS is a multiple of 8);
-  // lane L fills physical chunk L & 3 of row L >> 2 of them, i.e. logical chunk
-  // (L & 3) ^ ((L >> 4) & 3), the same for every j.
+  // DMA instruction j of this wave (ins = 8j + wid) fills 16 rows (8 lines) of
+  // sub-tile plane(j) (0 A hi, 1 A lo, 2 W; fixed by j as A_INS is a multiple of
+  // 8); lane L fills slot L & 7 of line L >> 3, i.e. logical slot
+  // t = (L & 7) ^ (L >> 3): chunk t & 3 of row 2 (L >> 3) + (t >> 2) of the
+  // block, the same for every j.
   // Row offsets in elements as size_t: rows x K passes 2^31 at large row counts.
   auto plane = [](int j) { return j * kGemmWaves < A_INS ? 0 : (j * kGemmWaves < 2 * A_INS ? 1 : 2); };
   size_t rowoff[IPW];
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
     const int pl = plane(j);
-    const int row = (j * kGemmWaves + wid - pl * A_INS) * 16 + (lane >> 2);
+    const int t = (lane & 7) ^ (lane >> 3);
+    const int row = (j * kGemmWaves + wid - pl * A_INS) * 16 + 2 * (lane >> 3) + (t >> 2);
     rowoff[j] = (size_t)(pl < 2 ? min(m0 + row, max_rows - 1) : wrow(row)) * K;
   }
-  const int ccol = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
+  const int ccol = 8 * (((lane & 7) ^ (lane >> 3)) & 3);
   // The wave index made uniform, so that the LDS destinations are scalar (M0) values.
   const int widu = __builtin_amdgcn_readfirstlane(wid);
   auto issue = [&](int step) {
@@ -357,12 +370,12 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
       const int row = wn * WN + 16 * tn + r16;
-      bw[tn] = *reinterpret_cast<const bf16x8*>(slot + 2 * SUB_A + row * RB + wswz(row, g) * 16);
+      bw[tn] = *reinterpret_cast<const bf16x8*>(slot + 2 * SUB_A + wlds(row, g));
     }
   };
   auto load_a = [&](const uint8_t* slot, int tm, bf16x8& ah, bf16x8& al) {
     const int row = wm * 64 + 16 * tm + r16;
-    const int off = row * RB + wswz(row, g) * 16;
+    const int off = wlds(row, g);
     ah = *reinterpret_cast<const bf16x8*>(slot + off);
     al = *reinterpret_cast<const bf16x8*>(slot + SUB_A + off);
   };
@@ -385,7 +398,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_wide(const bf16* __res
     for (int idx = threadIdx.x; idx < 2 * BM * 4; idx += kGemmWaves * 64) {
       const int c = idx & 3, row = (idx >> 2) % BM, pl = idx / (BM * 4);
       if (kst + 8 * c >= ke)
-        *reinterpret_cast<uint4*>(slot + pl * SUB_A + row * RB + wswz(row, c) * 16) = make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(slot + pl * SUB_A + wlds(row, c)) = make_uint4(0, 0, 0, 0);
     }
     __syncthreads();
   };
