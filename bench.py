@@ -149,11 +149,17 @@ COPY_BYTES = 1 << 29   # calibration copy: 512 MiB read + 512 MiB written
 
 
 def source_digest(kernel):
+    """SHA-256 of the kernel's sources with comments and whitespace runs removed, so
+    that a stored counter record goes stale when the code changes, not its comments."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for fn in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(ROOT, "paper_2606_09937_amd", "csrc", fn), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2606_09937_amd", "csrc", fn), encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 

@@ -37,8 +37,9 @@ namespace {
 // are typed bf16x8 loads, which the compiler does not order behind the
 // untyped DMA stores (it would otherwise wait for every outstanding DMA).
 // K needs only to be a multiple of 8: a chunk at or past the end of the split
-// reads the split's first chunk instead (valid memory), and activation
-// fragments past the end are zeroed when the last, partial stage is consumed.
+// reads the split's first chunk instead (valid memory), and the activation
+// chunks past the end are zeroed in LDS once the last, partial stage has
+// landed.
 //
 // TILED: the weight is read from its pre-tiled copy [N/BN][K/64][BN][64]
 // (launch_tile_rows), in which a stage's BN x 64 weight block is one
@@ -263,12 +264,9 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
 // 256 x 256 each wave reads 64 x 32 activation and 128 x 32 weight elements
 // from LDS per 32-wide K step for 64 MFMAs, a third fewer LDS bytes per MFMA
 // than the 128-row kernel's 64 x 64 wave tiles. A stage holds three sub-tiles
-// (A hi, A lo: BM rows; W: BN rows) of 64-byte rows; R stages fit the LDS and
-// R - 1 are in flight while one is contracted. A 128-row call of the 64-wide
-// stage kernel keeps one 64 KB stage in flight per CU, which at the weight
-// stream's latency holds it near a third of HBM bandwidth; 128 x 512 tiles in
-// three 48 KB stages keep twice the weight bytes in flight. Each DMA
-// instruction moves 16 rows x 64 bytes.
+// (A hi, A lo: BM rows; W: BN rows) of 64-byte rows; R stages fit the LDS,
+// all R are filled up front and R - 1 are in flight while one is contracted.
+// Each DMA instruction moves 16 rows x 64 bytes.
 //
 // LDS layout of a sub-tile: rows 2q and 2q + 1 form the 128-byte line q, row r
 // holding 16-byte slots 4 (r & 1) .. 4 (r & 1) + 3 of its line before the
