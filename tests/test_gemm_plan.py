@@ -78,3 +78,42 @@ def test_large_row_counts_take_wide_tiles():
     the 7B width) reach the 256 x 256-tile kernel through the planner; its row offsets are 64-bit."""
     for M in (153600, 262144):
         assert rk.rksc_test_gemm_plan(M, 4096, 14336)["kind"] == 1
+
+
+def _attn_chunks(B, n, s, H, Hkv, hd=128):
+    """Split-KV chunks of the attention planner, read back from the test hook's scratch size
+    (4096 bytes + one (hd + 2)-float partial per chunk, row and head; no partials for one chunk)."""
+    lib = rk.load_library()
+    size = int(lib.rksc_test_attention_scratch_size(1, B, n, s, H, Hkv, hd))
+    parts = (size - 4096) // (B * s * H * (hd + 2) * 4)
+    assert 4096 + parts * B * s * H * (hd + 2) * 4 == size
+    return max(parts, 1)
+
+
+@pytest.mark.parametrize("name,B,n,s,H,Hkv,chunks", [
+    ("7b_single", 1, 1024, 128, 32, 8, 8),       # 32 query tiles: 8 chunks fill one round of 256
+    ("7b_paper_verify", 8, 1024, 128, 28, 4, 1),   # 224 query tiles: a second chunk would need two rounds
+    ("7b_large_vocab", 8, 4096, 128, 28, 4, 1),
+    ("7b_tot", 16, 2048, 256, 32, 8, 1),
+    ("decode_8", 8, 1024, 1, 32, 8, 8),            # packed: 8 tiles, at least 2 prefix tiles per chunk
+    ("10b_decode", 32, 16384, 1, 32, 8, 32),       # packed: 8 tiles x 32 chunks = 256
+])
+def test_attention_split_fits_one_round(name, B, n, s, H, Hkv, chunks):
+    """The prefix is split into chunks only while the launch still fits one round of 256 workgroups
+    (one per CU), with at least two key tiles per chunk."""
+    assert _attn_chunks(B, n, s, H, Hkv) == chunks, name
+
+
+def test_attention_split_rule_over_a_sweep():
+    for B in (1, 2, 3, 8, 16, 32):
+        for s in (1, 16, 128, 256):
+            for n in (64, 1024, 16384):
+                G = 4
+                cross = G * s < 64
+                base = (-(-B * s * G // 128) if cross else -(-G * s // 128) * B) * 8
+                c = _attn_chunks(B, n, s, 32, 8)
+                min_tiles = -(-n // 64) + (0 if cross else 1)
+                assert 2 * c <= max(min_tiles, 2), (B, s, n, c)
+                assert c == 1 or base * c <= 256, (B, s, n, c, base)
+                # one more chunk would break a rule
+                assert base * (c + 1) > 256 or 2 * (c + 1) > min_tiles, (B, s, n, c, base)
