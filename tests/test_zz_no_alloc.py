@@ -75,6 +75,14 @@ def test_noalloc_headline_shape():
         log(f"[noalloc] 7b_single tau={tau}")
         got, ref = _both(mw, kv, toks, tau, wl.patience)
         _same(got, ref, f"7b_single tau={tau}")
+    # with the pre-tiled gate|up copy (the bench's setting) the outputs are the same bits
+    mt = workloads.ModelWeights(mw.shape, mw.embed, [dict(lw) for lw in mw.layers], mw.final_norm, mw.lm_head)
+    assert rk.tile_gate_up(mt)
+    log("[noalloc] 7b_single with the tiled gate|up copy")
+    got_t, ref_t = _both(mt, kv, toks, 0.2, wl.patience)
+    _same(got_t, ref_t, "7b_single tiled")
+    _same(got_t, ref, "7b_single tiled against untiled")
+    del mt
     # then a smaller call again, after the large one
     small = dataclasses.replace(wl.model, n_layers=3)
     mw3, kv3, toks3 = _inputs(small, 2, 64, 16, seed=9, n_layers=3)
