@@ -257,7 +257,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm_dma(const bf16* __rest
       interleave();
     }
   }
-  wait_vmcnt<0>();   // drain the look-ahead DMAs before the workgroup can exit
+  wait_vmcnt<0>();   // no DMA is left in flight (none past the split's end); kept as a guard
 
   float* out = P + tz * split_stride;
 #pragma unroll
