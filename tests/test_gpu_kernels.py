@@ -28,6 +28,8 @@ def _rand(shape, dtype, seed, std=1.0):
     (130, 14376, 1000, 0), (70, 6016, 4104, 0),
     # the planner's 256 x 256 tiles over K splits at 512 and 1024 rows (3 and 4 splits)
     (1024, 4608, 3584, 0), (512, 6144, 4096, 0),
+    # short K loops of the 128-row kernel's ring (3 slots): splits of 1, 2 and 3 stages, a partial last one
+    (128, 4096, 64, 1), (128, 4096, 136, 2), (128, 4096, 192, 1), (128, 4096, 200, 2),
 ])
 def test_gemm_matches_fp64(dtype, M, N, K, splits):
     log(f"gemm {dtype} M={M} N={N} K={K} splits={splits}")
