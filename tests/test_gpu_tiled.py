@@ -73,10 +73,13 @@ def test_fp32_and_untileable_models_have_no_tiled_copy():
     ("mid_256rows", 2, 128, 100, True),
     ("mid_1024rows", 8, 128, 64, False),
     ("7b_128rows_2layers", 1, 128, 1024, True),
+    ("28l_128rows_2layers", 1, 128, 512, True),    # d = 3584, 2F = 148 x 256
 ])
 def test_verify_with_tiled_copy_is_bitwise_identical(case, B, s, n, tiles):
     if case.startswith("7b"):
         shape, L = workloads.get("7b_single").model, 2
+    elif case.startswith("28l"):
+        shape, L = workloads.get("7b_paper_verify").model, 2
     else:
         shape, L = MID, None
     assert _uses_tiles(shape, B * s) == tiles
